@@ -1,0 +1,110 @@
+"""Planted mistakes: each test plants one plausible error in the oracle (on the
+CPU, through monkeypatching) and checks that one of the pins in
+test_oracle_pins.py fails.  This shows the pins are sharp enough to catch a
+dropped term, a wrong index, a transposed operand or a wrong scale."""
+import math
+import types
+
+import numpy as np
+import pytest
+
+from oracle import smem_oracle as O
+from tests import test_oracle_pins as P
+
+
+def _fails(fn, *a, **kw):
+    try:
+        fn(*a, **kw)
+    except (AssertionError, ValueError):
+        return True
+    return False
+
+
+class _NumpyProxy(types.ModuleType):
+    def __init__(self, **overrides):
+        super().__init__("np_proxy")
+        self._ov = overrides
+
+    def __getattr__(self, name):
+        if name in self.__dict__.get("_ov", {}):
+            return self._ov[name]
+        return getattr(np, name)
+
+
+def test_wrong_scale_is_caught(monkeypatch):
+    fake = types.SimpleNamespace(sqrt=lambda x: x)   # 1/d_h instead of 1/sqrt(d_h)
+    monkeypatch.setattr(O, "math", fake)
+    assert _fails(P.check_golden)
+    assert _fails(P.test_encoder_matches_sdpa, 16, 4, 32, O.MASK_BIDIR)
+
+
+def test_causal_without_diagonal_is_caught(monkeypatch):
+    monkeypatch.setattr(O, "np", _NumpyProxy(tril=lambda m, k=0: np.tril(m, k - 1)))
+    assert _fails(P.check_golden)
+
+
+def test_reading_own_block_is_caught(monkeypatch):
+    orig = O._memory_below
+    monkeypatch.setattr(O, "_memory_below", lambda st, s, J: orig(st, s, J + 1))
+    assert _fails(P.check_golden)
+    assert _fails(P.test_reader_matches_sdpa_over_concatenated_keys, False, True)
+
+
+def test_dropped_null_row_is_caught(monkeypatch):
+    orig = O._reader_keys
+    monkeypatch.setattr(O, "_reader_keys", lambda mk, mv, h, nkv, ki, vi, n, dh: orig(mk, mv, h, None, ki, vi, n, dh))
+    assert _fails(P.check_golden)
+    assert _fails(P.test_reader_matches_sdpa_over_concatenated_keys, True, True)
+
+
+def test_intra_off_by_one_is_caught(monkeypatch):
+    orig = O._reader_keys
+    monkeypatch.setattr(O, "_reader_keys", lambda mk, mv, h, nkv, ki, vi, n, dh: orig(mk, mv, h, nkv, ki, vi, n - 1, dh))
+    assert _fails(P.check_golden)
+    assert _fails(P.test_decode_equals_prefill_row) or _fails(P.test_closed_forms)
+
+
+def test_transposed_scores_are_caught(monkeypatch):
+    def encode_transposed(q, k, v, mask=O.MASK_BIDIR):
+        q, k, v = (np.asarray(x, np.float64) for x in (q, k, v))
+        nb, b, H, dh = q.shape
+        out = np.zeros_like(q)
+        for blk in range(nb):
+            for h in range(H):
+                Q, K, V = q[blk, :, h], k[blk, :, h], v[blk, :, h]
+                S = (K @ Q.T) / math.sqrt(dh)          # planted: K Q^T
+                if mask == O.MASK_CAUSAL:
+                    S = np.where(np.tril(np.ones((b, b), bool)), S, -np.inf)
+                E = np.exp(S - S.max(1, keepdims=True))
+                out[blk, :, h] = (E / E.sum(1, keepdims=True)) @ V
+        return out
+    monkeypatch.setattr(O, "encode_blocks", encode_transposed)
+    assert _fails(P.check_golden)
+
+
+def test_unnormalised_softmax_is_caught(monkeypatch):
+    def read_bad(q, keys, values, scale):
+        keys = np.asarray(keys, np.float64)
+        if keys.shape[0] == 0:
+            return np.zeros(np.asarray(values).shape[1])
+        s = keys @ np.asarray(q, np.float64) * scale
+        e = np.exp(s - s.max())
+        return (e / (e.sum() + 1.0)) @ np.asarray(values, np.float64)  # planted: extra term
+    monkeypatch.setattr(O, "softmax_read", read_bad)
+    assert _fails(P.check_golden)
+
+
+def test_unsorted_store_is_caught(monkeypatch):
+    monkeypatch.setattr(O.Store, "live", lambda self, seq: [j for (s, j) in self.rows if s == seq])
+    assert _fails(P.test_store_errors_and_canonical_order)
+    assert _fails(P.test_edit_path_independence_100_orders)
+
+
+def test_value_plane_swap_is_caught(monkeypatch):
+    orig = O._memory_below
+
+    def swapped(st, s, J):
+        k, v = orig(st, s, J)
+        return v, k                                    # planted: K and V planes swapped
+    monkeypatch.setattr(O, "_memory_below", swapped)
+    assert _fails(P.check_golden)
