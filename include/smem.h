@@ -1,0 +1,188 @@
+/*
+ * smem.h -- C ABI of the MI355X (gfx950) SMem attention hot path.
+ *
+ * SMem ("Memory as a Cache: Exact Context Reuse and Deletion by
+ * Construction") splits a sequence into blocks of b tokens.  An encoder
+ * attends only inside each block, so every block's memory rows are a function
+ * of that block and its index alone (Section 2, "Model"; Proposition 1).  The
+ * memory is the multiset of all blocks' rows, listed canonically by block
+ * index (Section 2, "Model").  Deleting a present block gives exactly the
+ * memory in which it was never encoded (Theorem 1).  A reader query at
+ * in-block position t of block J attends to its own block's keys 0..t and to
+ * the memory rows of strictly earlier blocks j < J (Section 2, "Model";
+ * Appendix A, "Reader").  Here the two key sets, plus an optional null row,
+ * are read under one softmax.
+ *
+ * Conventions shared by every call
+ *  - Tensors are caller-owned DEVICE pointers, row-major, with no padding:
+ *      token tensors   [rows, H, dh]    (rows = n_blocks*b, n_seq*b or n_seq)
+ *      null_kv         [2, H, dh]       (key vector per head, then value)
+ *    Their element type is the store's dtype: fp32, or bf16 computed with
+ *    fp32 accumulation.
+ *  - Index arrays (seq_ids, block_idx, query_block, pos, live_idx, n_live)
+ *    are HOST pointers.  They are read, or written, before the call returns.
+ *  - Every device operation is enqueued on the caller's stream `s`.  Store
+ *    metadata changes take effect on the host immediately.  Their device copy
+ *    is updated by kernels enqueued on `s`, so stream order decides which
+ *    memory state a later read sees.  Calls on one store from different
+ *    streams must be ordered by the caller.
+ *  - Errors: every argument and store-state check runs before anything is
+ *    enqueued.  A call that returns an error has changed nothing (no partial
+ *    edits).  SMEM_EHIP means a HIP launch or copy failed.
+ *    smem_last_error() gives a message for the calling thread's last error.
+ *  - No call allocates device memory.  The store lives in a caller-provided
+ *    device buffer of smem_store_bytes() bytes.
+ *  - Softmax scale is 1/sqrt(dh) (Lemma 1's 1/sqrt(d) for the head width).
+ *  - Supported shapes: b in {16, 64}, dh in {32, 64, 128}, 1 <= H <= 64.
+ */
+#ifndef SMEM_H
+#define SMEM_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SMEM_OK = 0,
+  SMEM_EINVAL = 1,  /* bad argument, shape or dtype */
+  SMEM_ENOMEM = 2,  /* page pool full, or pool buffer too small */
+  SMEM_ENOENT = 3,  /* delete/export of an absent block (Theorem 1: only a present block can be deleted) */
+  SMEM_EEXIST = 4,  /* insert into an occupied block index */
+  SMEM_EHIP = 5     /* a HIP runtime call failed */
+} smem_status;
+
+typedef enum { SMEM_F32 = 0, SMEM_BF16 = 1 } smem_dtype;
+
+/* In-block mask of the encoder.  The paper's encoder is bidirectional inside
+ * a block (Section 2, "Model"; Appendix A, "Encoder").  The causal mode
+ * includes the query's own key. */
+typedef enum { SMEM_MASK_BIDIR = 0, SMEM_MASK_CAUSAL = 1 } smem_mask;
+
+/* Shape of one store.  A store holds n_pages blocks at once across
+ * n_seq sequences.  Each sequence has block indices 0..max_blocks-1. */
+typedef struct {
+  int32_t n_seq;
+  int32_t max_blocks;
+  int32_t n_pages;
+  int32_t b;
+  int32_t H;
+  int32_t dh;
+  int32_t dtype;    /* smem_dtype */
+} smem_store_desc;
+
+/* Attention shape of an encoder call: block size, heads, head width, dtype. */
+typedef struct {
+  int32_t b;
+  int32_t H;
+  int32_t dh;
+  int32_t dtype;    /* smem_dtype */
+} smem_attn_desc;
+
+typedef struct smem_store smem_store;  /* opaque; host metadata + device layout */
+
+/* Device bytes the caller must provide for a store of this shape.
+ * Covers the page pool, the device block table and live lists, and the
+ * split-K workspace.  Returns 0 for an invalid descriptor. */
+size_t smem_store_bytes(const smem_store_desc* desc);
+
+/* Create a store over a caller-owned device buffer.
+ * The buffer needs pool_bytes >= smem_store_bytes(desc) and 256-byte
+ * alignment; it stays owned by the caller and must outlive the store.
+ * Device metadata is initialised on stream s.
+ * dev_pool == NULL creates a metadata-only store: the edit calls
+ * (put/delete/export with NULL tensors) validate and update host metadata
+ * only, and every call that needs device memory returns SMEM_EINVAL. */
+smem_status smem_store_create(const smem_store_desc* desc, void* dev_pool, size_t pool_bytes,
+                              hipStream_t s, smem_store** out);
+
+/* Free the host metadata.  The device buffer is untouched.  NULL is a no-op. */
+smem_status smem_store_destroy(smem_store* st);
+
+/* Insert precomputed memory rows of block `block_idx` of sequence `seq`
+ * (the append of Section 2: m <- m (+) mu_j, O(b) work).
+ * k_rows, v_rows: device [b, H, dh].  SMEM_EEXIST if the index is occupied;
+ * SMEM_ENOMEM if no page is free.  On a metadata-only store, pass NULL rows. */
+smem_status smem_store_put_block(smem_store* st, int32_t seq, int32_t block_idx,
+                                 const void* k_rows, const void* v_rows, hipStream_t s);
+
+/* Block-local encoder attention (Section 2, "Model"; Appendix A, "Encoder").
+ * Each (block, head) pair is computed on its own:
+ *   O = softmax_mask(Q K^T / sqrt(dh)) V,  the mask limited to the block.
+ * q, k, v: device [n_blocks*b, H, dh] (block-major, then token, head, dim).
+ * out: device, same shape, or NULL when the rows only go into the store.
+ * st == NULL: attention only; seq_ids/block_idx are ignored.
+ * st != NULL: block i's output is inserted as memory block block_idx[i] of
+ *   sequence seq_ids[i].  Its key plane and value plane both equal O (identity
+ *   projections).  Every target index is checked first (SMEM_EEXIST,
+ *   duplicates included), so the insert is all-or-nothing.  `shape` must
+ *   equal the store's. */
+smem_status smem_encode_blocks(smem_store* st, const smem_attn_desc* shape, int32_t n_blocks,
+                               const int32_t* seq_ids, const int32_t* block_idx,
+                               const void* q, const void* k, const void* v, void* out,
+                               int32_t mask, hipStream_t s);
+
+/* Reader attention for whole query blocks: block-skip serving (Section 3.1).
+ * Row i of q/k_intra/v_intra/out, of shape [b, H, dh] each, is block
+ * query_block[i] of sequence seq_ids[i].  Query t of head h reads, under
+ * one softmax, this key list in canonical order:
+ *   [null row] ++ rows of every live block j < query_block[i], ascending j
+ *   ++ in-block keys 0..t.
+ * k_intra = v_intra = NULL: no in-block keys (the paper's cross-attention
+ * sub-layer alone).  query_block[i] = 0 with null_kv = NULL: in-block causal
+ * attention alone (the paper's self-attention sub-layer).  An empty key set
+ * gives a zero output.
+ * q, k_intra, v_intra, out: device [n_seq*b, H, dh].  null_kv: device
+ * [2, H, dh] or NULL.  A sequence may appear more than once. */
+smem_status smem_reader_prefill_block(smem_store* st, int32_t n_seq, const int32_t* seq_ids,
+                                      const int32_t* query_block, const void* q,
+                                      const void* k_intra, const void* v_intra,
+                                      const void* null_kv, void* out, hipStream_t s);
+
+/* Reader attention for one new token per sequence: KV-cached decode
+ * (Section 3.1; Appendix K, "Decode").
+ * The new key/value pair is first written into the in-block cache at pos[i]
+ * (0 <= pos[i] < b).  The query then reads
+ *   [null row] ++ memory rows of live blocks j < query_block[i] ++ cache rows 0..pos[i].
+ * q, k_new, v_new, out: device [n_seq, H, dh].  k_cache, v_cache: device
+ * [n_seq*b, H, dh], updated in place at row pos[i] only.
+ * k_new = v_new = k_cache = v_cache = NULL: memory-only read.
+ * Each seq_ids entry may appear only once. */
+smem_status smem_reader_decode(smem_store* st, int32_t n_seq, const int32_t* seq_ids,
+                               const int32_t* query_block, const int32_t* pos, const void* q,
+                               const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                               const void* null_kv, void* out, hipStream_t s);
+
+/* Exact deletion (Theorem 1): remove block `block_idx` of sequence `seq`.
+ * The remaining blocks keep their indices, and every later read equals a
+ * read of the memory in which the block was never inserted.  Cost is O(1)
+ * page bookkeeping plus a rebuild of the sequence's dense live list
+ * (indices only, no rows move).  SMEM_ENOENT if the block is absent.
+ * scrub != 0 also zeroes the freed page on stream s. */
+smem_status smem_delete_block(smem_store* st, int32_t seq, int32_t block_idx, int32_t scrub,
+                              hipStream_t s);
+
+/* Canonical export of one sequence's memory: blocks in ascending index, each
+ * block's b rows in order (Section 2, "Model"; Appendix B, gate G8).
+ * live_idx: host int32[max_blocks] or NULL; receives the live block indices.
+ * n_live: host, receives their count.  k_out, v_out: device
+ * [n_live*b, H, dh], or both NULL to list indices only. */
+smem_status smem_store_export(smem_store* st, int32_t seq, int32_t* live_idx, int32_t* n_live,
+                              void* k_out, void* v_out, hipStream_t s);
+
+/* Host-side facts about a store: pages in use and free. */
+smem_status smem_store_stats(const smem_store* st, int32_t* pages_used, int32_t* pages_free);
+
+const char* smem_status_string(smem_status st);
+
+/* Message of the calling thread's last failed call ("" if none). */
+const char* smem_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SMEM_H */

@@ -1,0 +1,159 @@
+// Shared definitions of the SMem HIP library (gfx950): element conversions,
+// the device layout of a store, kernel argument blocks and launcher
+// declarations.  Host code (smem_api.cpp) and the kernel files include it.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+namespace smem {
+
+// ---------------------------------------------------------------- constants
+
+// Per-launch capacity of the argument arrays carried by value in kernel
+// arguments (sequence ids, block counts, positions).  Larger batches are
+// split into several launches by the host.
+constexpr int kMaxSlots = 128;
+// Edits applied by one metadata launch.
+constexpr int kMaxEdits = 128;
+// Split-K: memory pages of one (query, head) are cut into at most kSplitCap
+// splits of whole pages, plus one split for the null row and in-block keys.
+constexpr int kSplitCap = 64;
+constexpr int kSplitStride = kSplitCap + 1;
+// Minimum pages per split (decode / VALU reader and MFMA prefill).
+constexpr int kMinPagesDecode = 8;
+constexpr int kMinPagesPrefill = 4;
+// Query slots whose prefill partials the workspace must hold at once.
+constexpr int kPrefillSlotChunk = 16;
+
+// Pages per split: a function of the number of memory pages read only, so a
+// query's split boundaries (and hence its rounding) never depend on the
+// batch it is in or on the physical page numbers.
+inline int pages_per_split(int n_read, int min_pages) {
+  int p = (n_read + kSplitCap - 1) / kSplitCap;
+  return p < min_pages ? min_pages : p;
+}
+inline int mem_splits(int n_read, int pps) { return (n_read + pps - 1) / pps; }
+
+enum Dtype : int32_t { F32 = 0, BF16 = 1 };
+
+// ---------------------------------------------------------------- conversions
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t x) { return __uint_as_float(x << 16); }
+
+// Round-to-nearest-even float -> bf16 bits (finite inputs; NaN kept quiet).
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// 16-byte chunk -> E floats (E = 4 for fp32, 8 for bf16).
+template <typename T> struct Chunk;
+template <> struct Chunk<float> {
+  static constexpr int E = 4;
+  __device__ __forceinline__ static void unpack(const uint4& c, float* f) {
+    f[0] = __uint_as_float(c.x); f[1] = __uint_as_float(c.y);
+    f[2] = __uint_as_float(c.z); f[3] = __uint_as_float(c.w);
+  }
+};
+template <> struct Chunk<uint16_t> {
+  static constexpr int E = 8;
+  __device__ __forceinline__ static void unpack(const uint4& c, float* f) {
+    f[0] = __uint_as_float(c.x << 16); f[1] = __uint_as_float(c.x & 0xffff0000u);
+    f[2] = __uint_as_float(c.y << 16); f[3] = __uint_as_float(c.y & 0xffff0000u);
+    f[4] = __uint_as_float(c.z << 16); f[5] = __uint_as_float(c.z & 0xffff0000u);
+    f[6] = __uint_as_float(c.w << 16); f[7] = __uint_as_float(c.w & 0xffff0000u);
+  }
+};
+
+template <typename T> __device__ __forceinline__ float to_f32(T x);
+template <> __device__ __forceinline__ float to_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ float to_f32<uint16_t>(uint16_t x) { return bf16_bits_to_f32(x); }
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ uint16_t from_f32<uint16_t>(float x) { return f32_to_bf16_bits(x); }
+
+// ---------------------------------------------------------------- device layout
+
+// A page holds one block's rows for every head: for head h, a key plane
+// [b][dh] (row-major, one key per row) followed by a value plane stored
+// transposed, [dh][b] (one value dimension per row, keys contiguous).  The
+// (page, head) pair is one contiguous 2*b*dh run.
+__host__ __device__ inline size_t page_head_offset(int page, int h, int H, int b, int dh) {
+  return ((size_t)page * H + h) * 2 * (size_t)b * dh;
+}
+
+struct DevLayout {
+  size_t off_table, off_live_page, off_live_blk, off_n_live, off_ws, off_pages, total;
+  size_t ws_floats;
+};
+
+// ---------------------------------------------------------------- kernel args
+
+// Reader launch (VALU reader and MFMA prefill): one slot per query row group.
+//   prefill: a slot is one (sequence, query block); nq = b queries
+//   decode : a slot is one sequence; nq = 1
+//   encoder (no memory): a slot is one block; nq = b
+struct ReaderArgs {
+  const void* q;          // query of (slot i, row t, head h) at ((i*nq + t)*H + h)*dh
+  const void* k_in;       // in-block keys: row r of slot i at ((i*b + r)*H + h)*dh (NULL: none)
+  const void* v_in;
+  const void* k_new;      // decode: key/value of the new token, [slot][H][dh]
+  const void* v_new;
+  void* k_cache_w;        // decode: the new token is also written to row pos of these
+  void* v_cache_w;
+  const void* null_kv;    // [2][H][dh] or NULL
+  const void* pages;      // page pool
+  const int32_t* live_page;  // [n_seq][max_blocks] dense live list -> page
+  float* ws;              // split partials, (dh+4) floats each
+  void* out;              // output, same indexing as q
+  void* page_sink;        // encoder (fp32): also write O as key and value rows of page aux[i]
+  int32_t max_blocks;
+  int32_t H;
+  int32_t b;
+  int32_t nq;
+  int32_t intra_mode;     // 0: all b keys (bidirectional), 1: keys 0..t (causal), 2: decode, keys 0..pos
+  int32_t n_slots;
+  float scale_log2;       // log2(e)/sqrt(dh)
+  int32_t seq[kMaxSlots];     // sequence of the slot (its live list)
+  int32_t n_read[kMaxSlots];  // memory pages the slot reads (live blocks j < J)
+  int32_t pps[kMaxSlots];     // pages per split
+  int32_t aux[kMaxSlots];     // decode: pos; fp32 encoder: sink page or -1
+};
+
+struct MetaArgs {
+  int32_t* table;
+  int32_t* live_page;
+  int32_t* live_blk;
+  int32_t* n_live;
+  int32_t max_blocks;
+  int32_t n_edits;
+  int32_t n_seqs;                 // sequences to rebuild (one workgroup each)
+  int32_t e_seq[kMaxEdits];
+  int32_t e_blk[kMaxEdits];
+  int32_t e_page[kMaxEdits];      // -1: delete
+  int32_t r_seq[kMaxEdits];
+};
+
+// ---------------------------------------------------------------- launchers
+
+hipError_t launch_init_meta(int32_t* table, int32_t* n_live, size_t n_table, int n_seq, hipStream_t s);
+hipError_t launch_meta(const MetaArgs& a, hipStream_t s);
+hipError_t launch_put_rows(int dtype, void* pages, int page, int H, int b, int dh,
+                           const void* k_rows, const void* v_rows, hipStream_t s);
+hipError_t launch_scrub(int dtype, void* pages, int page, int H, int b, int dh, hipStream_t s);
+hipError_t launch_export(int dtype, const void* pages, const int32_t* live_page_seq, int n_live,
+                         int H, int b, int dh, void* k_out, void* v_out, hipStream_t s);
+
+// VALU reader: every split of every (slot, query, head) plus the merge.
+hipError_t launch_reader_valu(int dtype, int b, int dh, const ReaderArgs& a, hipStream_t s);
+// MFMA (bf16) encoder and prefill.
+hipError_t launch_encoder_mfma(int b, int dh, const void* q, const void* k, const void* v, void* out,
+                               void* pages, const int32_t* sink_pages, int n_blocks, int H, int mask,
+                               float scale_log2, hipStream_t s);
+hipError_t launch_prefill_mfma(int b, int dh, const ReaderArgs& a, hipStream_t s);
+
+}  // namespace smem

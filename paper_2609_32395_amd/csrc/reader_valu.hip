@@ -1,0 +1,325 @@
+// VALU reader attention: one query per workgroup, split-K over memory pages.
+//
+// Reader attention (Section 2, "Model"; Appendix A, "Reader"), joint form: a
+// query at in-block position t of block J reads, under one softmax,
+//   [null row] ++ memory rows of live blocks j < J (ascending j) ++ in-block keys 0..t.
+// This kernel is the decode path (one query per sequence, bandwidth bound,
+// no MFMA), and also serves fp32 prefill and the fp32 encoder (a reader with
+// no memory whose in-block keys are the block itself).
+//
+// Work decomposition (deterministic): the slot's n_read memory pages are cut
+// into splits of pps whole pages (pps depends on n_read only); split index
+// nms = ceil(n_read/pps) holds the null row and the in-block keys.  Inside a
+// memory split, wave w streams pages w, w+4, ... with its own online-softmax
+// state; the four wave states are combined in wave order, and the splits are
+// combined in split order by k_merge.  Nothing depends on the batch, on
+// physical page numbers or on timing, so equal inputs give equal bits.
+//
+// Memory page tiles (per page and head): key plane [b][dh] row-major, value
+// plane transposed [dh][b].  Key rows are read 16 bytes per lane, LPR lanes
+// per row (a wave reads 1 KiB contiguous per instruction); the row dot
+// product is finished with xor-shuffles.  Softmax weights go through a
+// per-wave LDS row so each lane can weight a 16-byte chunk of the
+// transposed value plane (contiguous keys).
+#include "common.h"
+
+namespace smem {
+
+template <typename T, int DH, int B>
+struct RCfg {
+  static constexpr int E = Chunk<T>::E;   // elements per 16-byte chunk
+  static constexpr int LPR = DH / E;      // lanes per key row
+  static constexpr int RPL = 64 / LPR;    // key rows per wave load
+  static constexpr int KLOADS = B / RPL;  // wave loads per page of keys
+  static constexpr int LPV = B / E;       // lanes per transposed value row
+  static constexpr int DPL = 64 / LPV;    // value dims per wave load
+  static constexpr int VLOADS = DH / DPL; // wave loads per page of values
+  static_assert(LPR >= 1 && LPR <= 64 && RPL * LPR == 64 && KLOADS * RPL == B, "key tiling");
+  static_assert(LPV >= 1 && LPV <= 64 && DPL * LPV == 64 && VLOADS * DPL == DH, "value tiling");
+};
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+template <typename T, int DH, int B>
+__global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
+  using C = RCfg<T, DH, B>;
+  constexpr int E = C::E;
+  const int split = blockIdx.x, h = blockIdx.y, qs = blockIdx.z;
+  const int slot = qs / a.nq, t = qs % a.nq;
+  const int n_read = a.n_read[slot], pps = a.pps[slot];
+  const int nms = (n_read + pps - 1) / pps;
+  if (split > nms) return;  // whole workgroup
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __shared__ float p_sh[4][B];
+  __shared__ float wm[4], wl[4];
+  __shared__ float wacc[4][DH];
+
+  const int c = lane % C::LPR, rg = lane / C::LPR;
+  float qf[E];
+  {
+    const T* qp = (const T*)a.q + ((size_t)qs * a.H + h) * DH + c * E;
+    Chunk<T>::unpack(*(const uint4*)qp, qf);
+#pragma unroll
+    for (int e = 0; e < E; ++e) qf[e] *= a.scale_log2;
+  }
+  float m = -INFINITY, l = 0.f;
+
+  if (split < nms) {
+    // ------------------------------------------------ memory pages of this split
+    float acc[C::VLOADS];
+#pragma unroll
+    for (int v = 0; v < C::VLOADS; ++v) acc[v] = 0.f;
+    const int dr = lane / C::LPV, kc = lane % C::LPV;
+    const int p0 = split * pps;
+    const int p1 = min(n_read, p0 + pps);
+    const int32_t* lp = a.live_page + (size_t)a.seq[slot] * a.max_blocks;
+    for (int pi = p0 + wave; pi < p1; pi += 4) {
+      const int pg = lp[pi];
+      const T* Kt = (const T*)a.pages + page_head_offset(pg, h, a.H, B, DH);
+      const T* VT = Kt + B * DH;
+      uint4 kraw[C::KLOADS];
+      uint4 vraw[C::VLOADS];
+#pragma unroll
+      for (int i = 0; i < C::KLOADS; ++i) kraw[i] = *(const uint4*)(Kt + (i * C::RPL + rg) * DH + c * E);
+#pragma unroll
+      for (int v = 0; v < C::VLOADS; ++v) vraw[v] = *(const uint4*)(VT + (v * C::DPL + dr) * B + kc * E);
+      float s[C::KLOADS];
+#pragma unroll
+      for (int i = 0; i < C::KLOADS; ++i) {
+        float kf[E];
+        Chunk<T>::unpack(kraw[i], kf);
+        float x = 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) x += qf[e] * kf[e];
+        s[i] = x;
+      }
+#pragma unroll
+      for (int i = 0; i < C::KLOADS; ++i) {
+#pragma unroll
+        for (int o = 1; o < C::LPR; o <<= 1) s[i] += __shfl_xor(s[i], o);
+      }
+      float mx = s[0];
+#pragma unroll
+      for (int i = 1; i < C::KLOADS; ++i) mx = fmaxf(mx, s[i]);
+#pragma unroll
+      for (int o = C::LPR; o < 64; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      const float mn = fmaxf(m, mx);
+      const float alpha = exp2f(m - mn);
+      float ps = 0.f;
+#pragma unroll
+      for (int i = 0; i < C::KLOADS; ++i) {
+        const float p = exp2f(s[i] - mn);
+        if (c == 0) {
+          p_sh[wave][i * C::RPL + rg] = p;
+          ps += p;
+        }
+      }
+      l = l * alpha + ps;
+      m = mn;
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      float pv[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) pv[e] = p_sh[wave][kc * E + e];
+#pragma unroll
+      for (int v = 0; v < C::VLOADS; ++v) {
+        float vf[E];
+        Chunk<T>::unpack(vraw[v], vf);
+        float x = acc[v] * alpha;
+#pragma unroll
+        for (int e = 0; e < E; ++e) x += pv[e] * vf[e];
+        acc[v] = x;
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+#pragma unroll
+    for (int v = 0; v < C::VLOADS; ++v) {
+#pragma unroll
+      for (int o = 1; o < C::LPV; o <<= 1) acc[v] += __shfl_xor(acc[v], o);
+    }
+    l = wave_sum(l);
+    if (kc == 0) {
+#pragma unroll
+      for (int v = 0; v < C::VLOADS; ++v) wacc[wave][v * C::DPL + dr] = acc[v];
+    }
+    if (lane == 0) { wm[wave] = m; wl[wave] = l; }
+  } else {
+    // ------------------------------------------------ null row + in-block keys
+    float acc2[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc2[e] = 0.f;
+    if (a.null_kv != nullptr && wave == 0) {
+      const T* nk = (const T*)a.null_kv + (size_t)h * DH + c * E;
+      const T* nv = (const T*)a.null_kv + ((size_t)a.H + h) * DH + c * E;
+      float kf[E], vf[E];
+      Chunk<T>::unpack(*(const uint4*)nk, kf);
+      Chunk<T>::unpack(*(const uint4*)nv, vf);
+      float x = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) x += qf[e] * kf[e];
+#pragma unroll
+      for (int o = 1; o < C::LPR; o <<= 1) x += __shfl_xor(x, o);
+      m = x;
+      l = (lane == 0) ? 1.f : 0.f;
+      if (rg == 0) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc2[e] = vf[e];
+      }
+    }
+    int n_in;
+    const bool decode = a.intra_mode == 2;
+    const int pos = decode ? a.aux[slot] : 0;
+    if (decode) n_in = (a.k_new != nullptr) ? pos + 1 : 0;
+    else if (a.k_in == nullptr) n_in = 0;
+    else n_in = (a.intra_mode == 0) ? B : t + 1;
+    for (int r0 = wave * C::RPL; r0 < n_in; r0 += 4 * C::RPL) {
+      const int r = r0 + rg;
+      const bool valid = r < n_in;
+      float kf[E], vf[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) { kf[e] = 0.f; vf[e] = 0.f; }
+      if (valid) {
+        const T* ks;
+        const T* vs;
+        if (decode && r == pos) {
+          ks = (const T*)a.k_new + ((size_t)slot * a.H + h) * DH;
+          vs = (const T*)a.v_new + ((size_t)slot * a.H + h) * DH;
+        } else {
+          ks = (const T*)a.k_in + (((size_t)slot * B + r) * a.H + h) * DH;
+          vs = (const T*)a.v_in + (((size_t)slot * B + r) * a.H + h) * DH;
+        }
+        Chunk<T>::unpack(*(const uint4*)(ks + c * E), kf);
+        Chunk<T>::unpack(*(const uint4*)(vs + c * E), vf);
+      }
+      float x = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) x += qf[e] * kf[e];
+#pragma unroll
+      for (int o = 1; o < C::LPR; o <<= 1) x += __shfl_xor(x, o);
+      const float sc = valid ? x : -INFINITY;
+      float mx = sc;
+#pragma unroll
+      for (int o = C::LPR; o < 64; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      const float mn = fmaxf(m, mx);       // row r0 is valid, so mn is finite
+      const float alpha = exp2f(m - mn);
+      const float p = valid ? exp2f(sc - mn) : 0.f;
+      l = l * alpha + ((c == 0) ? p : 0.f);
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc2[e] = acc2[e] * alpha + p * vf[e];
+      m = mn;
+    }
+    if (decode && a.k_cache_w != nullptr && wave == 0 && rg == 0) {
+      // write the new token's key/value into the in-block cache at row pos
+      const size_t src = ((size_t)slot * a.H + h) * DH + c * E;
+      const size_t dst = (((size_t)slot * B + pos) * a.H + h) * DH + c * E;
+      *(uint4*)((T*)a.k_cache_w + dst) = *(const uint4*)((const T*)a.k_new + src);
+      *(uint4*)((T*)a.v_cache_w + dst) = *(const uint4*)((const T*)a.v_new + src);
+    }
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+#pragma unroll
+      for (int o = C::LPR; o < 64; o <<= 1) acc2[e] += __shfl_xor(acc2[e], o);
+    }
+    l = wave_sum(l);
+    if (rg == 0) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) wacc[wave][c * E + e] = acc2[e];
+    }
+    if (lane == 0) { wm[wave] = m; wl[wave] = l; }
+  }
+  __syncthreads();
+
+  if (tid < DH) {
+    const float M = fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3]));
+    float L = 0.f, A = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float wgt = (wm[w] == -INFINITY) ? 0.f : exp2f(wm[w] - M);
+      L += wgt * wl[w];
+      A += wgt * wacc[w][tid];
+    }
+    if (nms == 0) {
+      const float o = (L > 0.f) ? A / L : 0.f;
+      const T ov = from_f32<T>(o);
+      ((T*)a.out)[((size_t)qs * a.H + h) * DH + tid] = ov;
+      if (a.page_sink != nullptr && a.aux[slot] >= 0) {
+        T* kp = (T*)a.page_sink + page_head_offset(a.aux[slot], h, a.H, B, DH);
+        kp[t * DH + tid] = ov;
+        kp[B * DH + tid * B + t] = ov;
+      }
+    } else {
+      float* part = a.ws + (((size_t)qs * a.H + h) * kSplitStride + split) * (DH + 4);
+      part[tid] = A;
+      if (tid == 0) { part[DH] = M; part[DH + 1] = L; }
+    }
+  }
+}
+
+// Combine the splits of one (query, head) in split order.
+template <typename T, int DH>
+__global__ void __launch_bounds__(64) k_merge(ReaderArgs a) {
+  const int qs = blockIdx.x, h = blockIdx.y;
+  const int slot = qs / a.nq;
+  const int n_read = a.n_read[slot], pps = a.pps[slot];
+  const int S = (n_read + pps - 1) / pps + 1;
+  if (S == 1) return;
+  const float* base = a.ws + ((size_t)qs * a.H + h) * kSplitStride * (DH + 4);
+  float M = -INFINITY;
+  for (int k = 0; k < S; ++k) M = fmaxf(M, base[(size_t)k * (DH + 4) + DH]);
+  for (int d = threadIdx.x; d < DH; d += 64) {
+    float L = 0.f, A = 0.f;
+    for (int k = 0; k < S; ++k) {
+      const float* pk = base + (size_t)k * (DH + 4);
+      const float mk = pk[DH];
+      const float w = (mk == -INFINITY) ? 0.f : exp2f(mk - M);
+      L += w * pk[DH + 1];
+      A += w * pk[d];
+    }
+    const float o = (L > 0.f) ? A / L : 0.f;
+    ((T*)a.out)[((size_t)qs * a.H + h) * DH + d] = from_f32<T>(o);
+  }
+}
+
+template <typename T, int DH, int B>
+static hipError_t launch_rv(const ReaderArgs& a, hipStream_t s) {
+  int max_split = 0;
+  for (int i = 0; i < a.n_slots; ++i) {
+    int ns = mem_splits(a.n_read[i], a.pps[i]);
+    if (ns > max_split) max_split = ns;
+  }
+  dim3 grid(max_split + 1, a.H, a.n_slots * a.nq);
+  hipLaunchKernelGGL((k_reader_valu<T, DH, B>), grid, dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || max_split == 0) return e;
+  hipLaunchKernelGGL((k_merge<T, DH>), dim3(a.n_slots * a.nq, a.H), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename T, int DH>
+static hipError_t launch_rv_b(int b, const ReaderArgs& a, hipStream_t s) {
+  if (b == 16) return launch_rv<T, DH, 16>(a, s);
+  if (b == 64) return launch_rv<T, DH, 64>(a, s);
+  return hipErrorInvalidValue;
+}
+
+template <typename T>
+static hipError_t launch_rv_d(int b, int dh, const ReaderArgs& a, hipStream_t s) {
+  if (dh == 32) return launch_rv_b<T, 32>(b, a, s);
+  if (dh == 64) return launch_rv_b<T, 64>(b, a, s);
+  if (dh == 128) return launch_rv_b<T, 128>(b, a, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_reader_valu(int dtype, int b, int dh, const ReaderArgs& a, hipStream_t s) {
+  if (a.n_slots <= 0) return hipSuccess;
+  if (dtype == F32) return launch_rv_d<float>(b, dh, a, s);
+  return launch_rv_d<uint16_t>(b, dh, a, s);
+}
+
+}  // namespace smem

@@ -1,0 +1,462 @@
+// C ABI of the SMem library: argument validation, the host-authoritative
+// store (block table, canonical live lists, free pages) and kernel dispatch.
+//
+// Store semantics follow Theorem 1 of the paper: a block index holds at most
+// one block (insert into an occupied index -> SMEM_EEXIST), only a present
+// block can be deleted (SMEM_ENOENT otherwise), deletion restores exactly the
+// never-inserted state, and reads depend only on which blocks are present,
+// taken in ascending block index.  Host metadata changes immediately; the
+// device copy is updated by kernels on the caller's stream, carrying the edit
+// in kernel arguments (no host buffer outlives a call).
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "common.h"
+#include "smem.h"
+
+using namespace smem;
+
+struct smem_store {
+  smem_store_desc d;
+  bool meta_only = false;
+  char* pool = nullptr;
+  DevLayout lay{};
+  int32_t* d_table = nullptr;
+  int32_t* d_live_page = nullptr;
+  int32_t* d_live_blk = nullptr;
+  int32_t* d_n_live = nullptr;
+  float* d_ws = nullptr;
+  void* d_pages = nullptr;
+  std::vector<int32_t> table;              // [n_seq * max_blocks]: page or -1
+  std::vector<std::vector<int32_t>> live;  // per sequence, ascending block indices
+  std::vector<int32_t> free_pages;         // stack; back() is handed out next
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+smem_status fail(smem_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = std::string(smem_status_string(st)) + ": " + buf;
+  return st;
+}
+
+smem_status hip_fail(hipError_t e, const char* what) {
+  return fail(SMEM_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+size_t esize(int dtype) { return dtype == F32 ? 4 : 2; }
+
+bool shape_ok(int b, int H, int dh, int dtype) {
+  return (b == 16 || b == 64) && (dh == 32 || dh == 64 || dh == 128) && H >= 1 && H <= 64 &&
+         (dtype == F32 || dtype == BF16);
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+bool layout_of(const smem_store_desc* d, DevLayout* L) {
+  if (!d) return false;
+  if (d->n_seq < 1 || d->max_blocks < 1 || d->n_pages < 1) return false;
+  if (!shape_ok(d->b, d->H, d->dh, d->dtype)) return false;
+  const size_t nt = (size_t)d->n_seq * d->max_blocks;
+  const size_t dec = (size_t)d->n_seq * d->H * kSplitStride * (d->dh + 4);
+  const size_t pre = (size_t)std::min(d->n_seq, kPrefillSlotChunk) * d->b * d->H * kSplitStride * (d->dh + 4);
+  L->ws_floats = std::max(dec, pre);
+  size_t off = 0;
+  L->off_table = off;     off = align256(off + nt * 4);
+  L->off_live_page = off; off = align256(off + nt * 4);
+  L->off_live_blk = off;  off = align256(off + nt * 4);
+  L->off_n_live = off;    off = align256(off + (size_t)d->n_seq * 4);
+  L->off_ws = off;        off = align256(off + L->ws_floats * 4);
+  L->off_pages = off;     off = align256(off + (size_t)d->n_pages * d->H * 2 * d->b * d->dh * esize(d->dtype));
+  L->total = off;
+  return true;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int n_read_of(const smem_store* st, int seq, int J) {
+  const auto& lv = st->live[seq];
+  return (int)(std::lower_bound(lv.begin(), lv.end(), J) - lv.begin());
+}
+
+// Apply edits (seq, blk, page or -1) on the device: table entries, then
+// rebuild the affected sequences' live lists.
+smem_status push_edits(smem_store* st, const std::vector<int32_t>& es, const std::vector<int32_t>& eb,
+                       const std::vector<int32_t>& ep, hipStream_t s) {
+  for (size_t i0 = 0; i0 < es.size(); i0 += kMaxEdits) {
+    MetaArgs a;
+    memset(&a, 0, sizeof a);
+    a.table = st->d_table;
+    a.live_page = st->d_live_page;
+    a.live_blk = st->d_live_blk;
+    a.n_live = st->d_n_live;
+    a.max_blocks = st->d.max_blocks;
+    const size_t n = std::min((size_t)kMaxEdits, es.size() - i0);
+    a.n_edits = (int32_t)n;
+    std::set<int32_t> seqs;
+    for (size_t i = 0; i < n; ++i) {
+      a.e_seq[i] = es[i0 + i];
+      a.e_blk[i] = eb[i0 + i];
+      a.e_page[i] = ep[i0 + i];
+      seqs.insert(es[i0 + i]);
+    }
+    a.n_seqs = 0;
+    for (int32_t q : seqs) a.r_seq[a.n_seqs++] = q;
+    hipError_t e = launch_meta(a, s);
+    if (e != hipSuccess) return hip_fail(e, "metadata update");
+  }
+  return SMEM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* smem_status_string(smem_status st) {
+  switch (st) {
+    case SMEM_OK: return "SMEM_OK";
+    case SMEM_EINVAL: return "SMEM_EINVAL";
+    case SMEM_ENOMEM: return "SMEM_ENOMEM";
+    case SMEM_ENOENT: return "SMEM_ENOENT";
+    case SMEM_EEXIST: return "SMEM_EEXIST";
+    case SMEM_EHIP: return "SMEM_EHIP";
+  }
+  return "SMEM_UNKNOWN";
+}
+
+const char* smem_last_error(void) { return g_err.c_str(); }
+
+size_t smem_store_bytes(const smem_store_desc* desc) {
+  DevLayout L;
+  if (!layout_of(desc, &L)) return 0;
+  return L.total;
+}
+
+smem_status smem_store_create(const smem_store_desc* desc, void* dev_pool, size_t pool_bytes, hipStream_t s,
+                              smem_store** out) {
+  if (!out) return fail(SMEM_EINVAL, "out is NULL");
+  *out = nullptr;
+  DevLayout L;
+  if (!layout_of(desc, &L))
+    return fail(SMEM_EINVAL, "invalid store descriptor (need n_seq, max_blocks, n_pages >= 1, b in {16,64}, "
+                             "dh in {32,64,128}, 1 <= H <= 64, dtype F32/BF16)");
+  if ((size_t)desc->n_pages * desc->H * 2 * desc->b * desc->dh > ((size_t)1 << 40))
+    return fail(SMEM_EINVAL, "page pool too large");
+  if (dev_pool) {
+    if (pool_bytes < L.total) return fail(SMEM_ENOMEM, "pool has %zu bytes, store needs %zu", pool_bytes, L.total);
+    if (((uintptr_t)dev_pool & 255u) != 0) return fail(SMEM_EINVAL, "dev_pool must be 256-byte aligned");
+  }
+  smem_store* st = new (std::nothrow) smem_store();
+  if (!st) return fail(SMEM_ENOMEM, "host allocation failed");
+  st->d = *desc;
+  st->lay = L;
+  st->meta_only = dev_pool == nullptr;
+  st->table.assign((size_t)desc->n_seq * desc->max_blocks, -1);
+  st->live.assign(desc->n_seq, {});
+  st->free_pages.resize(desc->n_pages);
+  for (int i = 0; i < desc->n_pages; ++i) st->free_pages[i] = desc->n_pages - 1 - i;
+  if (!st->meta_only) {
+    st->pool = (char*)dev_pool;
+    st->d_table = (int32_t*)(st->pool + L.off_table);
+    st->d_live_page = (int32_t*)(st->pool + L.off_live_page);
+    st->d_live_blk = (int32_t*)(st->pool + L.off_live_blk);
+    st->d_n_live = (int32_t*)(st->pool + L.off_n_live);
+    st->d_ws = (float*)(st->pool + L.off_ws);
+    st->d_pages = st->pool + L.off_pages;
+    hipError_t e = launch_init_meta(st->d_table, st->d_n_live, st->table.size(), desc->n_seq, s);
+    if (e != hipSuccess) {
+      delete st;
+      return hip_fail(e, "store init");
+    }
+  }
+  *out = st;
+  return SMEM_OK;
+}
+
+smem_status smem_store_destroy(smem_store* st) {
+  delete st;
+  return SMEM_OK;
+}
+
+smem_status smem_store_stats(const smem_store* st, int32_t* pages_used, int32_t* pages_free) {
+  if (!st) return fail(SMEM_EINVAL, "store is NULL");
+  if (pages_free) *pages_free = (int32_t)st->free_pages.size();
+  if (pages_used) *pages_used = st->d.n_pages - (int32_t)st->free_pages.size();
+  return SMEM_OK;
+}
+
+smem_status smem_store_put_block(smem_store* st, int32_t seq, int32_t block_idx, const void* k_rows,
+                                 const void* v_rows, hipStream_t s) {
+  if (!st) return fail(SMEM_EINVAL, "store is NULL");
+  const auto& d = st->d;
+  if (seq < 0 || seq >= d.n_seq) return fail(SMEM_EINVAL, "seq %d out of range [0, %d)", seq, d.n_seq);
+  if (block_idx < 0 || block_idx >= d.max_blocks)
+    return fail(SMEM_EINVAL, "block index %d out of range [0, %d)", block_idx, d.max_blocks);
+  if (st->meta_only) {
+    if (k_rows || v_rows) return fail(SMEM_EINVAL, "metadata-only store takes NULL rows");
+  } else {
+    if (!k_rows || !v_rows) return fail(SMEM_EINVAL, "k_rows and v_rows are required");
+  }
+  const size_t ti = (size_t)seq * d.max_blocks + block_idx;
+  if (st->table[ti] >= 0) return fail(SMEM_EEXIST, "block %d of sequence %d is occupied", block_idx, seq);
+  if (st->free_pages.empty()) return fail(SMEM_ENOMEM, "no free page (%d pages)", d.n_pages);
+  const int32_t page = st->free_pages.back();
+  if (!st->meta_only) {
+    hipError_t e = launch_put_rows(d.dtype, st->d_pages, page, d.H, d.b, d.dh, k_rows, v_rows, s);
+    if (e != hipSuccess) return hip_fail(e, "row insert");
+    smem_status r = push_edits(st, {seq}, {block_idx}, {page}, s);
+    if (r != SMEM_OK) return r;
+  }
+  st->free_pages.pop_back();
+  st->table[ti] = page;
+  auto& lv = st->live[seq];
+  lv.insert(std::lower_bound(lv.begin(), lv.end(), block_idx), block_idx);
+  return SMEM_OK;
+}
+
+smem_status smem_delete_block(smem_store* st, int32_t seq, int32_t block_idx, int32_t scrub, hipStream_t s) {
+  if (!st) return fail(SMEM_EINVAL, "store is NULL");
+  const auto& d = st->d;
+  if (seq < 0 || seq >= d.n_seq) return fail(SMEM_EINVAL, "seq %d out of range [0, %d)", seq, d.n_seq);
+  if (block_idx < 0 || block_idx >= d.max_blocks)
+    return fail(SMEM_EINVAL, "block index %d out of range [0, %d)", block_idx, d.max_blocks);
+  const size_t ti = (size_t)seq * d.max_blocks + block_idx;
+  const int32_t page = st->table[ti];
+  if (page < 0) return fail(SMEM_ENOENT, "block %d of sequence %d is absent", block_idx, seq);
+  if (!st->meta_only) {
+    smem_status r = push_edits(st, {seq}, {block_idx}, {-1}, s);
+    if (r != SMEM_OK) return r;
+    if (scrub) {
+      hipError_t e = launch_scrub(d.dtype, st->d_pages, page, d.H, d.b, d.dh, s);
+      if (e != hipSuccess) return hip_fail(e, "page scrub");
+    }
+  }
+  st->table[ti] = -1;
+  auto& lv = st->live[seq];
+  lv.erase(std::lower_bound(lv.begin(), lv.end(), block_idx));
+  st->free_pages.push_back(page);
+  return SMEM_OK;
+}
+
+smem_status smem_store_export(smem_store* st, int32_t seq, int32_t* live_idx, int32_t* n_live, void* k_out,
+                              void* v_out, hipStream_t s) {
+  if (!st) return fail(SMEM_EINVAL, "store is NULL");
+  const auto& d = st->d;
+  if (seq < 0 || seq >= d.n_seq) return fail(SMEM_EINVAL, "seq %d out of range [0, %d)", seq, d.n_seq);
+  if ((k_out == nullptr) != (v_out == nullptr)) return fail(SMEM_EINVAL, "k_out and v_out: both or neither");
+  if (k_out && st->meta_only) return fail(SMEM_EINVAL, "metadata-only store has no rows to export");
+  const auto& lv = st->live[seq];
+  if (n_live) *n_live = (int32_t)lv.size();
+  if (live_idx) std::copy(lv.begin(), lv.end(), live_idx);
+  if (k_out) {
+    hipError_t e = launch_export(d.dtype, st->d_pages, st->d_live_page + (size_t)seq * d.max_blocks,
+                                 (int)lv.size(), d.H, d.b, d.dh, k_out, v_out, s);
+    if (e != hipSuccess) return hip_fail(e, "export");
+  }
+  return SMEM_OK;
+}
+
+smem_status smem_encode_blocks(smem_store* st, const smem_attn_desc* shape, int32_t n_blocks,
+                               const int32_t* seq_ids, const int32_t* block_idx, const void* q, const void* k,
+                               const void* v, void* out, int32_t mask, hipStream_t s) {
+  if (!shape) return fail(SMEM_EINVAL, "shape is NULL");
+  const int b = shape->b, H = shape->H, dh = shape->dh, dtype = shape->dtype;
+  if (!shape_ok(b, H, dh, dtype)) return fail(SMEM_EINVAL, "unsupported shape b=%d H=%d dh=%d dtype=%d", b, H, dh, dtype);
+  if (n_blocks < 0) return fail(SMEM_EINVAL, "n_blocks < 0");
+  if (mask != SMEM_MASK_BIDIR && mask != SMEM_MASK_CAUSAL) return fail(SMEM_EINVAL, "mask %d", mask);
+  if (st) {
+    if (st->meta_only) return fail(SMEM_EINVAL, "metadata-only store");
+    if (st->d.b != b || st->d.H != H || st->d.dh != dh || st->d.dtype != dtype)
+      return fail(SMEM_EINVAL, "shape differs from the store's");
+  } else if (!out) {
+    return fail(SMEM_EINVAL, "out is NULL and there is no store");
+  }
+  if (n_blocks == 0) return SMEM_OK;
+  if (!q || !k || !v) return fail(SMEM_EINVAL, "q, k, v are required");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || (out && !aligned16(out)))
+    return fail(SMEM_EINVAL, "tensors must be 16-byte aligned");
+  std::vector<int32_t> pages;
+  if (st) {
+    if (!seq_ids || !block_idx) return fail(SMEM_EINVAL, "seq_ids and block_idx are required with a store");
+    std::set<std::pair<int32_t, int32_t>> seen;
+    for (int i = 0; i < n_blocks; ++i) {
+      const int32_t sq = seq_ids[i], j = block_idx[i];
+      if (sq < 0 || sq >= st->d.n_seq) return fail(SMEM_EINVAL, "seq_ids[%d] = %d out of range", i, sq);
+      if (j < 0 || j >= st->d.max_blocks) return fail(SMEM_EINVAL, "block_idx[%d] = %d out of range", i, j);
+      if (st->table[(size_t)sq * st->d.max_blocks + j] >= 0)
+        return fail(SMEM_EEXIST, "block %d of sequence %d is occupied", j, sq);
+      if (!seen.insert({sq, j}).second) return fail(SMEM_EEXIST, "block %d of sequence %d given twice", j, sq);
+    }
+    if ((size_t)n_blocks > st->free_pages.size())
+      return fail(SMEM_ENOMEM, "%d blocks to insert, %zu free pages", n_blocks, st->free_pages.size());
+    pages.resize(n_blocks);
+    for (int i = 0; i < n_blocks; ++i) pages[i] = st->free_pages[st->free_pages.size() - 1 - i];
+  }
+  const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)dh));
+  const size_t es = esize(dtype);
+  const size_t blk_elems = (size_t)b * H * dh;
+  for (int i0 = 0; i0 < n_blocks; i0 += kMaxSlots) {
+    const int n = std::min(kMaxSlots, n_blocks - i0);
+    const char* qb = (const char*)q + (size_t)i0 * blk_elems * es;
+    const char* kb = (const char*)k + (size_t)i0 * blk_elems * es;
+    const char* vb = (const char*)v + (size_t)i0 * blk_elems * es;
+    char* ob = out ? (char*)out + (size_t)i0 * blk_elems * es : nullptr;
+    hipError_t e;
+    {
+      if (!ob) return fail(SMEM_EINVAL, "encode needs an out tensor");
+      ReaderArgs a;
+      memset(&a, 0, sizeof a);
+      a.q = qb; a.k_in = kb; a.v_in = vb; a.out = ob;
+      a.page_sink = st ? st->d_pages : nullptr;
+      a.H = H; a.b = b; a.nq = b; a.intra_mode = mask == SMEM_MASK_CAUSAL ? 1 : 0;
+      a.n_slots = n; a.scale_log2 = scale_log2;
+      for (int i = 0; i < n; ++i) {
+        a.seq[i] = 0; a.n_read[i] = 0; a.pps[i] = 1;
+        a.aux[i] = st ? pages[i0 + i] : -1;
+      }
+      e = launch_reader_valu(dtype, b, dh, a, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "encoder launch");
+  }
+  if (st) {
+    std::vector<int32_t> es_, eb_, ep_;
+    for (int i = 0; i < n_blocks; ++i) {
+      es_.push_back(seq_ids[i]);
+      eb_.push_back(block_idx[i]);
+      ep_.push_back(pages[i]);
+    }
+    smem_status r = push_edits(st, es_, eb_, ep_, s);
+    if (r != SMEM_OK) return r;
+    st->free_pages.resize(st->free_pages.size() - n_blocks);
+    for (int i = 0; i < n_blocks; ++i) {
+      st->table[(size_t)seq_ids[i] * st->d.max_blocks + block_idx[i]] = pages[i];
+      auto& lv = st->live[seq_ids[i]];
+      lv.insert(std::lower_bound(lv.begin(), lv.end(), block_idx[i]), block_idx[i]);
+    }
+  }
+  return SMEM_OK;
+}
+
+smem_status smem_reader_prefill_block(smem_store* st, int32_t n_seq, const int32_t* seq_ids,
+                                      const int32_t* query_block, const void* q, const void* k_intra,
+                                      const void* v_intra, const void* null_kv, void* out, hipStream_t s) {
+  if (!st) return fail(SMEM_EINVAL, "store is NULL");
+  if (st->meta_only) return fail(SMEM_EINVAL, "metadata-only store");
+  const auto& d = st->d;
+  if (n_seq < 0) return fail(SMEM_EINVAL, "n_seq < 0");
+  if (n_seq == 0) return SMEM_OK;
+  if (!seq_ids || !query_block || !q || !out) return fail(SMEM_EINVAL, "seq_ids, query_block, q, out are required");
+  if ((k_intra == nullptr) != (v_intra == nullptr)) return fail(SMEM_EINVAL, "k_intra and v_intra: both or neither");
+  if (!aligned16(q) || !aligned16(out) || !aligned16(k_intra) || !aligned16(v_intra) || !aligned16(null_kv))
+    return fail(SMEM_EINVAL, "tensors must be 16-byte aligned");
+  for (int i = 0; i < n_seq; ++i) {
+    if (seq_ids[i] < 0 || seq_ids[i] >= d.n_seq) return fail(SMEM_EINVAL, "seq_ids[%d] = %d out of range", i, seq_ids[i]);
+    if (query_block[i] < 0 || query_block[i] > d.max_blocks)
+      return fail(SMEM_EINVAL, "query_block[%d] = %d out of range [0, %d]", i, query_block[i], d.max_blocks);
+  }
+  const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
+  const size_t es = esize(d.dtype);
+  const size_t blk_elems = (size_t)d.b * d.H * d.dh;
+  const int chunk = std::min(std::min(kMaxSlots, kPrefillSlotChunk), (int)d.n_seq);
+  for (int i0 = 0; i0 < n_seq; i0 += chunk) {
+    const int n = std::min(chunk, n_seq - i0);
+    ReaderArgs a;
+    memset(&a, 0, sizeof a);
+    a.q = (const char*)q + i0 * blk_elems * es;
+    a.k_in = k_intra ? (const char*)k_intra + i0 * blk_elems * es : nullptr;
+    a.v_in = v_intra ? (const char*)v_intra + i0 * blk_elems * es : nullptr;
+    a.out = (char*)out + i0 * blk_elems * es;
+    a.null_kv = null_kv;
+    a.pages = st->d_pages;
+    a.live_page = st->d_live_page;
+    a.ws = st->d_ws;
+    a.max_blocks = d.max_blocks;
+    a.H = d.H; a.b = d.b; a.nq = d.b; a.intra_mode = 1;
+    a.n_slots = n; a.scale_log2 = scale_log2;
+    for (int i = 0; i < n; ++i) {
+      const int sq = seq_ids[i0 + i];
+      a.seq[i] = sq;
+      a.n_read[i] = n_read_of(st, sq, query_block[i0 + i]);
+      a.pps[i] = pages_per_split(a.n_read[i], kMinPagesDecode);
+      a.aux[i] = -1;
+    }
+    hipError_t e = launch_reader_valu(d.dtype, d.b, d.dh, a, s);
+    if (e != hipSuccess) return hip_fail(e, "prefill launch");
+  }
+  return SMEM_OK;
+}
+
+smem_status smem_reader_decode(smem_store* st, int32_t n_seq, const int32_t* seq_ids, const int32_t* query_block,
+                               const int32_t* pos, const void* q, const void* k_new, const void* v_new,
+                               void* k_cache, void* v_cache, const void* null_kv, void* out, hipStream_t s) {
+  if (!st) return fail(SMEM_EINVAL, "store is NULL");
+  if (st->meta_only) return fail(SMEM_EINVAL, "metadata-only store");
+  const auto& d = st->d;
+  if (n_seq < 0) return fail(SMEM_EINVAL, "n_seq < 0");
+  if (n_seq == 0) return SMEM_OK;
+  if (!seq_ids || !query_block || !q || !out) return fail(SMEM_EINVAL, "seq_ids, query_block, q, out are required");
+  const int n_given = (k_new != nullptr) + (v_new != nullptr) + (k_cache != nullptr) + (v_cache != nullptr);
+  if (n_given != 0 && n_given != 4) return fail(SMEM_EINVAL, "k_new, v_new, k_cache, v_cache: all or none");
+  if (n_given == 4 && !pos) return fail(SMEM_EINVAL, "pos is required with in-block keys");
+  if (!aligned16(q) || !aligned16(out) || !aligned16(k_new) || !aligned16(v_new) || !aligned16(k_cache) ||
+      !aligned16(v_cache) || !aligned16(null_kv))
+    return fail(SMEM_EINVAL, "tensors must be 16-byte aligned");
+  std::set<int32_t> seen;
+  for (int i = 0; i < n_seq; ++i) {
+    if (seq_ids[i] < 0 || seq_ids[i] >= d.n_seq) return fail(SMEM_EINVAL, "seq_ids[%d] = %d out of range", i, seq_ids[i]);
+    if (query_block[i] < 0 || query_block[i] > d.max_blocks)
+      return fail(SMEM_EINVAL, "query_block[%d] = %d out of range [0, %d]", i, query_block[i], d.max_blocks);
+    if (n_given == 4 && (pos[i] < 0 || pos[i] >= d.b)) return fail(SMEM_EINVAL, "pos[%d] = %d out of range [0, %d)", i, pos[i], d.b);
+    if (!seen.insert(seq_ids[i]).second) return fail(SMEM_EINVAL, "sequence %d appears twice", seq_ids[i]);
+  }
+  const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
+  const size_t es = esize(d.dtype);
+  const size_t tok = (size_t)d.H * d.dh;
+  for (int i0 = 0; i0 < n_seq; i0 += kMaxSlots) {
+    const int n = std::min(kMaxSlots, n_seq - i0);
+    ReaderArgs a;
+    memset(&a, 0, sizeof a);
+    a.q = (const char*)q + i0 * tok * es;
+    a.out = (char*)out + i0 * tok * es;
+    if (n_given == 4) {
+      a.k_new = (const char*)k_new + i0 * tok * es;
+      a.v_new = (const char*)v_new + i0 * tok * es;
+      a.k_in = (const char*)k_cache + (size_t)i0 * d.b * tok * es;
+      a.v_in = (const char*)v_cache + (size_t)i0 * d.b * tok * es;
+      a.k_cache_w = (char*)k_cache + (size_t)i0 * d.b * tok * es;
+      a.v_cache_w = (char*)v_cache + (size_t)i0 * d.b * tok * es;
+    }
+    a.null_kv = null_kv;
+    a.pages = st->d_pages;
+    a.live_page = st->d_live_page;
+    a.ws = st->d_ws;
+    a.max_blocks = d.max_blocks;
+    a.H = d.H; a.b = d.b; a.nq = 1; a.intra_mode = 2;
+    a.n_slots = n; a.scale_log2 = scale_log2;
+    for (int i = 0; i < n; ++i) {
+      const int sq = seq_ids[i0 + i];
+      a.seq[i] = sq;
+      a.n_read[i] = n_read_of(st, sq, query_block[i0 + i]);
+      a.pps[i] = pages_per_split(a.n_read[i], kMinPagesDecode);
+      a.aux[i] = n_given == 4 ? pos[i0 + i] : 0;
+    }
+    hipError_t e = launch_reader_valu(d.dtype, d.b, d.dh, a, s);
+    if (e != hipSuccess) return hip_fail(e, "decode launch");
+  }
+  return SMEM_OK;
+}
+
+}  // extern "C"

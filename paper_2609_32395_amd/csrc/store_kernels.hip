@@ -1,0 +1,174 @@
+// Store kernels: device metadata (block table and dense live lists), row
+// insert into a page, page scrub and canonical export.
+//
+// The memory is the multiset of all blocks' rows, listed by block index
+// (Section 2, "Model").  Device metadata per sequence:
+//   table[seq][j]     page holding block j, or -1
+//   live_blk[seq][i]  i-th present block index, ascending
+//   live_page[seq][i] its page
+//   n_live[seq]
+// An edit sets table entries, then the sequence's dense lists are rebuilt
+// from the table by a stream compaction: indices move, rows never do
+// (Theorem 1: deleting a block leaves the other blocks' rows and indices
+// untouched).
+#include "common.h"
+
+namespace smem {
+
+__global__ void k_init_meta(int32_t* __restrict__ table, int32_t* __restrict__ n_live, size_t n_table, int n_seq) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t j = i; j < n_table; j += stride) table[j] = -1;
+  for (size_t j = i; j < (size_t)n_seq; j += stride) n_live[j] = 0;
+}
+
+hipError_t launch_init_meta(int32_t* table, int32_t* n_live, size_t n_table, int n_seq, hipStream_t s) {
+  size_t work = n_table > (size_t)n_seq ? n_table : (size_t)n_seq;
+  unsigned grid = (unsigned)((work + 255) / 256);
+  if (grid > 4096) grid = 4096;
+  if (grid == 0) grid = 1;
+  hipLaunchKernelGGL(k_init_meta, dim3(grid), dim3(256), 0, s, table, n_live, n_table, n_seq);
+  return hipGetLastError();
+}
+
+// One workgroup per sequence to rebuild: apply this launch's edits of that
+// sequence to the table, then compact the table into the live lists.
+__global__ void __launch_bounds__(256) k_meta(MetaArgs a) {
+  const int seq = a.r_seq[blockIdx.x];
+  const int tid = threadIdx.x;
+  int32_t* trow = a.table + (size_t)seq * a.max_blocks;
+  for (int e = tid; e < a.n_edits; e += 256)
+    if (a.e_seq[e] == seq) trow[a.e_blk[e]] = a.e_page[e];
+  __syncthreads();
+
+  __shared__ int wave_cnt[4];
+  __shared__ int base_sh;
+  if (tid == 0) base_sh = 0;
+  __syncthreads();
+  const int lane = tid & 63, wave = tid >> 6;
+  int32_t* lp = a.live_page + (size_t)seq * a.max_blocks;
+  int32_t* lb = a.live_blk + (size_t)seq * a.max_blocks;
+  for (int c0 = 0; c0 < a.max_blocks; c0 += 256) {
+    const int j = c0 + tid;
+    const int32_t pg = (j < a.max_blocks) ? trow[j] : -1;
+    const bool valid = pg >= 0;
+    const unsigned long long mask = __ballot(valid);
+    const int before = __popcll(mask & ((1ull << lane) - 1ull));
+    if (lane == 0) wave_cnt[wave] = __popcll(mask);
+    __syncthreads();
+    int off = base_sh;
+    for (int w = 0; w < wave; ++w) off += wave_cnt[w];
+    if (valid) {
+      lp[off + before] = pg;
+      lb[off + before] = j;
+    }
+    __syncthreads();
+    if (tid == 0) base_sh += wave_cnt[0] + wave_cnt[1] + wave_cnt[2] + wave_cnt[3];
+    __syncthreads();
+  }
+  if (tid == 0) a.n_live[seq] = base_sh;
+}
+
+hipError_t launch_meta(const MetaArgs& a, hipStream_t s) {
+  if (a.n_seqs <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_meta, dim3(a.n_seqs), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// Insert one block's rows: src rows [b][H][dh] -> key plane [b][dh] and
+// transposed value plane [dh][b] of every head.  One workgroup per head; the
+// value tile goes through LDS so both global reads and writes are coalesced.
+template <typename T>
+__global__ void __launch_bounds__(256) k_put_rows(T* __restrict__ pages, int page, int H, int b, int dh,
+                                                   const T* __restrict__ k_rows, const T* __restrict__ v_rows) {
+  extern __shared__ unsigned char smem_raw[];
+  T* tile = reinterpret_cast<T*>(smem_raw);  // [b][dh + 1]
+  const int h = blockIdx.x;
+  T* kp = pages + page_head_offset(page, h, H, b, dh);
+  T* vp = kp + (size_t)b * dh;
+  const int n = b * dh;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const int r = i / dh, d = i % dh;
+    kp[i] = k_rows[((size_t)r * H + h) * dh + d];
+    tile[r * (dh + 1) + d] = v_rows[((size_t)r * H + h) * dh + d];
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const int d = i / b, r = i % b;
+    vp[i] = tile[r * (dh + 1) + d];
+  }
+}
+
+hipError_t launch_put_rows(int dtype, void* pages, int page, int H, int b, int dh,
+                           const void* k_rows, const void* v_rows, hipStream_t s) {
+  if (dtype == F32) {
+    size_t lds = (size_t)b * (dh + 1) * sizeof(float);
+    hipLaunchKernelGGL(k_put_rows<float>, dim3(H), dim3(256), lds, s, (float*)pages, page, H, b, dh,
+                       (const float*)k_rows, (const float*)v_rows);
+  } else {
+    size_t lds = (size_t)b * (dh + 1) * sizeof(uint16_t);
+    hipLaunchKernelGGL(k_put_rows<uint16_t>, dim3(H), dim3(256), lds, s, (uint16_t*)pages, page, H, b, dh,
+                       (const uint16_t*)k_rows, (const uint16_t*)v_rows);
+  }
+  return hipGetLastError();
+}
+
+__global__ void k_scrub(uint4* __restrict__ p, size_t n16) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  size_t stride = (size_t)gridDim.x * blockDim.x;
+  const uint4 z = make_uint4(0, 0, 0, 0);
+  for (; i < n16; i += stride) p[i] = z;
+}
+
+hipError_t launch_scrub(int dtype, void* pages, int page, int H, int b, int dh, hipStream_t s) {
+  const size_t esz = dtype == F32 ? 4 : 2;
+  const size_t bytes = (size_t)H * 2 * b * dh * esz;  // a page is a multiple of 16 bytes
+  char* base = (char*)pages + page_head_offset(page, 0, H, b, dh) * esz;
+  size_t n16 = bytes / 16;
+  unsigned grid = (unsigned)((n16 + 255) / 256);
+  if (grid > 1024) grid = 1024;
+  hipLaunchKernelGGL(k_scrub, dim3(grid), dim3(256), 0, s, (uint4*)base, n16);
+  return hipGetLastError();
+}
+
+// Canonical export: live entry i, head h -> rows [i*b, (i+1)*b) of k_out and
+// v_out ([rows][H][dh]); the value plane is transposed back through LDS.
+template <typename T>
+__global__ void __launch_bounds__(256) k_export(const T* __restrict__ pages, const int32_t* __restrict__ live_page,
+                                                 int H, int b, int dh, T* __restrict__ k_out, T* __restrict__ v_out) {
+  extern __shared__ unsigned char smem_raw[];
+  T* tile = reinterpret_cast<T*>(smem_raw);  // [dh][b + 1]
+  const int i = blockIdx.x, h = blockIdx.y;
+  const int page = live_page[i];
+  const T* kp = pages + page_head_offset(page, h, H, b, dh);
+  const T* vp = kp + (size_t)b * dh;
+  const int n = b * dh;
+  for (int e = threadIdx.x; e < n; e += blockDim.x) {
+    const int r = e / dh, d = e % dh;
+    k_out[(((size_t)i * b + r) * H + h) * dh + d] = kp[e];
+    const int dd = e / b, rr = e % b;
+    tile[dd * (b + 1) + rr] = vp[e];
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < n; e += blockDim.x) {
+    const int r = e / dh, d = e % dh;
+    v_out[(((size_t)i * b + r) * H + h) * dh + d] = tile[d * (b + 1) + r];
+  }
+}
+
+hipError_t launch_export(int dtype, const void* pages, const int32_t* live_page_seq, int n_live,
+                         int H, int b, int dh, void* k_out, void* v_out, hipStream_t s) {
+  if (n_live <= 0) return hipSuccess;
+  if (dtype == F32) {
+    size_t lds = (size_t)dh * (b + 1) * sizeof(float);
+    hipLaunchKernelGGL(k_export<float>, dim3(n_live, H), dim3(256), lds, s, (const float*)pages, live_page_seq,
+                       H, b, dh, (float*)k_out, (float*)v_out);
+  } else {
+    size_t lds = (size_t)dh * (b + 1) * sizeof(uint16_t);
+    hipLaunchKernelGGL(k_export<uint16_t>, dim3(n_live, H), dim3(256), lds, s, (const uint16_t*)pages,
+                       live_page_seq, H, b, dh, (uint16_t*)k_out, (uint16_t*)v_out);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace smem

@@ -1,0 +1,285 @@
+"""ctypes binding of libsmem.so (the C ABI declared in include/smem.h).
+
+Argument marshalling only: every step of the attention path runs in the HIP
+library.  PyTorch provides device memory (tensors, the store's pool) and the
+stream.  The binding checks tensor shapes, dtypes, devices and contiguity
+before each call, because the C ABI takes bare device pointers and cannot
+check buffer sizes itself.
+
+Functions carry the C names: smem_encode_blocks, smem_reader_prefill_block,
+smem_reader_decode, smem_delete_block, smem_store_put_block,
+smem_store_export; a store is created and destroyed by the Store class.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+F32 = 0
+BF16 = 1
+MASK_BIDIR = 0
+MASK_CAUSAL = 1
+
+SMEM_OK, SMEM_EINVAL, SMEM_ENOMEM, SMEM_ENOENT, SMEM_EEXIST, SMEM_EHIP = range(6)
+CODE_NAMES = {0: "OK", 1: "EINVAL", 2: "ENOMEM", 3: "ENOENT", 4: "EEXIST", 5: "EHIP"}
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsmem.so")
+
+_TORCH_DTYPE = {F32: torch.float32, BF16: torch.bfloat16}
+
+
+class SmemError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(msg)
+        self.code = code
+        self.name = CODE_NAMES.get(code, str(code))
+
+
+class StoreDesc(ctypes.Structure):
+    _fields_ = [("n_seq", ctypes.c_int32), ("max_blocks", ctypes.c_int32), ("n_pages", ctypes.c_int32),
+                ("b", ctypes.c_int32), ("H", ctypes.c_int32), ("dh", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class AttnDesc(ctypes.Structure):
+    _fields_ = [("b", ctypes.c_int32), ("H", ctypes.c_int32), ("dh", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I = ctypes.c_int32
+_IP = ctypes.POINTER(ctypes.c_int32)
+
+# name -> (restype, argtypes); mirrors include/smem.h
+SIGNATURES = {
+    "smem_store_bytes": (ctypes.c_size_t, [ctypes.POINTER(StoreDesc)]),
+    "smem_store_create": (_I, [ctypes.POINTER(StoreDesc), _P, ctypes.c_size_t, _P, ctypes.POINTER(_P)]),
+    "smem_store_destroy": (_I, [_P]),
+    "smem_store_put_block": (_I, [_P, _I, _I, _P, _P, _P]),
+    "smem_encode_blocks": (_I, [_P, ctypes.POINTER(AttnDesc), _I, _IP, _IP, _P, _P, _P, _P, _I, _P]),
+    "smem_reader_prefill_block": (_I, [_P, _I, _IP, _IP, _P, _P, _P, _P, _P, _P]),
+    "smem_reader_decode": (_I, [_P, _I, _IP, _IP, _IP, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "smem_delete_block": (_I, [_P, _I, _I, _I, _P]),
+    "smem_store_export": (_I, [_P, _I, _IP, _IP, _P, _P, _P]),
+    "smem_store_stats": (_I, [_P, _IP, _IP]),
+    "smem_status_string": (ctypes.c_char_p, [_I]),
+    "smem_last_error": (ctypes.c_char_p, []),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsmem.so; raise if it has not been built (there is no fallback)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_32395_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(code: int):
+    if code != SMEM_OK:
+        msg = lib().smem_last_error().decode()
+        raise SmemError(code, msg)
+
+
+def _i32(xs):
+    arr = (ctypes.c_int32 * max(1, len(xs)))(*[int(x) for x in xs])
+    return arr
+
+
+def _stream(stream):
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _dtype_code(t: torch.dtype) -> int:
+    if t == torch.float32:
+        return F32
+    if t == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t} (float32 or bfloat16)")
+
+
+def _dev(t, shape, dtype, name):
+    """Check a device tensor argument; return its pointer (None -> NULL)."""
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+class Store:
+    """A memory-row store over a device pool allocated here with torch.
+
+    meta_only=True creates a store with host metadata only (no device
+    memory): edits are validated and recorded, nothing runs on a GPU."""
+
+    def __init__(self, n_seq, max_blocks, n_pages, b, H, dh, dtype=torch.bfloat16, device="cuda",
+                 stream=None, meta_only=False):
+        self.dtype = dtype
+        self.b, self.H, self.dh = b, H, dh
+        self.n_seq, self.max_blocks, self.n_pages = n_seq, max_blocks, n_pages
+        self.desc = StoreDesc(n_seq, max_blocks, n_pages, b, H, dh, _dtype_code(dtype))
+        L = lib()
+        nbytes = L.smem_store_bytes(ctypes.byref(self.desc))
+        if nbytes == 0:
+            raise SmemError(SMEM_EINVAL, "invalid store descriptor")
+        self.nbytes = nbytes
+        self.pool = None
+        handle = ctypes.c_void_p()
+        if meta_only:
+            _check(L.smem_store_create(ctypes.byref(self.desc), None, 0, None, ctypes.byref(handle)))
+        else:
+            self.pool = torch.empty(nbytes, dtype=torch.uint8, device=device)
+            _check(L.smem_store_create(ctypes.byref(self.desc), ctypes.c_void_p(self.pool.data_ptr()), nbytes,
+                                       _stream(stream), ctypes.byref(handle)))
+        self.handle = handle
+        self.meta_only = meta_only
+
+    # -- lifecycle
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().smem_store_destroy(self.handle)
+            self.handle = None
+        self.pool = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    @property
+    def row_shape(self):
+        return (self.b, self.H, self.dh)
+
+    def stats(self):
+        used, free = ctypes.c_int32(), ctypes.c_int32()
+        _check(lib().smem_store_stats(self.handle, ctypes.byref(used), ctypes.byref(free)))
+        return used.value, free.value
+
+
+def smem_store_put_block(st: Store, seq: int, block_idx: int, k_rows=None, v_rows=None, stream=None):
+    if st.meta_only:
+        kp = vp = None
+    else:
+        kp = _dev(k_rows, st.row_shape, st.dtype, "k_rows")
+        vp = _dev(v_rows, st.row_shape, st.dtype, "v_rows")
+    _check(lib().smem_store_put_block(st.handle, int(seq), int(block_idx), kp, vp,
+                                      None if st.meta_only else _stream(stream)))
+
+
+def smem_delete_block(st: Store, seq: int, block_idx: int, scrub: bool = False, stream=None):
+    _check(lib().smem_delete_block(st.handle, int(seq), int(block_idx), int(bool(scrub)),
+                                   None if st.meta_only else _stream(stream)))
+
+
+def smem_store_export(st: Store, seq: int, rows: bool = True, stream=None):
+    """Canonical memory of one sequence: (live block indices, K, V) with K, V of
+    shape [n_live*b, H, dh] (None when rows=False)."""
+    L = lib()
+    idx = (ctypes.c_int32 * st.max_blocks)()
+    n = ctypes.c_int32()
+    if not rows or st.meta_only:
+        _check(L.smem_store_export(st.handle, int(seq), idx, ctypes.byref(n), None, None, None))
+        return list(idx[: n.value]), None, None
+    _check(L.smem_store_export(st.handle, int(seq), None, ctypes.byref(n), None, None, None))
+    K = torch.empty((n.value * st.b, st.H, st.dh), dtype=st.dtype, device=st.pool.device)
+    V = torch.empty_like(K)
+    _check(L.smem_store_export(st.handle, int(seq), idx, ctypes.byref(n), ctypes.c_void_p(K.data_ptr()),
+                               ctypes.c_void_p(V.data_ptr()), _stream(stream)))
+    return list(idx[: n.value]), K, V
+
+
+def smem_encode_blocks(st, q, k, v, out=None, seq_ids=None, block_idx=None, mask=MASK_BIDIR, b=None, stream=None):
+    """Block-local encoder attention over q, k, v of shape [n_blocks*b, H, dh].
+
+    With a store, block i's output becomes memory block block_idx[i] of
+    sequence seq_ids[i].  Returns out (allocated when not given)."""
+    if st is not None:
+        b = st.b
+    if b is None:
+        raise ValueError("b is required without a store")
+    rows, H, dh = q.shape
+    if rows % b:
+        raise ValueError(f"q has {rows} rows, not a multiple of b={b}")
+    nb = rows // b
+    dt = q.dtype
+    if out is None:
+        out = torch.empty_like(q)
+    shape = (rows, H, dh)
+    ptrs = [_dev(x, shape, dt, n) for x, n in ((q, "q"), (k, "k"), (v, "v"), (out, "out"))]
+    desc = AttnDesc(b, H, dh, _dtype_code(dt))
+    if st is not None:
+        if seq_ids is None or block_idx is None or len(seq_ids) != nb or len(block_idx) != nb:
+            raise ValueError("seq_ids and block_idx need one entry per block")
+        sa, ba = _i32(seq_ids), _i32(block_idx)
+        h = st.handle
+    else:
+        sa = ba = None
+        h = None
+    _check(lib().smem_encode_blocks(h, ctypes.byref(desc), nb, sa, ba, *ptrs, int(mask), _stream(stream)))
+    return out
+
+
+def smem_reader_prefill_block(st: Store, seq_ids, query_block, q, k_intra=None, v_intra=None, null_kv=None,
+                              out=None, stream=None):
+    """Reader attention for whole query blocks; q etc. [n*b, H, dh]."""
+    n = len(seq_ids)
+    if len(query_block) != n:
+        raise ValueError("query_block needs one entry per sequence")
+    shape = (n * st.b, st.H, st.dh)
+    if out is None:
+        out = torch.empty(shape, dtype=st.dtype, device=q.device)
+    qp = _dev(q, shape, st.dtype, "q")
+    kp = _dev(k_intra, shape, st.dtype, "k_intra")
+    vp = _dev(v_intra, shape, st.dtype, "v_intra")
+    np_ = _dev(null_kv, (2, st.H, st.dh), st.dtype, "null_kv")
+    op = _dev(out, shape, st.dtype, "out")
+    _check(lib().smem_reader_prefill_block(st.handle, n, _i32(seq_ids), _i32(query_block), qp, kp, vp, np_, op,
+                                           _stream(stream)))
+    return out
+
+
+def smem_reader_decode(st: Store, seq_ids, query_block, pos, q, k_new=None, v_new=None, k_cache=None,
+                       v_cache=None, null_kv=None, out=None, stream=None):
+    """Reader attention for one new token per sequence; q etc. [n, H, dh],
+    caches [n*b, H, dh] (row pos[i] of sequence row i is written)."""
+    n = len(seq_ids)
+    if len(query_block) != n or (pos is not None and len(pos) != n):
+        raise ValueError("query_block and pos need one entry per sequence")
+    tok = (n, st.H, st.dh)
+    cache = (n * st.b, st.H, st.dh)
+    if out is None:
+        out = torch.empty(tok, dtype=st.dtype, device=q.device)
+    args = [_dev(q, tok, st.dtype, "q"), _dev(k_new, tok, st.dtype, "k_new"), _dev(v_new, tok, st.dtype, "v_new"),
+            _dev(k_cache, cache, st.dtype, "k_cache"), _dev(v_cache, cache, st.dtype, "v_cache"),
+            _dev(null_kv, (2, st.H, st.dh), st.dtype, "null_kv"), _dev(out, tok, st.dtype, "out")]
+    pa = _i32(pos) if pos is not None else None
+    _check(lib().smem_reader_decode(st.handle, n, _i32(seq_ids), _i32(query_block), pa, *args, _stream(stream)))
+    return out
