@@ -1,0 +1,309 @@
+"""Benchmark of the SMem attention hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1]
+
+Headline workload (the timed step): 410M-shaped batched decode -- 64
+sequences, 16 heads x dh 64, b = 64, 64 cached blocks (4096 memory rows) per
+sequence, bf16.  One step is one smem_reader_decode call that decodes one
+token for every sequence (one reader layer's attention); the in-block
+position of sequence s at step t is (p_s + t) mod 64 with p_s uniform per
+sequence, so 1..64 in-block keys are read besides the memory.  `value` is
+decoded tokens/s with every input already resident in HBM.
+
+Secondary workloads, timed in the same run and reported under "secondary":
+  * 160M-shaped encode + prefill: 8 sequences x 16 blocks, 12 heads x dh 64,
+    b = 64: block-local encoder attention over all 128 blocks (inserted into
+    the store), then reader prefill of the final block of each sequence;
+  * 1.5B-shaped single-block serve: 512 cached blocks (32768 rows), 16 heads
+    x dh 128, batch 1: reader prefill of one fresh block over all rows, then
+    100 random single-block deletions, each followed by a re-serve.
+
+Timing uses HIP events on the stream the kernels are launched on (torch's
+current stream, handed to the library).  The CPU baseline is the fp64 numpy
+oracle timed on a bounded sample of the headline workload on this host.
+Prints ONE JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+BF16_PEAK_TFLOPS = 2516.6      # MI355X dense bf16 MFMA, published
+
+
+def _events_time(fn, steps, stream):
+    import torch
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for t in range(steps):
+        fn(t)
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / 1e3  # seconds
+
+
+def decode_workload(args, torch, smem, synth):
+    """Headline: batched decode over a 4096-row memory per sequence."""
+    w = synth.DEC_410M
+    S, H, dh, b, NB = w.n_seq, w.H, w.dh, w.b, w.n_blocks
+    dt = torch.bfloat16
+    seed = args.seed
+    st = smem.Store(S, NB + 1, S * NB, b, H, dh, dt)
+    # memory rows: seeded per (sequence, block), uploaded one sequence at a time
+    for s in range(S):
+        K, V = synth.memory_blocks(w, seed, [s], range(NB), threads=16)
+        Kd = torch.from_numpy(K[0]).to("cuda").to(dt)
+        Vd = torch.from_numpy(V[0]).to("cuda").to(dt)
+        for j in range(NB):
+            smem.smem_store_put_block(st, s, j, Kd[j], Vd[j])
+    steps_total = args.warmup + args.steps
+    n_draw = min(steps_total, 256)
+    g = synth.rng(seed, w.wid, synth.ROLE_QDEC, 0, 0, 0)
+    qs = synth.bf16_round((g.standard_normal((n_draw, S, H, dh)) * w.scale).astype(np.float32))
+    kn = synth.bf16_round((g.standard_normal((n_draw, S, H, dh)) * w.scale).astype(np.float32))
+    vn = synth.bf16_round((g.standard_normal((n_draw, S, H, dh)) * w.scale).astype(np.float32))
+    kc0 = synth.bf16_round((g.standard_normal((S * b, H, dh)) * w.scale).astype(np.float32))
+    vc0 = synth.bf16_round((g.standard_normal((S * b, H, dh)) * w.scale).astype(np.float32))
+    p0 = synth.decode_positions(w, seed, S)
+    Q = torch.from_numpy(qs).to("cuda").to(dt)
+    KN = torch.from_numpy(kn).to("cuda").to(dt)
+    VN = torch.from_numpy(vn).to("cuda").to(dt)
+    kc = torch.from_numpy(kc0).to("cuda").to(dt)
+    vc = torch.from_numpy(vc0).to("cuda").to(dt)
+    out = torch.empty((S, H, dh), dtype=dt, device="cuda")
+    seq_ids = list(range(S))
+    qblk = [NB] * S
+    pos_tab = [[int((p0[s] + t) % b) for s in range(S)] for t in range(steps_total)]
+    stream = torch.cuda.current_stream()
+
+    def step(t, base=0):
+        i = (base + t) % n_draw
+        smem.smem_reader_decode(st, seq_ids, qblk, pos_tab[base + t], Q[i], KN[i], VN[i], kc, vc, None, out)
+
+    for t in range(args.warmup):
+        step(t)
+    secs = _events_time(lambda t: step(t, args.warmup), args.steps, stream)
+    torch.cuda.synchronize()
+    # algorithmic bytes: memory K+V rows read, in-block rows read (cache rows
+    # 0..p-1 plus the new pair), the query, the output and the cache write
+    esz = 2
+    mem_bytes = S * H * NB * b * dh * 2 * esz
+    per_step_intra = [sum(p for p in pos_tab[args.warmup + t]) * H * dh * 2 * esz for t in range(args.steps)]
+    tok_bytes = S * H * dh * esz
+    intra = float(np.mean(per_step_intra))
+    bytes_step = mem_bytes + intra + tok_bytes * (1 + 2 + 1 + 2)  # q, k_new+v_new, out, cache row write (K, V)
+    flops_step = 4.0 * S * H * dh * (NB * b + float(np.mean([np.mean(np.array(pos_tab[args.warmup + t]) + 1) for t in range(args.steps)])))
+    sec_step = secs / args.steps
+    res = dict(
+        tokens_per_s=S / sec_step,
+        ms_per_step=sec_step * 1e3,
+        bytes_per_step=bytes_step,
+        flops_per_step=flops_step,
+        gbs=bytes_step / sec_step / 1e9,
+        store=st, S=S, H=H, dh=dh, b=b, NB=NB, pos=pos_tab, qs=qs, kn=kn, vn=vn, kc0=kc0, vc0=vc0,
+    )
+    return res
+
+
+def encode_prefill_workload(args, torch, smem, synth):
+    """160M-shaped: encoder over 8 x 16 blocks, then prefill of the final blocks."""
+    w = synth.ENC_160M
+    S, H, dh, b, NB = w.n_seq, w.H, w.dh, w.b, w.n_blocks
+    dt = torch.bfloat16
+    seed = args.seed
+    nb = S * NB
+    q = np.stack([synth.block_tokens(w, seed, synth.ROLE_Q, s, j) for s in range(S) for j in range(NB)])
+    k = np.stack([synth.block_tokens(w, seed, synth.ROLE_K, s, j) for s in range(S) for j in range(NB)])
+    v = np.stack([synth.block_tokens(w, seed, synth.ROLE_V, s, j) for s in range(S) for j in range(NB)])
+    Qd, Kd, Vd = (torch.from_numpy(x.reshape(nb * b, H, dh)).to("cuda").to(dt) for x in (q, k, v))
+    out = torch.empty_like(Qd)
+    seq_ids = [s for s in range(S) for j in range(NB)]
+    blk = [j for s in range(S) for j in range(NB)]
+    stream = torch.cuda.current_stream()
+    reps = max(5, args.steps // 8)
+    # encoder alone (attention only), timed
+    for _ in range(3):
+        smem.smem_encode_blocks(None, Qd, Kd, Vd, out=out, mask=smem.MASK_BIDIR, b=b)
+    enc_s = _events_time(lambda t: smem.smem_encode_blocks(None, Qd, Kd, Vd, out=out, mask=smem.MASK_BIDIR, b=b),
+                         reps, stream) / reps
+    # encode + insert into a store, then prefill the final block of each sequence
+    st = smem.Store(S, NB, S * NB, b, H, dh, dt)
+    smem.smem_encode_blocks(st, Qd, Kd, Vd, out=out, seq_ids=seq_ids, block_idx=blk, mask=smem.MASK_BIDIR)
+    last = [s * NB + NB - 1 for s in range(S)]
+    qp = torch.cat([Qd[i * b:(i + 1) * b] for i in last])
+    kp = torch.cat([Kd[i * b:(i + 1) * b] for i in last])
+    vp = torch.cat([Vd[i * b:(i + 1) * b] for i in last])
+    pout = torch.empty_like(qp)
+    qb = [NB - 1] * S
+    for _ in range(3):
+        smem.smem_reader_prefill_block(st, list(range(S)), qb, qp, kp, vp, None, pout)
+    pre_s = _events_time(lambda t: smem.smem_reader_prefill_block(st, list(range(S)), qb, qp, kp, vp, None, pout),
+                         reps, stream) / reps
+    enc_flops = 4.0 * nb * H * b * b * dh
+    enc_bytes = 4.0 * nb * b * H * dh * 2
+    n_mem = (NB - 1) * b
+    pre_flops = 4.0 * S * H * b * dh * (n_mem + (b + 1) / 2.0)
+    pre_bytes = S * H * (n_mem * dh * 2 * 2 + 4 * b * dh * 2)
+    st.close()
+    return dict(encoder_ms=enc_s * 1e3, encoder_tflops=enc_flops / enc_s / 1e12, encoder_gbs=enc_bytes / enc_s / 1e9,
+                encoder_flops=enc_flops, encoder_bytes=enc_bytes,
+                prefill_ms=pre_s * 1e3, prefill_tflops=pre_flops / pre_s / 1e12, prefill_gbs=pre_bytes / pre_s / 1e9)
+
+
+def serve_workload(args, torch, smem, synth):
+    """1.5B-shaped: single-block serve over 32768 rows, then 100 delete + re-serve."""
+    w = synth.SERVE_1P5B
+    H, dh, b, NB = w.H, w.dh, w.b, w.n_blocks
+    dt = torch.bfloat16
+    seed = args.seed
+    st = smem.Store(1, NB + 1, NB, b, H, dh, dt)
+    for j0 in range(0, NB, 64):
+        K, V = synth.memory_blocks(w, seed, [0], range(j0, min(NB, j0 + 64)), threads=16)
+        Kd = torch.from_numpy(K[0]).to("cuda").to(dt)
+        Vd = torch.from_numpy(V[0]).to("cuda").to(dt)
+        for i in range(Kd.shape[0]):
+            smem.smem_store_put_block(st, 0, j0 + i, Kd[i], Vd[i])
+    q = torch.from_numpy(synth.block_tokens(w, seed, synth.ROLE_Q, 0, NB)).to("cuda").to(dt)
+    k = torch.from_numpy(synth.block_tokens(w, seed, synth.ROLE_K, 0, NB)).to("cuda").to(dt)
+    v = torch.from_numpy(synth.block_tokens(w, seed, synth.ROLE_V, 0, NB)).to("cuda").to(dt)
+    out = torch.empty_like(q)
+    stream = torch.cuda.current_stream()
+
+    def serve(t=0):
+        smem.smem_reader_prefill_block(st, [0], [NB], q, k, v, None, out)
+
+    for _ in range(3):
+        serve()
+    reps = max(5, args.steps // 8)
+    serve_s = _events_time(serve, reps, stream) / reps
+    order = synth.rng(seed, w.wid, synth.ROLE_EDIT, 0, 0, 0).permutation(NB)[:100]
+    start = torch.cuda.Event(enable_timing=True)
+    mid = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    del_t, re_t = [], []
+    for j in order:
+        torch.cuda.synchronize()
+        start.record(stream)
+        smem.smem_delete_block(st, 0, int(j))
+        mid.record(stream)
+        serve()
+        end.record(stream)
+        end.synchronize()
+        del_t.append(start.elapsed_time(mid))
+        re_t.append(mid.elapsed_time(end))
+    rows = NB * b
+    flops = 4.0 * H * b * dh * (rows + (b + 1) / 2.0)
+    bytes_ = H * (rows * dh * 2 * 2 + 4 * b * dh * 2)
+    st.close()
+    return dict(serve_ms=serve_s * 1e3, serve_tflops=flops / serve_s / 1e12, serve_gbs=bytes_ / serve_s / 1e9,
+                delete_us_median=float(np.median(del_t)) * 1e3, reserve_ms_median=float(np.median(re_t)),
+                rows_after_deletes=(NB - 100) * b)
+
+
+def cpu_baseline(dec, budget_s, seed):
+    """The fp64 oracle on a bounded sample of the headline decode workload.
+
+    The oracle's store is rebuilt from the seeded generator (never from the
+    GPU); only the oracle's decode calls are timed."""
+    from oracle import smem_oracle as O
+    from paper_2609_32395_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = 1
+    w = synth.DEC_410M
+    S, H, dh, b, NB = dec["S"], dec["H"], dec["dh"], dec["b"], dec["NB"]
+    n_tok, spent, s = 0, 0.0, 0
+    kc_all = dec["kc0"].reshape(S, b, H, dh)
+    vc_all = dec["vc0"].reshape(S, b, H, dh)
+    while spent < budget_s and s < S:
+        K, V = synth.memory_blocks(w, seed, [s], range(NB), threads=8)
+        ref = O.Store(S, NB + 1, b, H, dh)
+        for j in range(NB):
+            ref.put(s, j, K[0, j], V[0, j])
+        for t in range(len(dec["qs"])):
+            if spent >= budget_s:
+                break
+            p = dec["pos"][t][s]
+            t1 = time.perf_counter()
+            O.reader_decode(ref, [s], [NB], [p], dec["qs"][t, s:s + 1], dec["kn"][t, s:s + 1],
+                            dec["vn"][t, s:s + 1], kc_all[s:s + 1], vc_all[s:s + 1])
+            spent += time.perf_counter() - t1
+            n_tok += 1
+        s += 1
+    return {"value": round(n_tok / spent, 3), "unit": "tokens/s", "cores": int(blas_threads), "kind": "oracle",
+            "sample": f"{n_tok} decode tokens (16 heads each over 4096 memory rows + in-block keys), "
+                      f"fp64 numpy, {spent:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported (the path is single-GPU; "
+              f"sharding is described, not built).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2609_32395_amd import smem, synth
+    smem.lib()
+    torch.cuda.set_device(0)
+
+    dec = decode_workload(args, torch, smem, synth)
+    secondary = {}
+    if not args.no_secondary:
+        secondary["encode_prefill_160M"] = encode_prefill_workload(args, torch, smem, synth)
+        secondary["serve_1p5B"] = serve_workload(args, torch, smem, synth)
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(dec, args.cpu_budget, args.seed)
+    achieved = dec["gbs"]
+    line = {
+        "metric": "reader decode tokens/s + HBM GB/s; single-block serve ms; encoder attn TFLOP/s",
+        "value": round(dec["tokens_per_s"], 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(dec["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded normals, scale 1/8; random-init, no trained weights)",
+        "config": {"workload": "410M-shaped batched decode: 64 seq x 16 heads x dh 64, b=64, 4096 memory rows "
+                               "per sequence, one token per sequence per step, 1-64 in-block keys",
+                   "global_batch": 64, "memory_rows": 4096, "heads": 16, "head_dim": 64, "block": 64,
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "smem_reader_decode (k_reader_valu + k_merge)",
+                     "bytes_per_launch": dec["bytes_per_step"]},
+        "hbm_gbs": round(achieved, 1),
+        "secondary": secondary,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()
