@@ -1,0 +1,411 @@
+// MFMA (bf16, fp32 accumulation) encoder and reader-prefill attention for
+// blocks of b = 64 tokens.
+//
+// Encoder (Section 2, "Model"; Appendix A, "Encoder"): one workgroup per
+// (block, head); the whole 64 x 64 score tile fits, so the softmax is exact
+// in one pass.  Reader prefill (Section 3.1, block-skip serving): one
+// workgroup per (query block, head, split); it streams whole memory pages of
+// its split with an online softmax, and the split after the memory holds the
+// null row and the in-block causal tile.  Splits merge in split order.
+//
+// Both compute S^T = K Q^T and O^T = V^T P^T with
+// __builtin_amdgcn_mfma_f32_16x16x32_bf16 (A: 16 rows x 32 k, B: 32 k x 16
+// columns, D: 16 x 16).  Lane l of a wave supplies A row l%16 and B column
+// l%16; its 8 k-values per operand are k-slots (l/16, 0..7), and A and B pair
+// the same slot (checked on gfx950).  D element (4*(l/16)+i, l%16) lands in
+// lane l, value i.  With keys as the rows of S^T, every lane owns one query
+// column: the softmax statistics and the output rescale are per-lane
+// scalars, and P^T reaches the second product straight from the score
+// accumulators -- key tile 2c gives k-slots j<4 and tile 2c+1 gives j>=4, and
+// the A operand (transposed values) reads the same keys in the same slots.
+// The store keeps value planes transposed ([dh][b], keys contiguous) so that
+// operand is two contiguous 8-byte reads per lane.
+#include "common.h"
+
+namespace smem {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int BT = 64;         // block / page size handled here
+constexpr int KPAD = 8;        // LDS row padding (elements): 16 bytes per row
+
+template <int DH>
+struct Tiles {
+  static constexpr int KS = DH + KPAD;   // key tile row stride
+  static constexpr int VS = BT + KPAD;   // transposed value tile row stride
+  uint16_t k[BT * KS];
+  uint16_t vt[DH * VS];
+};
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) {
+  bf16x8 r;
+  __builtin_memcpy(&r, &u, 16);
+  return r;
+}
+
+__device__ __forceinline__ bf16x8 pack_p(const floatx4& a, const floatx4& b) {
+  bf16x8 r;
+  r[0] = (__bf16)a[0]; r[1] = (__bf16)a[1]; r[2] = (__bf16)a[2]; r[3] = (__bf16)a[3];
+  r[4] = (__bf16)b[0]; r[5] = (__bf16)b[1]; r[6] = (__bf16)b[2]; r[7] = (__bf16)b[3];
+  return r;
+}
+
+// Page tile chunks per thread (256 threads, 16-byte chunks).
+template <int DH>
+struct PageRegs {
+  static constexpr int NK = BT * DH / 8 / 256;
+  static constexpr int NV = DH * BT / 8 / 256;
+  uint4 k[NK];
+  uint4 v[NV];
+};
+
+template <int DH>
+__device__ __forceinline__ void page_load(PageRegs<DH>& r, const uint16_t* __restrict__ Kt,
+                                          const uint16_t* __restrict__ VT, int tid) {
+#pragma unroll
+  for (int i = 0; i < PageRegs<DH>::NK; ++i) r.k[i] = *(const uint4*)(Kt + (size_t)(tid + i * 256) * 8);
+#pragma unroll
+  for (int i = 0; i < PageRegs<DH>::NV; ++i) r.v[i] = *(const uint4*)(VT + (size_t)(tid + i * 256) * 8);
+}
+
+template <int DH>
+__device__ __forceinline__ void page_store(const PageRegs<DH>& r, Tiles<DH>& T, int tid) {
+#pragma unroll
+  for (int i = 0; i < PageRegs<DH>::NK; ++i) {
+    const int c = tid + i * 256;
+    const int row = c / (DH / 8), c8 = c % (DH / 8);
+    *(uint4*)&T.k[row * Tiles<DH>::KS + c8 * 8] = r.k[i];
+  }
+#pragma unroll
+  for (int i = 0; i < PageRegs<DH>::NV; ++i) {
+    const int c = tid + i * 256;
+    const int d = c / (BT / 8), c8 = c % (BT / 8);
+    *(uint4*)&T.vt[d * Tiles<DH>::VS + c8 * 8] = r.v[i];
+  }
+}
+
+// In-block tile from token-major tensors ([row][H][dh], row stride H*dh):
+// keys row-major, values transposed into LDS.
+template <int DH>
+__device__ __forceinline__ void intra_store(Tiles<DH>& T, const uint16_t* __restrict__ kin,
+                                            const uint16_t* __restrict__ vin, size_t row_stride, int tid) {
+  constexpr int NCH = BT * DH / 8;
+  for (int c = tid; c < NCH; c += 256) {
+    const int row = c / (DH / 8), c8 = c % (DH / 8);
+    const uint4 kv = *(const uint4*)(kin + row * row_stride + c8 * 8);
+    const uint4 vv = *(const uint4*)(vin + row * row_stride + c8 * 8);
+    *(uint4*)&T.k[row * Tiles<DH>::KS + c8 * 8] = kv;
+    const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      T.vt[(c8 * 8 + 2 * j) * Tiles<DH>::VS + row] = (uint16_t)(w[j] & 0xffffu);
+      T.vt[(c8 * 8 + 2 * j + 1) * Tiles<DH>::VS + row] = (uint16_t)(w[j] >> 16);
+    }
+  }
+}
+
+// Query fragments of one wave (B operand of S^T = K Q^T): query row
+// wave*16 + l%16, dims kk*32 + (l/16)*8 .. +8.
+template <int DH>
+__device__ __forceinline__ void load_q(bf16x8 (&qf)[DH / 32], const uint16_t* __restrict__ q, size_t row_stride,
+                                       int lane) {
+  const uint16_t* qr = q + (size_t)(lane & 15) * row_stride + (lane >> 4) * 8;
+#pragma unroll
+  for (int kk = 0; kk < DH / 32; ++kk) qf[kk] = as_bf16x8(*(const uint4*)(qr + kk * 32));
+}
+
+// S^T for this wave's 16 queries against the 64 keys in LDS.
+template <int DH>
+__device__ __forceinline__ void scores(floatx4 (&s)[4], const Tiles<DH>& T, const bf16x8 (&qf)[DH / 32], int lane) {
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt) {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    const uint16_t* kr = &T.k[(kt * 16 + (lane & 15)) * Tiles<DH>::KS + (lane >> 4) * 8];
+#pragma unroll
+    for (int kk = 0; kk < DH / 32; ++kk)
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(*(const uint4*)(kr + kk * 32)), qf[kk], acc, 0, 0, 0);
+    s[kt] = acc;
+  }
+}
+
+// O^T += V^T P^T over the 64 keys in LDS.
+template <int DH>
+__device__ __forceinline__ void pv(floatx4 (&o)[DH / 16], const Tiles<DH>& T, const floatx4 (&p)[4], int lane) {
+  const bf16x8 p0 = pack_p(p[0], p[1]);
+  const bf16x8 p1 = pack_p(p[2], p[3]);
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) {
+    const uint16_t* vr = &T.vt[(dt * 16 + (lane & 15)) * Tiles<DH>::VS + (lane >> 4) * 4];
+    uint4 a0, a1;
+    const uint2 x0 = *(const uint2*)(vr + 0), y0 = *(const uint2*)(vr + 16);
+    const uint2 x1 = *(const uint2*)(vr + 32), y1 = *(const uint2*)(vr + 48);
+    a0 = make_uint4(x0.x, x0.y, y0.x, y0.y);
+    a1 = make_uint4(x1.x, x1.y, y1.x, y1.y);
+    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a0), p0, o[dt], 0, 0, 0);
+    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a1), p1, o[dt], 0, 0, 0);
+  }
+}
+
+// Max / sum over the four lanes that hold one query column.
+__device__ __forceinline__ float qmax(float x) {
+  x = fmaxf(x, __shfl_xor(x, 16));
+  return fmaxf(x, __shfl_xor(x, 32));
+}
+__device__ __forceinline__ float qsum(float x) {
+  x += __shfl_xor(x, 16);
+  return x + __shfl_xor(x, 32);
+}
+
+// One online-softmax step over a 64-key tile for the lane's query.
+// valid(kt, i) says whether key kt*16 + 4*(lane/16) + i is visible.
+template <int DH, bool CAUSAL>
+__device__ __forceinline__ void online_step(floatx4 (&s)[4], float& m, float& l, floatx4 (&o)[DH / 16], int lane,
+                                            int qrow, float scale_log2) {
+  float mx = -INFINITY;
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float x = s[kt][i] * scale_log2;
+      if (CAUSAL) {
+        const int key = kt * 16 + (lane >> 4) * 4 + i;
+        if (key > qrow) x = -INFINITY;
+      }
+      s[kt][i] = x;
+      mx = fmaxf(mx, x);
+    }
+  }
+  mx = qmax(mx);
+  const float mn = fmaxf(m, mx);
+  const float alpha = (m == -INFINITY) ? 0.f : exp2f(m - mn);
+  float ps = 0.f;
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float p = (s[kt][i] == -INFINITY) ? 0.f : exp2f(s[kt][i] - mn);
+      s[kt][i] = p;
+      ps += p;
+    }
+  }
+  l = l * alpha + ps;
+  m = mn;
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[dt][i] *= alpha;
+  }
+}
+
+// ------------------------------------------------------------------ encoder
+
+struct EncArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* out;        // may be NULL
+  uint16_t* pages;      // may be NULL
+  int32_t H;
+  int32_t causal;
+  float scale_log2;
+  int32_t sink[kMaxSlots];   // page of block i, or -1
+};
+
+template <int DH, bool CAUSAL>
+__global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
+  __shared__ Tiles<DH> T;
+  const int blk = blockIdx.x, h = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const size_t rs = (size_t)a.H * DH;
+  const size_t base = (size_t)blk * BT * rs + (size_t)h * DH;
+  intra_store<DH>(T, a.k + base, a.v + base, rs, tid);
+  bf16x8 qf[DH / 32];
+  load_q<DH>(qf, a.q + base + (size_t)wave * 16 * rs, rs, lane);
+  __syncthreads();
+  floatx4 s[4];
+  scores<DH>(s, T, qf, lane);
+  floatx4 o[DH / 16];
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY, l = 0.f;
+  const int qrow = wave * 16 + (lane & 15);
+  online_step<DH, CAUSAL>(s, m, l, o, lane, qrow, a.scale_log2);
+  pv<DH>(o, T, s, lane);
+  l = qsum(l);
+  const float inv = 1.f / l;
+  const size_t orow = (size_t)blk * BT + qrow;
+  const int pg = a.sink[blk];
+  uint16_t* kp = (a.pages && pg >= 0) ? a.pages + page_head_offset(pg, h, a.H, BT, DH) : nullptr;
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) {
+    const int d0 = dt * 16 + (lane >> 4) * 4;
+    uint16_t r[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = f32_to_bf16_bits(o[dt][i] * inv);
+    const uint2 packed = make_uint2((uint32_t)r[0] | ((uint32_t)r[1] << 16), (uint32_t)r[2] | ((uint32_t)r[3] << 16));
+    if (a.out) *(uint2*)(a.out + orow * rs + (size_t)h * DH + d0) = packed;
+    if (kp) {
+      *(uint2*)(kp + qrow * DH + d0) = packed;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) kp[BT * DH + (d0 + i) * BT + qrow] = r[i];
+    }
+  }
+}
+
+template <int DH>
+static hipError_t launch_enc(const EncArgs& a, int n_blocks, hipStream_t s) {
+  if (a.causal)
+    hipLaunchKernelGGL((k_encoder_mfma<DH, true>), dim3(n_blocks, a.H), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_encoder_mfma<DH, false>), dim3(n_blocks, a.H), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_encoder_mfma(int b, int dh, const void* q, const void* k, const void* v, void* out, void* pages,
+                               const int32_t* sink_pages, int n_blocks, int H, int mask, float scale_log2,
+                               hipStream_t s) {
+  if (b != BT || n_blocks > kMaxSlots) return hipErrorInvalidValue;
+  if (n_blocks <= 0) return hipSuccess;
+  EncArgs a;
+  a.q = (const uint16_t*)q;
+  a.k = (const uint16_t*)k;
+  a.v = (const uint16_t*)v;
+  a.out = (uint16_t*)out;
+  a.pages = (uint16_t*)pages;
+  a.H = H;
+  a.causal = mask;
+  a.scale_log2 = scale_log2;
+  for (int i = 0; i < kMaxSlots; ++i) a.sink[i] = i < n_blocks ? sink_pages[i] : -1;
+  if (dh == 32) return launch_enc<32>(a, n_blocks, s);
+  if (dh == 64) return launch_enc<64>(a, n_blocks, s);
+  if (dh == 128) return launch_enc<128>(a, n_blocks, s);
+  return hipErrorInvalidValue;
+}
+
+// ------------------------------------------------------------------ reader prefill
+
+template <int DH>
+__global__ void __launch_bounds__(256) k_prefill_mfma(ReaderArgs a) {
+  __shared__ Tiles<DH> T;
+  const int split = blockIdx.x, h = blockIdx.y, slot = blockIdx.z;
+  const int n_read = a.n_read[slot], pps = a.pps[slot];
+  const int nms = (n_read + pps - 1) / pps;
+  if (split > nms) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const size_t rs = (size_t)a.H * DH;
+  const int qrow = wave * 16 + (lane & 15);
+
+  bf16x8 qf[DH / 32];
+  load_q<DH>(qf, (const uint16_t*)a.q + ((size_t)slot * BT + wave * 16) * rs + (size_t)h * DH, rs, lane);
+  floatx4 o[DH / 16];
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY, l = 0.f;
+
+  if (split < nms) {
+    const int p0 = split * pps, p1 = min(n_read, p0 + pps);
+    const int32_t* lp = a.live_page + (size_t)a.seq[slot] * a.max_blocks;
+    const uint16_t* pages = (const uint16_t*)a.pages;
+    PageRegs<DH> r;
+    {
+      const uint16_t* Kt = pages + page_head_offset(lp[p0], h, a.H, BT, DH);
+      page_load<DH>(r, Kt, Kt + BT * DH, tid);
+    }
+    for (int pi = p0; pi < p1; ++pi) {
+      __syncthreads();
+      page_store<DH>(r, T, tid);
+      __syncthreads();
+      if (pi + 1 < p1) {
+        const uint16_t* Kt = pages + page_head_offset(lp[pi + 1], h, a.H, BT, DH);
+        page_load<DH>(r, Kt, Kt + BT * DH, tid);
+      }
+      floatx4 s[4];
+      scores<DH>(s, T, qf, lane);
+      online_step<DH, false>(s, m, l, o, lane, qrow, a.scale_log2);
+      pv<DH>(o, T, s, lane);
+    }
+  } else {
+    if (a.null_kv != nullptr) {
+      // the null row: one always-visible key/value pair per head
+      const uint16_t* nk = (const uint16_t*)a.null_kv + (size_t)h * DH + (lane >> 4) * 8;
+      const uint16_t* nv = (const uint16_t*)a.null_kv + ((size_t)a.H + h) * DH;
+      float x = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < DH / 32; ++kk) {
+        const uint4 kr = *(const uint4*)(nk + kk * 32);
+        float kf[8];
+        Chunk<uint16_t>::unpack(kr, kf);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x += (float)qf[kk][j] * kf[j];
+      }
+      x = qsum(x) * a.scale_log2;
+      m = x;
+      l = ((lane >> 4) == 0) ? 1.f : 0.f;
+#pragma unroll
+      for (int dt = 0; dt < DH / 16; ++dt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[dt][i] = bf16_bits_to_f32(nv[dt * 16 + (lane >> 4) * 4 + i]);
+      }
+    }
+    if (a.k_in != nullptr) {
+      const size_t base = (size_t)slot * BT * rs + (size_t)h * DH;
+      intra_store<DH>(T, (const uint16_t*)a.k_in + base, (const uint16_t*)a.v_in + base, rs, tid);
+      __syncthreads();
+      floatx4 s[4];
+      scores<DH>(s, T, qf, lane);
+      online_step<DH, true>(s, m, l, o, lane, qrow, a.scale_log2);
+      pv<DH>(o, T, s, lane);
+    }
+  }
+  l = qsum(l);
+  const size_t qs = (size_t)slot * BT + qrow;
+  if (nms == 0) {
+    const float inv = (l > 0.f) ? 1.f / l : 0.f;
+    uint16_t* orow = (uint16_t*)a.out + qs * rs + (size_t)h * DH;
+#pragma unroll
+    for (int dt = 0; dt < DH / 16; ++dt) {
+      const int d0 = dt * 16 + (lane >> 4) * 4;
+      uint16_t r4[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) r4[i] = f32_to_bf16_bits(o[dt][i] * inv);
+      *(uint2*)(orow + d0) = make_uint2((uint32_t)r4[0] | ((uint32_t)r4[1] << 16),
+                                        (uint32_t)r4[2] | ((uint32_t)r4[3] << 16));
+    }
+  } else {
+    float* part = a.ws + ((qs * a.H + h) * kSplitStride + split) * (DH + 4);
+#pragma unroll
+    for (int dt = 0; dt < DH / 16; ++dt) {
+      const int d0 = dt * 16 + (lane >> 4) * 4;
+      *(float4*)(part + d0) = make_float4(o[dt][0], o[dt][1], o[dt][2], o[dt][3]);
+    }
+    if ((lane >> 4) == 0) {
+      part[DH] = m;
+      part[DH + 1] = l;
+    }
+  }
+}
+
+template <int DH>
+static hipError_t launch_pre(const ReaderArgs& a, hipStream_t s) {
+  int max_split = 0;
+  for (int i = 0; i < a.n_slots; ++i) {
+    const int ns = mem_splits(a.n_read[i], a.pps[i]);
+    if (ns > max_split) max_split = ns;
+  }
+  hipLaunchKernelGGL((k_prefill_mfma<DH>), dim3(max_split + 1, a.H, a.n_slots), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || max_split == 0) return e;
+  return launch_merge_bf16(DH, a, s);
+}
+
+hipError_t launch_prefill_mfma(int b, int dh, const ReaderArgs& a, hipStream_t s) {
+  if (b != BT || a.nq != BT) return hipErrorInvalidValue;
+  if (a.n_slots <= 0) return hipSuccess;
+  if (dh == 32) return launch_pre<32>(a, s);
+  if (dh == 64) return launch_pre<64>(a, s);
+  if (dh == 128) return launch_pre<128>(a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace smem

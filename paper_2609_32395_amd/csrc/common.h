@@ -150,7 +150,9 @@ hipError_t launch_export(int dtype, const void* pages, const int32_t* live_page_
 
 // VALU reader: every split of every (slot, query, head) plus the merge.
 hipError_t launch_reader_valu(int dtype, int b, int dh, const ReaderArgs& a, hipStream_t s);
-// MFMA (bf16) encoder and prefill.
+// Split merge of bf16 outputs (shared by the MFMA prefill).
+hipError_t launch_merge_bf16(int dh, const ReaderArgs& a, hipStream_t s);
+// MFMA (bf16, b = 64) encoder and prefill.
 hipError_t launch_encoder_mfma(int b, int dh, const void* q, const void* k, const void* v, void* out,
                                void* pages, const int32_t* sink_pages, int n_blocks, int H, int mask,
                                float scale_log2, hipStream_t s);

@@ -316,6 +316,15 @@ static hipError_t launch_rv_d(int b, int dh, const ReaderArgs& a, hipStream_t s)
   return hipErrorInvalidValue;
 }
 
+hipError_t launch_merge_bf16(int dh, const ReaderArgs& a, hipStream_t s) {
+  const dim3 grid(a.n_slots * a.nq, a.H);
+  if (dh == 32) hipLaunchKernelGGL((k_merge<uint16_t, 32>), grid, dim3(64), 0, s, a);
+  else if (dh == 64) hipLaunchKernelGGL((k_merge<uint16_t, 64>), grid, dim3(64), 0, s, a);
+  else if (dh == 128) hipLaunchKernelGGL((k_merge<uint16_t, 128>), grid, dim3(64), 0, s, a);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 hipError_t launch_reader_valu(int dtype, int b, int dh, const ReaderArgs& a, hipStream_t s) {
   if (a.n_slots <= 0) return hipSuccess;
   if (dtype == F32) return launch_rv_d<float>(b, dh, a, s);

@@ -315,8 +315,12 @@ smem_status smem_encode_blocks(smem_store* st, const smem_attn_desc* shape, int3
     const char* vb = (const char*)v + (size_t)i0 * blk_elems * es;
     char* ob = out ? (char*)out + (size_t)i0 * blk_elems * es : nullptr;
     hipError_t e;
-    {
-      if (!ob) return fail(SMEM_EINVAL, "encode needs an out tensor");
+    if (dtype == BF16 && b == 64) {
+      int32_t sink[kMaxSlots];
+      for (int i = 0; i < n; ++i) sink[i] = st ? pages[i0 + i] : -1;
+      e = launch_encoder_mfma(b, dh, qb, kb, vb, ob, st ? st->d_pages : nullptr, sink, n, H, mask, scale_log2, s);
+    } else {
+      if (!ob) return fail(SMEM_EINVAL, "this encoder shape needs an out tensor");
       ReaderArgs a;
       memset(&a, 0, sizeof a);
       a.q = qb; a.k_in = kb; a.v_in = vb; a.out = ob;
@@ -386,14 +390,16 @@ smem_status smem_reader_prefill_block(smem_store* st, int32_t n_seq, const int32
     a.max_blocks = d.max_blocks;
     a.H = d.H; a.b = d.b; a.nq = d.b; a.intra_mode = 1;
     a.n_slots = n; a.scale_log2 = scale_log2;
+    // bf16 blocks of 64 tokens run on the MFMA kernel, other shapes on the VALU reader
+    const bool mfma = d.dtype == BF16 && d.b == 64;
     for (int i = 0; i < n; ++i) {
       const int sq = seq_ids[i0 + i];
       a.seq[i] = sq;
       a.n_read[i] = n_read_of(st, sq, query_block[i0 + i]);
-      a.pps[i] = pages_per_split(a.n_read[i], kMinPagesDecode);
+      a.pps[i] = pages_per_split(a.n_read[i], mfma ? kMinPagesPrefill : kMinPagesDecode);
       a.aux[i] = -1;
     }
-    hipError_t e = launch_reader_valu(d.dtype, d.b, d.dh, a, s);
+    hipError_t e = mfma ? launch_prefill_mfma(d.b, d.dh, a, s) : launch_reader_valu(d.dtype, d.b, d.dh, a, s);
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
   }
   return SMEM_OK;
