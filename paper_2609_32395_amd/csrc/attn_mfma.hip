@@ -25,7 +25,7 @@
 namespace smem {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef f32x4 floatx4;
 
 constexpr int BT = 64;         // block / page size handled here
 constexpr int KPAD = 8;        // LDS row padding (elements): 16 bytes per row
@@ -38,7 +38,7 @@ struct Tiles {
   uint16_t vt[DH * VS];
 };
 
-__device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) {
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 u) {
   bf16x8 r;
   __builtin_memcpy(&r, &u, 16);
   return r;
@@ -56,17 +56,17 @@ template <int DH>
 struct PageRegs {
   static constexpr int NK = BT * DH / 8 / 256;
   static constexpr int NV = DH * BT / 8 / 256;
-  uint4 k[NK];
-  uint4 v[NV];
+  u32x4 k[NK];
+  u32x4 v[NV];
 };
 
 template <int DH>
 __device__ __forceinline__ void page_load(PageRegs<DH>& r, const uint16_t* __restrict__ Kt,
                                           const uint16_t* __restrict__ VT, int tid) {
 #pragma unroll
-  for (int i = 0; i < PageRegs<DH>::NK; ++i) r.k[i] = *(const uint4*)(Kt + (size_t)(tid + i * 256) * 8);
+  for (int i = 0; i < PageRegs<DH>::NK; ++i) r.k[i] = *(const u32x4*)(Kt + (size_t)(tid + i * 256) * 8);
 #pragma unroll
-  for (int i = 0; i < PageRegs<DH>::NV; ++i) r.v[i] = *(const uint4*)(VT + (size_t)(tid + i * 256) * 8);
+  for (int i = 0; i < PageRegs<DH>::NV; ++i) r.v[i] = *(const u32x4*)(VT + (size_t)(tid + i * 256) * 8);
 }
 
 template <int DH>
@@ -75,13 +75,13 @@ __device__ __forceinline__ void page_store(const PageRegs<DH>& r, Tiles<DH>& T, 
   for (int i = 0; i < PageRegs<DH>::NK; ++i) {
     const int c = tid + i * 256;
     const int row = c / (DH / 8), c8 = c % (DH / 8);
-    *(uint4*)&T.k[row * Tiles<DH>::KS + c8 * 8] = r.k[i];
+    *(u32x4*)&T.k[row * Tiles<DH>::KS + c8 * 8] = r.k[i];
   }
 #pragma unroll
   for (int i = 0; i < PageRegs<DH>::NV; ++i) {
     const int c = tid + i * 256;
     const int d = c / (BT / 8), c8 = c % (BT / 8);
-    *(uint4*)&T.vt[d * Tiles<DH>::VS + c8 * 8] = r.v[i];
+    *(u32x4*)&T.vt[d * Tiles<DH>::VS + c8 * 8] = r.v[i];
   }
 }
 
@@ -93,9 +93,9 @@ __device__ __forceinline__ void intra_store(Tiles<DH>& T, const uint16_t* __rest
   constexpr int NCH = BT * DH / 8;
   for (int c = tid; c < NCH; c += 256) {
     const int row = c / (DH / 8), c8 = c % (DH / 8);
-    const uint4 kv = *(const uint4*)(kin + row * row_stride + c8 * 8);
-    const uint4 vv = *(const uint4*)(vin + row * row_stride + c8 * 8);
-    *(uint4*)&T.k[row * Tiles<DH>::KS + c8 * 8] = kv;
+    const u32x4 kv = *(const u32x4*)(kin + row * row_stride + c8 * 8);
+    const u32x4 vv = *(const u32x4*)(vin + row * row_stride + c8 * 8);
+    *(u32x4*)&T.k[row * Tiles<DH>::KS + c8 * 8] = kv;
     const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -112,7 +112,7 @@ __device__ __forceinline__ void load_q(bf16x8 (&qf)[DH / 32], const uint16_t* __
                                        int lane) {
   const uint16_t* qr = q + (size_t)(lane & 15) * row_stride + (lane >> 4) * 8;
 #pragma unroll
-  for (int kk = 0; kk < DH / 32; ++kk) qf[kk] = as_bf16x8(*(const uint4*)(qr + kk * 32));
+  for (int kk = 0; kk < DH / 32; ++kk) qf[kk] = as_bf16x8(*(const u32x4*)(qr + kk * 32));
 }
 
 // S^T for this wave's 16 queries against the 64 keys in LDS.
@@ -124,7 +124,7 @@ __device__ __forceinline__ void scores(floatx4 (&s)[4], const Tiles<DH>& T, cons
     const uint16_t* kr = &T.k[(kt * 16 + (lane & 15)) * Tiles<DH>::KS + (lane >> 4) * 8];
 #pragma unroll
     for (int kk = 0; kk < DH / 32; ++kk)
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(*(const uint4*)(kr + kk * 32)), qf[kk], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(*(const u32x4*)(kr + kk * 32)), qf[kk], acc, 0, 0, 0);
     s[kt] = acc;
   }
 }
@@ -137,11 +137,11 @@ __device__ __forceinline__ void pv(floatx4 (&o)[DH / 16], const Tiles<DH>& T, co
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) {
     const uint16_t* vr = &T.vt[(dt * 16 + (lane & 15)) * Tiles<DH>::VS + (lane >> 4) * 4];
-    uint4 a0, a1;
-    const uint2 x0 = *(const uint2*)(vr + 0), y0 = *(const uint2*)(vr + 16);
-    const uint2 x1 = *(const uint2*)(vr + 32), y1 = *(const uint2*)(vr + 48);
-    a0 = make_uint4(x0.x, x0.y, y0.x, y0.y);
-    a1 = make_uint4(x1.x, x1.y, y1.x, y1.y);
+    u32x4 a0, a1;
+    const u32x2 x0 = *(const u32x2*)(vr + 0), y0 = *(const u32x2*)(vr + 16);
+    const u32x2 x1 = *(const u32x2*)(vr + 32), y1 = *(const u32x2*)(vr + 48);
+    a0 = u32x4{x0.x, x0.y, y0.x, y0.y};
+    a1 = u32x4{x1.x, x1.y, y1.x, y1.y};
     o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a0), p0, o[dt], 0, 0, 0);
     o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a1), p1, o[dt], 0, 0, 0);
   }
@@ -243,10 +243,10 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
     uint16_t r[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) r[i] = f32_to_bf16_bits(o[dt][i] * inv);
-    const uint2 packed = make_uint2((uint32_t)r[0] | ((uint32_t)r[1] << 16), (uint32_t)r[2] | ((uint32_t)r[3] << 16));
-    if (a.out) *(uint2*)(a.out + orow * rs + (size_t)h * DH + d0) = packed;
+    const u32x2 packed = u32x2{(uint32_t)r[0] | ((uint32_t)r[1] << 16), (uint32_t)r[2] | ((uint32_t)r[3] << 16)};
+    if (a.out) *(u32x2*)(a.out + orow * rs + (size_t)h * DH + d0) = packed;
     if (kp) {
-      *(uint2*)(kp + qrow * DH + d0) = packed;
+      *(u32x2*)(kp + qrow * DH + d0) = packed;
 #pragma unroll
       for (int i = 0; i < 4; ++i) kp[BT * DH + (d0 + i) * BT + qrow] = r[i];
     }
@@ -304,26 +304,38 @@ __global__ void __launch_bounds__(256) k_prefill_mfma(ReaderArgs a) {
   float m = -INFINITY, l = 0.f;
 
   if (split < nms) {
+    // Pages stream through a ring of kDepth register stages: page pi is moved
+    // to LDS while pages pi+1 .. pi+kDepth-1 are still in flight.
+    constexpr int kDepth = 3;
     const int p0 = split * pps, p1 = min(n_read, p0 + pps);
     const int32_t* lp = a.live_page + (size_t)a.seq[slot] * a.max_blocks;
     const uint16_t* pages = (const uint16_t*)a.pages;
-    PageRegs<DH> r;
-    {
-      const uint16_t* Kt = pages + page_head_offset(lp[p0], h, a.H, BT, DH);
-      page_load<DH>(r, Kt, Kt + BT * DH, tid);
-    }
-    for (int pi = p0; pi < p1; ++pi) {
-      __syncthreads();
-      page_store<DH>(r, T, tid);
-      __syncthreads();
-      if (pi + 1 < p1) {
-        const uint16_t* Kt = pages + page_head_offset(lp[pi + 1], h, a.H, BT, DH);
-        page_load<DH>(r, Kt, Kt + BT * DH, tid);
+    PageRegs<DH> r[kDepth];
+#pragma unroll
+    for (int u = 0; u < kDepth; ++u) {
+      if (p0 + u < p1) {
+        const uint16_t* Kt = pages + page_head_offset(lp[p0 + u], h, a.H, BT, DH);
+        page_load<DH>(r[u], Kt, Kt + BT * DH, tid);
       }
-      floatx4 s[4];
-      scores<DH>(s, T, qf, lane);
-      online_step<DH, false>(s, m, l, o, lane, qrow, a.scale_log2);
-      pv<DH>(o, T, s, lane);
+    }
+    for (int base = p0; base < p1; base += kDepth) {
+#pragma unroll
+      for (int u = 0; u < kDepth; ++u) {
+        const int pi = base + u;
+        if (pi < p1) {
+          __syncthreads();
+          page_store<DH>(r[u], T, tid);
+          __syncthreads();
+          if (pi + kDepth < p1) {
+            const uint16_t* Kt = pages + page_head_offset(lp[pi + kDepth], h, a.H, BT, DH);
+            page_load<DH>(r[u], Kt, Kt + BT * DH, tid);
+          }
+          floatx4 s[4];
+          scores<DH>(s, T, qf, lane);
+          online_step<DH, false>(s, m, l, o, lane, qrow, a.scale_log2);
+          pv<DH>(o, T, s, lane);
+        }
+      }
     }
   } else {
     if (a.null_kv != nullptr) {
@@ -333,7 +345,7 @@ __global__ void __launch_bounds__(256) k_prefill_mfma(ReaderArgs a) {
       float x = 0.f;
 #pragma unroll
       for (int kk = 0; kk < DH / 32; ++kk) {
-        const uint4 kr = *(const uint4*)(nk + kk * 32);
+        const u32x4 kr = *(const u32x4*)(nk + kk * 32);
         float kf[8];
         Chunk<uint16_t>::unpack(kr, kf);
 #pragma unroll
@@ -369,15 +381,15 @@ __global__ void __launch_bounds__(256) k_prefill_mfma(ReaderArgs a) {
       uint16_t r4[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) r4[i] = f32_to_bf16_bits(o[dt][i] * inv);
-      *(uint2*)(orow + d0) = make_uint2((uint32_t)r4[0] | ((uint32_t)r4[1] << 16),
-                                        (uint32_t)r4[2] | ((uint32_t)r4[3] << 16));
+      *(u32x2*)(orow + d0) = u32x2{(uint32_t)r4[0] | ((uint32_t)r4[1] << 16),
+                                   (uint32_t)r4[2] | ((uint32_t)r4[3] << 16)};
     }
   } else {
     float* part = a.ws + ((qs * a.H + h) * kSplitStride + split) * (DH + 4);
 #pragma unroll
     for (int dt = 0; dt < DH / 16; ++dt) {
       const int d0 = dt * 16 + (lane >> 4) * 4;
-      *(float4*)(part + d0) = make_float4(o[dt][0], o[dt][1], o[dt][2], o[dt][3]);
+      *(f32x4*)(part + d0) = o[dt];
     }
     if ((lane >> 4) == 0) {
       part[DH] = m;
@@ -396,7 +408,7 @@ static hipError_t launch_pre(const ReaderArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((k_prefill_mfma<DH>), dim3(max_split + 1, a.H, a.n_slots), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || max_split == 0) return e;
-  return launch_merge_bf16(DH, a, s);
+  return launch_merge(BF16, DH, a, s);
 }
 
 hipError_t launch_prefill_mfma(int b, int dh, const ReaderArgs& a, hipStream_t s) {

@@ -21,22 +21,32 @@ constexpr int kMaxEdits = 128;
 // splits of whole pages, plus one split for the null row and in-block keys.
 constexpr int kSplitCap = 64;
 constexpr int kSplitStride = kSplitCap + 1;
-// Minimum pages per split (decode / VALU reader and MFMA prefill).
+// Minimum pages per split and split caps (decode / VALU reader, MFMA prefill).
+// A prefill split's partial output is b rows of dh+4 floats, so prefill uses
+// fewer, longer splits to keep the partials small next to the pages read.
 constexpr int kMinPagesDecode = 8;
 constexpr int kMinPagesPrefill = 4;
+constexpr int kSplitCapPrefill = 32;
 // Query slots whose prefill partials the workspace must hold at once.
 constexpr int kPrefillSlotChunk = 16;
 
 // Pages per split: a function of the number of memory pages read only, so a
 // query's split boundaries (and hence its rounding) never depend on the
 // batch it is in or on the physical page numbers.
-inline int pages_per_split(int n_read, int min_pages) {
-  int p = (n_read + kSplitCap - 1) / kSplitCap;
+inline int pages_per_split(int n_read, int min_pages, int cap = kSplitCap) {
+  int p = (n_read + cap - 1) / cap;
   return p < min_pages ? min_pages : p;
 }
 inline int mem_splits(int n_read, int pps) { return (n_read + pps - 1) / pps; }
+__device__ __forceinline__ int mem_splits_dev(int n_read, int pps) { return (n_read + pps - 1) / pps; }
 
 enum Dtype : int32_t { F32 = 0, BF16 = 1 };
+
+// Native vector types (kept in registers by the compiler; used for every
+// 16- and 8-byte load, store and register stage).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------- conversions
 
@@ -54,14 +64,14 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
 template <typename T> struct Chunk;
 template <> struct Chunk<float> {
   static constexpr int E = 4;
-  __device__ __forceinline__ static void unpack(const uint4& c, float* f) {
+  __device__ __forceinline__ static void unpack(const u32x4& c, float* f) {
     f[0] = __uint_as_float(c.x); f[1] = __uint_as_float(c.y);
     f[2] = __uint_as_float(c.z); f[3] = __uint_as_float(c.w);
   }
 };
 template <> struct Chunk<uint16_t> {
   static constexpr int E = 8;
-  __device__ __forceinline__ static void unpack(const uint4& c, float* f) {
+  __device__ __forceinline__ static void unpack(const u32x4& c, float* f) {
     f[0] = __uint_as_float(c.x << 16); f[1] = __uint_as_float(c.x & 0xffff0000u);
     f[2] = __uint_as_float(c.y << 16); f[3] = __uint_as_float(c.y & 0xffff0000u);
     f[4] = __uint_as_float(c.z << 16); f[5] = __uint_as_float(c.z & 0xffff0000u);
@@ -88,7 +98,7 @@ __host__ __device__ inline size_t page_head_offset(int page, int h, int H, int b
 
 struct DevLayout {
   size_t off_table, off_live_page, off_live_blk, off_n_live, off_ws, off_pages, total;
-  size_t ws_floats;
+  size_t ws_floats;    // split partials
 };
 
 // ---------------------------------------------------------------- kernel args
@@ -148,10 +158,10 @@ hipError_t launch_scrub(int dtype, void* pages, int page, int H, int b, int dh, 
 hipError_t launch_export(int dtype, const void* pages, const int32_t* live_page_seq, int n_live,
                          int H, int b, int dh, void* k_out, void* v_out, hipStream_t s);
 
-// VALU reader: every split of every (slot, query, head) plus the merge.
+// VALU reader: every split of every (slot, query, head), then the merge.
 hipError_t launch_reader_valu(int dtype, int b, int dh, const ReaderArgs& a, hipStream_t s);
-// Split merge of bf16 outputs (shared by the MFMA prefill).
-hipError_t launch_merge_bf16(int dh, const ReaderArgs& a, hipStream_t s);
+// Merge the split partials of every (query row, head) in split order.
+hipError_t launch_merge(int dtype, int dh, const ReaderArgs& a, hipStream_t s);
 // MFMA (bf16, b = 64) encoder and prefill.
 hipError_t launch_encoder_mfma(int b, int dh, const void* q, const void* k, const void* v, void* out,
                                void* pages, const int32_t* sink_pages, int n_blocks, int H, int mask,

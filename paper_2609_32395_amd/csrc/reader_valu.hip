@@ -63,7 +63,7 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
   float qf[E];
   {
     const T* qp = (const T*)a.q + ((size_t)qs * a.H + h) * DH + c * E;
-    Chunk<T>::unpack(*(const uint4*)qp, qf);
+    Chunk<T>::unpack(*(const u32x4*)qp, qf);
 #pragma unroll
     for (int e = 0; e < E; ++e) qf[e] *= a.scale_log2;
   }
@@ -82,12 +82,12 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
       const int pg = lp[pi];
       const T* Kt = (const T*)a.pages + page_head_offset(pg, h, a.H, B, DH);
       const T* VT = Kt + B * DH;
-      uint4 kraw[C::KLOADS];
-      uint4 vraw[C::VLOADS];
+      u32x4 kraw[C::KLOADS];
+      u32x4 vraw[C::VLOADS];
 #pragma unroll
-      for (int i = 0; i < C::KLOADS; ++i) kraw[i] = *(const uint4*)(Kt + (i * C::RPL + rg) * DH + c * E);
+      for (int i = 0; i < C::KLOADS; ++i) kraw[i] = *(const u32x4*)(Kt + (i * C::RPL + rg) * DH + c * E);
 #pragma unroll
-      for (int v = 0; v < C::VLOADS; ++v) vraw[v] = *(const uint4*)(VT + (v * C::DPL + dr) * B + kc * E);
+      for (int v = 0; v < C::VLOADS; ++v) vraw[v] = *(const u32x4*)(VT + (v * C::DPL + dr) * B + kc * E);
       float s[C::KLOADS];
 #pragma unroll
       for (int i = 0; i < C::KLOADS; ++i) {
@@ -158,8 +158,8 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
       const T* nk = (const T*)a.null_kv + (size_t)h * DH + c * E;
       const T* nv = (const T*)a.null_kv + ((size_t)a.H + h) * DH + c * E;
       float kf[E], vf[E];
-      Chunk<T>::unpack(*(const uint4*)nk, kf);
-      Chunk<T>::unpack(*(const uint4*)nv, vf);
+      Chunk<T>::unpack(*(const u32x4*)nk, kf);
+      Chunk<T>::unpack(*(const u32x4*)nv, vf);
       float x = 0.f;
 #pragma unroll
       for (int e = 0; e < E; ++e) x += qf[e] * kf[e];
@@ -194,8 +194,8 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
           ks = (const T*)a.k_in + (((size_t)slot * B + r) * a.H + h) * DH;
           vs = (const T*)a.v_in + (((size_t)slot * B + r) * a.H + h) * DH;
         }
-        Chunk<T>::unpack(*(const uint4*)(ks + c * E), kf);
-        Chunk<T>::unpack(*(const uint4*)(vs + c * E), vf);
+        Chunk<T>::unpack(*(const u32x4*)(ks + c * E), kf);
+        Chunk<T>::unpack(*(const u32x4*)(vs + c * E), vf);
       }
       float x = 0.f;
 #pragma unroll
@@ -218,8 +218,8 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
       // write the new token's key/value into the in-block cache at row pos
       const size_t src = ((size_t)slot * a.H + h) * DH + c * E;
       const size_t dst = (((size_t)slot * B + pos) * a.H + h) * DH + c * E;
-      *(uint4*)((T*)a.k_cache_w + dst) = *(const uint4*)((const T*)a.k_new + src);
-      *(uint4*)((T*)a.v_cache_w + dst) = *(const uint4*)((const T*)a.v_new + src);
+      *(u32x4*)((T*)a.k_cache_w + dst) = *(const u32x4*)((const T*)a.k_new + src);
+      *(u32x4*)((T*)a.v_cache_w + dst) = *(const u32x4*)((const T*)a.v_new + src);
     }
 #pragma unroll
     for (int e = 0; e < E; ++e) {
@@ -261,29 +261,57 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
   }
 }
 
-// Combine the splits of one (query, head) in split order.
+// Merge the splits of one (query row, head) in split order: the split
+// statistics are loaded in parallel, the weights kept in LDS, and each thread
+// sums one output dimension over the splits.
 template <typename T, int DH>
-__global__ void __launch_bounds__(64) k_merge(ReaderArgs a) {
+__global__ void __launch_bounds__(128) k_merge(ReaderArgs a) {
   const int qs = blockIdx.x, h = blockIdx.y;
   const int slot = qs / a.nq;
-  const int n_read = a.n_read[slot], pps = a.pps[slot];
-  const int S = (n_read + pps - 1) / pps + 1;
+  const int S = mem_splits_dev(a.n_read[slot], a.pps[slot]) + 1;
   if (S == 1) return;
+  __shared__ float w_sh[kSplitStride];
+  __shared__ float l_sh[kSplitStride];
+  __shared__ float wmax[2];
+  __shared__ float inv_sh;
+  const int tid = threadIdx.x;
   const float* base = a.ws + ((size_t)qs * a.H + h) * kSplitStride * (DH + 4);
-  float M = -INFINITY;
-  for (int k = 0; k < S; ++k) M = fmaxf(M, base[(size_t)k * (DH + 4) + DH]);
-  for (int d = threadIdx.x; d < DH; d += 64) {
-    float L = 0.f, A = 0.f;
-    for (int k = 0; k < S; ++k) {
-      const float* pk = base + (size_t)k * (DH + 4);
-      const float mk = pk[DH];
-      const float w = (mk == -INFINITY) ? 0.f : exp2f(mk - M);
-      L += w * pk[DH + 1];
-      A += w * pk[d];
-    }
-    const float o = (L > 0.f) ? A / L : 0.f;
-    ((T*)a.out)[((size_t)qs * a.H + h) * DH + d] = from_f32<T>(o);
+  const float mk = (tid < S) ? base[(size_t)tid * (DH + 4) + DH] : -INFINITY;
+  if (tid < S) l_sh[tid] = base[(size_t)tid * (DH + 4) + DH + 1];
+  float mx = mk;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+  if ((tid & 63) == 0) wmax[tid >> 6] = mx;
+  __syncthreads();
+  const float M = fmaxf(wmax[0], wmax[1]);
+  if (tid < S) w_sh[tid] = (mk == -INFINITY) ? 0.f : exp2f(mk - M);
+  __syncthreads();
+  if (tid == 0) {
+    float L = 0.f;
+    for (int k = 0; k < S; ++k) L += w_sh[k] * l_sh[k];
+    inv_sh = (L > 0.f) ? 1.f / L : 0.f;
   }
+  __syncthreads();
+  for (int d = tid; d < DH; d += 128) {
+    float A = 0.f;
+#pragma unroll 8
+    for (int k = 0; k < S; ++k) A += w_sh[k] * base[(size_t)k * (DH + 4) + d];
+    ((T*)a.out)[((size_t)qs * a.H + h) * DH + d] = from_f32<T>(A * inv_sh);
+  }
+}
+
+template <typename T>
+static hipError_t launch_merge_t(int dh, const ReaderArgs& a, hipStream_t s) {
+  const dim3 grid(a.n_slots * a.nq, a.H);
+  if (dh == 32) hipLaunchKernelGGL((k_merge<T, 32>), grid, dim3(128), 0, s, a);
+  else if (dh == 64) hipLaunchKernelGGL((k_merge<T, 64>), grid, dim3(128), 0, s, a);
+  else if (dh == 128) hipLaunchKernelGGL((k_merge<T, 128>), grid, dim3(128), 0, s, a);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_merge(int dtype, int dh, const ReaderArgs& a, hipStream_t s) {
+  return dtype == F32 ? launch_merge_t<float>(dh, a, s) : launch_merge_t<uint16_t>(dh, a, s);
 }
 
 template <typename T, int DH, int B>
@@ -297,8 +325,7 @@ static hipError_t launch_rv(const ReaderArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((k_reader_valu<T, DH, B>), grid, dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || max_split == 0) return e;
-  hipLaunchKernelGGL((k_merge<T, DH>), dim3(a.n_slots * a.nq, a.H), dim3(64), 0, s, a);
-  return hipGetLastError();
+  return launch_merge(sizeof(T) == 4 ? F32 : BF16, DH, a, s);
 }
 
 template <typename T, int DH>
@@ -314,15 +341,6 @@ static hipError_t launch_rv_d(int b, int dh, const ReaderArgs& a, hipStream_t s)
   if (dh == 64) return launch_rv_b<T, 64>(b, a, s);
   if (dh == 128) return launch_rv_b<T, 128>(b, a, s);
   return hipErrorInvalidValue;
-}
-
-hipError_t launch_merge_bf16(int dh, const ReaderArgs& a, hipStream_t s) {
-  const dim3 grid(a.n_slots * a.nq, a.H);
-  if (dh == 32) hipLaunchKernelGGL((k_merge<uint16_t, 32>), grid, dim3(64), 0, s, a);
-  else if (dh == 64) hipLaunchKernelGGL((k_merge<uint16_t, 64>), grid, dim3(64), 0, s, a);
-  else if (dh == 128) hipLaunchKernelGGL((k_merge<uint16_t, 128>), grid, dim3(64), 0, s, a);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
 }
 
 hipError_t launch_reader_valu(int dtype, int b, int dh, const ReaderArgs& a, hipStream_t s) {

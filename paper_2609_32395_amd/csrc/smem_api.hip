@@ -71,9 +71,9 @@ bool layout_of(const smem_store_desc* d, DevLayout* L) {
   if (d->n_seq < 1 || d->max_blocks < 1 || d->n_pages < 1) return false;
   if (!shape_ok(d->b, d->H, d->dh, d->dtype)) return false;
   const size_t nt = (size_t)d->n_seq * d->max_blocks;
-  const size_t dec = (size_t)d->n_seq * d->H * kSplitStride * (d->dh + 4);
-  const size_t pre = (size_t)std::min(d->n_seq, kPrefillSlotChunk) * d->b * d->H * kSplitStride * (d->dh + 4);
-  L->ws_floats = std::max(dec, pre);
+  const size_t dec_rows = (size_t)d->n_seq * d->H;
+  const size_t pre_rows = (size_t)std::min(d->n_seq, kPrefillSlotChunk) * d->b * d->H;
+  L->ws_floats = std::max(dec_rows, pre_rows) * kSplitStride * (d->dh + 4);
   size_t off = 0;
   L->off_table = off;     off = align256(off + nt * 4);
   L->off_live_page = off; off = align256(off + nt * 4);
@@ -396,7 +396,8 @@ smem_status smem_reader_prefill_block(smem_store* st, int32_t n_seq, const int32
       const int sq = seq_ids[i0 + i];
       a.seq[i] = sq;
       a.n_read[i] = n_read_of(st, sq, query_block[i0 + i]);
-      a.pps[i] = pages_per_split(a.n_read[i], mfma ? kMinPagesPrefill : kMinPagesDecode);
+      a.pps[i] = mfma ? pages_per_split(a.n_read[i], kMinPagesPrefill, kSplitCapPrefill)
+                      : pages_per_split(a.n_read[i], kMinPagesDecode);
       a.aux[i] = -1;
     }
     hipError_t e = mfma ? launch_prefill_mfma(d.b, d.dh, a, s) : launch_reader_valu(d.dtype, d.b, d.dh, a, s);
