@@ -40,6 +40,22 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 BF16_PEAK_TFLOPS = 2516.6      # MI355X dense bf16 MFMA, published
 
+# HBM bytes per decode call measured with rocprofv3 FETCH_SIZE/WRITE_SIZE
+# (scaled by a plain copy of known size), keyed by a hash of the decode
+# kernel's sources: a changed kernel reports traffic as null until measured
+# again.  Figures: profiles/k_reader_valu_decode_410M_hbm_traffic.md
+DECODE_TRAFFIC_BYTES = {"299df4be05b1e948": 1.0897e9}
+DECODE_SOURCES = ("paper_2609_32395_amd/csrc/reader_valu.hip", "paper_2609_32395_amd/csrc/common.h")
+
+
+def _sources_hash(paths):
+    import hashlib
+    m = hashlib.sha1()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            m.update(f.read())
+    return m.hexdigest()[:16]
+
 
 def _events_time(fn, steps, stream):
     import torch
@@ -258,6 +274,9 @@ def main():
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="after the timed region, copy a MIB-MiB tensor once (a plain copy kernel of known "
+                         "size, used to scale hardware traffic counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported (the path is single-GPU; "
@@ -269,6 +288,13 @@ def main():
     torch.cuda.set_device(0)
 
     dec = decode_workload(args, torch, smem, synth)
+    if args.copy_probe:
+        src = torch.ones(args.copy_probe * (1 << 20) // 2, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     secondary = {}
     if not args.no_secondary:
         secondary["encode_prefill_160M"] = encode_prefill_workload(args, torch, smem, synth)
@@ -295,7 +321,8 @@ def main():
                    "global_batch": 64, "memory_rows": 4096, "heads": 16, "head_dim": 64, "block": 64,
                    "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": DECODE_TRAFFIC_BYTES.get(_sources_hash(DECODE_SOURCES)),
                      "kernel": "smem_reader_decode (k_reader_valu + k_merge)",
                      "bytes_per_launch": dec["bytes_per_step"]},
         "hbm_gbs": round(achieved, 1),
