@@ -143,3 +143,26 @@ def null_row(w: Workload, seed: int) -> np.ndarray:
 def decode_positions(w: Workload, seed: int, n_seq: int) -> np.ndarray:
     """In-block positions p in [0, b) of the decode query, uniform per sequence."""
     return rng(seed, w.wid, ROLE_POS, 0, 0, 0).integers(0, w.b, size=n_seq).astype(np.int32)
+
+
+# ---------------------------------------------------------------- device-side draws
+# The 1.5B-shaped stress store holds 16 x 4096 blocks (32 GiB of bf16 rows):
+# too much to draw on the host.  Its rows are drawn on the GPU by torch's
+# seeded generator, one generator seed per block key, so any block can be
+# re-drawn alone (for re-inserts and for the oracle's copy) with the same
+# bytes.  Both sides consume those bytes: the HIP path from device memory,
+# the oracle from a host copy of the generator's output.
+
+def block_seed(*key: int) -> int:
+    """64-bit generator seed for a block key (SeedSequence hash of the key)."""
+    return int(np.random.SeedSequence([int(k) for k in key]).generate_state(1, np.uint64)[0] >> np.uint64(1))
+
+
+def memory_block_device(w: Workload, seed: int, seq: int, block: int, version: int = 0, device="cuda"):
+    """K and V rows [b, H, dh] of a memory block drawn on the device (bf16 or fp32)."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(block_seed(seed, w.wid, ROLE_KMEM, seq, block, version))
+    x = torch.randn((2,) + w.row_shape, generator=g, device=device, dtype=torch.float32) * w.scale
+    x = x.to(torch.bfloat16 if w.dtype == "bf16" else torch.float32)
+    return x[0], x[1]

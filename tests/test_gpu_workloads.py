@@ -1,0 +1,245 @@
+"""Full-size workloads on the GPU, in the launch configuration bench.py times,
+checked against the fp64 oracle on sampled outputs (sequences / heads /
+steps the oracle finishes in seconds) and by bitwise GPU-vs-GPU invariants.
+
+Workloads (seeded synthetic inputs, shapes of the paper's model scales):
+  160M  encode 8 x 16 blocks (12 heads x dh 64) into the store, prefill the final blocks
+  410M  batched decode, 64 sequences x 4096 memory rows, 16 heads x dh 64
+  1.5B  single-block serve over 32768 rows (16 heads x dh 128), 100 delete + re-serve
+  1.5B  stress: 16 sequences x 4096 blocks (32 GiB), 128 decode steps with
+        interleaved deletions and re-insertions; final state checked bitwise
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import smem_oracle as O
+from paper_2609_32395_amd import smem, synth
+from tests.gpu_util import check, dev, host, require_gpu, say
+
+pytestmark = pytest.mark.gpu
+BF = torch.bfloat16
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def test_encode_prefill_160M():
+    w = synth.ENC_160M
+    S, H, dh, b, NB = w.n_seq, w.H, w.dh, w.b, w.n_blocks
+    say("160M encode+prefill", S, NB, H, dh)
+    q = np.stack([synth.block_tokens(w, 0, synth.ROLE_Q, s, j) for s in range(S) for j in range(NB)])
+    k = np.stack([synth.block_tokens(w, 0, synth.ROLE_K, s, j) for s in range(S) for j in range(NB)])
+    v = np.stack([synth.block_tokens(w, 0, synth.ROLE_V, s, j) for s in range(S) for j in range(NB)])
+    seqs = [s for s in range(S) for j in range(NB)]
+    blks = [j for s in range(S) for j in range(NB)]
+    st = smem.Store(S, NB, S * NB, b, H, dh, BF)
+    ref = O.Store(S, NB, b, H, dh)
+    Q, K, V = (dev(x.reshape(-1, H, dh), BF) for x in (q, k, v))
+    out = smem.smem_encode_blocks(st, Q, K, V, seq_ids=seqs, block_idx=blks, mask=smem.MASK_BIDIR)
+    renc = O.encode_into_store(ref, seqs, blks, q, k, v, O.MASK_BIDIR)
+    check(out, renc.reshape(-1, H, dh), BF, "encoder, 128 blocks")
+    # stored rows are the output bits
+    for s in (0, S - 1):
+        idx, Ks, Vs = smem.smem_store_export(st, s)
+        assert idx == list(range(NB))
+        exp = out[s * NB * b:(s + 1) * NB * b]
+        assert torch.equal(Ks, exp) and torch.equal(Vs, exp)
+    # prefill of each sequence's final block over blocks 0..14 (its own rows are present, not read)
+    last = [s * NB + NB - 1 for s in range(S)]
+    qp, kp, vp = (np.stack([x[i] for i in last]) for x in (q, k, v))
+    pout = smem.smem_reader_prefill_block(st, list(range(S)), [NB - 1] * S, dev(qp.reshape(-1, H, dh), BF),
+                                          dev(kp.reshape(-1, H, dh), BF), dev(vp.reshape(-1, H, dh), BF))
+    # end to end against the oracle's own encoder outputs (fp64 memory rows)
+    rpre = O.reader_prefill_block(ref, list(range(S)), [NB - 1] * S, qp, kp, vp)
+    check(pout, rpre.reshape(-1, H, dh), BF, "prefill over oracle-encoded memory")
+
+
+def _decode_inputs(w, seed, S, H, dh, b, steps):
+    g = synth.rng(seed, w.wid, synth.ROLE_QDEC, 0, 0, 0)
+    qs = synth.bf16_round((g.standard_normal((steps, S, H, dh)) * w.scale).astype(np.float32))
+    kn = synth.bf16_round((g.standard_normal((steps, S, H, dh)) * w.scale).astype(np.float32))
+    vn = synth.bf16_round((g.standard_normal((steps, S, H, dh)) * w.scale).astype(np.float32))
+    kc = synth.bf16_round((g.standard_normal((S * b, H, dh)) * w.scale).astype(np.float32))
+    vc = synth.bf16_round((g.standard_normal((S * b, H, dh)) * w.scale).astype(np.float32))
+    return qs, kn, vn, kc, vc
+
+
+def test_decode_410M_sampled():
+    w = synth.DEC_410M
+    S, H, dh, b, NB = w.n_seq, w.H, w.dh, w.b, w.n_blocks
+    say("410M decode", S, NB, H, dh)
+    st = smem.Store(S, NB + 1, S * NB, b, H, dh, BF)
+    for s in range(S):
+        Kh, Vh = synth.memory_blocks(w, 0, [s], range(NB), threads=16)
+        Kd, Vd = dev(Kh[0], BF), dev(Vh[0], BF)
+        for j in range(NB):
+            smem.smem_store_put_block(st, s, j, Kd[j], Vd[j])
+    steps = 3
+    qs, kn, vn, kc0, vc0 = _decode_inputs(w, 0, S, H, dh, b, steps)
+    p0 = synth.decode_positions(w, 0, S)
+    kc, vc = dev(kc0, BF), dev(vc0, BF)
+    kc_h, vc_h = kc0.reshape(S, b, H, dh).copy(), vc0.reshape(S, b, H, dh).copy()
+    sample = [0, 17, 42, 63]
+    refs = {s: O.Store(S, NB + 1, b, H, dh) for s in sample}
+    for s in sample:
+        Kh, Vh = synth.memory_blocks(w, 0, [s], range(NB), threads=16)
+        for j in range(NB):
+            refs[s].put(s, j, Kh[0, j], Vh[0, j])
+    for t in range(steps):
+        pos = [int((p0[s] + t) % b) for s in range(S)]
+        out = smem.smem_reader_decode(st, list(range(S)), [NB] * S, pos, dev(qs[t], BF), dev(kn[t], BF),
+                                      dev(vn[t], BF), kc, vc)
+        got = host(out)
+        for s in sample:
+            r, kcs, vcs = O.reader_decode(refs[s], [s], [NB], [pos[s]], qs[t, s:s + 1], kn[t, s:s + 1],
+                                          vn[t, s:s + 1], kc_h[s:s + 1], vc_h[s:s + 1])
+            kc_h[s], vc_h[s] = kcs[0], vcs[0]
+            check(got[s:s + 1], r, BF, f"decode step {t} seq {s}")
+        # the in-block caches of every sequence took the new row at pos
+        kch = host(kc).reshape(S, b, H, dh)
+        assert all(np.array_equal(kch[s, pos[s]], kn[t, s]) for s in range(S))
+
+
+def _heads(x, hs):
+    return np.ascontiguousarray(x[..., hs, :])
+
+
+def test_serve_1p5B_delete_reserve():
+    w = synth.SERVE_1P5B
+    H, dh, b, NB = w.H, w.dh, w.b, w.n_blocks
+    say("1.5B serve", NB, H, dh)
+    Kh, Vh = synth.memory_blocks(w, 0, [0], range(NB), threads=16)
+    Kh, Vh = Kh[0], Vh[0]
+    st = smem.Store(1, NB + 1, NB, b, H, dh, BF)
+    Kd, Vd = dev(Kh, BF), dev(Vh, BF)
+    for j in range(NB):
+        smem.smem_store_put_block(st, 0, j, Kd[j], Vd[j])
+    q = synth.block_tokens(w, 0, synth.ROLE_Q, 0, NB)
+    k = synth.block_tokens(w, 0, synth.ROLE_K, 0, NB)
+    v = synth.block_tokens(w, 0, synth.ROLE_V, 0, NB)
+    qd, kd, vd = dev(q, BF), dev(k, BF), dev(v, BF)
+    hs = [0, 5, 10, 15]   # oracle on a head subset: heads are independent
+
+    def oracle_serve(blocks):
+        ref = O.Store(1, NB + 1, b, len(hs), dh)
+        for j in blocks:
+            ref.put(0, j, _heads(Kh[j], hs), _heads(Vh[j], hs))
+        return O.reader_prefill_block(ref, [0], [NB], _heads(q, hs)[None], _heads(k, hs)[None], _heads(v, hs)[None])[0]
+
+    out = smem.smem_reader_prefill_block(st, [0], [NB], qd, kd, vd)
+    check(host(out)[:, hs], oracle_serve(range(NB)), BF, "serve over 32768 rows (4 heads)")
+    order = synth.rng(0, w.wid, synth.ROLE_EDIT, 0, 0, 0).permutation(NB)[:100]
+    for i, j in enumerate(order):
+        smem.smem_delete_block(st, 0, int(j))
+        out = smem.smem_reader_prefill_block(st, [0], [NB], qd, kd, vd)
+    remaining = sorted(set(range(NB)) - set(int(j) for j in order))
+    check(host(out)[:, hs], oracle_serve(remaining), BF, "re-serve after 100 deletes (4 heads)")
+    # exact deletion: bit-identical to a store where the 100 blocks were never inserted
+    fresh = smem.Store(1, NB + 1, NB, b, H, dh, BF)
+    for j in reversed(remaining):
+        smem.smem_store_put_block(fresh, 0, j, Kd[j], Vd[j])
+    assert torch.equal(smem.smem_reader_prefill_block(fresh, [0], [NB], qd, kd, vd), out)
+    assert smem.smem_store_export(st, 0, rows=False)[0] == remaining
+
+
+def test_stress_1p5B_edits_final_state():
+    """16 sequences x 4096 blocks (32 GiB); 128 batch-16 decode steps, each after
+    4 random deletions and 2 re-insertions (original bytes, same index) of
+    blocks deleted in earlier steps.  The final memory must match the oracle's
+    (live lists, every block's bytes) and equal, bit for bit, a store built
+    by a different edit path reaching the same multiset."""
+    w = synth.STRESS_1P5B
+    S, H, dh, b, NB = w.n_seq, w.H, w.dh, w.b, w.n_blocks
+    say("1.5B stress", S, NB, H, dh)
+    free = torch.cuda.mem_get_info()[0]
+    if free < 80 * 2 ** 30:
+        pytest.skip(f"needs ~80 GiB of device memory, {free / 2 ** 30:.0f} GiB free")
+    st = smem.Store(S, NB, S * NB, b, H, dh, BF)
+    for s in range(S):
+        for j in range(NB):
+            smem.smem_store_put_block(st, s, j, *synth.memory_block_device(w, 0, s, j))
+    torch.cuda.synchronize()
+    say("stress store filled")
+    live = [set(range(NB)) for _ in range(S)]
+    absent = []
+    er = synth.rng(0, w.wid, synth.ROLE_EDIT, 1, 0, 0)
+    steps = 128
+    qs, kn, vn, kc0, vc0 = _decode_inputs(w, 0, S, H, dh, b, steps)
+    p0 = synth.decode_positions(w, 0, S)
+    kc, vc = dev(kc0, BF), dev(vc0, BF)
+    kc_h, vc_h = kc0.reshape(S, b, H, dh).copy(), vc0.reshape(S, b, H, dh).copy()
+    sample_seqs, hs = [3, 11], [0, 9]
+    snap = {}
+    for t in range(steps):
+        back = []
+        if absent:
+            for _ in range(min(2, len(absent))):
+                back.append(absent.pop(int(er.integers(0, len(absent)))))
+        for _ in range(4):
+            s = int(er.integers(0, S))
+            j = int(er.choice(sorted(live[s])))
+            smem.smem_delete_block(st, s, j, scrub=bool(t % 2))
+            live[s].discard(j)
+            absent.append((s, j))
+        for s, j in back:
+            smem.smem_store_put_block(st, s, j, *synth.memory_block_device(w, 0, s, j))
+            live[s].add(j)
+        pos = [int((p0[s] + t) % b) for s in range(S)]
+        out = smem.smem_reader_decode(st, list(range(S)), [NB] * S, pos, dev(qs[t], BF), dev(kn[t], BF),
+                                      dev(vn[t], BF), kc, vc)
+        if t in (0, steps - 1):
+            snap[t] = (host(out), [sorted(live[s]) for s in sample_seqs], pos,
+                       kc_h[sample_seqs].copy(), vc_h[sample_seqs].copy())
+        for s in range(S):
+            kc_h[s, pos[s]], vc_h[s, pos[s]] = kn[t, s], vn[t, s]
+    torch.cuda.synchronize()
+    say("stress decode done; checking final state")
+    # final state: live lists and every block's bytes
+    for s in range(S):
+        idx, K, V = smem.smem_store_export(st, s)
+        assert idx == sorted(live[s])
+        for i0 in range(0, len(idx), 512):
+            chunk = idx[i0:i0 + 512]
+            pairs = [synth.memory_block_device(w, 0, s, j) for j in chunk]
+            ek = torch.cat([p[0] for p in pairs])
+            ev = torch.cat([p[1] for p in pairs])
+            assert torch.equal(K[i0 * b:(i0 + len(chunk)) * b], ek)
+            assert torch.equal(V[i0 * b:(i0 + len(chunk)) * b], ev)
+        del K, V
+    # a second edit path reaching the same multiset: inserts only, shuffled
+    alt = smem.Store(S, NB, S * NB, b, H, dh, BF)
+    rr = np.random.default_rng(5)
+    for s in rr.permutation(S):
+        for j in rr.permutation(sorted(live[s])):
+            smem.smem_store_put_block(alt, int(s), int(j), *synth.memory_block_device(w, 0, int(s), int(j)))
+    qlast = dev(qs[-1], BF)
+    r1 = smem.smem_reader_decode(st, list(range(S)), [NB] * S, None, qlast)
+    r2 = smem.smem_reader_decode(alt, list(range(S)), [NB] * S, None, qlast)
+    assert torch.equal(r1, r2)
+    for s in (0, 7, 15):
+        e1, e2 = smem.smem_store_export(st, s), smem.smem_store_export(alt, s)
+        assert e1[0] == e2[0] and torch.equal(e1[1], e2[1]) and torch.equal(e1[2], e2[2])
+        del e1, e2
+    alt.close()
+    del alt
+    torch.cuda.empty_cache()
+    # attention parity on sampled sequences and heads at the first and last step
+    for t, (got, lives, pos, kcs, vcs) in snap.items():
+        for i, s in enumerate(sample_seqs):
+            ref = O.Store(1, NB, b, len(hs), dh)
+            blocks = lives[i]
+            for j0 in range(0, len(blocks), 512):
+                pairs = [synth.memory_block_device(w, 0, s, j) for j in blocks[j0:j0 + 512]]
+                Kc = torch.stack([p[0] for p in pairs])[:, :, hs].float().cpu().numpy()
+                Vc = torch.stack([p[1] for p in pairs])[:, :, hs].float().cpu().numpy()
+                for n, j in enumerate(blocks[j0:j0 + 512]):
+                    ref.put(0, j, Kc[n], Vc[n])
+            r, _, _ = O.reader_decode(ref, [0], [NB], [pos[s]], _heads(qs[t, s:s + 1], hs), _heads(kn[t, s:s + 1], hs),
+                                      _heads(vn[t, s:s + 1], hs), _heads(kcs[i:i + 1], hs), _heads(vcs[i:i + 1], hs))
+            check(got[s:s + 1][:, hs], r, BF, f"stress decode step {t} seq {s} heads {hs}")
