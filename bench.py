@@ -16,7 +16,10 @@ Secondary workloads, timed in the same run and reported under "secondary":
     the store), then reader prefill of the final block of each sequence;
   * 1.5B-shaped single-block serve: 512 cached blocks (32768 rows), 16 heads
     x dh 128, batch 1: reader prefill of one fresh block over all rows, then
-    100 random single-block deletions, each followed by a re-serve.
+    100 random single-block deletions, each followed by a re-serve;
+  * 1.5B-shaped stress: 16 sequences x 4096 blocks (262144 rows each, a
+    32 GiB store): batch-16 decode over all rows, and single-block delete /
+    re-insert latency.
 
 Timing uses HIP events on the stream the kernels are launched on (torch's
 current stream, handed to the library).  The CPU baseline is the fp64 numpy
@@ -228,6 +231,55 @@ def serve_workload(args, torch, smem, synth):
                 rows_after_deletes=(NB - 100) * b)
 
 
+def stress_workload(args, torch, smem, synth):
+    """1.5B-shaped stress: 16 sequences x 4096 blocks (262144 rows, 32 GiB);
+    batch-16 decode over all rows, and single-block delete / re-insert latency."""
+    w = synth.STRESS_1P5B
+    S, H, dh, b, NB = w.n_seq, w.H, w.dh, w.b, w.n_blocks
+    dt = torch.bfloat16
+    st = smem.Store(S, NB, S * NB, b, H, dh, dt)
+    for s in range(S):
+        for j in range(NB):
+            smem.smem_store_put_block(st, s, j, *synth.memory_block_device(w, args.seed, s, j))
+    g = synth.rng(args.seed, w.wid, synth.ROLE_QDEC, 0, 0, 0)
+    mk = lambda shape: torch.from_numpy(synth.bf16_round((g.standard_normal(shape) * w.scale).astype(np.float32))).to("cuda").to(dt)
+    q, kn, vn = mk((S, H, dh)), mk((S, H, dh)), mk((S, H, dh))
+    kc, vc = mk((S * b, H, dh)), mk((S * b, H, dh))
+    out = torch.empty((S, H, dh), dtype=dt, device="cuda")
+    p0 = synth.decode_positions(w, args.seed, S)
+    stream = torch.cuda.current_stream()
+    seq_ids, qblk = list(range(S)), [NB] * S
+
+    def step(t):
+        pos = [int((p0[s] + t) % b) for s in range(S)]
+        smem.smem_reader_decode(st, seq_ids, qblk, pos, q, kn, vn, kc, vc, None, out)
+
+    for t in range(2):
+        step(t)
+    n = max(8, args.steps // 8)
+    secs = _events_time(step, n, stream) / n
+    er = synth.rng(args.seed, w.wid, synth.ROLE_EDIT, 2, 0, 0)
+    start, mid, end = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    d_t, p_t = [], []
+    for _ in range(32):
+        s, j = int(er.integers(0, S)), int(er.integers(0, NB))
+        kj, vj = synth.memory_block_device(w, args.seed, s, j)
+        torch.cuda.synchronize()
+        start.record(stream)
+        smem.smem_delete_block(st, s, j)
+        mid.record(stream)
+        smem.smem_store_put_block(st, s, j, kj, vj)
+        end.record(stream)
+        end.synchronize()
+        d_t.append(start.elapsed_time(mid))
+        p_t.append(mid.elapsed_time(end))
+    bytes_step = S * H * NB * b * dh * 2 * 2
+    st.close()
+    return dict(decode_ms=secs * 1e3, tokens_per_s=S / secs, decode_gbs=bytes_step / secs / 1e9,
+                memory_rows=NB * b, store_gib=S * NB * H * 2 * b * dh * 2 / 2 ** 30,
+                delete_us_median=float(np.median(d_t)) * 1e3, reinsert_us_median=float(np.median(p_t)) * 1e3)
+
+
 def cpu_baseline(dec, budget_s, seed):
     """The fp64 oracle on a bounded sample of the headline decode workload.
 
@@ -272,6 +324,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--workloads", default="encode,serve,stress",
+                    help="secondary workloads to run (comma list of encode, serve, stress)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -297,8 +351,13 @@ def main():
         del src, dst
     secondary = {}
     if not args.no_secondary:
-        secondary["encode_prefill_160M"] = encode_prefill_workload(args, torch, smem, synth)
-        secondary["serve_1p5B"] = serve_workload(args, torch, smem, synth)
+        wl = set(args.workloads.split(","))
+        if "encode" in wl:
+            secondary["encode_prefill_160M"] = encode_prefill_workload(args, torch, smem, synth)
+        if "serve" in wl:
+            secondary["serve_1p5B"] = serve_workload(args, torch, smem, synth)
+        if "stress" in wl:
+            secondary["stress_1p5B"] = stress_workload(args, torch, smem, synth)
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(dec, args.cpu_budget, args.seed)

@@ -64,9 +64,9 @@ template <int DH>
 __device__ __forceinline__ void page_load(PageRegs<DH>& r, const uint16_t* __restrict__ Kt,
                                           const uint16_t* __restrict__ VT, int tid) {
 #pragma unroll
-  for (int i = 0; i < PageRegs<DH>::NK; ++i) r.k[i] = *(const u32x4*)(Kt + (size_t)(tid + i * 256) * 8);
+  for (int i = 0; i < PageRegs<DH>::NK; ++i) r.k[i] = load_stream(Kt + (size_t)(tid + i * 256) * 8);
 #pragma unroll
-  for (int i = 0; i < PageRegs<DH>::NV; ++i) r.v[i] = *(const u32x4*)(VT + (size_t)(tid + i * 256) * 8);
+  for (int i = 0; i < PageRegs<DH>::NV; ++i) r.v[i] = load_stream(VT + (size_t)(tid + i * 256) * 8);
 }
 
 template <int DH>

@@ -85,9 +85,9 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
       u32x4 kraw[C::KLOADS];
       u32x4 vraw[C::VLOADS];
 #pragma unroll
-      for (int i = 0; i < C::KLOADS; ++i) kraw[i] = *(const u32x4*)(Kt + (i * C::RPL + rg) * DH + c * E);
+      for (int i = 0; i < C::KLOADS; ++i) kraw[i] = load_stream(Kt + (i * C::RPL + rg) * DH + c * E);
 #pragma unroll
-      for (int v = 0; v < C::VLOADS; ++v) vraw[v] = *(const u32x4*)(VT + (v * C::DPL + dr) * B + kc * E);
+      for (int v = 0; v < C::VLOADS; ++v) vraw[v] = load_stream(VT + (v * C::DPL + dr) * B + kc * E);
       float s[C::KLOADS];
 #pragma unroll
       for (int i = 0; i < C::KLOADS; ++i) {

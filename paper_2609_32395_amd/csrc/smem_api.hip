@@ -209,6 +209,7 @@ smem_status smem_store_put_block(smem_store* st, int32_t seq, int32_t block_idx,
     if (k_rows || v_rows) return fail(SMEM_EINVAL, "metadata-only store takes NULL rows");
   } else {
     if (!k_rows || !v_rows) return fail(SMEM_EINVAL, "k_rows and v_rows are required");
+    if (!aligned16(k_rows) || !aligned16(v_rows)) return fail(SMEM_EINVAL, "rows must be 16-byte aligned");
   }
   const size_t ti = (size_t)seq * d.max_blocks + block_idx;
   if (st->table[ti] >= 0) return fail(SMEM_EEXIST, "block %d of sequence %d is occupied", block_idx, seq);
@@ -257,6 +258,7 @@ smem_status smem_store_export(smem_store* st, int32_t seq, int32_t* live_idx, in
   const auto& d = st->d;
   if (seq < 0 || seq >= d.n_seq) return fail(SMEM_EINVAL, "seq %d out of range [0, %d)", seq, d.n_seq);
   if ((k_out == nullptr) != (v_out == nullptr)) return fail(SMEM_EINVAL, "k_out and v_out: both or neither");
+  if (!aligned16(k_out) || !aligned16(v_out)) return fail(SMEM_EINVAL, "k_out, v_out must be 16-byte aligned");
   if (k_out && st->meta_only) return fail(SMEM_EINVAL, "metadata-only store has no rows to export");
   const auto& lv = st->live[seq];
   if (n_live) *n_live = (int32_t)lv.size();

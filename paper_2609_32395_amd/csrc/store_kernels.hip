@@ -32,41 +32,57 @@ hipError_t launch_init_meta(int32_t* table, int32_t* n_live, size_t n_table, int
 }
 
 // One workgroup per sequence to rebuild: apply this launch's edits of that
-// sequence to the table, then compact the table into the live lists.
+// sequence to the table, then compact the table into the live lists.  Each
+// thread takes 16 consecutive table entries per 4096-entry chunk, so a table
+// of up to 4096 blocks is compacted in one scan (wave prefix sums by shuffle,
+// wave totals through LDS).
+constexpr int kMetaPerThread = 16;
+
 __global__ void __launch_bounds__(256) k_meta(MetaArgs a) {
   const int seq = a.r_seq[blockIdx.x];
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int32_t* trow = a.table + (size_t)seq * a.max_blocks;
   for (int e = tid; e < a.n_edits; e += 256)
     if (a.e_seq[e] == seq) trow[a.e_blk[e]] = a.e_page[e];
   __syncthreads();
 
-  __shared__ int wave_cnt[4];
-  __shared__ int base_sh;
-  if (tid == 0) base_sh = 0;
-  __syncthreads();
-  const int lane = tid & 63, wave = tid >> 6;
+  __shared__ int wave_tot[4];
   int32_t* lp = a.live_page + (size_t)seq * a.max_blocks;
   int32_t* lb = a.live_blk + (size_t)seq * a.max_blocks;
-  for (int c0 = 0; c0 < a.max_blocks; c0 += 256) {
-    const int j = c0 + tid;
-    const int32_t pg = (j < a.max_blocks) ? trow[j] : -1;
-    const bool valid = pg >= 0;
-    const unsigned long long mask = __ballot(valid);
-    const int before = __popcll(mask & ((1ull << lane) - 1ull));
-    if (lane == 0) wave_cnt[wave] = __popcll(mask);
-    __syncthreads();
-    int off = base_sh;
-    for (int w = 0; w < wave; ++w) off += wave_cnt[w];
-    if (valid) {
-      lp[off + before] = pg;
-      lb[off + before] = j;
+  int base = 0;
+  for (int c0 = 0; c0 < a.max_blocks; c0 += 256 * kMetaPerThread) {
+    const int j0 = c0 + tid * kMetaPerThread;
+    int32_t v[kMetaPerThread];
+    int cnt = 0;
+#pragma unroll
+    for (int e = 0; e < kMetaPerThread; ++e) {
+      const int j = j0 + e;
+      v[e] = (j < a.max_blocks) ? trow[j] : -1;
+      cnt += v[e] >= 0 ? 1 : 0;
     }
+    int incl = cnt;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
+    }
+    if (lane == 63) wave_tot[wave] = incl;
     __syncthreads();
-    if (tid == 0) base_sh += wave_cnt[0] + wave_cnt[1] + wave_cnt[2] + wave_cnt[3];
+    int off = base + incl - cnt;
+    for (int w = 0; w < wave; ++w) off += wave_tot[w];
+    const int total = wave_tot[0] + wave_tot[1] + wave_tot[2] + wave_tot[3];
+#pragma unroll
+    for (int e = 0; e < kMetaPerThread; ++e) {
+      if (v[e] >= 0) {
+        lp[off] = v[e];
+        lb[off] = j0 + e;
+        ++off;
+      }
+    }
+    base += total;
     __syncthreads();
   }
-  if (tid == 0) a.n_live[seq] = base_sh;
+  if (tid == 0) a.n_live[seq] = base;
 }
 
 hipError_t launch_meta(const MetaArgs& a, hipStream_t s) {
@@ -76,26 +92,38 @@ hipError_t launch_meta(const MetaArgs& a, hipStream_t s) {
 }
 
 // Insert one block's rows: src rows [b][H][dh] -> key plane [b][dh] and
-// transposed value plane [dh][b] of every head.  One workgroup per head; the
-// value tile goes through LDS so both global reads and writes are coalesced.
+// transposed value plane [dh][b] of every head.  One workgroup per head;
+// 16-byte loads and stores throughout, the value tile transposed through LDS.
 template <typename T>
 __global__ void __launch_bounds__(256) k_put_rows(T* __restrict__ pages, int page, int H, int b, int dh,
                                                    const T* __restrict__ k_rows, const T* __restrict__ v_rows) {
+  constexpr int E = 16 / sizeof(T);
   extern __shared__ unsigned char smem_raw[];
   T* tile = reinterpret_cast<T*>(smem_raw);  // [b][dh + 1]
   const int h = blockIdx.x;
   T* kp = pages + page_head_offset(page, h, H, b, dh);
   T* vp = kp + (size_t)b * dh;
-  const int n = b * dh;
-  for (int i = threadIdx.x; i < n; i += blockDim.x) {
-    const int r = i / dh, d = i % dh;
-    kp[i] = k_rows[((size_t)r * H + h) * dh + d];
-    tile[r * (dh + 1) + d] = v_rows[((size_t)r * H + h) * dh + d];
+  const int cpr = dh / E;
+  for (int i = threadIdx.x; i < b * cpr; i += blockDim.x) {
+    const int r = i / cpr, c = i % cpr;
+    const size_t src = ((size_t)r * H + h) * dh + c * E;
+    *(u32x4*)(kp + r * dh + c * E) = *(const u32x4*)(k_rows + src);
+    const u32x4 vv = *(const u32x4*)(v_rows + src);
+    T vals[E];
+    __builtin_memcpy(vals, &vv, 16);
+#pragma unroll
+    for (int e = 0; e < E; ++e) tile[r * (dh + 1) + c * E + e] = vals[e];
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < n; i += blockDim.x) {
-    const int d = i / b, r = i % b;
-    vp[i] = tile[r * (dh + 1) + d];
+  const int cpv = b / E;
+  for (int i = threadIdx.x; i < dh * cpv; i += blockDim.x) {
+    const int d = i / cpv, kc = i % cpv;
+    T vals[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) vals[e] = tile[(kc * E + e) * (dh + 1) + d];
+    u32x4 out;
+    __builtin_memcpy(&out, vals, 16);
+    *(u32x4*)(vp + d * b + kc * E) = out;
   }
 }
 

@@ -1,0 +1,102 @@
+"""CPU bounds model of the kernels' indexing.
+
+For every supported shape (b in {16, 64}, dh in {32, 64, 128}, fp32/bf16),
+this mirrors the largest element offset each kernel touches in each buffer
+(from its loop bounds and lane mappings) and checks it lies inside the buffer
+the ABI sizes for it.  It runs before any kernel change goes to a GPU: an
+access past a tensor's end is caught here, not as a memory fault."""
+import itertools
+
+import pytest
+
+SPLIT_CAP = 64
+SPLIT_STRIDE = SPLIT_CAP + 1
+SPLIT_CAP_PREFILL = 32
+MIN_PAGES_DECODE = 8
+MIN_PAGES_PREFILL = 4
+
+
+def pages_per_split(n_read, min_pages, cap=SPLIT_CAP):
+    return max(min_pages, -(-n_read // cap))
+
+
+def page_head_offset(page, h, H, b, dh):
+    return (page * H + h) * 2 * b * dh
+
+
+SHAPES = [(b, dh, es) for b in (16, 64) for dh in (32, 64, 128) for es in (4, 2)]
+
+
+@pytest.mark.parametrize("b,dh,es", SHAPES)
+def test_reader_valu_indexing(b, dh, es):
+    E = 16 // es
+    LPR = dh // E
+    RPL = 64 // LPR
+    KLOADS = b // RPL
+    LPV = b // E
+    DPL = 64 // LPV
+    VLOADS = dh // DPL
+    assert RPL * LPR == 64 and KLOADS * RPL == b and DPL * LPV == 64 and VLOADS * DPL == dh
+    for H, n_pages, n_slots, nq in [(1, 1, 1, 1), (16, 4096, 64, 1), (4, 9, 16, b), (64, 3, 128, 1)]:
+        pool = n_pages * H * 2 * b * dh
+        base = page_head_offset(n_pages - 1, H - 1, H, b, dh)
+        k_max = base + ((KLOADS - 1) * RPL + RPL - 1) * dh + (LPR - 1) * E + E - 1
+        v_max = base + b * dh + ((VLOADS - 1) * DPL + DPL - 1) * b + (LPV - 1) * E + E - 1
+        assert k_max < pool and v_max < pool
+        # query / output rows: ((qs*H + h)*dh + c*E) + E - 1
+        rows = n_slots * nq
+        assert ((rows - 1) * H + H - 1) * dh + (LPR - 1) * E + E - 1 < rows * H * dh
+        # in-block keys: ((slot*b + r)*H + h)*dh, r < b; decode cache write at pos < b
+        assert (((n_slots - 1) * b + b - 1) * H + H - 1) * dh + (LPR - 1) * E + E - 1 < n_slots * b * H * dh
+        # null row [2][H][dh]
+        assert ((1 * H + H - 1) * dh + (LPR - 1) * E + E - 1) < 2 * H * dh
+        # split partials: split index <= memory splits <= cap, rows (query rows x heads) fit the workspace
+        for n_read in (0, 1, 63, 64, 65, 4096, 65536):
+            pps = pages_per_split(n_read, MIN_PAGES_DECODE)
+            nms = -(-n_read // pps)
+            assert nms <= SPLIT_CAP
+            assert ((rows * H - 1) * SPLIT_STRIDE + nms) * (dh + 4) + dh + 1 < rows * H * SPLIT_STRIDE * (dh + 4)
+            # wave w of split k reads live entries k*pps + w + 4i < min(n_read, (k+1)*pps)
+            for k in {0, max(0, nms - 1)}:
+                p0, p1 = k * pps, min(n_read, k * pps + pps)
+                assert all(pi < n_read for pi in range(p0, p1))
+
+
+@pytest.mark.parametrize("dh", [32, 64, 128])
+def test_mfma_indexing(dh):
+    BT, KPAD = 64, 8
+    KS, VS = dh + KPAD, BT + KPAD
+    NK = BT * dh // 8 // 256
+    NV = dh * BT // 8 // 256
+    assert NK * 256 * 8 == BT * dh and NV * 256 * 8 == dh * BT
+    # page tile loads: chunk c = tid + i*256 < NK*256, 8 elements each, inside the (page, head) run
+    assert (255 + (NK - 1) * 256) * 8 + 7 < BT * dh
+    assert BT * dh + (255 + (NV - 1) * 256) * 8 + 7 < 2 * BT * dh
+    # LDS tile stores: key row = c / (dh/8) < 64, column c8*8 + 7 < dh
+    c = 255 + (NK - 1) * 256
+    assert c // (dh // 8) < BT and (c % (dh // 8)) * 8 + 7 < dh
+    c = 255 + (NV - 1) * 256
+    assert c // (BT // 8) < dh and (c % (BT // 8)) * 8 + 7 < BT
+    # LDS operand reads: key tile row kt*16 + 15 < 64, column kk*32 + 3*8 + 7 < dh
+    assert (3 * 16 + 15) < BT and (dh // 32 - 1) * 32 + 3 * 8 + 7 < dh
+    # transposed values: row dt*16 + 15 < dh, columns g*4 + {0,16,32,48} + 3 < 64
+    assert (dh // 16 - 1) * 16 + 15 < dh and 3 * 4 + 48 + 3 < BT
+    # LDS footprint (one buffer) fits the 64 KiB per-workgroup limit
+    assert (BT * KS + dh * VS) * 2 <= 64 * 1024
+    # prefill partials: split <= cap (32) inside the 65-wide stride
+    for n_read in (0, 1, 4, 5, 512, 4096, 65536):
+        pps = pages_per_split(n_read, MIN_PAGES_PREFILL, SPLIT_CAP_PREFILL)
+        assert -(-n_read // pps) <= SPLIT_CAP_PREFILL < SPLIT_STRIDE
+    # output/ws lane writes: d0 = dt*16 + g*4, 4 values
+    assert (dh // 16 - 1) * 16 + 3 * 4 + 3 < dh
+
+
+def test_prefill_workspace_fits_slot_chunk():
+    # prefill launches at most min(16, n_seq) slots of b query rows each
+    for n_seq, b, H, dh in itertools.product((1, 8, 16, 64), (16, 64), (1, 16), (32, 128)):
+        dec_rows = n_seq * H
+        pre_rows = min(n_seq, 16) * b * H
+        ws = max(dec_rows, pre_rows) * SPLIT_STRIDE * (dh + 4)
+        chunk = min(16, n_seq)
+        assert (chunk * b * H) * SPLIT_STRIDE * (dh + 4) <= ws
+        assert (min(128, n_seq) * 1 * H) * SPLIT_STRIDE * (dh + 4) <= ws
