@@ -402,7 +402,7 @@ template <int DH>
 static hipError_t launch_pre(const ReaderArgs& a, hipStream_t s) {
   int max_split = 0;
   for (int i = 0; i < a.n_slots; ++i) {
-    const int ns = mem_splits(a.n_read[i], a.pps[i]);
+    const int ns = total_splits(a.n_read[i], a.pps[i]) - 1;
     if (ns > max_split) max_split = ns;
   }
   hipLaunchKernelGGL((k_prefill_mfma<DH>), dim3(max_split + 1, a.H, a.n_slots), dim3(256), 0, s, a);

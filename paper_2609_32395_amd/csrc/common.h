@@ -18,7 +18,8 @@ constexpr int kMaxSlots = 128;
 // Edits applied by one metadata launch.
 constexpr int kMaxEdits = 128;
 // Split-K: memory pages of one (query, head) are cut into at most kSplitCap
-// splits of whole pages, plus one split for the null row and in-block keys.
+// splits of whole pages, plus possibly one split for the null row and the
+// in-block keys.
 constexpr int kSplitCap = 64;
 constexpr int kSplitStride = kSplitCap + 1;
 // Minimum pages per split and split caps (decode / VALU reader, MFMA prefill).
@@ -37,8 +38,9 @@ inline int pages_per_split(int n_read, int min_pages, int cap = kSplitCap) {
   int p = (n_read + cap - 1) / cap;
   return p < min_pages ? min_pages : p;
 }
-inline int mem_splits(int n_read, int pps) { return (n_read + pps - 1) / pps; }
-__device__ __forceinline__ int mem_splits_dev(int n_read, int pps) { return (n_read + pps - 1) / pps; }
+// Splits of one (query, head): ceil(n_read / pps) memory splits, then one
+// split for the null row and the in-block keys.
+__host__ __device__ inline int total_splits(int n_read, int pps) { return (n_read + pps - 1) / pps + 1; }
 
 enum Dtype : int32_t { F32 = 0, BF16 = 1 };
 

@@ -268,7 +268,7 @@ template <typename T, int DH>
 __global__ void __launch_bounds__(128) k_merge(ReaderArgs a) {
   const int qs = blockIdx.x, h = blockIdx.y;
   const int slot = qs / a.nq;
-  const int S = mem_splits_dev(a.n_read[slot], a.pps[slot]) + 1;
+  const int S = total_splits(a.n_read[slot], a.pps[slot]);
   if (S == 1) return;
   __shared__ float w_sh[kSplitStride];
   __shared__ float l_sh[kSplitStride];
@@ -318,7 +318,7 @@ template <typename T, int DH, int B>
 static hipError_t launch_rv(const ReaderArgs& a, hipStream_t s) {
   int max_split = 0;
   for (int i = 0; i < a.n_slots; ++i) {
-    int ns = mem_splits(a.n_read[i], a.pps[i]);
+    const int ns = total_splits(a.n_read[i], a.pps[i]) - 1;
     if (ns > max_split) max_split = ns;
   }
   dim3 grid(max_split + 1, a.H, a.n_slots * a.nq);

@@ -54,8 +54,9 @@ def test_reader_valu_indexing(b, dh, es):
         for n_read in (0, 1, 63, 64, 65, 4096, 65536):
             pps = pages_per_split(n_read, MIN_PAGES_DECODE)
             nms = -(-n_read // pps)
-            assert nms <= SPLIT_CAP
-            assert ((rows * H - 1) * SPLIT_STRIDE + nms) * (dh + 4) + dh + 1 < rows * H * SPLIT_STRIDE * (dh + 4)
+            nsplit = nms + 1   # the null row and in-block keys have their own split
+            assert nsplit <= SPLIT_STRIDE
+            assert ((rows * H - 1) * SPLIT_STRIDE + nsplit - 1) * (dh + 4) + dh + 1 < rows * H * SPLIT_STRIDE * (dh + 4)
             # wave w of split k reads live entries k*pps + w + 4i < min(n_read, (k+1)*pps)
             for k in {0, max(0, nms - 1)}:
                 p0, p1 = k * pps, min(n_read, k * pps + pps)
@@ -83,10 +84,10 @@ def test_mfma_indexing(dh):
     assert (dh // 16 - 1) * 16 + 15 < dh and 3 * 4 + 48 + 3 < BT
     # LDS footprint (one buffer) fits the 64 KiB per-workgroup limit
     assert (BT * KS + dh * VS) * 2 <= 64 * 1024
-    # prefill partials: split <= cap (32) inside the 65-wide stride
+    # prefill partials: at most 32 splits (split 0 also reads the in-block tile) inside the 65-wide stride
     for n_read in (0, 1, 4, 5, 512, 4096, 65536):
         pps = pages_per_split(n_read, MIN_PAGES_PREFILL, SPLIT_CAP_PREFILL)
-        assert -(-n_read // pps) <= SPLIT_CAP_PREFILL < SPLIT_STRIDE
+        assert max(-(-n_read // pps), 1) <= SPLIT_CAP_PREFILL <= SPLIT_STRIDE
     # output/ws lane writes: d0 = dt*16 + g*4, 4 values
     assert (dh // 16 - 1) * 16 + 3 * 4 + 3 < dh
 
