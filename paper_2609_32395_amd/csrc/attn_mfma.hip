@@ -86,17 +86,27 @@ __device__ __forceinline__ void page_store(const PageRegs<DH>& r, Tiles<DH>& T, 
 }
 
 // In-block tile from token-major tensors ([row][H][dh], row stride H*dh):
-// keys row-major, values transposed into LDS.
+// keys row-major, values transposed into LDS.  Every global load of the tile
+// is issued before the first LDS store, so a workgroup waits one load
+// latency for the whole tile.
 template <int DH>
 __device__ __forceinline__ void intra_store(Tiles<DH>& T, const uint16_t* __restrict__ kin,
                                             const uint16_t* __restrict__ vin, size_t row_stride, int tid) {
-  constexpr int NCH = BT * DH / 8;
-  for (int c = tid; c < NCH; c += 256) {
+  constexpr int NIT = BT * DH / 8 / 256;
+  u32x4 kv[NIT], vv[NIT];
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    const int c = tid + it * 256;
     const int row = c / (DH / 8), c8 = c % (DH / 8);
-    const u32x4 kv = *(const u32x4*)(kin + row * row_stride + c8 * 8);
-    const u32x4 vv = *(const u32x4*)(vin + row * row_stride + c8 * 8);
-    *(u32x4*)&T.k[row * Tiles<DH>::KS + c8 * 8] = kv;
-    const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+    kv[it] = *(const u32x4*)(kin + row * row_stride + c8 * 8);
+    vv[it] = *(const u32x4*)(vin + row * row_stride + c8 * 8);
+  }
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    const int c = tid + it * 256;
+    const int row = c / (DH / 8), c8 = c % (DH / 8);
+    *(u32x4*)&T.k[row * Tiles<DH>::KS + c8 * 8] = kv[it];
+    const uint32_t w[4] = {vv[it].x, vv[it].y, vv[it].z, vv[it].w};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       T.vt[(c8 * 8 + 2 * j) * Tiles<DH>::VS + row] = (uint16_t)(w[j] & 0xffffu);
@@ -215,13 +225,15 @@ struct EncArgs {
 template <int DH, bool CAUSAL>
 __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
   __shared__ Tiles<DH> T;
-  const int blk = blockIdx.x, h = blockIdx.y;
+  // heads fastest: neighbouring workgroups read neighbouring head slices of
+  // the same token rows
+  const int h = blockIdx.x, blk = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const size_t rs = (size_t)a.H * DH;
   const size_t base = (size_t)blk * BT * rs + (size_t)h * DH;
-  intra_store<DH>(T, a.k + base, a.v + base, rs, tid);
   bf16x8 qf[DH / 32];
   load_q<DH>(qf, a.q + base + (size_t)wave * 16 * rs, rs, lane);
+  intra_store<DH>(T, a.k + base, a.v + base, rs, tid);
   __syncthreads();
   floatx4 s[4];
   scores<DH>(s, T, qf, lane);
@@ -256,9 +268,9 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
 template <int DH>
 static hipError_t launch_enc(const EncArgs& a, int n_blocks, hipStream_t s) {
   if (a.causal)
-    hipLaunchKernelGGL((k_encoder_mfma<DH, true>), dim3(n_blocks, a.H), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_encoder_mfma<DH, true>), dim3(a.H, n_blocks), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((k_encoder_mfma<DH, false>), dim3(n_blocks, a.H), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_encoder_mfma<DH, false>), dim3(a.H, n_blocks), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -286,9 +298,10 @@ hipError_t launch_encoder_mfma(int b, int dh, const void* q, const void* k, cons
 // ------------------------------------------------------------------ reader prefill
 
 template <int DH>
-__global__ void __launch_bounds__(256) k_prefill_mfma(ReaderArgs a) {
-  __shared__ Tiles<DH> T;
-  const int split = blockIdx.x, h = blockIdx.y, slot = blockIdx.z;
+__device__ __forceinline__ void prefill_body(const ReaderArgs& a, Tiles<DH>& T) {
+  // heads fastest: neighbouring workgroups stream the adjacent head tiles of
+  // the same pages
+  const int h = blockIdx.x, split = blockIdx.y, slot = blockIdx.z;
   const int n_read = a.n_read[slot], pps = a.pps[slot];
   const int nms = (n_read + pps - 1) / pps;
   if (split > nms) return;
@@ -398,6 +411,18 @@ __global__ void __launch_bounds__(256) k_prefill_mfma(ReaderArgs a) {
   }
 }
 
+// dh <= 64 fits four workgroups per CU in registers and LDS; ask for it.
+template <int DH>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) k_prefill_mfma_occ4(ReaderArgs a) {
+  __shared__ Tiles<DH> T;
+  prefill_body<DH>(a, T);
+}
+template <int DH>
+__global__ void __launch_bounds__(256) k_prefill_mfma(ReaderArgs a) {
+  __shared__ Tiles<DH> T;
+  prefill_body<DH>(a, T);
+}
+
 template <int DH>
 static hipError_t launch_pre(const ReaderArgs& a, hipStream_t s) {
   int max_split = 0;
@@ -405,7 +430,10 @@ static hipError_t launch_pre(const ReaderArgs& a, hipStream_t s) {
     const int ns = total_splits(a.n_read[i], a.pps[i]) - 1;
     if (ns > max_split) max_split = ns;
   }
-  hipLaunchKernelGGL((k_prefill_mfma<DH>), dim3(max_split + 1, a.H, a.n_slots), dim3(256), 0, s, a);
+  if constexpr (DH <= 64)
+    hipLaunchKernelGGL((k_prefill_mfma_occ4<DH>), dim3(a.H, max_split + 1, a.n_slots), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_prefill_mfma<DH>), dim3(a.H, max_split + 1, a.n_slots), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || max_split == 0) return e;
   return launch_merge(BF16, DH, a, s);

@@ -48,7 +48,9 @@ template <typename T, int DH, int B>
 __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
   using C = RCfg<T, DH, B>;
   constexpr int E = C::E;
-  const int split = blockIdx.x, h = blockIdx.y, qs = blockIdx.z;
+  // heads fastest: neighbouring workgroups stream the adjacent head tiles of
+  // the same pages
+  const int h = blockIdx.x, split = blockIdx.y, qs = blockIdx.z;
   const int slot = qs / a.nq, t = qs % a.nq;
   const int n_read = a.n_read[slot], pps = a.pps[slot];
   const int nms = (n_read + pps - 1) / pps;
@@ -321,7 +323,7 @@ static hipError_t launch_rv(const ReaderArgs& a, hipStream_t s) {
     const int ns = total_splits(a.n_read[i], a.pps[i]) - 1;
     if (ns > max_split) max_split = ns;
   }
-  dim3 grid(max_split + 1, a.H, a.n_slots * a.nq);
+  dim3 grid(a.H, max_split + 1, a.n_slots * a.nq);
   hipLaunchKernelGGL((k_reader_valu<T, DH, B>), grid, dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || max_split == 0) return e;
