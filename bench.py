@@ -326,6 +326,8 @@ def main():
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--workloads", default="encode,serve,stress",
                     help="secondary workloads to run (comma list of encode, serve, stress)")
+    ap.add_argument("--no-headline", action="store_true",
+                    help="profiling runs only: skip the decode headline (value is then null)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -341,7 +343,7 @@ def main():
     smem.lib()
     torch.cuda.set_device(0)
 
-    dec = decode_workload(args, torch, smem, synth)
+    dec = None if args.no_headline else decode_workload(args, torch, smem, synth)
     if args.copy_probe:
         src = torch.ones(args.copy_probe * (1 << 20) // 2, dtype=torch.bfloat16, device="cuda")
         dst = torch.empty_like(src)
@@ -359,6 +361,9 @@ def main():
         if "stress" in wl:
             secondary["stress_1p5B"] = stress_workload(args, torch, smem, synth)
     cpu = None
+    if dec is None:
+        print(json.dumps({"metric": "profiling run (no headline)", "value": None, "secondary": secondary}))
+        return
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(dec, args.cpu_budget, args.seed)
     achieved = dec["gbs"]

@@ -28,12 +28,16 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef f32x4 floatx4;
 
 constexpr int BT = 64;         // block / page size handled here
-constexpr int KPAD = 8;        // LDS row padding (elements): 16 bytes per row
 
+// LDS tile strides, chosen against bank conflicts (32 four-byte banks; also
+// conflict-free with 64).  Key rows: 16-byte operand reads by 8 lanes of
+// consecutive rows -> a stride of 4 (mod 8) dwords puts each lane on its own
+// 4 banks.  Transposed value rows: 8-byte reads by 16 lanes of consecutive
+// rows -> a stride of 2 (mod 4) dwords, 136 bytes at 64 keys.
 template <int DH>
 struct Tiles {
-  static constexpr int KS = DH + KPAD;   // key tile row stride
-  static constexpr int VS = BT + KPAD;   // transposed value tile row stride
+  static constexpr int KS = DH + 8;      // key tile row stride (elements)
+  static constexpr int VS = BT + 4;      // transposed value tile row stride (elements)
   uint16_t k[BT * KS];
   uint16_t vt[DH * VS];
 };
@@ -81,36 +85,60 @@ __device__ __forceinline__ void page_store(const PageRegs<DH>& r, Tiles<DH>& T, 
   for (int i = 0; i < PageRegs<DH>::NV; ++i) {
     const int c = tid + i * 256;
     const int d = c / (BT / 8), c8 = c % (BT / 8);
-    *(u32x4*)&T.vt[d * Tiles<DH>::VS + c8 * 8] = r.v[i];
+    u32x2* dst = (u32x2*)&T.vt[d * Tiles<DH>::VS + c8 * 8];   // rows are 8-byte aligned
+    dst[0] = u32x2{r.v[i].x, r.v[i].y};
+    dst[1] = u32x2{r.v[i].z, r.v[i].w};
   }
 }
 
 // In-block tile from token-major tensors ([row][H][dh], row stride H*dh):
 // keys row-major, values transposed into LDS.  Every global load of the tile
-// is issued before the first LDS store, so a workgroup waits one load
-// latency for the whole tile.
+// is issued before the first LDS store.  The transpose packs two token rows
+// per 32-bit LDS write, consecutive lanes taking consecutive row pairs, so a
+// wave's writes to one value row are contiguous.
 template <int DH>
 __device__ __forceinline__ void intra_store(Tiles<DH>& T, const uint16_t* __restrict__ kin,
                                             const uint16_t* __restrict__ vin, size_t row_stride, int tid) {
-  constexpr int NIT = BT * DH / 8 / 256;
-  u32x4 kv[NIT], vv[NIT];
+  constexpr int CPR = DH / 8;                  // 16-byte chunks per token row
+  constexpr int NK = BT * CPR / 256;           // key chunks per thread
+  constexpr int NP = (BT / 2) * CPR;           // (row pair, chunk) jobs for the values
+  constexpr int NV = (NP + 255) / 256;
+  u32x4 kv[NK];
+  u32x4 va[NV], vb[NV];
 #pragma unroll
-  for (int it = 0; it < NIT; ++it) {
+  for (int it = 0; it < NK; ++it) {
     const int c = tid + it * 256;
-    const int row = c / (DH / 8), c8 = c % (DH / 8);
+    const int row = c / CPR, c8 = c % CPR;
     kv[it] = *(const u32x4*)(kin + row * row_stride + c8 * 8);
-    vv[it] = *(const u32x4*)(vin + row * row_stride + c8 * 8);
   }
 #pragma unroll
-  for (int it = 0; it < NIT; ++it) {
-    const int c = tid + it * 256;
-    const int row = c / (DH / 8), c8 = c % (DH / 8);
-    *(u32x4*)&T.k[row * Tiles<DH>::KS + c8 * 8] = kv[it];
-    const uint32_t w[4] = {vv[it].x, vv[it].y, vv[it].z, vv[it].w};
+  for (int it = 0; it < NV; ++it) {
+    const int j = tid + it * 256;
+    if (j < NP) {
+      const int pr = j % (BT / 2), c8 = j / (BT / 2);
+      va[it] = *(const u32x4*)(vin + (2 * pr) * row_stride + c8 * 8);
+      vb[it] = *(const u32x4*)(vin + (2 * pr + 1) * row_stride + c8 * 8);
+    }
+  }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      T.vt[(c8 * 8 + 2 * j) * Tiles<DH>::VS + row] = (uint16_t)(w[j] & 0xffffu);
-      T.vt[(c8 * 8 + 2 * j + 1) * Tiles<DH>::VS + row] = (uint16_t)(w[j] >> 16);
+  for (int it = 0; it < NK; ++it) {
+    const int c = tid + it * 256;
+    const int row = c / CPR, c8 = c % CPR;
+    *(u32x4*)&T.k[row * Tiles<DH>::KS + c8 * 8] = kv[it];
+  }
+#pragma unroll
+  for (int it = 0; it < NV; ++it) {
+    const int j = tid + it * 256;
+    if (j < NP) {
+      const int pr = j % (BT / 2), c8 = j / (BT / 2);
+      const uint32_t a4[4] = {va[it].x, va[it].y, va[it].z, va[it].w};
+      const uint32_t b4[4] = {vb[it].x, vb[it].y, vb[it].z, vb[it].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        // dims d = c8*8 + 2q (low halves) and d + 1 (high halves)
+        *(uint32_t*)&T.vt[(c8 * 8 + 2 * q) * Tiles<DH>::VS + 2 * pr] = (a4[q] & 0xffffu) | (b4[q] << 16);
+        *(uint32_t*)&T.vt[(c8 * 8 + 2 * q + 1) * Tiles<DH>::VS + 2 * pr] = (a4[q] >> 16) | (b4[q] & 0xffff0000u);
+      }
     }
   }
 }
@@ -411,12 +439,6 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, Tiles<DH>& T) 
   }
 }
 
-// dh <= 64 fits four workgroups per CU in registers and LDS; ask for it.
-template <int DH>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) k_prefill_mfma_occ4(ReaderArgs a) {
-  __shared__ Tiles<DH> T;
-  prefill_body<DH>(a, T);
-}
 template <int DH>
 __global__ void __launch_bounds__(256) k_prefill_mfma(ReaderArgs a) {
   __shared__ Tiles<DH> T;
@@ -430,10 +452,7 @@ static hipError_t launch_pre(const ReaderArgs& a, hipStream_t s) {
     const int ns = total_splits(a.n_read[i], a.pps[i]) - 1;
     if (ns > max_split) max_split = ns;
   }
-  if constexpr (DH <= 64)
-    hipLaunchKernelGGL((k_prefill_mfma_occ4<DH>), dim3(a.H, max_split + 1, a.n_slots), dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL((k_prefill_mfma<DH>), dim3(a.H, max_split + 1, a.n_slots), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((k_prefill_mfma<DH>), dim3(a.H, max_split + 1, a.n_slots), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || max_split == 0) return e;
   return launch_merge(BF16, DH, a, s);

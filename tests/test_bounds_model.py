@@ -65,8 +65,18 @@ def test_reader_valu_indexing(b, dh, es):
 
 @pytest.mark.parametrize("dh", [32, 64, 128])
 def test_mfma_indexing(dh):
-    BT, KPAD = 64, 8
-    KS, VS = dh + KPAD, BT + KPAD
+    BT = 64
+    KS, VS = dh + 8, BT + 4
+    # transposed-value rows are 8-byte aligned (u32x2 stores and reads), key rows 16-byte aligned
+    assert (VS * 2) % 8 == 0 and (KS * 2) % 16 == 0
+    # bank spread: 16 consecutive value rows (8-byte reads), 8 consecutive key rows (16-byte reads)
+    assert len({(VS * 2 // 4 * r) % 32 for r in range(16)}) == 16
+    assert len({(KS * 2 // 4 * r) % 32 for r in range(8)}) == 8
+    # in-block transpose: (row pair, chunk) jobs cover 64 rows x dh, each writes dims c8*8..+7 at rows 2p, 2p+1
+    NP = 32 * (dh // 8)
+    jobs = [((j % 32), (j // 32)) for j in range(NP)]
+    assert len(set(jobs)) == NP and max(p for p, _ in jobs) == 31 and max(c for _, c in jobs) * 8 + 7 < dh
+    assert (dh - 1) * VS + 2 * 31 + 1 < dh * VS
     NK = BT * dh // 8 // 256
     NV = dh * BT // 8 // 256
     assert NK * 256 * 8 == BT * dh and NV * 256 * 8 == dh * BT
