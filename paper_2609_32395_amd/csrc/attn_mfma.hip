@@ -92,47 +92,58 @@ __device__ __forceinline__ void page_store(const PageRegs<DH>& r, Tiles<DH>& T, 
 }
 
 // In-block tile from token-major tensors ([row][H][dh], row stride H*dh):
-// keys row-major, values transposed into LDS.  Every global load of the tile
-// is issued before the first LDS store.  The transpose packs two token rows
-// per 32-bit LDS write, consecutive lanes taking consecutive row pairs, so a
-// wave's writes to one value row are contiguous.
+// keys row-major, values transposed into LDS.  tile_load issues every global
+// load of the tile into registers; tile_store writes them to LDS.  The
+// transpose packs two token rows per 32-bit LDS write, consecutive lanes
+// taking consecutive row pairs, so a wave's writes to one value row are
+// contiguous.
 template <int DH>
-__device__ __forceinline__ void intra_store(Tiles<DH>& T, const uint16_t* __restrict__ kin,
-                                            const uint16_t* __restrict__ vin, size_t row_stride, int tid) {
-  constexpr int CPR = DH / 8;                  // 16-byte chunks per token row
-  constexpr int NK = BT * CPR / 256;           // key chunks per thread
-  constexpr int NP = (BT / 2) * CPR;           // (row pair, chunk) jobs for the values
-  constexpr int NV = (NP + 255) / 256;
-  u32x4 kv[NK];
+struct TileRegs {
+  static constexpr int CPR = DH / 8;                  // 16-byte chunks per token row
+  static constexpr int NK = BT * CPR / 256;           // key chunks per thread
+  static constexpr int NP = (BT / 2) * CPR;           // (row pair, chunk) jobs for the values
+  static constexpr int NV = (NP + 255) / 256;
+  u32x4 k[NK];
   u32x4 va[NV], vb[NV];
+};
+
+template <int DH>
+__device__ __forceinline__ void tile_load(TileRegs<DH>& r, const uint16_t* __restrict__ kin,
+                                          const uint16_t* __restrict__ vin, size_t row_stride, int tid) {
+  using R = TileRegs<DH>;
 #pragma unroll
-  for (int it = 0; it < NK; ++it) {
+  for (int it = 0; it < R::NK; ++it) {
     const int c = tid + it * 256;
-    const int row = c / CPR, c8 = c % CPR;
-    kv[it] = *(const u32x4*)(kin + row * row_stride + c8 * 8);
+    const int row = c / R::CPR, c8 = c % R::CPR;
+    r.k[it] = *(const u32x4*)(kin + row * row_stride + c8 * 8);
   }
 #pragma unroll
-  for (int it = 0; it < NV; ++it) {
+  for (int it = 0; it < R::NV; ++it) {
     const int j = tid + it * 256;
-    if (j < NP) {
+    if (j < R::NP) {
       const int pr = j % (BT / 2), c8 = j / (BT / 2);
-      va[it] = *(const u32x4*)(vin + (2 * pr) * row_stride + c8 * 8);
-      vb[it] = *(const u32x4*)(vin + (2 * pr + 1) * row_stride + c8 * 8);
+      r.va[it] = *(const u32x4*)(vin + (2 * pr) * row_stride + c8 * 8);
+      r.vb[it] = *(const u32x4*)(vin + (2 * pr + 1) * row_stride + c8 * 8);
     }
   }
+}
+
+template <int DH>
+__device__ __forceinline__ void tile_store(const TileRegs<DH>& r, Tiles<DH>& T, int tid) {
+  using R = TileRegs<DH>;
 #pragma unroll
-  for (int it = 0; it < NK; ++it) {
+  for (int it = 0; it < R::NK; ++it) {
     const int c = tid + it * 256;
-    const int row = c / CPR, c8 = c % CPR;
-    *(u32x4*)&T.k[row * Tiles<DH>::KS + c8 * 8] = kv[it];
+    const int row = c / R::CPR, c8 = c % R::CPR;
+    *(u32x4*)&T.k[row * Tiles<DH>::KS + c8 * 8] = r.k[it];
   }
 #pragma unroll
-  for (int it = 0; it < NV; ++it) {
+  for (int it = 0; it < R::NV; ++it) {
     const int j = tid + it * 256;
-    if (j < NP) {
+    if (j < R::NP) {
       const int pr = j % (BT / 2), c8 = j / (BT / 2);
-      const uint32_t a4[4] = {va[it].x, va[it].y, va[it].z, va[it].w};
-      const uint32_t b4[4] = {vb[it].x, vb[it].y, vb[it].z, vb[it].w};
+      const uint32_t a4[4] = {r.va[it].x, r.va[it].y, r.va[it].z, r.va[it].w};
+      const uint32_t b4[4] = {r.vb[it].x, r.vb[it].y, r.vb[it].z, r.vb[it].w};
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         // dims d = c8*8 + 2q (low halves) and d + 1 (high halves)
@@ -141,6 +152,14 @@ __device__ __forceinline__ void intra_store(Tiles<DH>& T, const uint16_t* __rest
       }
     }
   }
+}
+
+template <int DH>
+__device__ __forceinline__ void intra_store(Tiles<DH>& T, const uint16_t* __restrict__ kin,
+                                            const uint16_t* __restrict__ vin, size_t row_stride, int tid) {
+  TileRegs<DH> r;
+  tile_load<DH>(r, kin, vin, row_stride, tid);
+  tile_store<DH>(r, T, tid);
 }
 
 // Query fragments of one wave (B operand of S^T = K Q^T): query row
@@ -216,13 +235,13 @@ __device__ __forceinline__ void online_step(floatx4 (&s)[4], float& m, float& l,
   }
   mx = qmax(mx);
   const float mn = fmaxf(m, mx);
-  const float alpha = (m == -INFINITY) ? 0.f : exp2f(m - mn);
+  const float alpha = (m == -INFINITY) ? 0.f : exp2w(m - mn);
   float ps = 0.f;
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float p = (s[kt][i] == -INFINITY) ? 0.f : exp2f(s[kt][i] - mn);
+      const float p = (s[kt][i] == -INFINITY) ? 0.f : exp2w(s[kt][i] - mn);
       s[kt][i] = p;
       ps += p;
     }
@@ -245,16 +264,19 @@ struct EncArgs {
   uint16_t* out;        // may be NULL
   uint16_t* pages;      // may be NULL
   int32_t H;
+  int32_t n_blocks;
   int32_t causal;
   float scale_log2;
   int32_t sink[kMaxSlots];   // page of block i, or -1
 };
 
+// One workgroup per (block, head) tile, heads fastest: neighbouring
+// workgroups read neighbouring head slices of the same token rows.  Every
+// tile's loads are issued at once; with all tiles resident, tiles whose data
+// arrive first compute while the rest are still loading.
 template <int DH, bool CAUSAL>
 __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
   __shared__ Tiles<DH> T;
-  // heads fastest: neighbouring workgroups read neighbouring head slices of
-  // the same token rows
   const int h = blockIdx.x, blk = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const size_t rs = (size_t)a.H * DH;
@@ -263,15 +285,15 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
   load_q<DH>(qf, a.q + base + (size_t)wave * 16 * rs, rs, lane);
   intra_store<DH>(T, a.k + base, a.v + base, rs, tid);
   __syncthreads();
-  floatx4 s[4];
-  scores<DH>(s, T, qf, lane);
+  floatx4 s4[4];
+  scores<DH>(s4, T, qf, lane);
   floatx4 o[DH / 16];
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, l = 0.f;
   const int qrow = wave * 16 + (lane & 15);
-  online_step<DH, CAUSAL>(s, m, l, o, lane, qrow, a.scale_log2);
-  pv<DH>(o, T, s, lane);
+  online_step<DH, CAUSAL>(s4, m, l, o, lane, qrow, a.scale_log2);
+  pv<DH>(o, T, s4, lane);
   l = qsum(l);
   const float inv = 1.f / l;
   const size_t orow = (size_t)blk * BT + qrow;
@@ -280,15 +302,15 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) {
     const int d0 = dt * 16 + (lane >> 4) * 4;
-    uint16_t r[4];
+    uint16_t rr[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) r[i] = f32_to_bf16_bits(o[dt][i] * inv);
-    const u32x2 packed = u32x2{(uint32_t)r[0] | ((uint32_t)r[1] << 16), (uint32_t)r[2] | ((uint32_t)r[3] << 16)};
+    for (int i = 0; i < 4; ++i) rr[i] = f32_to_bf16_bits(o[dt][i] * inv);
+    const u32x2 packed = u32x2{(uint32_t)rr[0] | ((uint32_t)rr[1] << 16), (uint32_t)rr[2] | ((uint32_t)rr[3] << 16)};
     if (a.out) *(u32x2*)(a.out + orow * rs + (size_t)h * DH + d0) = packed;
     if (kp) {
       *(u32x2*)(kp + qrow * DH + d0) = packed;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) kp[BT * DH + (d0 + i) * BT + qrow] = r[i];
+      for (int i = 0; i < 4; ++i) kp[BT * DH + (d0 + i) * BT + qrow] = rr[i];
     }
   }
 }
@@ -314,6 +336,7 @@ hipError_t launch_encoder_mfma(int b, int dh, const void* q, const void* k, cons
   a.out = (uint16_t*)out;
   a.pages = (uint16_t*)pages;
   a.H = H;
+  a.n_blocks = n_blocks;
   a.causal = mask;
   a.scale_log2 = scale_log2;
   for (int i = 0; i < kMaxSlots; ++i) a.sink[i] = i < n_blocks ? sink_pages[i] : -1;

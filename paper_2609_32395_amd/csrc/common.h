@@ -60,13 +60,16 @@ __device__ __forceinline__ u32x4 load_stream(const void* p) {
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t x) { return __uint_as_float(x << 16); }
 
-// Round-to-nearest-even float -> bf16 bits (finite inputs; NaN kept quiet).
+// float -> bf16 bits, round to nearest even (the gfx950 conversion instruction).
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (uint16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+  const __bf16 h = (__bf16)f;
+  return __builtin_bit_cast(uint16_t, h);
 }
+
+// 2^x for softmax weights, x <= 0: the hardware exponential.  Arguments below
+// -126 come out as 0 or a denormal, a weight that is negligible next to the
+// maximum's weight of 1; 2^-inf = 0 exactly.
+__device__ __forceinline__ float exp2w(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // 16-byte chunk -> E floats (E = 4 for fp32, 8 for bf16).
 template <typename T> struct Chunk;

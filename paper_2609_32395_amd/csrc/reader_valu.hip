@@ -111,11 +111,11 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
 #pragma unroll
       for (int o = C::LPR; o < 64; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
       const float mn = fmaxf(m, mx);
-      const float alpha = exp2f(m - mn);
+      const float alpha = exp2w(m - mn);
       float ps = 0.f;
 #pragma unroll
       for (int i = 0; i < C::KLOADS; ++i) {
-        const float p = exp2f(s[i] - mn);
+        const float p = exp2w(s[i] - mn);
         if (c == 0) {
           p_sh[wave][i * C::RPL + rg] = p;
           ps += p;
@@ -209,8 +209,8 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
 #pragma unroll
       for (int o = C::LPR; o < 64; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
       const float mn = fmaxf(m, mx);       // row r0 is valid, so mn is finite
-      const float alpha = exp2f(m - mn);
-      const float p = valid ? exp2f(sc - mn) : 0.f;
+      const float alpha = exp2w(m - mn);
+      const float p = valid ? exp2w(sc - mn) : 0.f;
       l = l * alpha + ((c == 0) ? p : 0.f);
 #pragma unroll
       for (int e = 0; e < E; ++e) acc2[e] = acc2[e] * alpha + p * vf[e];
@@ -242,7 +242,7 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
     float L = 0.f, A = 0.f;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      const float wgt = (wm[w] == -INFINITY) ? 0.f : exp2f(wm[w] - M);
+      const float wgt = (wm[w] == -INFINITY) ? 0.f : exp2w(wm[w] - M);
       L += wgt * wl[w];
       A += wgt * wacc[w][tid];
     }
@@ -286,7 +286,7 @@ __global__ void __launch_bounds__(128) k_merge(ReaderArgs a) {
   if ((tid & 63) == 0) wmax[tid >> 6] = mx;
   __syncthreads();
   const float M = fmaxf(wmax[0], wmax[1]);
-  if (tid < S) w_sh[tid] = (mk == -INFINITY) ? 0.f : exp2f(mk - M);
+  if (tid < S) w_sh[tid] = (mk == -INFINITY) ? 0.f : exp2w(mk - M);
   __syncthreads();
   if (tid == 0) {
     float L = 0.f;
