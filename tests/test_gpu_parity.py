@@ -344,3 +344,45 @@ def test_tiny_workload_end_to_end():
     out2 = smem.smem_reader_prefill_block(st, [0], [8], q8, k8, v8)
     check(out2, O.reader_prefill_block(ref, [0], [8], qs[8:9], ks[8:9], vs[8:9])[0], dtype, "re-read")
     assert smem.smem_store_export(st, 0, rows=False)[0] == [0, 1, 2, 4, 5, 6, 7]
+
+
+# ------------------------------------------------------------------ launch chunking
+
+def test_large_batches_span_several_launches():
+    """More sequences, slots, blocks and edits than one launch carries: decode of
+    130 sequences (128 per launch), prefill of 20 query blocks (16 per launch),
+    encode of 130 blocks into a store (128 per launch, 128 edits per metadata
+    launch)."""
+    say("large batches")
+    dtype = torch.bfloat16
+    b, H, dh = 64, 1, 32       # bf16 blocks of 64: the MFMA encoder and prefill
+    g = np.random.default_rng(21)
+    n = 130
+    st = smem.Store(n, 3, 3 * n, b, H, dh, dtype)
+    ref = O.Store(n, 3, b, H, dh)
+    q, k, v = (rows(g, (n, b, H, dh), dtype) for _ in range(3))
+    enc = smem.smem_encode_blocks(st, dev(q.reshape(-1, H, dh), dtype), dev(k.reshape(-1, H, dh), dtype),
+                                  dev(v.reshape(-1, H, dh), dtype), seq_ids=list(range(n)), block_idx=[0] * n)
+    renc = O.encode_into_store(ref, list(range(n)), [0] * n, q, k, v)
+    check(enc, renc.reshape(-1, H, dh), dtype, "encode 130 blocks")
+    hb = host(enc).reshape(n, b, H, dh)
+    for s in (0, 64, 127, 128, 129):
+        idx, K, V = smem.smem_store_export(st, s)
+        assert idx == [0] and np.array_equal(host(K), hb[s]) and np.array_equal(host(V), hb[s])
+        ref.delete(s, 0)
+        ref.put(s, 0, hb[s], hb[s])   # the oracle reads the stored rows from here on
+    for s in range(n):
+        if s not in (0, 64, 127, 128, 129):
+            ref.delete(s, 0)
+            ref.put(s, 0, hb[s], hb[s])
+    _fill(g, st, ref, 7, [1], dtype)
+    qd = rows(g, (n, H, dh), dtype)
+    out = smem.smem_reader_decode(st, list(range(n)), [2] * n, None, dev(qd, dtype))
+    exp, _, _ = O.reader_decode(ref, list(range(n)), [2] * n, [0] * n, qd)
+    check(out, exp, dtype, "decode 130 sequences")
+    seqs = list(range(20))
+    qp = rows(g, (20, b, H, dh), dtype)
+    out = smem.smem_reader_prefill_block(st, seqs, [3] * 20, dev(qp.reshape(-1, H, dh), dtype),
+                                         dev(qp.reshape(-1, H, dh), dtype), dev(qp.reshape(-1, H, dh), dtype))
+    exp = O.reader_prefill_block(ref, seqs, [3] * 20, qp, qp, qp)
+    check(out, exp.reshape(-1, H, dh), dtype, "prefill 20 query blocks")
