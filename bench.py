@@ -17,6 +17,9 @@ Secondary workloads, timed in the same run and reported under "secondary":
   * 1.5B-shaped single-block serve: 512 cached blocks (32768 rows), 16 heads
     x dh 128, batch 1: reader prefill of one fresh block over all rows, then
     100 random single-block deletions, each followed by a re-serve;
+  * 410M-shaped streaming decode: the headline shape decoding 128 tokens
+    from a fresh block, appending each completed block (64 blocks per
+    append, encoder attention + insert) as the stream crosses a boundary;
   * 1.5B-shaped stress: 16 sequences x 4096 blocks (262144 rows each, a
     32 GiB store): batch-16 decode over all rows, and single-block delete /
     re-insert latency.
@@ -231,6 +234,60 @@ def serve_workload(args, torch, smem, synth):
                 rows_after_deletes=(NB - 100) * b)
 
 
+def stream_workload(args, torch, smem, synth):
+    """410M-shaped streaming decode: 64 sequences with 64 cached blocks each
+    decode 128 tokens from the start of a fresh block; after every 64th token
+    the completed block of every sequence is encoded and appended (64 blocks
+    per append), and the next block's tokens read it."""
+    w = synth.DEC_410M
+    S, H, dh, b, NB = w.n_seq, w.H, w.dh, w.b, w.n_blocks
+    dt = torch.bfloat16
+    T = 2 * b
+    st = smem.Store(S, NB + 2, S * (NB + 2), b, H, dh, dt)
+    for s in range(S):
+        for j in range(NB):
+            smem.smem_store_put_block(st, s, j, *synth.memory_block_device(w, args.seed, s, j))
+    g = torch.Generator(device="cuda")
+    g.manual_seed(synth.block_seed(args.seed, w.wid, synth.ROLE_QDEC, 1, 0, 0))
+    # per token: reader q, k_new, v_new and encoder q, k, v, token-major
+    X = (torch.randn((6, T, S, H, dh), generator=g, device="cuda") * w.scale).to(dt)
+    enc = [[X[r, blk * b:(blk + 1) * b].transpose(0, 1).reshape(S * b, H, dh).contiguous() for r in (3, 4, 5)]
+           for blk in range(2)]
+    kc = torch.zeros((S * b, H, dh), dtype=dt, device="cuda")
+    vc = torch.zeros_like(kc)
+    out = torch.empty((S, H, dh), dtype=dt, device="cuda")
+    seqs = list(range(S))
+    stream = torch.cuda.current_stream()
+
+    def run(_=0):
+        for t in range(T):
+            p, J = t % b, NB + t // b
+            smem.smem_reader_decode(st, seqs, [J] * S, [p] * S, X[0, t], X[1, t], X[2, t], kc, vc, None, out)
+            if p == b - 1:
+                smem.smem_encode_blocks(st, *enc[t // b], seq_ids=seqs, block_idx=[J] * S)
+
+    def undo():
+        torch.cuda.synchronize()
+        for blk in range(2):
+            for s in seqs:
+                smem.smem_delete_block(st, s, NB + blk)
+
+    run()
+    undo()
+    secs = _events_time(run, 1, stream)
+    undo()
+    reps = 5
+    app = []
+    for _ in range(reps):
+        app.append(_events_time(lambda _t: smem.smem_encode_blocks(st, *enc[0], seq_ids=seqs,
+                                                                   block_idx=[NB] * S), 1, stream))
+        for s in seqs:
+            smem.smem_delete_block(st, s, NB)
+    st.close()
+    return dict(tokens=S * T, appends=2, blocks_per_append=S, tokens_per_s=S * T / secs,
+                ms_per_step=secs / T * 1e3, append_ms_median=float(np.median(app)) * 1e3)
+
+
 def stress_workload(args, torch, smem, synth):
     """1.5B-shaped stress: 16 sequences x 4096 blocks (262144 rows, 32 GiB);
     batch-16 decode over all rows, and single-block delete / re-insert latency."""
@@ -324,8 +381,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-secondary", action="store_true")
-    ap.add_argument("--workloads", default="encode,serve,stress",
-                    help="secondary workloads to run (comma list of encode, serve, stress)")
+    ap.add_argument("--workloads", default="encode,serve,stream,stress",
+                    help="secondary workloads to run (comma list of encode, serve, stream, stress)")
     ap.add_argument("--no-headline", action="store_true",
                     help="profiling runs only: skip the decode headline (value is then null)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -358,6 +415,8 @@ def main():
             secondary["encode_prefill_160M"] = encode_prefill_workload(args, torch, smem, synth)
         if "serve" in wl:
             secondary["serve_1p5B"] = serve_workload(args, torch, smem, synth)
+        if "stream" in wl:
+            secondary["stream_410M"] = stream_workload(args, torch, smem, synth)
         if "stress" in wl:
             secondary["stress_1p5B"] = stress_workload(args, torch, smem, synth)
     cpu = None

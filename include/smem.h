@@ -125,6 +125,21 @@ smem_status smem_encode_blocks(smem_store* st, const smem_attn_desc* shape, int3
                                const void* q, const void* k, const void* v, void* out,
                                int32_t mask, hipStream_t s);
 
+/* Re-encode present blocks in place (Section 2, the slot scheme; Appendix A,
+ * "Length extension"): beyond the trained block count an append moves the
+ * most recent blocks to new slots, and each such block is encoded again from
+ * its new inputs at O(b) cost.  Arguments are those of smem_encode_blocks;
+ * st is required.  Every (seq_ids[i], block_idx[i]) must hold a block
+ * (SMEM_ENOENT otherwise, duplicates are SMEM_EINVAL), all checked before
+ * anything is enqueued.  The new rows overwrite the block's own page on
+ * stream s: the table and the live lists do not change, and the result is
+ * the store obtained by deleting the blocks and encoding them anew.  Reads
+ * enqueued earlier on s see the old rows, later ones the new rows. */
+smem_status smem_reencode_blocks(smem_store* st, const smem_attn_desc* shape, int32_t n_blocks,
+                                 const int32_t* seq_ids, const int32_t* block_idx,
+                                 const void* q, const void* k, const void* v, void* out,
+                                 int32_t mask, hipStream_t s);
+
 /* Reader attention for whole query blocks: block-skip serving (Section 3.1).
  * Row i of q/k_intra/v_intra/out, of shape [b, H, dh] each, is block
  * query_block[i] of sequence seq_ids[i].  Query t of head h reads, under

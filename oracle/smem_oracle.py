@@ -26,7 +26,11 @@ float64, with no blocking, tiling, online softmax or split reduction:
   softmax; the paper's separate self-attention and cross-attention sub-layers
   are the special cases with no memory rows or with no in-block keys.
 * Decode: the same read for one query at position p, after the new key/value
-  pair is written into the in-block cache at p.
+  pair is written into the in-block cache at p.  Streamed decode appends each
+  block to the memory once its last token is decoded.
+* Slot scheme (Section 2; Appendix A, "Length extension"): beyond B blocks
+  the most recent B blocks take slots 1..B and older ones slot 1, so an
+  append re-encodes the B-1 blocks whose slot moved.
 
 Readings of the paper used here (silent or ambiguous passages):
 * softmax scale 1/sqrt(d_h) with d_h the head dimension (the scale Lemma 1
@@ -265,6 +269,67 @@ def reader_decode(store, seq_ids, query_block, pos, q, k_new=None, v_new=None,
             K, V = _reader_keys(mem_k, mem_v, h, null_kv, kin, vin, p + 1, dh)
             out[i, h] = softmax_read(q[i, h], K, V, scale)
     return out, kc, vc
+
+
+def stream_decode(store, seq_ids, start_block, q, k_new, v_new, q_enc, k_enc, v_enc,
+                  null_kv=None, mask=MASK_BIDIR):
+    """Token-by-token decode that appends each block as it completes
+    (Section 3.1 "Decode"; Appendix K "Decode", read across block boundaries).
+
+    Every sequence starts at in-block position 0 of block start_block[i] with
+    an empty in-block cache.  Token t of sequence i sits in block
+    start_block[i] + t // b at position t % b; it is decoded by reader_decode
+    against the memory of the blocks below its own.  After the token at
+    position b-1 the block's b encoder inputs (q_enc, k_enc, v_enc rows of
+    that block) are encoded and inserted at that block's index, so the next
+    token, the first of the following block, reads it.
+
+    q, k_new, v_new: reader inputs [n, T, H, dh]; q_enc, k_enc, v_enc:
+    encoder inputs [n, T, H, dh].  Mutates ``store``.  Returns [n, T, H, dh]."""
+    q = _f64(q)
+    n, T, H, dh = q.shape
+    b = store.b
+    out = np.zeros_like(q)
+    kc = np.zeros((n, b, H, dh))
+    vc = np.zeros((n, b, H, dh))
+    for t in range(T):
+        p = t % b
+        J = [int(start_block[i]) + t // b for i in range(n)]
+        o, kc, vc = reader_decode(store, seq_ids, J, [p] * n, q[:, t], k_new[:, t], v_new[:, t],
+                                  kc, vc, null_kv)
+        out[:, t] = o
+        if p == b - 1:
+            lo = t - b + 1
+            encode_into_store(store, seq_ids, J, q_enc[:, lo:t + 1], k_enc[:, lo:t + 1],
+                              v_enc[:, lo:t + 1], mask)
+            kc[:] = 0.0
+            vc[:] = 0.0
+    return out
+
+
+def reencode_into_store(store: Store, seq_ids, block_idx, q, k, v, mask=MASK_BIDIR):
+    """Encode present blocks again from new inputs (Section 2, slot scheme;
+    Appendix A, "Length extension").  Defined as deleting every listed block
+    and encoding it anew at the same index; every block must be present
+    (ENOENT otherwise) and listed once (EINVAL), checked before any change.
+    Returns the encoder output."""
+    pairs = [(int(s), int(j)) for s, j in zip(seq_ids, block_idx)]
+    for s, j in pairs:
+        store._check(s, j)
+        if (s, j) not in store.rows:
+            raise StoreError(ENOENT, f"(seq {s}, block {j}) is absent")
+    if len(set(pairs)) != len(pairs):
+        raise StoreError(EINVAL, "duplicate target index")
+    for s, j in pairs:
+        store.delete(s, j)
+    return encode_into_store(store, [s for s, _ in pairs], [j for _, j in pairs], q, k, v, mask)
+
+
+def slot_indices(n_blocks: int, B: int):
+    """Slot of every block under the saturating slot scheme (Section 2): with
+    at most B blocks, block j (0-based) has slot j + 1; beyond that the most
+    recent B blocks have slots 1..B in order and every older block slot 1."""
+    return [max(1, j - n_blocks + B + 1) if n_blocks > B else j + 1 for j in range(n_blocks)]
 
 
 def rel_err(y, ref):

@@ -271,9 +271,9 @@ smem_status smem_store_export(smem_store* st, int32_t seq, int32_t* live_idx, in
   return SMEM_OK;
 }
 
-smem_status smem_encode_blocks(smem_store* st, const smem_attn_desc* shape, int32_t n_blocks,
+static smem_status encode_impl(smem_store* st, const smem_attn_desc* shape, int32_t n_blocks,
                                const int32_t* seq_ids, const int32_t* block_idx, const void* q, const void* k,
-                               const void* v, void* out, int32_t mask, hipStream_t s) {
+                               const void* v, void* out, int32_t mask, bool replace, hipStream_t s) {
   if (!shape) return fail(SMEM_EINVAL, "shape is NULL");
   const int b = shape->b, H = shape->H, dh = shape->dh, dtype = shape->dtype;
   if (!shape_ok(b, H, dh, dtype)) return fail(SMEM_EINVAL, "unsupported shape b=%d H=%d dh=%d dtype=%d", b, H, dh, dtype);
@@ -298,14 +298,25 @@ smem_status smem_encode_blocks(smem_store* st, const smem_attn_desc* shape, int3
       const int32_t sq = seq_ids[i], j = block_idx[i];
       if (sq < 0 || sq >= st->d.n_seq) return fail(SMEM_EINVAL, "seq_ids[%d] = %d out of range", i, sq);
       if (j < 0 || j >= st->d.max_blocks) return fail(SMEM_EINVAL, "block_idx[%d] = %d out of range", i, j);
-      if (st->table[(size_t)sq * st->d.max_blocks + j] >= 0)
-        return fail(SMEM_EEXIST, "block %d of sequence %d is occupied", j, sq);
-      if (!seen.insert({sq, j}).second) return fail(SMEM_EEXIST, "block %d of sequence %d given twice", j, sq);
+      const int32_t page = st->table[(size_t)sq * st->d.max_blocks + j];
+      if (replace) {
+        if (page < 0) return fail(SMEM_ENOENT, "block %d of sequence %d is absent", j, sq);
+        if (!seen.insert({sq, j}).second) return fail(SMEM_EINVAL, "block %d of sequence %d given twice", j, sq);
+      } else {
+        if (page >= 0) return fail(SMEM_EEXIST, "block %d of sequence %d is occupied", j, sq);
+        if (!seen.insert({sq, j}).second) return fail(SMEM_EEXIST, "block %d of sequence %d given twice", j, sq);
+      }
     }
-    if ((size_t)n_blocks > st->free_pages.size())
-      return fail(SMEM_ENOMEM, "%d blocks to insert, %zu free pages", n_blocks, st->free_pages.size());
     pages.resize(n_blocks);
-    for (int i = 0; i < n_blocks; ++i) pages[i] = st->free_pages[st->free_pages.size() - 1 - i];
+    if (replace) {
+      for (int i = 0; i < n_blocks; ++i) pages[i] = st->table[(size_t)seq_ids[i] * st->d.max_blocks + block_idx[i]];
+    } else {
+      if ((size_t)n_blocks > st->free_pages.size())
+        return fail(SMEM_ENOMEM, "%d blocks to insert, %zu free pages", n_blocks, st->free_pages.size());
+      for (int i = 0; i < n_blocks; ++i) pages[i] = st->free_pages[st->free_pages.size() - 1 - i];
+    }
+  } else if (replace) {
+    return fail(SMEM_EINVAL, "re-encoding needs a store");
   }
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)dh));
   const size_t es = esize(dtype);
@@ -337,7 +348,7 @@ smem_status smem_encode_blocks(smem_store* st, const smem_attn_desc* shape, int3
     }
     if (e != hipSuccess) return hip_fail(e, "encoder launch");
   }
-  if (st) {
+  if (st && !replace) {
     std::vector<int32_t> es_, eb_, ep_;
     for (int i = 0; i < n_blocks; ++i) {
       es_.push_back(seq_ids[i]);
@@ -354,6 +365,19 @@ smem_status smem_encode_blocks(smem_store* st, const smem_attn_desc* shape, int3
     }
   }
   return SMEM_OK;
+}
+
+smem_status smem_encode_blocks(smem_store* st, const smem_attn_desc* shape, int32_t n_blocks,
+                               const int32_t* seq_ids, const int32_t* block_idx, const void* q, const void* k,
+                               const void* v, void* out, int32_t mask, hipStream_t s) {
+  return encode_impl(st, shape, n_blocks, seq_ids, block_idx, q, k, v, out, mask, false, s);
+}
+
+smem_status smem_reencode_blocks(smem_store* st, const smem_attn_desc* shape, int32_t n_blocks,
+                                 const int32_t* seq_ids, const int32_t* block_idx, const void* q, const void* k,
+                                 const void* v, void* out, int32_t mask, hipStream_t s) {
+  if (!st) return fail(SMEM_EINVAL, "store is NULL");
+  return encode_impl(st, shape, n_blocks, seq_ids, block_idx, q, k, v, out, mask, true, s);
 }
 
 smem_status smem_reader_prefill_block(smem_store* st, int32_t n_seq, const int32_t* seq_ids,

@@ -6,9 +6,10 @@ stream.  The binding checks tensor shapes, dtypes, devices and contiguity
 before each call, because the C ABI takes bare device pointers and cannot
 check buffer sizes itself.
 
-Functions carry the C names: smem_encode_blocks, smem_reader_prefill_block,
-smem_reader_decode, smem_delete_block, smem_store_put_block,
-smem_store_export; a store is created and destroyed by the Store class.
+Functions carry the C names: smem_encode_blocks, smem_reencode_blocks,
+smem_reader_prefill_block, smem_reader_decode, smem_delete_block,
+smem_store_put_block, smem_store_export; a store is created and destroyed by
+the Store class.
 """
 from __future__ import annotations
 
@@ -58,6 +59,7 @@ SIGNATURES = {
     "smem_store_destroy": (_I, [_P]),
     "smem_store_put_block": (_I, [_P, _I, _I, _P, _P, _P]),
     "smem_encode_blocks": (_I, [_P, ctypes.POINTER(AttnDesc), _I, _IP, _IP, _P, _P, _P, _P, _I, _P]),
+    "smem_reencode_blocks": (_I, [_P, ctypes.POINTER(AttnDesc), _I, _IP, _IP, _P, _P, _P, _P, _I, _P]),
     "smem_reader_prefill_block": (_I, [_P, _I, _IP, _IP, _P, _P, _P, _P, _P, _P]),
     "smem_reader_decode": (_I, [_P, _I, _IP, _IP, _IP, _P, _P, _P, _P, _P, _P, _P, _P]),
     "smem_delete_block": (_I, [_P, _I, _I, _I, _P]),
@@ -221,6 +223,18 @@ def smem_encode_blocks(st, q, k, v, out=None, seq_ids=None, block_idx=None, mask
 
     With a store, block i's output becomes memory block block_idx[i] of
     sequence seq_ids[i].  Returns out (allocated when not given)."""
+    return _encode(lib().smem_encode_blocks, st, q, k, v, out, seq_ids, block_idx, mask, b, stream)
+
+
+def smem_reencode_blocks(st, q, k, v, out=None, seq_ids=None, block_idx=None, mask=MASK_BIDIR, stream=None):
+    """Encode present blocks again from new inputs, overwriting their rows in
+    place (the slot scheme's re-encode).  Returns out."""
+    if st is None:
+        raise ValueError("re-encoding needs a store")
+    return _encode(lib().smem_reencode_blocks, st, q, k, v, out, seq_ids, block_idx, mask, None, stream)
+
+
+def _encode(fn, st, q, k, v, out, seq_ids, block_idx, mask, b, stream):
     if st is not None:
         b = st.b
     if b is None:
@@ -243,7 +257,7 @@ def smem_encode_blocks(st, q, k, v, out=None, seq_ids=None, block_idx=None, mask
     else:
         sa = ba = None
         h = None
-    _check(lib().smem_encode_blocks(h, ctypes.byref(desc), nb, sa, ba, *ptrs, int(mask), _stream(stream)))
+    _check(fn(h, ctypes.byref(desc), nb, sa, ba, *ptrs, int(mask), _stream(stream)))
     return out
 
 

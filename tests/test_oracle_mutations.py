@@ -108,3 +108,33 @@ def test_value_plane_swap_is_caught(monkeypatch):
         return v, k                                    # planted: K and V planes swapped
     monkeypatch.setattr(O, "_memory_below", swapped)
     assert _fails(P.check_golden)
+
+
+def test_append_before_last_token_is_caught(monkeypatch):
+    def stream_early(store, seq_ids, start_block, q, k_new, v_new, q_enc, k_enc, v_enc, null_kv=None,
+                     mask=O.MASK_BIDIR):
+        q = np.asarray(q, np.float64)
+        n, T, H, dh = q.shape
+        b = store.b
+        out = np.zeros_like(q)
+        kc = np.zeros((n, b, H, dh))
+        vc = np.zeros((n, b, H, dh))
+        for t in range(T):
+            p = t % b
+            J = [int(start_block[i]) + t // b for i in range(n)]
+            if p == b - 1:                               # planted: append before the last token's read
+                lo = t - b + 1
+                O.encode_into_store(store, seq_ids, J, q_enc[:, lo:t + 1], k_enc[:, lo:t + 1],
+                                    v_enc[:, lo:t + 1], mask)
+            o, kc, vc = O.reader_decode(store, seq_ids, [j + (p == b - 1) for j in J], [p] * n, q[:, t],
+                                        k_new[:, t], v_new[:, t], kc, vc, null_kv)
+            out[:, t] = o
+        return out
+    monkeypatch.setattr(O, "stream_decode", stream_early)
+    assert _fails(P.test_stream_decode_equals_prefill_of_each_block)
+
+
+def test_slot_off_by_one_is_caught(monkeypatch):
+    monkeypatch.setattr(O, "slot_indices",
+                        lambda n, B: [max(1, j - n + B) if n > B else j + 1 for j in range(n)])
+    assert _fails(P.test_slot_scheme)

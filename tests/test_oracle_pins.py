@@ -409,3 +409,110 @@ def test_synth_bf16_rounding_and_keys():
     K, V = synth.memory_blocks(w2, 0, [0, 1], [5, 6], threads=2)
     k1, v1 = synth.memory_block(w2, 0, 1, 6)
     assert np.array_equal(K[1, 1], k1) and np.array_equal(V[1, 1], v1)
+
+
+# ---------------------------------------------------------------- streaming append, re-encode, slots
+
+def _stream_case(seed=31, b=4, H=2, dh=8, T=10):
+    g = np.random.default_rng(seed)
+    st = O.Store(2, 12, b, H, dh)
+    for s, blocks in ((0, (0, 1, 2)), (1, (0, 3, 4))):
+        for j in blocks:
+            st.put(s, j, g.standard_normal((b, H, dh)), g.standard_normal((b, H, dh)))
+    start = [3, 5]
+    dec = [g.standard_normal((2, T, H, dh)) for _ in range(3)]
+    enc = [g.standard_normal((2, T, H, dh)) for _ in range(3)]
+    nkv = g.standard_normal((2, H, dh))
+    return st, start, dec, enc, nkv
+
+
+def test_stream_decode_equals_prefill_of_each_block():
+    """Decode across block boundaries (Appendix K) reads, for every token,
+    exactly what the block-skip reader reads for that token's block: the
+    memory of the blocks below it (streamed blocks included) and the block's
+    own tokens up to the token.  A block appended before its last token is
+    decoded, or at the wrong index, changes some row."""
+    st, start, (q, kn, vn), (qe, ke, ve), nkv = _stream_case()
+    b, T = st.b, q.shape[1]
+    run = st.copy()
+    out = O.stream_decode(run, [0, 1], start, q, kn, vn, qe, ke, ve, nkv)
+    for blk in range(-(-T // b)):
+        lo, hi = blk * b, min(T, blk * b + b)
+        J = [start[0] + blk, start[1] + blk]
+        pad = lambda x: np.concatenate([x[:, lo:hi], np.zeros((2, b - (hi - lo)) + x.shape[2:])], 1)
+        pre = O.reader_prefill_block(run, [0, 1], J, pad(q), pad(kn), pad(vn), nkv)
+        np.testing.assert_allclose(out[:, lo:hi], pre[:, :hi - lo], atol=1e-13, rtol=0)
+    # the two complete blocks went in at start, start+1; the partial third did not
+    assert run.live(0) == [0, 1, 2, 3, 4] and run.live(1) == [0, 3, 4, 5, 6]
+
+
+def test_stream_appended_rows_equal_joint_encode():
+    """Proposition 1: the blocks appended one by one during decode equal the
+    joint encode of the same blocks (block-diagonal mask), bitwise."""
+    st, start, (q, kn, vn), (qe, ke, ve), nkv = _stream_case()
+    b = st.b
+    run = st.copy()
+    O.stream_decode(run, [0, 1], start, q, kn, vn, qe, ke, ve, nkv)
+    for s in (0, 1):
+        for blk in range(2):
+            lo = blk * b
+            # joint encode of both complete blocks of this sequence at once
+            both = O.encode_blocks(qe[s, :2 * b].reshape(2, b, *qe.shape[2:]),
+                                   ke[s, :2 * b].reshape(2, b, *ke.shape[2:]),
+                                   ve[s, :2 * b].reshape(2, b, *ve.shape[2:]))
+            K, V = run.rows[(s, start[s] + blk)]
+            assert np.array_equal(K, both[blk]) and np.array_equal(V, both[blk])
+            mask = np.kron(np.eye(2, dtype=bool), np.ones((b, b), bool))
+            qq, kk, vv = (torch.from_numpy(x[s, :2 * b].transpose(1, 0, 2).copy()) for x in (qe, ke, ve))
+            ref = F.scaled_dot_product_attention(qq, kk, vv, attn_mask=torch.from_numpy(mask)).numpy()
+            np.testing.assert_allclose(K, ref.transpose(1, 0, 2)[lo:lo + b], atol=1e-12, rtol=0)
+
+
+def test_reencode_matches_fresh_insert_and_errors_change_nothing():
+    """Re-encoding present blocks equals a store where those blocks were
+    encoded from the new inputs in the first place (Theorem 1: a delete is
+    exact, so the old rows leave no trace); re-encoding with the original
+    inputs is the identity; an absent or repeated block changes nothing."""
+    g = np.random.default_rng(44)
+    b, H, dh = 4, 2, 8
+    x1 = [g.standard_normal((3, b, H, dh)) for _ in range(3)]
+    x2 = [g.standard_normal((2, b, H, dh)) for _ in range(3)]
+    st = O.Store(1, 6, b, H, dh)
+    O.encode_into_store(st, [0, 0, 0], [1, 2, 4], *x1)
+    same = st.copy()
+    O.reencode_into_store(same, [0, 0, 0], [1, 2, 4], *x1)
+    for j in (1, 2, 4):
+        assert all(np.array_equal(a, c) for a, c in zip(same.rows[(0, j)], st.rows[(0, j)]))
+    O.reencode_into_store(st, [0, 0], [4, 1], *x2)
+    fresh = O.Store(1, 6, b, H, dh)
+    O.encode_into_store(fresh, [0], [2], x1[0][1:2], x1[1][1:2], x1[2][1:2])
+    O.encode_into_store(fresh, [0, 0], [4, 1], *x2)
+    assert st.live(0) == fresh.live(0) == [1, 2, 4]
+    for a, c in zip(st.export(0), fresh.export(0)):
+        assert np.array_equal(a, c)
+    q = g.standard_normal((1, b, H, dh))
+    assert np.array_equal(O.reader_prefill_block(st, [0], [5], q, q, q),
+                          O.reader_prefill_block(fresh, [0], [5], q, q, q))
+    before = st.copy()
+    for seqs, idx, code in (([0, 0], [1, 3], O.ENOENT), ([0, 0], [2, 2], O.EINVAL)):
+        with pytest.raises(O.StoreError) as e:
+            O.reencode_into_store(st, seqs, idx, *x2)
+        assert e.value.code == code
+        assert st.live(0) == before.live(0)
+        for a, c in zip(st.export(0), before.export(0)):
+            assert np.array_equal(a, c)
+
+
+def test_slot_scheme():
+    """Section 2 / Appendix A: up to B blocks every block keeps its own slot;
+    beyond, the newest B blocks hold slots 1..B and older blocks share slot 1,
+    so each append past B moves exactly the B-1 most recent earlier blocks."""
+    B = 4
+    assert O.slot_indices(3, B) == [1, 2, 3]
+    assert O.slot_indices(4, B) == [1, 2, 3, 4]
+    assert O.slot_indices(6, B) == [1, 1, 1, 2, 3, 4]
+    for n in range(1, 12):
+        sl = O.slot_indices(n, B)
+        assert len(sl) == n and sl[-1] == min(n, B) and min(sl) == 1 and max(sl) == min(n, B)
+        moved = [j for j, (a, c) in enumerate(zip(sl, O.slot_indices(n + 1, B))) if a != c]
+        assert moved == (list(range(n - B + 1, n)) if n >= B else [])
