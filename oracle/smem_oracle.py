@@ -28,6 +28,12 @@ float64, with no blocking, tiling, online softmax or split reduction:
 * Decode: the same read for one query at position p, after the new key/value
   pair is written into the in-block cache at p.  Streamed decode appends each
   block to the memory once its last token is decoded.
+* SMem+RoPE composite (Section 3; the composite's appendix, variant v2):
+  rotary phases on queries and keys only -- in-block offsets inside the
+  block, block indices (0 for the null row) across blocks, key phases
+  optionally clipped to max(j, i - W).  Readings: adjacent dimensions form a
+  rotary pair; under the joint softmax the query takes phase t against its
+  in-block keys and phase i against the null row and memory rows.
 * Slot scheme (Section 2; Appendix A, "Length extension"): beyond B blocks
   the most recent B blocks take slots 1..B and older ones slot 1, so an
   append re-encodes the B-1 blocks whose slot moved.
@@ -330,6 +336,133 @@ def slot_indices(n_blocks: int, B: int):
     at most B blocks, block j (0-based) has slot j + 1; beyond that the most
     recent B blocks have slots 1..B in order and every older block slot 1."""
     return [max(1, j - n_blocks + B + 1) if n_blocks > B else j + 1 for j in range(n_blocks)]
+
+
+# ---------------------------------------------------------------- SMem+RoPE composite
+# Section 3 ("SMem composes with RoPE") and the appendix on the composite
+# (variant v2): no position enters the rows; rotary phases are applied to
+# queries and keys, never to values.  Self-attention inside a block uses the
+# in-block offsets of query and key; cross-attention uses block indices: the
+# query's block i, the memory row's block j, index 0 for the null row.  The
+# saturating reading (the needle appendix) clips every key phase to
+# max(j, i - W) with W = B - 1, the query phase staying i.
+
+
+class Rope:
+    """Rotary configuration: frequency base and the saturation window W
+    (None: block phases are used as they are)."""
+
+    def __init__(self, base: float = 10000.0, max_offset=None):
+        self.base = float(base)
+        self.max_offset = max_offset
+
+    def key_phase(self, j, i):
+        """Cross-attention phase of a key of block j (0 for the null row) read
+        from query block i."""
+        return j if self.max_offset is None else max(j, i - self.max_offset)
+
+
+def rope_rotate(x, phase, base):
+    """Rotate the last axis of x by the rotary phase(s): dimensions (2k, 2k+1)
+    form pair k, turned by the angle phase * base^(-2k/d_h) (the rotary
+    embedding's frequencies; pairs are adjacent dimensions).  ``phase`` is a
+    scalar or broadcasts against x[..., 0]."""
+    x = _f64(x)
+    dh = x.shape[-1]
+    theta = base ** (-2.0 * np.arange(dh // 2) / dh)
+    ang = np.asarray(phase, np.float64)[..., None] * theta
+    c, s = np.cos(ang), np.sin(ang)
+    x0, x1 = x[..., 0::2], x[..., 1::2]
+    out = np.empty_like(x)
+    out[..., 0::2] = x0 * c - x1 * s
+    out[..., 1::2] = x0 * s + x1 * c
+    return out
+
+
+def encode_blocks_rope(q, k, v, rope: Rope, mask=MASK_BIDIR):
+    """Encoder attention of the composite: queries and keys of token t carry
+    rotary phase t (its in-block offset); values are not rotated."""
+    q, k = _f64(q), _f64(k)
+    t = np.arange(q.shape[1])[None, :, None]
+    return encode_blocks(rope_rotate(q, t, rope.base), rope_rotate(k, t, rope.base), v, mask)
+
+
+def _softmax_scores(s, values):
+    """Two-pass softmax of scores s [n] and the weighted sum of values [n, dh]."""
+    if s.shape[0] == 0:
+        return np.zeros(values.shape[1], np.float64)
+    e = np.exp(s - np.max(s))
+    return (e / np.sum(e)) @ values
+
+
+def _rope_read(store, seq, i, t, q, h, null_kv, k_in, v_in, n_in, rope: Rope, scale):
+    """One query of the composite's reader: query q [dh] at in-block offset t
+    of block i, head h.  Keys in canonical order, each scored against the
+    query rotated for its key set: the null row and the memory rows with the
+    query at phase i and the key at rope.key_phase(block, i); the in-block
+    keys 0..n_in-1 with the query at phase t and key t' at phase t'."""
+    base = rope.base
+    qs, ks, vs = [], [], []
+    if null_kv is not None:
+        nkv = _f64(null_kv)
+        qs.append(rope_rotate(q, i, base)[None])
+        ks.append(rope_rotate(nkv[0, h], rope.key_phase(0, i), base)[None])
+        vs.append(nkv[1, h][None])
+    if store is not None and i > 0:
+        idx, Km, Vm = store.export(seq, below=i)
+        if idx:
+            blk = np.repeat(np.array(idx), store.b)
+            phases = np.array([rope.key_phase(int(j), i) for j in blk], np.float64)
+            ks.append(rope_rotate(_f64(Km)[:, h], phases, base))
+            vs.append(_f64(Vm)[:, h])
+            qs.append(np.repeat(rope_rotate(q, i, base)[None], len(blk), 0))
+    if k_in is not None and n_in > 0:
+        ks.append(rope_rotate(_f64(k_in)[:n_in, h], np.arange(n_in), base))
+        vs.append(_f64(v_in)[:n_in, h])
+        qs.append(np.repeat(rope_rotate(q, t, base)[None], n_in, 0))
+    if not ks:
+        return np.zeros(q.shape[-1])
+    Q, K, V = np.concatenate(qs), np.concatenate(ks), np.concatenate(vs)
+    return _softmax_scores(np.sum(Q * K, axis=1) * scale, V)
+
+
+def reader_prefill_block_rope(store, seq_ids, query_block, q, k_intra, v_intra, null_kv, rope: Rope):
+    """reader_prefill_block for the composite (phases as in _rope_read)."""
+    q = _f64(q)
+    n, b, H, dh = q.shape
+    scale = 1.0 / math.sqrt(dh)
+    out = np.zeros_like(q)
+    for r in range(n):
+        s, J = int(seq_ids[r]), int(query_block[r])
+        kin = None if k_intra is None else _f64(k_intra[r])
+        vin = None if v_intra is None else _f64(v_intra[r])
+        for h in range(H):
+            for t in range(b):
+                out[r, t, h] = _rope_read(store, s, J, t, q[r, t, h], h, null_kv, kin, vin, t + 1, rope, scale)
+    return out
+
+
+def reader_decode_rope(store, seq_ids, query_block, pos, q, k_new, v_new, k_cache, v_cache, null_kv,
+                       rope: Rope):
+    """reader_decode for the composite: the new pair is written unrotated at
+    pos, then the query at offset pos reads as in _rope_read.  Returns
+    (out, updated k_cache, updated v_cache)."""
+    q = _f64(q)
+    n, H, dh = q.shape
+    scale = 1.0 / math.sqrt(dh)
+    out = np.zeros_like(q)
+    kc = None if k_cache is None else np.array(k_cache, copy=True)
+    vc = None if v_cache is None else np.array(v_cache, copy=True)
+    for r in range(n):
+        s, J, p = int(seq_ids[r]), int(query_block[r]), int(pos[r])
+        if kc is not None:
+            kc[r, p] = k_new[r]
+            vc[r, p] = v_new[r]
+        kin = None if kc is None else kc[r]
+        vin = None if vc is None else vc[r]
+        for h in range(H):
+            out[r, h] = _rope_read(store, s, J, p, q[r, h], h, null_kv, kin, vin, p + 1, rope, scale)
+    return out, kc, vc
 
 
 def rel_err(y, ref):

@@ -138,3 +138,46 @@ def test_slot_off_by_one_is_caught(monkeypatch):
     monkeypatch.setattr(O, "slot_indices",
                         lambda n, B: [max(1, j - n + B) if n > B else j + 1 for j in range(n)])
     assert _fails(P.test_slot_scheme)
+
+
+def test_rope_reversed_rotation_is_caught(monkeypatch):
+    orig = O.rope_rotate
+    monkeypatch.setattr(O, "rope_rotate", lambda x, phase, base: orig(x, -np.asarray(phase, np.float64), base))
+    assert _fails(P.test_rope_rotation_closed_forms)
+    assert _fails(P.test_rope_reader_matches_complex_sdpa, None, True)
+
+
+def test_rope_half_split_pairs_are_caught(monkeypatch):
+    orig = O.rope_rotate
+
+    def half_split(x, phase, base):        # planted: pairs (k, k + d/2) instead of (2k, 2k+1)
+        x = np.asarray(x, np.float64)
+        dh = x.shape[-1]
+        perm = np.stack([np.arange(dh // 2), np.arange(dh // 2) + dh // 2], 1).reshape(-1)
+        inv = np.argsort(perm)
+        return orig(x[..., perm], phase, base)[..., inv]
+    monkeypatch.setattr(O, "rope_rotate", half_split)
+    assert _fails(P.test_rope_rotation_closed_forms)
+    assert _fails(P.test_rope_encoder_matches_complex_sdpa, O.MASK_BIDIR)
+
+
+def test_rope_clip_off_by_one_is_caught(monkeypatch):
+    monkeypatch.setattr(O.Rope, "key_phase",
+                        lambda self, j, i: j if self.max_offset is None else max(j, i - self.max_offset - 1))
+    assert _fails(P.test_rope_reader_matches_complex_sdpa, 3, True)
+
+
+def test_rope_unrotated_null_row_is_caught(monkeypatch):
+    # planted: the null row read at the query's own phase (no turn) instead of index 0
+    monkeypatch.setattr(O, "_rope_read", _rope_read_null_at_query_phase(O._rope_read))
+    assert _fails(P.test_rope_reader_matches_complex_sdpa, None, True)
+
+
+def _rope_read_null_at_query_phase(orig):
+    def read(store, seq, i, t, q, h, null_kv, k_in, v_in, n_in, rope, scale):
+        if null_kv is None:
+            return orig(store, seq, i, t, q, h, null_kv, k_in, v_in, n_in, rope, scale)
+        nkv = np.array(null_kv, np.float64, copy=True)
+        nkv[0, h] = O.rope_rotate(nkv[0, h], i - rope.key_phase(0, i), rope.base)
+        return orig(store, seq, i, t, q, h, nkv, k_in, v_in, n_in, rope, scale)
+    return read

@@ -516,3 +516,153 @@ def test_slot_scheme():
         assert len(sl) == n and sl[-1] == min(n, B) and min(sl) == 1 and max(sl) == min(n, B)
         moved = [j for j, (a, c) in enumerate(zip(sl, O.slot_indices(n + 1, B))) if a != c]
         assert moved == (list(range(n - B + 1, n)) if n >= B else [])
+
+
+# ---------------------------------------------------------------- SMem+RoPE composite
+
+def test_rope_rotation_closed_forms():
+    """Rotary pairs are adjacent dimensions turned by phase * base^(-2k/d_h):
+    textbook values cos 1, sin 1 and exact identities of plane rotations."""
+    c1, s1 = 0.5403023058681398, 0.8414709848078965          # cos(1), sin(1)
+    np.testing.assert_allclose(O.rope_rotate([1.0, 0.0], 1.0, 1e4), [c1, s1], atol=1e-15)
+    np.testing.assert_allclose(O.rope_rotate([0.0, 1.0], 1.0, 1e4), [-s1, c1], atol=1e-15)
+    # d_h = 4, base 100: pair 1 turns at 100^(-1/2) = 0.1 rad per unit of phase
+    np.testing.assert_allclose(O.rope_rotate([0.0, 0.0, 1.0, 0.0], 10.0, 100.0), [0, 0, c1, s1], atol=1e-14)
+    np.testing.assert_allclose(O.rope_rotate([1.0, 0.0, 0.0, 0.0], 1.0, 100.0), [c1, s1, 0, 0], atol=1e-15)
+    g = np.random.default_rng(5)
+    x, y = g.standard_normal((2, 7, 64))
+    a, b_, c = 13.0, 5.0, 1000.0
+    R = lambda z, ph: O.rope_rotate(z, ph, 1e4)
+    np.testing.assert_allclose(np.linalg.norm(R(x, a), axis=1), np.linalg.norm(x, axis=1), rtol=1e-14)
+    np.testing.assert_allclose(R(R(x, a), b_), R(x, a + b_), atol=1e-12)
+    np.testing.assert_allclose(R(R(x, a), -a), x, atol=1e-13)
+    # scores depend on the phase difference only
+    np.testing.assert_allclose(np.sum(R(x, a) * R(y, b_), 1), np.sum(R(x, a + c) * R(y, b_ + c), 1), atol=1e-11)
+
+
+def _complex_rotate(x, phase, base):
+    """Independent rotary map: adjacent pairs as complex numbers times e^{i angle}."""
+    x = torch.as_tensor(np.asarray(x, np.float64))
+    dh = x.shape[-1]
+    z = torch.view_as_complex(x.reshape(*x.shape[:-1], dh // 2, 2).contiguous())
+    theta = torch.tensor(base ** (-2.0 * np.arange(dh // 2) / dh))
+    ang = torch.as_tensor(np.asarray(phase, np.float64))[..., None] * theta
+    return torch.view_as_real(z * torch.polar(torch.ones_like(ang), ang)).reshape(x.shape)
+
+
+@pytest.mark.parametrize("mask", [O.MASK_BIDIR, O.MASK_CAUSAL])
+def test_rope_encoder_matches_complex_sdpa(mask):
+    g = np.random.default_rng(23)
+    nb, b, H, dh = 3, 8, 2, 16
+    q, k, v = (g.standard_normal((nb, b, H, dh)) for _ in range(3))
+    rope = O.Rope(base=1e4)
+    out = O.encode_blocks_rope(q, k, v, rope, mask)
+    t = np.arange(b)[None, :, None]
+    qr, kr = _complex_rotate(q, t, 1e4), _complex_rotate(k, t, 1e4)
+    ref = F.scaled_dot_product_attention(qr.permute(0, 2, 1, 3), kr.permute(0, 2, 1, 3),
+                                         torch.as_tensor(v).permute(0, 2, 1, 3),
+                                         is_causal=mask == O.MASK_CAUSAL).permute(0, 2, 1, 3).numpy()
+    np.testing.assert_allclose(out, ref, atol=1e-12, rtol=0)
+
+
+@pytest.mark.parametrize("max_offset", [None, 3])
+@pytest.mark.parametrize("with_null", [False, True])
+def test_rope_reader_matches_complex_sdpa(max_offset, with_null):
+    """The composite's reader against SDPA over concatenated keys, with the
+    rotary phases applied as relative turns of the keys by complex products:
+    memory and null keys by (key phase - i), in-block keys by (t' - t)."""
+    g = np.random.default_rng(29 + with_null)
+    b, H, dh, J = 4, 2, 8, 7
+    st = _random_store(g, 1, J + 2, b, H, dh, live_frac=0.7)
+    rope = O.Rope(base=100.0, max_offset=max_offset)
+    nkv = g.standard_normal((2, H, dh)) if with_null else None
+    q, ki, vi = (g.standard_normal((1, b, H, dh)) for _ in range(3))
+    out = O.reader_prefill_block_rope(st, [0], [J], q, ki, vi, nkv, rope)
+    idx, Km, Vm = st.export(0, below=J)
+    blk = np.repeat(np.array(idx, int), b)
+    for t in range(b):
+        for h in range(H):
+            ks, vs = [], []
+            # relative turn of a block-j key: j - J, or -min(J - j, W) when clipped
+            turn = (lambda j: j - J) if max_offset is None else (lambda j: -min(J - j, max_offset))
+            if with_null:
+                ks.append(_complex_rotate(nkv[0, h][None], turn(0), 100.0))
+                vs.append(torch.as_tensor(nkv[1, h][None]))
+            if len(blk):
+                ph = np.array([turn(int(j)) for j in blk], np.float64)
+                ks.append(_complex_rotate(Km[:, h], ph, 100.0))
+                vs.append(torch.as_tensor(Vm[:, h]))
+            ks.append(_complex_rotate(ki[0, :t + 1, h], np.arange(t + 1) - t, 100.0))
+            vs.append(torch.as_tensor(vi[0, :t + 1, h]))
+            K, V = torch.cat(ks), torch.cat(vs)
+            ref = F.scaled_dot_product_attention(torch.as_tensor(q[0, t, h])[None, None], K[None], V[None])
+            np.testing.assert_allclose(out[0, t, h], ref[0, 0].numpy(), atol=1e-12, rtol=0)
+
+
+def test_rope_saturation():
+    """Saturated block phases (the needle appendix): identity while the query
+    block is within W of block 0; beyond, all blocks at distance >= W share
+    one phase, so their rows are interchangeable, and nearer ones are not."""
+    g = np.random.default_rng(37)
+    b, H, dh, W = 2, 1, 8, 3
+    mk = lambda: (g.standard_normal((b, H, dh)), g.standard_normal((b, H, dh)))
+    blocks = {j: mk() for j in range(9)}
+
+    def store(perm):
+        st = O.Store(1, 10, b, H, dh)
+        for j in range(9):
+            st.put(0, j, *blocks[perm.get(j, j)])
+        return st
+    q, ki, vi = (g.standard_normal((1, b, H, dh)) for _ in range(3))
+    clip, free = O.Rope(100.0, W), O.Rope(100.0, None)
+    a = O.reader_prefill_block_rope(store({}), [0], [3], q, ki, vi, None, clip)
+    assert np.array_equal(a, O.reader_prefill_block_rope(store({}), [0], [3], q, ki, vi, None, free))
+    base = O.reader_prefill_block_rope(store({}), [0], [9], q, ki, vi, None, clip)
+    far = O.reader_prefill_block_rope(store({0: 5, 5: 0}), [0], [9], q, ki, vi, None, clip)  # both j <= 9 - W
+    np.testing.assert_allclose(far, base, atol=1e-13, rtol=0)
+    near = O.reader_prefill_block_rope(store({0: 7, 7: 0}), [0], [9], q, ki, vi, None, clip)
+    assert np.max(np.abs(near - base)) > 1e-3
+    unclipped = O.reader_prefill_block_rope(store({0: 5, 5: 0}), [0], [9], q, ki, vi, None, free)
+    assert np.max(np.abs(unclipped - O.reader_prefill_block_rope(store({}), [0], [9], q, ki, vi, None, free))) > 1e-3
+
+
+@pytest.mark.parametrize("max_offset", [None, 2])
+def test_rope_null_row_has_block_zero_phase(max_offset):
+    """The null row carries index 0: with one-row blocks, a null row equal to
+    block 0's row reads exactly like block 0 itself (both clipped alike)."""
+    g = np.random.default_rng(41)
+    b, H, dh, J = 1, 2, 8, 6
+    rows = [(g.standard_normal((1, H, dh)), g.standard_normal((1, H, dh))) for _ in range(J)]
+    with_block0, without = O.Store(1, J, b, H, dh), O.Store(1, J, b, H, dh)
+    for j in range(J):
+        with_block0.put(0, j, *rows[j])
+        if j:
+            without.put(0, j, *rows[j])
+    nkv = np.stack([rows[0][0][0], rows[0][1][0]])            # [2, H, dh]
+    q, ki, vi = (g.standard_normal((1, b, H, dh)) for _ in range(3))
+    rope = O.Rope(100.0, max_offset)
+    a = O.reader_prefill_block_rope(with_block0, [0], [J], q, ki, vi, None, rope)
+    c = O.reader_prefill_block_rope(without, [0], [J], q, ki, vi, nkv, rope)
+    np.testing.assert_allclose(c, a, atol=1e-13, rtol=0)
+
+
+def test_rope_values_not_rotated_and_decode_equals_prefill():
+    g = np.random.default_rng(43)
+    b, H, dh, J = 4, 2, 8, 5
+    st = _random_store(g, 1, J, b, H, dh, live_frac=1.0)
+    rope = O.Rope(1e4, 2)
+    zero = np.zeros((1, b, H, dh))
+    ki, vi = g.standard_normal((2, 1, b, H, dh))
+    out = O.reader_prefill_block_rope(st, [0], [J], zero, ki, vi, None, rope)
+    _, _, Vm = st.export(0, below=J)
+    for t in range(b):   # all scores 0: the plain mean of the visible values
+        np.testing.assert_allclose(out[0, t], np.concatenate([Vm, vi[0, :t + 1]]).mean(0), atol=1e-14)
+    q = g.standard_normal((1, b, H, dh))
+    nkv = g.standard_normal((2, H, dh))
+    pre = O.reader_prefill_block_rope(st, [0], [J], q, ki, vi, nkv, rope)
+    for p in (0, 2, b - 1):
+        kc = np.full((1, b, H, dh), 7.0)
+        vc = np.full((1, b, H, dh), 7.0)
+        kc[:, :p], vc[:, :p] = ki[:, :p], vi[:, :p]
+        dec, _, _ = O.reader_decode_rope(st, [0], [J], [p], q[:, p], ki[:, p], vi[:, p], kc, vc, nkv, rope)
+        np.testing.assert_allclose(dec, pre[:, p], atol=1e-13, rtol=0)
