@@ -20,6 +20,8 @@ Secondary workloads, timed in the same run and reported under "secondary":
   * 410M-shaped streaming decode: the headline shape decoding 128 tokens
     from a fresh block, appending each completed block (64 blocks per
     append, encoder attention + insert) as the stream crosses a boundary;
+  * the SMem+RoPE composite (saturating block phases, W = 15) timed on the
+    headline decode and on the 1.5B serve, beside the base reads;
   * 1.5B-shaped stress: 16 sequences x 4096 blocks (262144 rows each, a
     32 GiB store): batch-16 decode over all rows, and single-block delete /
     re-insert latency.
@@ -50,7 +52,7 @@ BF16_PEAK_TFLOPS = 2516.6      # MI355X dense bf16 MFMA, published
 # (scaled by a plain copy of known size), keyed by a hash of the decode
 # kernel's sources: a changed kernel reports traffic as null until measured
 # again.  Figures: profiles/k_reader_valu_decode_410M_hbm_traffic.md
-DECODE_TRAFFIC_BYTES = {"2219a48ada0d03c2": 1.0885e+09}
+DECODE_TRAFFIC_BYTES = {"675c2c2ac9d978d4": 1.0885e+09}
 DECODE_SOURCES = ("paper_2609_32395_amd/csrc/reader_valu.hip", "paper_2609_32395_amd/csrc/common.h")
 
 
@@ -118,6 +120,23 @@ def decode_workload(args, torch, smem, synth):
         step(t)
     secs = _events_time(lambda t: step(t, args.warmup), args.steps, stream)
     torch.cuda.synchronize()
+    rope_res = None
+    if "rope" in args.workloads.split(",") and not args.no_secondary:
+        # the SMem+RoPE composite on the same store and inputs: saturating
+        # block phases (W = 15), in-block phases 0..63
+        rope = smem.Rope(dh, b, 10000.0, 15)
+
+        def rstep(t, base=0):
+            i = (base + t) % n_draw
+            smem.smem_reader_decode_rope(st, rope, seq_ids, qblk, pos_tab[base + t], Q[i], KN[i], VN[i], kc, vc,
+                                         None, out)
+
+        for t in range(args.warmup):
+            rstep(t)
+        rsecs = _events_time(lambda t: rstep(t, args.warmup), args.steps, stream)
+        rope_res = dict(tokens_per_s=S * args.steps / rsecs, ms_per_step=rsecs / args.steps * 1e3,
+                        base_ms_per_step=secs / args.steps * 1e3, max_offset=15)
+        rope.close()
     # algorithmic bytes: memory K+V rows read, in-block rows read (cache rows
     # 0..p-1 plus the new pair), the query, the output and the cache write
     esz = 2
@@ -134,6 +153,7 @@ def decode_workload(args, torch, smem, synth):
         bytes_per_step=bytes_step,
         flops_per_step=flops_step,
         gbs=bytes_step / sec_step / 1e9,
+        rope=rope_res,
         store=st, S=S, H=H, dh=dh, b=b, NB=NB, pos=pos_tab, qs=qs, kn=kn, vn=vn, kc0=kc0, vc0=vc0,
     )
     return res
@@ -210,6 +230,17 @@ def serve_workload(args, torch, smem, synth):
         serve()
     reps = max(5, args.steps // 8)
     serve_s = _events_time(serve, reps, stream) / reps
+    rope_ms = None
+    if "rope" in args.workloads.split(","):
+        rope = smem.Rope(dh, b, 10000.0, 15)
+
+        def rserve(t=0):
+            smem.smem_reader_prefill_block_rope(st, rope, [0], [NB], q, k, v, None, out)
+
+        for _ in range(3):
+            rserve()
+        rope_ms = _events_time(rserve, reps, stream) / reps * 1e3
+        rope.close()
     order = synth.rng(seed, w.wid, synth.ROLE_EDIT, 0, 0, 0).permutation(NB)[:100]
     start = torch.cuda.Event(enable_timing=True)
     mid = torch.cuda.Event(enable_timing=True)
@@ -230,6 +261,7 @@ def serve_workload(args, torch, smem, synth):
     bytes_ = H * (rows * dh * 2 * 2 + 4 * b * dh * 2)
     st.close()
     return dict(serve_ms=serve_s * 1e3, serve_tflops=flops / serve_s / 1e12, serve_gbs=bytes_ / serve_s / 1e9,
+                rope_serve_ms=rope_ms,
                 delete_us_median=float(np.median(del_t)) * 1e3, reserve_ms_median=float(np.median(re_t)),
                 rows_after_deletes=(NB - 100) * b)
 
@@ -381,8 +413,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-secondary", action="store_true")
-    ap.add_argument("--workloads", default="encode,serve,stream,stress",
-                    help="secondary workloads to run (comma list of encode, serve, stream, stress)")
+    ap.add_argument("--workloads", default="encode,serve,stream,stress,rope",
+                    help="secondary workloads to run (comma list of encode, serve, stream, stress, rope: the "
+                         "rotary composite timed beside the headline decode and the serve)")
     ap.add_argument("--no-headline", action="store_true",
                     help="profiling runs only: skip the decode headline (value is then null)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -417,6 +450,8 @@ def main():
             secondary["serve_1p5B"] = serve_workload(args, torch, smem, synth)
         if "stream" in wl:
             secondary["stream_410M"] = stream_workload(args, torch, smem, synth)
+        if dec is not None and dec.get("rope"):
+            secondary["rope_decode_410M"] = dec["rope"]
         if "stress" in wl:
             secondary["stress_1p5B"] = stress_workload(args, torch, smem, synth)
     cpu = None

@@ -188,6 +188,65 @@ smem_status smem_delete_block(smem_store* st, int32_t seq, int32_t block_idx, in
 smem_status smem_store_export(smem_store* st, int32_t seq, int32_t* live_idx, int32_t* n_live,
                               void* k_out, void* v_out, hipStream_t s);
 
+/* ------------------------------------------------------------------------
+ * SMem+RoPE composite (Section 3, "SMem composes with RoPE"; the composite's
+ * appendix, variant v2; saturating reading in the needle appendix).
+ * Memory rows carry no position.  Rotary phases turn queries and keys, never
+ * values: adjacent dimensions (2k, 2k+1) form pair k, turned by the angle
+ * phase * base^(-2k/dh).  Inside a block the phase is the in-block offset
+ * (queries and keys of the encoder and of the reader's in-block keys).
+ * Across blocks it is the block index: the query of block J has phase J, a
+ * memory row of block j has phase max(j, J - W) when max_offset = W > 0 (the
+ * saturating reading) and j when max_offset = 0, and the null row is a row of
+ * index 0 (phase max(0, J - W), or 0).  Under the joint softmax the query
+ * takes phase t (its in-block offset) against its in-block keys and phase J
+ * against the null row and the memory.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t dh;          /* head width served: 32, 64 or 128 */
+  int32_t n_phases;    /* phases 0..n_phases-1 are tabulated */
+  int32_t max_offset;  /* W > 0: saturating block phases; 0: none */
+  int32_t reserved;    /* must be 0 */
+  double base;         /* frequency base (10^4 in the paper), > 1 */
+} smem_rope_desc;
+
+typedef struct smem_rope smem_rope;   /* opaque; a rotary table in device memory */
+
+/* Device bytes of the rotary table: n_phases * dh fp32 (cos, sin pairs),
+ * rounded up to 256.  0 for an invalid descriptor. */
+size_t smem_rope_bytes(const smem_rope_desc* desc);
+
+/* Create a rotary configuration over a caller-owned device buffer (256-byte
+ * aligned, >= smem_rope_bytes); the table is computed on stream s in fp64 and
+ * stored as fp32.  The buffer stays owned by the caller. */
+smem_status smem_rope_create(const smem_rope_desc* desc, void* dev_buf, size_t bytes, hipStream_t s,
+                             smem_rope** out);
+smem_status smem_rope_destroy(smem_rope* rope);
+
+/* smem_encode_blocks with rotary phases on queries and keys (in-block
+ * offsets 0..b-1; needs n_phases >= b and rope dh == shape dh).  The rows put
+ * into the store are the attention outputs, unturned, as in the base call. */
+smem_status smem_encode_blocks_rope(smem_store* st, const smem_attn_desc* shape, const smem_rope* rope,
+                                    int32_t n_blocks, const int32_t* seq_ids, const int32_t* block_idx,
+                                    const void* q, const void* k, const void* v, void* out,
+                                    int32_t mask, hipStream_t s);
+
+/* smem_reader_prefill_block with rotary phases as above.  The table must hold
+ * every phase the call uses: n_phases > max(b - 1, P) with P = min(J, W)
+ * (saturating) or J (none) over the calls' query blocks J; SMEM_EINVAL
+ * otherwise. */
+smem_status smem_reader_prefill_block_rope(smem_store* st, const smem_rope* rope, int32_t n_seq,
+                                           const int32_t* seq_ids, const int32_t* query_block,
+                                           const void* q, const void* k_intra, const void* v_intra,
+                                           const void* null_kv, void* out, hipStream_t s);
+
+/* smem_reader_decode with rotary phases as above (the query's in-block
+ * offset is pos[i]; the cache holds unturned keys).  Same table bound. */
+smem_status smem_reader_decode_rope(smem_store* st, const smem_rope* rope, int32_t n_seq,
+                                    const int32_t* seq_ids, const int32_t* query_block, const int32_t* pos,
+                                    const void* q, const void* k_new, const void* v_new, void* k_cache,
+                                    void* v_cache, const void* null_kv, void* out, hipStream_t s);
+
 /* Host-side facts about a store: pages in use and free. */
 smem_status smem_store_stats(const smem_store* st, int32_t* pages_used, int32_t* pages_free);
 

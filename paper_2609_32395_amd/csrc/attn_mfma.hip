@@ -20,6 +20,14 @@
 // the A operand (transposed values) reads the same keys in the same slots.
 // The store keeps value planes transposed ([dh][b], keys contiguous) so that
 // operand is two contiguous 8-byte reads per lane.
+//
+// SMem+RoPE composite (ROPE = true; Section 3, "SMem composes with RoPE"):
+// queries and keys take rotary phases, values never do.  Inside a block the
+// phase is the in-block offset (query row turned when its fragments are
+// loaded, key rows when the tile passes through registers).  A memory page of
+// block j read from block J turns the query by min(J - j, W) against the
+// stored keys (the same turn for all b rows, so the fragments are re-turned
+// only when it changes); the null row is a key of index 0.
 #include "common.h"
 
 namespace smem {
@@ -154,11 +162,38 @@ __device__ __forceinline__ void tile_store(const TileRegs<DH>& r, Tiles<DH>& T, 
   }
 }
 
+__device__ __forceinline__ u32x4 pack8(const float (&x)[8]) {
+  u32x4 r;
+  r.x = (uint32_t)f32_to_bf16_bits(x[0]) | ((uint32_t)f32_to_bf16_bits(x[1]) << 16);
+  r.y = (uint32_t)f32_to_bf16_bits(x[2]) | ((uint32_t)f32_to_bf16_bits(x[3]) << 16);
+  r.z = (uint32_t)f32_to_bf16_bits(x[4]) | ((uint32_t)f32_to_bf16_bits(x[5]) << 16);
+  r.w = (uint32_t)f32_to_bf16_bits(x[6]) | ((uint32_t)f32_to_bf16_bits(x[7]) << 16);
+  return r;
+}
+
+// Turn the tile's key rows by their in-block offsets (rotary phase = row).
+template <int DH>
+__device__ __forceinline__ void tile_rope(TileRegs<DH>& r, const float* __restrict__ tab, int tid) {
+  using R = TileRegs<DH>;
+#pragma unroll
+  for (int it = 0; it < R::NK; ++it) {
+    const int c = tid + it * 256;
+    const int row = c / R::CPR, c8 = c % R::CPR;
+    float x[8];
+    Chunk<uint16_t>::unpack(r.k[it], x);
+    rope_turn<8>(x, tab + (size_t)row * DH, c8 * 4);
+    r.k[it] = pack8(x);
+  }
+}
+
+// tab == NULL: no rotary phases.
 template <int DH>
 __device__ __forceinline__ void intra_store(Tiles<DH>& T, const uint16_t* __restrict__ kin,
-                                            const uint16_t* __restrict__ vin, size_t row_stride, int tid) {
+                                            const uint16_t* __restrict__ vin, size_t row_stride, int tid,
+                                            const float* __restrict__ tab = nullptr) {
   TileRegs<DH> r;
   tile_load<DH>(r, kin, vin, row_stride, tid);
+  if (tab) tile_rope<DH>(r, tab, tid);
   tile_store<DH>(r, T, tid);
 }
 
@@ -170,6 +205,37 @@ __device__ __forceinline__ void load_q(bf16x8 (&qf)[DH / 32], const uint16_t* __
   const uint16_t* qr = q + (size_t)(lane & 15) * row_stride + (lane >> 4) * 8;
 #pragma unroll
   for (int kk = 0; kk < DH / 32; ++kk) qf[kk] = as_bf16x8(*(const u32x4*)(qr + kk * 32));
+}
+
+// Query fragments turned by one phase row: dst = R(phase) src.
+template <int DH>
+__device__ __forceinline__ void rope_q(bf16x8 (&dst)[DH / 32], const bf16x8 (&src)[DH / 32],
+                                       const float* __restrict__ row, int lane) {
+#pragma unroll
+  for (int kk = 0; kk < DH / 32; ++kk) {
+    float x[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = (float)src[kk][j];
+    rope_turn<8>(x, row, kk * 16 + (lane >> 4) * 4);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) dst[kk][j] = (__bf16)x[j];
+  }
+}
+
+// Re-turn the query fragments from their unturned copy in LDS, one k-chunk
+// at a time (a scheduling barrier per chunk keeps the temporaries few).
+template <int DH>
+__device__ __forceinline__ void rope_q_from_lds(bf16x8 (&dst)[DH / 32], const u32x4* __restrict__ qb,
+                                                const float* __restrict__ row, int wave, int lane) {
+#pragma unroll
+  for (int kk = 0; kk < DH / 32; ++kk) {
+    float x[8];
+    Chunk<uint16_t>::unpack(qb[(kk * 4 + wave) * 64 + lane], x);
+    rope_turn<8>(x, row, kk * 16 + (lane >> 4) * 4);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) dst[kk][j] = (__bf16)x[j];
+    __builtin_amdgcn_sched_barrier(0);
+  }
 }
 
 // S^T for this wave's 16 queries against the 64 keys in LDS.
@@ -267,6 +333,7 @@ struct EncArgs {
   int32_t n_blocks;
   int32_t causal;
   float scale_log2;
+  const float* rope;         // rotary table (in-block phases) or NULL
   int32_t sink[kMaxSlots];   // page of block i, or -1
 };
 
@@ -274,16 +341,18 @@ struct EncArgs {
 // workgroups read neighbouring head slices of the same token rows.  Every
 // tile's loads are issued at once; with all tiles resident, tiles whose data
 // arrive first compute while the rest are still loading.
-template <int DH, bool CAUSAL>
+template <int DH, bool CAUSAL, bool ROPE>
 __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
   __shared__ Tiles<DH> T;
   const int h = blockIdx.x, blk = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const size_t rs = (size_t)a.H * DH;
   const size_t base = (size_t)blk * BT * rs + (size_t)h * DH;
+  const int qrow = wave * 16 + (lane & 15);
   bf16x8 qf[DH / 32];
   load_q<DH>(qf, a.q + base + (size_t)wave * 16 * rs, rs, lane);
-  intra_store<DH>(T, a.k + base, a.v + base, rs, tid);
+  if constexpr (ROPE) rope_q<DH>(qf, qf, a.rope + (size_t)qrow * DH, lane);
+  intra_store<DH>(T, a.k + base, a.v + base, rs, tid, ROPE ? a.rope : nullptr);
   __syncthreads();
   floatx4 s4[4];
   scores<DH>(s4, T, qf, lane);
@@ -291,7 +360,6 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, l = 0.f;
-  const int qrow = wave * 16 + (lane & 15);
   online_step<DH, CAUSAL>(s4, m, l, o, lane, qrow, a.scale_log2);
   pv<DH>(o, T, s4, lane);
   l = qsum(l);
@@ -317,16 +385,20 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
 
 template <int DH>
 static hipError_t launch_enc(const EncArgs& a, int n_blocks, hipStream_t s) {
-  if (a.causal)
-    hipLaunchKernelGGL((k_encoder_mfma<DH, true>), dim3(a.H, n_blocks), dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL((k_encoder_mfma<DH, false>), dim3(a.H, n_blocks), dim3(256), 0, s, a);
+  const dim3 grid(a.H, n_blocks);
+  if (a.rope) {
+    if (a.causal) hipLaunchKernelGGL((k_encoder_mfma<DH, true, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_encoder_mfma<DH, false, true>), grid, dim3(256), 0, s, a);
+  } else {
+    if (a.causal) hipLaunchKernelGGL((k_encoder_mfma<DH, true, false>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_encoder_mfma<DH, false, false>), grid, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_encoder_mfma(int b, int dh, const void* q, const void* k, const void* v, void* out, void* pages,
                                const int32_t* sink_pages, int n_blocks, int H, int mask, float scale_log2,
-                               hipStream_t s) {
+                               const float* rope, hipStream_t s) {
   if (b != BT || n_blocks > kMaxSlots) return hipErrorInvalidValue;
   if (n_blocks <= 0) return hipSuccess;
   EncArgs a;
@@ -339,6 +411,7 @@ hipError_t launch_encoder_mfma(int b, int dh, const void* q, const void* k, cons
   a.n_blocks = n_blocks;
   a.causal = mask;
   a.scale_log2 = scale_log2;
+  a.rope = rope;
   for (int i = 0; i < kMaxSlots; ++i) a.sink[i] = i < n_blocks ? sink_pages[i] : -1;
   if (dh == 32) return launch_enc<32>(a, n_blocks, s);
   if (dh == 64) return launch_enc<64>(a, n_blocks, s);
@@ -348,8 +421,26 @@ hipError_t launch_encoder_mfma(int b, int dh, const void* q, const void* k, cons
 
 // ------------------------------------------------------------------ reader prefill
 
+// Rotary rows a memory split keeps in LDS: the turns of one split form a
+// contiguous range (turn = min(J - j, W) falls as j rises); a split whose range
+// fits reads its cos/sin from LDS, so re-turning the query inside the page loop
+// never waits on a global load issued behind the in-flight pages.
+constexpr int kRopeRows = 24;
+
+template <int DH, bool ROPE>
+struct PrefillLds {
+  Tiles<DH> T;
+};
 template <int DH>
-__device__ __forceinline__ void prefill_body(const ReaderArgs& a, Tiles<DH>& T) {
+struct PrefillLds<DH, true> {
+  Tiles<DH> T;
+  float rows[kRopeRows * DH];          // turns d_lo .. d_lo + kRopeRows - 1
+  u32x4 qb[(DH / 32) * 4 * 64];        // unturned query fragments, [kk][wave][lane]
+};
+
+template <int DH, bool ROPE>
+__device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH, ROPE>& L) {
+  Tiles<DH>& T = L.T;
   // heads fastest: neighbouring workgroups stream the adjacent head tiles of
   // the same pages
   const int h = blockIdx.x, split = blockIdx.y, slot = blockIdx.z;
@@ -373,6 +464,25 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, Tiles<DH>& T) 
     constexpr int kDepth = 3;
     const int p0 = split * pps, p1 = min(n_read, p0 + pps);
     const int32_t* lp = a.live_page + (size_t)a.seq[slot] * a.max_blocks;
+    [[maybe_unused]] const int32_t* lb = a.live_blk + (size_t)a.seq[slot] * a.max_blocks;
+    [[maybe_unused]] int turned = -1, d_lo = 0;
+    [[maybe_unused]] bool rows_lds = false;
+    if constexpr (ROPE) {
+      // before the first page load: these waits drain nothing
+      const int J = a.qblk[slot];
+      const int d_hi = min(J - lb[p0], a.rope_clip);
+      d_lo = min(J - lb[p1 - 1], a.rope_clip);
+      rows_lds = d_hi - d_lo < kRopeRows;
+      if (rows_lds) {
+        const int n4 = (d_hi - d_lo + 1) * DH / 4;
+        const f32x4* src = (const f32x4*)(a.rope + (size_t)d_lo * DH);
+        for (int i = tid; i < n4; i += 256) ((f32x4*)L.rows)[i] = src[i];
+      }
+#pragma unroll
+      for (int kk = 0; kk < DH / 32; ++kk) L.qb[(kk * 4 + wave) * 64 + lane] = __builtin_bit_cast(u32x4, qf[kk]);
+      // L.rows is read after the barrier that precedes the first page_store;
+      // each lane reads back only its own L.qb entries
+    }
     const uint16_t* pages = (const uint16_t*)a.pages;
     PageRegs<DH> r[kDepth];
 #pragma unroll
@@ -390,6 +500,16 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, Tiles<DH>& T) 
           __syncthreads();
           page_store<DH>(r[u], T, tid);
           __syncthreads();
+          if constexpr (ROPE) {
+            // between the store of stage u and its refill, so the turn's
+            // temporaries take the stage's registers
+            const int dlt = min(a.qblk[slot] - lb[pi], a.rope_clip);
+            if (dlt != turned) {
+              if (rows_lds) rope_q_from_lds<DH>(qf, L.qb, L.rows + (dlt - d_lo) * DH, wave, lane);
+              else rope_q_from_lds<DH>(qf, L.qb, a.rope + (size_t)dlt * DH, wave, lane);
+              turned = dlt;
+            }
+          }
           if (pi + kDepth < p1) {
             const uint16_t* Kt = pages + page_head_offset(lp[pi + kDepth], h, a.H, BT, DH);
             page_load<DH>(r[u], Kt, Kt + BT * DH, tid);
@@ -406,6 +526,13 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, Tiles<DH>& T) 
       // the null row: one always-visible key/value pair per head
       const uint16_t* nk = (const uint16_t*)a.null_kv + (size_t)h * DH + (lane >> 4) * 8;
       const uint16_t* nv = (const uint16_t*)a.null_kv + ((size_t)a.H + h) * DH;
+      bf16x8 qn[DH / 32];
+      if constexpr (ROPE) {
+        rope_q<DH>(qn, qf, a.rope + (size_t)min(a.qblk[slot], a.rope_clip) * DH, lane);
+      } else {
+#pragma unroll
+        for (int kk = 0; kk < DH / 32; ++kk) qn[kk] = qf[kk];
+      }
       float x = 0.f;
 #pragma unroll
       for (int kk = 0; kk < DH / 32; ++kk) {
@@ -413,7 +540,7 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, Tiles<DH>& T) 
         float kf[8];
         Chunk<uint16_t>::unpack(kr, kf);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) x += (float)qf[kk][j] * kf[j];
+        for (int j = 0; j < 8; ++j) x += (float)qn[kk][j] * kf[j];
       }
       x = qsum(x) * a.scale_log2;
       m = x;
@@ -426,7 +553,9 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, Tiles<DH>& T) 
     }
     if (a.k_in != nullptr) {
       const size_t base = (size_t)slot * BT * rs + (size_t)h * DH;
-      intra_store<DH>(T, (const uint16_t*)a.k_in + base, (const uint16_t*)a.v_in + base, rs, tid);
+      if constexpr (ROPE) rope_q<DH>(qf, qf, a.rope + (size_t)qrow * DH, lane);
+      intra_store<DH>(T, (const uint16_t*)a.k_in + base, (const uint16_t*)a.v_in + base, rs, tid,
+                      ROPE ? a.rope : nullptr);
       __syncthreads();
       floatx4 s[4];
       scores<DH>(s, T, qf, lane);
@@ -464,8 +593,17 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, Tiles<DH>& T) 
 
 template <int DH>
 __global__ void __launch_bounds__(256) k_prefill_mfma(ReaderArgs a) {
-  __shared__ Tiles<DH> T;
-  prefill_body<DH>(a, T);
+  __shared__ PrefillLds<DH, false> L;
+  prefill_body<DH, false>(a, L);
+}
+
+// The rotary variant asks for at least two waves per SIMD: left free, the
+// compiler spends registers on the query turn and falls to one wave at
+// dh = 128 (it fits two without spilling).
+template <int DH>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_prefill_mfma_rope(ReaderArgs a) {
+  __shared__ PrefillLds<DH, true> L;
+  prefill_body<DH, true>(a, L);
 }
 
 template <int DH>
@@ -475,7 +613,9 @@ static hipError_t launch_pre(const ReaderArgs& a, hipStream_t s) {
     const int ns = total_splits(a.n_read[i], a.pps[i]) - 1;
     if (ns > max_split) max_split = ns;
   }
-  hipLaunchKernelGGL((k_prefill_mfma<DH>), dim3(a.H, max_split + 1, a.n_slots), dim3(256), 0, s, a);
+  const dim3 grid(a.H, max_split + 1, a.n_slots);
+  if (a.rope) hipLaunchKernelGGL((k_prefill_mfma_rope<DH>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((k_prefill_mfma<DH>), grid, dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || max_split == 0) return e;
   return launch_merge(BF16, DH, a, s);

@@ -49,6 +49,7 @@ enum Dtype : int32_t { F32 = 0, BF16 = 1 };
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 // Streamed page data is read once per call: non-temporal loads keep it from
 // displacing reused lines in the caches.
@@ -89,6 +90,27 @@ template <> struct Chunk<uint16_t> {
     f[6] = __uint_as_float(c.w << 16); f[7] = __uint_as_float(c.w & 0xffff0000u);
   }
 };
+
+// ---------------------------------------------------------------- rotary phases
+
+// Rotary table: row p (p = 0 .. n_phases-1) holds, for each adjacent pair k
+// of a head's dh dimensions, (cos, sin) of the angle p * base^(-2k/dh) as
+// fp32; a row is dh floats.  rope_turn rotates E consecutive elements
+// (E/2 pairs starting at pair k0, k0 even) by the phase of one row:
+// (x0, x1) -> (x0 cos - x1 sin, x0 sin + x1 cos).
+template <int E>
+__device__ __forceinline__ void rope_turn(float (&x)[E], const float* __restrict__ row, int k0) {
+  static_assert(E % 4 == 0, "two pairs per 16-byte table read");
+#pragma unroll
+  for (int m = 0; m < E / 4; ++m) {
+    const f32x4 cs = *(const f32x4*)(row + 2 * k0 + 4 * m);
+    const float a0 = x[4 * m], a1 = x[4 * m + 1], b0 = x[4 * m + 2], b1 = x[4 * m + 3];
+    x[4 * m] = a0 * cs.x - a1 * cs.y;
+    x[4 * m + 1] = a0 * cs.y + a1 * cs.x;
+    x[4 * m + 2] = b0 * cs.z - b1 * cs.w;
+    x[4 * m + 3] = b0 * cs.w + b1 * cs.z;
+  }
+}
 
 template <typename T> __device__ __forceinline__ float to_f32(T x);
 template <> __device__ __forceinline__ float to_f32<float>(float x) { return x; }
@@ -143,6 +165,11 @@ struct ReaderArgs {
   int32_t n_read[kMaxSlots];  // memory pages the slot reads (live blocks j < J)
   int32_t pps[kMaxSlots];     // pages per split
   int32_t aux[kMaxSlots];     // decode: pos; fp32 encoder: sink page or -1
+  // SMem+RoPE composite (NULL rope: no rotary phases)
+  const float* rope;          // rotary table, rows of dh floats
+  const int32_t* live_blk;    // [n_seq][max_blocks] dense live list -> block index
+  int32_t rope_clip;          // W: a block-j key read from block J is turned by min(J - j, W)
+  int32_t qblk[kMaxSlots];    // query block J of the slot
 };
 
 struct MetaArgs {
@@ -174,9 +201,12 @@ hipError_t launch_reader_valu(int dtype, int b, int dh, const ReaderArgs& a, hip
 // Merge the split partials of every (query row, head) in split order.
 hipError_t launch_merge(int dtype, int dh, const ReaderArgs& a, hipStream_t s);
 // MFMA (bf16, b = 64) encoder and prefill.
+// rope: rotary table (in-block phases), or NULL.
 hipError_t launch_encoder_mfma(int b, int dh, const void* q, const void* k, const void* v, void* out,
                                void* pages, const int32_t* sink_pages, int n_blocks, int H, int mask,
-                               float scale_log2, hipStream_t s);
+                               float scale_log2, const float* rope, hipStream_t s);
 hipError_t launch_prefill_mfma(int b, int dh, const ReaderArgs& a, hipStream_t s);
+// Rotary table of n_phases rows for heads of width dh, computed in fp64.
+hipError_t launch_rope_table(float* table, int dh, int n_phases, double base, hipStream_t s);
 
 }  // namespace smem

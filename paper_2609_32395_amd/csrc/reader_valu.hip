@@ -21,6 +21,15 @@
 // product is finished with xor-shuffles.  Softmax weights go through a
 // per-wave LDS row so each lane can weight a 16-byte chunk of the
 // transposed value plane (contiguous keys).
+//
+// SMem+RoPE composite (ROPE = true; Section 3, "SMem composes with RoPE"):
+// rows carry no position, so the rotary phases are applied here.  A memory
+// key of block j read from block J scores as <R(J) q, R(j') k> with
+// j' = max(j, J - W), i.e. the query turned by min(J - j, W) against the
+// stored key; the null row is a key of index 0; in-block keys score as
+// <R(t) q, R(t') k> with t, t' the in-block offsets.  Values are never
+// turned.  Every row of one page shares a turn, so the query is re-turned
+// only when the turn changes from one page to the next.
 #include "common.h"
 
 namespace smem {
@@ -44,7 +53,7 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
-template <typename T, int DH, int B>
+template <typename T, int DH, int B, bool ROPE>
 __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
   using C = RCfg<T, DH, B>;
   constexpr int E = C::E;
@@ -69,6 +78,11 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
 #pragma unroll
     for (int e = 0; e < E; ++e) qf[e] *= a.scale_log2;
   }
+  [[maybe_unused]] float qb[E];   // the unturned query (rotary phases only)
+  if constexpr (ROPE) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) qb[e] = qf[e];
+  }
   float m = -INFINITY, l = 0.f;
 
   if (split < nms) {
@@ -80,8 +94,19 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
     const int p0 = split * pps;
     const int p1 = min(n_read, p0 + pps);
     const int32_t* lp = a.live_page + (size_t)a.seq[slot] * a.max_blocks;
+    [[maybe_unused]] const int32_t* lb = a.live_blk + (size_t)a.seq[slot] * a.max_blocks;
+    [[maybe_unused]] int turned = -1;
     for (int pi = p0 + wave; pi < p1; pi += 4) {
       const int pg = lp[pi];
+      if constexpr (ROPE) {
+        const int dlt = min(a.qblk[slot] - lb[pi], a.rope_clip);
+        if (dlt != turned) {
+#pragma unroll
+          for (int e = 0; e < E; ++e) qf[e] = qb[e];
+          rope_turn<E>(qf, a.rope + (size_t)dlt * DH, c * (E / 2));
+          turned = dlt;
+        }
+      }
       const T* Kt = (const T*)a.pages + page_head_offset(pg, h, a.H, B, DH);
       const T* VT = Kt + B * DH;
       u32x4 kraw[C::KLOADS];
@@ -162,9 +187,13 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
       float kf[E], vf[E];
       Chunk<T>::unpack(*(const u32x4*)nk, kf);
       Chunk<T>::unpack(*(const u32x4*)nv, vf);
+      float qn[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) qn[e] = qf[e];
+      if constexpr (ROPE) rope_turn<E>(qn, a.rope + (size_t)min(a.qblk[slot], a.rope_clip) * DH, c * (E / 2));
       float x = 0.f;
 #pragma unroll
-      for (int e = 0; e < E; ++e) x += qf[e] * kf[e];
+      for (int e = 0; e < E; ++e) x += qn[e] * kf[e];
 #pragma unroll
       for (int o = 1; o < C::LPR; o <<= 1) x += __shfl_xor(x, o);
       m = x;
@@ -180,6 +209,7 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
     if (decode) n_in = (a.k_new != nullptr) ? pos + 1 : 0;
     else if (a.k_in == nullptr) n_in = 0;
     else n_in = (a.intra_mode == 0) ? B : t + 1;
+    if constexpr (ROPE) rope_turn<E>(qf, a.rope + (size_t)(decode ? pos : t) * DH, c * (E / 2));
     for (int r0 = wave * C::RPL; r0 < n_in; r0 += 4 * C::RPL) {
       const int r = r0 + rg;
       const bool valid = r < n_in;
@@ -198,6 +228,7 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
         }
         Chunk<T>::unpack(*(const u32x4*)(ks + c * E), kf);
         Chunk<T>::unpack(*(const u32x4*)(vs + c * E), vf);
+        if constexpr (ROPE) rope_turn<E>(kf, a.rope + (size_t)r * DH, c * (E / 2));
       }
       float x = 0.f;
 #pragma unroll
@@ -324,7 +355,10 @@ static hipError_t launch_rv(const ReaderArgs& a, hipStream_t s) {
     if (ns > max_split) max_split = ns;
   }
   dim3 grid(a.H, max_split + 1, a.n_slots * a.nq);
-  hipLaunchKernelGGL((k_reader_valu<T, DH, B>), grid, dim3(256), 0, s, a);
+  if (a.rope != nullptr)
+    hipLaunchKernelGGL((k_reader_valu<T, DH, B, true>), grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_reader_valu<T, DH, B, false>), grid, dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || max_split == 0) return e;
   return launch_merge(sizeof(T) == 4 ? F32 : BF16, DH, a, s);

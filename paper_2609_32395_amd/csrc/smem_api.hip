@@ -39,6 +39,11 @@ struct smem_store {
   std::vector<int32_t> free_pages;         // stack; back() is handed out next
 };
 
+struct smem_rope {
+  smem_rope_desc d;
+  float* table = nullptr;                  // [n_phases][dh/2] (cos, sin)
+};
+
 namespace {
 
 thread_local std::string g_err;
@@ -86,6 +91,35 @@ bool layout_of(const smem_store_desc* d, DevLayout* L) {
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+size_t rope_bytes_of(const smem_rope_desc* d) {
+  if (!d || !(d->dh == 32 || d->dh == 64 || d->dh == 128) || d->n_phases < 1 || d->n_phases > (1 << 20) ||
+      d->max_offset < 0 || d->reserved != 0 || !(d->base > 1.0) || !std::isfinite(d->base))
+    return 0;
+  return align256((size_t)d->n_phases * d->dh * sizeof(float));
+}
+
+// Check a rotary configuration against a call: head width, and that the
+// table holds every phase used (in-block offsets < b, block turns <= max_turn).
+smem_status rope_check(const smem_rope* rope, int dh, int b, int max_turn) {
+  if (rope->d.dh != dh) return fail(SMEM_EINVAL, "rotary table is for dh=%d, the call has dh=%d", rope->d.dh, dh);
+  const int need = std::max(b - 1, max_turn);
+  if (need >= rope->d.n_phases)
+    return fail(SMEM_EINVAL, "phase %d needed, the rotary table holds 0..%d", need, rope->d.n_phases - 1);
+  return SMEM_OK;
+}
+
+// Largest block turn of a read from query block J: min(J, W), or J.
+int rope_turn_of(const smem_rope* rope, int J) {
+  return rope->d.max_offset > 0 ? std::min(J, rope->d.max_offset) : J;
+}
+
+void rope_args(ReaderArgs& a, const smem_store* st, const smem_rope* rope) {
+  if (!rope) return;
+  a.rope = rope->table;
+  a.live_blk = st->d_live_blk;
+  a.rope_clip = rope->d.max_offset > 0 ? rope->d.max_offset : INT32_MAX;
+}
 
 int n_read_of(const smem_store* st, int seq, int J) {
   const auto& lv = st->live[seq];
@@ -273,10 +307,15 @@ smem_status smem_store_export(smem_store* st, int32_t seq, int32_t* live_idx, in
 
 static smem_status encode_impl(smem_store* st, const smem_attn_desc* shape, int32_t n_blocks,
                                const int32_t* seq_ids, const int32_t* block_idx, const void* q, const void* k,
-                               const void* v, void* out, int32_t mask, bool replace, hipStream_t s) {
+                               const void* v, void* out, int32_t mask, bool replace, const smem_rope* rope,
+                               hipStream_t s) {
   if (!shape) return fail(SMEM_EINVAL, "shape is NULL");
   const int b = shape->b, H = shape->H, dh = shape->dh, dtype = shape->dtype;
   if (!shape_ok(b, H, dh, dtype)) return fail(SMEM_EINVAL, "unsupported shape b=%d H=%d dh=%d dtype=%d", b, H, dh, dtype);
+  if (rope) {
+    const smem_status r = rope_check(rope, dh, b, 0);
+    if (r != SMEM_OK) return r;
+  }
   if (n_blocks < 0) return fail(SMEM_EINVAL, "n_blocks < 0");
   if (mask != SMEM_MASK_BIDIR && mask != SMEM_MASK_CAUSAL) return fail(SMEM_EINVAL, "mask %d", mask);
   if (st) {
@@ -331,7 +370,8 @@ static smem_status encode_impl(smem_store* st, const smem_attn_desc* shape, int3
     if (dtype == BF16 && b == 64) {
       int32_t sink[kMaxSlots];
       for (int i = 0; i < n; ++i) sink[i] = st ? pages[i0 + i] : -1;
-      e = launch_encoder_mfma(b, dh, qb, kb, vb, ob, st ? st->d_pages : nullptr, sink, n, H, mask, scale_log2, s);
+      e = launch_encoder_mfma(b, dh, qb, kb, vb, ob, st ? st->d_pages : nullptr, sink, n, H, mask, scale_log2,
+                              rope ? rope->table : nullptr, s);
     } else {
       if (!ob) return fail(SMEM_EINVAL, "this encoder shape needs an out tensor");
       ReaderArgs a;
@@ -340,6 +380,7 @@ static smem_status encode_impl(smem_store* st, const smem_attn_desc* shape, int3
       a.page_sink = st ? st->d_pages : nullptr;
       a.H = H; a.b = b; a.nq = b; a.intra_mode = mask == SMEM_MASK_CAUSAL ? 1 : 0;
       a.n_slots = n; a.scale_log2 = scale_log2;
+      a.rope = rope ? rope->table : nullptr;
       for (int i = 0; i < n; ++i) {
         a.seq[i] = 0; a.n_read[i] = 0; a.pps[i] = 1;
         a.aux[i] = st ? pages[i0 + i] : -1;
@@ -370,19 +411,27 @@ static smem_status encode_impl(smem_store* st, const smem_attn_desc* shape, int3
 smem_status smem_encode_blocks(smem_store* st, const smem_attn_desc* shape, int32_t n_blocks,
                                const int32_t* seq_ids, const int32_t* block_idx, const void* q, const void* k,
                                const void* v, void* out, int32_t mask, hipStream_t s) {
-  return encode_impl(st, shape, n_blocks, seq_ids, block_idx, q, k, v, out, mask, false, s);
+  return encode_impl(st, shape, n_blocks, seq_ids, block_idx, q, k, v, out, mask, false, nullptr, s);
+}
+
+smem_status smem_encode_blocks_rope(smem_store* st, const smem_attn_desc* shape, const smem_rope* rope,
+                                    int32_t n_blocks, const int32_t* seq_ids, const int32_t* block_idx,
+                                    const void* q, const void* k, const void* v, void* out, int32_t mask,
+                                    hipStream_t s) {
+  if (!rope) return fail(SMEM_EINVAL, "rope is NULL");
+  return encode_impl(st, shape, n_blocks, seq_ids, block_idx, q, k, v, out, mask, false, rope, s);
 }
 
 smem_status smem_reencode_blocks(smem_store* st, const smem_attn_desc* shape, int32_t n_blocks,
                                  const int32_t* seq_ids, const int32_t* block_idx, const void* q, const void* k,
                                  const void* v, void* out, int32_t mask, hipStream_t s) {
   if (!st) return fail(SMEM_EINVAL, "store is NULL");
-  return encode_impl(st, shape, n_blocks, seq_ids, block_idx, q, k, v, out, mask, true, s);
+  return encode_impl(st, shape, n_blocks, seq_ids, block_idx, q, k, v, out, mask, true, nullptr, s);
 }
 
-smem_status smem_reader_prefill_block(smem_store* st, int32_t n_seq, const int32_t* seq_ids,
-                                      const int32_t* query_block, const void* q, const void* k_intra,
-                                      const void* v_intra, const void* null_kv, void* out, hipStream_t s) {
+static smem_status prefill_impl(smem_store* st, const smem_rope* rope, int32_t n_seq, const int32_t* seq_ids,
+                                const int32_t* query_block, const void* q, const void* k_intra,
+                                const void* v_intra, const void* null_kv, void* out, hipStream_t s) {
   if (!st) return fail(SMEM_EINVAL, "store is NULL");
   if (st->meta_only) return fail(SMEM_EINVAL, "metadata-only store");
   const auto& d = st->d;
@@ -396,6 +445,10 @@ smem_status smem_reader_prefill_block(smem_store* st, int32_t n_seq, const int32
     if (seq_ids[i] < 0 || seq_ids[i] >= d.n_seq) return fail(SMEM_EINVAL, "seq_ids[%d] = %d out of range", i, seq_ids[i]);
     if (query_block[i] < 0 || query_block[i] > d.max_blocks)
       return fail(SMEM_EINVAL, "query_block[%d] = %d out of range [0, %d]", i, query_block[i], d.max_blocks);
+    if (rope) {
+      const smem_status r = rope_check(rope, d.dh, d.b, rope_turn_of(rope, query_block[i]));
+      if (r != SMEM_OK) return r;
+    }
   }
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
   const size_t es = esize(d.dtype);
@@ -416,11 +469,13 @@ smem_status smem_reader_prefill_block(smem_store* st, int32_t n_seq, const int32
     a.max_blocks = d.max_blocks;
     a.H = d.H; a.b = d.b; a.nq = d.b; a.intra_mode = 1;
     a.n_slots = n; a.scale_log2 = scale_log2;
+    rope_args(a, st, rope);
     // bf16 blocks of 64 tokens run on the MFMA kernel, other shapes on the VALU reader
     const bool mfma = d.dtype == BF16 && d.b == 64;
     for (int i = 0; i < n; ++i) {
       const int sq = seq_ids[i0 + i];
       a.seq[i] = sq;
+      a.qblk[i] = query_block[i0 + i];
       a.n_read[i] = n_read_of(st, sq, query_block[i0 + i]);
       a.pps[i] = mfma ? pages_per_split(a.n_read[i], kMinPagesPrefill, kSplitCapPrefill)
                       : pages_per_split(a.n_read[i], kMinPagesDecode);
@@ -432,9 +487,10 @@ smem_status smem_reader_prefill_block(smem_store* st, int32_t n_seq, const int32
   return SMEM_OK;
 }
 
-smem_status smem_reader_decode(smem_store* st, int32_t n_seq, const int32_t* seq_ids, const int32_t* query_block,
-                               const int32_t* pos, const void* q, const void* k_new, const void* v_new,
-                               void* k_cache, void* v_cache, const void* null_kv, void* out, hipStream_t s) {
+static smem_status decode_impl(smem_store* st, const smem_rope* rope, int32_t n_seq, const int32_t* seq_ids,
+                               const int32_t* query_block, const int32_t* pos, const void* q, const void* k_new,
+                               const void* v_new, void* k_cache, void* v_cache, const void* null_kv, void* out,
+                               hipStream_t s) {
   if (!st) return fail(SMEM_EINVAL, "store is NULL");
   if (st->meta_only) return fail(SMEM_EINVAL, "metadata-only store");
   const auto& d = st->d;
@@ -454,6 +510,10 @@ smem_status smem_reader_decode(smem_store* st, int32_t n_seq, const int32_t* seq
       return fail(SMEM_EINVAL, "query_block[%d] = %d out of range [0, %d]", i, query_block[i], d.max_blocks);
     if (n_given == 4 && (pos[i] < 0 || pos[i] >= d.b)) return fail(SMEM_EINVAL, "pos[%d] = %d out of range [0, %d)", i, pos[i], d.b);
     if (!seen.insert(seq_ids[i]).second) return fail(SMEM_EINVAL, "sequence %d appears twice", seq_ids[i]);
+    if (rope) {
+      const smem_status r = rope_check(rope, d.dh, d.b, rope_turn_of(rope, query_block[i]));
+      if (r != SMEM_OK) return r;
+    }
   }
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
   const size_t es = esize(d.dtype);
@@ -479,9 +539,11 @@ smem_status smem_reader_decode(smem_store* st, int32_t n_seq, const int32_t* seq
     a.max_blocks = d.max_blocks;
     a.H = d.H; a.b = d.b; a.nq = 1; a.intra_mode = 2;
     a.n_slots = n; a.scale_log2 = scale_log2;
+    rope_args(a, st, rope);
     for (int i = 0; i < n; ++i) {
       const int sq = seq_ids[i0 + i];
       a.seq[i] = sq;
+      a.qblk[i] = query_block[i0 + i];
       a.n_read[i] = n_read_of(st, sq, query_block[i0 + i]);
       a.pps[i] = pages_per_split(a.n_read[i], kMinPagesDecode);
       a.aux[i] = n_given == 4 ? pos[i0 + i] : 0;
@@ -489,6 +551,65 @@ smem_status smem_reader_decode(smem_store* st, int32_t n_seq, const int32_t* seq
     hipError_t e = launch_reader_valu(d.dtype, d.b, d.dh, a, s);
     if (e != hipSuccess) return hip_fail(e, "decode launch");
   }
+  return SMEM_OK;
+}
+
+smem_status smem_reader_prefill_block(smem_store* st, int32_t n_seq, const int32_t* seq_ids,
+                                      const int32_t* query_block, const void* q, const void* k_intra,
+                                      const void* v_intra, const void* null_kv, void* out, hipStream_t s) {
+  return prefill_impl(st, nullptr, n_seq, seq_ids, query_block, q, k_intra, v_intra, null_kv, out, s);
+}
+
+smem_status smem_reader_prefill_block_rope(smem_store* st, const smem_rope* rope, int32_t n_seq,
+                                           const int32_t* seq_ids, const int32_t* query_block, const void* q,
+                                           const void* k_intra, const void* v_intra, const void* null_kv,
+                                           void* out, hipStream_t s) {
+  if (!rope) return fail(SMEM_EINVAL, "rope is NULL");
+  return prefill_impl(st, rope, n_seq, seq_ids, query_block, q, k_intra, v_intra, null_kv, out, s);
+}
+
+smem_status smem_reader_decode(smem_store* st, int32_t n_seq, const int32_t* seq_ids, const int32_t* query_block,
+                               const int32_t* pos, const void* q, const void* k_new, const void* v_new,
+                               void* k_cache, void* v_cache, const void* null_kv, void* out, hipStream_t s) {
+  return decode_impl(st, nullptr, n_seq, seq_ids, query_block, pos, q, k_new, v_new, k_cache, v_cache, null_kv,
+                     out, s);
+}
+
+smem_status smem_reader_decode_rope(smem_store* st, const smem_rope* rope, int32_t n_seq, const int32_t* seq_ids,
+                                    const int32_t* query_block, const int32_t* pos, const void* q,
+                                    const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                                    const void* null_kv, void* out, hipStream_t s) {
+  if (!rope) return fail(SMEM_EINVAL, "rope is NULL");
+  return decode_impl(st, rope, n_seq, seq_ids, query_block, pos, q, k_new, v_new, k_cache, v_cache, null_kv,
+                     out, s);
+}
+
+size_t smem_rope_bytes(const smem_rope_desc* desc) { return rope_bytes_of(desc); }
+
+smem_status smem_rope_create(const smem_rope_desc* desc, void* dev_buf, size_t bytes, hipStream_t s,
+                             smem_rope** out) {
+  if (!out) return fail(SMEM_EINVAL, "out is NULL");
+  *out = nullptr;
+  const size_t need = rope_bytes_of(desc);
+  if (need == 0) return fail(SMEM_EINVAL, "invalid rotary descriptor");
+  if (!dev_buf) return fail(SMEM_EINVAL, "dev_buf is NULL");
+  if (((uintptr_t)dev_buf & 255u) != 0) return fail(SMEM_EINVAL, "dev_buf must be 256-byte aligned");
+  if (bytes < need) return fail(SMEM_ENOMEM, "rotary table needs %zu bytes, %zu given", need, bytes);
+  smem_rope* r = new (std::nothrow) smem_rope;
+  if (!r) return fail(SMEM_ENOMEM, "host allocation failed");
+  r->d = *desc;
+  r->table = (float*)dev_buf;
+  hipError_t e = launch_rope_table(r->table, desc->dh, desc->n_phases, desc->base, s);
+  if (e != hipSuccess) {
+    delete r;
+    return hip_fail(e, "rotary table");
+  }
+  *out = r;
+  return SMEM_OK;
+}
+
+smem_status smem_rope_destroy(smem_rope* rope) {
+  delete rope;
   return SMEM_OK;
 }
 

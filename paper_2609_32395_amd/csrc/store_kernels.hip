@@ -199,4 +199,24 @@ hipError_t launch_export(int dtype, const void* pages, const int32_t* live_page_
   return hipGetLastError();
 }
 
+// Rotary table (the SMem+RoPE composite): entry (p, k) = (cos, sin) of
+// p * base^(-2k/dh), evaluated in fp64 and stored as fp32.
+__global__ void __launch_bounds__(256) k_rope_table(float* __restrict__ tab, int dh, int n_phases, double base) {
+  const int half = dh / 2;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_phases * half) return;
+  const int p = i / half, k = i % half;
+  const double ang = (double)p * pow(base, -2.0 * (double)k / (double)dh);
+  double sn, cs;
+  sincos(ang, &sn, &cs);
+  *(f32x2*)(tab + 2 * (size_t)i) = f32x2{(float)cs, (float)sn};
+}
+
+hipError_t launch_rope_table(float* table, int dh, int n_phases, double base, hipStream_t s) {
+  const int n = n_phases * (dh / 2);
+  if (n <= 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_rope_table, dim3((n + 255) / 256), dim3(256), 0, s, table, dh, n_phases, base);
+  return hipGetLastError();
+}
+
 }  // namespace smem

@@ -8,8 +8,10 @@ check buffer sizes itself.
 
 Functions carry the C names: smem_encode_blocks, smem_reencode_blocks,
 smem_reader_prefill_block, smem_reader_decode, smem_delete_block,
-smem_store_put_block, smem_store_export; a store is created and destroyed by
-the Store class.
+smem_store_put_block, smem_store_export, and the rotary variants
+smem_encode_blocks_rope, smem_reader_prefill_block_rope,
+smem_reader_decode_rope; a store is created and destroyed by the Store class,
+a rotary table by the Rope class.
 """
 from __future__ import annotations
 
@@ -47,6 +49,11 @@ class AttnDesc(ctypes.Structure):
     _fields_ = [("b", ctypes.c_int32), ("H", ctypes.c_int32), ("dh", ctypes.c_int32), ("dtype", ctypes.c_int32)]
 
 
+class RopeDesc(ctypes.Structure):
+    _fields_ = [("dh", ctypes.c_int32), ("n_phases", ctypes.c_int32), ("max_offset", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("base", ctypes.c_double)]
+
+
 _lib = None
 _P = ctypes.c_void_p
 _I = ctypes.c_int32
@@ -64,6 +71,12 @@ SIGNATURES = {
     "smem_reader_decode": (_I, [_P, _I, _IP, _IP, _IP, _P, _P, _P, _P, _P, _P, _P, _P]),
     "smem_delete_block": (_I, [_P, _I, _I, _I, _P]),
     "smem_store_export": (_I, [_P, _I, _IP, _IP, _P, _P, _P]),
+    "smem_rope_bytes": (ctypes.c_size_t, [ctypes.POINTER(RopeDesc)]),
+    "smem_rope_create": (_I, [ctypes.POINTER(RopeDesc), _P, ctypes.c_size_t, _P, ctypes.POINTER(_P)]),
+    "smem_rope_destroy": (_I, [_P]),
+    "smem_encode_blocks_rope": (_I, [_P, ctypes.POINTER(AttnDesc), _P, _I, _IP, _IP, _P, _P, _P, _P, _I, _P]),
+    "smem_reader_prefill_block_rope": (_I, [_P, _P, _I, _IP, _IP, _P, _P, _P, _P, _P, _P]),
+    "smem_reader_decode_rope": (_I, [_P, _P, _I, _IP, _IP, _IP, _P, _P, _P, _P, _P, _P, _P, _P]),
     "smem_store_stats": (_I, [_P, _IP, _IP]),
     "smem_status_string": (ctypes.c_char_p, [_I]),
     "smem_last_error": (ctypes.c_char_p, []),
@@ -186,6 +199,37 @@ class Store:
         return used.value, free.value
 
 
+class Rope:
+    """Rotary configuration of the SMem+RoPE composite: a table of
+    n_phases phases for heads of width dh in a torch-allocated buffer.
+    max_offset = W > 0 clips block phases to max(j, J - W); 0 does not."""
+
+    def __init__(self, dh, n_phases, base=10000.0, max_offset=0, device="cuda", stream=None):
+        self.dh, self.n_phases, self.base, self.max_offset = dh, n_phases, float(base), int(max_offset)
+        self.desc = RopeDesc(dh, n_phases, int(max_offset), 0, float(base))
+        L = lib()
+        nbytes = L.smem_rope_bytes(ctypes.byref(self.desc))
+        if nbytes == 0:
+            raise SmemError(SMEM_EINVAL, "invalid rotary descriptor")
+        self.buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        handle = ctypes.c_void_p()
+        _check(L.smem_rope_create(ctypes.byref(self.desc), ctypes.c_void_p(self.buf.data_ptr()), nbytes,
+                                  _stream(stream), ctypes.byref(handle)))
+        self.handle = handle
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().smem_rope_destroy(self.handle)
+            self.handle = None
+        self.buf = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 def smem_store_put_block(st: Store, seq: int, block_idx: int, k_rows=None, v_rows=None, stream=None):
     if st.meta_only:
         kp = vp = None
@@ -226,6 +270,14 @@ def smem_encode_blocks(st, q, k, v, out=None, seq_ids=None, block_idx=None, mask
     return _encode(lib().smem_encode_blocks, st, q, k, v, out, seq_ids, block_idx, mask, b, stream)
 
 
+def smem_encode_blocks_rope(st, rope: Rope, q, k, v, out=None, seq_ids=None, block_idx=None, mask=MASK_BIDIR,
+                            b=None, stream=None):
+    """smem_encode_blocks with rotary phases (in-block offsets) on q and k."""
+    fn = lib().smem_encode_blocks_rope
+    return _encode(lambda h, d, *rest: fn(h, d, rope.handle, *rest), st, q, k, v, out, seq_ids, block_idx, mask,
+                   b, stream)
+
+
 def smem_reencode_blocks(st, q, k, v, out=None, seq_ids=None, block_idx=None, mask=MASK_BIDIR, stream=None):
     """Encode present blocks again from new inputs, overwriting their rows in
     place (the slot scheme's re-encode).  Returns out."""
@@ -264,6 +316,16 @@ def _encode(fn, st, q, k, v, out, seq_ids, block_idx, mask, b, stream):
 def smem_reader_prefill_block(st: Store, seq_ids, query_block, q, k_intra=None, v_intra=None, null_kv=None,
                               out=None, stream=None):
     """Reader attention for whole query blocks; q etc. [n*b, H, dh]."""
+    return _prefill(st, None, seq_ids, query_block, q, k_intra, v_intra, null_kv, out, stream)
+
+
+def smem_reader_prefill_block_rope(st: Store, rope: Rope, seq_ids, query_block, q, k_intra=None, v_intra=None,
+                                   null_kv=None, out=None, stream=None):
+    """smem_reader_prefill_block with the composite's rotary phases."""
+    return _prefill(st, rope, seq_ids, query_block, q, k_intra, v_intra, null_kv, out, stream)
+
+
+def _prefill(st, rope, seq_ids, query_block, q, k_intra, v_intra, null_kv, out, stream):
     n = len(seq_ids)
     if len(query_block) != n:
         raise ValueError("query_block needs one entry per sequence")
@@ -275,8 +337,11 @@ def smem_reader_prefill_block(st: Store, seq_ids, query_block, q, k_intra=None, 
     vp = _dev(v_intra, shape, st.dtype, "v_intra")
     np_ = _dev(null_kv, (2, st.H, st.dh), st.dtype, "null_kv")
     op = _dev(out, shape, st.dtype, "out")
-    _check(lib().smem_reader_prefill_block(st.handle, n, _i32(seq_ids), _i32(query_block), qp, kp, vp, np_, op,
-                                           _stream(stream)))
+    rest = (n, _i32(seq_ids), _i32(query_block), qp, kp, vp, np_, op, _stream(stream))
+    if rope is None:
+        _check(lib().smem_reader_prefill_block(st.handle, *rest))
+    else:
+        _check(lib().smem_reader_prefill_block_rope(st.handle, rope.handle, *rest))
     return out
 
 
@@ -284,6 +349,16 @@ def smem_reader_decode(st: Store, seq_ids, query_block, pos, q, k_new=None, v_ne
                        v_cache=None, null_kv=None, out=None, stream=None):
     """Reader attention for one new token per sequence; q etc. [n, H, dh],
     caches [n*b, H, dh] (row pos[i] of sequence row i is written)."""
+    return _decode(st, None, seq_ids, query_block, pos, q, k_new, v_new, k_cache, v_cache, null_kv, out, stream)
+
+
+def smem_reader_decode_rope(st: Store, rope: Rope, seq_ids, query_block, pos, q, k_new=None, v_new=None,
+                            k_cache=None, v_cache=None, null_kv=None, out=None, stream=None):
+    """smem_reader_decode with the composite's rotary phases."""
+    return _decode(st, rope, seq_ids, query_block, pos, q, k_new, v_new, k_cache, v_cache, null_kv, out, stream)
+
+
+def _decode(st, rope, seq_ids, query_block, pos, q, k_new, v_new, k_cache, v_cache, null_kv, out, stream):
     n = len(seq_ids)
     if len(query_block) != n or (pos is not None and len(pos) != n):
         raise ValueError("query_block and pos need one entry per sequence")
@@ -295,5 +370,9 @@ def smem_reader_decode(st: Store, seq_ids, query_block, pos, q, k_new=None, v_ne
             _dev(k_cache, cache, st.dtype, "k_cache"), _dev(v_cache, cache, st.dtype, "v_cache"),
             _dev(null_kv, (2, st.H, st.dh), st.dtype, "null_kv"), _dev(out, tok, st.dtype, "out")]
     pa = _i32(pos) if pos is not None else None
-    _check(lib().smem_reader_decode(st.handle, n, _i32(seq_ids), _i32(query_block), pa, *args, _stream(stream)))
+    rest = (n, _i32(seq_ids), _i32(query_block), pa, *args, _stream(stream))
+    if rope is None:
+        _check(lib().smem_reader_decode(st.handle, *rest))
+    else:
+        _check(lib().smem_reader_decode_rope(st.handle, rope.handle, *rest))
     return out

@@ -136,3 +136,15 @@ def test_store_create_rejects_small_or_misaligned_pool():
     # these checks return before the pool pointer is ever dereferenced
     assert L.smem_store_create(ctypes.byref(d), ctypes.c_void_p(4096), need - 1, None, ctypes.byref(h)) == smem.SMEM_ENOMEM
     assert L.smem_store_create(ctypes.byref(d), ctypes.c_void_p(4096 + 16), need, None, ctypes.byref(h)) == smem.SMEM_EINVAL
+
+
+def test_rope_bytes_and_invalid_descriptors():
+    L = smem.lib()
+    d = smem.RopeDesc(128, 100, 15, 0, 1e4)
+    assert L.smem_rope_bytes(ctypes.byref(d)) == (100 * 128 * 4 + 255) // 256 * 256
+    for bad in [(96, 100, 15, 0, 1e4), (64, 0, 15, 0, 1e4), (64, 10, -1, 0, 1e4), (64, 10, 0, 1, 1e4),
+                (64, 10, 0, 0, 1.0), (64, 10, 0, 0, float("nan")), (64, 10, 0, 0, float("inf"))]:
+        assert L.smem_rope_bytes(ctypes.byref(smem.RopeDesc(*bad))) == 0, bad
+    out = ctypes.c_void_p()
+    assert L.smem_rope_create(ctypes.byref(d), None, 1 << 20, None, ctypes.byref(out)) == smem.SMEM_EINVAL
+    assert not out.value

@@ -111,3 +111,59 @@ def test_prefill_workspace_fits_slot_chunk():
         chunk = min(16, n_seq)
         assert (chunk * b * H) * SPLIT_STRIDE * (dh + 4) <= ws
         assert (min(128, n_seq) * 1 * H) * SPLIT_STRIDE * (dh + 4) <= ws
+
+
+@pytest.mark.parametrize("b,dh,es", SHAPES)
+def test_rope_table_indexing(b, dh, es):
+    """Rotary table reads: row phase * dh, columns 2*k0 + 4m .. +3 per 16-byte read.
+    The host admits a call only when every phase it uses is below n_phases."""
+    E = 16 // es
+    LPR = dh // E
+    for c in range(LPR):                      # VALU reader: lane chunk c, pairs c*E/2 ..
+        k0 = c * (E // 2)
+        assert k0 % 2 == 0 and 2 * k0 + 4 * (E // 4 - 1) + 3 < dh
+    for kk in range(dh // 32):                # MFMA query fragments
+        for g in range(4):
+            k0 = kk * 16 + g * 4
+            assert 2 * k0 + 4 + 3 < dh
+    for c8 in range(dh // 8):                 # MFMA key tile rows
+        assert 2 * (c8 * 4) + 4 + 3 < dh
+    for J, W in [(0, 0), (1, 15), (40, 15), (4096, 0), (4096, 15)]:
+        turn = min(J, W) if W > 0 else J
+        n_phases = max(b - 1, turn) + 1       # smallest table the host admits
+        clip = W if W > 0 else 2 ** 31 - 1
+        for j in {0, max(0, J - 1), max(0, J - W)} if J > 0 else set():
+            if j < J:
+                dlt = min(J - j, clip)
+                assert 1 <= dlt < n_phases
+        assert min(J, clip) < n_phases and b - 1 < n_phases
+        assert (n_phases - 1) * dh + dh - 1 < n_phases * dh
+
+
+@pytest.mark.parametrize("dh", [32, 64, 128])
+def test_rope_prefill_lds_rows(dh):
+    """Rotary prefill split: turns of its pages (ascending block index) fall
+    monotonically, so every page's turn lies in [d_lo, d_hi]; the LDS copy of
+    rows d_lo..d_hi (taken when it has fewer than 24 rows) fits its array and
+    reads inside the table; query fragments fit their LDS copy."""
+    ROWS = 24
+    rng = __import__("random").Random(dh)
+    for _ in range(200):
+        J = rng.randint(1, 5000)
+        W = rng.choice([0, 1, 3, 15, 31, 100])
+        clip = W if W > 0 else 2 ** 31 - 1
+        blocks = sorted(rng.sample(range(J), min(J, rng.randint(1, 40))))
+        n_phases = max(63, min(J, W) if W > 0 else J) + 1
+        d = [min(J - j, clip) for j in blocks]
+        assert d == sorted(d, reverse=True)
+        d_hi, d_lo = d[0], d[-1]
+        assert all(d_lo <= x <= d_hi for x in d) and d_hi < n_phases
+        if d_hi - d_lo < ROWS:
+            n4 = (d_hi - d_lo + 1) * dh // 4
+            assert n4 * 4 <= ROWS * dh
+            assert d_lo * dh + n4 * 4 <= n_phases * dh
+            assert all((x - d_lo) * dh + dh <= ROWS * dh for x in d)
+    assert ((dh // 32 - 1) * 4 + 3) * 64 + 63 < (dh // 32) * 4 * 64
+    # LDS per workgroup: tiles + rows + query copy stay within 64 KiB
+    tiles = (64 * (dh + 8) + dh * (64 + 4)) * 2
+    assert tiles + ROWS * dh * 4 + (dh // 32) * 4 * 64 * 16 <= 64 * 1024
