@@ -20,6 +20,8 @@ Secondary workloads, timed in the same run and reported under "secondary":
   * 410M-shaped streaming decode: the headline shape decoding 128 tokens
     from a fresh block, appending each completed block (64 blocks per
     append, encoder attention + insert) as the stream crosses a boundary;
+  * 410M-shaped decode from the row plane (rows of width 1024 shared by all
+    layers; one layer's key/value maps folded into the query and output);
   * the SMem+RoPE composite (saturating block phases, W = 15) timed on the
     headline decode and on the 1.5B serve, beside the base reads;
   * 1.5B-shaped stress: 16 sequences x 4096 blocks (262144 rows each, a
@@ -320,6 +322,49 @@ def stream_workload(args, torch, smem, synth):
                 ms_per_step=secs / T * 1e3, append_ms_median=float(np.median(app)) * 1e3)
 
 
+def rows_workload(args, torch, smem, synth):
+    """410M-shaped decode from the row plane: 64 sequences x 64 blocks of 64
+    rows of width d = 1024 (one plane shared by all layers), one layer's maps
+    (16 heads x dh 64), one token per sequence per step with 1-64 in-block
+    keys; timed like the headline."""
+    w = synth.DEC_410M
+    S, H, dh, b, NB = w.n_seq, w.H, w.dh, w.b, w.n_blocks
+    d = H * dh
+    dt = torch.bfloat16
+    st = smem.RowStore(S, NB + 1, S * NB, b, d)
+    g = torch.Generator(device="cuda")
+    for s in range(S):
+        g.manual_seed(synth.block_seed(args.seed, w.wid, synth.ROLE_KMEM, s, 0, 1))
+        R = torch.randn((NB, b, d), generator=g, device="cuda").to(dt)
+        for j in range(NB):
+            smem.smem_rows_put_block(st, s, j, R[j])
+    g.manual_seed(synth.block_seed(args.seed, w.wid, synth.ROLE_QDEC, 2, 0, 0))
+    wk = (torch.randn((H * dh, d), generator=g, device="cuda") / d ** 0.5).to(dt)
+    wv = (torch.randn((H * dh, d), generator=g, device="cuda") / d ** 0.5).to(dt)
+    n_draw = 64
+    X = (torch.randn((3, n_draw, S, H, dh), generator=g, device="cuda") * w.scale).to(dt)
+    kc = (torch.randn((S * b, H, dh), generator=g, device="cuda") * w.scale).to(dt)
+    vc = torch.empty_like(kc).copy_(kc)
+    p0 = synth.decode_positions(w, args.seed, S)
+    out = torch.empty((S, H, dh), dtype=dt, device="cuda")
+    seqs = list(range(S))
+    qblk = [NB] * S
+    stream = torch.cuda.current_stream()
+
+    def step(t):
+        i = t % n_draw
+        pos = [int((p0[s] + t) % b) for s in range(S)]
+        smem.smem_reader_decode_rows(st, wk, wv, seqs, qblk, pos, X[0, i], X[1, i], X[2, i], kc, vc, None, out)
+
+    for t in range(args.warmup):
+        step(t)
+    secs = _events_time(step, args.steps, stream)
+    row_bytes = S * NB * b * d * 2
+    st.close()
+    return dict(tokens_per_s=S * args.steps / secs, ms_per_step=secs / args.steps * 1e3, d=d,
+                row_bytes_per_step=row_bytes, row_gbs=row_bytes / (secs / args.steps) / 1e9)
+
+
 def stress_workload(args, torch, smem, synth):
     """1.5B-shaped stress: 16 sequences x 4096 blocks (262144 rows, 32 GiB);
     batch-16 decode over all rows, and single-block delete / re-insert latency."""
@@ -413,9 +458,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-secondary", action="store_true")
-    ap.add_argument("--workloads", default="encode,serve,stream,stress,rope",
-                    help="secondary workloads to run (comma list of encode, serve, stream, stress, rope: the "
-                         "rotary composite timed beside the headline decode and the serve)")
+    ap.add_argument("--workloads", default="encode,serve,stream,rows,stress,rope",
+                    help="secondary workloads to run (comma list of encode, serve, stream, rows, stress, rope: "
+                         "the rotary composite timed beside the headline decode and the serve)")
     ap.add_argument("--no-headline", action="store_true",
                     help="profiling runs only: skip the decode headline (value is then null)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -450,6 +495,8 @@ def main():
             secondary["serve_1p5B"] = serve_workload(args, torch, smem, synth)
         if "stream" in wl:
             secondary["stream_410M"] = stream_workload(args, torch, smem, synth)
+        if "rows" in wl:
+            secondary["rows_decode_410M"] = rows_workload(args, torch, smem, synth)
         if dec is not None and dec.get("rope"):
             secondary["rope_decode_410M"] = dec["rope"]
         if "stress" in wl:

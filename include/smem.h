@@ -247,6 +247,70 @@ smem_status smem_reader_decode_rope(smem_store* st, const smem_rope* rope, int32
                                     const void* q, const void* k_new, const void* v_new, void* k_cache,
                                     void* v_cache, const void* null_kv, void* out, hipStream_t s);
 
+/* ------------------------------------------------------------------------
+ * Row stores: decode from the memory rows (Appendix K, recomputing K/V from
+ * the memory rows instead of storing it; Appendix A, "Positions and memory":
+ * one row plane is shared by all D reader layers, and each layer applies its
+ * own key and value maps, the null row included).
+ * A row store is an smem_store whose pages hold one block's b rows of width
+ * d (bf16), no key/value planes.  smem_store_destroy, smem_store_stats and
+ * smem_delete_block apply to it; the key/value calls (put_block, export,
+ * encode into it, prefill, decode) return SMEM_EINVAL, and the row calls
+ * return SMEM_EINVAL on a key/value store.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t n_seq;
+  int32_t max_blocks;
+  int32_t n_pages;
+  int32_t b;          /* 16 or 64 */
+  int32_t d;          /* row width: 512, 1024 or 2048 */
+  int32_t dtype;      /* SMEM_BF16 */
+} smem_rows_desc;
+
+/* One reader layer's maps, device bf16: w_k, w_v [H*dh, d] (a linear
+ * layer's out x in layout: the key of row r is w_k r, head h taking outputs
+ * h*dh .. h*dh+dh-1), null_row [d] or NULL.  1 <= H <= 16, dh in
+ * {32, 64, 128}. */
+typedef struct {
+  int32_t H;
+  int32_t dh;
+  const void* w_k;
+  const void* w_v;
+  const void* null_row;
+} smem_rows_layer;
+
+/* Device bytes of a row store: pages, block table, live lists and the
+ * decode workspace.  0 for an invalid descriptor. */
+size_t smem_rows_bytes(const smem_rows_desc* desc);
+
+/* Create a row store over a caller-owned device buffer (256-byte aligned,
+ * >= smem_rows_bytes); metadata initialised on stream s. */
+smem_status smem_rows_create(const smem_rows_desc* desc, void* dev_pool, size_t pool_bytes, hipStream_t s,
+                             smem_store** out);
+
+/* Insert the rows [b, d] of block block_idx of sequence seq (device, copied
+ * into a free page).  Errors as smem_store_put_block. */
+smem_status smem_rows_put_block(smem_store* st, int32_t seq, int32_t block_idx, const void* rows, hipStream_t s);
+
+/* Canonical export of one sequence's rows: live_idx as in smem_store_export,
+ * rows_out device [n_live*b, d] or NULL. */
+smem_status smem_rows_export(smem_store* st, int32_t seq, int32_t* live_idx, int32_t* n_live, void* rows_out,
+                             hipStream_t s);
+
+/* Reader decode of one layer from the row plane: the same read as
+ * smem_reader_decode with every memory row's key and value given by the
+ * layer's maps (k = w_k row, v = w_v row, per head slice) and the null row
+ * (if any) mapped the same way.  The maps are never applied row by row: the
+ * query is mapped into row space (w_k^h q), rows are weighted there, and the
+ * weighted row sum is mapped back once (w_v^h), which is the same
+ * arithmetic up to rounding.  q, k_new, v_new, out: [n_seq, H, dh];
+ * k_cache, v_cache: [n_seq*b, H, dh] or all four NULL; pos as in
+ * smem_reader_decode.  bf16. */
+smem_status smem_reader_decode_rows(smem_store* st, const smem_rows_layer* layer, int32_t n_seq,
+                                    const int32_t* seq_ids, const int32_t* query_block, const int32_t* pos,
+                                    const void* q, const void* k_new, const void* v_new, void* k_cache,
+                                    void* v_cache, void* out, hipStream_t s);
+
 /* Host-side facts about a store: pages in use and free. */
 smem_status smem_store_stats(const smem_store* st, int32_t* pages_used, int32_t* pages_free);
 

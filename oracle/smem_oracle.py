@@ -28,6 +28,9 @@ float64, with no blocking, tiling, online softmax or split reduction:
 * Decode: the same read for one query at position p, after the new key/value
   pair is written into the in-block cache at p.  Streamed decode appends each
   block to the memory once its last token is decoded.
+* Decode from the row plane (Appendix K; Appendix A, "Positions and
+  memory"): keys and values recomputed from the shared rows by the layer's
+  maps, then the same read.
 * SMem+RoPE composite (Section 3; the composite's appendix, variant v2):
   rotary phases on queries and keys only -- in-block offsets inside the
   block, block indices (0 for the null row) across blocks, key phases
@@ -336,6 +339,35 @@ def slot_indices(n_blocks: int, B: int):
     at most B blocks, block j (0-based) has slot j + 1; beyond that the most
     recent B blocks have slots 1..B in order and every older block slot 1."""
     return [max(1, j - n_blocks + B + 1) if n_blocks > B else j + 1 for j in range(n_blocks)]
+
+
+# ---------------------------------------------------------------- decode from the row plane
+# Appendix K (recomputing K/V from the memory rows instead of storing it) and
+# Appendix A ("Positions and memory"): one plane of rows per block, shared by
+# all reader layers; a layer's keys and values are the rows through that
+# layer's key and value maps, the null row a d-vector mapped the same way.
+
+
+def reader_decode_rows(rows_store: Store, w_k, w_v, null_row, seq_ids, query_block, pos, q,
+                       k_new=None, v_new=None, k_cache=None, v_cache=None):
+    """Recompute the keys and values from the rows, then read as reader_decode.
+
+    rows_store: a Store of shape (b, 1, d) whose entries hold the rows as
+    the key element of each pair; w_k, w_v: [H*dh, d] (the key of row r is
+    w_k r); null_row [d] or None; q etc. as in reader_decode.  Returns
+    (out, k_cache, v_cache)."""
+    q = _f64(q)
+    n, H, dh = q.shape
+    w_k, w_v = _f64(w_k), _f64(w_v)
+    kv = Store(rows_store.n_seq, rows_store.max_blocks, rows_store.b, H, dh)
+    for (s, j), (R, _) in rows_store.rows.items():
+        R = _f64(R).reshape(rows_store.b, rows_store.dh)
+        kv.put(s, j, (R @ w_k.T).reshape(R.shape[0], H, dh), (R @ w_v.T).reshape(R.shape[0], H, dh))
+    nkv = None
+    if null_row is not None:
+        nr = _f64(null_row)
+        nkv = np.stack([(w_k @ nr).reshape(H, dh), (w_v @ nr).reshape(H, dh)])
+    return reader_decode(kv, seq_ids, query_block, pos, q, k_new, v_new, k_cache, v_cache, nkv)
 
 
 # ---------------------------------------------------------------- SMem+RoPE composite

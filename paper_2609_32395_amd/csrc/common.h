@@ -30,6 +30,11 @@ constexpr int kMinPagesPrefill = 4;
 constexpr int kSplitCapPrefill = 32;
 // Query slots whose prefill partials the workspace must hold at once.
 constexpr int kPrefillSlotChunk = 16;
+// Row-plane decode: pages per split max(kMinPagesRows, ceil(n_read /
+// kRowsSplitCap)), and at most kRowsPartials split partials per launch.
+constexpr int kMinPagesRows = 8;
+constexpr int kRowsSplitCap = 32;
+constexpr int kRowsPartials = 1024;
 
 // Pages per split: a function of the number of memory pages read only, so a
 // query's split boundaries (and hence its rounding) never depend on the
@@ -132,6 +137,10 @@ __host__ __device__ inline size_t page_head_offset(int page, int h, int H, int b
 struct DevLayout {
   size_t off_table, off_live_page, off_live_blk, off_n_live, off_ws, off_pages, total;
   size_t ws_floats;    // split partials
+  // row stores only: absorbed queries, in-block partials, projected null row,
+  // row-split partials (part_cap of them)
+  size_t off_qabs, off_intra, off_null_kv, off_sw, off_part;
+  int32_t part_cap;
 };
 
 // ---------------------------------------------------------------- kernel args
@@ -170,6 +179,42 @@ struct ReaderArgs {
   const int32_t* live_blk;    // [n_seq][max_blocks] dense live list -> block index
   int32_t rope_clip;          // W: a block-j key read from block J is turned by min(J - j, W)
   int32_t qblk[kMaxSlots];    // query block J of the slot
+  int32_t intra_partial;      // 1: the in-block / null split always writes a compact partial
+                              //    ws[(qs*H + h)*(dh+4)] (row-plane decode merges it)
+};
+
+// Row-plane decode (bf16): rows of width d, absorbed queries, split partials.
+struct RowsArgs {
+  const uint16_t* pages;      // row pages [n_pages][b][d]
+  const int32_t* live_page;   // [n_seq][max_blocks]
+  const uint16_t* qabs;       // absorbed queries [slot][16][d]
+  float* part;                // split partials: U[16][d], m[16], l[16]
+  const float* intra;         // in-block / null partials [slot][H][dh+4]
+  const uint16_t* w_v;        // value map [H*dh][d]
+  uint16_t* ubuf;             // combined weighted rows [slot][16][d] (bf16)
+  float* sw;                  // in-block weight / L per [slot][16]
+  uint16_t* out;              // [slot][H][dh]
+  int32_t max_blocks;
+  int32_t b;
+  int32_t H;
+  int32_t n_slots;
+  int32_t seq[kMaxSlots];
+  int32_t n_read[kMaxSlots];
+  int32_t pps[kMaxSlots];
+  int32_t pbase[kMaxSlots];   // first partial of the slot
+};
+
+struct RowsPrepArgs {
+  const uint16_t* q;          // [slot][H][dh]
+  const uint16_t* w_k;        // key map [H*dh][d]
+  const uint16_t* w_v;
+  const uint16_t* null_row;   // [d] or NULL
+  uint16_t* qabs;             // [slot][16][d]
+  uint16_t* null_kv;          // [2][H][dh]
+  int32_t d;
+  int32_t H;
+  int32_t n_slots;
+  float scale_log2;
 };
 
 struct MetaArgs {
@@ -192,7 +237,7 @@ hipError_t launch_init_meta(int32_t* table, int32_t* n_live, size_t n_table, int
 hipError_t launch_meta(const MetaArgs& a, hipStream_t s);
 hipError_t launch_put_rows(int dtype, void* pages, int page, int H, int b, int dh,
                            const void* k_rows, const void* v_rows, hipStream_t s);
-hipError_t launch_scrub(int dtype, void* pages, int page, int H, int b, int dh, hipStream_t s);
+hipError_t launch_scrub(void* page_base, size_t bytes, hipStream_t s);
 hipError_t launch_export(int dtype, const void* pages, const int32_t* live_page_seq, int n_live,
                          int H, int b, int dh, void* k_out, void* v_out, hipStream_t s);
 
@@ -206,6 +251,11 @@ hipError_t launch_encoder_mfma(int b, int dh, const void* q, const void* k, cons
                                void* pages, const int32_t* sink_pages, int n_blocks, int H, int mask,
                                float scale_log2, const float* rope, hipStream_t s);
 hipError_t launch_prefill_mfma(int b, int dh, const ReaderArgs& a, hipStream_t s);
+// Row-plane decode: stage 0 = absorbed queries (+ null row projection),
+// stage 1 = row reader + merge.
+hipError_t launch_rows(int d, int dh, const RowsArgs& a, const RowsPrepArgs& pa, int stage, hipStream_t s);
+// Plain device copy (16-byte multiples).
+hipError_t launch_copy16(void* dst, const void* src, size_t bytes, hipStream_t s);
 // Rotary table of n_phases rows for heads of width dh, computed in fp64.
 hipError_t launch_rope_table(float* table, int dh, int n_phases, double base, hipStream_t s);
 

@@ -277,7 +277,7 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
       L += wgt * wl[w];
       A += wgt * wacc[w][tid];
     }
-    if (nms == 0) {
+    if (nms == 0 && !a.intra_partial) {
       const float o = (L > 0.f) ? A / L : 0.f;
       const T ov = from_f32<T>(o);
       ((T*)a.out)[((size_t)qs * a.H + h) * DH + tid] = ov;
@@ -287,7 +287,8 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
         kp[B * DH + tid * B + t] = ov;
       }
     } else {
-      float* part = a.ws + (((size_t)qs * a.H + h) * kSplitStride + split) * (DH + 4);
+      float* part = a.intra_partial ? a.ws + ((size_t)qs * a.H + h) * (DH + 4)
+                                    : a.ws + (((size_t)qs * a.H + h) * kSplitStride + split) * (DH + 4);
       part[tid] = A;
       if (tid == 0) { part[DH] = M; part[DH + 1] = L; }
     }

@@ -1,0 +1,414 @@
+// Decode from the memory rows themselves (Appendix K, recomputing K/V from
+// the memory rows; Appendix A, "Positions and memory": the rows are shared by
+// all D reader layers, each layer projecting them with its own key and value
+// maps).
+//
+// A row store page holds one block's b rows of width d.  Instead of forming
+// K = mu W_K and V = mu W_V for every row read, the projections are folded
+// into the query and the output (both exact identities):
+//   score(q_h, row r) = <q_h, W_K^h^T mu_r> = <W_K^h q_h, mu_r>
+//   sum_r a_r W_V^h^T mu_r = W_V^h^T (sum_r a_r mu_r)
+// so the reader streams each row once for all heads: per 16-row chunk,
+// S = Q' mu^T (heads x rows, MFMA over d) and U += P mu (heads x d, MFMA over
+// the rows), with an online softmax per head.  The merge combines the splits'
+// U in split order, applies W_V^h once per (query, head) and adds the
+// in-block / null-row partial (dh-wide, from the VALU reader).
+#include "common.h"
+
+namespace smem {
+
+typedef __bf16 bf16x8r __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kRowChunk = 16;     // rows per chunk (one MFMA column tile)
+
+// Chunks stream global -> LDS by DMA (global_load_lds, 16 bytes per lane)
+// through a ring of NS stages, so no register holds them in transit.
+#ifndef SMEM_ROWS_STAGES
+#define SMEM_ROWS_STAGES 2
+#endif
+template <int D>
+struct RowsCfg {
+  static constexpr int MP = D + 8;                 // LDS row pitch (elements): 16-byte pad per row
+  // ring stages (LDS: NS * 16 rows * MP * 2 bytes; at most 2 at d = 2048)
+  static constexpr int NS = D >= 2048 ? 2 : SMEM_ROWS_STAGES;
+  static constexpr int KW = kRowChunk * D / 512 / 4;   // 1 KiB DMA instructions per wave per chunk
+  static constexpr int DW = D / 4;                 // dims per wave (score reduction, U ownership)
+  static constexpr int NT = DW / 16;               // U tiles per wave
+};
+
+template <int D>
+struct RowsLds {
+  uint16_t mu[RowsCfg<D>::NS][kRowChunk * RowsCfg<D>::MP];
+  float sred[4][256];                       // per-wave partial scores
+  uint16_t p[16 * 16];                      // P[head][row], bf16
+  float alpha[16];
+  int rescale;                              // some head's reference maximum moved this chunk
+};
+
+// Lazy rescaling: a head's reference maximum moves only when a score exceeds
+// it by more than kLazy (log2 units), so P <= 2^kLazy and the accumulated U
+// needs rescaling only in those chunks.  Every weight and U share the
+// reference, so the result is the same up to rounding.
+constexpr float kLazy = 8.f;
+
+// s_waitcnt with only the vector-memory counter limited to n (0..63).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
+
+// One 16-byte-per-lane global -> LDS load: lane l's 16 bytes land at LDS
+// byte address lds + 16*l (M0 holds the uniform base).  Issued as assembly
+// so that the compiler does not tie later LDS reads or barriers to it with a
+// full vector-memory wait; completion is waited for explicitly (wait_vm).
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(lds) : "memory", "m0");
+}
+
+// Barrier for LDS hand-offs between waves: this wave's LDS writes complete
+// (lgkmcnt 0), then s_barrier; vector-memory loads (the DMA ring) stay in
+// flight.  The empty asm statements keep the compiler from moving memory
+// operations across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" : : : "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // vmcnt 63, expcnt 7, lgkmcnt 0
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" : : : "memory");
+}
+
+// Wave `wave` moves rows 4*wave .. 4*wave+3 of chunk c into stage st: each
+// row is D*2 bytes = D/512 DMA instructions of 1 KiB.
+template <int D>
+__device__ __forceinline__ void chunk_dma(RowsLds<D>& L, int st, const uint16_t* __restrict__ src, int wave,
+                                          int lane) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int row = wave * 4 + r;
+#pragma unroll
+    for (int hk = 0; hk < D / 512; ++hk) {
+      const uint16_t* g = src + (size_t)row * D + hk * 512 + lane * 8;
+      const uint32_t l = (uint32_t)(uintptr_t)&L.mu[st][row * RowsCfg<D>::MP + hk * 512];
+      dma16(g, __builtin_amdgcn_readfirstlane(l));
+    }
+  }
+}
+
+// Wait until this wave's DMA for the current chunk is done, with `ahead`
+// later chunks (0 .. NS-1) allowed to stay in flight.
+template <int D>
+__device__ __forceinline__ void wait_chunk(int ahead) {
+  constexpr int K = RowsCfg<D>::KW;
+  if (ahead >= 3) wait_vm<(3 * K < 63 ? 3 * K : 63)>();
+  else if (ahead == 2) wait_vm<2 * K>();
+  else if (ahead == 1) wait_vm<K>();
+  else wait_vm<0>();
+}
+
+// One workgroup per (sequence slot, split).  Wave w reduces dims
+// [w*D/4, (w+1)*D/4) of the scores and owns the same dims of U.
+template <int D>
+__global__ void __launch_bounds__(256) k_reader_rows(RowsArgs a) {
+  using C = RowsCfg<D>;
+  __shared__ RowsLds<D> L;
+  const int split = blockIdx.x, slot = blockIdx.y;
+  const int n_read = a.n_read[slot], pps = a.pps[slot];
+  const int nsp = (n_read + pps - 1) / pps;
+  if (split >= nsp) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int MP = C::MP, DW = C::DW, NT = C::NT, NS = C::NS;
+  const int b = a.b;
+
+  // absorbed-query fragments of this wave's dims stay in registers (A operand)
+  u32x4 qa[DW / 32];
+  {
+    const uint16_t* qs = a.qabs + ((size_t)slot * 16 + (lane & 15)) * D + wave * DW + (lane >> 4) * 8;
+#pragma unroll
+    for (int kk = 0; kk < DW / 32; ++kk) qa[kk] = *(const u32x4*)(qs + kk * 32);
+  }
+  // softmax role of this thread: (head, row) of one score
+  const int sl = tid >> 2, si = tid & 3;
+  const int s_head = 4 * (sl >> 4) + si, s_row = sl & 15;
+  float m_h = -INFINITY, l_h = 0.f;
+  f32x4 u[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) u[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int p0 = split * pps, p1 = min(n_read, p0 + pps);
+  const int cpp = b / kRowChunk;            // chunks per page
+  const int n_chunks = (p1 - p0) * cpp;
+  // The live list is read-only while a reader runs: reading it through the
+  // constant address space keeps each lookup a scalar load (a vector load
+  // would be waited for together with the chunk DMA in flight).
+  const __attribute__((address_space(4))) int32_t* lpc =
+      (const __attribute__((address_space(4))) int32_t*)(a.live_page + (size_t)a.seq[slot] * a.max_blocks);
+  auto chunk_src = [&](int c) {
+    const int pg = lpc[p0 + c / cpp];
+    return a.pages + ((size_t)pg * b + (size_t)(c % cpp) * kRowChunk) * D;
+  };
+  wait_vm<0>();                             // the query fragments
+#pragma unroll
+  for (int c = 0; c < NS - 1; ++c)
+    if (c < n_chunks) chunk_dma<D>(L, c, chunk_src(c), wave, lane);
+
+  for (int c = 0; c < n_chunks; ++c) {
+    const int st = c % NS;
+    lds_barrier();                        // every wave is done with chunk c-1 (its stage, sred, p)
+    const int nxt = c + NS - 1;
+    if (nxt < n_chunks) chunk_dma<D>(L, nxt % NS, chunk_src(nxt), wave, lane);
+    wait_chunk<D>(min(NS - 1, n_chunks - 1 - c));
+    lds_barrier();                        // chunk c is in LDS for every wave
+    // S partial over this wave's dims: D[m = head][n = row]
+    const uint16_t* mu = L.mu[st];
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < DW / 32; kk += 2) {
+      const int k0 = wave * DW + kk * 32 + (lane >> 4) * 8;
+      const u32x4 m0 = *(const u32x4*)&mu[(lane & 15) * MP + k0];
+      const u32x4 m1 = *(const u32x4*)&mu[(lane & 15) * MP + k0 + 32];
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8r, qa[kk]),
+                                                   __builtin_bit_cast(bf16x8r, m0), s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8r, qa[kk + 1]),
+                                                   __builtin_bit_cast(bf16x8r, m1), s1, 0, 0, 0);
+    }
+    *(f32x4*)&L.sred[wave][lane * 4] = s0 + s1;
+    if (tid == 0) L.rescale = 0;
+    lds_barrier();
+    // online softmax per head over the chunk's 16 rows, lazily rescaled
+    {
+      const float x = L.sred[0][tid] + L.sred[1][tid] + L.sred[2][tid] + L.sred[3][tid];
+      float mx = x;
+      mx = fmaxf(mx, __shfl_xor(mx, 4));
+      mx = fmaxf(mx, __shfl_xor(mx, 8));
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      float al = 1.f;
+      if (mx > m_h + kLazy) {               // the same for the 16 threads of a head
+        al = exp2w(m_h - mx);
+        m_h = mx;
+        if (s_row == 0) L.rescale = 1;
+      }
+      const float p = exp2w(x - m_h);
+      float ps = p;
+      ps += __shfl_xor(ps, 4);
+      ps += __shfl_xor(ps, 8);
+      ps += __shfl_xor(ps, 16);
+      ps += __shfl_xor(ps, 32);
+      l_h = l_h * al + ps;
+      L.p[s_head * 16 + s_row] = f32_to_bf16_bits(p);
+      if (s_row == 0) L.alpha[s_head] = al;
+    }
+    lds_barrier();
+    // U = U * alpha + P mu over this wave's dims
+    {
+      if (L.rescale) {
+        float al4[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) al4[i] = L.alpha[4 * (lane >> 4) + i];
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) u[n][i] *= al4[i];
+        }
+      }
+      const u32x2 pa = *(const u32x2*)&L.p[(lane & 15) * 16 + (lane >> 4) * 4];
+      const s16x4 A = __builtin_bit_cast(s16x4, pa);
+      const int rbase = (lane >> 4) * 4;
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        const int dim = wave * DW + n * 16 + (lane & 15);
+        s16x4 B;
+        B[0] = (short)mu[(rbase + 0) * MP + dim];
+        B[1] = (short)mu[(rbase + 1) * MP + dim];
+        B[2] = (short)mu[(rbase + 2) * MP + dim];
+        B[3] = (short)mu[(rbase + 3) * MP + dim];
+        u[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(A, B, u[n], 0, 0, 0);
+      }
+    }
+  }
+  // partial: U[16][D], then m[16], l[16]
+  float* part = a.part + (size_t)(a.pbase[slot] + split) * (16 * D + 32);
+#pragma unroll
+  for (int n = 0; n < NT; ++n) {
+    const int dim = wave * DW + n * 16 + (lane & 15);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) part[(size_t)(4 * (lane >> 4) + i) * D + dim] = u[n][i];
+  }
+  if (s_row == 0) {
+    part[16 * D + s_head] = m_h;
+    part[16 * D + 16 + s_head] = l_h;
+  }
+}
+
+// Absorbed queries: qabs[slot][h][c] = scale_log2 * sum_j W_K[h*dh + j][c] q[slot][h][j]
+// (bf16; zero rows for heads h >= H).  The maps are [H*dh][d] (a linear
+// layer's out x in layout), so a thread per c reads them coalesced; a
+// workgroup serves kAbsorbSlots query slots, the j loop unrolled so several
+// map loads are in flight.
+constexpr int kAbsorbSlots = 4;
+template <int DHq>
+__global__ void __launch_bounds__(256) k_rows_absorb_q(RowsPrepArgs a) {
+  const int c = blockIdx.x * 256 + threadIdx.x, h = blockIdx.y, s0 = blockIdx.z * kAbsorbSlots;
+  const int ns = min(kAbsorbSlots, a.n_slots - s0);
+  __shared__ float qs[kAbsorbSlots][DHq];
+  if (h < a.H) {
+    for (int e = threadIdx.x; e < kAbsorbSlots * DHq; e += 256) {
+      const int sl = e / DHq, j = e % DHq;
+      qs[sl][j] = sl < ns ? bf16_bits_to_f32(a.q[((size_t)(s0 + sl) * a.H + h) * DHq + j]) : 0.f;
+    }
+  }
+  __syncthreads();
+  if (c >= a.d) return;
+  float acc[kAbsorbSlots];
+#pragma unroll
+  for (int sl = 0; sl < kAbsorbSlots; ++sl) acc[sl] = 0.f;
+  if (h < a.H) {
+    const uint16_t* w = a.w_k + (size_t)h * DHq * a.d + c;
+#pragma unroll 8
+    for (int j = 0; j < DHq; ++j) {
+      const float wj = bf16_bits_to_f32(w[(size_t)j * a.d]);
+#pragma unroll
+      for (int sl = 0; sl < kAbsorbSlots; ++sl) acc[sl] += wj * qs[sl][j];
+    }
+  }
+#pragma unroll
+  for (int sl = 0; sl < kAbsorbSlots; ++sl)
+    if (sl < ns) a.qabs[((size_t)(s0 + sl) * 16 + h) * a.d + c] = f32_to_bf16_bits(acc[sl] * a.scale_log2);
+}
+
+// The null row through each head's key and value maps:
+// null_kv[m][h][j] = sum_c row[c] W_m[h*dh + j][c].  One workgroup per
+// (head, map); each wave takes every fourth j, its lanes split the sum over c.
+template <int DHq>
+__global__ void __launch_bounds__(256) k_rows_null(RowsPrepArgs a) {
+  const int h = blockIdx.x, which = blockIdx.y;
+  const uint16_t* w = which == 0 ? a.w_k : a.w_v;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int j = wave; j < DHq; j += 4) {
+    const uint16_t* wr = w + ((size_t)h * DHq + j) * a.d;
+    float acc = 0.f;
+    for (int c = lane; c < a.d; c += 64) acc += bf16_bits_to_f32(a.null_row[c]) * bf16_bits_to_f32(wr[c]);
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) acc += __shfl_xor(acc, o);
+    if (lane == 0) a.null_kv[((size_t)which * a.H + h) * DHq + j] = f32_to_bf16_bits(acc);
+  }
+}
+
+// Combine the row splits of one (slot, head) in split order with the
+// in-block / null partial's statistics: u = sum_k w_k U_k / L (bf16, into
+// ubuf) and the in-block weight w_i / L (into sw).
+template <int D, int DHq>
+__global__ void __launch_bounds__(256) k_rows_combine(RowsArgs a) {
+  const int slot = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+  const int n_read = a.n_read[slot], pps = a.pps[slot];
+  const int nsp = n_read > 0 ? (n_read + pps - 1) / pps : 0;
+  __shared__ float w_sh[kRowsSplitCap];
+  __shared__ float inv_sh;
+  const float* ip = a.intra + ((size_t)slot * a.H + h) * (DHq + 4);
+  const float* pb = a.part + (size_t)a.pbase[slot] * (16 * D + 32);
+  if (tid < 64) {
+    // split statistics in parallel, the sums in split order by lane 0
+    const float mk = tid < nsp ? pb[(size_t)tid * (16 * D + 32) + 16 * D + h] : -INFINITY;
+    float M = fmaxf(mk, ip[DHq]);
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) M = fmaxf(M, __shfl_xor(M, o));
+    const float wk = (tid < nsp && mk != -INFINITY) ? exp2w(mk - M) : 0.f;
+    if (tid < nsp) w_sh[tid] = wk;
+    if (tid == 0) {
+      float L = 0.f;
+      for (int k = 0; k < nsp; ++k) L += w_sh[k] * pb[(size_t)k * (16 * D + 32) + 16 * D + 16 + h];
+      const float wi = (ip[DHq] == -INFINITY) ? 0.f : exp2w(ip[DHq] - M);
+      L += wi * ip[DHq + 1];
+      const float inv = (L > 0.f) ? 1.f / L : 0.f;
+      inv_sh = inv;
+      a.sw[(size_t)slot * 16 + h] = wi * inv;
+    }
+  }
+  __syncthreads();
+  const float inv = inv_sh;
+  for (int c = tid; c < D; c += 256) {
+    float x = 0.f;
+    for (int k = 0; k < nsp; ++k) x += w_sh[k] * pb[(size_t)k * (16 * D + 32) + (size_t)h * D + c];
+    a.ubuf[((size_t)slot * 16 + h) * D + c] = f32_to_bf16_bits(x * inv);
+  }
+}
+
+// out[s][h][j] = sum_c u[s][h][c] W_V[h*dh + j][c] + (w_i/L)[s][h] acc_i[s][h][j]:
+// per head a (slots x d) x (d x dh) product on MFMA, one 16 x 16 tile per
+// workgroup, its four waves splitting d (A: u rows, B: W_V rows, both
+// contiguous in c), partial tiles summed in LDS.
+template <int D, int DHq>
+__global__ void __launch_bounds__(256) k_rows_project(RowsArgs a) {
+  const int h = blockIdx.x, s0 = blockIdx.y * 16, j0 = blockIdx.z * 16;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int srow = s0 + (lane & 15);
+  const bool valid = srow < a.n_slots;
+  const uint16_t* ua = a.ubuf + ((size_t)(valid ? srow : 0) * 16 + h) * D + (lane >> 4) * 8;
+  const uint16_t* wb = a.w_v + ((size_t)h * DHq + j0 + (lane & 15)) * D + (lane >> 4) * 8;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int k0 = wave * (D / 4); k0 < (wave + 1) * (D / 4); k0 += 32) {
+    u32x4 av = *(const u32x4*)(ua + k0);
+    if (!valid) av = u32x4{0u, 0u, 0u, 0u};
+    const u32x4 bv = *(const u32x4*)(wb + k0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8r, av), __builtin_bit_cast(bf16x8r, bv),
+                                                  acc, 0, 0, 0);
+  }
+  __shared__ f32x4 red[4][64];
+  red[wave][lane] = acc;
+  __syncthreads();
+  if (wave != 0) return;
+  acc = red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane];
+  const int j = j0 + (lane & 15);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int s = s0 + 4 * (lane >> 4) + i;
+    if (s < a.n_slots) {
+      const float* ip = a.intra + ((size_t)s * a.H + h) * (DHq + 4);
+      const float o = acc[i] + a.sw[(size_t)s * 16 + h] * ip[j];
+      a.out[((size_t)s * a.H + h) * DHq + j] = f32_to_bf16_bits(o);
+    }
+  }
+}
+
+template <int D, int DHq>
+static hipError_t launch_rows_dd(const RowsArgs& a, const RowsPrepArgs& pa, int max_split, int stage,
+                                 hipStream_t s) {
+  if (stage == 0) {   // absorbed queries (and the null row's keys and values)
+    hipLaunchKernelGGL((k_rows_absorb_q<DHq>), dim3((D + 255) / 256, 16, (pa.n_slots + kAbsorbSlots - 1) / kAbsorbSlots),
+                       dim3(256), 0, s, pa);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || pa.null_row == nullptr) return e;
+    hipLaunchKernelGGL((k_rows_null<DHq>), dim3(pa.H, 2), dim3(256), 0, s, pa);
+    return hipGetLastError();
+  }
+  if (max_split > 0) hipLaunchKernelGGL((k_reader_rows<D>), dim3(max_split, a.n_slots), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((k_rows_combine<D, DHq>), dim3(a.n_slots, a.H), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((k_rows_project<D, DHq>), dim3(a.H, (a.n_slots + 15) / 16, DHq / 16), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_rows_d(int dh, const RowsArgs& a, const RowsPrepArgs& pa, int max_split, int stage,
+                                hipStream_t s) {
+  if (dh == 32) return launch_rows_dd<D, 32>(a, pa, max_split, stage, s);
+  if (dh == 64) return launch_rows_dd<D, 64>(a, pa, max_split, stage, s);
+  if (dh == 128) return launch_rows_dd<D, 128>(a, pa, max_split, stage, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_rows(int d, int dh, const RowsArgs& a, const RowsPrepArgs& pa, int stage, hipStream_t s) {
+  if (a.n_slots <= 0) return hipSuccess;
+  int max_split = 0;
+  for (int i = 0; i < a.n_slots; ++i) {
+    const int ns = a.n_read[i] > 0 ? (a.n_read[i] + a.pps[i] - 1) / a.pps[i] : 0;
+    if (ns > max_split) max_split = ns;
+  }
+  if (d == 512) return launch_rows_d<512>(dh, a, pa, max_split, stage, s);
+  if (d == 1024) return launch_rows_d<1024>(dh, a, pa, max_split, stage, s);
+  if (d == 2048) return launch_rows_d<2048>(dh, a, pa, max_split, stage, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace smem

@@ -24,7 +24,9 @@
 using namespace smem;
 
 struct smem_store {
-  smem_store_desc d;
+  smem_store_desc d;          // row stores: H = 1, dh = 0; the row width is rows_d
+  int kind = 0;               // 0: key/value planes, 1: rows of width rows_d
+  int32_t rows_d = 0;
   bool meta_only = false;
   char* pool = nullptr;
   DevLayout lay{};
@@ -91,6 +93,41 @@ bool layout_of(const smem_store_desc* d, DevLayout* L) {
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// ---------------------------------------------------------------- row stores
+
+int pps_rows(int n_read) { return pages_per_split(n_read, kMinPagesRows, kRowsSplitCap); }
+int splits_rows(int n_read) { return n_read > 0 ? (n_read + pps_rows(n_read) - 1) / pps_rows(n_read) : 0; }
+
+bool rows_layout_of(const smem_rows_desc* d, DevLayout* L) {
+  if (!d) return false;
+  if (d->n_seq < 1 || d->max_blocks < 1 || d->n_pages < 1) return false;
+  if (!(d->b == 16 || d->b == 64) || !(d->d == 512 || d->d == 1024 || d->d == 2048) || d->dtype != BF16) return false;
+  const size_t nt = (size_t)d->n_seq * d->max_blocks;
+  // splits of one read never exceed min(kRowsSplitCap, ceil(n_read / kMinPagesRows)), n_read <= max_blocks
+  const int64_t per_seq = std::min(kRowsSplitCap, (d->max_blocks + kMinPagesRows - 1) / kMinPagesRows);
+  const int64_t cap = std::min<int64_t>(kRowsPartials, (int64_t)d->n_seq * per_seq);
+  L->part_cap = (int32_t)std::max<int64_t>(cap, 1);
+  L->ws_floats = 0;
+  size_t off = 0;
+  L->off_table = off;     off = align256(off + nt * 4);
+  L->off_live_page = off; off = align256(off + nt * 4);
+  L->off_live_blk = off;  off = align256(off + nt * 4);
+  L->off_n_live = off;    off = align256(off + (size_t)d->n_seq * 4);
+  L->off_qabs = off;      off = align256(off + (size_t)kMaxSlots * 16 * d->d * 2);
+  L->off_intra = off;     off = align256(off + (size_t)kMaxSlots * 16 * (128 + 4) * 4);
+  L->off_null_kv = off;   off = align256(off + (size_t)2 * 16 * 128 * 2);
+  L->off_sw = off;        off = align256(off + (size_t)kMaxSlots * 16 * 4);
+  L->off_part = off;      off = align256(off + (size_t)L->part_cap * (16 * (size_t)d->d + 32) * 4);
+  L->off_ws = L->off_part;
+  L->off_pages = off;     off = align256(off + (size_t)d->n_pages * d->b * d->d * 2);
+  L->total = off;
+  return true;
+}
+
+size_t page_bytes(const smem_store* st) {
+  return st->kind == 1 ? (size_t)st->d.b * st->rows_d * 2 : (size_t)st->d.H * 2 * st->d.b * st->d.dh * esize(st->d.dtype);
+}
 
 size_t rope_bytes_of(const smem_rope_desc* d) {
   if (!d || !(d->dh == 32 || d->dh == 64 || d->dh == 128) || d->n_phases < 1 || d->n_phases > (1 << 20) ||
@@ -235,6 +272,7 @@ smem_status smem_store_stats(const smem_store* st, int32_t* pages_used, int32_t*
 smem_status smem_store_put_block(smem_store* st, int32_t seq, int32_t block_idx, const void* k_rows,
                                  const void* v_rows, hipStream_t s) {
   if (!st) return fail(SMEM_EINVAL, "store is NULL");
+  if (st->kind != 0) return fail(SMEM_EINVAL, "a row store takes smem_rows_put_block");
   const auto& d = st->d;
   if (seq < 0 || seq >= d.n_seq) return fail(SMEM_EINVAL, "seq %d out of range [0, %d)", seq, d.n_seq);
   if (block_idx < 0 || block_idx >= d.max_blocks)
@@ -275,7 +313,7 @@ smem_status smem_delete_block(smem_store* st, int32_t seq, int32_t block_idx, in
     smem_status r = push_edits(st, {seq}, {block_idx}, {-1}, s);
     if (r != SMEM_OK) return r;
     if (scrub) {
-      hipError_t e = launch_scrub(d.dtype, st->d_pages, page, d.H, d.b, d.dh, s);
+      hipError_t e = launch_scrub((char*)st->d_pages + (size_t)page * page_bytes(st), page_bytes(st), s);
       if (e != hipSuccess) return hip_fail(e, "page scrub");
     }
   }
@@ -289,6 +327,7 @@ smem_status smem_delete_block(smem_store* st, int32_t seq, int32_t block_idx, in
 smem_status smem_store_export(smem_store* st, int32_t seq, int32_t* live_idx, int32_t* n_live, void* k_out,
                               void* v_out, hipStream_t s) {
   if (!st) return fail(SMEM_EINVAL, "store is NULL");
+  if (st->kind != 0) return fail(SMEM_EINVAL, "a row store takes smem_rows_export");
   const auto& d = st->d;
   if (seq < 0 || seq >= d.n_seq) return fail(SMEM_EINVAL, "seq %d out of range [0, %d)", seq, d.n_seq);
   if ((k_out == nullptr) != (v_out == nullptr)) return fail(SMEM_EINVAL, "k_out and v_out: both or neither");
@@ -320,6 +359,7 @@ static smem_status encode_impl(smem_store* st, const smem_attn_desc* shape, int3
   if (mask != SMEM_MASK_BIDIR && mask != SMEM_MASK_CAUSAL) return fail(SMEM_EINVAL, "mask %d", mask);
   if (st) {
     if (st->meta_only) return fail(SMEM_EINVAL, "metadata-only store");
+    if (st->kind != 0) return fail(SMEM_EINVAL, "the encoder inserts into key/value stores only");
     if (st->d.b != b || st->d.H != H || st->d.dh != dh || st->d.dtype != dtype)
       return fail(SMEM_EINVAL, "shape differs from the store's");
   } else if (!out) {
@@ -434,6 +474,7 @@ static smem_status prefill_impl(smem_store* st, const smem_rope* rope, int32_t n
                                 const void* v_intra, const void* null_kv, void* out, hipStream_t s) {
   if (!st) return fail(SMEM_EINVAL, "store is NULL");
   if (st->meta_only) return fail(SMEM_EINVAL, "metadata-only store");
+  if (st->kind != 0) return fail(SMEM_EINVAL, "a row store is read by smem_reader_decode_rows");
   const auto& d = st->d;
   if (n_seq < 0) return fail(SMEM_EINVAL, "n_seq < 0");
   if (n_seq == 0) return SMEM_OK;
@@ -493,6 +534,7 @@ static smem_status decode_impl(smem_store* st, const smem_rope* rope, int32_t n_
                                hipStream_t s) {
   if (!st) return fail(SMEM_EINVAL, "store is NULL");
   if (st->meta_only) return fail(SMEM_EINVAL, "metadata-only store");
+  if (st->kind != 0) return fail(SMEM_EINVAL, "a row store is read by smem_reader_decode_rows");
   const auto& d = st->d;
   if (n_seq < 0) return fail(SMEM_EINVAL, "n_seq < 0");
   if (n_seq == 0) return SMEM_OK;
@@ -582,6 +624,206 @@ smem_status smem_reader_decode_rope(smem_store* st, const smem_rope* rope, int32
   if (!rope) return fail(SMEM_EINVAL, "rope is NULL");
   return decode_impl(st, rope, n_seq, seq_ids, query_block, pos, q, k_new, v_new, k_cache, v_cache, null_kv,
                      out, s);
+}
+
+size_t smem_rows_bytes(const smem_rows_desc* desc) {
+  DevLayout L;
+  if (!rows_layout_of(desc, &L)) return 0;
+  return L.total;
+}
+
+smem_status smem_rows_create(const smem_rows_desc* desc, void* dev_pool, size_t pool_bytes, hipStream_t s,
+                             smem_store** out) {
+  if (!out) return fail(SMEM_EINVAL, "out is NULL");
+  *out = nullptr;
+  DevLayout L;
+  if (!rows_layout_of(desc, &L))
+    return fail(SMEM_EINVAL, "invalid row store descriptor (need n_seq, max_blocks, n_pages >= 1, b in {16,64}, "
+                             "d in {512,1024,2048}, dtype BF16)");
+  if (!dev_pool) return fail(SMEM_EINVAL, "dev_pool is NULL");
+  if (pool_bytes < L.total) return fail(SMEM_ENOMEM, "pool has %zu bytes, row store needs %zu", pool_bytes, L.total);
+  if (((uintptr_t)dev_pool & 255u) != 0) return fail(SMEM_EINVAL, "dev_pool must be 256-byte aligned");
+  smem_store* st = new (std::nothrow) smem_store();
+  if (!st) return fail(SMEM_ENOMEM, "host allocation failed");
+  st->d = smem_store_desc{desc->n_seq, desc->max_blocks, desc->n_pages, desc->b, 1, 0, BF16};
+  st->kind = 1;
+  st->rows_d = desc->d;
+  st->lay = L;
+  st->table.assign((size_t)desc->n_seq * desc->max_blocks, -1);
+  st->live.assign(desc->n_seq, {});
+  st->free_pages.resize(desc->n_pages);
+  for (int i = 0; i < desc->n_pages; ++i) st->free_pages[i] = desc->n_pages - 1 - i;
+  st->pool = (char*)dev_pool;
+  st->d_table = (int32_t*)(st->pool + L.off_table);
+  st->d_live_page = (int32_t*)(st->pool + L.off_live_page);
+  st->d_live_blk = (int32_t*)(st->pool + L.off_live_blk);
+  st->d_n_live = (int32_t*)(st->pool + L.off_n_live);
+  st->d_ws = (float*)(st->pool + L.off_ws);
+  st->d_pages = st->pool + L.off_pages;
+  hipError_t e = launch_init_meta(st->d_table, st->d_n_live, st->table.size(), desc->n_seq, s);
+  if (e != hipSuccess) {
+    delete st;
+    return hip_fail(e, "row store init");
+  }
+  *out = st;
+  return SMEM_OK;
+}
+
+smem_status smem_rows_put_block(smem_store* st, int32_t seq, int32_t block_idx, const void* rows, hipStream_t s) {
+  if (!st) return fail(SMEM_EINVAL, "store is NULL");
+  if (st->kind != 1) return fail(SMEM_EINVAL, "not a row store");
+  const auto& d = st->d;
+  if (seq < 0 || seq >= d.n_seq) return fail(SMEM_EINVAL, "seq %d out of range [0, %d)", seq, d.n_seq);
+  if (block_idx < 0 || block_idx >= d.max_blocks)
+    return fail(SMEM_EINVAL, "block index %d out of range [0, %d)", block_idx, d.max_blocks);
+  if (!rows || !aligned16(rows)) return fail(SMEM_EINVAL, "rows must be a 16-byte aligned device pointer");
+  const size_t ti = (size_t)seq * d.max_blocks + block_idx;
+  if (st->table[ti] >= 0) return fail(SMEM_EEXIST, "block %d of sequence %d is occupied", block_idx, seq);
+  if (st->free_pages.empty()) return fail(SMEM_ENOMEM, "no free page (%d pages)", d.n_pages);
+  const int32_t page = st->free_pages.back();
+  hipError_t e = launch_copy16((char*)st->d_pages + (size_t)page * page_bytes(st), rows, page_bytes(st), s);
+  if (e != hipSuccess) return hip_fail(e, "row insert");
+  smem_status r = push_edits(st, {seq}, {block_idx}, {page}, s);
+  if (r != SMEM_OK) return r;
+  st->free_pages.pop_back();
+  st->table[ti] = page;
+  auto& lv = st->live[seq];
+  lv.insert(std::lower_bound(lv.begin(), lv.end(), block_idx), block_idx);
+  return SMEM_OK;
+}
+
+smem_status smem_rows_export(smem_store* st, int32_t seq, int32_t* live_idx, int32_t* n_live, void* rows_out,
+                             hipStream_t s) {
+  if (!st) return fail(SMEM_EINVAL, "store is NULL");
+  if (st->kind != 1) return fail(SMEM_EINVAL, "not a row store");
+  if (seq < 0 || seq >= st->d.n_seq) return fail(SMEM_EINVAL, "seq %d out of range [0, %d)", seq, st->d.n_seq);
+  if (!aligned16(rows_out)) return fail(SMEM_EINVAL, "rows_out must be 16-byte aligned");
+  const auto& lv = st->live[seq];
+  if (n_live) *n_live = (int32_t)lv.size();
+  if (live_idx) std::copy(lv.begin(), lv.end(), live_idx);
+  if (rows_out) {
+    const size_t pb = page_bytes(st);
+    for (size_t i = 0; i < lv.size(); ++i) {
+      const int32_t page = st->table[(size_t)seq * st->d.max_blocks + lv[i]];
+      hipError_t e = launch_copy16((char*)rows_out + i * pb, (const char*)st->d_pages + (size_t)page * pb, pb, s);
+      if (e != hipSuccess) return hip_fail(e, "row export");
+    }
+  }
+  return SMEM_OK;
+}
+
+smem_status smem_reader_decode_rows(smem_store* st, const smem_rows_layer* layer, int32_t n_seq,
+                                    const int32_t* seq_ids, const int32_t* query_block, const int32_t* pos,
+                                    const void* q, const void* k_new, const void* v_new, void* k_cache,
+                                    void* v_cache, void* out, hipStream_t s) {
+  if (!st) return fail(SMEM_EINVAL, "store is NULL");
+  if (st->kind != 1) return fail(SMEM_EINVAL, "not a row store");
+  if (!layer) return fail(SMEM_EINVAL, "layer is NULL");
+  const int H = layer->H, dh = layer->dh, D = st->rows_d, b = st->d.b;
+  if (H < 1 || H > 16 || !(dh == 32 || dh == 64 || dh == 128))
+    return fail(SMEM_EINVAL, "layer shape H=%d dh=%d (need 1 <= H <= 16, dh in {32,64,128})", H, dh);
+  if (!layer->w_k || !layer->w_v) return fail(SMEM_EINVAL, "w_k and w_v are required");
+  if (n_seq < 0) return fail(SMEM_EINVAL, "n_seq < 0");
+  if (n_seq == 0) return SMEM_OK;
+  if (!seq_ids || !query_block || !q || !out) return fail(SMEM_EINVAL, "seq_ids, query_block, q, out are required");
+  const int n_given = (k_new != nullptr) + (v_new != nullptr) + (k_cache != nullptr) + (v_cache != nullptr);
+  if (n_given != 0 && n_given != 4) return fail(SMEM_EINVAL, "k_new, v_new, k_cache, v_cache: all or none");
+  if (n_given == 4 && !pos) return fail(SMEM_EINVAL, "pos is required with in-block keys");
+  if (!aligned16(q) || !aligned16(out) || !aligned16(k_new) || !aligned16(v_new) || !aligned16(k_cache) ||
+      !aligned16(v_cache) || !aligned16(layer->w_k) || !aligned16(layer->w_v) || !aligned16(layer->null_row))
+    return fail(SMEM_EINVAL, "tensors must be 16-byte aligned");
+  std::set<int32_t> seen;
+  for (int i = 0; i < n_seq; ++i) {
+    if (seq_ids[i] < 0 || seq_ids[i] >= st->d.n_seq) return fail(SMEM_EINVAL, "seq_ids[%d] = %d out of range", i, seq_ids[i]);
+    if (query_block[i] < 0 || query_block[i] > st->d.max_blocks)
+      return fail(SMEM_EINVAL, "query_block[%d] = %d out of range [0, %d]", i, query_block[i], st->d.max_blocks);
+    if (n_given == 4 && (pos[i] < 0 || pos[i] >= b)) return fail(SMEM_EINVAL, "pos[%d] = %d out of range [0, %d)", i, pos[i], b);
+    if (!seen.insert(seq_ids[i]).second) return fail(SMEM_EINVAL, "sequence %d appears twice", seq_ids[i]);
+  }
+  const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)dh));
+  const size_t tok = (size_t)H * dh;
+  const auto& L = st->lay;
+  uint16_t* qabs = (uint16_t*)(st->pool + L.off_qabs);
+  float* intra = (float*)(st->pool + L.off_intra);
+  uint16_t* null_kv = (uint16_t*)(st->pool + L.off_null_kv);
+  float* part = (float*)(st->pool + L.off_part);
+  bool null_done = false;
+  int i0 = 0;
+  while (i0 < n_seq) {
+    // a launch: at most kMaxSlots sequences whose split partials fit the workspace
+    int n = 0, used = 0;
+    int32_t nread[kMaxSlots];
+    while (i0 + n < n_seq && n < kMaxSlots) {
+      const int nr = n_read_of(st, seq_ids[i0 + n], query_block[i0 + n]);
+      const int sp = splits_rows(nr);
+      if (n > 0 && used + sp > L.part_cap) break;
+      nread[n] = nr;
+      used += sp;
+      ++n;
+    }
+    RowsPrepArgs pa;
+    memset(&pa, 0, sizeof pa);
+    pa.q = (const uint16_t*)q + i0 * tok;
+    pa.w_k = (const uint16_t*)layer->w_k;
+    pa.w_v = (const uint16_t*)layer->w_v;
+    pa.null_row = null_done ? nullptr : (const uint16_t*)layer->null_row;
+    pa.qabs = qabs;
+    pa.null_kv = null_kv;
+    pa.d = D; pa.H = H; pa.n_slots = n; pa.scale_log2 = scale_log2;
+    RowsArgs ra;
+    memset(&ra, 0, sizeof ra);
+    ra.pages = (const uint16_t*)st->d_pages;
+    ra.live_page = st->d_live_page;
+    ra.qabs = qabs;
+    ra.part = part;
+    ra.intra = intra;
+    ra.w_v = (const uint16_t*)layer->w_v;
+    ra.ubuf = qabs;     // the absorbed queries are spent once the row reader has run
+    ra.sw = (float*)(st->pool + L.off_sw);
+    ra.out = (uint16_t*)out + i0 * tok;
+    ra.max_blocks = st->d.max_blocks; ra.b = b; ra.H = H; ra.n_slots = n;
+    int base = 0;
+    for (int i = 0; i < n; ++i) {
+      ra.seq[i] = seq_ids[i0 + i];
+      ra.n_read[i] = nread[i];
+      ra.pps[i] = pps_rows(nread[i]);
+      ra.pbase[i] = base;
+      base += splits_rows(nread[i]);
+    }
+    hipError_t e = launch_rows(D, dh, ra, pa, 0, s);
+    if (e != hipSuccess) return hip_fail(e, "absorbed queries");
+    null_done = true;
+    // in-block keys and the mapped null row: one compact partial per (sequence, head)
+    ReaderArgs a;
+    memset(&a, 0, sizeof a);
+    a.q = (const char*)q + i0 * tok * 2;
+    if (n_given == 4) {
+      a.k_new = (const char*)k_new + i0 * tok * 2;
+      a.v_new = (const char*)v_new + i0 * tok * 2;
+      a.k_in = (const char*)k_cache + (size_t)i0 * b * tok * 2;
+      a.v_in = (const char*)v_cache + (size_t)i0 * b * tok * 2;
+      a.k_cache_w = (char*)k_cache + (size_t)i0 * b * tok * 2;
+      a.v_cache_w = (char*)v_cache + (size_t)i0 * b * tok * 2;
+    }
+    a.null_kv = layer->null_row ? null_kv : nullptr;
+    a.ws = intra;
+    a.intra_partial = 1;
+    a.max_blocks = st->d.max_blocks;
+    a.H = H; a.b = b; a.nq = 1; a.intra_mode = 2;
+    a.n_slots = n; a.scale_log2 = scale_log2;
+    for (int i = 0; i < n; ++i) {
+      a.seq[i] = seq_ids[i0 + i];
+      a.n_read[i] = 0;
+      a.pps[i] = 1;
+      a.aux[i] = n_given == 4 ? pos[i0 + i] : 0;
+    }
+    e = launch_reader_valu(BF16, b, dh, a, s);
+    if (e != hipSuccess) return hip_fail(e, "in-block partial");
+    e = launch_rows(D, dh, ra, pa, 1, s);
+    if (e != hipSuccess) return hip_fail(e, "row reader");
+    i0 += n;
+  }
+  return SMEM_OK;
 }
 
 size_t smem_rope_bytes(const smem_rope_desc* desc) { return rope_bytes_of(desc); }

@@ -148,10 +148,8 @@ __global__ void k_scrub(uint4* __restrict__ p, size_t n16) {
   for (; i < n16; i += stride) p[i] = z;
 }
 
-hipError_t launch_scrub(int dtype, void* pages, int page, int H, int b, int dh, hipStream_t s) {
-  const size_t esz = dtype == F32 ? 4 : 2;
-  const size_t bytes = (size_t)H * 2 * b * dh * esz;  // a page is a multiple of 16 bytes
-  char* base = (char*)pages + page_head_offset(page, 0, H, b, dh) * esz;
+hipError_t launch_scrub(void* page_base, size_t bytes, hipStream_t s) {
+  char* base = (char*)page_base;     // a page is a multiple of 16 bytes
   size_t n16 = bytes / 16;
   unsigned grid = (unsigned)((n16 + 255) / 256);
   if (grid > 1024) grid = 1024;
@@ -196,6 +194,21 @@ hipError_t launch_export(int dtype, const void* pages, const int32_t* live_page_
     hipLaunchKernelGGL(k_export<uint16_t>, dim3(n_live, H), dim3(256), lds, s, (const uint16_t*)pages,
                        live_page_seq, H, b, dh, (uint16_t*)k_out, (uint16_t*)v_out);
   }
+  return hipGetLastError();
+}
+
+__global__ void __launch_bounds__(256) k_copy16(u32x4* __restrict__ dst, const u32x4* __restrict__ src, size_t n16) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (; i < n16; i += stride) dst[i] = src[i];
+}
+
+hipError_t launch_copy16(void* dst, const void* src, size_t bytes, hipStream_t s) {
+  const size_t n16 = bytes / 16;
+  unsigned grid = (unsigned)((n16 + 255) / 256);
+  if (grid > 1024) grid = 1024;
+  if (grid == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_copy16, dim3(grid), dim3(256), 0, s, (u32x4*)dst, (const u32x4*)src, n16);
   return hipGetLastError();
 }
 

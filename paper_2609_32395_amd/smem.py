@@ -10,8 +10,10 @@ Functions carry the C names: smem_encode_blocks, smem_reencode_blocks,
 smem_reader_prefill_block, smem_reader_decode, smem_delete_block,
 smem_store_put_block, smem_store_export, and the rotary variants
 smem_encode_blocks_rope, smem_reader_prefill_block_rope,
-smem_reader_decode_rope; a store is created and destroyed by the Store class,
-a rotary table by the Rope class.
+smem_reader_decode_rope, and the row-plane calls smem_rows_put_block,
+smem_rows_export, smem_reader_decode_rows; a store is created and destroyed
+by the Store class (RowStore for a row store), a rotary table by the Rope
+class.
 """
 from __future__ import annotations
 
@@ -49,6 +51,16 @@ class AttnDesc(ctypes.Structure):
     _fields_ = [("b", ctypes.c_int32), ("H", ctypes.c_int32), ("dh", ctypes.c_int32), ("dtype", ctypes.c_int32)]
 
 
+class RowsDesc(ctypes.Structure):
+    _fields_ = [("n_seq", ctypes.c_int32), ("max_blocks", ctypes.c_int32), ("n_pages", ctypes.c_int32),
+                ("b", ctypes.c_int32), ("d", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class RowsLayer(ctypes.Structure):
+    _fields_ = [("H", ctypes.c_int32), ("dh", ctypes.c_int32), ("w_k", ctypes.c_void_p), ("w_v", ctypes.c_void_p),
+                ("null_row", ctypes.c_void_p)]
+
+
 class RopeDesc(ctypes.Structure):
     _fields_ = [("dh", ctypes.c_int32), ("n_phases", ctypes.c_int32), ("max_offset", ctypes.c_int32),
                 ("reserved", ctypes.c_int32), ("base", ctypes.c_double)]
@@ -77,6 +89,11 @@ SIGNATURES = {
     "smem_encode_blocks_rope": (_I, [_P, ctypes.POINTER(AttnDesc), _P, _I, _IP, _IP, _P, _P, _P, _P, _I, _P]),
     "smem_reader_prefill_block_rope": (_I, [_P, _P, _I, _IP, _IP, _P, _P, _P, _P, _P, _P]),
     "smem_reader_decode_rope": (_I, [_P, _P, _I, _IP, _IP, _IP, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "smem_rows_bytes": (ctypes.c_size_t, [ctypes.POINTER(RowsDesc)]),
+    "smem_rows_create": (_I, [ctypes.POINTER(RowsDesc), _P, ctypes.c_size_t, _P, ctypes.POINTER(_P)]),
+    "smem_rows_put_block": (_I, [_P, _I, _I, _P, _P]),
+    "smem_rows_export": (_I, [_P, _I, _IP, _IP, _P, _P]),
+    "smem_reader_decode_rows": (_I, [_P, ctypes.POINTER(RowsLayer), _I, _IP, _IP, _IP, _P, _P, _P, _P, _P, _P, _P]),
     "smem_store_stats": (_I, [_P, _IP, _IP]),
     "smem_status_string": (ctypes.c_char_p, [_I]),
     "smem_last_error": (ctypes.c_char_p, []),
@@ -197,6 +214,77 @@ class Store:
         used, free = ctypes.c_int32(), ctypes.c_int32()
         _check(lib().smem_store_stats(self.handle, ctypes.byref(used), ctypes.byref(free)))
         return used.value, free.value
+
+
+class RowStore(Store):
+    """A row store (one plane of b rows of width d per block, bf16), read by
+    smem_reader_decode_rows with each layer's key and value maps."""
+
+    def __init__(self, n_seq, max_blocks, n_pages, b, d, device="cuda", stream=None):
+        self.dtype = torch.bfloat16
+        self.b, self.d = b, d
+        self.H, self.dh = 1, 0
+        self.n_seq, self.max_blocks, self.n_pages = n_seq, max_blocks, n_pages
+        self.desc = RowsDesc(n_seq, max_blocks, n_pages, b, d, BF16)
+        L = lib()
+        nbytes = L.smem_rows_bytes(ctypes.byref(self.desc))
+        if nbytes == 0:
+            raise SmemError(SMEM_EINVAL, "invalid row store descriptor")
+        self.nbytes = nbytes
+        self.pool = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        handle = ctypes.c_void_p()
+        _check(L.smem_rows_create(ctypes.byref(self.desc), ctypes.c_void_p(self.pool.data_ptr()), nbytes,
+                                  _stream(stream), ctypes.byref(handle)))
+        self.handle = handle
+        self.meta_only = False
+
+    @property
+    def row_shape(self):
+        return (self.b, self.d)
+
+
+def smem_rows_put_block(st: RowStore, seq: int, block_idx: int, rows, stream=None):
+    rp = _dev(rows, st.row_shape, torch.bfloat16, "rows")
+    _check(lib().smem_rows_put_block(st.handle, int(seq), int(block_idx), rp, _stream(stream)))
+
+
+def smem_rows_export(st: RowStore, seq: int, rows: bool = True, stream=None):
+    """(live block indices, rows [n_live*b, d] or None)."""
+    L = lib()
+    idx = (ctypes.c_int32 * st.max_blocks)()
+    n = ctypes.c_int32()
+    _check(L.smem_rows_export(st.handle, int(seq), idx, ctypes.byref(n), None, None))
+    if not rows:
+        return list(idx[: n.value]), None
+    R = torch.empty((n.value * st.b, st.d), dtype=torch.bfloat16, device=st.pool.device)
+    _check(L.smem_rows_export(st.handle, int(seq), idx, ctypes.byref(n), ctypes.c_void_p(R.data_ptr()),
+                              _stream(stream)))
+    return list(idx[: n.value]), R
+
+
+def smem_reader_decode_rows(st: RowStore, w_k, w_v, seq_ids, query_block, pos, q, k_new=None, v_new=None,
+                            k_cache=None, v_cache=None, null_row=None, out=None, stream=None):
+    """One layer's reader decode from the row plane: w_k, w_v [H*dh, d]
+    (bf16, a linear layer's out x in layout), q etc. [n, H, dh], null_row
+    [d] or None."""
+    n, H, dh = q.shape
+    if len(seq_ids) != n or len(query_block) != n or (pos is not None and len(pos) != n):
+        raise ValueError("seq_ids, query_block and pos need one entry per query")
+    bt = torch.bfloat16
+    wk = _dev(w_k, (H * dh, st.d), bt, "w_k")
+    wv = _dev(w_v, (H * dh, st.d), bt, "w_v")
+    nr = _dev(null_row, (st.d,), bt, "null_row")
+    layer = RowsLayer(H, dh, wk.value, wv.value, nr.value if nr is not None else None)
+    tok = (n, H, dh)
+    cache = (n * st.b, H, dh)
+    if out is None:
+        out = torch.empty(tok, dtype=bt, device=q.device)
+    args = [_dev(q, tok, bt, "q"), _dev(k_new, tok, bt, "k_new"), _dev(v_new, tok, bt, "v_new"),
+            _dev(k_cache, cache, bt, "k_cache"), _dev(v_cache, cache, bt, "v_cache"), _dev(out, tok, bt, "out")]
+    pa = _i32(pos) if pos is not None else None
+    _check(lib().smem_reader_decode_rows(st.handle, ctypes.byref(layer), n, _i32(seq_ids), _i32(query_block), pa,
+                                         *args, _stream(stream)))
+    return out
 
 
 class Rope:

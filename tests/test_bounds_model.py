@@ -167,3 +167,32 @@ def test_rope_prefill_lds_rows(dh):
     # LDS per workgroup: tiles + rows + query copy stay within 64 KiB
     tiles = (64 * (dh + 8) + dh * (64 + 4)) * 2
     assert tiles + ROWS * dh * 4 + (dh // 32) * 4 * 64 * 16 <= 64 * 1024
+
+
+def _pps_rows(n):
+    return max(8, -(-n // 32))
+
+
+@pytest.mark.parametrize("b,D", [(b, D) for b in (16, 64) for D in (512, 1024, 2048)])
+def test_rows_reader_indexing(b, D):
+    """Row-plane reader: chunk loads stay inside a page, LDS reads inside the
+    chunk and query tiles, and a launch's split partials inside the workspace."""
+    N = 16 * D // 8 // 256
+    assert N * 256 * 8 == 16 * D
+    assert (255 + (N - 1) * 256) * 8 + 7 < 16 * D               # one 16-row chunk
+    assert (b // 16 - 1) * 16 * D + 16 * D <= b * D              # last chunk of a page
+    DW = D // 4
+    for wave in range(4):
+        for kk in range(DW // 32):
+            for g4 in range(4):
+                assert wave * DW + kk * 32 + g4 * 8 + 7 < D
+        for n in range(DW // 16):
+            assert wave * DW + n * 16 + 15 < D
+    # splits per read stay within the per-sequence bound the workspace is sized for
+    for max_blocks in (1, 7, 8, 9, 64, 255, 256, 257, 300, 4096):
+        per_seq = min(32, -(-max_blocks // 8))
+        for n_read in range(0, max_blocks + 1):
+            sp = -(-n_read // _pps_rows(n_read)) if n_read else 0
+            assert sp <= per_seq
+    # k_merge_rows keeps split weights in a 64-entry array
+    assert 32 <= 64

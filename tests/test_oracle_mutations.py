@@ -181,3 +181,10 @@ def _rope_read_null_at_query_phase(orig):
         nkv[0, h] = O.rope_rotate(nkv[0, h], i - rope.key_phase(0, i), rope.base)
         return orig(store, seq, i, t, q, h, nkv, k_in, v_in, n_in, rope, scale)
     return read
+
+
+def test_rows_swapped_maps_are_caught(monkeypatch):
+    orig = O.reader_decode_rows
+    monkeypatch.setattr(O, "reader_decode_rows",
+                        lambda st, wk, wv, *a, **k: orig(st, wv, wk, *a, **k))   # planted: maps swapped
+    assert _fails(P.test_rows_decode_matches_sdpa_on_mapped_rows)

@@ -666,3 +666,54 @@ def test_rope_values_not_rotated_and_decode_equals_prefill():
         kc[:, :p], vc[:, :p] = ki[:, :p], vi[:, :p]
         dec, _, _ = O.reader_decode_rope(st, [0], [J], [p], q[:, p], ki[:, p], vi[:, p], kc, vc, nkv, rope)
         np.testing.assert_allclose(dec, pre[:, p], atol=1e-13, rtol=0)
+
+
+# ---------------------------------------------------------------- decode from the row plane
+
+def test_rows_decode_with_identity_maps_is_the_plain_read():
+    """With d = H*dh and identity key/value maps, the recomputed read is the
+    plain read of a store whose keys and values are the rows themselves."""
+    g = np.random.default_rng(51)
+    b, H, dh, J = 4, 2, 8, 5
+    d = H * dh
+    rows = O.Store(2, J + 1, b, 1, d)
+    kv = O.Store(2, J + 1, b, H, dh)
+    for s in range(2):
+        for j in range(J):
+            if (s + j) % 3:
+                R = g.standard_normal((b, d))
+                rows.put(s, j, R[:, None], R[:, None])
+                kv.put(s, j, R.reshape(b, H, dh), R.reshape(b, H, dh))
+    nr = g.standard_normal(d)
+    q, kn, vn = (g.standard_normal((2, H, dh)) for _ in range(3))
+    kc, vc = g.standard_normal((2, 2, b, H, dh))
+    eye = np.eye(d)
+    a, _, _ = O.reader_decode_rows(rows, eye, eye, nr, [0, 1], [J, 3], [1, 3], q, kn, vn, kc, vc)
+    c, _, _ = O.reader_decode(kv, [0, 1], [J, 3], [1, 3], q, kn, vn, kc, vc, nr.reshape(1, H, dh).repeat(2, 0))
+    assert np.array_equal(a, c)
+
+
+def test_rows_decode_matches_sdpa_on_mapped_rows():
+    """Against torch: rows mapped by matmul, SDPA over [null] ++ mapped rows ++ in-block keys."""
+    g = np.random.default_rng(53)
+    b, H, dh, d, J = 4, 3, 8, 20, 4
+    rows = O.Store(1, J, b, 1, d)
+    for j in (0, 2, 3):
+        R = g.standard_normal((b, d))
+        rows.put(0, j, R[:, None], R[:, None])
+    wk, wv = g.standard_normal((2, H * dh, d)) / np.sqrt(d)
+    nr = g.standard_normal(d)
+    q, kn, vn = (g.standard_normal((1, H, dh)) for _ in range(3))
+    kc, vc = g.standard_normal((2, 1, b, H, dh))
+    p = 2
+    out, kc2, _ = O.reader_decode_rows(rows, wk, wv, nr, [0], [J], [p], q, kn, vn, kc, vc)
+    _, R, _ = rows.export(0)
+    T = lambda x: torch.as_tensor(np.asarray(x, np.float64))
+    lin = lambda x, w: torch.nn.functional.linear(T(x), T(w))      # x w^T, the linear layer
+    K = torch.cat([lin(nr[None], wk), lin(R[:, 0], wk)]).reshape(-1, H, dh)
+    V = torch.cat([lin(nr[None], wv), lin(R[:, 0], wv)]).reshape(-1, H, dh)
+    K = torch.cat([K, T(kc2[0, :p + 1])])
+    V = torch.cat([V, T(vc[0, :p]), T(vn[0])[None]])
+    for h in range(H):
+        ref = F.scaled_dot_product_attention(T(q[0, h])[None, None], K[:, h][None], V[:, h][None])
+        np.testing.assert_allclose(out[0, h], ref[0, 0].numpy(), atol=1e-12, rtol=0)
