@@ -194,6 +194,15 @@ struct RowsArgs {
   uint16_t* ubuf;             // combined weighted rows [slot][16][d] (bf16)
   float* sw;                  // in-block weight / L per [slot][16]
   uint16_t* out;              // [slot][H][dh]
+  // in-block keys and the mapped null row (the split after the row splits)
+  const uint16_t* q;          // [slot][H][dh]
+  const uint16_t* k_new;      // [slot][H][dh] or NULL (no in-block keys)
+  const uint16_t* v_new;
+  uint16_t* k_cache;          // [slot*b + r][H][dh], row pos written
+  uint16_t* v_cache;
+  const uint16_t* null_kv;    // [2][H][dh] or NULL
+  float* intra_w;             // in-block / null partials written here ([slot][H][dh+4])
+  float scale_log2;
   int32_t max_blocks;
   int32_t b;
   int32_t H;
@@ -202,6 +211,7 @@ struct RowsArgs {
   int32_t n_read[kMaxSlots];
   int32_t pps[kMaxSlots];
   int32_t pbase[kMaxSlots];   // first partial of the slot
+  int32_t pos[kMaxSlots];     // in-block position of the new token
 };
 
 struct RowsPrepArgs {

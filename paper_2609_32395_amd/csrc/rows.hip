@@ -106,9 +106,75 @@ __device__ __forceinline__ void wait_chunk(int ahead) {
   else wait_vm<0>();
 }
 
+// The splits after the row splits: the query's in-block keys 0..pos (the
+// new key/value pair at pos, also written into the cache) and the mapped
+// null row, under the query's own scale.  Workgroup g of them takes heads
+// 4g .. 4g+3, one per wave: a lane scores one in-block row, then the lanes
+// take the value dimensions (weights read back from LDS).  Writes the
+// compact partial (acc[dh], max, sum) of each head.
+template <int DHq>
+__device__ __forceinline__ void rows_intra(const RowsArgs& a, int slot, int h, int lane, float* pw, float& M_out,
+                                           float& L_out) {
+  const int H = a.H, pos = a.pos[slot];
+  const int n_in = a.k_new ? pos + 1 : 0;
+  const size_t tok = (size_t)H * DHq;
+  const uint16_t* qh = a.q + ((size_t)slot * H + h) * DHq;
+  auto dot = [&](const uint16_t* kr) {   // the query is re-read per chunk (cached), not held
+    float x = 0.f;
+#pragma unroll 4
+    for (int c8 = 0; c8 < DHq / 8; ++c8) {
+      float kf[8], qf[8];
+      Chunk<uint16_t>::unpack(*(const u32x4*)(kr + c8 * 8), kf);
+      Chunk<uint16_t>::unpack(*(const u32x4*)(qh + c8 * 8), qf);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x += qf[e] * kf[e];
+    }
+    return x * a.scale_log2;
+  };
+  const uint16_t* knew = a.k_new ? a.k_new + ((size_t)slot * H + h) * DHq : nullptr;
+  const uint16_t* vnew = a.v_new ? a.v_new + ((size_t)slot * H + h) * DHq : nullptr;
+  float sc = -INFINITY;
+  if (lane < n_in) sc = dot(lane == pos ? knew : a.k_cache + ((size_t)slot * a.b + lane) * tok + (size_t)h * DHq);
+  const float sn = a.null_kv ? dot(a.null_kv + (size_t)h * DHq) : -INFINITY;
+  float M = sc;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) M = fmaxf(M, __shfl_xor(M, o));
+  M = fmaxf(M, sn);
+  const float p = (lane < n_in) ? exp2w(sc - M) : 0.f;
+  const float pn = a.null_kv ? exp2w(sn - M) : 0.f;
+  float Lsum = p;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) Lsum += __shfl_xor(Lsum, o);
+  Lsum += pn;
+  pw[lane] = p;                            // this wave's row of weights
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  float* part = a.intra_w + ((size_t)slot * H + h) * (DHq + 4);
+  const uint16_t* vc = a.v_cache + (size_t)slot * a.b * tok + (size_t)h * DHq;
+#pragma unroll
+  for (int dd = 0; dd < (DHq + 63) / 64; ++dd) {
+    const int d = lane + dd * 64;
+    if (d < DHq) {
+      float acc = a.null_kv ? pn * bf16_bits_to_f32(a.null_kv[((size_t)H + h) * DHq + d]) : 0.f;
+      if (n_in > 0) acc += pw[pos] * bf16_bits_to_f32(vnew[d]);
+#pragma unroll 8
+      for (int r = 0; r < pos && r < n_in; ++r) acc += pw[r] * bf16_bits_to_f32(vc[(size_t)r * tok + d]);
+      part[d] = acc;
+    }
+  }
+  M_out = M;
+  L_out = Lsum;
+  if (n_in > 0 && lane < DHq / 8) {         // the new pair into the cache at row pos
+    const size_t off = ((size_t)slot * a.b + pos) * tok + (size_t)h * DHq + lane * 8;
+    *(u32x4*)(a.k_cache + off) = *(const u32x4*)(knew + lane * 8);
+    *(u32x4*)(a.v_cache + off) = *(const u32x4*)(vnew + lane * 8);
+  }
+}
+
 // One workgroup per (sequence slot, split).  Wave w reduces dims
 // [w*D/4, (w+1)*D/4) of the scores and owns the same dims of U.
-template <int D>
+template <int D, int DHq>
 __global__ void __launch_bounds__(256) k_reader_rows(RowsArgs a) {
   using C = RowsCfg<D>;
   __shared__ RowsLds<D> L;
@@ -295,43 +361,66 @@ __global__ void __launch_bounds__(256) k_rows_null(RowsPrepArgs a) {
   }
 }
 
-// Combine the row splits of one (slot, head) in split order with the
-// in-block / null partial's statistics: u = sum_k w_k U_k / L (bf16, into
-// ubuf) and the in-block weight w_i / L (into sw).
+// Per (slot, head): wave 0 reads the in-block keys and the null row
+// (rows_intra) while waves 1-3 combine the row splits in split order against
+// their own maximum Mr: u' = sum_k 2^(m_k - Mr) U_k, l' likewise.  Then with
+// M = max(Mr, m_i): u = u' 2^(Mr - M) / L (bf16, into ubuf) and the in-block
+// weight 2^(m_i - M) / L (into sw), L = l' 2^(Mr - M) + l_i 2^(m_i - M).
 template <int D, int DHq>
 __global__ void __launch_bounds__(256) k_rows_combine(RowsArgs a) {
   const int slot = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
   const int n_read = a.n_read[slot], pps = a.pps[slot];
   const int nsp = n_read > 0 ? (n_read + pps - 1) / pps : 0;
-  __shared__ float w_sh[kRowsSplitCap];
-  __shared__ float inv_sh;
-  const float* ip = a.intra + ((size_t)slot * a.H + h) * (DHq + 4);
+  __shared__ float w_sh[4][kRowsSplitCap];
+  __shared__ float u_sh[D];
+  __shared__ float pw[64];
+  __shared__ float stat[4];   // m_i, l_i, Mr, l'
+  __shared__ float fin[1];    // scale of u' (times 1/L)
   const float* pb = a.part + (size_t)a.pbase[slot] * (16 * D + 32);
-  if (tid < 64) {
-    // split statistics in parallel, the sums in split order by lane 0
-    const float mk = tid < nsp ? pb[(size_t)tid * (16 * D + 32) + 16 * D + h] : -INFINITY;
-    float M = fmaxf(mk, ip[DHq]);
+  const int lane = tid & 63, wave = tid >> 6;
+  if (wave == 0) {
+    float mi, li;
+    rows_intra<DHq>(a, slot, h, lane, pw, mi, li);
+    if (lane == 0) {
+      stat[0] = mi;
+      stat[1] = li;
+    }
+  } else {
+    // each of waves 1-3 derives the split weights itself (no block barrier)
+    const float mk = lane < nsp ? pb[(size_t)lane * (16 * D + 32) + 16 * D + h] : -INFINITY;
+    float Mr = mk;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) M = fmaxf(M, __shfl_xor(M, o));
-    const float wk = (tid < nsp && mk != -INFINITY) ? exp2w(mk - M) : 0.f;
-    if (tid < nsp) w_sh[tid] = wk;
-    if (tid == 0) {
-      float L = 0.f;
-      for (int k = 0; k < nsp; ++k) L += w_sh[k] * pb[(size_t)k * (16 * D + 32) + 16 * D + 16 + h];
-      const float wi = (ip[DHq] == -INFINITY) ? 0.f : exp2w(ip[DHq] - M);
-      L += wi * ip[DHq + 1];
-      const float inv = (L > 0.f) ? 1.f / L : 0.f;
-      inv_sh = inv;
-      a.sw[(size_t)slot * 16 + h] = wi * inv;
+    for (int o = 1; o < 64; o <<= 1) Mr = fmaxf(Mr, __shfl_xor(Mr, o));
+    if (lane < nsp) w_sh[wave][lane] = (mk == -INFINITY) ? 0.f : exp2w(mk - Mr);
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (wave == 1 && lane == 0) {
+      float l = 0.f;
+      for (int k = 0; k < nsp; ++k) l += w_sh[1][k] * pb[(size_t)k * (16 * D + 32) + 16 * D + 16 + h];
+      stat[2] = Mr;
+      stat[3] = l;
+    }
+    for (int c = (wave - 1) * 64 + lane; c < D; c += 192) {
+      float x = 0.f;
+      for (int k = 0; k < nsp; ++k) x += w_sh[wave][k] * pb[(size_t)k * (16 * D + 32) + (size_t)h * D + c];
+      u_sh[c] = x;
     }
   }
   __syncthreads();
-  const float inv = inv_sh;
-  for (int c = tid; c < D; c += 256) {
-    float x = 0.f;
-    for (int k = 0; k < nsp; ++k) x += w_sh[k] * pb[(size_t)k * (16 * D + 32) + (size_t)h * D + c];
-    a.ubuf[((size_t)slot * 16 + h) * D + c] = f32_to_bf16_bits(x * inv);
+  if (tid == 0) {
+    const float mi = stat[0], Mr = stat[2];
+    const float M = fmaxf(mi, Mr);
+    const float wr = (Mr == -INFINITY) ? 0.f : exp2w(Mr - M);
+    const float wi = (mi == -INFINITY) ? 0.f : exp2w(mi - M);
+    const float L = wr * stat[3] + wi * stat[1];
+    const float inv = (L > 0.f) ? 1.f / L : 0.f;
+    fin[0] = wr * inv;
+    a.sw[(size_t)slot * 16 + h] = wi * inv;
   }
+  __syncthreads();
+  const float sc = fin[0];
+  for (int c = tid; c < D; c += 256) a.ubuf[((size_t)slot * 16 + h) * D + c] = f32_to_bf16_bits(u_sh[c] * sc);
 }
 
 // out[s][h][j] = sum_c u[s][h][c] W_V[h*dh + j][c] + (w_i/L)[s][h] acc_i[s][h][j]:
@@ -383,7 +472,7 @@ static hipError_t launch_rows_dd(const RowsArgs& a, const RowsPrepArgs& pa, int 
     hipLaunchKernelGGL((k_rows_null<DHq>), dim3(pa.H, 2), dim3(256), 0, s, pa);
     return hipGetLastError();
   }
-  if (max_split > 0) hipLaunchKernelGGL((k_reader_rows<D>), dim3(max_split, a.n_slots), dim3(256), 0, s, a);
+  if (max_split > 0) hipLaunchKernelGGL((k_reader_rows<D, DHq>), dim3(max_split, a.n_slots), dim3(256), 0, s, a);
   hipLaunchKernelGGL((k_rows_combine<D, DHq>), dim3(a.n_slots, a.H), dim3(256), 0, s, a);
   hipLaunchKernelGGL((k_rows_project<D, DHq>), dim3(a.H, (a.n_slots + 15) / 16, DHq / 16), dim3(256), 0, s, a);
   return hipGetLastError();

@@ -793,32 +793,18 @@ smem_status smem_reader_decode_rows(smem_store* st, const smem_rows_layer* layer
     hipError_t e = launch_rows(D, dh, ra, pa, 0, s);
     if (e != hipSuccess) return hip_fail(e, "absorbed queries");
     null_done = true;
-    // in-block keys and the mapped null row: one compact partial per (sequence, head)
-    ReaderArgs a;
-    memset(&a, 0, sizeof a);
-    a.q = (const char*)q + i0 * tok * 2;
+    // in-block keys and the mapped null row: the reader's extra split
+    ra.q = (const uint16_t*)q + i0 * tok;
     if (n_given == 4) {
-      a.k_new = (const char*)k_new + i0 * tok * 2;
-      a.v_new = (const char*)v_new + i0 * tok * 2;
-      a.k_in = (const char*)k_cache + (size_t)i0 * b * tok * 2;
-      a.v_in = (const char*)v_cache + (size_t)i0 * b * tok * 2;
-      a.k_cache_w = (char*)k_cache + (size_t)i0 * b * tok * 2;
-      a.v_cache_w = (char*)v_cache + (size_t)i0 * b * tok * 2;
+      ra.k_new = (const uint16_t*)k_new + i0 * tok;
+      ra.v_new = (const uint16_t*)v_new + i0 * tok;
+      ra.k_cache = (uint16_t*)k_cache + (size_t)i0 * b * tok;
+      ra.v_cache = (uint16_t*)v_cache + (size_t)i0 * b * tok;
     }
-    a.null_kv = layer->null_row ? null_kv : nullptr;
-    a.ws = intra;
-    a.intra_partial = 1;
-    a.max_blocks = st->d.max_blocks;
-    a.H = H; a.b = b; a.nq = 1; a.intra_mode = 2;
-    a.n_slots = n; a.scale_log2 = scale_log2;
-    for (int i = 0; i < n; ++i) {
-      a.seq[i] = seq_ids[i0 + i];
-      a.n_read[i] = 0;
-      a.pps[i] = 1;
-      a.aux[i] = n_given == 4 ? pos[i0 + i] : 0;
-    }
-    e = launch_reader_valu(BF16, b, dh, a, s);
-    if (e != hipSuccess) return hip_fail(e, "in-block partial");
+    ra.null_kv = layer->null_row ? null_kv : nullptr;
+    ra.intra_w = intra;
+    ra.scale_log2 = scale_log2;
+    for (int i = 0; i < n; ++i) ra.pos[i] = n_given == 4 ? pos[i0 + i] : 0;
     e = launch_rows(D, dh, ra, pa, 1, s);
     if (e != hipSuccess) return hip_fail(e, "row reader");
     i0 += n;
