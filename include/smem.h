@@ -109,6 +109,14 @@ smem_status smem_store_destroy(smem_store* st);
 smem_status smem_store_put_block(smem_store* st, int32_t seq, int32_t block_idx,
                                  const void* k_rows, const void* v_rows, hipStream_t s);
 
+/* Insert precomputed rows of n_blocks blocks at once: block i's rows are
+ * rows i*b .. i*b+b-1 of k_rows, v_rows (device [n_blocks*b, H, dh]) and go to
+ * block block_idx[i] of sequence seq_ids[i].  All-or-nothing, errors as
+ * smem_store_put_block (duplicates are SMEM_EEXIST). */
+smem_status smem_store_put_blocks(smem_store* st, int32_t n_blocks, const int32_t* seq_ids,
+                                  const int32_t* block_idx, const void* k_rows, const void* v_rows,
+                                  hipStream_t s);
+
 /* Block-local encoder attention (Section 2, "Model"; Appendix A, "Encoder").
  * Each (block, head) pair is computed on its own:
  *   O = softmax_mask(Q K^T / sqrt(dh)) V,  the mask limited to the block.

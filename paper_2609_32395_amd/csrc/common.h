@@ -247,6 +247,15 @@ hipError_t launch_init_meta(int32_t* table, int32_t* n_live, size_t n_table, int
 hipError_t launch_meta(const MetaArgs& a, hipStream_t s);
 hipError_t launch_put_rows(int dtype, void* pages, int page, int H, int b, int dh,
                            const void* k_rows, const void* v_rows, hipStream_t s);
+// Row insert of n <= kMaxSlots blocks: block i's rows (k_rows/v_rows + i*b*H*dh) into page a.page[i].
+struct PutArgs {
+  void* pages;
+  const void* k_rows;
+  const void* v_rows;
+  int32_t H, b, dh;
+  int32_t page[kMaxSlots];
+};
+hipError_t launch_put_blocks(int dtype, const PutArgs& a, int n, hipStream_t s);
 hipError_t launch_scrub(void* page_base, size_t bytes, hipStream_t s);
 hipError_t launch_export(int dtype, const void* pages, const int32_t* live_page_seq, int n_live,
                          int H, int b, int dh, void* k_out, void* v_out, hipStream_t s);

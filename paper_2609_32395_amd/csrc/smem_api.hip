@@ -300,6 +300,56 @@ smem_status smem_store_put_block(smem_store* st, int32_t seq, int32_t block_idx,
   return SMEM_OK;
 }
 
+smem_status smem_store_put_blocks(smem_store* st, int32_t n_blocks, const int32_t* seq_ids, const int32_t* block_idx,
+                                  const void* k_rows, const void* v_rows, hipStream_t s) {
+  if (!st) return fail(SMEM_EINVAL, "store is NULL");
+  if (st->kind != 0) return fail(SMEM_EINVAL, "a row store takes smem_rows_put_block");
+  if (st->meta_only) return fail(SMEM_EINVAL, "metadata-only store");
+  const auto& d = st->d;
+  if (n_blocks < 0) return fail(SMEM_EINVAL, "n_blocks < 0");
+  if (n_blocks == 0) return SMEM_OK;
+  if (!seq_ids || !block_idx || !k_rows || !v_rows) return fail(SMEM_EINVAL, "seq_ids, block_idx, k_rows, v_rows are required");
+  if (!aligned16(k_rows) || !aligned16(v_rows)) return fail(SMEM_EINVAL, "rows must be 16-byte aligned");
+  std::set<std::pair<int32_t, int32_t>> seen;
+  for (int i = 0; i < n_blocks; ++i) {
+    const int32_t sq = seq_ids[i], j = block_idx[i];
+    if (sq < 0 || sq >= d.n_seq) return fail(SMEM_EINVAL, "seq_ids[%d] = %d out of range", i, sq);
+    if (j < 0 || j >= d.max_blocks) return fail(SMEM_EINVAL, "block_idx[%d] = %d out of range", i, j);
+    if (st->table[(size_t)sq * d.max_blocks + j] >= 0) return fail(SMEM_EEXIST, "block %d of sequence %d is occupied", j, sq);
+    if (!seen.insert({sq, j}).second) return fail(SMEM_EEXIST, "block %d of sequence %d given twice", j, sq);
+  }
+  if ((size_t)n_blocks > st->free_pages.size())
+    return fail(SMEM_ENOMEM, "%d blocks to insert, %zu free pages", n_blocks, st->free_pages.size());
+  std::vector<int32_t> pages(n_blocks), es_(n_blocks), eb_(n_blocks);
+  for (int i = 0; i < n_blocks; ++i) {
+    pages[i] = st->free_pages[st->free_pages.size() - 1 - i];
+    es_[i] = seq_ids[i];
+    eb_[i] = block_idx[i];
+  }
+  const size_t blk_bytes = (size_t)d.b * d.H * d.dh * esize(d.dtype);
+  for (int i0 = 0; i0 < n_blocks; i0 += kMaxSlots) {
+    const int n = std::min(kMaxSlots, n_blocks - i0);
+    PutArgs a;
+    memset(&a, 0, sizeof a);
+    a.pages = st->d_pages;
+    a.k_rows = (const char*)k_rows + i0 * blk_bytes;
+    a.v_rows = (const char*)v_rows + i0 * blk_bytes;
+    a.H = d.H; a.b = d.b; a.dh = d.dh;
+    for (int i = 0; i < n; ++i) a.page[i] = pages[i0 + i];
+    hipError_t e = launch_put_blocks(d.dtype, a, n, s);
+    if (e != hipSuccess) return hip_fail(e, "row insert");
+  }
+  smem_status r = push_edits(st, es_, eb_, pages, s);
+  if (r != SMEM_OK) return r;
+  st->free_pages.resize(st->free_pages.size() - n_blocks);
+  for (int i = 0; i < n_blocks; ++i) {
+    st->table[(size_t)seq_ids[i] * d.max_blocks + block_idx[i]] = pages[i];
+    auto& lv = st->live[seq_ids[i]];
+    lv.insert(std::lower_bound(lv.begin(), lv.end(), block_idx[i]), block_idx[i]);
+  }
+  return SMEM_OK;
+}
+
 smem_status smem_delete_block(smem_store* st, int32_t seq, int32_t block_idx, int32_t scrub, hipStream_t s) {
   if (!st) return fail(SMEM_EINVAL, "store is NULL");
   const auto& d = st->d;

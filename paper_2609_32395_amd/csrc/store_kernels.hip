@@ -95,17 +95,19 @@ hipError_t launch_meta(const MetaArgs& a, hipStream_t s) {
 // transposed value plane [dh][b] of every head.  One workgroup per head;
 // 16-byte loads and stores throughout, the value tile transposed through LDS.
 template <typename T>
-__global__ void __launch_bounds__(256) k_put_rows(T* __restrict__ pages, int page, int H, int b, int dh,
-                                                   const T* __restrict__ k_rows, const T* __restrict__ v_rows) {
+__global__ void __launch_bounds__(256) k_put_rows(PutArgs a) {
   constexpr int E = 16 / sizeof(T);
   extern __shared__ unsigned char smem_raw[];
   T* tile = reinterpret_cast<T*>(smem_raw);  // [b][dh + 1]
-  const int h = blockIdx.x;
-  T* kp = pages + page_head_offset(page, h, H, b, dh);
+  const int h = blockIdx.x, i = blockIdx.y;
+  const int H = a.H, b = a.b, dh = a.dh;
+  T* kp = (T*)a.pages + page_head_offset(a.page[i], h, H, b, dh);
   T* vp = kp + (size_t)b * dh;
+  const T* k_rows = (const T*)a.k_rows + (size_t)i * b * H * dh;
+  const T* v_rows = (const T*)a.v_rows + (size_t)i * b * H * dh;
   const int cpr = dh / E;
-  for (int i = threadIdx.x; i < b * cpr; i += blockDim.x) {
-    const int r = i / cpr, c = i % cpr;
+  for (int j = threadIdx.x; j < b * cpr; j += blockDim.x) {
+    const int r = j / cpr, c = j % cpr;
     const size_t src = ((size_t)r * H + h) * dh + c * E;
     *(u32x4*)(kp + r * dh + c * E) = *(const u32x4*)(k_rows + src);
     const u32x4 vv = *(const u32x4*)(v_rows + src);
@@ -116,8 +118,8 @@ __global__ void __launch_bounds__(256) k_put_rows(T* __restrict__ pages, int pag
   }
   __syncthreads();
   const int cpv = b / E;
-  for (int i = threadIdx.x; i < dh * cpv; i += blockDim.x) {
-    const int d = i / cpv, kc = i % cpv;
+  for (int j = threadIdx.x; j < dh * cpv; j += blockDim.x) {
+    const int d = j / cpv, kc = j % cpv;
     T vals[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) vals[e] = tile[(kc * E + e) * (dh + 1) + d];
@@ -127,18 +129,22 @@ __global__ void __launch_bounds__(256) k_put_rows(T* __restrict__ pages, int pag
   }
 }
 
+hipError_t launch_put_blocks(int dtype, const PutArgs& a, int n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const size_t es = dtype == F32 ? 4 : 2;
+  const size_t lds = (size_t)a.b * (a.dh + 1) * es;
+  if (dtype == F32) hipLaunchKernelGGL(k_put_rows<float>, dim3(a.H, n), dim3(256), lds, s, a);
+  else hipLaunchKernelGGL(k_put_rows<uint16_t>, dim3(a.H, n), dim3(256), lds, s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_put_rows(int dtype, void* pages, int page, int H, int b, int dh,
                            const void* k_rows, const void* v_rows, hipStream_t s) {
-  if (dtype == F32) {
-    size_t lds = (size_t)b * (dh + 1) * sizeof(float);
-    hipLaunchKernelGGL(k_put_rows<float>, dim3(H), dim3(256), lds, s, (float*)pages, page, H, b, dh,
-                       (const float*)k_rows, (const float*)v_rows);
-  } else {
-    size_t lds = (size_t)b * (dh + 1) * sizeof(uint16_t);
-    hipLaunchKernelGGL(k_put_rows<uint16_t>, dim3(H), dim3(256), lds, s, (uint16_t*)pages, page, H, b, dh,
-                       (const uint16_t*)k_rows, (const uint16_t*)v_rows);
-  }
-  return hipGetLastError();
+  PutArgs a;
+  a.pages = pages; a.k_rows = k_rows; a.v_rows = v_rows;
+  a.H = H; a.b = b; a.dh = dh;
+  a.page[0] = page;
+  return launch_put_blocks(dtype, a, 1, s);
 }
 
 __global__ void k_scrub(uint4* __restrict__ p, size_t n16) {

@@ -77,6 +77,7 @@ SIGNATURES = {
     "smem_store_create": (_I, [ctypes.POINTER(StoreDesc), _P, ctypes.c_size_t, _P, ctypes.POINTER(_P)]),
     "smem_store_destroy": (_I, [_P]),
     "smem_store_put_block": (_I, [_P, _I, _I, _P, _P, _P]),
+    "smem_store_put_blocks": (_I, [_P, _I, _IP, _IP, _P, _P, _P]),
     "smem_encode_blocks": (_I, [_P, ctypes.POINTER(AttnDesc), _I, _IP, _IP, _P, _P, _P, _P, _I, _P]),
     "smem_reencode_blocks": (_I, [_P, ctypes.POINTER(AttnDesc), _I, _IP, _IP, _P, _P, _P, _P, _I, _P]),
     "smem_reader_prefill_block": (_I, [_P, _I, _IP, _IP, _P, _P, _P, _P, _P, _P]),
@@ -326,6 +327,17 @@ def smem_store_put_block(st: Store, seq: int, block_idx: int, k_rows=None, v_row
         vp = _dev(v_rows, st.row_shape, st.dtype, "v_rows")
     _check(lib().smem_store_put_block(st.handle, int(seq), int(block_idx), kp, vp,
                                       None if st.meta_only else _stream(stream)))
+
+
+def smem_store_put_blocks(st: Store, seq_ids, block_idx, k_rows, v_rows, stream=None):
+    """Insert len(seq_ids) blocks at once; k_rows, v_rows [n*b, H, dh]."""
+    n = len(seq_ids)
+    if len(block_idx) != n:
+        raise ValueError("block_idx needs one entry per block")
+    shape = (n * st.b, st.H, st.dh)
+    kp = _dev(k_rows, shape, st.dtype, "k_rows")
+    vp = _dev(v_rows, shape, st.dtype, "v_rows")
+    _check(lib().smem_store_put_blocks(st.handle, n, _i32(seq_ids), _i32(block_idx), kp, vp, _stream(stream)))
 
 
 def smem_delete_block(st: Store, seq: int, block_idx: int, scrub: bool = False, stream=None):

@@ -188,3 +188,41 @@ def test_rows_swapped_maps_are_caught(monkeypatch):
     monkeypatch.setattr(O, "reader_decode_rows",
                         lambda st, wk, wv, *a, **k: orig(st, wv, wk, *a, **k))   # planted: maps swapped
     assert _fails(P.test_rows_decode_matches_sdpa_on_mapped_rows)
+
+
+# ---------------------------------------------------------------- whole-model oracle
+from oracle import smem_model as MO  # noqa: E402
+from tests import test_model_pins as MP  # noqa: E402
+
+
+def test_model_bidirectional_reader_self_attention_is_caught(monkeypatch):
+    orig = O.encode_blocks
+    monkeypatch.setattr(O, "encode_blocks", lambda q, k, v, mask=O.MASK_BIDIR: orig(q, k, v, O.MASK_BIDIR))
+    assert _fails(MP.test_blockwise_model_equals_masked_dense_pass, 12)
+
+
+def test_model_memory_without_layer_norm_is_caught(monkeypatch):
+    monkeypatch.setattr(MO.Model, "memory_rows", lambda self, tokens, blocks: _rows_no_ln(self, tokens, blocks))
+    assert _fails(MP.test_blockwise_model_equals_masked_dense_pass, 12)
+
+
+def _rows_no_ln(self, tokens, blocks):
+    x = self.embed(tokens, blocks)
+    W = self.W
+    for l in range(self.E):
+        p = f"enc{l}."
+        q, k, v = self._attn_in(MO.layer_norm(x, W[p + "ln1_g"], W[p + "ln1_b"]), W[p + "w_qkv"])
+        x = x + MO.linear(O.encode_blocks(q, k, v, O.MASK_BIDIR).reshape(x.shape), W[p + "w_o"])
+        h = MO.layer_norm(x, W[p + "ln2_g"], W[p + "ln2_b"])
+        x = x + MO.linear(MO.gelu(MO.linear(h, W[p + "w_ff1"])), W[p + "w_ff2"])
+    return x                                        # planted: the memory LayerNorm dropped
+
+
+def test_model_unclamped_positions_are_caught(monkeypatch):
+    def embed(self, tokens, blocks):
+        tokens = np.asarray(tokens)
+        b = tokens.shape[1]
+        pos = (np.asarray(blocks)[:, None] % (self.n_pos // b)) * b + np.arange(b)[None, :]   # planted: wraps
+        return self.W["tok_emb"][tokens] + self.W["pos_emb"][pos]
+    monkeypatch.setattr(MO.Model, "embed", embed)
+    assert _fails(MP.test_blockwise_model_equals_masked_dense_pass, 12)
