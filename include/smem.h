@@ -159,7 +159,8 @@ smem_status smem_reencode_blocks(smem_store* st, const smem_attn_desc* shape, in
  * attention alone (the paper's self-attention sub-layer).  An empty key set
  * gives a zero output.
  * q, k_intra, v_intra, out: device [n_seq*b, H, dh].  null_kv: device
- * [2, H, dh] or NULL.  A sequence may appear more than once. */
+ * [2, H, dh] or NULL.  A sequence may appear more than once (with several
+ * query blocks: a block-parallel pass over one sequence). */
 smem_status smem_reader_prefill_block(smem_store* st, int32_t n_seq, const int32_t* seq_ids,
                                       const int32_t* query_block, const void* q,
                                       const void* k_intra, const void* v_intra,
@@ -318,6 +319,75 @@ smem_status smem_reader_decode_rows(smem_store* st, const smem_rows_layer* layer
                                     const int32_t* seq_ids, const int32_t* query_block, const int32_t* pos,
                                     const void* q, const void* k_new, const void* v_new, void* k_cache,
                                     void* v_cache, void* out, hipStream_t s);
+
+/* ------------------------------------------------------------------------
+ * The whole model at given weights (Section 2, "Model"; Appendix A).
+ * Encoder: E pre-LN layers of block-local bidirectional attention and a GELU
+ * feed-forward (hidden 4d); a block's memory rows are the LayerNorm of the
+ * encoder's final state.  Reader: D pre-LN layers, each block-local causal
+ * self-attention, cross-attention into the memory of strictly earlier blocks
+ * with the null row (one learned d-vector through each layer's key and value
+ * maps), and the feed-forward; then a final LayerNorm and the output head.
+ * Input: token embedding plus a learned position embedding indexed by
+ * min(block, n_pos/b - 1) * b + in-block offset (none when n_pos = 0).
+ * Linear maps are x -> x W^T, W stored [out, in], no biases; LayerNorm
+ * eps 1e-5 with a scale and a shift; GELU is the exact (erf) form.  bf16
+ * weights and activations, fp32 accumulation, fp32 logits.
+ * Each reader layer keeps its keys and values (the memory rows through its
+ * maps) in a store of its own, so encode, serve, delete and re-encode are the
+ * store operations applied to every layer.
+ *
+ * Weights: an array of smem_model_n_weights() device pointers, in order:
+ *   tok_emb [vocab, d], pos_emb [n_pos, d] (NULL when n_pos = 0),
+ *   per encoder layer: ln1_g, ln1_b [d], w_qkv [3d, d], w_o [d, d],
+ *                      ln2_g, ln2_b [d], w_ff1 [4d, d], w_ff2 [d, 4d],
+ *   mem_ln_g, mem_ln_b [d], null_row [d],
+ *   per reader layer:  ln1_g, ln1_b, w_qkv [3d, d], w_o [d, d], ln2_g, ln2_b,
+ *                      w_q, w_k, w_v, w_oc [d, d], ln3_g, ln3_b,
+ *                      w_ff1 [4d, d], w_ff2 [d, 4d],
+ *   fin_g, fin_b [d], w_head [vocab, d].
+ * The weights stay owned by the caller and must outlive the model.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t E;            /* encoder layers (>= 0) */
+  int32_t D;            /* reader layers (>= 1) */
+  int32_t d, H, dh;     /* width = H * dh, a multiple of 64, <= 2048; dh in {32, 64, 128} */
+  int32_t b;            /* block size: 64 */
+  int32_t vocab;
+  int32_t n_pos;        /* learned positions, a multiple of b; 0: none */
+  int32_t n_seq, max_blocks, n_pages;   /* every reader layer's memory store */
+  int32_t max_tokens;   /* tokens one launch sequence processes (a multiple of b, <= 128 b);
+                           longer calls are cut into chunks of this size */
+} smem_model_desc;
+
+typedef struct smem_model smem_model;
+
+/* Number of weight pointers, and device bytes of the model's pool (the
+ * reader layers' stores, the activation workspace, the mapped null rows). */
+int32_t smem_model_n_weights(const smem_model_desc* desc);
+size_t smem_model_bytes(const smem_model_desc* desc);
+
+smem_status smem_model_create(const smem_model_desc* desc, const void* const* weights, void* dev_pool,
+                              size_t pool_bytes, hipStream_t s, smem_model** out);
+smem_status smem_model_destroy(smem_model* m);
+
+/* Encode n_blocks blocks of sequence seq (tokens: device int32 [n_blocks*b];
+ * block_idx host) and insert their keys and values into every reader layer:
+ * the append of Section 2.  All-or-nothing as smem_encode_blocks. */
+smem_status smem_model_encode(smem_model* m, int32_t seq, int32_t n_blocks, const int32_t* block_idx,
+                              const int32_t* tokens, hipStream_t s);
+
+/* Reader pass for n_blocks query blocks of sequence seq (tokens: device int32
+ * [n_blocks*b]; query_block host): each block reads the memory of the live
+ * blocks below it.  logits: device fp32 [n_blocks*b, vocab].  A fully cached
+ * context is served by reading its final block alone (block-skip serving,
+ * Section 3.1); the cold pass encodes every block and reads every block. */
+smem_status smem_model_read(smem_model* m, int32_t seq, int32_t n_blocks, const int32_t* query_block,
+                            const int32_t* tokens, float* logits, hipStream_t s);
+
+/* Exact deletion of block block_idx of sequence seq from every reader layer
+ * (Theorem 1).  SMEM_ENOENT if absent. */
+smem_status smem_model_delete_block(smem_model* m, int32_t seq, int32_t block_idx, hipStream_t s);
 
 /* Host-side facts about a store: pages in use and free. */
 smem_status smem_store_stats(const smem_store* st, int32_t* pages_used, int32_t* pages_free);

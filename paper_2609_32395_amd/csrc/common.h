@@ -7,6 +7,8 @@
 #include <stdint.h>
 #include <stddef.h>
 
+#include "smem.h"
+
 namespace smem {
 
 // ---------------------------------------------------------------- constants
@@ -275,6 +277,8 @@ hipError_t launch_prefill_mfma(int b, int dh, const ReaderArgs& a, hipStream_t s
 hipError_t launch_rows(int d, int dh, const RowsArgs& a, const RowsPrepArgs& pa, int stage, hipStream_t s);
 // Plain device copy (16-byte multiples).
 hipError_t launch_copy16(void* dst, const void* src, size_t bytes, hipStream_t s);
+// Record a failure for smem_last_error() (defined with the C ABI); returns st.
+smem_status set_error(smem_status st, const char* msg);
 // Rotary table of n_phases rows for heads of width dh, computed in fp64.
 hipError_t launch_rope_table(float* table, int dh, int n_phases, double base, hipStream_t s);
 

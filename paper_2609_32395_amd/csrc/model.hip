@@ -1,0 +1,518 @@
+// The whole SMem model at given weights (Section 2, "Model"; Appendix A):
+// the encoder stack producing memory rows, one key/value store per reader
+// layer, the reader stack and the output head, driven from the host on the
+// caller's stream.  Attention runs on the library's kernels (block-local
+// encoder kernel for the encoder and the readers' self-attention, the
+// block-skip reader for their cross-attention); the linear maps, LayerNorm
+// and the embedding run on the kernels below.
+//
+// Linear maps are y = x W^T with W stored [out, in] (a linear layer's
+// layout): both MFMA operands then run along the reduction dimension, so a
+// lane's 8 k-values are 16 contiguous bytes of an x row and of a W row.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <set>
+#include <vector>
+
+#include "common.h"
+#include "smem.h"
+
+namespace smem {
+
+typedef __bf16 bf16x8m __attribute__((ext_vector_type(8)));
+
+enum LinEpi : int { kLinStore = 0, kLinGelu = 1, kLinResid = 2, kLinF32 = 3, kLinSplit = 4 };
+
+struct LinArgs {
+  const uint16_t* x;   // [M][ldx], K used
+  const uint16_t* w;   // output rows n < n2: w + n*K
+  const uint16_t* w2;  // output rows n >= n2: w2 + (n - n2)*K
+  const uint16_t* res; // residual [M][ldy] (kLinResid; may equal y)
+  uint16_t* y;         // [M][ldy]
+  uint16_t* y1;        // kLinSplit: columns [ns, 2ns) -> y1, [2ns, 3ns) -> y2 (each [M][ns])
+  uint16_t* y2;
+  float* yf;           // kLinF32: [M][ldy]
+  int32_t M, N, K, ldx, ldy, n2, ns;
+};
+
+__device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
+
+// One 64 x 64 output tile per workgroup, each wave a 32 x 32 quarter as 2 x 2
+// MFMA tiles (16x16x32 bf16); operands straight from global memory (rows of
+// x and of W, 16 bytes per lane), fp32 accumulation, fused epilogue.
+template <int EPI>
+__global__ void __launch_bounds__(256) k_linear(LinArgs a) {
+  const int n0 = blockIdx.x * 64, m0 = blockIdx.y * 64;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int kofs = (lane >> 4) * 8;
+  const uint16_t* ap[2];
+  bool av[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = m0 + wm * 32 + i * 16 + (lane & 15);
+    av[i] = r < a.M;
+    ap[i] = a.x + (size_t)(av[i] ? r : 0) * a.ldx + kofs;
+  }
+  const uint16_t* bp[2];
+  bool bv[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int n = n0 + wn * 32 + j * 16 + (lane & 15);
+    bv[j] = n < a.N;
+    const int nn = bv[j] ? n : 0;
+    bp[j] = (nn < a.n2 ? a.w + (size_t)nn * a.K : a.w2 + (size_t)(nn - a.n2) * a.K) + kofs;
+  }
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+#pragma unroll 4
+  for (int k0 = 0; k0 < a.K; k0 += 32) {
+    u32x4 A[2], B[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) A[i] = av[i] ? *(const u32x4*)(ap[i] + k0) : zero;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) B[j] = bv[j] ? *(const u32x4*)(bp[j] + k0) : zero;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8m, A[i]),
+                                                            __builtin_bit_cast(bf16x8m, B[j]), acc[i][j], 0, 0, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int n = n0 + wn * 32 + j * 16 + (lane & 15);
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const int m = m0 + wm * 32 + i * 16 + 4 * (lane >> 4) + ii;
+        if (m >= a.M || n >= a.N) continue;
+        const float v = acc[i][j][ii];
+        if constexpr (EPI == kLinF32) {
+          a.yf[(size_t)m * a.ldy + n] = v;
+        } else if constexpr (EPI == kLinGelu) {
+          a.y[(size_t)m * a.ldy + n] = f32_to_bf16_bits(gelu_erf(v));
+        } else if constexpr (EPI == kLinResid) {
+          const size_t o = (size_t)m * a.ldy + n;
+          a.y[o] = f32_to_bf16_bits(v + bf16_bits_to_f32(a.res[o]));
+        } else if constexpr (EPI == kLinSplit) {
+          const int g = n / a.ns, c = n - g * a.ns;
+          uint16_t* dst = g == 0 ? a.y : (g == 1 ? a.y1 : a.y2);
+          dst[(size_t)m * a.ns + c] = f32_to_bf16_bits(v);
+        } else {
+          a.y[(size_t)m * a.ldy + n] = f32_to_bf16_bits(v);
+        }
+      }
+    }
+  }
+}
+
+template <int EPI>
+static hipError_t linear(const LinArgs& a, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (a.K % 32) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((k_linear<EPI>), dim3((a.N + 63) / 64, (a.M + 63) / 64), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// LayerNorm of rows of width d (d % 8 == 0, d <= 2048): one wave per row,
+// statistics in fp32 (mean, then the centred second moment), eps 1e-5.
+__global__ void __launch_bounds__(256) k_layernorm(const uint16_t* __restrict__ x, const uint16_t* __restrict__ g,
+                                                   const uint16_t* __restrict__ bta, uint16_t* __restrict__ y,
+                                                   int rows, int d) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const uint16_t* xr = x + (size_t)row * d;
+  float v[4][8];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = i * 512 + lane * 8;
+    if (c < d) {
+      Chunk<uint16_t>::unpack(*(const u32x4*)(xr + c), v[i]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s += v[i][e];
+    }
+  }
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) s += __shfl_xor(s, o);
+  const float mean = s / d;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = i * 512 + lane * 8;
+    if (c < d) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float t = v[i][e] - mean;
+        q += t * t;
+      }
+    }
+  }
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) q += __shfl_xor(q, o);
+  const float rstd = 1.f / sqrtf(q / d + 1e-5f);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = i * 512 + lane * 8;
+    if (c < d) {
+      float gf[8], bf[8];
+      Chunk<uint16_t>::unpack(*(const u32x4*)(g + c), gf);
+      Chunk<uint16_t>::unpack(*(const u32x4*)(bta + c), bf);
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float y0 = (v[i][2 * e] - mean) * rstd * gf[2 * e] + bf[2 * e];
+        const float y1 = (v[i][2 * e + 1] - mean) * rstd * gf[2 * e + 1] + bf[2 * e + 1];
+        w[e] = (uint32_t)f32_to_bf16_bits(y0) | ((uint32_t)f32_to_bf16_bits(y1) << 16);
+      }
+      *(u32x4*)(y + (size_t)row * d + c) = u32x4{w[0], w[1], w[2], w[3]};
+    }
+  }
+}
+
+struct EmbArgs {
+  const int32_t* tokens;   // [rows]
+  const uint16_t* tok_emb; // [vocab][d]
+  const uint16_t* pos_emb; // [n_pos][d] or NULL
+  uint16_t* x;             // [rows][d]
+  int32_t rows, d, b, vocab, slots;
+  int32_t blk[kMaxSlots];  // block index of each b-row group
+};
+
+// x[r] = tok_emb[token] + pos_emb[min(block, slots-1)*b + offset]; one wave per
+// row.  A token id outside [0, vocab) reads row 0 (it cannot read past the table).
+__global__ void __launch_bounds__(256) k_embed(EmbArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= a.rows) return;
+  int tok = a.tokens[r];
+  if (tok < 0 || tok >= a.vocab) tok = 0;
+  const int t = r % a.b;
+  const int pos = min(a.blk[r / a.b], a.slots - 1) * a.b + t;
+  for (int c = lane * 8; c < a.d; c += 512) {
+    float e[8], p[8];
+    Chunk<uint16_t>::unpack(*(const u32x4*)(a.tok_emb + (size_t)tok * a.d + c), e);
+    if (a.pos_emb) {
+      Chunk<uint16_t>::unpack(*(const u32x4*)(a.pos_emb + (size_t)pos * a.d + c), p);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) e[i] += p[i];
+    }
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f32_to_bf16_bits(e[2 * i]) | ((uint32_t)f32_to_bf16_bits(e[2 * i + 1]) << 16);
+    *(u32x4*)(a.x + (size_t)r * a.d + c) = u32x4{w[0], w[1], w[2], w[3]};
+  }
+}
+
+}  // namespace smem
+
+using namespace smem;
+
+// ---------------------------------------------------------------- host runtime
+
+struct smem_model {
+  smem_model_desc d;
+  std::vector<const uint16_t*> W;
+  std::vector<smem_store*> stores;   // one per reader layer
+  char* pool = nullptr;
+  uint16_t *x = nullptr, *h = nullptr, *q = nullptr, *k = nullptr, *v = nullptr, *o = nullptr, *f = nullptr;
+  uint16_t* null_kv = nullptr;       // [D][2][d]
+};
+
+namespace {
+
+smem_status mfail(smem_status st, const char* msg) { return set_error(st, msg); }
+
+size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int n_weights(const smem_model_desc* d) { return 2 + 8 * d->E + 3 + 14 * d->D + 3; }
+
+bool desc_ok(const smem_model_desc* d) {
+  if (!d) return false;
+  if (d->E < 0 || d->D < 1 || d->b != 64 || d->H < 1 || !(d->dh == 32 || d->dh == 64 || d->dh == 128)) return false;
+  if (d->d != d->H * d->dh || d->d % 64 || d->d > 2048) return false;
+  if (d->vocab < 1 || d->n_pos < 0 || d->n_pos % d->b) return false;
+  if (d->n_seq < 1 || d->max_blocks < 1 || d->n_pages < 1) return false;
+  if (d->max_tokens < d->b || d->max_tokens % d->b || d->max_tokens > kMaxSlots * d->b) return false;
+  return true;
+}
+
+smem_store_desc store_desc(const smem_model_desc* d) {
+  return smem_store_desc{d->n_seq, d->max_blocks, d->n_pages, d->b, d->H, d->dh, SMEM_BF16};
+}
+
+struct Layout {
+  size_t store_bytes, off_ws, off_null, total;
+};
+
+bool layout(const smem_model_desc* d, Layout* L) {
+  if (!desc_ok(d)) return false;
+  const smem_store_desc sd = store_desc(d);
+  L->store_bytes = a256(smem_store_bytes(&sd));
+  if (L->store_bytes == 0) return false;
+  size_t off = L->store_bytes * d->D;
+  L->off_ws = off;
+  off += a256((size_t)d->max_tokens * d->d * 2) * 6 + a256((size_t)d->max_tokens * 4 * d->d * 2);
+  L->off_null = off;
+  off += a256((size_t)d->D * 2 * d->d * 2);
+  L->total = off;
+  return true;
+}
+
+// weight pointers by role
+struct Wts {
+  const smem_model* m;
+  const uint16_t* at(int i) const { return m->W[i]; }
+  const uint16_t* tok() const { return at(0); }
+  const uint16_t* pos() const { return m->d.n_pos ? at(1) : nullptr; }
+  const uint16_t* enc(int l, int i) const { return at(2 + 8 * l + i); }
+  int base_mem() const { return 2 + 8 * m->d.E; }
+  const uint16_t* mem_g() const { return at(base_mem()); }
+  const uint16_t* mem_b() const { return at(base_mem() + 1); }
+  const uint16_t* null_row() const { return at(base_mem() + 2); }
+  const uint16_t* dec(int l, int i) const { return at(base_mem() + 3 + 14 * l + i); }
+  int base_fin() const { return base_mem() + 3 + 14 * m->d.D; }
+  const uint16_t* fin_g() const { return at(base_fin()); }
+  const uint16_t* fin_b() const { return at(base_fin() + 1); }
+  const uint16_t* head() const { return at(base_fin() + 2); }
+};
+enum { E_LN1G, E_LN1B, E_QKV, E_O, E_LN2G, E_LN2B, E_FF1, E_FF2 };
+enum { R_LN1G, R_LN1B, R_QKV, R_O, R_LN2G, R_LN2B, R_Q, R_K, R_V, R_OC, R_LN3G, R_LN3B, R_FF1, R_FF2 };
+
+hipError_t lnorm(const uint16_t* x, const uint16_t* g, const uint16_t* b, uint16_t* y, int rows, int d, hipStream_t s) {
+  hipLaunchKernelGGL(k_layernorm, dim3((rows + 3) / 4), dim3(256), 0, s, x, g, b, y, rows, d);
+  return hipGetLastError();
+}
+
+LinArgs lin(const uint16_t* x, int ldx, const uint16_t* w, int M, int N, int K, uint16_t* y, int ldy) {
+  LinArgs a;
+  memset(&a, 0, sizeof a);
+  a.x = x; a.ldx = ldx; a.w = w; a.w2 = w; a.n2 = N;
+  a.M = M; a.N = N; a.K = K; a.y = y; a.ldy = ldy;
+  return a;
+}
+
+#define MCHECK(expr, what)                                   \
+  do {                                                       \
+    hipError_t e_ = (expr);                                  \
+    if (e_ != hipSuccess) return mfail(SMEM_EHIP, what);     \
+  } while (0)
+#define MSTATUS(expr)                                        \
+  do {                                                       \
+    smem_status r_ = (expr);                                 \
+    if (r_ != SMEM_OK) return r_;                            \
+  } while (0)
+
+// embed one chunk of nb blocks (tokens [nb*b] on the device) into m->x
+smem_status embed(smem_model* m, int nb, const int32_t* blocks, const int32_t* tokens, hipStream_t s) {
+  const auto& d = m->d;
+  Wts w{m};
+  EmbArgs a;
+  memset(&a, 0, sizeof a);
+  a.tokens = tokens; a.tok_emb = w.tok(); a.pos_emb = w.pos(); a.x = m->x;
+  a.rows = nb * d.b; a.d = d.d; a.b = d.b; a.vocab = d.vocab; a.slots = d.n_pos ? d.n_pos / d.b : 1;
+  for (int i = 0; i < nb; ++i) a.blk[i] = blocks[i];
+  hipLaunchKernelGGL(k_embed, dim3((a.rows + 3) / 4), dim3(256), 0, s, a);
+  MCHECK(hipGetLastError(), "embedding");
+  return SMEM_OK;
+}
+
+// x += attention-sublayer / feed-forward sublayer helpers
+smem_status ffn(smem_model* m, int rows, const uint16_t* g, const uint16_t* b, const uint16_t* w1, const uint16_t* w2,
+                hipStream_t s) {
+  const int D = m->d.d;
+  MCHECK(lnorm(m->x, g, b, m->h, rows, D, s), "layernorm");
+  MCHECK(linear<kLinGelu>(lin(m->h, D, w1, rows, 4 * D, D, m->f, 4 * D), s), "ffn up");
+  LinArgs a = lin(m->f, 4 * D, w2, rows, D, 4 * D, m->x, D);
+  a.res = m->x;
+  MCHECK(linear<kLinResid>(a, s), "ffn down");
+  return SMEM_OK;
+}
+
+smem_status self_attn(smem_model* m, int rows, int nb, const uint16_t* g, const uint16_t* b, const uint16_t* wqkv,
+                      const uint16_t* wo, int mask, hipStream_t s) {
+  const int D = m->d.d;
+  MCHECK(lnorm(m->x, g, b, m->h, rows, D, s), "layernorm");
+  LinArgs a = lin(m->h, D, wqkv, rows, 3 * D, D, m->q, D);
+  a.y1 = m->k; a.y2 = m->v; a.ns = D;
+  MCHECK(linear<kLinSplit>(a, s), "qkv");
+  const smem_attn_desc shape{m->d.b, m->d.H, m->d.dh, SMEM_BF16};
+  MSTATUS(smem_encode_blocks(nullptr, &shape, nb, nullptr, nullptr, m->q, m->k, m->v, m->o, mask, s));
+  LinArgs o = lin(m->o, D, wo, rows, D, D, m->x, D);
+  o.res = m->x;
+  MCHECK(linear<kLinResid>(o, s), "attention out");
+  return SMEM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t smem_model_bytes(const smem_model_desc* desc) {
+  Layout L;
+  return layout(desc, &L) ? L.total : 0;
+}
+
+int32_t smem_model_n_weights(const smem_model_desc* desc) { return desc_ok(desc) ? n_weights(desc) : 0; }
+
+smem_status smem_model_create(const smem_model_desc* desc, const void* const* weights, void* dev_pool,
+                              size_t pool_bytes, hipStream_t s, smem_model** out) {
+  if (!out) return mfail(SMEM_EINVAL, "out is NULL");
+  *out = nullptr;
+  Layout L;
+  if (!layout(desc, &L))
+    return mfail(SMEM_EINVAL, "invalid model descriptor (b = 64; dh in {32,64,128}; d = H*dh, a multiple of 64, "
+                              "<= 2048; n_pos a multiple of b; max_tokens a multiple of b, <= 128*b)");
+  if (!weights || !dev_pool) return mfail(SMEM_EINVAL, "weights and dev_pool are required");
+  if (((uintptr_t)dev_pool & 255u) != 0) return mfail(SMEM_EINVAL, "dev_pool must be 256-byte aligned");
+  if (pool_bytes < L.total) return mfail(SMEM_ENOMEM, "pool too small for the model");
+  const int nw = n_weights(desc);
+  for (int i = 0; i < nw; ++i) {
+    if (i == 1 && desc->n_pos == 0) continue;
+    if (!weights[i] || ((uintptr_t)weights[i] & 15u)) return mfail(SMEM_EINVAL, "a weight pointer is NULL or not 16-byte aligned");
+  }
+  smem_model* m = new (std::nothrow) smem_model();
+  if (!m) return mfail(SMEM_ENOMEM, "host allocation failed");
+  m->d = *desc;
+  m->pool = (char*)dev_pool;
+  for (int i = 0; i < nw; ++i) m->W.push_back((const uint16_t*)weights[i]);
+  const smem_store_desc sd = store_desc(desc);
+  for (int l = 0; l < desc->D; ++l) {
+    smem_store* st = nullptr;
+    smem_status r = smem_store_create(&sd, m->pool + L.store_bytes * l, L.store_bytes, s, &st);
+    if (r != SMEM_OK) {
+      smem_model_destroy(m);
+      return r;
+    }
+    m->stores.push_back(st);
+  }
+  const size_t T = desc->max_tokens, D = desc->d;
+  char* ws = m->pool + L.off_ws;
+  uint16_t** bufs[6] = {&m->x, &m->h, &m->q, &m->k, &m->v, &m->o};
+  for (int i = 0; i < 6; ++i) {
+    *bufs[i] = (uint16_t*)ws;
+    ws += a256(T * D * 2);
+  }
+  m->f = (uint16_t*)ws;
+  m->null_kv = (uint16_t*)(m->pool + L.off_null);
+  // the null row through every reader layer's key and value maps, once
+  Wts w{m};
+  for (int l = 0; l < desc->D; ++l) {
+    LinArgs a = lin(w.null_row(), (int)D, w.dec(l, R_K), 1, 2 * (int)D, (int)D, m->null_kv + (size_t)l * 2 * D, 2 * (int)D);
+    a.w2 = w.dec(l, R_V);
+    a.n2 = (int)D;
+    if (linear<kLinStore>(a, s) != hipSuccess) {
+      smem_model_destroy(m);
+      return mfail(SMEM_EHIP, "null row maps");
+    }
+  }
+  *out = m;
+  return SMEM_OK;
+}
+
+smem_status smem_model_destroy(smem_model* m) {
+  if (!m) return SMEM_OK;
+  for (smem_store* st : m->stores) smem_store_destroy(st);
+  delete m;
+  return SMEM_OK;
+}
+
+smem_status smem_model_encode(smem_model* m, int32_t seq, int32_t n_blocks, const int32_t* block_idx,
+                              const int32_t* tokens, hipStream_t s) {
+  if (!m) return mfail(SMEM_EINVAL, "model is NULL");
+  const auto& d = m->d;
+  if (n_blocks < 0) return mfail(SMEM_EINVAL, "n_blocks < 0");
+  if (n_blocks == 0) return SMEM_OK;
+  if (!block_idx || !tokens) return mfail(SMEM_EINVAL, "block_idx and tokens are required");
+  if (seq < 0 || seq >= d.n_seq) return mfail(SMEM_EINVAL, "seq out of range");
+  std::set<int32_t> seen;
+  for (int i = 0; i < n_blocks; ++i) {
+    if (block_idx[i] < 0 || block_idx[i] >= d.max_blocks) return mfail(SMEM_EINVAL, "block index out of range");
+    if (!seen.insert(block_idx[i]).second) return mfail(SMEM_EEXIST, "a block index is given twice");
+  }
+  // every layer's store holds the same blocks: check occupancy and space on the first
+  {
+    int32_t n_live = 0;
+    std::vector<int32_t> live(d.max_blocks);
+    MSTATUS(smem_store_export(m->stores[0], seq, live.data(), &n_live, nullptr, nullptr, s));
+    for (int i = 0; i < n_live; ++i)
+      if (seen.count(live[i])) return mfail(SMEM_EEXIST, "a block index is occupied");
+    int32_t used = 0, free_pages = 0;
+    MSTATUS(smem_store_stats(m->stores[0], &used, &free_pages));
+    if (free_pages < n_blocks) return mfail(SMEM_ENOMEM, "not enough free pages");
+  }
+  Wts w{m};
+  const int cb = d.max_tokens / d.b, D = d.d;
+  for (int i0 = 0; i0 < n_blocks; i0 += cb) {
+    const int nb = std::min(cb, n_blocks - i0), rows = nb * d.b;
+    MSTATUS(embed(m, nb, block_idx + i0, tokens + (size_t)i0 * d.b, s));
+    for (int l = 0; l < d.E; ++l) {
+      MSTATUS(self_attn(m, rows, nb, w.enc(l, E_LN1G), w.enc(l, E_LN1B), w.enc(l, E_QKV), w.enc(l, E_O),
+                        SMEM_MASK_BIDIR, s));
+      MSTATUS(ffn(m, rows, w.enc(l, E_LN2G), w.enc(l, E_LN2B), w.enc(l, E_FF1), w.enc(l, E_FF2), s));
+    }
+    MCHECK(lnorm(m->x, w.mem_g(), w.mem_b(), m->h, rows, D, s), "memory layernorm");
+    std::vector<int32_t> seqs(nb, seq);
+    for (int l = 0; l < d.D; ++l) {
+      LinArgs a = lin(m->h, D, w.dec(l, R_K), rows, 2 * D, D, m->q, D);
+      a.w2 = w.dec(l, R_V); a.n2 = D; a.y1 = m->k; a.ns = D;
+      MCHECK(linear<kLinSplit>(a, s), "memory key/value maps");
+      MSTATUS(smem_store_put_blocks(m->stores[l], nb, seqs.data(), block_idx + i0, m->q, m->k, s));
+    }
+  }
+  return SMEM_OK;
+}
+
+smem_status smem_model_read(smem_model* m, int32_t seq, int32_t n_blocks, const int32_t* query_block,
+                            const int32_t* tokens, float* logits, hipStream_t s) {
+  if (!m) return mfail(SMEM_EINVAL, "model is NULL");
+  const auto& d = m->d;
+  if (n_blocks < 0) return mfail(SMEM_EINVAL, "n_blocks < 0");
+  if (n_blocks == 0) return SMEM_OK;
+  if (!query_block || !tokens || !logits) return mfail(SMEM_EINVAL, "query_block, tokens and logits are required");
+  if (seq < 0 || seq >= d.n_seq) return mfail(SMEM_EINVAL, "seq out of range");
+  for (int i = 0; i < n_blocks; ++i)
+    if (query_block[i] < 0 || query_block[i] > d.max_blocks) return mfail(SMEM_EINVAL, "query block out of range");
+  Wts w{m};
+  const int cb = d.max_tokens / d.b, D = d.d;
+  for (int i0 = 0; i0 < n_blocks; i0 += cb) {
+    const int nb = std::min(cb, n_blocks - i0), rows = nb * d.b;
+    MSTATUS(embed(m, nb, query_block + i0, tokens + (size_t)i0 * d.b, s));
+    std::vector<int32_t> seqs(nb, seq);
+    for (int l = 0; l < d.D; ++l) {
+      MSTATUS(self_attn(m, rows, nb, w.dec(l, R_LN1G), w.dec(l, R_LN1B), w.dec(l, R_QKV), w.dec(l, R_O),
+                        SMEM_MASK_CAUSAL, s));
+      // cross-attention into the memory of strictly earlier blocks, with the null row
+      MCHECK(lnorm(m->x, w.dec(l, R_LN2G), w.dec(l, R_LN2B), m->h, rows, D, s), "layernorm");
+      MCHECK(linear<kLinStore>(lin(m->h, D, w.dec(l, R_Q), rows, D, D, m->q, D), s), "cross-attention query");
+      MSTATUS(smem_reader_prefill_block(m->stores[l], nb, seqs.data(), query_block + i0, m->q, nullptr, nullptr,
+                                        m->null_kv + (size_t)l * 2 * D, m->o, s));
+      LinArgs o = lin(m->o, D, w.dec(l, R_OC), rows, D, D, m->x, D);
+      o.res = m->x;
+      MCHECK(linear<kLinResid>(o, s), "cross-attention out");
+      MSTATUS(ffn(m, rows, w.dec(l, R_LN3G), w.dec(l, R_LN3B), w.dec(l, R_FF1), w.dec(l, R_FF2), s));
+    }
+    MCHECK(lnorm(m->x, w.fin_g(), w.fin_b(), m->h, rows, D, s), "final layernorm");
+    LinArgs hd = lin(m->h, D, w.head(), rows, d.vocab, D, nullptr, d.vocab);
+    hd.yf = logits + (size_t)i0 * d.b * d.vocab;
+    MCHECK(linear<kLinF32>(hd, s), "output head");
+  }
+  return SMEM_OK;
+}
+
+smem_status smem_model_delete_block(smem_model* m, int32_t seq, int32_t block_idx, hipStream_t s) {
+  if (!m) return mfail(SMEM_EINVAL, "model is NULL");
+  for (smem_store* st : m->stores) MSTATUS(smem_delete_block(st, seq, block_idx, 0, s));
+  return SMEM_OK;
+}
+
+}  // extern "C"

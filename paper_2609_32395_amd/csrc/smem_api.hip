@@ -60,6 +60,12 @@ smem_status fail(smem_status st, const char* fmt, ...) {
   return st;
 }
 
+}  // namespace
+
+smem_status smem::set_error(smem_status st, const char* msg) { return fail(st, "%s", msg); }
+
+namespace {
+
 smem_status hip_fail(hipError_t e, const char* what) {
   return fail(SMEM_EHIP, "%s: %s", what, hipGetErrorString(e));
 }
@@ -73,13 +79,19 @@ bool shape_ok(int b, int H, int dh, int dtype) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Query slots of one prefill launch: a slot is a (sequence, query block) pair,
+// so one sequence may fill several (a block-parallel pass over its blocks).
+int prefill_slots(const smem_store_desc* d) {
+  return (int)std::min<int64_t>((int64_t)d->n_seq * d->max_blocks, std::min(kMaxSlots, kPrefillSlotChunk));
+}
+
 bool layout_of(const smem_store_desc* d, DevLayout* L) {
   if (!d) return false;
   if (d->n_seq < 1 || d->max_blocks < 1 || d->n_pages < 1) return false;
   if (!shape_ok(d->b, d->H, d->dh, d->dtype)) return false;
   const size_t nt = (size_t)d->n_seq * d->max_blocks;
   const size_t dec_rows = (size_t)d->n_seq * d->H;
-  const size_t pre_rows = (size_t)std::min(d->n_seq, kPrefillSlotChunk) * d->b * d->H;
+  const size_t pre_rows = (size_t)prefill_slots(d) * d->b * d->H;
   L->ws_floats = std::max(dec_rows, pre_rows) * kSplitStride * (d->dh + 4);
   size_t off = 0;
   L->off_table = off;     off = align256(off + nt * 4);
@@ -544,7 +556,7 @@ static smem_status prefill_impl(smem_store* st, const smem_rope* rope, int32_t n
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
   const size_t es = esize(d.dtype);
   const size_t blk_elems = (size_t)d.b * d.H * d.dh;
-  const int chunk = std::min(std::min(kMaxSlots, kPrefillSlotChunk), (int)d.n_seq);
+  const int chunk = prefill_slots(&d);
   for (int i0 = 0; i0 < n_seq; i0 += chunk) {
     const int n = std::min(chunk, n_seq - i0);
     ReaderArgs a;

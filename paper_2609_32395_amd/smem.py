@@ -61,6 +61,11 @@ class RowsLayer(ctypes.Structure):
                 ("null_row", ctypes.c_void_p)]
 
 
+class ModelDesc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("E", "D", "d", "H", "dh", "b", "vocab", "n_pos", "n_seq", "max_blocks",
+                                               "n_pages", "max_tokens")]
+
+
 class RopeDesc(ctypes.Structure):
     _fields_ = [("dh", ctypes.c_int32), ("n_phases", ctypes.c_int32), ("max_offset", ctypes.c_int32),
                 ("reserved", ctypes.c_int32), ("base", ctypes.c_double)]
@@ -95,6 +100,14 @@ SIGNATURES = {
     "smem_rows_put_block": (_I, [_P, _I, _I, _P, _P]),
     "smem_rows_export": (_I, [_P, _I, _IP, _IP, _P, _P]),
     "smem_reader_decode_rows": (_I, [_P, ctypes.POINTER(RowsLayer), _I, _IP, _IP, _IP, _P, _P, _P, _P, _P, _P, _P]),
+    "smem_model_n_weights": (_I, [ctypes.POINTER(ModelDesc)]),
+    "smem_model_bytes": (ctypes.c_size_t, [ctypes.POINTER(ModelDesc)]),
+    "smem_model_create": (_I, [ctypes.POINTER(ModelDesc), ctypes.POINTER(_P), _P, ctypes.c_size_t, _P,
+                               ctypes.POINTER(_P)]),
+    "smem_model_destroy": (_I, [_P]),
+    "smem_model_encode": (_I, [_P, _I, _I, _IP, _P, _P]),
+    "smem_model_read": (_I, [_P, _I, _I, _IP, _P, _P, _P]),
+    "smem_model_delete_block": (_I, [_P, _I, _I, _P]),
     "smem_store_stats": (_I, [_P, _IP, _IP]),
     "smem_status_string": (ctypes.c_char_p, [_I]),
     "smem_last_error": (ctypes.c_char_p, []),
@@ -286,6 +299,118 @@ def smem_reader_decode_rows(st: RowStore, w_k, w_v, seq_ids, query_block, pos, q
     _check(lib().smem_reader_decode_rows(st.handle, ctypes.byref(layer), n, _i32(seq_ids), _i32(query_block), pa,
                                          *args, _stream(stream)))
     return out
+
+
+MODEL_ENC = ["ln1_g", "ln1_b", "w_qkv", "w_o", "ln2_g", "ln2_b", "w_ff1", "w_ff2"]
+MODEL_DEC = ["ln1_g", "ln1_b", "w_qkv", "w_o", "ln2_g", "ln2_b", "w_q", "w_k", "w_v", "w_oc", "ln3_g", "ln3_b",
+             "w_ff1", "w_ff2"]
+
+
+def model_weight_names(E, D):
+    """Weight names in the order smem_model_create takes them."""
+    names = ["tok_emb", "pos_emb"]
+    for l in range(E):
+        names += [f"enc{l}.{n}" for n in MODEL_ENC]
+    names += ["mem_ln_g", "mem_ln_b", "null_row"]
+    for l in range(D):
+        names += [f"dec{l}.{n}" for n in MODEL_DEC]
+    return names + ["fin_g", "fin_b", "w_head"]
+
+
+def model_weight_shapes(E, D, d, vocab, n_pos):
+    """(name, shape) of every weight in smem_model_create's order; linear maps
+    are [out, in], the feed-forward hidden width is 4d."""
+    f = 4 * d
+    enc = {"ln1_g": (d,), "ln1_b": (d,), "w_qkv": (3 * d, d), "w_o": (d, d), "ln2_g": (d,), "ln2_b": (d,),
+           "w_ff1": (f, d), "w_ff2": (d, f)}
+    dec = dict(enc, w_q=(d, d), w_k=(d, d), w_v=(d, d), w_oc=(d, d), ln3_g=(d,), ln3_b=(d,))
+    shape = {"tok_emb": (vocab, d), "pos_emb": (max(n_pos, 1), d), "mem_ln_g": (d,), "mem_ln_b": (d,),
+             "null_row": (d,), "fin_g": (d,), "fin_b": (d,), "w_head": (vocab, d)}
+    out = []
+    for nm in model_weight_names(E, D):
+        if nm.startswith("enc"):
+            out.append((nm, enc[nm.split(".", 1)[1]]))
+        elif nm.startswith("dec"):
+            out.append((nm, dec[nm.split(".", 1)[1]]))
+        else:
+            out.append((nm, shape[nm]))
+    return out
+
+
+class Model:
+    """The whole model over caller-owned bf16 weights (a dict name -> device
+    tensor, names as model_weight_names; pos_emb may be absent when n_pos is
+    0).  The pool (the reader layers' stores and the workspace) is allocated
+    here with torch."""
+
+    def __init__(self, weights, E, D, d, H, b, vocab, n_pos, n_seq, max_blocks, n_pages, max_tokens=4096,
+                 device="cuda", stream=None):
+        self.E, self.D, self.d, self.H, self.b, self.vocab = E, D, d, H, b, vocab
+        self.dh = d // H
+        self.desc = ModelDesc(E, D, d, H, d // H, b, vocab, n_pos, n_seq, max_blocks, n_pages, max_tokens)
+        L = lib()
+        n = L.smem_model_n_weights(ctypes.byref(self.desc))
+        if n == 0:
+            raise SmemError(SMEM_EINVAL, "invalid model descriptor")
+        names = model_weight_names(E, D)
+        assert len(names) == n
+        self.weights = weights        # kept alive
+        ptrs = (ctypes.c_void_p * n)()
+        for i, nm in enumerate(names):
+            t = weights.get(nm)
+            if t is None:
+                if nm == "pos_emb" and n_pos == 0:
+                    continue
+                raise KeyError(nm)
+            if t.dtype != torch.bfloat16 or not t.is_contiguous() or t.device.type != "cuda":
+                raise ValueError(f"{nm} must be a contiguous bf16 device tensor")
+            ptrs[i] = t.data_ptr()
+        nbytes = L.smem_model_bytes(ctypes.byref(self.desc))
+        self.pool = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        handle = ctypes.c_void_p()
+        _check(L.smem_model_create(ctypes.byref(self.desc), ptrs, ctypes.c_void_p(self.pool.data_ptr()), nbytes,
+                                   _stream(stream), ctypes.byref(handle)))
+        self.handle = handle
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().smem_model_destroy(self.handle)
+            self.handle = None
+        self.pool = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _tokens(tokens, n_blocks, b):
+    if tokens.dtype != torch.int32 or tokens.device.type != "cuda" or not tokens.is_contiguous():
+        raise ValueError("tokens must be a contiguous int32 device tensor")
+    if tokens.numel() != n_blocks * b:
+        raise ValueError(f"tokens has {tokens.numel()} ids, expected {n_blocks * b}")
+    return ctypes.c_void_p(tokens.data_ptr())
+
+
+def smem_model_encode(m: Model, seq: int, block_idx, tokens, stream=None):
+    n = len(block_idx)
+    _check(lib().smem_model_encode(m.handle, int(seq), n, _i32(block_idx), _tokens(tokens, n, m.b), _stream(stream)))
+
+
+def smem_model_read(m: Model, seq: int, query_block, tokens, logits=None, stream=None):
+    """Logits [n*b, vocab] fp32 of the query blocks."""
+    n = len(query_block)
+    if logits is None:
+        logits = torch.empty((n * m.b, m.vocab), dtype=torch.float32, device=tokens.device)
+    lp = _dev(logits, (n * m.b, m.vocab), torch.float32, "logits")
+    _check(lib().smem_model_read(m.handle, int(seq), n, _i32(query_block), _tokens(tokens, n, m.b), lp,
+                                 _stream(stream)))
+    return logits
+
+
+def smem_model_delete_block(m: Model, seq: int, block_idx: int, stream=None):
+    _check(lib().smem_model_delete_block(m.handle, int(seq), int(block_idx), _stream(stream)))
 
 
 class Rope:

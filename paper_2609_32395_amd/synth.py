@@ -166,3 +166,25 @@ def memory_block_device(w: Workload, seed: int, seq: int, block: int, version: i
     x = torch.randn((2,) + w.row_shape, generator=g, device=device, dtype=torch.float32) * w.scale
     x = x.to(torch.bfloat16 if w.dtype == "bf16" else torch.float32)
     return x[0], x[1]
+
+
+ROLE_WEIGHT = 11
+
+
+def model_weights(shapes, seed: int) -> dict:
+    """Random model weights, bf16-representable float32, one array per
+    (name, shape): LayerNorm scales 1 + 0.1 N, shifts 0.1 N, embedding and
+    null rows N(0, 1), linear maps [out, in] N(0, 1) / sqrt(in).  Each array
+    is drawn from its own key (seed, weight role, index in the list)."""
+    W = {}
+    for i, (name, shape) in enumerate(shapes):
+        g = rng(seed, ROLE_WEIGHT, i)
+        x = g.standard_normal(size=shape, dtype=np.float32)
+        if name.endswith("_g"):
+            x = 1.0 + 0.1 * x
+        elif name.endswith("_b"):
+            x = 0.1 * x
+        elif len(shape) == 2 and not name.endswith("_emb"):
+            x = x * np.float32(1.0 / np.sqrt(shape[1]))
+        W[name] = bf16_round(x)
+    return W

@@ -148,3 +148,26 @@ def test_rope_bytes_and_invalid_descriptors():
     out = ctypes.c_void_p()
     assert L.smem_rope_create(ctypes.byref(d), None, 1 << 20, None, ctypes.byref(out)) == smem.SMEM_EINVAL
     assert not out.value
+
+
+def test_model_descriptor_and_weight_list():
+    """Host-side model checks: weight count, pool size, descriptor limits,
+    and the binding's weight list against the oracle's (the C ABI order)."""
+    from oracle import smem_model as MO
+    L = smem.lib()
+    E, D, d, H, b, vocab, n_pos = 3, 7, 768, 24, 64, 50257, 1024
+    desc = smem.ModelDesc(E, D, d, H, d // H, b, vocab, n_pos, 1, 128, 128, 4096)
+    assert L.smem_model_n_weights(ctypes.byref(desc)) == len(smem.model_weight_names(E, D)) == 2 + 8 * E + 3 + 14 * D + 3
+    assert smem.model_weight_shapes(E, D, d, vocab, n_pos) == MO.weight_shapes(E, D, d, vocab, n_pos)
+    sd = smem.StoreDesc(1, 128, 128, b, H, d // H, smem.BF16)
+    store = (L.smem_store_bytes(ctypes.byref(sd)) + 255) // 256 * 256
+    ws = 6 * 4096 * d * 2 + 4096 * 4 * d * 2 + (D * 2 * d * 2 + 255) // 256 * 256
+    assert L.smem_model_bytes(ctypes.byref(desc)) == D * store + ws
+    for field, bad in (("b", 16), ("dh", 48), ("d", 700), ("n_pos", 100), ("max_tokens", 100),
+                       ("max_tokens", 129 * 64), ("D", 0), ("vocab", 0)):
+        bd = smem.ModelDesc.from_buffer_copy(desc)
+        setattr(bd, field, bad)
+        assert L.smem_model_n_weights(ctypes.byref(bd)) == 0, field
+        assert L.smem_model_bytes(ctypes.byref(bd)) == 0, field
+    out = ctypes.c_void_p()
+    assert L.smem_model_create(ctypes.byref(desc), None, None, 0, None, ctypes.byref(out)) == smem.SMEM_EINVAL

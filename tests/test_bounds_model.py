@@ -103,13 +103,15 @@ def test_mfma_indexing(dh):
 
 
 def test_prefill_workspace_fits_slot_chunk():
-    # prefill launches at most min(16, n_seq) slots of b query rows each
-    for n_seq, b, H, dh in itertools.product((1, 8, 16, 64), (16, 64), (1, 16), (32, 128)):
+    # prefill launches at most min(16, n_seq * max_blocks) slots of b query
+    # rows each (one sequence may fill several slots); decode at most
+    # min(128, n_seq) slots of one row (a sequence appears once)
+    for n_seq, mb, b, H, dh in itertools.product((1, 8, 16, 64), (1, 3, 40), (16, 64), (1, 16), (32, 128)):
         dec_rows = n_seq * H
-        pre_rows = min(n_seq, 16) * b * H
+        slots = min(n_seq * mb, 16)
+        pre_rows = slots * b * H
         ws = max(dec_rows, pre_rows) * SPLIT_STRIDE * (dh + 4)
-        chunk = min(16, n_seq)
-        assert (chunk * b * H) * SPLIT_STRIDE * (dh + 4) <= ws
+        assert (slots * b * H) * SPLIT_STRIDE * (dh + 4) <= ws
         assert (min(128, n_seq) * 1 * H) * SPLIT_STRIDE * (dh + 4) <= ws
 
 
@@ -196,3 +198,61 @@ def test_rows_reader_indexing(b, D):
             assert sp <= per_seq
     # k_merge_rows keeps split weights in a 64-entry array
     assert 32 <= 64
+
+
+def _linear_ranges(M, N, K, ldx, ldy, n2, ns, split):
+    """Largest element index each k_linear access touches, from the kernel's
+    own index arithmetic (64 x 64 tile, waves 2 x 2, lanes 16 x 4)."""
+    hi = {"x": -1, "w": -1, "w2": -1, "y": -1}
+    for bx, by in itertools.product(range(-(-N // 64)), range(-(-M // 64))):
+        for wave, lane in itertools.product(range(4), (0, 15, 16, 47, 48, 63)):
+            wm, wn, kofs = wave & 1, wave >> 1, (lane >> 4) * 8
+            for i in range(2):
+                r = by * 64 + wm * 32 + i * 16 + (lane & 15)
+                rr = r if r < M else 0
+                hi["x"] = max(hi["x"], rr * ldx + kofs + (K - 32) + 7)
+            for j in range(2):
+                n = bx * 64 + wn * 32 + j * 16 + (lane & 15)
+                nn = n if n < N else 0
+                key, row = ("w", nn) if nn < n2 else ("w2", nn - n2)
+                hi[key] = max(hi[key], row * K + kofs + (K - 32) + 7)
+                for i, ii in itertools.product(range(2), range(4)):
+                    m = by * 64 + wm * 32 + i * 16 + 4 * (lane >> 4) + ii
+                    if m < M and n < N:
+                        if split:
+                            g, c = divmod(n, ns)
+                            assert g < 3 and c < ns
+                            hi["y"] = max(hi["y"], m * ns + c)
+                        else:
+                            hi["y"] = max(hi["y"], m * ldy + n)
+    return hi
+
+
+@pytest.mark.parametrize("d,vocab,rows", [(128, 256, 448), (768, 1000, 130), (2048, 77, 64)])
+def test_model_kernel_indexing(d, vocab, rows):
+    """Every k_linear call the model makes stays inside its operands (x
+    [rows, K] in a [max_tokens, ldx] buffer, W [N or n2, K] and [N - n2, K],
+    y [rows, ldy]); LayerNorm and embedding lanes stay inside a d-wide row."""
+    calls = [  # M, N, K, ldx, ldy, n2, ns, split, rows of W (first, second)
+        (rows, 3 * d, d, d, d, 3 * d, d, True, 3 * d, 0),        # qkv, split into q, k, v
+        (rows, d, d, d, d, d, 0, False, d, 0),                   # attention out (+ residual)
+        (rows, 4 * d, d, d, 4 * d, 4 * d, 0, False, 4 * d, 0),   # ffn up
+        (rows, d, 4 * d, 4 * d, d, d, 0, False, d, 0),           # ffn down (+ residual)
+        (rows, 2 * d, d, d, d, d, d, True, d, d),                # memory K | V maps
+        (1, 2 * d, d, d, 2 * d, d, 0, False, d, d),              # null row through K | V
+        (rows, vocab, d, d, vocab, vocab, 0, False, vocab, 0),   # output head (fp32)
+    ]
+    for M, N, K, ldx, ldy, n2, ns, split, wrows, w2rows in calls:
+        assert K % 32 == 0 and K <= ldx
+        hi = _linear_ranges(M, N, K, ldx, ldy, n2, ns, split)
+        assert hi["x"] < M * ldx
+        assert hi["w"] < wrows * K
+        assert hi["w2"] < max(w2rows, 0) * K or hi["w2"] == -1
+        assert hi["y"] < (M * ns if split else M * ldy)
+    # LayerNorm / embedding: lane chunks c = i*512 + 8*lane (i < 4) guarded by c < d, 8 values each
+    assert d % 8 == 0 and d <= 2048
+    for i, lane in itertools.product(range(4), range(64)):
+        c = i * 512 + lane * 8
+        if c < d:
+            assert c + 7 < d
+    assert 3 * 512 + 63 * 8 + 8 >= 2048         # the four chunks cover d = 2048

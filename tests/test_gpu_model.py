@@ -1,0 +1,111 @@
+"""GPU parity of the whole model at random weights (Section 2, "Model";
+Appendix A) through the C ABI, against the fp64 model oracle.
+
+* logits of a served block against the oracle (bf16 weights and activations,
+  fp32 accumulation; tolerance below);
+* block-skip serving equals the cold full pass on the served block, bitwise
+  (Section 3.1: the reader state of a block depends only on its tokens and
+  the cached memory; every kernel here is row- and batch-invariant);
+* deleting a block equals never encoding it, bitwise (Theorem 1);
+* error codes of the store operations.
+
+Tolerance.  Every activation is rounded to bf16 (unit roundoff u = 2^-9)
+once per producing step: about 6 roundings per layer on the residual path
+(embedding, attention inputs and outputs, LayerNorm outputs, feed-forward
+hidden), 20 for this 3-layer model.  Independent roundings add as a random
+walk, so the logits' relative RMS error is about sqrt(20) u ~ 0.009, and the
+largest of 16k logits lies within ~4.5 RMS: max |y - y_ref| / rms(y_ref)
+<= 5e-2.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import smem_model as MO
+from paper_2609_32395_amd import smem, synth
+from tests.gpu_util import host, require_gpu, say
+
+pytestmark = pytest.mark.gpu
+
+TOL = 5e-2
+SHAPE = dict(E=1, D=2, d=128, H=4, b=64, vocab=256, n_pos=256)
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+    yield
+    torch.cuda.synchronize()
+
+
+def build(seed=5, n_pages=16, max_blocks=12, max_tokens=256, **over):
+    s = dict(SHAPE, **over)
+    W = synth.model_weights(smem.model_weight_shapes(s["E"], s["D"], s["d"], s["vocab"], s["n_pos"]), seed)
+    dW = {k: torch.from_numpy(v).to("cuda").to(torch.bfloat16).contiguous() for k, v in W.items()}
+    m = smem.Model(dW, s["E"], s["D"], s["d"], s["H"], s["b"], s["vocab"], s["n_pos"], 1, max_blocks, n_pages,
+                   max_tokens)
+    ref = MO.Model(W, s["E"], s["D"], s["d"], s["H"], s["b"], s["vocab"], s["n_pos"], 1, max_blocks)
+    return m, ref, dW
+
+
+def tok(x):
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.int32).reshape(-1)).to("cuda")
+
+
+def test_served_block_matches_oracle():
+    say("model: served block vs oracle")
+    m, ref, _ = build()
+    g = np.random.default_rng(11)
+    B = 7                                    # 6 cached blocks, two launches of 4 + 2; block 6 is past the position table
+    tokens = g.integers(0, SHAPE["vocab"], size=(B, SHAPE["b"]))
+    smem.smem_model_encode(m, 0, list(range(B - 1)), tok(tokens[:B - 1]))
+    logits = smem.smem_model_read(m, 0, [B - 1], tok(tokens[B - 1:]))
+    ref.encode(0, tokens[:B - 1], list(range(B - 1)))
+    expect = ref.read(0, tokens[B - 1:], [B - 1])[0]
+    y = host(logits)
+    err = float(np.max(np.abs(y - expect)) / np.sqrt(np.mean(expect ** 2)))
+    say("model rel err", err, "argmax agreement", float(np.mean(y.argmax(-1) == expect.argmax(-1))))
+    assert np.all(np.isfinite(y))
+    assert err <= TOL, err
+
+
+def test_block_skip_equals_cold_pass_bitwise():
+    say("model: block-skip vs cold pass")
+    g = np.random.default_rng(12)
+    B = 6
+    tokens = g.integers(0, SHAPE["vocab"], size=(B, SHAPE["b"]))
+    cached, _, dW = build()
+    smem.smem_model_encode(cached, 0, list(range(B - 1)), tok(tokens[:B - 1]))
+    skip = smem.smem_model_read(cached, 0, [B - 1], tok(tokens[B - 1:]))
+    cold, _, _ = build()
+    smem.smem_model_encode(cold, 0, list(range(B)), tok(tokens))
+    full = smem.smem_model_read(cold, 0, list(range(B)), tok(tokens))
+    assert torch.equal(skip, full[(B - 1) * SHAPE["b"]:])
+
+
+def test_delete_equals_never_encoded_bitwise_and_errors():
+    say("model: delete vs never encoded")
+    g = np.random.default_rng(13)
+    B = 6
+    tokens = g.integers(0, SHAPE["vocab"], size=(B, SHAPE["b"]))
+    a, _, _ = build()
+    smem.smem_model_encode(a, 0, list(range(B - 1)), tok(tokens[:B - 1]))
+    smem.smem_model_delete_block(a, 0, 2)
+    c, _, _ = build()
+    keep = [0, 1, 3, 4]
+    smem.smem_model_encode(c, 0, keep, tok(tokens[keep]))
+    la = smem.smem_model_read(a, 0, [B - 1], tok(tokens[B - 1:]))
+    lc = smem.smem_model_read(c, 0, [B - 1], tok(tokens[B - 1:]))
+    assert torch.equal(la, lc)
+    with pytest.raises(smem.SmemError) as e:
+        smem.smem_model_encode(a, 0, [1], tok(tokens[1:2]))
+    assert e.value.code == smem.SMEM_EEXIST
+    with pytest.raises(smem.SmemError) as e:
+        smem.smem_model_delete_block(a, 0, 2)
+    assert e.value.code == smem.SMEM_ENOENT
+    # re-encoding the deleted block restores the full read exactly
+    smem.smem_model_encode(a, 0, [2], tok(tokens[2:3]))
+    full, _, _ = build()
+    smem.smem_model_encode(full, 0, list(range(B - 1)), tok(tokens[:B - 1]))
+    assert torch.equal(smem.smem_model_read(a, 0, [B - 1], tok(tokens[B - 1:])),
+                       smem.smem_model_read(full, 0, [B - 1], tok(tokens[B - 1:])))
