@@ -26,7 +26,11 @@ Secondary workloads, timed in the same run and reported under "secondary":
     headline decode and on the 1.5B serve, beside the base reads;
   * 1.5B-shaped stress: 16 sequences x 4096 blocks (262144 rows each, a
     32 GiB store): batch-16 decode over all rows, and single-block delete /
-    re-insert latency.
+    re-insert latency;
+  * the whole model at random weights, 160M / 410M / 1.5B scales (d 768 /
+    1024 / 2048, E:D 3:7 / 4:15 / 4:15, heads of 32, GPT-2 vocabulary, 1024
+    learned positions): block-skip serving of a fully cached context against
+    the cold prefill, batch 1, contexts 1k / 2k / 4k / 8k.
 
 Timing uses HIP events on the stream the kernels are launched on (torch's
 current stream, handed to the library).  The 160M encoder and prefill calls
@@ -444,6 +448,67 @@ def stress_workload(args, torch, smem, synth):
                 delete_us_median=float(np.median(d_t)) * 1e3, reinsert_us_median=float(np.median(p_t)) * 1e3)
 
 
+def model_workload(args, torch, smem, synth):
+    """Whole model at random weights (Appendix A scales): block-skip serving
+    of a fully cached context (the reader on the final block alone) against
+    the model's own cold prefill (encoder over every block, reader over every
+    block, final-block logits), batch 1, contexts 1k-8k."""
+    stream = torch.cuda.current_stream()
+    lengths = [int(x) for x in args.model_lengths.split(",")]
+    scales = [sc for sc in synth.MODEL_SCALES if sc[0] in args.model_scales.split(",")]
+    out = {}
+    for name, d, E, D in scales:
+        H, b, vocab, T = d // 32, 64, synth.MODEL_VOCAB, synth.MODEL_T
+        nb_max = max(lengths) // b
+        W = synth.model_weights_device(smem.model_weight_shapes(E, D, d, vocab, T), args.seed)
+        m = smem.Model(W, E, D, d, H, b, vocab, T, 1, nb_max, nb_max, max_tokens=min(nb_max, 128) * b)
+        cells = {}
+        for n in lengths:
+            J = n // b
+            tokens = torch.from_numpy(synth.model_tokens(args.seed, name, n)).to("cuda")
+            last = tokens[(J - 1) * b:].contiguous()
+            cold_t = []
+            for rep in range(args.model_reps + 1):
+                for j in range(J if rep else 0):
+                    smem.smem_model_delete_block(m, 0, j)
+                torch.cuda.synchronize()
+                t0 = torch.cuda.Event(enable_timing=True)
+                t1 = torch.cuda.Event(enable_timing=True)
+                t0.record(stream)
+                cold = smem.smem_model_prefill(m, 0, 0, J, tokens)
+                t1.record(stream)
+                t1.synchronize()
+                if rep:                                   # rep 0 warms the path
+                    cold_t.append(t0.elapsed_time(t1))
+            skip_t = []
+            for rep in range(args.model_reps + 2):
+                torch.cuda.synchronize()
+                t0 = torch.cuda.Event(enable_timing=True)
+                t1 = torch.cuda.Event(enable_timing=True)
+                t0.record(stream)
+                skip = smem.smem_model_read(m, 0, [J - 1], last)
+                t1.record(stream)
+                t1.synchronize()
+                if rep >= 2:
+                    skip_t.append(t0.elapsed_time(t1))
+            same = bool(torch.equal(skip, cold))
+            graph_ms = _graph_time(lambda t: smem.smem_model_read(m, 0, [J - 1], last, logits=skip), 4, stream) * 1e3
+            for j in range(J):
+                smem.smem_model_delete_block(m, 0, j)
+            print(f"[bench] model {name} n={n}: cold {np.median(cold_t):.3f} ms, block-skip "
+                  f"{np.median(skip_t):.3f} ms (graph {graph_ms:.3f} ms)", file=sys.stderr, flush=True)
+            cells[str(n)] = dict(cold_prefill_ms=round(float(np.median(cold_t)), 3),
+                                 block_skip_ms=round(float(np.median(skip_t)), 3),
+                                 block_skip_graph_ms=round(graph_ms, 3),
+                                 ttft_reduction=round(1.0 - float(np.median(skip_t)) / float(np.median(cold_t)), 4),
+                                 skip_equals_cold_bitwise=same)
+        m.close()
+        del W
+        torch.cuda.empty_cache()
+        out[name] = dict(d=d, E=E, D=D, H=H, cells=cells)
+    return out
+
+
 def cpu_baseline(dec, budget_s, seed):
     """The fp64 oracle on a bounded sample of the headline decode workload.
 
@@ -488,9 +553,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-secondary", action="store_true")
-    ap.add_argument("--workloads", default="encode,serve,stream,rows,stress,rope",
+    ap.add_argument("--workloads", default="encode,serve,stream,rows,stress,rope,model",
                     help="secondary workloads to run (comma list of encode, serve, stream, rows, stress, rope: "
-                         "the rotary composite timed beside the headline decode and the serve)")
+                         "the rotary composite timed beside the headline decode and the serve; model: the whole "
+                         "model's block-skip serve against its cold prefill)")
+    ap.add_argument("--model-scales", default="160M,410M,1.5B")
+    ap.add_argument("--model-lengths", default="1024,2048,4096,8192")
+    ap.add_argument("--model-reps", type=int, default=3)
     ap.add_argument("--no-headline", action="store_true",
                     help="profiling runs only: skip the decode headline (value is then null)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -531,6 +600,8 @@ def main():
             secondary["rope_decode_410M"] = dec["rope"]
         if "stress" in wl:
             secondary["stress_1p5B"] = stress_workload(args, torch, smem, synth)
+        if "model" in wl:
+            secondary["model_block_skip"] = model_workload(args, torch, smem, synth)
     cpu = None
     if dec is None:
         print(json.dumps({"metric": "profiling run (no headline)", "value": None, "secondary": secondary}))

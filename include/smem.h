@@ -385,6 +385,16 @@ smem_status smem_model_encode(smem_model* m, int32_t seq, int32_t n_blocks, cons
 smem_status smem_model_read(smem_model* m, int32_t seq, int32_t n_blocks, const int32_t* query_block,
                             const int32_t* tokens, float* logits, hipStream_t s);
 
+/* Prefill of blocks first_block .. first_block + n_blocks - 1 of sequence
+ * seq (tokens: device int32 [n_blocks*b]): encode and insert them into every
+ * reader layer, then run the reader on each of them; logits (device fp32
+ * [b, vocab]) of the final block only.  first_block = 0 is the cold prefill
+ * of a context; first_block > 0 with blocks 0 .. first_block - 1 cached is
+ * partial reuse: the reader runs from the first uncached block (Section 3.1).
+ * The blocks must be absent (SMEM_EEXIST otherwise; nothing is changed). */
+smem_status smem_model_prefill(smem_model* m, int32_t seq, int32_t first_block, int32_t n_blocks,
+                               const int32_t* tokens, float* logits, hipStream_t s);
+
 /* Exact deletion of block block_idx of sequence seq from every reader layer
  * (Theorem 1).  SMEM_ENOENT if absent. */
 smem_status smem_model_delete_block(smem_model* m, int32_t seq, int32_t block_idx, hipStream_t s);

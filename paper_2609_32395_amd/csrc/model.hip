@@ -353,6 +353,38 @@ smem_status self_attn(smem_model* m, int rows, int nb, const uint16_t* g, const 
   return SMEM_OK;
 }
 
+// Reader stack over one chunk of nb query blocks (rows = nb*b <= max_tokens).
+// With logits, the final LayerNorm and the head run on chunk rows [h0, rows)
+// and logits row 0 is chunk row h0; without, they are skipped.
+smem_status read_chunk(smem_model* m, int seq, int nb, const int32_t* qblk, const int32_t* tokens, float* logits,
+                       int h0, hipStream_t s) {
+  const auto& d = m->d;
+  Wts w{m};
+  const int rows = nb * d.b, D = d.d;
+  MSTATUS(embed(m, nb, qblk, tokens, s));
+  std::vector<int32_t> seqs(nb, seq);
+  for (int l = 0; l < d.D; ++l) {
+    MSTATUS(self_attn(m, rows, nb, w.dec(l, R_LN1G), w.dec(l, R_LN1B), w.dec(l, R_QKV), w.dec(l, R_O),
+                      SMEM_MASK_CAUSAL, s));
+    // cross-attention into the memory of strictly earlier blocks, with the null row
+    MCHECK(lnorm(m->x, w.dec(l, R_LN2G), w.dec(l, R_LN2B), m->h, rows, D, s), "layernorm");
+    MCHECK(linear<kLinStore>(lin(m->h, D, w.dec(l, R_Q), rows, D, D, m->q, D), s), "cross-attention query");
+    MSTATUS(smem_reader_prefill_block(m->stores[l], nb, seqs.data(), qblk, m->q, nullptr, nullptr,
+                                      m->null_kv + (size_t)l * 2 * D, m->o, s));
+    LinArgs o = lin(m->o, D, w.dec(l, R_OC), rows, D, D, m->x, D);
+    o.res = m->x;
+    MCHECK(linear<kLinResid>(o, s), "cross-attention out");
+    MSTATUS(ffn(m, rows, w.dec(l, R_LN3G), w.dec(l, R_LN3B), w.dec(l, R_FF1), w.dec(l, R_FF2), s));
+  }
+  if (!logits) return SMEM_OK;
+  const int hr = rows - h0;
+  MCHECK(lnorm(m->x + (size_t)h0 * D, w.fin_g(), w.fin_b(), m->h + (size_t)h0 * D, hr, D, s), "final layernorm");
+  LinArgs hd = lin(m->h + (size_t)h0 * D, D, w.head(), hr, d.vocab, D, nullptr, d.vocab);
+  hd.yf = logits;
+  MCHECK(linear<kLinF32>(hd, s), "output head");
+  return SMEM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -482,29 +514,32 @@ smem_status smem_model_read(smem_model* m, int32_t seq, int32_t n_blocks, const 
   if (seq < 0 || seq >= d.n_seq) return mfail(SMEM_EINVAL, "seq out of range");
   for (int i = 0; i < n_blocks; ++i)
     if (query_block[i] < 0 || query_block[i] > d.max_blocks) return mfail(SMEM_EINVAL, "query block out of range");
-  Wts w{m};
-  const int cb = d.max_tokens / d.b, D = d.d;
+  const int cb = d.max_tokens / d.b;
   for (int i0 = 0; i0 < n_blocks; i0 += cb) {
-    const int nb = std::min(cb, n_blocks - i0), rows = nb * d.b;
-    MSTATUS(embed(m, nb, query_block + i0, tokens + (size_t)i0 * d.b, s));
-    std::vector<int32_t> seqs(nb, seq);
-    for (int l = 0; l < d.D; ++l) {
-      MSTATUS(self_attn(m, rows, nb, w.dec(l, R_LN1G), w.dec(l, R_LN1B), w.dec(l, R_QKV), w.dec(l, R_O),
-                        SMEM_MASK_CAUSAL, s));
-      // cross-attention into the memory of strictly earlier blocks, with the null row
-      MCHECK(lnorm(m->x, w.dec(l, R_LN2G), w.dec(l, R_LN2B), m->h, rows, D, s), "layernorm");
-      MCHECK(linear<kLinStore>(lin(m->h, D, w.dec(l, R_Q), rows, D, D, m->q, D), s), "cross-attention query");
-      MSTATUS(smem_reader_prefill_block(m->stores[l], nb, seqs.data(), query_block + i0, m->q, nullptr, nullptr,
-                                        m->null_kv + (size_t)l * 2 * D, m->o, s));
-      LinArgs o = lin(m->o, D, w.dec(l, R_OC), rows, D, D, m->x, D);
-      o.res = m->x;
-      MCHECK(linear<kLinResid>(o, s), "cross-attention out");
-      MSTATUS(ffn(m, rows, w.dec(l, R_LN3G), w.dec(l, R_LN3B), w.dec(l, R_FF1), w.dec(l, R_FF2), s));
-    }
-    MCHECK(lnorm(m->x, w.fin_g(), w.fin_b(), m->h, rows, D, s), "final layernorm");
-    LinArgs hd = lin(m->h, D, w.head(), rows, d.vocab, D, nullptr, d.vocab);
-    hd.yf = logits + (size_t)i0 * d.b * d.vocab;
-    MCHECK(linear<kLinF32>(hd, s), "output head");
+    const int nb = std::min(cb, n_blocks - i0);
+    MSTATUS(read_chunk(m, seq, nb, query_block + i0, tokens + (size_t)i0 * d.b, logits + (size_t)i0 * d.b * d.vocab,
+                       0, s));
+  }
+  return SMEM_OK;
+}
+
+smem_status smem_model_prefill(smem_model* m, int32_t seq, int32_t first_block, int32_t n_blocks,
+                               const int32_t* tokens, float* logits, hipStream_t s) {
+  if (!m) return mfail(SMEM_EINVAL, "model is NULL");
+  const auto& d = m->d;
+  if (n_blocks < 1) return mfail(SMEM_EINVAL, "n_blocks < 1");
+  if (!tokens || !logits) return mfail(SMEM_EINVAL, "tokens and logits are required");
+  if (first_block < 0 || (int64_t)first_block + n_blocks > d.max_blocks)
+    return mfail(SMEM_EINVAL, "blocks first_block .. first_block + n_blocks - 1 out of range");
+  std::vector<int32_t> blocks(n_blocks);
+  for (int i = 0; i < n_blocks; ++i) blocks[i] = first_block + i;
+  MSTATUS(smem_model_encode(m, seq, n_blocks, blocks.data(), tokens, s));
+  const int cb = d.max_tokens / d.b;
+  for (int i0 = 0; i0 < n_blocks; i0 += cb) {
+    const int nb = std::min(cb, n_blocks - i0);
+    const bool last = i0 + nb == n_blocks;
+    MSTATUS(read_chunk(m, seq, nb, blocks.data() + i0, tokens + (size_t)i0 * d.b, last ? logits : nullptr,
+                       (nb - 1) * d.b, s));
   }
   return SMEM_OK;
 }

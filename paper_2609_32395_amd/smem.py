@@ -107,6 +107,7 @@ SIGNATURES = {
     "smem_model_destroy": (_I, [_P]),
     "smem_model_encode": (_I, [_P, _I, _I, _IP, _P, _P]),
     "smem_model_read": (_I, [_P, _I, _I, _IP, _P, _P, _P]),
+    "smem_model_prefill": (_I, [_P, _I, _I, _I, _P, _P, _P]),
     "smem_model_delete_block": (_I, [_P, _I, _I, _P]),
     "smem_store_stats": (_I, [_P, _IP, _IP]),
     "smem_status_string": (ctypes.c_char_p, [_I]),
@@ -406,6 +407,16 @@ def smem_model_read(m: Model, seq: int, query_block, tokens, logits=None, stream
     lp = _dev(logits, (n * m.b, m.vocab), torch.float32, "logits")
     _check(lib().smem_model_read(m.handle, int(seq), n, _i32(query_block), _tokens(tokens, n, m.b), lp,
                                  _stream(stream)))
+    return logits
+
+
+def smem_model_prefill(m: Model, seq: int, first_block: int, n_blocks: int, tokens, logits=None, stream=None):
+    """Encode and read blocks first_block .. first_block + n_blocks - 1; logits [b, vocab] of the last."""
+    if logits is None:
+        logits = torch.empty((m.b, m.vocab), dtype=torch.float32, device=tokens.device)
+    lp = _dev(logits, (m.b, m.vocab), torch.float32, "logits")
+    _check(lib().smem_model_prefill(m.handle, int(seq), int(first_block), int(n_blocks), _tokens(tokens, n_blocks, m.b),
+                                    lp, _stream(stream)))
     return logits
 
 

@@ -188,3 +188,37 @@ def model_weights(shapes, seed: int) -> dict:
             x = x * np.float32(1.0 / np.sqrt(shape[1]))
         W[name] = bf16_round(x)
     return W
+
+
+def model_weights_device(shapes, seed: int, device="cuda") -> dict:
+    """The distribution of model_weights, drawn on the device by torch's
+    seeded generator (one generator seed per weight) as bf16 tensors: for
+    models too large to draw on the host."""
+    import torch
+    W = {}
+    g = torch.Generator(device=device)
+    for i, (name, shape) in enumerate(shapes):
+        g.manual_seed(block_seed(seed, ROLE_WEIGHT, i))
+        x = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+        if name.endswith("_g"):
+            x = 1.0 + 0.1 * x
+        elif name.endswith("_b"):
+            x = 0.1 * x
+        elif len(shape) == 2 and not name.endswith("_emb"):
+            x = x * (1.0 / float(np.sqrt(shape[1])))
+        W[name] = x.to(torch.bfloat16).contiguous()
+        del x
+    return W
+
+
+# Model scales of Appendix A: (name, d, E, D); heads of width 32, the GPT-2
+# vocabulary, T = 1024 learned positions, b = 64.
+MODEL_SCALES = [("160M", 768, 3, 7), ("410M", 1024, 4, 15), ("1.5B", 2048, 4, 15)]
+MODEL_VOCAB = 50257
+MODEL_T = 1024
+ROLE_TOKENS = 12
+
+
+def model_tokens(seed: int, scale: str, n_tokens: int, vocab: int = MODEL_VOCAB) -> np.ndarray:
+    """Uniform token ids int32 [n_tokens] of one synthetic context."""
+    return rng(seed, ROLE_TOKENS, sum(map(ord, scale)), n_tokens).integers(0, vocab, size=n_tokens, dtype=np.int32)

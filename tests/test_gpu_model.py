@@ -52,12 +52,19 @@ def tok(x):
     return torch.from_numpy(np.ascontiguousarray(x, dtype=np.int32).reshape(-1)).to("cuda")
 
 
-def test_served_block_matches_oracle():
-    say("model: served block vs oracle")
-    m, ref, _ = build()
+# (E, D, d, H, vocab, n_pos): heads of 32 (the paper's), 64 and 128; a ragged
+# head tile (vocab 1000 = 15 * 64 + 40); no encoder layer; no position table
+SHAPES = [dict(), dict(E=2, D=1, d=256, H=4, vocab=1000, n_pos=0), dict(E=0, D=2, d=128, H=1, vocab=77, n_pos=128)]
+
+
+@pytest.mark.parametrize("over", SHAPES, ids=["d128h4", "d256h4-nopos", "d128h1-E0"])
+def test_served_block_matches_oracle(over):
+    say("model: served block vs oracle", over)
+    m, ref, _ = build(**over)
+    s = dict(SHAPE, **over)
     g = np.random.default_rng(11)
     B = 7                                    # 6 cached blocks, two launches of 4 + 2; block 6 is past the position table
-    tokens = g.integers(0, SHAPE["vocab"], size=(B, SHAPE["b"]))
+    tokens = g.integers(0, s["vocab"], size=(B, s["b"]))
     smem.smem_model_encode(m, 0, list(range(B - 1)), tok(tokens[:B - 1]))
     logits = smem.smem_model_read(m, 0, [B - 1], tok(tokens[B - 1:]))
     ref.encode(0, tokens[:B - 1], list(range(B - 1)))
@@ -67,6 +74,34 @@ def test_served_block_matches_oracle():
     say("model rel err", err, "argmax agreement", float(np.mean(y.argmax(-1) == expect.argmax(-1))))
     assert np.all(np.isfinite(y))
     assert err <= TOL, err
+    # the first block reads the null row alone
+    first = host(smem.smem_model_read(m, 0, [0], tok(tokens[:1])))
+    e0 = ref.read(0, tokens[:1], [0])[0]
+    assert float(np.max(np.abs(first - e0)) / np.sqrt(np.mean(e0 ** 2))) <= TOL
+
+
+def test_prefill_cold_and_partial_reuse_bitwise():
+    """Cold prefill's final-block logits equal block-skip serving over the
+    cached context and the cold pass's last rows; partial reuse (reader from
+    the first uncached block) equals the cold prefill."""
+    say("model: cold prefill / partial reuse")
+    g = np.random.default_rng(14)
+    B = 9                                    # three read launches of 4 + 4 + 1 blocks
+    tokens = g.integers(0, SHAPE["vocab"], size=(B, SHAPE["b"]))
+    m, _, _ = build()
+    cold = smem.smem_model_prefill(m, 0, 0, B, tok(tokens))
+    skip = smem.smem_model_read(m, 0, [B - 1], tok(tokens[B - 1:]))
+    assert torch.equal(cold, skip)
+    full = smem.smem_model_read(m, 0, list(range(B)), tok(tokens))
+    assert torch.equal(cold, full[(B - 1) * SHAPE["b"]:])
+    p, _, _ = build()
+    smem.smem_model_encode(p, 0, [0, 1, 2], tok(tokens[:3]))
+    part = smem.smem_model_prefill(p, 0, 3, B - 3, tok(tokens[3:]))
+    assert torch.equal(part, cold)
+    with pytest.raises(smem.SmemError) as e:            # blocks already cached: nothing changes
+        smem.smem_model_prefill(p, 0, 2, 2, tok(tokens[2:4]))
+    assert e.value.code == smem.SMEM_EEXIST
+    assert torch.equal(smem.smem_model_read(p, 0, [B - 1], tok(tokens[B - 1:])), cold)
 
 
 def test_block_skip_equals_cold_pass_bitwise():
