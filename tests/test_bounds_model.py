@@ -200,37 +200,80 @@ def test_rows_reader_indexing(b, D):
     assert 32 <= 64
 
 
+def lin_chunk(K):
+    return 256 * ((K + 256 * 16 - 1) // (256 * 16))
+
+
 def _linear_ranges(M, N, K, ldx, ldy, n2, ns, split):
-    """Largest element index each k_linear access touches, from the kernel's
-    own index arithmetic (64 x 64 tile, waves 2 x 2, lanes 16 x 4)."""
-    hi = {"x": -1, "w": -1, "w2": -1, "y": -1}
-    for bx, by in itertools.product(range(-(-N // 64)), range(-(-M // 64))):
-        for wave, lane in itertools.product(range(4), (0, 15, 16, 47, 48, 63)):
-            wm, wn, kofs = wave & 1, wave >> 1, (lane >> 4) * 8
-            for i in range(2):
-                r = by * 64 + wm * 32 + i * 16 + (lane & 15)
-                rr = r if r < M else 0
-                hi["x"] = max(hi["x"], rr * ldx + kofs + (K - 32) + 7)
-            for j in range(2):
-                n = bx * 64 + wn * 32 + j * 16 + (lane & 15)
-                nn = n if n < N else 0
-                key, row = ("w", nn) if nn < n2 else ("w2", nn - n2)
-                hi[key] = max(hi[key], row * K + kofs + (K - 32) + 7)
-                for i, ii in itertools.product(range(2), range(4)):
-                    m = by * 64 + wm * 32 + i * 16 + 4 * (lane >> 4) + ii
-                    if m < M and n < N:
-                        if split:
-                            g, c = divmod(n, ns)
-                            assert g < 3 and c < ns
-                            hi["y"] = max(hi["y"], m * ns + c)
-                        else:
-                            hi["y"] = max(hi["y"], m * ldy + n)
+    """Largest element index each linear-map kernel touches, from the
+    kernels' own index arithmetic, for the kernel the host picks:
+    k_linear_skinny (M <= 128), k_gemm<128,128> or k_gemm<64,64>."""
+    hi = {"x": -1, "w": -1, "w2": -1, "y": -1, "lds": -1}
+
+    def wrow(n, k_last):
+        key, row = ("w", n) if n < n2 else ("w2", n - n2)
+        hi[key] = max(hi[key], row * K + k_last)
+
+    def out(m, n):
+        if m < M and n < N:
+            if split:
+                g, c = divmod(n, ns)
+                assert g < 3 and c < ns
+                hi["y"] = max(hi["y"], m * ns + c)
+            else:
+                hi["y"] = max(hi["y"], m * ldy + n)
+
+    lanes = (0, 15, 16, 47, 48, 63)
+    if M <= 128:
+        KS, CS = K // 32, lin_chunk(K) // 32
+        NC = -(-KS // CS)
+        assert NC * 64 * 16 * 4 <= 64 * 1024
+        for bx, by in itertools.product(range(-(-N // 16)), range(-(-M // 64))):
+            n0, m0 = bx * 16, by * 64
+            for lane in lanes:
+                kofs = (lane >> 4) * 8
+                last = (KS - 1) * 32 + kofs + 7             # st = min(u0 + u, s1 - 1) * 32 <= (KS - 1) * 32
+                for i in range(4):
+                    hi["x"] = max(hi["x"], min(m0 + i * 16 + (lane & 15), M - 1) * ldx + last)
+                    for ii in range(4):
+                        hi["lds"] = max(hi["lds"], (NC - 1) * 1024 + (i * 16 + 4 * (lane >> 4) + ii) * 16 + (lane & 15))
+                wrow(min(n0 + (lane & 15), N - 1), last)
+            for t in range(0, 256, 17):
+                row, c0 = t >> 2, (t & 3) * 4
+                hi["lds"] = max(hi["lds"], (NC - 1) * 1024 + row * 16 + c0 + 3)
+                for e in range(4):
+                    out(m0 + row, n0 + c0 + e)
+        assert hi["lds"] < NC * 1024
+        return hi
+    BM = BN = 128 if -(-N // 128) * -(-M // 128) >= 256 else 64
+    WM, WN = BM // 2, BN // 2
+    for bx, by in itertools.product(range(-(-N // BN)), range(-(-M // BM))):
+        n0, m0 = bx * BN, by * BM
+        for i in range((BM + BN) * 8 // 256):
+            for t in (0, 7, 8, 255):
+                q = t + 256 * i
+                A = q < BM * 8
+                r = q >> 3 if A else (q - BM * 8) >> 3
+                c = q & 7
+                last = c * 8 + (K // 64 - 1) * 64 + 7
+                if A:
+                    hi["x"] = max(hi["x"], min(m0 + r, M - 1) * ldx + last)
+                    assert r * 64 + ((c ^ (r & 7)) << 3) + 7 < BM * 64
+                else:
+                    wrow(min(n0 + r, N - 1), last)
+                    assert r * 64 + ((c ^ (r & 7)) << 3) + 7 < BN * 64
+        for wave, lane in itertools.product(range(4), lanes):
+            wm, wn = wave & 1, wave >> 1
+            for i, j, ii in itertools.product(range(WM // 16), range(WN // 16), range(4)):
+                assert wm * WM + i * 16 + (lane & 15) < BM and wn * WN + j * 16 + (lane & 15) < BN
+                out(m0 + wm * WM + i * 16 + 4 * (lane >> 4) + ii, n0 + wn * WN + j * 16 + (lane & 15))
     return hi
 
 
-@pytest.mark.parametrize("d,vocab,rows", [(128, 256, 448), (768, 1000, 130), (2048, 77, 64)])
+@pytest.mark.parametrize("d,vocab,rows", [(128, 256, 448), (768, 1000, 130), (2048, 77, 64), (256, 300, 100),
+                                         (768, 50257, 64), (1024, 4000, 4096)])
 def test_model_kernel_indexing(d, vocab, rows):
-    """Every k_linear call the model makes stays inside its operands (x
+    """Every linear-map launch the model makes stays inside its operands (x
     [rows, K] in a [max_tokens, ldx] buffer, W [N or n2, K] and [N - n2, K],
     y [rows, ldy]); LayerNorm and embedding lanes stay inside a d-wide row."""
     calls = [  # M, N, K, ldx, ldy, n2, ns, split, rows of W (first, second)
@@ -243,7 +286,7 @@ def test_model_kernel_indexing(d, vocab, rows):
         (rows, vocab, d, d, vocab, vocab, 0, False, vocab, 0),   # output head (fp32)
     ]
     for M, N, K, ldx, ldy, n2, ns, split, wrows, w2rows in calls:
-        assert K % 32 == 0 and K <= ldx
+        assert K % 64 == 0 and K <= ldx
         hi = _linear_ranges(M, N, K, ldx, ldy, n2, ns, split)
         assert hi["x"] < M * ldx
         assert hi["w"] < wrows * K

@@ -144,3 +144,27 @@ def test_delete_equals_never_encoded_bitwise_and_errors():
     smem.smem_model_encode(full, 0, list(range(B - 1)), tok(tokens[:B - 1]))
     assert torch.equal(smem.smem_model_read(a, 0, [B - 1], tok(tokens[B - 1:])),
                        smem.smem_model_read(full, 0, [B - 1], tok(tokens[B - 1:])))
+
+
+def test_tilings_agree_bitwise():
+    """Every linear map keeps one reduction order per output whatever the
+    kernel: a one-block read (few-row kernel), a 4-block read (64 x 64
+    tiles) and a 16-block read (the 50257-like wide head on 128 x 128 tiles)
+    give the same logits bit for bit, and match the oracle."""
+    say("model: tilings agree")
+    over = dict(vocab=4096, n_pos=1024)
+    m, ref, _ = build(max_blocks=20, n_pages=20, max_tokens=1024, **over)
+    g = np.random.default_rng(15)
+    B = 16
+    tokens = g.integers(0, 4096, size=(B, SHAPE["b"]))
+    smem.smem_model_encode(m, 0, list(range(B)), tok(tokens))
+    full = smem.smem_model_read(m, 0, list(range(B)), tok(tokens))
+    four = smem.smem_model_read(m, 0, [9, 10, 11, 12], tok(tokens[9:13]))
+    assert torch.equal(four, full[9 * 64:13 * 64])
+    for j in (0, 5, 15):
+        one = smem.smem_model_read(m, 0, [j], tok(tokens[j:j + 1]))
+        assert torch.equal(one, full[j * 64:(j + 1) * 64]), j
+    ref.encode(0, tokens[:15], list(range(15)))
+    expect = ref.read(0, tokens[15:], [15])[0]
+    y = host(full[15 * 64:])
+    assert float(np.max(np.abs(y - expect)) / np.sqrt(np.mean(expect ** 2))) <= TOL
