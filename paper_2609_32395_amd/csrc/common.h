@@ -30,6 +30,15 @@ constexpr int kSplitStride = kSplitCap + 1;
 constexpr int kMinPagesDecode = 8;
 constexpr int kMinPagesPrefill = 4;
 constexpr int kSplitCapPrefill = 32;
+// Memory splits of one prefill (query block, head): enough that a single
+// query block fills the chip (about 512 workgroups over the H heads), no more,
+// since every split writes a b x (d_h + 4) partial that the merge reads back.
+// A function of the store's H alone, so a block's result never depends on the
+// batch it is read in.
+inline int prefill_split_cap(int H) {
+  const int c = 512 / (H > 0 ? H : 1);
+  return c < 1 ? 1 : (c > kSplitCapPrefill ? kSplitCapPrefill : c);
+}
 // Query slots whose prefill partials the workspace must hold at once.
 constexpr int kPrefillSlotChunk = 16;
 // Row-plane decode: pages per split max(kMinPagesRows, ceil(n_read /
@@ -62,6 +71,34 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 // displacing reused lines in the caches.
 __device__ __forceinline__ u32x4 load_stream(const void* p) {
   return __builtin_nontemporal_load((const u32x4*)p);
+}
+
+// ---------------------------------------------------------------- LDS DMA
+
+// s_waitcnt with only the vector-memory counter limited to n (0..63).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
+
+// One 16-byte-per-lane global -> LDS load: lane l's 16 bytes land at LDS
+// byte address lds + 16*l (M0 holds the uniform base).  Issued as assembly
+// so that the compiler does not tie later LDS reads or barriers to it with a
+// full vector-memory wait; completion is waited for explicitly (wait_vm).
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(lds) : "memory", "m0");
+}
+
+// Barrier for LDS hand-offs between waves: this wave's LDS writes complete
+// (lgkmcnt 0), then s_barrier; vector-memory loads (the DMA ring) stay in
+// flight.  The empty asm statements keep the compiler from moving memory
+// operations across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" : : : "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // vmcnt 63, expcnt 7, lgkmcnt 0
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" : : : "memory");
 }
 
 // ---------------------------------------------------------------- conversions

@@ -1,0 +1,326 @@
+// Linear maps y = x W^T (W stored [out, in], a linear layer's layout) on
+// MFMA for the whole-model runtime: a few-row kernel and an LDS-tiled GEMM
+// that share one reduction order, and the host dispatch between them.
+// Both MFMA operands run along the reduction dimension, so a lane's 8
+// k-values are 16 contiguous bytes of an x row and of a W row.
+#pragma once
+
+#include "common.h"
+
+namespace smem {
+
+typedef __bf16 bf16x8m __attribute__((ext_vector_type(8)));
+
+enum LinEpi : int { kLinStore = 0, kLinGelu = 1, kLinResid = 2, kLinF32 = 3, kLinSplit = 4 };
+
+struct LinArgs {
+  const uint16_t* x;   // [M][ldx], K used
+  const uint16_t* w;   // output rows n < n2: w + n*K
+  const uint16_t* w2;  // output rows n >= n2: w2 + (n - n2)*K
+  const uint16_t* res; // residual [M][ldy] (kLinResid; may equal y)
+  uint16_t* y;         // [M][ldy]
+  uint16_t* y1;        // kLinSplit: columns [ns, 2ns) -> y1, [2ns, 3ns) -> y2 (each [M][ns])
+  uint16_t* y2;
+  float* yf;           // kLinF32: [M][ldy]
+  int32_t M, N, K, ldx, ldy, n2, ns;
+};
+
+// erf by Abramowitz and Stegun, Handbook of Mathematical Functions, formula
+// 7.1.26: erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),
+// t = 1 / (1 + p x), x >= 0, absolute error <= 1.5e-7 (odd extension for
+// x < 0); far below the bf16 rounding of the activations it feeds.
+__device__ __forceinline__ float erf_as(float x) {
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(1.f + 0.3275911f * ax);
+  const float poly = ((((1.061405429f * t - 1.453152027f) * t + 1.421413741f) * t - 0.284496736f) * t + 0.254829592f) * t;
+  const float e = __builtin_amdgcn_exp2f(-ax * ax * 1.4426950408889634f);
+  return copysignf(1.f - poly * e, x);
+}
+
+// GELU, exact (erf) form: x * Phi(x) = x/2 * (1 + erf(x / sqrt 2)).
+__device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.f + erf_as(x * 0.70710678118654752f)); }
+
+// Reduction order of every linear map, whatever kernel computes it: the
+// K-range is cut into chunks of lin_chunk(K) (a multiple of 256); inside a
+// chunk, one 16x16x32 bf16 MFMA per 32-wide k step accumulates from zero in
+// ascending k; the chunk sums are then added in ascending chunk order to a
+// total that starts at zero.  Each output element therefore sees the same
+// operations in the same order for any M and any tiling, which keeps a
+// row's result independent of the other rows in the call (block-skip serving
+// reproduces the cold pass bit for bit).
+__host__ __device__ constexpr int lin_chunk(int K) { return 256 * ((K + 256 * 16 - 1) / (256 * 16)); }
+
+template <int EPI>
+__device__ __forceinline__ void lin_store(const LinArgs& a, int m, int n, float v) {
+  if constexpr (EPI == kLinF32) {
+    a.yf[(size_t)m * a.ldy + n] = v;
+  } else if constexpr (EPI == kLinGelu) {
+    a.y[(size_t)m * a.ldy + n] = f32_to_bf16_bits(gelu_erf(v));
+  } else if constexpr (EPI == kLinResid) {
+    const size_t o = (size_t)m * a.ldy + n;
+    a.y[o] = f32_to_bf16_bits(v + bf16_bits_to_f32(a.res[o]));
+  } else if constexpr (EPI == kLinSplit) {
+    const int g = n / a.ns, c = n - g * a.ns;
+    uint16_t* dst = g == 0 ? a.y : (g == 1 ? a.y1 : a.y2);
+    dst[(size_t)m * a.ns + c] = f32_to_bf16_bits(v);
+  } else {
+    a.y[(size_t)m * a.ldy + n] = f32_to_bf16_bits(v);
+  }
+}
+
+// Four consecutive outputs n .. n+3 of row m (n % 4 == 0; bf16 rows have
+// ldy % 4 == 0, so the four share one 8-byte word; a split's column groups
+// are multiples of 4 wide).  Columns >= N are dropped.
+template <int EPI>
+__device__ __forceinline__ void lin_store4(const LinArgs& a, int m, int n, const f32x4& v) {
+  if constexpr (EPI == kLinF32) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (n + e < a.N) a.yf[(size_t)m * a.ldy + n + e] = v[e];
+  } else {
+    if (n + 3 >= a.N) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (n + e < a.N) lin_store<EPI>(a, m, n + e, v[e]);
+      return;
+    }
+    float o[4];
+    uint16_t* dst;
+    if constexpr (EPI == kLinSplit) {
+      const int g = n / a.ns, c = n - g * a.ns;
+      dst = (g == 0 ? a.y : (g == 1 ? a.y1 : a.y2)) + (size_t)m * a.ns + c;
+    } else {
+      dst = a.y + (size_t)m * a.ldy + n;
+    }
+    if constexpr (EPI == kLinResid) {
+      const u32x2 r = *(const u32x2*)(a.res + (size_t)m * a.ldy + n);
+      o[0] = v[0] + bf16_bits_to_f32(r.x & 0xffffu);
+      o[1] = v[1] + bf16_bits_to_f32(r.x >> 16);
+      o[2] = v[2] + bf16_bits_to_f32(r.y & 0xffffu);
+      o[3] = v[3] + bf16_bits_to_f32(r.y >> 16);
+    } else if constexpr (EPI == kLinGelu) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = gelu_erf(v[e]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = v[e];
+    }
+    *(u32x2*)dst = u32x2{(uint32_t)f32_to_bf16_bits(o[0]) | ((uint32_t)f32_to_bf16_bits(o[1]) << 16),
+                         (uint32_t)f32_to_bf16_bits(o[2]) | ((uint32_t)f32_to_bf16_bits(o[3]) << 16)};
+  }
+}
+
+__device__ __forceinline__ const uint16_t* lin_wrow(const LinArgs& a, int n) {
+  return n < a.n2 ? a.w + (size_t)n * a.K : a.w2 + (size_t)(n - a.n2) * a.K;
+}
+
+// One 16x16x32 step with the W tile as the MFMA's row operand and the x
+// tile as its column operand: lane l then holds outputs (x row l % 16,
+// W rows 4 (l / 16) .. +3), four consecutive output columns of one row.
+__device__ __forceinline__ f32x4 mfma16(const u32x4& A, const u32x4& B, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8m, A), __builtin_bit_cast(bf16x8m, B), c,
+                                                 0, 0, 0);
+}
+
+// Few rows (one or two blocks): the weights stream from HBM once and the
+// time is load latency.  A workgroup owns 64 rows x 16 output columns; its
+// 4 waves take the reduction chunks round-robin, each chunk's steps of
+// operands (4 row tiles of x, 1 tile of W) loaded 8 steps at a time, and
+// leave the chunk sums in LDS, where they are added in chunk order.
+// Dynamic LDS: ceil(K / lin_chunk(K)) x 4 KiB <= 64 KiB.
+template <int EPI>
+__global__ void __launch_bounds__(256) k_linear_skinny(LinArgs a) {
+  extern __shared__ float part[];   // [n_chunks][64][16]
+  const int n0 = blockIdx.x * 16, m0 = blockIdx.y * 64;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int kofs = (lane >> 4) * 8;
+  const int KS = a.K / 32, CS = lin_chunk(a.K) / 32, NC = (KS + CS - 1) / CS;
+  const uint16_t* ap[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) ap[i] = a.x + (size_t)min(m0 + i * 16 + (lane & 15), a.M - 1) * a.ldx + kofs;
+  const uint16_t* bp = lin_wrow(a, min(n0 + (lane & 15), a.N - 1)) + kofs;
+  for (int c = wave; c < NC; c += 4) {
+    const int s0 = c * CS, s1 = min(KS, s0 + CS);
+    f32x4 acc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int u0 = s0; u0 < s1; u0 += 8) {
+      u32x4 A[8][4], B[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int st = min(u0 + u, s1 - 1) * 32;
+        B[u] = *(const u32x4*)(bp + st);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) A[u][i] = *(const u32x4*)(ap[i] + st);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (u0 + u < s1) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[i] = mfma16(B[u], A[u][i], acc[i]);
+        }
+      }
+    }
+    float* pc = part + c * 1024;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) *(f32x4*)(pc + (i * 16 + (lane & 15)) * 16 + 4 * (lane >> 4)) = acc[i];
+  }
+  __syncthreads();
+  const int row = threadIdx.x >> 2, c0 = (threadIdx.x & 3) * 4;
+  f32x4 v = {0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c < NC; ++c) v += *(const f32x4*)(part + c * 1024 + row * 16 + c0);
+  const int m = m0 + row;
+  if (m < a.M) lin_store4<EPI>(a, m, n0 + c0, v);
+}
+
+// Many rows: BM x BN tiles, WAVES_M x WAVES_N waves (each (BM/WAVES_M) x
+// (BN/WAVES_N) as 16x16 MFMA tiles), K in BK-wide stages moved global -> LDS
+// by DMA through a ring of NS stages, so no register holds an operand in
+// transit and NS - 1 stages are in flight during each stage's MFMAs.  An LDS
+// row is BK bf16 = BK/8 chunks of 16 B; chunk c of row r sits at slot
+// c ^ swz(r), so the 16 rows one MFMA operand read touches cover every bank
+// once.  Tiles are visited in groups of 8 row tiles, and consecutive groups
+// of the launch order land on one XCD, so the A and W tiles a group shares
+// stay in that XCD's L2.
+template <int BM_, int BN_, int BK_, int NS_, int WAVES_M, int WAVES_N>
+struct GemmCfg {
+  static constexpr int BM = BM_, BN = BN_, BK = BK_, NS = NS_;
+  static constexpr int NW = WAVES_M * WAVES_N, NT = 64 * NW;
+  static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N, TM = WM / 16, TN = WN / 16;
+  static constexpr int CPR = BK / 8;                 // 16-byte chunks per LDS row
+  static constexpr int RPI = 1024 / (BK * 2);        // rows per DMA instruction (1 KiB)
+  static constexpr int R256 = 256 / (BK * 2);        // rows per 256 bytes
+  static constexpr int IA = BM / RPI / NW, IB = BN / RPI / NW;
+  static constexpr int STAGE = (BM + BN) * BK;       // elements per stage
+  static_assert(IA * RPI * NW == BM && IB * RPI * NW == BN, "DMA rows must tile the stage");
+  static_assert(NS >= 2 && NS <= 5, "ring depth");
+  __device__ static constexpr int swz(int r) { return (r / R256) % CPR; }
+};
+
+template <int N>
+__device__ __forceinline__ void wait_stages(int ahead) {
+  if (ahead >= 3) wait_vm<3 * N < 63 ? 3 * N : 63>();
+  else if (ahead == 2) wait_vm<2 * N>();
+  else if (ahead == 1) wait_vm<N>();
+  else wait_vm<0>();
+}
+
+template <int EPI, class C>
+__global__ void __launch_bounds__(C::NT, 2 * 4 / C::NW) k_gemm(LinArgs a, int tiles_m, int tiles_n) {
+  constexpr int BM = C::BM, BN = C::BN, BK = C::BK, NS = C::NS, WM = C::WM, WN = C::WN;
+  constexpr int TM = C::TM, TN = C::TN, IA = C::IA, IB = C::IB, STAGE = C::STAGE;
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[NS * STAGE];
+  // launch order -> tile: consecutive pids of one XCD, then groups of 8 row tiles
+  const int T = tiles_m * tiles_n;
+  int pid = blockIdx.x;
+  if ((T & 7) == 0) pid = (pid & 7) * (T >> 3) + (pid >> 3);
+  const int per_group = 8 * tiles_n, g0 = (pid / per_group) * 8, gsz = min(tiles_m - g0, 8);
+  const int tm = g0 + (pid % per_group) % gsz, tn = (pid % per_group) / gsz;
+  const int n0 = tn * BN, m0 = tm * BM;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave % (BM / WM), wn = wave / (BM / WM);
+  const int KT = a.K / BK, CT = lin_chunk(a.K) / BK;
+  const uint16_t* ga[IA];
+  const uint16_t* gb[IB];
+#pragma unroll
+  for (int i = 0; i < IA; ++i) {
+    const int r = (wave * IA + i) * C::RPI + lane / C::CPR, c = (lane % C::CPR) ^ C::swz(r);
+    ga[i] = a.x + (size_t)min(m0 + r, a.M - 1) * a.ldx + c * 8;
+  }
+#pragma unroll
+  for (int i = 0; i < IB; ++i) {
+    const int r = (wave * IB + i) * C::RPI + lane / C::CPR, c = (lane % C::CPR) ^ C::swz(r);
+    gb[i] = lin_wrow(a, min(n0 + r, a.N - 1)) + c * 8;
+  }
+  const uint32_t lbase = (uint32_t)(uintptr_t)lds;
+  auto issue = [&](int kt) {
+    const uint32_t sb = lbase + (uint32_t)((kt % NS) * STAGE * 2);
+#pragma unroll
+    for (int i = 0; i < IA; ++i)
+      dma16(ga[i] + kt * BK, __builtin_amdgcn_readfirstlane(sb + (wave * IA + i) * 1024));
+#pragma unroll
+    for (int i = 0; i < IB; ++i)
+      dma16(gb[i] + kt * BK, __builtin_amdgcn_readfirstlane(sb + BM * BK * 2 + (wave * IB + i) * 1024));
+  };
+  f32x4 acc[TM][TN], tot[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = tot[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int p = 0; p < NS - 1 && p < KT; ++p) issue(p);
+  for (int kt = 0; kt < KT; ++kt) {
+    wait_stages<IA + IB>(min(NS - 2, KT - 1 - kt));
+    lds_barrier();                       // stage kt is in LDS; every wave is done with stage kt - 1
+    if (kt + NS - 1 < KT) issue(kt + NS - 1);
+    const uint16_t* sa = lds + (kt % NS) * STAGE;
+    const uint16_t* sb = sa + BM * BK;
+#pragma unroll
+    for (int ks = 0; ks < BK / 32; ++ks) {
+      const int c = ks * 4 + (lane >> 4);
+      u32x4 B[TN];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int r = wn * WN + j * 16 + (lane & 15);
+        B[j] = *(const u32x4*)(sb + r * BK + ((c ^ C::swz(r)) << 3));
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int r = wm * WM + i * 16 + (lane & 15);
+        const u32x4 A = *(const u32x4*)(sa + r * BK + ((c ^ C::swz(r)) << 3));
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma16(B[j], A, acc[i][j]);
+      }
+    }
+    if ((kt + 1) % CT == 0 || kt + 1 == KT) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          tot[i][j] += acc[i][j];
+          acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int m = m0 + wm * WM + i * 16 + (lane & 15);
+    if (m < a.M) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) lin_store4<EPI>(a, m, n0 + wn * WN + j * 16 + 4 * (lane >> 4), tot[i][j]);
+    }
+  }
+}
+
+template <int EPI, class C>
+static void launch_gemm(const LinArgs& a, hipStream_t s) {
+  const int tm = (a.M + C::BM - 1) / C::BM, tn = (a.N + C::BN - 1) / C::BN;
+  hipLaunchKernelGGL((k_gemm<EPI, C>), dim3(tm * tn), dim3(C::NT), 0, s, a, tm, tn);
+}
+
+#ifndef GEMM_BIG
+#define GEMM_BIG GemmCfg<128, 128, 64, 2, 2, 2>
+#endif
+#ifndef GEMM_MID
+#define GEMM_MID GemmCfg<64, 64, 64, 2, 2, 2>
+#endif
+using GemmBig = GEMM_BIG;
+using GemmMid = GEMM_MID;
+
+template <int EPI>
+static hipError_t linear(const LinArgs& a, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (a.K <= 0 || a.K % 64) return hipErrorInvalidValue;
+  if (EPI != kLinF32 && (a.ldy % 4 || (EPI == kLinSplit && a.ns % 4))) return hipErrorInvalidValue;
+  if (a.M <= 128) {
+    const int nc = (a.K + lin_chunk(a.K) - 1) / lin_chunk(a.K);
+    hipLaunchKernelGGL((k_linear_skinny<EPI>), dim3((a.N + 15) / 16, (a.M + 63) / 64), dim3(256),
+                       (size_t)nc * 64 * 16 * 4, s, a);
+  } else if ((size_t)((a.N + GemmBig::BN - 1) / GemmBig::BN) * ((a.M + GemmBig::BM - 1) / GemmBig::BM) >= 256) {
+    launch_gemm<EPI, GemmBig>(a, s);
+  } else {
+    launch_gemm<EPI, GemmMid>(a, s);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace smem

@@ -3,12 +3,8 @@
 // layer, the reader stack and the output head, driven from the host on the
 // caller's stream.  Attention runs on the library's kernels (block-local
 // encoder kernel for the encoder and the readers' self-attention, the
-// block-skip reader for their cross-attention); the linear maps, LayerNorm
-// and the embedding run on the kernels below.
-//
-// Linear maps are y = x W^T with W stored [out, in] (a linear layer's
-// layout): both MFMA operands then run along the reduction dimension, so a
-// lane's 8 k-values are 16 contiguous bytes of an x row and of a W row.
+// block-skip reader for their cross-attention); the linear maps run on the
+// kernels of linear.h, LayerNorm and the embedding on the kernels below.
 #include <algorithm>
 #include <cmath>
 #include <cstring>
@@ -17,227 +13,10 @@
 #include <vector>
 
 #include "common.h"
+#include "linear.h"
 #include "smem.h"
 
 namespace smem {
-
-typedef __bf16 bf16x8m __attribute__((ext_vector_type(8)));
-
-enum LinEpi : int { kLinStore = 0, kLinGelu = 1, kLinResid = 2, kLinF32 = 3, kLinSplit = 4 };
-
-struct LinArgs {
-  const uint16_t* x;   // [M][ldx], K used
-  const uint16_t* w;   // output rows n < n2: w + n*K
-  const uint16_t* w2;  // output rows n >= n2: w2 + (n - n2)*K
-  const uint16_t* res; // residual [M][ldy] (kLinResid; may equal y)
-  uint16_t* y;         // [M][ldy]
-  uint16_t* y1;        // kLinSplit: columns [ns, 2ns) -> y1, [2ns, 3ns) -> y2 (each [M][ns])
-  uint16_t* y2;
-  float* yf;           // kLinF32: [M][ldy]
-  int32_t M, N, K, ldx, ldy, n2, ns;
-};
-
-__device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
-
-// Reduction order of every linear map, whatever kernel computes it: the
-// K-range is cut into chunks of lin_chunk(K) (a multiple of 256); inside a
-// chunk, one 16x16x32 bf16 MFMA per 32-wide k step accumulates from zero in
-// ascending k; the chunk sums are then added in ascending chunk order to a
-// total that starts at zero.  Each output element therefore sees the same
-// operations in the same order for any M and any tiling, which keeps a
-// row's result independent of the other rows in the call (block-skip serving
-// reproduces the cold pass bit for bit).
-__host__ __device__ constexpr int lin_chunk(int K) { return 256 * ((K + 256 * 16 - 1) / (256 * 16)); }
-
-template <int EPI>
-__device__ __forceinline__ void lin_store(const LinArgs& a, int m, int n, float v) {
-  if constexpr (EPI == kLinF32) {
-    a.yf[(size_t)m * a.ldy + n] = v;
-  } else if constexpr (EPI == kLinGelu) {
-    a.y[(size_t)m * a.ldy + n] = f32_to_bf16_bits(gelu_erf(v));
-  } else if constexpr (EPI == kLinResid) {
-    const size_t o = (size_t)m * a.ldy + n;
-    a.y[o] = f32_to_bf16_bits(v + bf16_bits_to_f32(a.res[o]));
-  } else if constexpr (EPI == kLinSplit) {
-    const int g = n / a.ns, c = n - g * a.ns;
-    uint16_t* dst = g == 0 ? a.y : (g == 1 ? a.y1 : a.y2);
-    dst[(size_t)m * a.ns + c] = f32_to_bf16_bits(v);
-  } else {
-    a.y[(size_t)m * a.ldy + n] = f32_to_bf16_bits(v);
-  }
-}
-
-__device__ __forceinline__ const uint16_t* lin_wrow(const LinArgs& a, int n) {
-  return n < a.n2 ? a.w + (size_t)n * a.K : a.w2 + (size_t)(n - a.n2) * a.K;
-}
-
-__device__ __forceinline__ f32x4 mfma16(const u32x4& A, const u32x4& B, const f32x4& c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8m, A), __builtin_bit_cast(bf16x8m, B), c,
-                                                 0, 0, 0);
-}
-
-// Few rows (one or two blocks): the weights stream from HBM once and the
-// time is load latency.  A workgroup owns 64 rows x 16 output columns; its
-// 4 waves take the reduction chunks round-robin, each chunk's steps of
-// operands (4 row tiles of x, 1 tile of W) loaded 8 steps at a time, and
-// leave the chunk sums in LDS, where they are added in chunk order.
-// Dynamic LDS: ceil(K / lin_chunk(K)) x 4 KiB <= 64 KiB.
-template <int EPI>
-__global__ void __launch_bounds__(256) k_linear_skinny(LinArgs a) {
-  extern __shared__ float part[];   // [n_chunks][64][16]
-  const int n0 = blockIdx.x * 16, m0 = blockIdx.y * 64;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int kofs = (lane >> 4) * 8;
-  const int KS = a.K / 32, CS = lin_chunk(a.K) / 32, NC = (KS + CS - 1) / CS;
-  const uint16_t* ap[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) ap[i] = a.x + (size_t)min(m0 + i * 16 + (lane & 15), a.M - 1) * a.ldx + kofs;
-  const uint16_t* bp = lin_wrow(a, min(n0 + (lane & 15), a.N - 1)) + kofs;
-  for (int c = wave; c < NC; c += 4) {
-    const int s0 = c * CS, s1 = min(KS, s0 + CS);
-    f32x4 acc[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int u0 = s0; u0 < s1; u0 += 8) {
-      u32x4 A[8][4], B[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int st = min(u0 + u, s1 - 1) * 32;
-        B[u] = *(const u32x4*)(bp + st);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) A[u][i] = *(const u32x4*)(ap[i] + st);
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (u0 + u < s1) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) acc[i] = mfma16(A[u][i], B[u], acc[i]);
-        }
-      }
-    }
-    float* pc = part + c * 1024;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int ii = 0; ii < 4; ++ii) pc[(i * 16 + 4 * (lane >> 4) + ii) * 16 + (lane & 15)] = acc[i][ii];
-  }
-  __syncthreads();
-  const int row = threadIdx.x >> 2, c0 = (threadIdx.x & 3) * 4;
-  f32x4 v = {0.f, 0.f, 0.f, 0.f};
-  for (int c = 0; c < NC; ++c) v += *(const f32x4*)(part + c * 1024 + row * 16 + c0);
-  const int m = m0 + row;
-  if (m >= a.M) return;
-#pragma unroll
-  for (int e = 0; e < 4; ++e)
-    if (n0 + c0 + e < a.N) lin_store<EPI>(a, m, n0 + c0 + e, v[e]);
-}
-
-// Many rows: BM x BN tiles, 4 waves as 2 x 2 (each (BM/2) x (BN/2) as 16x16
-// MFMA tiles), K in 64-wide stages through a double-buffered LDS tile
-// (operands staged through registers, the next stage's global loads in
-// flight during the current stage's MFMAs).  LDS rows are 64 bf16 = 8
-// chunks of 16 B; chunk c of row r sits at slot c ^ (r & 7), so the 16 rows
-// an MFMA operand read touches fall on distinct banks.
-template <int EPI, int BM, int BN>
-__global__ void __launch_bounds__(256, 2) k_gemm(LinArgs a) {
-  constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 16, TN = WN / 16;
-  constexpr int LOADS = (BM + BN) * 8 / 256;
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * 64];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * 64];
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int wm = wave & 1, wn = wave >> 1;
-  const int KT = a.K / 64, CT = lin_chunk(a.K) / 64;
-  const uint16_t* gp[LOADS];
-  int lo[LOADS];
-#pragma unroll
-  for (int i = 0; i < LOADS; ++i) {
-    const int q = t + 256 * i;
-    const bool A = q < BM * 8;             // uniform per i: BM * 8 is a multiple of 256
-    const int r = A ? q >> 3 : (q - BM * 8) >> 3, c = q & 7;
-    gp[i] = (A ? a.x + (size_t)min(m0 + r, a.M - 1) * a.ldx : lin_wrow(a, min(n0 + r, a.N - 1))) + c * 8;
-    lo[i] = r * 64 + ((c ^ (r & 7)) << 3);
-  }
-  u32x4 stg[LOADS];
-  auto gload = [&](int kt) {
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) stg[i] = *(const u32x4*)(gp[i] + kt * 64);
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      uint16_t* dst = (256 * i < BM * 8) ? sA[buf] : sB[buf];
-      *(u32x4*)(dst + lo[i]) = stg[i];
-    }
-  };
-  f32x4 acc[TM][TN], tot[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = tot[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) gload(kt + 1);
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int c = ks * 4 + (lane >> 4);
-      u32x4 B[TN];
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int r = wn * WN + j * 16 + (lane & 15);
-        B[j] = *(const u32x4*)(sB[buf] + r * 64 + ((c ^ (r & 7)) << 3));
-      }
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int r = wm * WM + i * 16 + (lane & 15);
-        const u32x4 A = *(const u32x4*)(sA[buf] + r * 64 + ((c ^ (r & 7)) << 3));
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma16(A, B[j], acc[i][j]);
-      }
-    }
-    if ((kt + 1) % CT == 0 || kt + 1 == KT) {
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          tot[i][j] += acc[i][j];
-          acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-    }
-    if (kt + 1 < KT) lstore(buf ^ 1);
-    __syncthreads();
-  }
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int n = n0 + wn * WN + j * 16 + (lane & 15);
-#pragma unroll
-      for (int ii = 0; ii < 4; ++ii) {
-        const int m = m0 + wm * WM + i * 16 + 4 * (lane >> 4) + ii;
-        if (m < a.M && n < a.N) lin_store<EPI>(a, m, n, tot[i][j][ii]);
-      }
-    }
-}
-
-template <int EPI>
-static hipError_t linear(const LinArgs& a, hipStream_t s) {
-  if (a.M <= 0 || a.N <= 0) return hipSuccess;
-  if (a.K <= 0 || a.K % 64) return hipErrorInvalidValue;
-  if (a.M <= 128) {
-    const int nc = (a.K + lin_chunk(a.K) - 1) / lin_chunk(a.K);
-    hipLaunchKernelGGL((k_linear_skinny<EPI>), dim3((a.N + 15) / 16, (a.M + 63) / 64), dim3(256),
-                       (size_t)nc * 64 * 16 * 4, s, a);
-  } else if ((size_t)((a.N + 127) / 128) * ((a.M + 127) / 128) >= 256) {
-    hipLaunchKernelGGL((k_gemm<EPI, 128, 128>), dim3((a.N + 127) / 128, (a.M + 127) / 128), dim3(256), 0, s, a);
-  } else {
-    hipLaunchKernelGGL((k_gemm<EPI, 64, 64>), dim3((a.N + 63) / 64, (a.M + 63) / 64), dim3(256), 0, s, a);
-  }
-  return hipGetLastError();
-}
 
 // LayerNorm of rows of width d (d % 8 == 0, d <= 2048): one wave per row,
 // statistics in fp32 (mean, then the centred second moment), eps 1e-5.

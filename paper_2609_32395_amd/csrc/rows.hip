@@ -52,32 +52,6 @@ struct RowsLds {
 // reference, so the result is the same up to rounding.
 constexpr float kLazy = 8.f;
 
-// s_waitcnt with only the vector-memory counter limited to n (0..63).
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
-}
-
-// One 16-byte-per-lane global -> LDS load: lane l's 16 bytes land at LDS
-// byte address lds + 16*l (M0 holds the uniform base).  Issued as assembly
-// so that the compiler does not tie later LDS reads or barriers to it with a
-// full vector-memory wait; completion is waited for explicitly (wait_vm).
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(lds) : "memory", "m0");
-}
-
-// Barrier for LDS hand-offs between waves: this wave's LDS writes complete
-// (lgkmcnt 0), then s_barrier; vector-memory loads (the DMA ring) stay in
-// flight.  The empty asm statements keep the compiler from moving memory
-// operations across it.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("" : : : "memory");
-  __builtin_amdgcn_s_waitcnt(0xC07F);   // vmcnt 63, expcnt 7, lgkmcnt 0
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" : : : "memory");
-}
-
 // Wave `wave` moves rows 4*wave .. 4*wave+3 of chunk c into stage st: each
 // row is D*2 bytes = D/512 DMA instructions of 1 KiB.
 template <int D>

@@ -580,7 +580,7 @@ static smem_status prefill_impl(smem_store* st, const smem_rope* rope, int32_t n
       a.seq[i] = sq;
       a.qblk[i] = query_block[i0 + i];
       a.n_read[i] = n_read_of(st, sq, query_block[i0 + i]);
-      a.pps[i] = mfma ? pages_per_split(a.n_read[i], kMinPagesPrefill, kSplitCapPrefill)
+      a.pps[i] = mfma ? pages_per_split(a.n_read[i], kMinPagesPrefill, prefill_split_cap(d.H))
                       : pages_per_split(a.n_read[i], kMinPagesDecode);
       a.aux[i] = -1;
     }

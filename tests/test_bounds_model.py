@@ -96,8 +96,10 @@ def test_mfma_indexing(dh):
     assert (BT * KS + dh * VS) * 2 <= 64 * 1024
     # prefill partials: at most 32 splits (split 0 also reads the in-block tile) inside the 65-wide stride
     for n_read in (0, 1, 4, 5, 512, 4096, 65536):
-        pps = pages_per_split(n_read, MIN_PAGES_PREFILL, SPLIT_CAP_PREFILL)
-        assert max(-(-n_read // pps), 1) <= SPLIT_CAP_PREFILL <= SPLIT_STRIDE
+        for H in (1, 12, 16, 24, 32, 64, 600):
+            cap = min(SPLIT_CAP_PREFILL, max(1, 512 // H))       # prefill_split_cap(H)
+            pps = pages_per_split(n_read, MIN_PAGES_PREFILL, cap)
+            assert max(-(-n_read // pps), 1) <= cap <= SPLIT_CAP_PREFILL <= SPLIT_STRIDE
     # output/ws lane writes: d0 = dt*16 + g*4, 4 values
     assert (dh // 16 - 1) * 16 + 3 * 4 + 3 < dh
 
@@ -223,6 +225,11 @@ def _linear_ranges(M, N, K, ldx, ldy, n2, ns, split):
             else:
                 hi["y"] = max(hi["y"], m * ldy + n)
 
+    def out4(m, n):                           # lin_store4: columns n .. n+3 of row m, n % 4 == 0
+        assert n % 4 == 0 and (ldy % 4 == 0 or not split)
+        for e in range(4):
+            out(m, n + e)
+
     lanes = (0, 15, 16, 47, 48, 63)
     if M <= 128:
         KS, CS = K // 32, lin_chunk(K) // 32
@@ -235,38 +242,63 @@ def _linear_ranges(M, N, K, ldx, ldy, n2, ns, split):
                 last = (KS - 1) * 32 + kofs + 7             # st = min(u0 + u, s1 - 1) * 32 <= (KS - 1) * 32
                 for i in range(4):
                     hi["x"] = max(hi["x"], min(m0 + i * 16 + (lane & 15), M - 1) * ldx + last)
-                    for ii in range(4):
-                        hi["lds"] = max(hi["lds"], (NC - 1) * 1024 + (i * 16 + 4 * (lane >> 4) + ii) * 16 + (lane & 15))
+                    hi["lds"] = max(hi["lds"], (NC - 1) * 1024 + (i * 16 + (lane & 15)) * 16 + 4 * (lane >> 4) + 3)
                 wrow(min(n0 + (lane & 15), N - 1), last)
             for t in range(0, 256, 17):
                 row, c0 = t >> 2, (t & 3) * 4
                 hi["lds"] = max(hi["lds"], (NC - 1) * 1024 + row * 16 + c0 + 3)
-                for e in range(4):
-                    out(m0 + row, n0 + c0 + e)
+                out4(m0 + row, n0 + c0)
         assert hi["lds"] < NC * 1024
         return hi
-    BM = BN = 128 if -(-N // 128) * -(-M // 128) >= 256 else 64
-    WM, WN = BM // 2, BN // 2
-    for bx, by in itertools.product(range(-(-N // BN)), range(-(-M // BM))):
+    big = -(-N // 128) * -(-M // 128) >= 256
+    BM = BN = 128 if big else 64
+    BK, NS, WAVES_M, WAVES_N = 64, 2, 2, 2         # GemmCfg of both tile sizes
+    NW = WAVES_M * WAVES_N
+    WM, WN = BM // WAVES_M, BN // WAVES_N
+    CPR, RPI, R256 = BK // 8, 1024 // (BK * 2), 256 // (BK * 2)
+    IA, IB = BM // RPI // NW, BN // RPI // NW
+    STAGE = (BM + BN) * BK
+    KT = K // BK
+    swz = lambda r: (r // R256) % CPR
+    tm_, tn_ = -(-M // BM), -(-N // BN)
+    T = tm_ * tn_
+    seen = set()
+    for p in range(T):                             # launch order -> tile: a bijection onto the tiles
+        pid = (p & 7) * (T >> 3) + (p >> 3) if T % 8 == 0 else p
+        per_group = 8 * tn_
+        g0 = (pid // per_group) * 8
+        gsz = min(tm_ - g0, 8)
+        seen.add((g0 + (pid % per_group) % gsz, (pid % per_group) // gsz))
+    assert seen == set(itertools.product(range(tm_), range(tn_)))
+    for by, bx in sorted(seen)[:: max(1, len(seen) // 40)] + [(tm_ - 1, tn_ - 1)]:
         n0, m0 = bx * BN, by * BM
-        for i in range((BM + BN) * 8 // 256):
-            for t in (0, 7, 8, 255):
-                q = t + 256 * i
-                A = q < BM * 8
-                r = q >> 3 if A else (q - BM * 8) >> 3
-                c = q & 7
-                last = c * 8 + (K // 64 - 1) * 64 + 7
-                if A:
-                    hi["x"] = max(hi["x"], min(m0 + r, M - 1) * ldx + last)
-                    assert r * 64 + ((c ^ (r & 7)) << 3) + 7 < BM * 64
-                else:
-                    wrow(min(n0 + r, N - 1), last)
-                    assert r * 64 + ((c ^ (r & 7)) << 3) + 7 < BN * 64
-        for wave, lane in itertools.product(range(4), lanes):
-            wm, wn = wave & 1, wave >> 1
-            for i, j, ii in itertools.product(range(WM // 16), range(WN // 16), range(4)):
-                assert wm * WM + i * 16 + (lane & 15) < BM and wn * WN + j * 16 + (lane & 15) < BN
-                out(m0 + wm * WM + i * 16 + 4 * (lane >> 4) + ii, n0 + wn * WN + j * 16 + (lane & 15))
+        for wave, lane in itertools.product(range(NW), range(64)):
+            for i in range(IA):                  # A: DMA source and LDS destination of instruction i
+                r = (wave * IA + i) * RPI + lane // CPR
+                c = (lane % CPR) ^ swz(r)
+                hi["x"] = max(hi["x"], min(m0 + r, M - 1) * ldx + c * 8 + (KT - 1) * BK + 7)
+                dst = (NS - 1) * STAGE * 2 + (wave * IA + i) * 1024 + 16 * lane + 15
+                assert r < BM and dst - (NS - 1) * STAGE * 2 < BM * BK * 2
+            for i in range(IB):
+                r = (wave * IB + i) * RPI + lane // CPR
+                c = (lane % CPR) ^ swz(r)
+                wrow(min(n0 + r, N - 1), c * 8 + (KT - 1) * BK + 7)
+                dst = (NS - 1) * STAGE * 2 + BM * BK * 2 + (wave * IB + i) * 1024 + 16 * lane + 15
+                assert r < BN and dst < NS * STAGE * 2
+        for wave, lane in itertools.product(range(NW), lanes):
+            wm, wn = wave % WAVES_M, wave // WAVES_M
+            for ks in range(BK // 32):
+                c = ks * 4 + (lane >> 4)
+                for i in range(WM // 16):        # operand reads: row r, slot c ^ swz(r), 8 elements
+                    r = wm * WM + i * 16 + (lane & 15)
+                    assert r < BM and r * BK + ((c ^ swz(r)) << 3) + 7 < BM * BK
+                for j in range(WN // 16):
+                    r = wn * WN + j * 16 + (lane & 15)
+                    assert r < BN and BM * BK + r * BK + ((c ^ swz(r)) << 3) + 7 < STAGE
+            for i, j in itertools.product(range(WM // 16), range(WN // 16)):
+                m = m0 + wm * WM + i * 16 + (lane & 15)
+                if m < M:
+                    out4(m, n0 + wn * WN + j * 16 + 4 * (lane >> 4))
     return hi
 
 
