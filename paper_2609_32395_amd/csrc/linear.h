@@ -123,54 +123,94 @@ __device__ __forceinline__ f32x4 mfma16(const u32x4& A, const u32x4& B, const f3
 }
 
 // Few rows (one or two blocks): the weights stream from HBM once and the
-// time is load latency.  A workgroup owns 64 rows x 16 output columns; its
-// 4 waves take the reduction chunks round-robin, each chunk's steps of
-// operands (4 row tiles of x, 1 tile of W) loaded 8 steps at a time, and
-// leave the chunk sums in LDS, where they are added in chunk order.
-// Dynamic LDS: ceil(K / lin_chunk(K)) x 4 KiB <= 64 KiB.
-template <int EPI>
-__global__ void __launch_bounds__(256) k_linear_skinny(LinArgs a) {
-  extern __shared__ float part[];   // [n_chunks][64][16]
-  const int n0 = blockIdx.x * 16, m0 = blockIdx.y * 64;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// time is load latency, so the reduction chunks run side by side.  A
+// workgroup owns RT x 16 rows and G x 16 output columns and has one wave per
+// chunk; each wave keeps U steps of operands (RT tiles of x, G tiles of W) in
+// flight and leaves its chunk sums in LDS, where they are added in chunk
+// order.  Launch order puts the row tiles of one column group next to each
+// other on one XCD, so their W tiles are read from HBM once.
+// Dynamic LDS: n_chunks x RT x G x 1 KiB <= 64 KiB.
+template <int RT_, int G_, int U_>
+struct SkinnyCfg {
+  static constexpr int RT = RT_, G = G_, U = U_;
+};
+
+template <int EPI, class C>
+__global__ void __launch_bounds__(1024) k_linear_skinny(LinArgs a, int row_tiles, int col_groups) {
+  constexpr int RT = C::RT, G = C::G, U = C::U, W16 = 16 * G;
+  extern __shared__ float part[];   // [n_chunks][16 RT][16 G]
+  const int T = row_tiles * col_groups;
+  int pid = blockIdx.x;
+  if ((T & 7) == 0) pid = (pid & 7) * (T >> 3) + (pid >> 3);
+  const int m0 = (pid % row_tiles) * 16 * RT, n0 = (pid / row_tiles) * W16;
+  const int lane = threadIdx.x & 63, c = threadIdx.x >> 6;       // wave c computes chunk c
   const int kofs = (lane >> 4) * 8;
   const int KS = a.K / 32, CS = lin_chunk(a.K) / 32, NC = (KS + CS - 1) / CS;
-  const uint16_t* ap[4];
+  const uint16_t* ap[RT];
+  const uint16_t* bp[G];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) ap[i] = a.x + (size_t)min(m0 + i * 16 + (lane & 15), a.M - 1) * a.ldx + kofs;
-  const uint16_t* bp = lin_wrow(a, min(n0 + (lane & 15), a.N - 1)) + kofs;
-  for (int c = wave; c < NC; c += 4) {
-    const int s0 = c * CS, s1 = min(KS, s0 + CS);
-    f32x4 acc[4];
+  for (int i = 0; i < RT; ++i) ap[i] = a.x + (size_t)min(m0 + i * 16 + (lane & 15), a.M - 1) * a.ldx + kofs;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int u0 = s0; u0 < s1; u0 += 8) {
-      u32x4 A[8][4], B[8];
+  for (int j = 0; j < G; ++j) bp[j] = lin_wrow(a, min(n0 + j * 16 + (lane & 15), a.N - 1)) + kofs;
+  const int s0 = c * CS, s1 = min(KS, s0 + CS);
+  f32x4 acc[RT][G];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int st = min(u0 + u, s1 - 1) * 32;
-        B[u] = *(const u32x4*)(bp + st);
+  for (int i = 0; i < RT; ++i)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) A[u][i] = *(const u32x4*)(ap[i] + st);
-      }
+    for (int j = 0; j < G; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int u0 = s0; u0 < s1; u0 += U) {
+    u32x4 A[U][RT], B[U][G];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (u0 + u < s1) {
+    for (int u = 0; u < U; ++u) {
+      const int st = min(u0 + u, s1 - 1) * 32;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) acc[i] = mfma16(B[u], A[u][i], acc[i]);
-        }
+      for (int j = 0; j < G; ++j) B[u][j] = *(const u32x4*)(bp[j] + st);
+#pragma unroll
+      for (int i = 0; i < RT; ++i) A[u][i] = *(const u32x4*)(ap[i] + st);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (u0 + u < s1) {
+#pragma unroll
+        for (int i = 0; i < RT; ++i)
+#pragma unroll
+          for (int j = 0; j < G; ++j) acc[i][j] = mfma16(B[u][j], A[u][i], acc[i][j]);
       }
     }
-    float* pc = part + c * 1024;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) *(f32x4*)(pc + (i * 16 + (lane & 15)) * 16 + 4 * (lane >> 4)) = acc[i];
   }
+  float* pc = part + c * (256 * RT * G);
+#pragma unroll
+  for (int i = 0; i < RT; ++i)
+#pragma unroll
+    for (int j = 0; j < G; ++j)
+      *(f32x4*)(pc + (i * 16 + (lane & 15)) * W16 + j * 16 + 4 * (lane >> 4)) = acc[i][j];
   __syncthreads();
-  const int row = threadIdx.x >> 2, c0 = (threadIdx.x & 3) * 4;
-  f32x4 v = {0.f, 0.f, 0.f, 0.f};
-  for (int c = 0; c < NC; ++c) v += *(const f32x4*)(part + c * 1024 + row * 16 + c0);
-  const int m = m0 + row;
-  if (m < a.M) lin_store4<EPI>(a, m, n0 + c0, v);
+  for (int q = threadIdx.x; q < 64 * RT * G; q += blockDim.x) {
+    const int row = q / (4 * G), c0 = (q % (4 * G)) * 4;
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    for (int ch = 0; ch < NC; ++ch) v += *(const f32x4*)(part + ch * (256 * RT * G) + row * W16 + c0);
+    const int m = m0 + row;
+    if (m < a.M) lin_store4<EPI>(a, m, n0 + c0, v);
+  }
+}
+
+template <int EPI, class C>
+static void launch_skinny_cfg(const LinArgs& a, int nc, hipStream_t s) {
+  const int rt = (a.M + 16 * C::RT - 1) / (16 * C::RT), cg = (a.N + 16 * C::G - 1) / (16 * C::G);
+  hipLaunchKernelGGL((k_linear_skinny<EPI, C>), dim3(rt * cg), dim3(64 * nc), (size_t)nc * 1024 * C::RT * C::G, s,
+                     a, rt, cg);
+}
+
+// The largest tile that still gives at least 256 workgroups (one per CU):
+// wide maps reuse each x and W tile more, narrow ones need the parallelism.
+// All three compute every output in the same order.
+template <int EPI>
+static void launch_skinny(const LinArgs& a, hipStream_t s) {
+  const int nc = (a.K + lin_chunk(a.K) - 1) / lin_chunk(a.K);
+  auto wgs = [&](int rows, int cols) { return (long)((a.M + rows - 1) / rows) * ((a.N + cols - 1) / cols); };
+  if (wgs(32, 32) >= 256) launch_skinny_cfg<EPI, SkinnyCfg<2, 2, 4>>(a, nc, s);
+  else if (wgs(16, 32) >= 256) launch_skinny_cfg<EPI, SkinnyCfg<1, 2, 8>>(a, nc, s);
+  else launch_skinny_cfg<EPI, SkinnyCfg<1, 1, 8>>(a, nc, s);
 }
 
 // Many rows: BM x BN tiles, WAVES_M x WAVES_N waves (each (BM/WAVES_M) x
@@ -312,9 +352,7 @@ static hipError_t linear(const LinArgs& a, hipStream_t s) {
   if (a.K <= 0 || a.K % 64) return hipErrorInvalidValue;
   if (EPI != kLinF32 && (a.ldy % 4 || (EPI == kLinSplit && a.ns % 4))) return hipErrorInvalidValue;
   if (a.M <= 128) {
-    const int nc = (a.K + lin_chunk(a.K) - 1) / lin_chunk(a.K);
-    hipLaunchKernelGGL((k_linear_skinny<EPI>), dim3((a.N + 15) / 16, (a.M + 63) / 64), dim3(256),
-                       (size_t)nc * 64 * 16 * 4, s, a);
+    launch_skinny<EPI>(a, s);
   } else if ((size_t)((a.N + GemmBig::BN - 1) / GemmBig::BN) * ((a.M + GemmBig::BM - 1) / GemmBig::BM) >= 256) {
     launch_gemm<EPI, GemmBig>(a, s);
   } else {
