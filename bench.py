@@ -55,6 +55,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+MFMA_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
 BF16_PEAK_TFLOPS = 2516.6      # MI355X dense bf16 MFMA, published
 
 # HBM bytes per decode call measured with rocprofv3 FETCH_SIZE/WRITE_SIZE
@@ -465,7 +466,7 @@ def model_workload(args, torch, smem, synth):
         cells = {}
         for n in lengths:
             J = n // b
-            tokens = torch.from_numpy(synth.model_tokens(args.seed, name, n)).to("cuda")
+            tokens = torch.from_numpy(synth.model_tokens(args.seed, name, n, vocab)).to("cuda")
             last = tokens[(J - 1) * b:].contiguous()
             cold_t = []
             for rep in range(args.model_reps + 1):
@@ -492,6 +493,14 @@ def model_workload(args, torch, smem, synth):
                 if rep >= 2:
                     skip_t.append(t0.elapsed_time(t1))
             same = bool(torch.equal(skip, cold))
+            # algorithmic work: block-skip reads every reader weight once, the
+            # head, and the memory keys/values of J - 1 blocks in every layer;
+            # the cold pass's flops are the linear maps over all n tokens (the
+            # head on the final block) plus every attention score and value product
+            skip_bytes = 2.0 * (14 * D * d * d + vocab * d) + 4.0 * D * (J - 1) * b * d
+            lin = 2.0 * n * (E * 12 * d * d + D * 16 * d * d) + 2.0 * b * d * vocab
+            pairs = E * J * b * b + D * J * b * (b + 1) / 2 + D * sum(b * (b * j + 1) for j in range(J))
+            cold_flops = lin + 4.0 * pairs * d
             graph_ms = _graph_time(lambda t: smem.smem_model_read(m, 0, [J - 1], last, logits=skip), 4, stream) * 1e3
             for j in range(J):
                 smem.smem_model_delete_block(m, 0, j)
@@ -501,12 +510,43 @@ def model_workload(args, torch, smem, synth):
                                  block_skip_ms=round(float(np.median(skip_t)), 3),
                                  block_skip_graph_ms=round(graph_ms, 3),
                                  ttft_reduction=round(1.0 - float(np.median(skip_t)) / float(np.median(cold_t)), 4),
-                                 skip_equals_cold_bitwise=same)
+                                 skip_equals_cold_bitwise=same,
+                                 block_skip_gbs=round(skip_bytes / float(np.median(skip_t)) / 1e6, 1),
+                                 block_skip_hbm_frac=round(skip_bytes / float(np.median(skip_t)) / 1e6 / HBM_PEAK_GBS, 4),
+                                 cold_tflops=round(cold_flops / float(np.median(cold_t)) / 1e9, 1),
+                                 cold_mfma_frac=round(cold_flops / float(np.median(cold_t)) / 1e9 / MFMA_BF16_TFLOPS, 4))
+        oracle = None
+        if name == "160M" and not args.no_cpu_baseline:
+            oracle = model_oracle_time(args, torch, smem, synth, W, E, D, d, H, b, vocab, T, min(lengths))
         m.close()
         del W
         torch.cuda.empty_cache()
         out[name] = dict(d=d, E=E, D=D, H=H, cells=cells)
+        if oracle:
+            out[name]["cpu_oracle"] = oracle
     return out
+
+
+def model_oracle_time(args, torch, smem, synth, W, E, D, d, H, b, vocab, T, n):
+    """The fp64 model oracle's block-skip read of the final block of an
+    n-token context (the same unit as the GPU's block_skip_ms), on this host;
+    the cached blocks are encoded first, untimed."""
+    from oracle import smem_model as MO
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    J = n // b
+    Wh = {k: v.float().cpu().numpy().astype(np.float64) for k, v in W.items()}
+    ref = MO.Model(Wh, E, D, d, H, b, vocab, T, 1, J)
+    tokens = synth.model_tokens(args.seed, "160M", n, vocab).reshape(J, b)
+    ref.encode(0, tokens[:J - 1], list(range(J - 1)))
+    t0 = time.perf_counter()
+    ref.read(0, tokens[J - 1:], [J - 1])
+    dt = time.perf_counter() - t0
+    return {"block_skip_ms": round(dt * 1e3, 1), "cores": int(threads), "kind": "oracle",
+            "sample": f"160M, {n}-token context: one block-skip read (fp64 numpy)"}
 
 
 def cpu_baseline(dec, budget_s, seed):
