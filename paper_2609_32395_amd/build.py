@@ -32,6 +32,10 @@ COMMON_FLAGS = [
     "-Wno-unused-result",
     # packed fp32 instructions are kept out of every kernel
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in ordinary VGPRs: the softmax and epilogue code that
+    # reads them then needs no accumulator-register moves (measured: equal or
+    # faster for every kernel here)
+    "-mllvm", "-amdgpu-mfma-vgpr-form=true",
     f"-I{os.path.join(ROOT, 'include')}",
     f"-I{CSRC}",
 ]

@@ -270,15 +270,29 @@ __device__ __forceinline__ void pv(floatx4 (&o)[DH / 16], const Tiles<DH>& T, co
   }
 }
 
-// Max / sum over the four lanes that hold one query column.
-__device__ __forceinline__ float qmax(float x) {
-  x = fmaxf(x, __shfl_xor(x, 16));
-  return fmaxf(x, __shfl_xor(x, 32));
+// Max / sum over the four lanes that hold one query column (lanes l, l^16,
+// l^32, l^48).  permlane16/32_swap of a value with itself leaves, in the
+// pair it returns, the lane's own value and its partner's (l^16, l^32), so
+// op(pair) is the two-lane reduction -- a VALU exchange instead of an LDS
+// permute; both operations are commutative, so every lane gets the same bits.
+__device__ __forceinline__ float xor16_op_max(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
-__device__ __forceinline__ float qsum(float x) {
-  x += __shfl_xor(x, 16);
-  return x + __shfl_xor(x, 32);
+__device__ __forceinline__ float xor32_op_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
+__device__ __forceinline__ float xor16_op_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float xor32_op_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float qmax(float x) { return xor32_op_max(xor16_op_max(x)); }
+__device__ __forceinline__ float qsum(float x) { return xor32_op_sum(xor16_op_sum(x)); }
 
 // One online-softmax step over a 64-key tile for the lane's query.
 // valid(kt, i) says whether key kt*16 + 4*(lane/16) + i is visible.
@@ -301,13 +315,16 @@ __device__ __forceinline__ void online_step(floatx4 (&s)[4], float& m, float& l,
   }
   mx = qmax(mx);
   const float mn = fmaxf(m, mx);
-  const float alpha = (m == -INFINITY) ? 0.f : exp2w(m - mn);
+  // Without the causal mask every score is finite, so mn is finite and
+  // 2^(m - mn) = 2^-inf = 0 on the first tile: the guards are only needed
+  // when masked (-inf) scores can make mn = -inf.
+  const float alpha = (CAUSAL && m == -INFINITY) ? 0.f : exp2w(m - mn);
   float ps = 0.f;
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float p = (s[kt][i] == -INFINITY) ? 0.f : exp2w(s[kt][i] - mn);
+      const float p = (CAUSAL && s[kt][i] == -INFINITY) ? 0.f : exp2w(s[kt][i] - mn);
       s[kt][i] = p;
       ps += p;
     }
@@ -427,9 +444,42 @@ hipError_t launch_encoder_mfma(int b, int dh, const void* q, const void* k, cons
 // never waits on a global load issued behind the in-flight pages.
 constexpr int kRopeRows = 24;
 
+// Memory pages of the non-rotary prefill move global -> LDS by DMA
+// (global_load_lds_dwordx4, 16 bytes per lane) through a ring of NS page
+// stages, so NS - 1 pages are in flight while one is read and no register
+// holds a page in transit.  A (page, head) tile is the key plane [b][d_h]
+// followed by the transposed value plane [d_h][b]; in LDS both keep that
+// layout with 16-byte slots permuted per row (key row r: slot = chunk ^
+// kswz(r); value row d: slot = chunk ^ vswz(d)), so the 16 rows one MFMA
+// operand read touches cover every bank once.
+#ifndef SMEM_PREFILL_STAGES32
+#define SMEM_PREFILL_STAGES32 4
+#endif
+#ifndef SMEM_PREFILL_STAGES64
+#define SMEM_PREFILL_STAGES64 4
+#endif
+#ifndef SMEM_PREFILL_STAGES128
+#define SMEM_PREFILL_STAGES128 2
+#endif
+template <int DH>
+struct PageRing {
+  static constexpr int TILE = 2 * BT * DH * 2;         // bytes per (page, head)
+  static constexpr int KBYTES = BT * DH * 2;           // key plane bytes
+  static constexpr int KRB = DH * 2;                   // key row bytes
+  static constexpr int KCH = DH / 8;                   // 16-byte chunks per key row
+  static constexpr int NS = DH == 32 ? SMEM_PREFILL_STAGES32 : DH == 64 ? SMEM_PREFILL_STAGES64 : SMEM_PREFILL_STAGES128;
+  static constexpr int IPW = TILE / 1024 / 4;          // DMA instructions per wave per page
+  static_assert(NS >= 2 && NS <= 5, "wait_pages covers up to 3 pages ahead");
+  __device__ static constexpr int kswz(int r) { return (r / (256 / KRB)) % KCH; }
+  __device__ static constexpr int vswz(int d) { return (d >> 1) & 7; }
+};
+
 template <int DH, bool ROPE>
 struct PrefillLds {
-  Tiles<DH> T;
+  union {
+    Tiles<DH> T;                                       // final split: null row and in-block keys
+    __attribute__((aligned(1024))) uint8_t ring[PageRing<DH>::NS * PageRing<DH>::TILE];
+  };
 };
 template <int DH>
 struct PrefillLds<DH, true> {
@@ -437,6 +487,56 @@ struct PrefillLds<DH, true> {
   float rows[kRopeRows * DH];          // turns d_lo .. d_lo + kRopeRows - 1
   u32x4 qb[(DH / 32) * 4 * 64];        // unturned query fragments, [kk][wave][lane]
 };
+
+// S^T for this wave's 16 queries against a page's 64 keys in a ring stage.
+template <int DH>
+__device__ __forceinline__ void scores_ring(floatx4 (&s)[4], const uint8_t* tile, const bf16x8 (&qf)[DH / 32],
+                                            int lane) {
+  using R = PageRing<DH>;
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt) {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    const int r = kt * 16 + (lane & 15);
+#pragma unroll
+    for (int kk = 0; kk < DH / 32; ++kk) {
+      const int c = kk * 4 + (lane >> 4);
+      const u32x4 kf = *(const u32x4*)(tile + r * R::KRB + ((c ^ R::kswz(r)) << 4));
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kf), qf[kk], acc, 0, 0, 0);
+    }
+    s[kt] = acc;
+  }
+}
+
+// O^T += V^T P^T over a page's 64 keys in a ring stage: lane reads keys
+// 4 (l/16) + 16 q .. +3 of value row dt*16 + l%16, q = 0..3.
+template <int DH>
+__device__ __forceinline__ void pv_ring(floatx4 (&o)[DH / 16], const uint8_t* tile, const floatx4 (&p)[4],
+                                        int lane) {
+  using R = PageRing<DH>;
+  const bf16x8 p0 = pack_p(p[0], p[1]);
+  const bf16x8 p1 = pack_p(p[2], p[3]);
+  const int g = lane >> 4;
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) {
+    const int d = dt * 16 + (lane & 15);
+    const uint8_t* row = tile + R::KBYTES + d * 128 + (g & 1) * 8;
+    u32x2 x[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) x[q] = *(const u32x2*)(row + ((((g >> 1) + 2 * q) ^ R::vswz(d)) << 4));
+    const u32x4 a0 = u32x4{x[0].x, x[0].y, x[1].x, x[1].y};
+    const u32x4 a1 = u32x4{x[2].x, x[2].y, x[3].x, x[3].y};
+    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a0), p0, o[dt], 0, 0, 0);
+    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a1), p1, o[dt], 0, 0, 0);
+  }
+}
+
+template <int N>
+__device__ __forceinline__ void wait_pages(int ahead) {
+  if (ahead >= 3) wait_vm<3 * N < 63 ? 3 * N : 63>();
+  else if (ahead == 2) wait_vm<2 * N>();
+  else if (ahead == 1) wait_vm<N>();
+  else wait_vm<0>();
+}
 
 template <int DH, bool ROPE>
 __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH, ROPE>& L) {
@@ -459,65 +559,109 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
   float m = -INFINITY, l = 0.f;
 
   if (split < nms) {
-    // Pages stream through a ring of kDepth register stages: page pi is moved
-    // to LDS while pages pi+1 .. pi+kDepth-1 are still in flight.
-    constexpr int kDepth = 3;
-    const int p0 = split * pps, p1 = min(n_read, p0 + pps);
-    const int32_t* lp = a.live_page + (size_t)a.seq[slot] * a.max_blocks;
-    [[maybe_unused]] const int32_t* lb = a.live_blk + (size_t)a.seq[slot] * a.max_blocks;
-    [[maybe_unused]] int turned = -1, d_lo = 0;
-    [[maybe_unused]] bool rows_lds = false;
-    if constexpr (ROPE) {
-      // before the first page load: these waits drain nothing
-      const int J = a.qblk[slot];
-      const int d_hi = min(J - lb[p0], a.rope_clip);
-      d_lo = min(J - lb[p1 - 1], a.rope_clip);
-      rows_lds = d_hi - d_lo < kRopeRows;
-      if (rows_lds) {
-        const int n4 = (d_hi - d_lo + 1) * DH / 4;
-        const f32x4* src = (const f32x4*)(a.rope + (size_t)d_lo * DH);
-        for (int i = tid; i < n4; i += 256) ((f32x4*)L.rows)[i] = src[i];
+    if constexpr (!ROPE) {
+      using R = PageRing<DH>;
+      const int p0 = split * pps, p1 = min(n_read, p0 + pps);
+      const __attribute__((address_space(4))) int32_t* lpc =
+          (const __attribute__((address_space(4))) int32_t*)(a.live_page + (size_t)a.seq[slot] * a.max_blocks);
+      // this lane's 16 bytes of each DMA instruction: LDS byte (wave*IPW + i)*1024 + 16*lane of
+      // the stage, read from the tile byte that the slot permutation puts there
+      uint32_t src[R::IPW];
+  #pragma unroll
+      for (int i = 0; i < R::IPW; ++i) {
+        const int byte = (wave * R::IPW + i) * 1024 + lane * 16;
+        if (byte < R::KBYTES) {
+          const int r = byte / R::KRB, sl = (byte % R::KRB) >> 4;
+          src[i] = r * R::KRB + ((sl ^ R::kswz(r)) << 4);
+        } else {
+          const int vb = byte - R::KBYTES, d = vb >> 7, sl = (vb & 127) >> 4;
+          src[i] = R::KBYTES + d * 128 + ((sl ^ R::vswz(d)) << 4);
+        }
       }
-#pragma unroll
-      for (int kk = 0; kk < DH / 32; ++kk) L.qb[(kk * 4 + wave) * 64 + lane] = __builtin_bit_cast(u32x4, qf[kk]);
-      // L.rows is read after the barrier that precedes the first page_store;
-      // each lane reads back only its own L.qb entries
-    }
-    const uint16_t* pages = (const uint16_t*)a.pages;
-    PageRegs<DH> r[kDepth];
-#pragma unroll
-    for (int u = 0; u < kDepth; ++u) {
-      if (p0 + u < p1) {
-        const uint16_t* Kt = pages + page_head_offset(lp[p0 + u], h, a.H, BT, DH);
-        page_load<DH>(r[u], Kt, Kt + BT * DH, tid);
+      const uint8_t* gpages = (const uint8_t*)a.pages;
+      const uint32_t lds0 = (uint32_t)(uintptr_t)L.ring;
+      auto issue = [&](int pi, int stage) {
+        const uint8_t* t = gpages + page_head_offset(lpc[pi], h, a.H, BT, DH) * 2;
+        const uint32_t d0 = lds0 + (uint32_t)(stage * R::TILE + wave * R::IPW * 1024);
+  #pragma unroll
+        for (int i = 0; i < R::IPW; ++i) dma16(t + src[i], __builtin_amdgcn_readfirstlane(d0 + i * 1024));
+      };
+      wait_vm<0>();                        // the query fragments, before any DMA is in flight
+  #pragma unroll
+      for (int k = 0; k < R::NS - 1; ++k)
+        if (p0 + k < p1) issue(p0 + k, k);
+      for (int pi = p0; pi < p1; ++pi) {
+        const int k = pi - p0;
+        wait_pages<R::IPW>(min(R::NS - 2, p1 - 1 - pi));
+        lds_barrier();                     // page pi is in LDS; every wave is done with page pi - 1
+        if (pi + R::NS - 1 < p1) issue(pi + R::NS - 1, (k + R::NS - 1) % R::NS);
+        const uint8_t* tile = L.ring + (k % R::NS) * R::TILE;
+        floatx4 s[4];
+        scores_ring<DH>(s, tile, qf, lane);
+        online_step<DH, false>(s, m, l, o, lane, qrow, a.scale_log2);
+        pv_ring<DH>(o, tile, s, lane);
       }
-    }
-    for (int base = p0; base < p1; base += kDepth) {
-#pragma unroll
+    } else {
+      // Rotary path: pages stream through a ring of kDepth register stages:
+      // page pi is moved to LDS while pages pi+1 .. pi+kDepth-1 are in flight.
+      constexpr int kDepth = 3;
+      const int p0 = split * pps, p1 = min(n_read, p0 + pps);
+      const int32_t* lp = a.live_page + (size_t)a.seq[slot] * a.max_blocks;
+      [[maybe_unused]] const int32_t* lb = a.live_blk + (size_t)a.seq[slot] * a.max_blocks;
+      [[maybe_unused]] int turned = -1, d_lo = 0;
+      [[maybe_unused]] bool rows_lds = false;
+      if constexpr (ROPE) {
+        // before the first page load: these waits drain nothing
+        const int J = a.qblk[slot];
+        const int d_hi = min(J - lb[p0], a.rope_clip);
+        d_lo = min(J - lb[p1 - 1], a.rope_clip);
+        rows_lds = d_hi - d_lo < kRopeRows;
+        if (rows_lds) {
+          const int n4 = (d_hi - d_lo + 1) * DH / 4;
+          const f32x4* src = (const f32x4*)(a.rope + (size_t)d_lo * DH);
+          for (int i = tid; i < n4; i += 256) ((f32x4*)L.rows)[i] = src[i];
+        }
+  #pragma unroll
+        for (int kk = 0; kk < DH / 32; ++kk) L.qb[(kk * 4 + wave) * 64 + lane] = __builtin_bit_cast(u32x4, qf[kk]);
+        // L.rows is read after the barrier that precedes the first page_store;
+        // each lane reads back only its own L.qb entries
+      }
+      const uint16_t* pages = (const uint16_t*)a.pages;
+      PageRegs<DH> r[kDepth];
+  #pragma unroll
       for (int u = 0; u < kDepth; ++u) {
-        const int pi = base + u;
-        if (pi < p1) {
-          __syncthreads();
-          page_store<DH>(r[u], T, tid);
-          __syncthreads();
-          if constexpr (ROPE) {
-            // between the store of stage u and its refill, so the turn's
-            // temporaries take the stage's registers
-            const int dlt = min(a.qblk[slot] - lb[pi], a.rope_clip);
-            if (dlt != turned) {
-              if (rows_lds) rope_q_from_lds<DH>(qf, L.qb, L.rows + (dlt - d_lo) * DH, wave, lane);
-              else rope_q_from_lds<DH>(qf, L.qb, a.rope + (size_t)dlt * DH, wave, lane);
-              turned = dlt;
+        if (p0 + u < p1) {
+          const uint16_t* Kt = pages + page_head_offset(lp[p0 + u], h, a.H, BT, DH);
+          page_load<DH>(r[u], Kt, Kt + BT * DH, tid);
+        }
+      }
+      for (int base = p0; base < p1; base += kDepth) {
+  #pragma unroll
+        for (int u = 0; u < kDepth; ++u) {
+          const int pi = base + u;
+          if (pi < p1) {
+            __syncthreads();
+            page_store<DH>(r[u], T, tid);
+            __syncthreads();
+            if constexpr (ROPE) {
+              // between the store of stage u and its refill, so the turn's
+              // temporaries take the stage's registers
+              const int dlt = min(a.qblk[slot] - lb[pi], a.rope_clip);
+              if (dlt != turned) {
+                if (rows_lds) rope_q_from_lds<DH>(qf, L.qb, L.rows + (dlt - d_lo) * DH, wave, lane);
+                else rope_q_from_lds<DH>(qf, L.qb, a.rope + (size_t)dlt * DH, wave, lane);
+                turned = dlt;
+              }
             }
+            if (pi + kDepth < p1) {
+              const uint16_t* Kt = pages + page_head_offset(lp[pi + kDepth], h, a.H, BT, DH);
+              page_load<DH>(r[u], Kt, Kt + BT * DH, tid);
+            }
+            floatx4 s[4];
+            scores<DH>(s, T, qf, lane);
+            online_step<DH, false>(s, m, l, o, lane, qrow, a.scale_log2);
+            pv<DH>(o, T, s, lane);
           }
-          if (pi + kDepth < p1) {
-            const uint16_t* Kt = pages + page_head_offset(lp[pi + kDepth], h, a.H, BT, DH);
-            page_load<DH>(r[u], Kt, Kt + BT * DH, tid);
-          }
-          floatx4 s[4];
-          scores<DH>(s, T, qf, lane);
-          online_step<DH, false>(s, m, l, o, lane, qrow, a.scale_log2);
-          pv<DH>(o, T, s, lane);
         }
       }
     }

@@ -35,8 +35,11 @@ constexpr int kSplitCapPrefill = 32;
 // since every split writes a b x (d_h + 4) partial that the merge reads back.
 // A function of the store's H alone, so a block's result never depends on the
 // batch it is read in.
+#ifndef SMEM_PREFILL_WG_TARGET
+#define SMEM_PREFILL_WG_TARGET 512
+#endif
 inline int prefill_split_cap(int H) {
-  const int c = 512 / (H > 0 ? H : 1);
+  const int c = SMEM_PREFILL_WG_TARGET / (H > 0 ? H : 1);
   return c < 1 ? 1 : (c > kSplitCapPrefill ? kSplitCapPrefill : c);
 }
 // Query slots whose prefill partials the workspace must hold at once.

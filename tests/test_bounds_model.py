@@ -372,3 +372,46 @@ def test_gelu_erf_formula_in_source():
         y = np.copysign(1 - poly * np.exp2(-ax * ax * dt(1.4426950408889634)), xs)
         ref = np.array([math.erf(float(v)) for v in xs[::50]])
         assert np.max(np.abs(y[::50] - ref)) <= bound, dt
+
+
+@pytest.mark.parametrize("dh,ns", [(32, 4), (64, 4), (128, 2)])
+def test_prefill_page_ring_indexing(dh, ns):
+    """Non-rotary prefill's DMA page ring: every lane's source byte lies in
+    its (page, head) tile, every LDS byte of a stage is written exactly once,
+    and each operand read finds the chunk the DMA put there (key rows and
+    transposed value rows, 16-byte slots permuted per row)."""
+    BT = 64
+    TILE, KBYTES, KRB, KCH = 2 * BT * dh * 2, BT * dh * 2, dh * 2, dh // 8
+    IPW = TILE // 1024 // 4
+    kswz = lambda r: (r // (256 // KRB)) % KCH
+    vswz = lambda d: (d >> 1) & 7
+    placed = {}                                   # LDS byte offset in the stage -> source byte offset
+    for wave, i, lane in itertools.product(range(4), range(IPW), range(64)):
+        byte = (wave * IPW + i) * 1024 + lane * 16
+        if byte < KBYTES:
+            r, sl = byte // KRB, (byte % KRB) >> 4
+            src = r * KRB + ((sl ^ kswz(r)) << 4)
+        else:
+            vb = byte - KBYTES
+            d, sl = vb >> 7, (vb & 127) >> 4
+            src = KBYTES + d * 128 + ((sl ^ vswz(d)) << 4)
+        assert 0 <= src and src + 16 <= TILE
+        assert byte not in placed
+        placed[byte] = src
+    assert sorted(placed) == list(range(0, TILE, 16)) and sorted(placed.values()) == list(range(0, TILE, 16))
+    assert ns * TILE <= 64 * 1024 and 3 * IPW < 64
+    for lane in range(64):                        # key operand: row r, chunk c
+        for kt, kk in itertools.product(range(4), range(dh // 32)):
+            r, c = kt * 16 + (lane & 15), kk * 4 + (lane >> 4)
+            assert placed[r * KRB + ((c ^ kswz(r)) << 4)] == r * KRB + c * 16
+        g = lane >> 4                             # value operand: row d, keys 4g + 16q .. +3
+        for dt, q in itertools.product(range(dh // 16), range(4)):
+            d = dt * 16 + (lane & 15)
+            lds = KBYTES + d * 128 + ((((g >> 1) + 2 * q) ^ vswz(d)) << 4)
+            key0 = 4 * g + 16 * q
+            assert placed[lds] + (g & 1) * 8 == KBYTES + d * 128 + key0 * 2
+    # banks: the 16 rows one key read touches fall on distinct 16-byte bank groups
+    for c in range(KCH):
+        for kt in range(4):
+            groups = {((r * KRB + ((c ^ kswz(r)) << 4)) % 256) // 16 for r in range(kt * 16, kt * 16 + 16)}
+            assert len(groups) == 16
