@@ -36,8 +36,12 @@ Timing uses HIP events on the stream the kernels are launched on (torch's
 current stream, handed to the library).  The 160M encoder and prefill calls
 are shorter than the host's cost of issuing them, so they are captured in a
 HIP graph (repetitions of the call, no memory sets) and the replays are
-timed.  The CPU baseline is the fp64 numpy
-oracle timed on a bounded sample of the headline workload on this host.
+timed.  The 160M encoder/prefill and the 1.5B serve also report one call
+issued on an idle GPU after a 512 MiB read pass (`*_single_flushed`): the
+latency of a call whose data are out of the caches, against the
+back-to-back throughput above.  The CPU baseline is the fp64 numpy
+oracle timed on a bounded sample of the headline workload on this host
+(all threads, and one thread for reference).
 Prints ONE JSON line.
 """
 from __future__ import annotations
@@ -86,6 +90,27 @@ def _events_time(fn, steps, stream):
     end.record(stream)
     torch.cuda.synchronize()
     return start.elapsed_time(end) / 1e3  # seconds
+
+
+def _flushed_time(fn, reps, stream, scratch):
+    """Median seconds of single calls of fn, each issued on an idle GPU after
+    a read pass over `scratch` (512 MiB, twice the 256 MiB last-level cache),
+    so every call starts with its working set out of the caches.  The flush
+    only reads: dirty lines left by a writing flush would be written back
+    during the timed call and slow it for reasons of its own."""
+    import torch
+    ts = []
+    for r in range(reps):
+        scratch.sum()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn(r)
+        e1.record(stream)
+        e1.synchronize()
+        ts.append(e0.elapsed_time(e1) / 1e3)
+    return float(np.median(ts))
 
 
 def _graph_time(fn, reps, stream, replays=8):
@@ -217,6 +242,9 @@ def encode_prefill_workload(args, torch, smem, synth):
         smem.smem_encode_blocks(None, Qd, Kd, Vd, out=out, mask=smem.MASK_BIDIR, b=b)
     enc_s = _graph_time(lambda t: smem.smem_encode_blocks(None, Qd, Kd, Vd, out=out, mask=smem.MASK_BIDIR, b=b),
                         reps, stream)
+    scratch = torch.zeros(512 << 20 >> 1, dtype=torch.bfloat16, device="cuda")
+    enc_flushed_s = _flushed_time(lambda t: smem.smem_encode_blocks(None, Qd, Kd, Vd, out=out, mask=smem.MASK_BIDIR,
+                                                                    b=b), 9, stream, scratch)
     # encode + insert into a store, then prefill the final block of each sequence
     st = smem.Store(S, NB, S * NB, b, H, dh, dt)
     smem.smem_encode_blocks(st, Qd, Kd, Vd, out=out, seq_ids=seq_ids, block_idx=blk, mask=smem.MASK_BIDIR)
@@ -230,6 +258,9 @@ def encode_prefill_workload(args, torch, smem, synth):
         smem.smem_reader_prefill_block(st, list(range(S)), qb, qp, kp, vp, None, pout)
     pre_s = _graph_time(lambda t: smem.smem_reader_prefill_block(st, list(range(S)), qb, qp, kp, vp, None, pout),
                         reps, stream)
+    pre_flushed_s = _flushed_time(lambda t: smem.smem_reader_prefill_block(st, list(range(S)), qb, qp, kp, vp, None,
+                                                                           pout), 9, stream, scratch)
+    del scratch
     enc_flops = 4.0 * nb * H * b * b * dh
     enc_bytes = 4.0 * nb * b * H * dh * 2
     n_mem = (NB - 1) * b
@@ -238,7 +269,9 @@ def encode_prefill_workload(args, torch, smem, synth):
     st.close()
     return dict(encoder_ms=enc_s * 1e3, encoder_tflops=enc_flops / enc_s / 1e12, encoder_gbs=enc_bytes / enc_s / 1e9,
                 encoder_flops=enc_flops, encoder_bytes=enc_bytes,
-                prefill_ms=pre_s * 1e3, prefill_tflops=pre_flops / pre_s / 1e12, prefill_gbs=pre_bytes / pre_s / 1e9)
+                encoder_ms_single_flushed=enc_flushed_s * 1e3, encoder_gbs_single_flushed=enc_bytes / enc_flushed_s / 1e9,
+                prefill_ms=pre_s * 1e3, prefill_tflops=pre_flops / pre_s / 1e12, prefill_gbs=pre_bytes / pre_s / 1e9,
+                prefill_ms_single_flushed=pre_flushed_s * 1e3, prefill_gbs_single_flushed=pre_bytes / pre_flushed_s / 1e9)
 
 
 def serve_workload(args, torch, smem, synth):
@@ -267,6 +300,9 @@ def serve_workload(args, torch, smem, synth):
         serve()
     reps = max(5, args.steps // 8)
     serve_s = _events_time(serve, reps, stream) / reps
+    scratch = torch.zeros(512 << 20 >> 1, dtype=torch.bfloat16, device="cuda")
+    serve_flushed_s = _flushed_time(serve, 9, stream, scratch)
+    del scratch
     rope_ms = None
     if "rope" in args.workloads.split(","):
         rope = smem.Rope(dh, b, 10000.0, 15)
@@ -298,6 +334,7 @@ def serve_workload(args, torch, smem, synth):
     bytes_ = H * (rows * dh * 2 * 2 + 4 * b * dh * 2)
     st.close()
     return dict(serve_ms=serve_s * 1e3, serve_tflops=flops / serve_s / 1e12, serve_gbs=bytes_ / serve_s / 1e9,
+                serve_ms_single_flushed=serve_flushed_s * 1e3, serve_gbs_single_flushed=bytes_ / serve_flushed_s / 1e9,
                 rope_serve_ms=rope_ms,
                 delete_us_median=float(np.median(del_t)) * 1e3, reserve_ms_median=float(np.median(re_t)),
                 rows_after_deletes=(NB - 100) * b)
@@ -581,9 +618,34 @@ def cpu_baseline(dec, budget_s, seed):
             spent += time.perf_counter() - t1
             n_tok += 1
         s += 1
+    single = None
+    try:
+        from threadpoolctl import threadpool_limits
+        ref = O.Store(S, NB + 1, b, H, dh)
+        K, V = synth.memory_blocks(w, seed, [0], range(NB), threads=8)
+        for j in range(NB):
+            ref.put(0, j, K[0, j], V[0, j])
+        with threadpool_limits(limits=1):
+            n1, t1s = 0, 0.0
+            while t1s < budget_s / 4 and n1 < len(dec["qs"]):
+                p = dec["pos"][n1][0]
+                t1 = time.perf_counter()
+                O.reader_decode(ref, [0], [NB], [p], dec["qs"][n1, 0:1], dec["kn"][n1, 0:1], dec["vn"][n1, 0:1],
+                                kc_all[0:1], vc_all[0:1])
+                t1s += time.perf_counter() - t1
+                n1 += 1
+        single = round(n1 / t1s, 3)
+    except Exception:
+        pass
+    cpu_model = ""
+    try:
+        cpu_model = next(l.split(":", 1)[1].strip() for l in open("/proc/cpuinfo") if l.startswith("model name"))
+    except Exception:
+        pass
     return {"value": round(n_tok / spent, 3), "unit": "tokens/s", "cores": int(blas_threads), "kind": "oracle",
             "sample": f"{n_tok} decode tokens (16 heads each over 4096 memory rows + in-block keys), "
-                      f"fp64 numpy, {spent:.1f} s"}
+                      f"fp64 numpy, {spent:.1f} s",
+            "single_thread_value": single, "affinity_cpus": len(os.sched_getaffinity(0)), "cpu_model": cpu_model}
 
 
 def main():
