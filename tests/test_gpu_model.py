@@ -204,3 +204,36 @@ def test_160m_full_size_block_skip_matches_oracle():
     err = float(np.max(np.abs(y - expect)) / np.sqrt(np.mean(expect ** 2)))
     say("160M rel err", err, "argmax agreement", float(np.mean(y.argmax(-1) == expect.argmax(-1))))
     assert err <= tol(E, D, y.size), err
+
+
+def test_model_edge_cases():
+    """Empty calls are no-ops; a read at query block = max_blocks reads every
+    cached block; token ids outside the vocabulary read embedding row 0 (the
+    oracle is given token 0 there); argument errors change nothing."""
+    say("model: edge cases")
+    m, ref, _ = build(max_blocks=6, n_pages=6)
+    g = np.random.default_rng(16)
+    tokens = g.integers(0, SHAPE["vocab"], size=(6, SHAPE["b"]))
+    empty = torch.empty(0, dtype=torch.int32, device="cuda")
+    smem.smem_model_encode(m, 0, [], empty)
+    assert smem.smem_model_read(m, 0, [], empty).shape == (0, SHAPE["vocab"])
+    smem.smem_model_encode(m, 0, list(range(6)), tok(tokens))
+    ref.encode(0, tokens, list(range(6)))
+    q = tokens[:1].copy()
+    q[0, 3], q[0, 9] = -5, SHAPE["vocab"] + 7              # out of range -> row 0
+    y = host(smem.smem_model_read(m, 0, [6], tok(q)))      # query block = max_blocks: all 6 blocks below
+    q_ref = q.copy()
+    q_ref[0, 3] = q_ref[0, 9] = 0
+    expect = ref.read(0, q_ref, [6])[0]
+    assert float(np.max(np.abs(y - expect)) / np.sqrt(np.mean(expect ** 2))) <= tol(SHAPE["E"], SHAPE["D"], y.size)
+    with pytest.raises(smem.SmemError) as e:
+        smem.smem_model_read(m, 0, [7], tok(q))            # beyond max_blocks
+    assert e.value.code == smem.SMEM_EINVAL
+    with pytest.raises(smem.SmemError) as e:
+        smem.smem_model_encode(m, 1, [0], tok(q))          # no sequence 1
+    assert e.value.code == smem.SMEM_EINVAL
+    with pytest.raises(smem.SmemError) as e:
+        smem.smem_model_prefill(m, 0, 4, 3, tok(tokens[:3]))   # blocks 4..6: past max_blocks
+    assert e.value.code == smem.SMEM_EINVAL
+    # the store is unchanged by the failed calls
+    assert torch.equal(smem.smem_model_read(m, 0, [6], tok(q)), torch.from_numpy(y).to("cuda"))
