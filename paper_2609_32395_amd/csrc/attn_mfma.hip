@@ -299,12 +299,16 @@ __device__ __forceinline__ float qsum(float x) { return xor32_op_sum(xor16_op_su
 template <int DH, bool CAUSAL>
 __device__ __forceinline__ void online_step(floatx4 (&s)[4], float& m, float& l, floatx4 (&o)[DH / 16], int lane,
                                             int qrow, float scale_log2) {
+  // The maximum is taken over the raw scores and scaled once (the scale is
+  // positive and rounding is monotone, so this is the maximum of the scaled
+  // scores); each weight is then 2^(s*scale - max) with the scale and the
+  // shift in one fused multiply-add.
   float mx = -INFINITY;
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float x = s[kt][i] * scale_log2;
+      float x = s[kt][i];
       if (CAUSAL) {
         const int key = kt * 16 + (lane >> 4) * 4 + i;
         if (key > qrow) x = -INFINITY;
@@ -313,7 +317,7 @@ __device__ __forceinline__ void online_step(floatx4 (&s)[4], float& m, float& l,
       mx = fmaxf(mx, x);
     }
   }
-  mx = qmax(mx);
+  mx = qmax(mx) * scale_log2;
   const float mn = fmaxf(m, mx);
   // Without the causal mask every score is finite, so mn is finite and
   // 2^(m - mn) = 2^-inf = 0 on the first tile: the guards are only needed
@@ -324,7 +328,7 @@ __device__ __forceinline__ void online_step(floatx4 (&s)[4], float& m, float& l,
   for (int kt = 0; kt < 4; ++kt) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float p = (CAUSAL && s[kt][i] == -INFINITY) ? 0.f : exp2w(s[kt][i] - mn);
+      const float p = (CAUSAL && s[kt][i] == -INFINITY) ? 0.f : exp2w(__builtin_fmaf(s[kt][i], scale_log2, -mn));
       s[kt][i] = p;
       ps += p;
     }
