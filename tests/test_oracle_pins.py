@@ -10,6 +10,7 @@
   the leak test (Appendix E) and decode/prefill agreement (Appendix K);
 * special cases with closed forms.
 """
+import itertools
 import json
 import math
 import os
@@ -717,3 +718,48 @@ def test_rows_decode_matches_sdpa_on_mapped_rows():
     for h in range(H):
         ref = F.scaled_dot_product_attention(T(q[0, h])[None, None], K[:, h][None], V[:, h][None])
         np.testing.assert_allclose(out[0, h], ref[0, 0].numpy(), atol=1e-12, rtol=0)
+
+
+def _brute_attention(qv, keys, vals):
+    """One query over an explicit key list, in pure Python: scores by loops,
+    the maximum subtracted, exponentials, and every sum by math.fsum."""
+    dh = len(qv)
+    sc = [math.fsum(qv[i] * k[i] for i in range(dh)) / math.sqrt(dh) for k in keys]
+    if not sc:
+        return [0.0] * len(qv)
+    mx = max(sc)
+    w = [math.exp(x - mx) for x in sc]
+    z = math.fsum(w)
+    return [math.fsum(w[j] * vals[j][i] for j in range(len(keys))) / z for i in range(len(vals[0]))]
+
+
+@pytest.mark.parametrize("b,dh,mask", [(1, 2, O.MASK_BIDIR), (3, 2, O.MASK_CAUSAL), (4, 3, O.MASK_BIDIR),
+                                       (4, 4, O.MASK_CAUSAL)])
+def test_brute_force_tiny(b, dh, mask):
+    """Tiny shapes (H = 1) against a pure-Python brute force of the
+    definitions: the encoder (Section 2, "Model") block by block, and the
+    reader (Section 3.1) over [null] ++ memory of live blocks below J ++
+    in-block keys 0..t, with a deleted block and a block at J present."""
+    g = np.random.default_rng(1000 + b * 10 + dh)
+    nb = 3
+    q, k, v = (g.standard_normal((nb, b, 1, dh)) for _ in range(3))
+    enc = O.encode_blocks(q, k, v, mask)
+    for blk, t in itertools.product(range(nb), range(b)):
+        vis = range(b) if mask == O.MASK_BIDIR else range(t + 1)
+        ref = _brute_attention(list(q[blk, t, 0]), [list(k[blk, j, 0]) for j in vis], [list(v[blk, j, 0]) for j in vis])
+        assert np.allclose(enc[blk, t, 0], ref, rtol=0, atol=1e-13)
+    st = O.Store(1, 6, b, 1, dh)
+    mem = {j: (g.standard_normal((b, 1, dh)), g.standard_normal((b, 1, dh))) for j in (0, 1, 2, 4)}
+    for j, (K, V) in mem.items():
+        st.put(0, j, K, V)
+    st.delete(0, 1)
+    J = 4                                          # reads blocks 0 and 2; block 4 is present and ignored
+    qr, ki, vi = (g.standard_normal((1, b, 1, dh)) for _ in range(3))
+    nkv = g.standard_normal((2, 1, dh))
+    out = O.reader_prefill_block(st, [0], [J], qr, ki, vi, nkv)
+    for t in range(b):
+        keys = [list(nkv[0, 0])] + [list(mem[j][0][r, 0]) for j in (0, 2) for r in range(b)] + \
+               [list(ki[0, r, 0]) for r in range(t + 1)]
+        vals = [list(nkv[1, 0])] + [list(mem[j][1][r, 0]) for j in (0, 2) for r in range(b)] + \
+               [list(vi[0, r, 0]) for r in range(t + 1)]
+        assert np.allclose(out[0, t, 0], _brute_attention(list(qr[0, t, 0]), keys, vals), rtol=0, atol=1e-13)
