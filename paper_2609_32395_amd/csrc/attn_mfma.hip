@@ -63,42 +63,6 @@ __device__ __forceinline__ bf16x8 pack_p(const floatx4& a, const floatx4& b) {
   return r;
 }
 
-// Page tile chunks per thread (256 threads, 16-byte chunks).
-template <int DH>
-struct PageRegs {
-  static constexpr int NK = BT * DH / 8 / 256;
-  static constexpr int NV = DH * BT / 8 / 256;
-  u32x4 k[NK];
-  u32x4 v[NV];
-};
-
-template <int DH>
-__device__ __forceinline__ void page_load(PageRegs<DH>& r, const uint16_t* __restrict__ Kt,
-                                          const uint16_t* __restrict__ VT, int tid) {
-#pragma unroll
-  for (int i = 0; i < PageRegs<DH>::NK; ++i) r.k[i] = load_stream(Kt + (size_t)(tid + i * 256) * 8);
-#pragma unroll
-  for (int i = 0; i < PageRegs<DH>::NV; ++i) r.v[i] = load_stream(VT + (size_t)(tid + i * 256) * 8);
-}
-
-template <int DH>
-__device__ __forceinline__ void page_store(const PageRegs<DH>& r, Tiles<DH>& T, int tid) {
-#pragma unroll
-  for (int i = 0; i < PageRegs<DH>::NK; ++i) {
-    const int c = tid + i * 256;
-    const int row = c / (DH / 8), c8 = c % (DH / 8);
-    *(u32x4*)&T.k[row * Tiles<DH>::KS + c8 * 8] = r.k[i];
-  }
-#pragma unroll
-  for (int i = 0; i < PageRegs<DH>::NV; ++i) {
-    const int c = tid + i * 256;
-    const int d = c / (BT / 8), c8 = c % (BT / 8);
-    u32x2* dst = (u32x2*)&T.vt[d * Tiles<DH>::VS + c8 * 8];   // rows are 8-byte aligned
-    dst[0] = u32x2{r.v[i].x, r.v[i].y};
-    dst[1] = u32x2{r.v[i].z, r.v[i].w};
-  }
-}
-
 // In-block tile from token-major tensors ([row][H][dh], row stride H*dh):
 // keys row-major, values transposed into LDS.  tile_load issues every global
 // load of the tile into registers; tile_store writes them to LDS.  The
@@ -219,22 +183,6 @@ __device__ __forceinline__ void rope_q(bf16x8 (&dst)[DH / 32], const bf16x8 (&sr
     rope_turn<8>(x, row, kk * 16 + (lane >> 4) * 4);
 #pragma unroll
     for (int j = 0; j < 8; ++j) dst[kk][j] = (__bf16)x[j];
-  }
-}
-
-// Re-turn the query fragments from their unturned copy in LDS, one k-chunk
-// at a time (a scheduling barrier per chunk keeps the temporaries few).
-template <int DH>
-__device__ __forceinline__ void rope_q_from_lds(bf16x8 (&dst)[DH / 32], const u32x4* __restrict__ qb,
-                                                const float* __restrict__ row, int wave, int lane) {
-#pragma unroll
-  for (int kk = 0; kk < DH / 32; ++kk) {
-    float x[8];
-    Chunk<uint16_t>::unpack(qb[(kk * 4 + wave) * 64 + lane], x);
-    rope_turn<8>(x, row, kk * 16 + (lane >> 4) * 4);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) dst[kk][j] = (__bf16)x[j];
-    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -487,9 +435,11 @@ struct PrefillLds {
 };
 template <int DH>
 struct PrefillLds<DH, true> {
-  Tiles<DH> T;
-  float rows[kRopeRows * DH];          // turns d_lo .. d_lo + kRopeRows - 1
-  u32x4 qb[(DH / 32) * 4 * 64];        // unturned query fragments, [kk][wave][lane]
+  union {
+    Tiles<DH> T;                                       // final split: null row and in-block keys
+    __attribute__((aligned(1024))) uint8_t ring[PageRing<DH>::NS * PageRing<DH>::TILE];
+  };
+  float rows[kRopeRows * DH];                          // turns d_lo .. d_lo + kRopeRows - 1
 };
 
 // S^T for this wave's 16 queries against a page's 64 keys in a ring stage.
@@ -563,111 +513,75 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
   float m = -INFINITY, l = 0.f;
 
   if (split < nms) {
-    if constexpr (!ROPE) {
-      using R = PageRing<DH>;
-      const int p0 = split * pps, p1 = min(n_read, p0 + pps);
-      const __attribute__((address_space(4))) int32_t* lpc =
-          (const __attribute__((address_space(4))) int32_t*)(a.live_page + (size_t)a.seq[slot] * a.max_blocks);
-      // this lane's 16 bytes of each DMA instruction: LDS byte (wave*IPW + i)*1024 + 16*lane of
-      // the stage, read from the tile byte that the slot permutation puts there
-      uint32_t src[R::IPW];
-  #pragma unroll
-      for (int i = 0; i < R::IPW; ++i) {
-        const int byte = (wave * R::IPW + i) * 1024 + lane * 16;
-        if (byte < R::KBYTES) {
-          const int r = byte / R::KRB, sl = (byte % R::KRB) >> 4;
-          src[i] = r * R::KRB + ((sl ^ R::kswz(r)) << 4);
-        } else {
-          const int vb = byte - R::KBYTES, d = vb >> 7, sl = (vb & 127) >> 4;
-          src[i] = R::KBYTES + d * 128 + ((sl ^ R::vswz(d)) << 4);
-        }
+    using R = PageRing<DH>;
+    const int p0 = split * pps, p1 = min(n_read, p0 + pps);
+    const __attribute__((address_space(4))) int32_t* lpc =
+        (const __attribute__((address_space(4))) int32_t*)(a.live_page + (size_t)a.seq[slot] * a.max_blocks);
+    // this lane's 16 bytes of each DMA instruction: LDS byte (wave*IPW + i)*1024 + 16*lane of
+    // the stage, read from the tile byte that the slot permutation puts there
+    uint32_t src[R::IPW];
+#pragma unroll
+    for (int i = 0; i < R::IPW; ++i) {
+      const int byte = (wave * R::IPW + i) * 1024 + lane * 16;
+      if (byte < R::KBYTES) {
+        const int r = byte / R::KRB, sl = (byte % R::KRB) >> 4;
+        src[i] = r * R::KRB + ((sl ^ R::kswz(r)) << 4);
+      } else {
+        const int vb = byte - R::KBYTES, d = vb >> 7, sl = (vb & 127) >> 4;
+        src[i] = R::KBYTES + d * 128 + ((sl ^ R::vswz(d)) << 4);
       }
-      const uint8_t* gpages = (const uint8_t*)a.pages;
-      const uint32_t lds0 = (uint32_t)(uintptr_t)L.ring;
-      auto issue = [&](int pi, int stage) {
-        const uint8_t* t = gpages + page_head_offset(lpc[pi], h, a.H, BT, DH) * 2;
-        const uint32_t d0 = lds0 + (uint32_t)(stage * R::TILE + wave * R::IPW * 1024);
-  #pragma unroll
-        for (int i = 0; i < R::IPW; ++i) dma16(t + src[i], __builtin_amdgcn_readfirstlane(d0 + i * 1024));
-      };
-      wait_vm<0>();                        // the query fragments, before any DMA is in flight
-  #pragma unroll
-      for (int k = 0; k < R::NS - 1; ++k)
-        if (p0 + k < p1) issue(p0 + k, k);
-      for (int pi = p0; pi < p1; ++pi) {
-        const int k = pi - p0;
-        wait_pages<R::IPW>(min(R::NS - 2, p1 - 1 - pi));
-        lds_barrier();                     // page pi is in LDS; every wave is done with page pi - 1
-        if (pi + R::NS - 1 < p1) issue(pi + R::NS - 1, (k + R::NS - 1) % R::NS);
-        const uint8_t* tile = L.ring + (k % R::NS) * R::TILE;
-        floatx4 s[4];
-        scores_ring<DH>(s, tile, qf, lane);
-        online_step<DH, false>(s, m, l, o, lane, qrow, a.scale_log2);
-        pv_ring<DH>(o, tile, s, lane);
+    }
+    const uint8_t* gpages = (const uint8_t*)a.pages;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)L.ring;
+    auto issue = [&](int pi, int stage) {
+      const uint8_t* t = gpages + page_head_offset(lpc[pi], h, a.H, BT, DH) * 2;
+      const uint32_t d0 = lds0 + (uint32_t)(stage * R::TILE + wave * R::IPW * 1024);
+#pragma unroll
+      for (int i = 0; i < R::IPW; ++i) dma16(t + src[i], __builtin_amdgcn_readfirstlane(d0 + i * 1024));
+    };
+    // Rotary phases: a page of block j turns the query by min(J - j, W); the
+    // turns of one split form a contiguous range, whose table rows are copied
+    // to LDS when few enough (they are then read behind the DMA ring without
+    // a load-counter wait); the unturned query fragments stay in registers.
+    [[maybe_unused]] const __attribute__((address_space(4))) int32_t* lbc =
+        (const __attribute__((address_space(4))) int32_t*)(a.live_blk + (size_t)a.seq[slot] * a.max_blocks);
+    [[maybe_unused]] int turned = -1, d_lo = 0;
+    [[maybe_unused]] bool rows_lds = false;
+    [[maybe_unused]] bf16x8 qu[DH / 32];
+    if constexpr (ROPE) {
+      const int J = a.qblk[slot];
+      const int d_hi = min(J - lbc[p0], a.rope_clip);
+      d_lo = min(J - lbc[p1 - 1], a.rope_clip);
+      rows_lds = d_hi - d_lo < kRopeRows;
+      if (rows_lds) {
+        const int n4 = (d_hi - d_lo + 1) * DH / 4;
+        const f32x4* rsrc = (const f32x4*)(a.rope + (size_t)d_lo * DH);
+        for (int i = tid; i < n4; i += 256) ((f32x4*)L.rows)[i] = rsrc[i];
       }
-    } else {
-      // Rotary path: pages stream through a ring of kDepth register stages:
-      // page pi is moved to LDS while pages pi+1 .. pi+kDepth-1 are in flight.
-      constexpr int kDepth = 3;
-      const int p0 = split * pps, p1 = min(n_read, p0 + pps);
-      const int32_t* lp = a.live_page + (size_t)a.seq[slot] * a.max_blocks;
-      [[maybe_unused]] const int32_t* lb = a.live_blk + (size_t)a.seq[slot] * a.max_blocks;
-      [[maybe_unused]] int turned = -1, d_lo = 0;
-      [[maybe_unused]] bool rows_lds = false;
+#pragma unroll
+      for (int kk = 0; kk < DH / 32; ++kk) qu[kk] = qf[kk];
+    }
+    wait_vm<0>();                          // query fragments and rotary rows, before any DMA is in flight
+#pragma unroll
+    for (int k = 0; k < R::NS - 1; ++k)
+      if (p0 + k < p1) issue(p0 + k, k);
+    for (int pi = p0; pi < p1; ++pi) {
+      const int k = pi - p0;
+      wait_pages<R::IPW>(min(R::NS - 2, p1 - 1 - pi));
+      lds_barrier();                       // page pi is in LDS; every wave is done with page pi - 1
+      if (pi + R::NS - 1 < p1) issue(pi + R::NS - 1, (k + R::NS - 1) % R::NS);
       if constexpr (ROPE) {
-        // before the first page load: these waits drain nothing
-        const int J = a.qblk[slot];
-        const int d_hi = min(J - lb[p0], a.rope_clip);
-        d_lo = min(J - lb[p1 - 1], a.rope_clip);
-        rows_lds = d_hi - d_lo < kRopeRows;
-        if (rows_lds) {
-          const int n4 = (d_hi - d_lo + 1) * DH / 4;
-          const f32x4* src = (const f32x4*)(a.rope + (size_t)d_lo * DH);
-          for (int i = tid; i < n4; i += 256) ((f32x4*)L.rows)[i] = src[i];
-        }
-  #pragma unroll
-        for (int kk = 0; kk < DH / 32; ++kk) L.qb[(kk * 4 + wave) * 64 + lane] = __builtin_bit_cast(u32x4, qf[kk]);
-        // L.rows is read after the barrier that precedes the first page_store;
-        // each lane reads back only its own L.qb entries
-      }
-      const uint16_t* pages = (const uint16_t*)a.pages;
-      PageRegs<DH> r[kDepth];
-  #pragma unroll
-      for (int u = 0; u < kDepth; ++u) {
-        if (p0 + u < p1) {
-          const uint16_t* Kt = pages + page_head_offset(lp[p0 + u], h, a.H, BT, DH);
-          page_load<DH>(r[u], Kt, Kt + BT * DH, tid);
+        const int dlt = min(a.qblk[slot] - lbc[pi], a.rope_clip);
+        if (dlt != turned) {
+          rope_q<DH>(qf, qu, rows_lds ? L.rows + (dlt - d_lo) * DH : a.rope + (size_t)dlt * DH, lane);
+          turned = dlt;
         }
       }
-      for (int base = p0; base < p1; base += kDepth) {
-  #pragma unroll
-        for (int u = 0; u < kDepth; ++u) {
-          const int pi = base + u;
-          if (pi < p1) {
-            __syncthreads();
-            page_store<DH>(r[u], T, tid);
-            __syncthreads();
-            if constexpr (ROPE) {
-              // between the store of stage u and its refill, so the turn's
-              // temporaries take the stage's registers
-              const int dlt = min(a.qblk[slot] - lb[pi], a.rope_clip);
-              if (dlt != turned) {
-                if (rows_lds) rope_q_from_lds<DH>(qf, L.qb, L.rows + (dlt - d_lo) * DH, wave, lane);
-                else rope_q_from_lds<DH>(qf, L.qb, a.rope + (size_t)dlt * DH, wave, lane);
-                turned = dlt;
-              }
-            }
-            if (pi + kDepth < p1) {
-              const uint16_t* Kt = pages + page_head_offset(lp[pi + kDepth], h, a.H, BT, DH);
-              page_load<DH>(r[u], Kt, Kt + BT * DH, tid);
-            }
-            floatx4 s[4];
-            scores<DH>(s, T, qf, lane);
-            online_step<DH, false>(s, m, l, o, lane, qrow, a.scale_log2);
-            pv<DH>(o, T, s, lane);
-          }
-        }
-      }
+      const uint8_t* tile = L.ring + (k % R::NS) * R::TILE;
+      floatx4 s[4];
+      scores_ring<DH>(s, tile, qf, lane);
+      online_step<DH, false>(s, m, l, o, lane, qrow, a.scale_log2);
+      pv_ring<DH>(o, tile, s, lane);
     }
   } else {
     if (a.null_kv != nullptr) {

@@ -150,7 +150,8 @@ def test_rope_prefill_lds_rows(dh):
     """Rotary prefill split: turns of its pages (ascending block index) fall
     monotonically, so every page's turn lies in [d_lo, d_hi]; the LDS copy of
     rows d_lo..d_hi (taken when it has fewer than 24 rows) fits its array and
-    reads inside the table; query fragments fit their LDS copy."""
+    reads inside the table; the page ring and the rows fit two workgroups
+    per CU (160 KiB of LDS)."""
     ROWS = 24
     rng = __import__("random").Random(dh)
     for _ in range(200):
@@ -168,10 +169,10 @@ def test_rope_prefill_lds_rows(dh):
             assert n4 * 4 <= ROWS * dh
             assert d_lo * dh + n4 * 4 <= n_phases * dh
             assert all((x - d_lo) * dh + dh <= ROWS * dh for x in d)
-    assert ((dh // 32 - 1) * 4 + 3) * 64 + 63 < (dh // 32) * 4 * 64
-    # LDS per workgroup: tiles + rows + query copy stay within 64 KiB
+    # LDS per workgroup: max(in-block tiles, page ring) + rows; two workgroups per CU
     tiles = (64 * (dh + 8) + dh * (64 + 4)) * 2
-    assert tiles + ROWS * dh * 4 + (dh // 32) * 4 * 64 * 16 <= 64 * 1024
+    ring = {32: 4, 64: 4, 128: 2}[dh] * 2 * 64 * dh * 2
+    assert 2 * (max(tiles, ring) + ROWS * dh * 4) <= 160 * 1024
 
 
 def _pps_rows(n):
