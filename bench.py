@@ -30,7 +30,9 @@ Secondary workloads, timed in the same run and reported under "secondary":
   * the whole model at random weights, 160M / 410M / 1.5B scales (d 768 /
     1024 / 2048, E:D 3:7 / 4:15 / 4:15, heads of 32, GPT-2 vocabulary, 1024
     learned positions): block-skip serving of a fully cached context against
-    the cold prefill, batch 1, contexts 1k / 2k / 4k / 8k.
+    the cold prefill, batch 1, contexts 1k / 2k / 4k / 8k; and batched
+    KV-cached decode at the paper's (scale, context, batch) cells, 128 timed
+    tokens after 66 warm-up tokens, completed blocks appended in the loop.
 
 Timing uses HIP events on the stream the kernels are launched on (torch's
 current stream, handed to the library).  The 160M encoder and prefill calls
@@ -564,6 +566,79 @@ def model_workload(args, torch, smem, synth):
     return out
 
 
+# The paper's batched decode cells (its serving appendix): scale, context, batch
+DECODE_CELLS = [("160M", 4096, 64), ("160M", 8192, 16), ("160M", 8192, 64), ("410M", 1024, 64), ("410M", 4096, 16),
+                ("410M", 8192, 16), ("1.5B", 1024, 64), ("1.5B", 4096, 16)]
+
+
+def model_decode_workload(args, torch, smem, synth):
+    """Whole-model KV-cached batched decode at the paper's cells: every
+    sequence holds a context of n tokens (n / b encoded blocks) and decodes
+    the next tokens one step at a time, appending each block as it completes
+    (one multi-sequence encode per boundary, inside the timed steps).  Token
+    ids are drawn, not sampled from the logits: the work per step is the same."""
+    stream = torch.cuda.current_stream()
+    out = {}
+    scales = {sc[0]: sc for sc in synth.MODEL_SCALES}
+    cells = [c for c in DECODE_CELLS if c[0] in args.model_scales.split(",")]
+    weights = {}
+    for name, n, S in cells:
+        _, d, E, D = scales[name]
+        H, b, vocab, T = d // 32, 64, synth.MODEL_VOCAB, synth.MODEL_T
+        if name not in weights:
+            weights.clear()
+            torch.cuda.empty_cache()
+            weights[name] = synth.model_weights_device(smem.model_weight_shapes(E, D, d, vocab, T), args.seed)
+        W = weights[name]
+        J0 = n // b
+        steps, warm = args.decode_steps, args.decode_warmup
+        nb = J0 + (steps + warm) // b + 2
+        m = smem.Model(W, E, D, d, H, b, vocab, T, S, nb, S * nb, max_tokens=8192)
+        ctx = torch.from_numpy(synth.model_tokens(args.seed, name, S * n, vocab)).to("cuda")
+        per = max(1, 128 // J0)                     # sequences per encode call (128 blocks)
+        for s0 in range(0, S, per):
+            s1 = min(S, s0 + per)
+            smem.smem_model_encode_blocks(m, [q for q in range(s0, s1) for j in range(J0)],
+                                          [j for q in range(s0, s1) for j in range(J0)], ctx[s0 * n:s1 * n])
+        gen = torch.from_numpy(synth.model_tokens(args.seed + 1, name, S * (steps + warm + b), vocab)).to("cuda")
+        gen = gen.view(S, -1)
+        logits = torch.empty((S, vocab), dtype=torch.float32, device="cuda")
+        state = {"t": 0}
+
+        def step():
+            t = state["t"]
+            J, p = J0 + t // b, t % b
+            smem.smem_model_decode(m, 0, [J] * S, [p] * S, gen[:, t].contiguous(), logits)
+            if p == b - 1:                              # the block is complete: append it
+                blk = gen[:, t - b + 1:t + 1].contiguous().view(-1)
+                smem.smem_model_encode_blocks(m, list(range(S)), [J] * S, blk)
+            state["t"] = t + 1
+
+        for _ in range(warm):
+            step()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            step()
+        e1.record(stream)
+        e1.synchronize()
+        ms = e0.elapsed_time(e1)
+        kv = S * D * (J0 + (warm + steps / 2) / b) * b * d * 2 * 2     # memory K/V read per step (average)
+        wbytes = 2.0 * (14 * D * d * d + vocab * d)
+        key = f"{name} {n}/{S}"
+        out[key] = dict(tokens_per_s=round(S * steps / (ms / 1e3), 1), ms_per_step=round(ms / steps, 4),
+                        hbm_gbs=round((kv + wbytes) / (ms / steps / 1e3) / 1e9, 1),
+                        appends_timed=sum(1 for t in range(warm, warm + steps) if t % b == b - 1))
+        print(f"[bench] decode {key}: {out[key]['tokens_per_s']:.0f} tok/s, {out[key]['ms_per_step']:.3f} ms/step",
+              file=sys.stderr, flush=True)
+        m.close()
+        del ctx, gen
+        torch.cuda.empty_cache()
+    return out
+
+
 def model_oracle_time(args, torch, smem, synth, W, E, D, d, H, b, vocab, T, n):
     """The fp64 model oracle's block-skip read of the final block of an
     n-token context (the same unit as the GPU's block_skip_ms), on this host;
@@ -655,13 +730,16 @@ def main():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-secondary", action="store_true")
-    ap.add_argument("--workloads", default="encode,serve,stream,rows,stress,rope,model",
+    ap.add_argument("--workloads", default="encode,serve,stream,rows,stress,rope,model,model_decode",
                     help="secondary workloads to run (comma list of encode, serve, stream, rows, stress, rope: "
                          "the rotary composite timed beside the headline decode and the serve; model: the whole "
-                         "model's block-skip serve against its cold prefill)")
+                         "model's block-skip serve against its cold prefill; model_decode: the whole model's "
+                         "batched KV-cached decode at the paper's cells)")
     ap.add_argument("--model-scales", default="160M,410M,1.5B")
     ap.add_argument("--model-lengths", default="1024,2048,4096,8192")
     ap.add_argument("--model-reps", type=int, default=3)
+    ap.add_argument("--decode-steps", type=int, default=128)
+    ap.add_argument("--decode-warmup", type=int, default=66)
     ap.add_argument("--no-headline", action="store_true",
                     help="profiling runs only: skip the decode headline (value is then null)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -704,6 +782,8 @@ def main():
             secondary["stress_1p5B"] = stress_workload(args, torch, smem, synth)
         if "model" in wl:
             secondary["model_block_skip"] = model_workload(args, torch, smem, synth)
+        if "model_decode" in wl:
+            secondary["model_decode"] = model_decode_workload(args, torch, smem, synth)
     cpu = None
     if dec is None:
         print(json.dumps({"metric": "profiling run (no headline)", "value": None, "secondary": secondary}))

@@ -363,7 +363,8 @@ typedef struct {
 typedef struct smem_model smem_model;
 
 /* Number of weight pointers, and device bytes of the model's pool (the
- * reader layers' stores, the activation workspace, the mapped null rows). */
+ * reader layers' stores, the activation workspace, the mapped null rows, the
+ * decode caches of in-block keys and values, D x 2 x n_seq x b x d bf16). */
 int32_t smem_model_n_weights(const smem_model_desc* desc);
 size_t smem_model_bytes(const smem_model_desc* desc);
 
@@ -376,6 +377,13 @@ smem_status smem_model_destroy(smem_model* m);
  * the append of Section 2.  All-or-nothing as smem_encode_blocks. */
 smem_status smem_model_encode(smem_model* m, int32_t seq, int32_t n_blocks, const int32_t* block_idx,
                               const int32_t* tokens, hipStream_t s);
+
+/* The same for blocks of several sequences at once: block i is block
+ * block_idx[i] of sequence seq_ids[i] (host arrays), its tokens
+ * tokens[i*b .. i*b + b - 1] (device int32) -- e.g. the blocks completed by a
+ * batch of decoding sequences.  All-or-nothing. */
+smem_status smem_model_encode_blocks(smem_model* m, int32_t n_blocks, const int32_t* seq_ids,
+                                     const int32_t* block_idx, const int32_t* tokens, hipStream_t s);
 
 /* Reader pass for n_blocks query blocks of sequence seq (tokens: device int32
  * [n_blocks*b]; query_block host): each block reads the memory of the live
@@ -394,6 +402,22 @@ smem_status smem_model_read(smem_model* m, int32_t seq, int32_t n_blocks, const 
  * The blocks must be absent (SMEM_EEXIST otherwise; nothing is changed). */
 smem_status smem_model_prefill(smem_model* m, int32_t seq, int32_t first_block, int32_t n_blocks,
                                const int32_t* tokens, float* logits, hipStream_t s);
+
+/* One KV-cached decode step (Section 3.1, "Decode"; the serving appendix's
+ * batched decode) for sequences first_seq .. first_seq + n_seq - 1: token
+ * tokens[i] (device int32) at in-block position pos[i] of block
+ * query_block[i] (host arrays).  In every reader layer the token's key and
+ * value go into the model's in-block cache of the sequence at pos[i]; the
+ * self-attention reads cached positions 0..pos[i] of the block, the
+ * cross-attention the memory of the live blocks below query_block[i] with
+ * the null row.  logits: device fp32 [n_seq, vocab].  Decoding a block's
+ * positions 0..b-1 in order reproduces the reader pass over the block up to
+ * rounding; once its last token is decoded the caller appends the block with
+ * smem_model_encode (its b tokens) and moves on to block + 1, position 0.
+ * Positions of one sequence are decoded in order: position p reads the
+ * cache entries 0..p-1 written by earlier steps. */
+smem_status smem_model_decode(smem_model* m, int32_t first_seq, int32_t n_seq, const int32_t* query_block,
+                              const int32_t* pos, const int32_t* tokens, float* logits, hipStream_t s);
 
 /* Exact deletion of block block_idx of sequence seq from every reader layer
  * (Theorem 1).  SMEM_ENOENT if absent. */

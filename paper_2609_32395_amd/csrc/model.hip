@@ -81,7 +81,10 @@ struct EmbArgs {
   const uint16_t* pos_emb; // [n_pos][d] or NULL
   uint16_t* x;             // [rows][d]
   int32_t rows, d, b, vocab, slots;
-  int32_t blk[kMaxSlots];  // block index of each b-row group
+  int32_t per_row;         // 0: rows are whole blocks (row r: block blk[r / b], offset r % b);
+                           // 1: one row per entry (row r: block blk[r], offset off[r])
+  int32_t blk[kMaxSlots];  // block index of each b-row group, or of each row
+  int32_t off[kMaxSlots];  // in-block offset of each row (per_row)
 };
 
 // x[r] = tok_emb[token] + pos_emb[min(block, slots-1)*b + offset]; one wave per
@@ -92,8 +95,8 @@ __global__ void __launch_bounds__(256) k_embed(EmbArgs a) {
   if (r >= a.rows) return;
   int tok = a.tokens[r];
   if (tok < 0 || tok >= a.vocab) tok = 0;
-  const int t = r % a.b;
-  const int pos = min(a.blk[r / a.b], a.slots - 1) * a.b + t;
+  const int t = a.per_row ? a.off[r] : r % a.b;
+  const int pos = min(a.blk[a.per_row ? r : r / a.b], a.slots - 1) * a.b + t;
   for (int c = lane * 8; c < a.d; c += 512) {
     float e[8], p[8];
     Chunk<uint16_t>::unpack(*(const u32x4*)(a.tok_emb + (size_t)tok * a.d + c), e);
@@ -122,6 +125,7 @@ struct smem_model {
   char* pool = nullptr;
   uint16_t *x = nullptr, *h = nullptr, *q = nullptr, *k = nullptr, *v = nullptr, *o = nullptr, *f = nullptr;
   uint16_t* null_kv = nullptr;       // [D][2][d]
+  uint16_t* cache = nullptr;         // decode: in-block keys/values [D][2][n_seq][b][d]
 };
 
 namespace {
@@ -147,7 +151,7 @@ smem_store_desc store_desc(const smem_model_desc* d) {
 }
 
 struct Layout {
-  size_t store_bytes, off_ws, off_null, total;
+  size_t store_bytes, off_ws, off_null, off_cache, total;
 };
 
 bool layout(const smem_model_desc* d, Layout* L) {
@@ -160,6 +164,8 @@ bool layout(const smem_model_desc* d, Layout* L) {
   off += a256((size_t)d->max_tokens * d->d * 2) * 6 + a256((size_t)d->max_tokens * 4 * d->d * 2);
   L->off_null = off;
   off += a256((size_t)d->D * 2 * d->d * 2);
+  L->off_cache = off;
+  off += a256((size_t)d->D * 2 * d->n_seq * d->b * d->d * 2);
   L->total = off;
   return true;
 }
@@ -281,6 +287,60 @@ smem_status read_chunk(smem_model* m, int seq, int nb, const int32_t* qblk, cons
   return SMEM_OK;
 }
 
+// One decode step for sequences first .. first + n - 1 (n <= kMaxSlots):
+// rows are single tokens; each reader layer's self-attention reads the
+// sequence's in-block cache (the new key/value written at pos first), its
+// cross-attention the memory of the live blocks below J with the null row.
+smem_status decode_chunk(smem_model* m, int first, int n, const int32_t* qblk, const int32_t* pos,
+                         const int32_t* tokens, float* logits, hipStream_t s) {
+  const auto& d = m->d;
+  Wts w{m};
+  const int D = d.d;
+  {
+    EmbArgs e;
+    memset(&e, 0, sizeof e);
+    e.tokens = tokens; e.tok_emb = w.tok(); e.pos_emb = w.pos(); e.x = m->x;
+    e.rows = n; e.d = D; e.b = d.b; e.vocab = d.vocab; e.slots = d.n_pos ? d.n_pos / d.b : 1; e.per_row = 1;
+    for (int i = 0; i < n; ++i) {
+      e.blk[i] = qblk[i];
+      e.off[i] = pos[i];
+    }
+    hipLaunchKernelGGL(k_embed, dim3((n + 3) / 4), dim3(256), 0, s, e);
+    MCHECK(hipGetLastError(), "embedding");
+  }
+  std::vector<int32_t> seqs(n), zero(n, 0);
+  for (int i = 0; i < n; ++i) seqs[i] = first + i;
+  const size_t plane = (size_t)d.n_seq * d.b * D;              // one layer's key (or value) cache
+  for (int l = 0; l < d.D; ++l) {
+    uint16_t* kc = m->cache + (size_t)l * 2 * plane + (size_t)first * d.b * D;
+    uint16_t* vc = kc + plane;
+    // self-attention over the block's cached tokens 0..pos
+    MCHECK(lnorm(m->x, w.dec(l, R_LN1G), w.dec(l, R_LN1B), m->h, n, D, s), "layernorm");
+    LinArgs a = lin(m->h, D, w.dec(l, R_QKV), n, 3 * D, D, m->q, D);
+    a.y1 = m->k; a.y2 = m->v; a.ns = D;
+    MCHECK(linear<kLinSplit>(a, s), "qkv");
+    MSTATUS(smem_reader_decode(m->stores[l], n, seqs.data(), zero.data(), pos, m->q, m->k, m->v, kc, vc, nullptr,
+                               m->o, s));
+    LinArgs o = lin(m->o, D, w.dec(l, R_O), n, D, D, m->x, D);
+    o.res = m->x;
+    MCHECK(linear<kLinResid>(o, s), "attention out");
+    // cross-attention into the memory of strictly earlier blocks, with the null row
+    MCHECK(lnorm(m->x, w.dec(l, R_LN2G), w.dec(l, R_LN2B), m->h, n, D, s), "layernorm");
+    MCHECK(linear<kLinStore>(lin(m->h, D, w.dec(l, R_Q), n, D, D, m->q, D), s), "cross-attention query");
+    MSTATUS(smem_reader_decode(m->stores[l], n, seqs.data(), qblk, pos, m->q, nullptr, nullptr, nullptr, nullptr,
+                               m->null_kv + (size_t)l * 2 * D, m->o, s));
+    LinArgs oc = lin(m->o, D, w.dec(l, R_OC), n, D, D, m->x, D);
+    oc.res = m->x;
+    MCHECK(linear<kLinResid>(oc, s), "cross-attention out");
+    MSTATUS(ffn(m, n, w.dec(l, R_LN3G), w.dec(l, R_LN3B), w.dec(l, R_FF1), w.dec(l, R_FF2), s));
+  }
+  MCHECK(lnorm(m->x, w.fin_g(), w.fin_b(), m->h, n, D, s), "final layernorm");
+  LinArgs hd = lin(m->h, D, w.head(), n, d.vocab, D, nullptr, d.vocab);
+  hd.yf = logits;
+  MCHECK(linear<kLinF32>(hd, s), "output head");
+  return SMEM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -332,6 +392,7 @@ smem_status smem_model_create(const smem_model_desc* desc, const void* const* we
   }
   m->f = (uint16_t*)ws;
   m->null_kv = (uint16_t*)(m->pool + L.off_null);
+  m->cache = (uint16_t*)(m->pool + L.off_cache);
   // the null row through every reader layer's key and value maps, once
   Wts w{m};
   for (int l = 0; l < desc->D; ++l) {
@@ -354,26 +415,30 @@ smem_status smem_model_destroy(smem_model* m) {
   return SMEM_OK;
 }
 
-smem_status smem_model_encode(smem_model* m, int32_t seq, int32_t n_blocks, const int32_t* block_idx,
-                              const int32_t* tokens, hipStream_t s) {
+smem_status smem_model_encode_blocks(smem_model* m, int32_t n_blocks, const int32_t* seq_ids,
+                                     const int32_t* block_idx, const int32_t* tokens, hipStream_t s) {
   if (!m) return mfail(SMEM_EINVAL, "model is NULL");
   const auto& d = m->d;
   if (n_blocks < 0) return mfail(SMEM_EINVAL, "n_blocks < 0");
   if (n_blocks == 0) return SMEM_OK;
-  if (!block_idx || !tokens) return mfail(SMEM_EINVAL, "block_idx and tokens are required");
-  if (seq < 0 || seq >= d.n_seq) return mfail(SMEM_EINVAL, "seq out of range");
-  std::set<int32_t> seen;
+  if (!seq_ids || !block_idx || !tokens) return mfail(SMEM_EINVAL, "seq_ids, block_idx and tokens are required");
+  std::set<std::pair<int32_t, int32_t>> seen;
   for (int i = 0; i < n_blocks; ++i) {
+    if (seq_ids[i] < 0 || seq_ids[i] >= d.n_seq) return mfail(SMEM_EINVAL, "seq out of range");
     if (block_idx[i] < 0 || block_idx[i] >= d.max_blocks) return mfail(SMEM_EINVAL, "block index out of range");
-    if (!seen.insert(block_idx[i]).second) return mfail(SMEM_EEXIST, "a block index is given twice");
+    if (!seen.insert({seq_ids[i], block_idx[i]}).second) return mfail(SMEM_EEXIST, "a block is given twice");
   }
   // every layer's store holds the same blocks: check occupancy and space on the first
   {
-    int32_t n_live = 0;
+    std::set<int32_t> seqs_in;
+    for (int i = 0; i < n_blocks; ++i) seqs_in.insert(seq_ids[i]);
     std::vector<int32_t> live(d.max_blocks);
-    MSTATUS(smem_store_export(m->stores[0], seq, live.data(), &n_live, nullptr, nullptr, s));
-    for (int i = 0; i < n_live; ++i)
-      if (seen.count(live[i])) return mfail(SMEM_EEXIST, "a block index is occupied");
+    for (int32_t q : seqs_in) {
+      int32_t n_live = 0;
+      MSTATUS(smem_store_export(m->stores[0], q, live.data(), &n_live, nullptr, nullptr, s));
+      for (int i = 0; i < n_live; ++i)
+        if (seen.count({q, live[i]})) return mfail(SMEM_EEXIST, "a block index is occupied");
+    }
     int32_t used = 0, free_pages = 0;
     MSTATUS(smem_store_stats(m->stores[0], &used, &free_pages));
     if (free_pages < n_blocks) return mfail(SMEM_ENOMEM, "not enough free pages");
@@ -389,15 +454,21 @@ smem_status smem_model_encode(smem_model* m, int32_t seq, int32_t n_blocks, cons
       MSTATUS(ffn(m, rows, w.enc(l, E_LN2G), w.enc(l, E_LN2B), w.enc(l, E_FF1), w.enc(l, E_FF2), s));
     }
     MCHECK(lnorm(m->x, w.mem_g(), w.mem_b(), m->h, rows, D, s), "memory layernorm");
-    std::vector<int32_t> seqs(nb, seq);
     for (int l = 0; l < d.D; ++l) {
       LinArgs a = lin(m->h, D, w.dec(l, R_K), rows, 2 * D, D, m->q, D);
       a.w2 = w.dec(l, R_V); a.n2 = D; a.y1 = m->k; a.ns = D;
       MCHECK(linear<kLinSplit>(a, s), "memory key/value maps");
-      MSTATUS(smem_store_put_blocks(m->stores[l], nb, seqs.data(), block_idx + i0, m->q, m->k, s));
+      MSTATUS(smem_store_put_blocks(m->stores[l], nb, seq_ids + i0, block_idx + i0, m->q, m->k, s));
     }
   }
   return SMEM_OK;
+}
+
+smem_status smem_model_encode(smem_model* m, int32_t seq, int32_t n_blocks, const int32_t* block_idx,
+                              const int32_t* tokens, hipStream_t s) {
+  if (n_blocks < 0) return mfail(SMEM_EINVAL, "n_blocks < 0");
+  const std::vector<int32_t> seqs(n_blocks, seq);
+  return smem_model_encode_blocks(m, n_blocks, seqs.data(), block_idx, tokens, s);
 }
 
 smem_status smem_model_read(smem_model* m, int32_t seq, int32_t n_blocks, const int32_t* query_block,
@@ -436,6 +507,27 @@ smem_status smem_model_prefill(smem_model* m, int32_t seq, int32_t first_block, 
     const bool last = i0 + nb == n_blocks;
     MSTATUS(read_chunk(m, seq, nb, blocks.data() + i0, tokens + (size_t)i0 * d.b, last ? logits : nullptr,
                        (nb - 1) * d.b, s));
+  }
+  return SMEM_OK;
+}
+
+smem_status smem_model_decode(smem_model* m, int32_t first_seq, int32_t n_seq, const int32_t* query_block,
+                              const int32_t* pos, const int32_t* tokens, float* logits, hipStream_t s) {
+  if (!m) return mfail(SMEM_EINVAL, "model is NULL");
+  const auto& d = m->d;
+  if (n_seq < 0) return mfail(SMEM_EINVAL, "n_seq < 0");
+  if (n_seq == 0) return SMEM_OK;
+  if (!query_block || !pos || !tokens || !logits) return mfail(SMEM_EINVAL, "query_block, pos, tokens and logits are required");
+  if (first_seq < 0 || (int64_t)first_seq + n_seq > d.n_seq) return mfail(SMEM_EINVAL, "sequences out of range");
+  for (int i = 0; i < n_seq; ++i) {
+    if (query_block[i] < 0 || query_block[i] > d.max_blocks) return mfail(SMEM_EINVAL, "query block out of range");
+    if (pos[i] < 0 || pos[i] >= d.b) return mfail(SMEM_EINVAL, "pos out of range [0, b)");
+  }
+  const int chunk = std::min(kMaxSlots, (int)d.max_tokens);
+  for (int i0 = 0; i0 < n_seq; i0 += chunk) {
+    const int n = std::min(chunk, n_seq - i0);
+    MSTATUS(decode_chunk(m, first_seq + i0, n, query_block + i0, pos + i0, tokens + i0,
+                         logits + (size_t)i0 * d.vocab, s));
   }
   return SMEM_OK;
 }

@@ -106,8 +106,10 @@ SIGNATURES = {
                                ctypes.POINTER(_P)]),
     "smem_model_destroy": (_I, [_P]),
     "smem_model_encode": (_I, [_P, _I, _I, _IP, _P, _P]),
+    "smem_model_encode_blocks": (_I, [_P, _I, _IP, _IP, _P, _P]),
     "smem_model_read": (_I, [_P, _I, _I, _IP, _P, _P, _P]),
     "smem_model_prefill": (_I, [_P, _I, _I, _I, _P, _P, _P]),
+    "smem_model_decode": (_I, [_P, _I, _I, _IP, _IP, _P, _P, _P]),
     "smem_model_delete_block": (_I, [_P, _I, _I, _P]),
     "smem_store_stats": (_I, [_P, _IP, _IP]),
     "smem_status_string": (ctypes.c_char_p, [_I]),
@@ -399,6 +401,14 @@ def smem_model_encode(m: Model, seq: int, block_idx, tokens, stream=None):
     _check(lib().smem_model_encode(m.handle, int(seq), n, _i32(block_idx), _tokens(tokens, n, m.b), _stream(stream)))
 
 
+def smem_model_encode_blocks(m: Model, seq_ids, block_idx, tokens, stream=None):
+    n = len(block_idx)
+    if len(seq_ids) != n:
+        raise ValueError("seq_ids and block_idx differ in length")
+    _check(lib().smem_model_encode_blocks(m.handle, n, _i32(seq_ids), _i32(block_idx), _tokens(tokens, n, m.b),
+                                          _stream(stream)))
+
+
 def smem_model_read(m: Model, seq: int, query_block, tokens, logits=None, stream=None):
     """Logits [n*b, vocab] fp32 of the query blocks."""
     n = len(query_block)
@@ -417,6 +427,21 @@ def smem_model_prefill(m: Model, seq: int, first_block: int, n_blocks: int, toke
     lp = _dev(logits, (m.b, m.vocab), torch.float32, "logits")
     _check(lib().smem_model_prefill(m.handle, int(seq), int(first_block), int(n_blocks), _tokens(tokens, n_blocks, m.b),
                                     lp, _stream(stream)))
+    return logits
+
+
+def smem_model_decode(m: Model, first_seq: int, query_block, pos, tokens, logits=None, stream=None):
+    """One decode step for sequences first_seq .. first_seq + n - 1; logits [n, vocab]."""
+    n = len(query_block)
+    if len(pos) != n:
+        raise ValueError("query_block and pos differ in length")
+    if logits is None:
+        logits = torch.empty((n, m.vocab), dtype=torch.float32, device=tokens.device)
+    lp = _dev(logits, (n, m.vocab), torch.float32, "logits")
+    if tokens.dtype != torch.int32 or tokens.device.type != "cuda" or not tokens.is_contiguous() or tokens.numel() != n:
+        raise ValueError("tokens must be a contiguous int32 device tensor of n ids")
+    _check(lib().smem_model_decode(m.handle, int(first_seq), n, _i32(query_block), _i32(pos),
+                                   ctypes.c_void_p(tokens.data_ptr()), lp, _stream(stream)))
     return logits
 
 

@@ -162,7 +162,8 @@ def test_model_descriptor_and_weight_list():
     sd = smem.StoreDesc(1, 128, 128, b, H, d // H, smem.BF16)
     store = (L.smem_store_bytes(ctypes.byref(sd)) + 255) // 256 * 256
     ws = 6 * 4096 * d * 2 + 4096 * 4 * d * 2 + (D * 2 * d * 2 + 255) // 256 * 256
-    assert L.smem_model_bytes(ctypes.byref(desc)) == D * store + ws
+    cache = D * 2 * 1 * b * d * 2                     # decode caches: [D][2][n_seq][b][d] bf16
+    assert L.smem_model_bytes(ctypes.byref(desc)) == D * store + ws + cache
     for field, bad in (("b", 16), ("dh", 48), ("d", 700), ("n_pos", 100), ("max_tokens", 100),
                        ("max_tokens", 129 * 64), ("D", 0), ("vocab", 0)):
         bd = smem.ModelDesc.from_buffer_copy(desc)

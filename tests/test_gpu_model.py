@@ -237,3 +237,59 @@ def test_model_edge_cases():
     assert e.value.code == smem.SMEM_EINVAL
     # the store is unchanged by the failed calls
     assert torch.equal(smem.smem_model_read(m, 0, [6], tok(q)), torch.from_numpy(y).to("cuda"))
+
+
+def test_decode_matches_reader_and_oracle_across_a_boundary():
+    """KV-cached decode (Section 3.1, "Decode"): decoding block J's tokens in
+    order gives, at position p, the reader pass's row p of the block (the
+    oracle's, within the rounding tolerance; the GPU block read's too); the
+    completed block is appended and decoding continues into block J + 1."""
+    say("model: decode across a boundary")
+    m, ref, _ = build(max_blocks=10, n_pages=10)
+    g = np.random.default_rng(17)
+    J = 5
+    tokens = g.integers(0, SHAPE["vocab"], size=(J + 2, SHAPE["b"]))
+    smem.smem_model_encode(m, 0, list(range(J)), tok(tokens[:J]))
+    ref.encode(0, tokens[:J], list(range(J)))
+    block = smem.smem_model_read(m, 0, [J], tok(tokens[J:J + 1]))
+    expect = ref.read(0, tokens[J:J + 1], [J])[0]
+    rows = []
+    for p in range(SHAPE["b"]):
+        rows.append(smem.smem_model_decode(m, 0, [J], [p], tok(tokens[J, p:p + 1])))
+    y = host(torch.cat(rows))
+    t = tol(SHAPE["E"], SHAPE["D"], y.size)
+    err = float(np.max(np.abs(y - expect)) / np.sqrt(np.mean(expect ** 2)))
+    say("decode vs oracle", err, "vs GPU block read",
+        float(np.max(np.abs(y - host(block))) / np.sqrt(np.mean(expect ** 2))))
+    assert err <= t
+    assert float(np.max(np.abs(y - host(block))) / np.sqrt(np.mean(expect ** 2))) <= t
+    # append the completed block, continue into block J + 1
+    smem.smem_model_encode(m, 0, [J], tok(tokens[J:J + 1]))
+    ref.encode(0, tokens[J:J + 1], [J])
+    nxt = [host(smem.smem_model_decode(m, 0, [J + 1], [p], tok(tokens[J + 1, p:p + 1])))[0] for p in range(4)]
+    e2 = ref.read(0, tokens[J + 1:J + 2], [J + 1])[0][:4]
+    assert float(np.max(np.abs(np.stack(nxt) - e2)) / np.sqrt(np.mean(e2 ** 2))) <= t
+
+
+def test_decode_batch_invariant_bitwise():
+    """Three sequences at different blocks and positions decoded in one call
+    give, bit for bit, what each gives decoded alone."""
+    say("model: decode batch invariance")
+    s = dict(SHAPE)
+    W = synth.model_weights(smem.model_weight_shapes(s["E"], s["D"], s["d"], s["vocab"], s["n_pos"]), 5)
+    dW = {k: torch.from_numpy(v).to("cuda").to(torch.bfloat16).contiguous() for k, v in W.items()}
+    m = smem.Model(dW, s["E"], s["D"], s["d"], s["H"], s["b"], s["vocab"], s["n_pos"], 3, 8, 24, 256)
+    g = np.random.default_rng(18)
+    J, P = [2, 5, 0], [3, 7, 5]
+    for q in range(3):
+        if J[q]:
+            smem.smem_model_encode(m, q, list(range(J[q])), tok(g.integers(0, s["vocab"], size=(J[q], s["b"]))))
+    toks = g.integers(0, s["vocab"], size=(3, max(P) + 1))
+    for p in range(max(P)):                      # fill each sequence's in-block cache up to its position
+        for q in range(3):
+            if p < P[q]:
+                smem.smem_model_decode(m, q, [J[q]], [p], tok(toks[q, p:p + 1]))
+    batch = smem.smem_model_decode(m, 0, J, P, tok(toks[np.arange(3), P]))
+    for q in range(3):
+        alone = smem.smem_model_decode(m, q, [J[q]], [P[q]], tok(toks[q, P[q]:P[q] + 1]))
+        assert torch.equal(alone[0], batch[q]), q
