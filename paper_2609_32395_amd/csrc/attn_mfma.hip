@@ -46,8 +46,8 @@ template <int DH>
 struct Tiles {
   static constexpr int KS = DH + 8;      // key tile row stride (elements)
   static constexpr int VS = BT + 4;      // transposed value tile row stride (elements)
-  uint16_t k[BT * KS];
-  uint16_t vt[DH * VS];
+  __attribute__((aligned(16))) uint16_t k[BT * KS];
+  __attribute__((aligned(16))) uint16_t vt[DH * VS];
 };
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 u) {
@@ -66,8 +66,8 @@ __device__ __forceinline__ bf16x8 pack_p(const floatx4& a, const floatx4& b) {
 // In-block tile from token-major tensors ([row][H][dh], row stride H*dh):
 // keys row-major, values transposed into LDS.  tile_load issues every global
 // load of the tile into registers; tile_store writes them to LDS.  The
-// transpose packs two token rows per 32-bit LDS write, consecutive lanes
-// taking consecutive row pairs, so a wave's writes to one value row are
+// transpose packs two token rows per 32-bit LDS write; consecutive lanes take
+// consecutive 16-byte chunks of a row pair, so the global loads of a row are
 // contiguous.
 template <int DH>
 struct TileRegs {
@@ -93,7 +93,7 @@ __device__ __forceinline__ void tile_load(TileRegs<DH>& r, const uint16_t* __res
   for (int it = 0; it < R::NV; ++it) {
     const int j = tid + it * 256;
     if (j < R::NP) {
-      const int pr = j % (BT / 2), c8 = j / (BT / 2);
+      const int pr = j / R::CPR, c8 = j % R::CPR;
       r.va[it] = *(const u32x4*)(vin + (2 * pr) * row_stride + c8 * 8);
       r.vb[it] = *(const u32x4*)(vin + (2 * pr + 1) * row_stride + c8 * 8);
     }
@@ -113,7 +113,7 @@ __device__ __forceinline__ void tile_store(const TileRegs<DH>& r, Tiles<DH>& T, 
   for (int it = 0; it < R::NV; ++it) {
     const int j = tid + it * 256;
     if (j < R::NP) {
-      const int pr = j % (BT / 2), c8 = j / (BT / 2);
+      const int pr = j / R::CPR, c8 = j % R::CPR;
       const uint32_t a4[4] = {r.va[it].x, r.va[it].y, r.va[it].z, r.va[it].w};
       const uint32_t b4[4] = {r.vb[it].x, r.vb[it].y, r.vb[it].z, r.vb[it].w};
 #pragma unroll
@@ -333,21 +333,39 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
   pv<DH>(o, T, s4, lane);
   l = qsum(l);
   const float inv = 1.f / l;
-  const size_t orow = (size_t)blk * BT + qrow;
   const int pg = a.sink[blk];
   uint16_t* kp = (a.pages && pg >= 0) ? a.pages + page_head_offset(pg, h, a.H, BT, DH) : nullptr;
+  // The block's output rows go through LDS (the key tile's space, row pitch
+  // KS) so that global stores are whole 16-byte chunks of consecutive rows:
+  // a lane's fragment is 4 dims of one query row, 8 bytes scattered over 64
+  // rows.  A page insert writes the key plane from the same rows and the
+  // transposed value plane by gathering 8 rows per chunk.
+  constexpr int KS = Tiles<DH>::KS;
+  __syncthreads();                           // every wave is done with the key and value tiles
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) {
     const int d0 = dt * 16 + (lane >> 4) * 4;
     uint16_t rr[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) rr[i] = f32_to_bf16_bits(o[dt][i] * inv);
-    const u32x2 packed = u32x2{(uint32_t)rr[0] | ((uint32_t)rr[1] << 16), (uint32_t)rr[2] | ((uint32_t)rr[3] << 16)};
-    if (a.out) *(u32x2*)(a.out + orow * rs + (size_t)h * DH + d0) = packed;
-    if (kp) {
-      *(u32x2*)(kp + qrow * DH + d0) = packed;
+    *(u32x2*)&T.k[qrow * KS + d0] = u32x2{(uint32_t)rr[0] | ((uint32_t)rr[1] << 16),
+                                          (uint32_t)rr[2] | ((uint32_t)rr[3] << 16)};
+  }
+  __syncthreads();
+  for (int c = tid; c < BT * DH / 8; c += 256) {
+    const int row = c / (DH / 8), c8 = c % (DH / 8);
+    const u32x4 v16 = *(const u32x4*)&T.k[row * KS + c8 * 8];
+    if (a.out) *(u32x4*)(a.out + ((size_t)blk * BT + row) * rs + (size_t)h * DH + c8 * 8) = v16;
+    if (kp) *(u32x4*)(kp + row * DH + c8 * 8) = v16;
+  }
+  if (kp) {
+    for (int c = tid; c < DH * BT / 8; c += 256) {
+      const int d = c / (BT / 8), r8 = c % (BT / 8);
+      uint32_t w[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) kp[BT * DH + (d0 + i) * BT + qrow] = rr[i];
+      for (int j = 0; j < 4; ++j)
+        w[j] = (uint32_t)T.k[(r8 * 8 + 2 * j) * KS + d] | ((uint32_t)T.k[(r8 * 8 + 2 * j + 1) * KS + d] << 16);
+      *(u32x4*)(kp + BT * DH + d * BT + r8 * 8) = u32x4{w[0], w[1], w[2], w[3]};
     }
   }
 }

@@ -75,7 +75,8 @@ def test_mfma_indexing(dh):
     assert len({(KS * 2 // 4 * r) % 32 for r in range(8)}) == 8
     # in-block transpose: (row pair, chunk) jobs cover 64 rows x dh, each writes dims c8*8..+7 at rows 2p, 2p+1
     NP = 32 * (dh // 8)
-    jobs = [((j % 32), (j // 32)) for j in range(NP)]
+    CPR = dh // 8
+    jobs = [((j // CPR), (j % CPR)) for j in range(NP)]       # (row pair, chunk): chunks of a pair adjacent
     assert len(set(jobs)) == NP and max(p for p, _ in jobs) == 31 and max(c for _, c in jobs) * 8 + 7 < dh
     assert (dh - 1) * VS + 2 * 31 + 1 < dh * VS
     NK = BT * dh // 8 // 256
