@@ -510,12 +510,21 @@ __device__ __forceinline__ void wait_pages(int ahead) {
   else wait_vm<0>();
 }
 
-template <int DH, bool ROPE>
+// One (query block, head) over its splits.  FUSE = false: workgroup
+// (h, split, slot) reads one split and writes its partial (m, l, o) -- or,
+// with no memory split, the output.  FUSE = true: workgroup (h, 0, z) reads
+// every split of slot order[z] in split order, the memory pages through one
+// DMA ring, and folds each split's (m, l, o) into a running state as the
+// merge does (fold_scale / fold_value), so both modes produce the same bits.
+template <int DH, bool ROPE, bool FUSE>
 __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH, ROPE>& L) {
+  static_assert(!(FUSE && ROPE), "the one-workgroup mode has no rotary variant");
   Tiles<DH>& T = L.T;
   // heads fastest: neighbouring workgroups stream the adjacent head tiles of
   // the same pages
-  const int h = blockIdx.x, split = blockIdx.y, slot = blockIdx.z;
+  const int h = blockIdx.x;
+  const int split = FUSE ? 0 : (int)blockIdx.y;
+  const int slot = FUSE ? (int)a.order[blockIdx.z] : (int)blockIdx.z;
   const int n_read = a.n_read[slot], pps = a.pps[slot];
   const int nms = (n_read + pps - 1) / pps;
   if (split > nms) return;
@@ -529,10 +538,34 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, l = 0.f;
+  // FUSE: the folded state of the splits read so far
+  [[maybe_unused]] floatx4 acc[DH / 16];
+  [[maybe_unused]] float fm = 0.f, fl = 0.f;
+  // close the current split: fold its (m, l, o) into the state, start afresh
+  [[maybe_unused]] auto fold = [&](bool first) {
+    const float ls = qsum(l);
+    if (first) {
+      fm = m;
+      fl = ls;
+#pragma unroll
+      for (int dt = 0; dt < DH / 16; ++dt) acc[dt] = o[dt];
+    } else {
+      const FoldScale c = fold_scale(fm, m);
+      fl = fold_value(fl, c, ls);
+#pragma unroll
+      for (int dt = 0; dt < DH / 16; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[dt][i] = fold_value(acc[dt][i], c, o[dt][i]);
+    }
+    m = -INFINITY;
+    l = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DH / 16; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  };
 
   if (split < nms) {
     using R = PageRing<DH>;
-    const int p0 = split * pps, p1 = min(n_read, p0 + pps);
+    const int p0 = split * pps, p1 = FUSE ? n_read : min(n_read, p0 + pps);
     const __attribute__((address_space(4))) int32_t* lpc =
         (const __attribute__((address_space(4))) int32_t*)(a.live_page + (size_t)a.seq[slot] * a.max_blocks);
     // this lane's 16 bytes of each DMA instruction: LDS byte (wave*IPW + i)*1024 + 16*lane of
@@ -583,6 +616,7 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
 #pragma unroll
     for (int k = 0; k < R::NS - 1; ++k)
       if (p0 + k < p1) issue(p0 + k, k);
+    [[maybe_unused]] int split_end = p0 + pps;
     for (int pi = p0; pi < p1; ++pi) {
       const int k = pi - p0;
       wait_pages<R::IPW>(min(R::NS - 2, p1 - 1 - pi));
@@ -600,8 +634,16 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
       scores_ring<DH>(s, tile, qf, lane);
       online_step<DH, false>(s, m, l, o, lane, qrow, a.scale_log2);
       pv_ring<DH>(o, tile, s, lane);
+      if constexpr (FUSE) {
+        if (pi + 1 == split_end || pi + 1 == p1) {
+          fold(split_end == pps);
+          split_end += pps;
+        }
+      }
     }
-  } else {
+    if constexpr (FUSE) __syncthreads();   // every wave is done with the ring before the tiles reuse it
+  }
+  if (FUSE || split == nms) {
     if (a.null_kv != nullptr) {
       // the null row: one always-visible key/value pair per head
       const uint16_t* nk = (const uint16_t*)a.null_kv + (size_t)h * DH + (lane >> 4) * 8;
@@ -643,8 +685,23 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
       pv<DH>(o, T, s, lane);
     }
   }
-  l = qsum(l);
   const size_t qs = (size_t)slot * BT + qrow;
+  if (FUSE && nms > 0) {
+    fold(false);
+    const float inv = (fl > 0.f) ? 1.f / fl : 0.f;
+    uint16_t* orow = (uint16_t*)a.out + qs * rs + (size_t)h * DH;
+#pragma unroll
+    for (int dt = 0; dt < DH / 16; ++dt) {
+      const int d0 = dt * 16 + (lane >> 4) * 4;
+      uint16_t r4[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) r4[i] = f32_to_bf16_bits(acc[dt][i] * inv);
+      *(u32x2*)(orow + d0) = u32x2{(uint32_t)r4[0] | ((uint32_t)r4[1] << 16),
+                                   (uint32_t)r4[2] | ((uint32_t)r4[3] << 16)};
+    }
+    return;
+  }
+  l = qsum(l);
   if (nms == 0) {
     const float inv = (l > 0.f) ? 1.f / l : 0.f;
     uint16_t* orow = (uint16_t*)a.out + qs * rs + (size_t)h * DH;
@@ -674,7 +731,13 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
 template <int DH>
 __global__ void __launch_bounds__(256) k_prefill_mfma(ReaderArgs a) {
   __shared__ PrefillLds<DH, false> L;
-  prefill_body<DH, false>(a, L);
+  prefill_body<DH, false, false>(a, L);
+}
+
+template <int DH>
+__global__ void __launch_bounds__(256) k_prefill_mfma_fused(ReaderArgs a) {
+  __shared__ PrefillLds<DH, false> L;
+  prefill_body<DH, false, true>(a, L);
 }
 
 // The rotary variant asks for at least two waves per SIMD: left free, the
@@ -683,7 +746,7 @@ __global__ void __launch_bounds__(256) k_prefill_mfma(ReaderArgs a) {
 template <int DH>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_prefill_mfma_rope(ReaderArgs a) {
   __shared__ PrefillLds<DH, true> L;
-  prefill_body<DH, true>(a, L);
+  prefill_body<DH, true, false>(a, L);
 }
 
 template <int DH>
@@ -692,6 +755,11 @@ static hipError_t launch_pre(const ReaderArgs& a, hipStream_t s) {
   for (int i = 0; i < a.n_slots; ++i) {
     const int ns = total_splits(a.n_read[i], a.pps[i]) - 1;
     if (ns > max_split) max_split = ns;
+  }
+  if (a.fuse) {
+    if (a.rope) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_prefill_mfma_fused<DH>), dim3(a.H, 1, a.n_slots), dim3(256), 0, s, a);
+    return hipGetLastError();
   }
   const dim3 grid(a.H, max_split + 1, a.n_slots);
   if (a.rope) hipLaunchKernelGGL((k_prefill_mfma_rope<DH>), grid, dim3(256), 0, s, a);

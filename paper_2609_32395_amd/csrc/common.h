@@ -42,6 +42,22 @@ inline int prefill_split_cap(int H) {
   const int c = SMEM_PREFILL_WG_TARGET / (H > 0 ? H : 1);
   return c < 1 ? 1 : (c > kSplitCapPrefill ? kSplitCapPrefill : c);
 }
+// A prefill launch runs one workgroup per (query block, head) pair that
+// folds its splits itself when it has at least kPrefillFusePairs pairs (a
+// block-parallel pass over a long context: the pairs fill the chip, and the
+// split partials would cost more than the longest pair's serial read), or
+// when its longest pair reads at most kPrefillFuseSerial / d_h pages (a short
+// serial read beats a second launch).  Otherwise one workgroup per split and
+// a merge.  Either way the splits and their fold are the same, so the choice
+// never changes a result.
+#ifndef SMEM_PREFILL_FUSE_PAIRS
+#define SMEM_PREFILL_FUSE_PAIRS 512
+#endif
+#ifndef SMEM_PREFILL_FUSE_SERIAL
+#define SMEM_PREFILL_FUSE_SERIAL 1024
+#endif
+constexpr int kPrefillFusePairs = SMEM_PREFILL_FUSE_PAIRS;
+constexpr int kPrefillFuseSerial = SMEM_PREFILL_FUSE_SERIAL;
 // Query slots whose prefill partials the workspace must hold at once.
 constexpr int kPrefillSlotChunk = 16;
 // Row-plane decode: pages per split max(kMinPagesRows, ceil(n_read /
@@ -118,6 +134,28 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
 // -126 come out as 0 or a denormal, a weight that is negligible next to the
 // maximum's weight of 1; 2^-inf = 0 exactly.
 __device__ __forceinline__ float exp2w(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Split partials of one (query, head) -- running maximum m (log2 units), sum
+// of weights l, unnormalised output o -- are combined in split order by a
+// running rescale, starting from split 0's triple as it is:
+//   M' = max(M, m_s), alpha = 2^(M - M'), beta = 2^(m_s - M'),
+//   L <- fma(l_s, beta, L alpha), O <- fma(o_s, beta, O alpha), M <- M'.
+// The split merge and the one-workgroup prefill both call these two
+// functions, so a (query, head) gets the same bits whichever of them
+// combines its splits.  An empty split (m_s = -inf, l_s = 0, o_s = 0) leaves
+// the state unchanged; M stays finite because split 0 reads memory rows.
+struct FoldScale {
+  float alpha, beta;
+};
+__device__ __forceinline__ FoldScale fold_scale(float& M, float m_s) {
+  const float Mn = fmaxf(M, m_s);
+  const FoldScale c{exp2w(M - Mn), exp2w(m_s - Mn)};
+  M = Mn;
+  return c;
+}
+__device__ __forceinline__ float fold_value(float acc, const FoldScale& c, float x) {
+  return __builtin_fmaf(x, c.beta, acc * c.alpha);
+}
 
 // 16-byte chunk -> E floats (E = 4 for fp32, 8 for bf16).
 template <typename T> struct Chunk;
@@ -223,6 +261,11 @@ struct ReaderArgs {
   int32_t qblk[kMaxSlots];    // query block J of the slot
   int32_t intra_partial;      // 1: the in-block / null split always writes a compact partial
                               //    ws[(qs*H + h)*(dh+4)] (row-plane decode merges it)
+  // MFMA prefill, one workgroup per (slot, head) reading every split in turn
+  // and folding them as the merge would (no partials, no merge launch);
+  // workgroup z takes slot order[z] (slots with the most pages first).
+  int32_t fuse;
+  int16_t order[kMaxSlots];
 };
 
 // Row-plane decode (bf16): rows of width d, absorbed queries, split partials.

@@ -295,41 +295,41 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
   }
 }
 
-// Merge the splits of one (query row, head) in split order: the split
-// statistics are loaded in parallel, the weights kept in LDS, and each thread
-// sums one output dimension over the splits.
+// Merge the splits of one (query row, head) in split order by the running
+// rescale of fold_scale / fold_value: the split statistics are loaded in
+// parallel, one thread walks them for the per-split scales (kept in LDS) and
+// the weight sum, and each thread folds one output dimension over the splits.
 template <typename T, int DH>
 __global__ void __launch_bounds__(128) k_merge(ReaderArgs a) {
   const int qs = blockIdx.x, h = blockIdx.y;
   const int slot = qs / a.nq;
   const int S = total_splits(a.n_read[slot], a.pps[slot]);
   if (S == 1) return;
-  __shared__ float w_sh[kSplitStride];
+  __shared__ float m_sh[kSplitStride];
   __shared__ float l_sh[kSplitStride];
-  __shared__ float wmax[2];
+  __shared__ FoldScale c_sh[kSplitStride];
   __shared__ float inv_sh;
   const int tid = threadIdx.x;
   const float* base = a.ws + ((size_t)qs * a.H + h) * kSplitStride * (DH + 4);
-  const float mk = (tid < S) ? base[(size_t)tid * (DH + 4) + DH] : -INFINITY;
-  if (tid < S) l_sh[tid] = base[(size_t)tid * (DH + 4) + DH + 1];
-  float mx = mk;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
-  if ((tid & 63) == 0) wmax[tid >> 6] = mx;
-  __syncthreads();
-  const float M = fmaxf(wmax[0], wmax[1]);
-  if (tid < S) w_sh[tid] = (mk == -INFINITY) ? 0.f : exp2w(mk - M);
+  if (tid < S) {
+    m_sh[tid] = base[(size_t)tid * (DH + 4) + DH];
+    l_sh[tid] = base[(size_t)tid * (DH + 4) + DH + 1];
+  }
   __syncthreads();
   if (tid == 0) {
-    float L = 0.f;
-    for (int k = 0; k < S; ++k) L += w_sh[k] * l_sh[k];
+    float M = m_sh[0], L = l_sh[0];
+    for (int k = 1; k < S; ++k) {
+      const FoldScale c = fold_scale(M, m_sh[k]);
+      c_sh[k] = c;
+      L = fold_value(L, c, l_sh[k]);
+    }
     inv_sh = (L > 0.f) ? 1.f / L : 0.f;
   }
   __syncthreads();
   for (int d = tid; d < DH; d += 128) {
-    float A = 0.f;
+    float A = base[d];
 #pragma unroll 8
-    for (int k = 0; k < S; ++k) A += w_sh[k] * base[(size_t)k * (DH + 4) + d];
+    for (int k = 1; k < S; ++k) A = fold_value(A, c_sh[k], base[(size_t)k * (DH + 4) + d]);
     ((T*)a.out)[((size_t)qs * a.H + h) * DH + d] = from_f32<T>(A * inv_sh);
   }
 }

@@ -556,9 +556,24 @@ static smem_status prefill_impl(smem_store* st, const smem_rope* rope, int32_t n
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
   const size_t es = esize(d.dtype);
   const size_t blk_elems = (size_t)d.b * d.H * d.dh;
-  const int chunk = prefill_slots(&d);
-  for (int i0 = 0; i0 < n_seq; i0 += chunk) {
-    const int n = std::min(chunk, n_seq - i0);
+  // bf16 blocks of 64 tokens run on the MFMA kernel, other shapes on the VALU reader
+  const bool mfma = d.dtype == BF16 && d.b == 64;
+  std::vector<int> nr(n_seq);
+  for (int i = 0; i < n_seq; ++i) nr[i] = n_read_of(st, seq_ids[i], query_block[i]);
+  // One workgroup per (query block, head) folding its own splits, when the
+  // launch has enough pairs to fill the chip or its longest pair reads few
+  // pages (either way it saves the partials and the merge); no rotary variant.
+  auto fold_in_workgroup = [&](int i0, int n) {
+    if (!mfma || rope != nullptr) return false;
+    if ((int64_t)n * d.H >= kPrefillFusePairs) return true;
+    int pm = 0;
+    for (int i = 0; i < n; ++i) pm = std::max(pm, nr[i0 + i]);
+    return (int64_t)pm * d.dh <= kPrefillFuseSerial;
+  };
+  for (int i0 = 0, n = 0; i0 < n_seq; i0 += n) {
+    n = std::min(kMaxSlots, n_seq - i0);
+    const bool fuse = fold_in_workgroup(i0, n);
+    if (!fuse) n = std::min(n, prefill_slots(&d));      // the split partials of n slots fit the workspace
     ReaderArgs a;
     memset(&a, 0, sizeof a);
     a.q = (const char*)q + i0 * blk_elems * es;
@@ -573,16 +588,22 @@ static smem_status prefill_impl(smem_store* st, const smem_rope* rope, int32_t n
     a.H = d.H; a.b = d.b; a.nq = d.b; a.intra_mode = 1;
     a.n_slots = n; a.scale_log2 = scale_log2;
     rope_args(a, st, rope);
-    // bf16 blocks of 64 tokens run on the MFMA kernel, other shapes on the VALU reader
-    const bool mfma = d.dtype == BF16 && d.b == 64;
     for (int i = 0; i < n; ++i) {
       const int sq = seq_ids[i0 + i];
       a.seq[i] = sq;
       a.qblk[i] = query_block[i0 + i];
-      a.n_read[i] = n_read_of(st, sq, query_block[i0 + i]);
+      a.n_read[i] = nr[i0 + i];
       a.pps[i] = mfma ? pages_per_split(a.n_read[i], kMinPagesPrefill, prefill_split_cap(d.H))
                       : pages_per_split(a.n_read[i], kMinPagesDecode);
       a.aux[i] = -1;
+    }
+    a.fuse = fuse;
+    if (a.fuse) {
+      // the longest reads start first, so no long pair is left for the tail
+      int idx[kMaxSlots];
+      for (int i = 0; i < n; ++i) idx[i] = i;
+      std::stable_sort(idx, idx + n, [&](int x, int y) { return a.n_read[x] > a.n_read[y]; });
+      for (int i = 0; i < n; ++i) a.order[i] = (int16_t)idx[i];
     }
     hipError_t e = mfma ? launch_prefill_mfma(d.b, d.dh, a, s) : launch_reader_valu(d.dtype, d.b, d.dh, a, s);
     if (e != hipSuccess) return hip_fail(e, "prefill launch");

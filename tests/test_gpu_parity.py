@@ -173,6 +173,55 @@ def test_prefill_parity(dt, b, H, dh, with_null, with_intra):
     check(out, exp, dtype, "prefill")
 
 
+
+@pytest.mark.parametrize("dh", [32, 64, 128])
+@pytest.mark.parametrize("with_null,with_intra", [(True, True), (False, False)])
+def test_prefill_one_workgroup_mode_bitwise(dh, with_null, with_intra):
+    """A prefill launch of at least 512 (query block, head) pairs reads every
+    split of a pair in one workgroup and folds them itself; the same block
+    served alone (16 pairs) does so only if its read is short (at most
+    1024 / d_h pages), else it runs one workgroup per split and the merge.
+    Both must agree bitwise for every block, and each block must match the
+    oracle.  Query blocks 0..32 of a sequence of 32 blocks (blocks 5 and 17
+    deleted: 0 to 30 memory pages, 1 to 9 splits) and blocks 48, 3 and 20 of
+    a sequence of 48 (up to 48 pages, 13 splits): 36 x 16 = 576 pairs."""
+    say("prefill one-workgroup mode", dh, with_null, with_intra)
+    dtype = torch.bfloat16
+    b, H, J0, J1 = 64, 16, 32, 48
+    g = np.random.default_rng(31 + dh)
+    st = smem.Store(2, J1 + 1, J0 + J1, b, H, dh, dtype)
+    ref = O.Store(2, J1 + 1, b, H, dh)
+    _fill(g, st, ref, 0, range(J0), dtype)
+    _fill(g, st, ref, 1, range(J1), dtype)
+    for j in (5, 17):
+        smem.smem_delete_block(st, 0, j)
+        ref.delete(0, j)
+    seq_ids = [0] * (J0 + 1) + [1, 1, 1]
+    qblk = list(range(J0 + 1)) + [J1, 3, 20]
+    n = len(seq_ids)
+    assert n * H >= 512
+    q = rows(g, (n, b, H, dh), dtype)
+    ki = rows(g, (n, b, H, dh), dtype) if with_intra else None
+    vi = rows(g, (n, b, H, dh), dtype) if with_intra else None
+    nkv = rows(g, (2, H, dh), dtype) if with_null else None
+    d = lambda x: None if x is None else dev(x.reshape(-1, H, dh), dtype)
+    dn = None if nkv is None else dev(nkv, dtype)
+    out = smem.smem_reader_prefill_block(st, seq_ids, qblk, d(q), d(ki), d(vi), dn)
+    for i in range(n):
+        one = smem.smem_reader_prefill_block(st, [seq_ids[i]], [qblk[i]], d(q[i]),
+                                             None if ki is None else d(ki[i]), None if vi is None else d(vi[i]), dn)
+        assert torch.equal(one, out[i * b:(i + 1) * b]), f"slot {i} (block {qblk[i]} of sequence {seq_ids[i]})"
+    exp = O.reader_prefill_block(ref, seq_ids, qblk, q, ki, vi, nkv).reshape(n * b, H, dh)
+    if not with_null and not with_intra:
+        # query block 0 of sequence 0 reads nothing: its output is zero
+        assert not torch.any(out[:b])
+    # each query block is its own attention problem, checked at its own RMS: a
+    # block with few keys has outputs of the values' size, one with a thousand
+    # keys outputs about thirty times smaller
+    for i in range(n):
+        check(out[i * b:(i + 1) * b], exp[i * b:(i + 1) * b], dtype, f"slot {i} (block {qblk[i]})")
+
+
 def test_prefill_empty_key_set_is_zero():
     say("prefill empty")
     st = smem.Store(1, 4, 4, 16, 2, 32, torch.float32)
