@@ -42,22 +42,28 @@ inline int prefill_split_cap(int H) {
   const int c = SMEM_PREFILL_WG_TARGET / (H > 0 ? H : 1);
   return c < 1 ? 1 : (c > kSplitCapPrefill ? kSplitCapPrefill : c);
 }
-// A prefill launch runs one workgroup per (query block, head) pair that
-// folds its splits itself when it has at least kPrefillFusePairs pairs (a
-// block-parallel pass over a long context: the pairs fill the chip, and the
-// split partials would cost more than the longest pair's serial read), or
-// when its longest pair reads at most kPrefillFuseSerial / d_h pages (a short
-// serial read beats a second launch).  Otherwise one workgroup per split and
-// a merge.  Either way the splits and their fold are the same, so the choice
-// never changes a result.
-#ifndef SMEM_PREFILL_FUSE_PAIRS
-#define SMEM_PREFILL_FUSE_PAIRS 512
+// An MFMA prefill launch runs one workgroup per (query block, head) pair that
+// reads the pair's splits in turn and folds them itself when it has at least
+// kFoldPairs pairs (the pairs fill the chip, and the split partials would
+// cost more than the longest pair's serial read), or when its longest pair
+// reads at most kFoldSerial / max(d_h, 64) pages (16 pages up to d_h = 64: a
+// short serial read beats a second launch and the split workgroups' own
+// set-up; measured, a single block over 31 pages is faster split).
+// Otherwise one workgroup per split and a merge.  Either way the splits and
+// their fold are the same, so the choice never changes a result.
+// (Decode keeps the split launch and the merge: its one-query workgroups
+// stream a page per wave at a time, and folding them was measured slower.)
+#ifndef SMEM_FOLD_PAIRS
+#define SMEM_FOLD_PAIRS 512
 #endif
-#ifndef SMEM_PREFILL_FUSE_SERIAL
-#define SMEM_PREFILL_FUSE_SERIAL 1024
+#ifndef SMEM_FOLD_SERIAL
+#define SMEM_FOLD_SERIAL 1024
 #endif
-constexpr int kPrefillFusePairs = SMEM_PREFILL_FUSE_PAIRS;
-constexpr int kPrefillFuseSerial = SMEM_PREFILL_FUSE_SERIAL;
+constexpr int kFoldPairs = SMEM_FOLD_PAIRS;
+constexpr int kFoldSerial = SMEM_FOLD_SERIAL;
+inline bool fold_in_workgroup(long n_pairs, int max_pages, int dh) {
+  return n_pairs >= kFoldPairs || (long)max_pages * (dh > 64 ? dh : 64) <= kFoldSerial;
+}
 // Query slots whose prefill partials the workspace must hold at once.
 constexpr int kPrefillSlotChunk = 16;
 // Row-plane decode: pages per split max(kMinPagesRows, ceil(n_read /

@@ -531,6 +531,15 @@ smem_status smem_reencode_blocks(smem_store* st, const smem_attn_desc* shape, in
   return encode_impl(st, shape, n_blocks, seq_ids, block_idx, q, k, v, out, mask, true, nullptr, s);
 }
 
+// Launch order of a folding prefill: the slots that read the most pages
+// first, so no long pair is left for the tail.
+static void longest_first(ReaderArgs& a) {
+  int idx[kMaxSlots];
+  for (int i = 0; i < a.n_slots; ++i) idx[i] = i;
+  std::stable_sort(idx, idx + a.n_slots, [&](int x, int y) { return a.n_read[x] > a.n_read[y]; });
+  for (int i = 0; i < a.n_slots; ++i) a.order[i] = (int16_t)idx[i];
+}
+
 static smem_status prefill_impl(smem_store* st, const smem_rope* rope, int32_t n_seq, const int32_t* seq_ids,
                                 const int32_t* query_block, const void* q, const void* k_intra,
                                 const void* v_intra, const void* null_kv, void* out, hipStream_t s) {
@@ -560,19 +569,15 @@ static smem_status prefill_impl(smem_store* st, const smem_rope* rope, int32_t n
   const bool mfma = d.dtype == BF16 && d.b == 64;
   std::vector<int> nr(n_seq);
   for (int i = 0; i < n_seq; ++i) nr[i] = n_read_of(st, seq_ids[i], query_block[i]);
-  // One workgroup per (query block, head) folding its own splits, when the
-  // launch has enough pairs to fill the chip or its longest pair reads few
-  // pages (either way it saves the partials and the merge); no rotary variant.
-  auto fold_in_workgroup = [&](int i0, int n) {
+  // One workgroup per (query block, head) folding its own splits (the MFMA
+  // kernel; no rotary variant), when the launch has enough pairs or short reads
+  auto fold_launch = [&](int i0, int n) {
     if (!mfma || rope != nullptr) return false;
-    if ((int64_t)n * d.H >= kPrefillFusePairs) return true;
-    int pm = 0;
-    for (int i = 0; i < n; ++i) pm = std::max(pm, nr[i0 + i]);
-    return (int64_t)pm * d.dh <= kPrefillFuseSerial;
+    return fold_in_workgroup((long)n * d.H, *std::max_element(nr.begin() + i0, nr.begin() + i0 + n), d.dh);
   };
   for (int i0 = 0, n = 0; i0 < n_seq; i0 += n) {
     n = std::min(kMaxSlots, n_seq - i0);
-    const bool fuse = fold_in_workgroup(i0, n);
+    const bool fuse = fold_launch(i0, n);
     if (!fuse) n = std::min(n, prefill_slots(&d));      // the split partials of n slots fit the workspace
     ReaderArgs a;
     memset(&a, 0, sizeof a);
@@ -598,13 +603,7 @@ static smem_status prefill_impl(smem_store* st, const smem_rope* rope, int32_t n
       a.aux[i] = -1;
     }
     a.fuse = fuse;
-    if (a.fuse) {
-      // the longest reads start first, so no long pair is left for the tail
-      int idx[kMaxSlots];
-      for (int i = 0; i < n; ++i) idx[i] = i;
-      std::stable_sort(idx, idx + n, [&](int x, int y) { return a.n_read[x] > a.n_read[y]; });
-      for (int i = 0; i < n; ++i) a.order[i] = (int16_t)idx[i];
-    }
+    if (a.fuse) longest_first(a);
     hipError_t e = mfma ? launch_prefill_mfma(d.b, d.dh, a, s) : launch_reader_valu(d.dtype, d.b, d.dh, a, s);
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
   }

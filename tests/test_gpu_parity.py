@@ -179,9 +179,9 @@ def test_prefill_parity(dt, b, H, dh, with_null, with_intra):
 def test_prefill_one_workgroup_mode_bitwise(dh, with_null, with_intra):
     """A prefill launch of at least 512 (query block, head) pairs reads every
     split of a pair in one workgroup and folds them itself; the same block
-    served alone (16 pairs) does so only if its read is short (at most
-    1024 / d_h pages), else it runs one workgroup per split and the merge.
-    Both must agree bitwise for every block, and each block must match the
+    served alone (16 pairs) does so only if its read is short (at most 16
+    pages, 8 at d_h 128), else it runs one workgroup per split and the
+    merge.  Both must agree bitwise for every block, and each block must match the
     oracle.  Query blocks 0..32 of a sequence of 32 blocks (blocks 5 and 17
     deleted: 0 to 30 memory pages, 1 to 9 splits) and blocks 48, 3 and 20 of
     a sequence of 48 (up to 48 pages, 13 splits): 36 x 16 = 576 pairs."""
