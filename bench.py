@@ -68,7 +68,7 @@ BF16_PEAK_TFLOPS = 2516.6      # MI355X dense bf16 MFMA, published
 # (scaled by a plain copy of known size), keyed by a hash of the decode
 # kernel's sources: a changed kernel reports traffic as null until measured
 # again.  Figures: profiles/k_reader_valu_decode_410M_hbm_traffic.md
-DECODE_TRAFFIC_BYTES = {"690545f1c51fd361": 1.0885e+09}
+DECODE_TRAFFIC_BYTES = {"14938d8a7ab2c12d": 1.0885e+09}
 DECODE_SOURCES = ("paper_2609_32395_amd/csrc/reader_valu.hip", "paper_2609_32395_amd/csrc/common.h")
 
 

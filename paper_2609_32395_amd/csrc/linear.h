@@ -122,6 +122,18 @@ __device__ __forceinline__ f32x4 mfma16(const u32x4& A, const u32x4& B, const f3
                                                  0, 0, 0);
 }
 
+// Launch order -> work item.  Workgroups are dealt to the 8 XCDs round-robin
+// (workgroup i to XCD i mod 8); the grid is padded to a multiple of 8 and
+// item p = (i mod 8) * (T8 / 8) + i / 8, so each XCD takes one contiguous
+// range of items and neighbouring items share that XCD's L2.  Padding
+// workgroups get -1 and exit.
+__device__ __forceinline__ int xcd_order(int i, int T) {
+  const int T8 = (T + 7) & ~7;
+  const int p = (i & 7) * (T8 >> 3) + (i >> 3);
+  return p < T ? p : -1;
+}
+__host__ __device__ constexpr int xcd_grid(int T) { return (T + 7) & ~7; }
+
 // Few rows (one or two blocks): the weights stream from HBM once and the
 // time is load latency, so the reduction chunks run side by side.  A
 // workgroup owns RT x 16 rows and G x 16 output columns and has one wave per
@@ -139,9 +151,8 @@ template <int EPI, class C>
 __global__ void __launch_bounds__(1024) k_linear_skinny(LinArgs a, int row_tiles, int col_groups) {
   constexpr int RT = C::RT, G = C::G, U = C::U, W16 = 16 * G;
   extern __shared__ float part[];   // [n_chunks][16 RT][16 G]
-  const int T = row_tiles * col_groups;
-  int pid = blockIdx.x;
-  if ((T & 7) == 0) pid = (pid & 7) * (T >> 3) + (pid >> 3);
+  const int pid = xcd_order(blockIdx.x, row_tiles * col_groups);
+  if (pid < 0) return;
   const int m0 = (pid % row_tiles) * 16 * RT, n0 = (pid / row_tiles) * W16;
   const int lane = threadIdx.x & 63, c = threadIdx.x >> 6;       // wave c computes chunk c
   const int kofs = (lane >> 4) * 8;
@@ -197,7 +208,7 @@ __global__ void __launch_bounds__(1024) k_linear_skinny(LinArgs a, int row_tiles
 template <int EPI, class C>
 static void launch_skinny_cfg(const LinArgs& a, int nc, hipStream_t s) {
   const int rt = (a.M + 16 * C::RT - 1) / (16 * C::RT), cg = (a.N + 16 * C::G - 1) / (16 * C::G);
-  hipLaunchKernelGGL((k_linear_skinny<EPI, C>), dim3(rt * cg), dim3(64 * nc), (size_t)nc * 1024 * C::RT * C::G, s,
+  hipLaunchKernelGGL((k_linear_skinny<EPI, C>), dim3(xcd_grid(rt * cg)), dim3(64 * nc), (size_t)nc * 1024 * C::RT * C::G, s,
                      a, rt, cg);
 }
 
@@ -251,9 +262,8 @@ __global__ void __launch_bounds__(C::NT, 2 * 4 / C::NW) k_gemm(LinArgs a, int ti
   constexpr int TM = C::TM, TN = C::TN, IA = C::IA, IB = C::IB, STAGE = C::STAGE;
   __shared__ __attribute__((aligned(1024))) uint16_t lds[NS * STAGE];
   // launch order -> tile: consecutive pids of one XCD, then groups of 8 row tiles
-  const int T = tiles_m * tiles_n;
-  int pid = blockIdx.x;
-  if ((T & 7) == 0) pid = (pid & 7) * (T >> 3) + (pid >> 3);
+  const int pid = xcd_order(blockIdx.x, tiles_m * tiles_n);
+  if (pid < 0) return;
   const int per_group = 8 * tiles_n, g0 = (pid / per_group) * 8, gsz = min(tiles_m - g0, 8);
   const int tm = g0 + (pid % per_group) % gsz, tn = (pid % per_group) / gsz;
   const int n0 = tn * BN, m0 = tm * BM;
@@ -334,7 +344,7 @@ __global__ void __launch_bounds__(C::NT, 2 * 4 / C::NW) k_gemm(LinArgs a, int ti
 template <int EPI, class C>
 static void launch_gemm(const LinArgs& a, hipStream_t s) {
   const int tm = (a.M + C::BM - 1) / C::BM, tn = (a.N + C::BN - 1) / C::BN;
-  hipLaunchKernelGGL((k_gemm<EPI, C>), dim3(tm * tn), dim3(C::NT), 0, s, a, tm, tn);
+  hipLaunchKernelGGL((k_gemm<EPI, C>), dim3(xcd_grid(tm * tn)), dim3(C::NT), 0, s, a, tm, tn);
 }
 
 #ifndef GEMM_BIG

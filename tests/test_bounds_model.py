@@ -21,6 +21,27 @@ def pages_per_split(n_read, min_pages, cap=SPLIT_CAP):
     return max(min_pages, -(-n_read // cap))
 
 
+def xcd_grid(T):
+    return (T + 7) // 8 * 8
+
+
+def xcd_order(i, T):
+    """Launch order -> work item of the linear-map kernels: workgroup i runs on
+    XCD i % 8; each XCD takes a contiguous range of items; padding gets -1."""
+    p = (i & 7) * (xcd_grid(T) >> 3) + (i >> 3)
+    return p if p < T else -1
+
+
+def test_xcd_order_is_a_bijection():
+    for T in list(range(1, 70)) + [384, 3142, 50257]:
+        items = [xcd_order(i, T) for i in range(xcd_grid(T))]
+        assert sorted(p for p in items if p >= 0) == list(range(T))
+        per = xcd_grid(T) // 8          # each XCD's items are one contiguous range
+        for x in range(8):
+            mine = [p for i, p in enumerate(items) if i % 8 == x and p >= 0]
+            assert mine == list(range(x * per, min(T, (x + 1) * per)))
+
+
 def page_head_offset(page, h, H, b, dh):
     return (page * H + h) * 2 * b * dh
 
@@ -244,9 +265,10 @@ def _linear_ranges(M, N, K, ldx, ldy, n2, ns, split):
         rt, cg = -(-M // (16 * RT)), -(-N // (16 * G))
         T = rt * cg
         tiles = set()
-        for p in range(T):
-            pid = (p & 7) * (T >> 3) + (p >> 3) if T % 8 == 0 else p
-            tiles.add((pid % rt, pid // rt))
+        for p in range(xcd_grid(T)):
+            pid = xcd_order(p, T)
+            if pid >= 0:
+                tiles.add((pid % rt, pid // rt))
         assert tiles == set(itertools.product(range(rt), range(cg)))
         for r_t, g in tiles:
             m0, n0 = r_t * 16 * RT, g * 16 * G
@@ -280,8 +302,10 @@ def _linear_ranges(M, N, K, ldx, ldy, n2, ns, split):
     tm_, tn_ = -(-M // BM), -(-N // BN)
     T = tm_ * tn_
     seen = set()
-    for p in range(T):                             # launch order -> tile: a bijection onto the tiles
-        pid = (p & 7) * (T >> 3) + (p >> 3) if T % 8 == 0 else p
+    for p in range(xcd_grid(T)):                   # launch order -> tile: a bijection onto the tiles
+        pid = xcd_order(p, T)
+        if pid < 0:
+            continue
         per_group = 8 * tn_
         g0 = (pid // per_group) * 8
         gsz = min(tm_ - g0, 8)
