@@ -49,6 +49,7 @@ Prints ONE JSON line.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import math
 import os
@@ -482,10 +483,30 @@ def stress_workload(args, torch, smem, synth):
         d_t.append(start.elapsed_time(mid))
         p_t.append(mid.elapsed_time(end))
     bytes_step = S * H * NB * b * dh * 2 * 2
+    # canonical export of one sequence (every live page gathered in block order,
+    # the value plane transposed back): 2 GiB read and 2 GiB written, into
+    # preallocated outputs through the C ABI
+    L = smem.lib()
+    n_live = ctypes.c_int32()
+    smem.check_status(L.smem_store_export(st.handle, 0, None, ctypes.byref(n_live), None, None, None))
+    K_out = torch.empty((n_live.value * b, H, dh), dtype=dt, device="cuda")
+    V_out = torch.empty_like(K_out)
+    raw = stream.cuda_stream
+
+    def export(_t=0):
+        smem.check_status(L.smem_store_export(st.handle, 0, None, ctypes.byref(n_live), ctypes.c_void_p(K_out.data_ptr()),
+                                          ctypes.c_void_p(V_out.data_ptr()), ctypes.c_void_p(raw)))
+
+    export()
+    ex_secs = _events_time(export, 4, stream) / 4
+    ex_bytes = 2.0 * 2 * n_live.value * H * b * dh * 2
+    del K_out, V_out
     st.close()
     return dict(decode_ms=secs * 1e3, tokens_per_s=S / secs, decode_gbs=bytes_step / secs / 1e9,
                 memory_rows=NB * b, store_gib=S * NB * H * 2 * b * dh * 2 / 2 ** 30,
-                delete_us_median=float(np.median(d_t)) * 1e3, reinsert_us_median=float(np.median(p_t)) * 1e3)
+                delete_us_median=float(np.median(d_t)) * 1e3, reinsert_us_median=float(np.median(p_t)) * 1e3,
+                export_ms=ex_secs * 1e3, export_gib=ex_bytes / 2 / 2 ** 30, export_gbs=ex_bytes / ex_secs / 1e9,
+                export_hbm_frac=ex_bytes / ex_secs / 1e9 / HBM_PEAK_GBS)
 
 
 def model_workload(args, torch, smem, synth):

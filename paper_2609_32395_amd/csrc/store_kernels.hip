@@ -164,27 +164,44 @@ hipError_t launch_scrub(void* page_base, size_t bytes, hipStream_t s) {
 }
 
 // Canonical export: live entry i, head h -> rows [i*b, (i+1)*b) of k_out and
-// v_out ([rows][H][dh]); the value plane is transposed back through LDS.
+// v_out ([rows][H][dh]).  Every global access is a whole 16-byte chunk: the
+// key plane is copied row chunk by row chunk (a key row is contiguous in the
+// page and in the output); the value plane [dh][b] goes through LDS, where
+// chunk rc of value row d sits at slot rc ^ ((d / E) mod (b / E)), so the
+// gather of one output chunk (E dims of one row) by neighbouring lanes
+// (neighbouring chunks of the row) spreads over the banks.
 template <typename T>
 __global__ void __launch_bounds__(256) k_export(const T* __restrict__ pages, const int32_t* __restrict__ live_page,
                                                  int H, int b, int dh, T* __restrict__ k_out, T* __restrict__ v_out) {
-  extern __shared__ unsigned char smem_raw[];
-  T* tile = reinterpret_cast<T*>(smem_raw);  // [dh][b + 1]
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+  T* tile = reinterpret_cast<T*>(smem_raw);  // [dh][b], 16-byte slots permuted per row
+  constexpr int E = 16 / sizeof(T);          // elements per 16-byte chunk
   const int i = blockIdx.x, h = blockIdx.y;
-  const int page = live_page[i];
-  const T* kp = pages + page_head_offset(page, h, H, b, dh);
+  const T* kp = pages + page_head_offset(live_page[i], h, H, b, dh);
   const T* vp = kp + (size_t)b * dh;
-  const int n = b * dh;
-  for (int e = threadIdx.x; e < n; e += blockDim.x) {
-    const int r = e / dh, d = e % dh;
-    k_out[(((size_t)i * b + r) * H + h) * dh + d] = kp[e];
-    const int dd = e / b, rr = e % b;
-    tile[dd * (b + 1) + rr] = vp[e];
+  const int CR = dh / E, CB = b / E;         // chunks per output row, per value row
+  const size_t rs = (size_t)H * dh;          // output row stride
+  T* ko = k_out + ((size_t)i * b * H + h) * dh;
+  T* vo = v_out + ((size_t)i * b * H + h) * dh;
+  for (int q = threadIdx.x; q < b * CR; q += blockDim.x) {
+    const int r = q / CR, cc = q % CR;
+    *(u32x4*)(ko + r * rs + cc * E) = *(const u32x4*)(kp + r * dh + cc * E);
+  }
+  for (int q = threadIdx.x; q < dh * CB; q += blockDim.x) {
+    const int d = q / CB, rc = q % CB;
+    *(u32x4*)(tile + d * b + ((rc ^ ((d / E) % CB)) * E)) = *(const u32x4*)(vp + d * b + rc * E);
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < n; e += blockDim.x) {
-    const int r = e / dh, d = e % dh;
-    v_out[(((size_t)i * b + r) * H + h) * dh + d] = tile[d * (b + 1) + r];
+  for (int q = threadIdx.x; q < b * CR; q += blockDim.x) {
+    const int r = q / CR, cc = q % CR;
+    const int off = ((r / E) ^ (cc % CB)) * E + r % E;
+    union {
+      u32x4 u;
+      T e[E];
+    } v;
+#pragma unroll
+    for (int j = 0; j < E; ++j) v.e[j] = tile[(cc * E + j) * b + off];
+    *(u32x4*)(vo + r * rs + cc * E) = v.u;
   }
 }
 
@@ -192,13 +209,11 @@ hipError_t launch_export(int dtype, const void* pages, const int32_t* live_page_
                          int H, int b, int dh, void* k_out, void* v_out, hipStream_t s) {
   if (n_live <= 0) return hipSuccess;
   if (dtype == F32) {
-    size_t lds = (size_t)dh * (b + 1) * sizeof(float);
-    hipLaunchKernelGGL(k_export<float>, dim3(n_live, H), dim3(256), lds, s, (const float*)pages, live_page_seq,
-                       H, b, dh, (float*)k_out, (float*)v_out);
+    hipLaunchKernelGGL(k_export<float>, dim3(n_live, H), dim3(256), (size_t)dh * b * sizeof(float), s,
+                       (const float*)pages, live_page_seq, H, b, dh, (float*)k_out, (float*)v_out);
   } else {
-    size_t lds = (size_t)dh * (b + 1) * sizeof(uint16_t);
-    hipLaunchKernelGGL(k_export<uint16_t>, dim3(n_live, H), dim3(256), lds, s, (const uint16_t*)pages,
-                       live_page_seq, H, b, dh, (uint16_t*)k_out, (uint16_t*)v_out);
+    hipLaunchKernelGGL(k_export<uint16_t>, dim3(n_live, H), dim3(256), (size_t)dh * b * sizeof(uint16_t), s,
+                       (const uint16_t*)pages, live_page_seq, H, b, dh, (uint16_t*)k_out, (uint16_t*)v_out);
   }
   return hipGetLastError();
 }

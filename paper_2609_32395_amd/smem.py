@@ -138,6 +138,11 @@ def _check(code: int):
         raise SmemError(code, msg)
 
 
+def check_status(code: int):
+    """Raise SmemError for a status returned by a direct call into lib()."""
+    _check(code)
+
+
 def _i32(xs):
     arr = (ctypes.c_int32 * max(1, len(xs)))(*[int(x) for x in xs])
     return arr

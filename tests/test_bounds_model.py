@@ -441,3 +441,34 @@ def test_prefill_page_ring_indexing(dh, ns):
         for kt in range(4):
             groups = {((r * KRB + ((c ^ kswz(r)) << 4)) % 256) // 16 for r in range(kt * 16, kt * 16 + 16)}
             assert len(groups) == 16
+
+
+@pytest.mark.parametrize("b,dh,es", SHAPES)
+def test_export_indexing_and_transpose(b, dh, es):
+    """k_export: 16-byte chunks of the key plane and of the output rows stay in
+    their buffers; the value plane's LDS slots (chunk rc of row d at
+    rc ^ ((d / E) mod (b / E))) are a permutation of each row, and the gather
+    of output chunk (r, cc) reads exactly value (d = cc*E + j, r) for j < E."""
+    E = 16 // es
+    CR, CB = dh // E, b // E
+    for H, n_pages, n_live in [(1, 1, 1), (16, 4096, 4096), (4, 9, 5)]:
+        pool = n_pages * H * 2 * b * dh
+        base = page_head_offset(n_pages - 1, H - 1, H, b, dh)
+        assert base + b * dh + (dh - 1) * b + (CB - 1) * E + E - 1 < pool          # value plane chunk reads
+        assert base + (b - 1) * dh + (CR - 1) * E + E - 1 < pool                    # key plane chunk reads
+        out = n_live * b * H * dh
+        assert ((n_live - 1) * b * H + H - 1) * dh + (b - 1) * H * dh + (CR - 1) * E + E - 1 < out
+    tile = {}
+    for d in range(dh):
+        for rc in range(CB):
+            slot = rc ^ ((d // E) % CB)
+            assert 0 <= slot < CB
+            for e in range(E):
+                pos = d * b + slot * E + e
+                assert pos < dh * b and pos not in tile
+                tile[pos] = (d, rc * E + e)
+    assert len(tile) == dh * b
+    for r in range(b):
+        for cc in range(CR):
+            off = ((r // E) ^ (cc % CB)) * E + r % E
+            assert [tile[(cc * E + j) * b + off] for j in range(E)] == [(cc * E + j, r) for j in range(E)]
