@@ -510,6 +510,79 @@ __device__ __forceinline__ void wait_pages(int ahead) {
   else wait_vm<0>();
 }
 
+// The null row, one always-visible key/value pair per head, as the first key
+// of the final split (m, l, o start empty).
+template <int DH, bool ROPE>
+__device__ __forceinline__ void null_row(const ReaderArgs& a, int slot, int h, const bf16x8 (&qf)[DH / 32], int lane,
+                                         float& m, float& l, floatx4 (&o)[DH / 16]) {
+  const uint16_t* nk = (const uint16_t*)a.null_kv + (size_t)h * DH + (lane >> 4) * 8;
+  const uint16_t* nv = (const uint16_t*)a.null_kv + ((size_t)a.H + h) * DH;
+  bf16x8 qn[DH / 32];
+  if constexpr (ROPE) {
+    rope_q<DH>(qn, qf, a.rope + (size_t)min(a.qblk[slot], a.rope_clip) * DH, lane);
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < DH / 32; ++kk) qn[kk] = qf[kk];
+  }
+  float x = 0.f;
+#pragma unroll
+  for (int kk = 0; kk < DH / 32; ++kk) {
+    const u32x4 kr = *(const u32x4*)(nk + kk * 32);
+    float kf[8];
+    Chunk<uint16_t>::unpack(kr, kf);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x += (float)qn[kk][j] * kf[j];
+  }
+  x = qsum(x) * a.scale_log2;
+  m = x;
+  l = ((lane >> 4) == 0) ? 1.f : 0.f;
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[dt][i] = bf16_bits_to_f32(nv[dt * 16 + (lane >> 4) * 4 + i]);
+  }
+}
+
+// Fold one split's (m, l, o) into the running state (fm, fl, acc) -- the
+// merge's arithmetic -- and start the next split empty.  l is this lane's
+// share; the split's weight sum is its sum over the four lanes of the query.
+template <int DH>
+__device__ __forceinline__ void fold_split(bool first, float& m, float& l, floatx4 (&o)[DH / 16], float& fm,
+                                           float& fl, floatx4 (&acc)[DH / 16]) {
+  const float ls = qsum(l);
+  if (first) {
+    fm = m;
+    fl = ls;
+#pragma unroll
+    for (int dt = 0; dt < DH / 16; ++dt) acc[dt] = o[dt];
+  } else {
+    const FoldScale c = fold_scale(fm, m);
+    fl = fold_value(fl, c, ls);
+#pragma unroll
+    for (int dt = 0; dt < DH / 16; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[dt][i] = fold_value(acc[dt][i], c, o[dt][i]);
+  }
+  m = -INFINITY;
+  l = 0.f;
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+}
+
+// Output rows of one wave: o * (1 / l) as bf16, l the weight sum (0 -> 0).
+template <int DH>
+__device__ __forceinline__ void store_out(uint16_t* orow, const floatx4 (&o)[DH / 16], float l, int lane) {
+  const float inv = (l > 0.f) ? 1.f / l : 0.f;
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) {
+    const int d0 = dt * 16 + (lane >> 4) * 4;
+    uint16_t r4[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r4[i] = f32_to_bf16_bits(o[dt][i] * inv);
+    *(u32x2*)(orow + d0) = u32x2{(uint32_t)r4[0] | ((uint32_t)r4[1] << 16), (uint32_t)r4[2] | ((uint32_t)r4[3] << 16)};
+  }
+}
+
 // One (query block, head) over its splits.  FUSE = false: workgroup
 // (h, split, slot) reads one split and writes its partial (m, l, o) -- or,
 // with no memory split, the output.  FUSE = true: workgroup (h, 0, z) reads
@@ -541,27 +614,6 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
   // FUSE: the folded state of the splits read so far
   [[maybe_unused]] floatx4 acc[DH / 16];
   [[maybe_unused]] float fm = 0.f, fl = 0.f;
-  // close the current split: fold its (m, l, o) into the state, start afresh
-  [[maybe_unused]] auto fold = [&](bool first) {
-    const float ls = qsum(l);
-    if (first) {
-      fm = m;
-      fl = ls;
-#pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt) acc[dt] = o[dt];
-    } else {
-      const FoldScale c = fold_scale(fm, m);
-      fl = fold_value(fl, c, ls);
-#pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc[dt][i] = fold_value(acc[dt][i], c, o[dt][i]);
-    }
-    m = -INFINITY;
-    l = 0.f;
-#pragma unroll
-    for (int dt = 0; dt < DH / 16; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-  };
 
   if (split < nms) {
     using R = PageRing<DH>;
@@ -636,7 +688,7 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
       pv_ring<DH>(o, tile, s, lane);
       if constexpr (FUSE) {
         if (pi + 1 == split_end || pi + 1 == p1) {
-          fold(split_end == pps);
+          fold_split<DH>(split_end == pps, m, l, o, fm, fl, acc);
           split_end += pps;
         }
       }
@@ -644,35 +696,7 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
     if constexpr (FUSE) __syncthreads();   // every wave is done with the ring before the tiles reuse it
   }
   if (FUSE || split == nms) {
-    if (a.null_kv != nullptr) {
-      // the null row: one always-visible key/value pair per head
-      const uint16_t* nk = (const uint16_t*)a.null_kv + (size_t)h * DH + (lane >> 4) * 8;
-      const uint16_t* nv = (const uint16_t*)a.null_kv + ((size_t)a.H + h) * DH;
-      bf16x8 qn[DH / 32];
-      if constexpr (ROPE) {
-        rope_q<DH>(qn, qf, a.rope + (size_t)min(a.qblk[slot], a.rope_clip) * DH, lane);
-      } else {
-#pragma unroll
-        for (int kk = 0; kk < DH / 32; ++kk) qn[kk] = qf[kk];
-      }
-      float x = 0.f;
-#pragma unroll
-      for (int kk = 0; kk < DH / 32; ++kk) {
-        const u32x4 kr = *(const u32x4*)(nk + kk * 32);
-        float kf[8];
-        Chunk<uint16_t>::unpack(kr, kf);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) x += (float)qn[kk][j] * kf[j];
-      }
-      x = qsum(x) * a.scale_log2;
-      m = x;
-      l = ((lane >> 4) == 0) ? 1.f : 0.f;
-#pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) o[dt][i] = bf16_bits_to_f32(nv[dt * 16 + (lane >> 4) * 4 + i]);
-      }
-    }
+    if (a.null_kv != nullptr) null_row<DH, ROPE>(a, slot, h, qf, lane, m, l, o);
     if (a.k_in != nullptr) {
       const size_t base = (size_t)slot * BT * rs + (size_t)h * DH;
       if constexpr (ROPE) rope_q<DH>(qf, qf, a.rope + (size_t)qrow * DH, lane);
@@ -687,33 +711,13 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
   }
   const size_t qs = (size_t)slot * BT + qrow;
   if (FUSE && nms > 0) {
-    fold(false);
-    const float inv = (fl > 0.f) ? 1.f / fl : 0.f;
-    uint16_t* orow = (uint16_t*)a.out + qs * rs + (size_t)h * DH;
-#pragma unroll
-    for (int dt = 0; dt < DH / 16; ++dt) {
-      const int d0 = dt * 16 + (lane >> 4) * 4;
-      uint16_t r4[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) r4[i] = f32_to_bf16_bits(acc[dt][i] * inv);
-      *(u32x2*)(orow + d0) = u32x2{(uint32_t)r4[0] | ((uint32_t)r4[1] << 16),
-                                   (uint32_t)r4[2] | ((uint32_t)r4[3] << 16)};
-    }
+    fold_split<DH>(false, m, l, o, fm, fl, acc);
+    store_out<DH>((uint16_t*)a.out + qs * rs + (size_t)h * DH, acc, fl, lane);
     return;
   }
   l = qsum(l);
   if (nms == 0) {
-    const float inv = (l > 0.f) ? 1.f / l : 0.f;
-    uint16_t* orow = (uint16_t*)a.out + qs * rs + (size_t)h * DH;
-#pragma unroll
-    for (int dt = 0; dt < DH / 16; ++dt) {
-      const int d0 = dt * 16 + (lane >> 4) * 4;
-      uint16_t r4[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) r4[i] = f32_to_bf16_bits(o[dt][i] * inv);
-      *(u32x2*)(orow + d0) = u32x2{(uint32_t)r4[0] | ((uint32_t)r4[1] << 16),
-                                   (uint32_t)r4[2] | ((uint32_t)r4[3] << 16)};
-    }
+    store_out<DH>((uint16_t*)a.out + qs * rs + (size_t)h * DH, o, l, lane);
   } else {
     float* part = a.ws + ((qs * a.H + h) * kSplitStride + split) * (DH + 4);
 #pragma unroll
