@@ -6,7 +6,10 @@
 // in one pass.  Reader prefill (Section 3.1, block-skip serving): one
 // workgroup per (query block, head, split); it streams whole memory pages of
 // its split with an online softmax, and the split after the memory holds the
-// null row and the in-block causal tile.  Splits merge in split order.
+// null row and the in-block causal tile.  Splits merge in split order -- by
+// the merge launch, or, in a launch of many query blocks or short reads, by
+// one workgroup per (query block, head) that reads all its splits and folds
+// them with the merge's own arithmetic.
 //
 // Both compute S^T = K Q^T and O^T = V^T P^T with
 // __builtin_amdgcn_mfma_f32_16x16x32_bf16 (A: 16 rows x 32 k, B: 32 k x 16
