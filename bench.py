@@ -469,18 +469,19 @@ def stress_workload(args, torch, smem, synth):
     secs = _events_time(step, n, stream) / n
     er = synth.rng(args.seed, w.wid, synth.ROLE_EDIT, 2, 0, 0)
     start, mid, end = (torch.cuda.Event(enable_timing=True) for _ in range(3))
-    d_t, p_t = [], []
-    for _ in range(32):
+    d_t, p_t, ds_t = [], [], []
+    for it in range(32):
         s, j = int(er.integers(0, S)), int(er.integers(0, NB))
         kj, vj = synth.memory_block_device(w, args.seed, s, j)
+        scrub = it % 2 == 1                  # every other delete also zeroes the freed page
         torch.cuda.synchronize()
         start.record(stream)
-        smem.smem_delete_block(st, s, j)
+        smem.smem_delete_block(st, s, j, scrub=scrub)
         mid.record(stream)
         smem.smem_store_put_block(st, s, j, kj, vj)
         end.record(stream)
         end.synchronize()
-        d_t.append(start.elapsed_time(mid))
+        (ds_t if scrub else d_t).append(start.elapsed_time(mid))
         p_t.append(mid.elapsed_time(end))
     bytes_step = S * H * NB * b * dh * 2 * 2
     # canonical export of one sequence (every live page gathered in block order,
@@ -505,6 +506,7 @@ def stress_workload(args, torch, smem, synth):
     return dict(decode_ms=secs * 1e3, tokens_per_s=S / secs, decode_gbs=bytes_step / secs / 1e9,
                 memory_rows=NB * b, store_gib=S * NB * H * 2 * b * dh * 2 / 2 ** 30,
                 delete_us_median=float(np.median(d_t)) * 1e3, reinsert_us_median=float(np.median(p_t)) * 1e3,
+                delete_scrub_us_median=float(np.median(ds_t)) * 1e3, page_bytes=H * 2 * b * dh * 2,
                 export_ms=ex_secs * 1e3, export_gib=ex_bytes / 2 / 2 ** 30, export_gbs=ex_bytes / ex_secs / 1e9,
                 export_hbm_frac=ex_bytes / ex_secs / 1e9 / HBM_PEAK_GBS)
 
