@@ -222,6 +222,36 @@ def test_prefill_one_workgroup_mode_bitwise(dh, with_null, with_intra):
         check(out[i * b:(i + 1) * b], exp[i * b:(i + 1) * b], dtype, f"slot {i} (block {qblk[i]})")
 
 
+
+def test_prefill_fold_with_odd_split_sizes_bitwise():
+    """32 heads of 32 (the model's heads): splits of max(4, ceil(n/16)) pages,
+    so reads of 65-79 pages take splits of 5 pages.  Query blocks 60..80 of one
+    sequence in one launch (672 pairs: one workgroup per pair folds its
+    splits) equal each block served alone (32 pairs over more than 16 pages:
+    split launch and merge), bitwise; a sample matches the oracle."""
+    say("prefill fold, odd split sizes")
+    dtype = torch.bfloat16
+    b, H, dh, J = 64, 32, 32, 80
+    g = np.random.default_rng(61)
+    st = smem.Store(1, J + 1, J, b, H, dh, dtype)
+    ref = O.Store(1, J + 1, b, H, dh)
+    _fill(g, st, ref, 0, range(J), dtype)
+    qblk = list(range(60, J + 1))
+    n = len(qblk)
+    q, ki, vi = (rows(g, (n, b, H, dh), dtype) for _ in range(3))
+    nkv = rows(g, (2, H, dh), dtype)
+    d = lambda x: dev(x.reshape(-1, H, dh), dtype)
+    dn = dev(nkv, dtype)
+    out = smem.smem_reader_prefill_block(st, [0] * n, qblk, d(q), d(ki), d(vi), dn)
+    for i in range(n):
+        one = smem.smem_reader_prefill_block(st, [0], [qblk[i]], d(q[i]), d(ki[i]), d(vi[i]), dn)
+        assert torch.equal(one, out[i * b:(i + 1) * b]), f"block {qblk[i]}"
+    sample = [0, 5, 12, 20]
+    exp = O.reader_prefill_block(ref, [0] * len(sample), [qblk[i] for i in sample], q[sample], ki[sample],
+                                 vi[sample], nkv)
+    for k, i in enumerate(sample):
+        check(out[i * b:(i + 1) * b], exp[k].reshape(b, H, dh), dtype, f"block {qblk[i]}")
+
 def test_prefill_empty_key_set_is_zero():
     say("prefill empty")
     st = smem.Store(1, 4, 4, 16, 2, 32, torch.float32)
