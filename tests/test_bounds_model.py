@@ -291,7 +291,8 @@ def _linear_ranges(M, N, K, ldx, ldy, n2, ns, split):
         return hi
     big = -(-N // 128) * -(-M // 128) >= 256
     BM = BN = 128 if big else 64
-    BK, NS, WAVES_M, WAVES_N = 64, 2, 2, 2         # GemmCfg of both tile sizes
+    BK, WAVES_M, WAVES_N = 64, 2, 2                # GemmCfg of every tile size
+    NS = 4 if not big and K >= 3072 else 2         # mid tiles over a long reduction keep four stages
     NW = WAVES_M * WAVES_N
     WM, WN = BM // WAVES_M, BN // WAVES_N
     CPR, RPI, R256 = BK // 8, 1024 // (BK * 2), 256 // (BK * 2)
