@@ -212,15 +212,23 @@ static void launch_skinny_cfg(const LinArgs& a, int nc, hipStream_t s) {
                      a, rt, cg);
 }
 
-// The largest tile that still gives at least 256 workgroups (one per CU):
-// wide maps reuse each x and W tile more, narrow ones need the parallelism.
-// All three compute every output in the same order.
+// The widest tile that still gives at least 192 workgroups: every workgroup
+// reads its rows of x and its columns of W whole, and reads issued at the
+// same time by several workgroups each cost close to a full read, so wider
+// tiles (fewer duplicated reads) win until too few workgroups remain to keep
+// the loads in flight (measured on the 64-row maps of the three model
+// scales).  Partial sums need n_chunks x RT x G KiB of LDS (at most 64).  All
+// tilings compute every output in the same order.
 template <int EPI>
 static void launch_skinny(const LinArgs& a, hipStream_t s) {
   const int nc = (a.K + lin_chunk(a.K) - 1) / lin_chunk(a.K);
-  auto wgs = [&](int rows, int cols) { return (long)((a.M + rows - 1) / rows) * ((a.N + cols - 1) / cols); };
-  if (wgs(32, 32) >= 256) launch_skinny_cfg<EPI, SkinnyCfg<2, 2, 4>>(a, nc, s);
-  else if (wgs(16, 32) >= 256) launch_skinny_cfg<EPI, SkinnyCfg<1, 2, 8>>(a, nc, s);
+  auto fits = [&](int rt, int g) {
+    const long wgs = (long)((a.M + 16 * rt - 1) / (16 * rt)) * ((a.N + 16 * g - 1) / (16 * g));
+    return wgs >= 192 && nc * rt * g <= 64;
+  };
+  if (fits(2, 4)) launch_skinny_cfg<EPI, SkinnyCfg<2, 4, 4>>(a, nc, s);
+  else if (fits(2, 2)) launch_skinny_cfg<EPI, SkinnyCfg<2, 2, 4>>(a, nc, s);
+  else if (fits(1, 2)) launch_skinny_cfg<EPI, SkinnyCfg<1, 2, 8>>(a, nc, s);
   else launch_skinny_cfg<EPI, SkinnyCfg<1, 1, 8>>(a, nc, s);
 }
 

@@ -256,10 +256,10 @@ def _linear_ranges(M, N, K, ldx, ldy, n2, ns, split):
 
     lanes = (0, 15, 16, 47, 48, 63)
     if M <= 128:
-        wgs = lambda r, c: -(-M // r) * -(-N // c)
-        RT, G = (2, 2) if wgs(32, 32) >= 256 else (1, 2) if wgs(16, 32) >= 256 else (1, 1)   # launch_skinny
         KS, CS = K // 32, lin_chunk(K) // 32
         NC = -(-KS // CS)
+        fits = lambda rt, g: -(-M // (16 * rt)) * -(-N // (16 * g)) >= 192 and NC * rt * g <= 64
+        RT, G = next(c for c in ((2, 4), (2, 2), (1, 2), (1, 1)) if c == (1, 1) or fits(*c))   # launch_skinny
         PART = 256 * RT * G                      # floats per chunk
         assert NC <= 16 and NC * PART * 4 <= 64 * 1024
         rt, cg = -(-M // (16 * RT)), -(-N // (16 * G))
