@@ -5,6 +5,8 @@
 // k-values are 16 contiguous bytes of an x row and of a W row.
 #pragma once
 
+#include <algorithm>
+
 #include "common.h"
 
 namespace smem {
@@ -22,6 +24,9 @@ struct LinArgs {
   uint16_t* y1;        // kLinSplit: columns [ns, 2ns) -> y1, [2ns, 3ns) -> y2 (each [M][ns])
   uint16_t* y2;
   float* yf;           // kLinF32: [M][ldy]
+  const uint16_t* lng; // y = LN(x) W^T when set: LayerNorm gain and bias [K]
+  const uint16_t* lnb;
+  uint16_t* lnout;     // many rows: LN(x) written here ([M][K]) before the map
   int32_t M, N, K, ldx, ldy, n2, ns;
 };
 
@@ -49,6 +54,90 @@ __device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.f + er
 // row's result independent of the other rows in the call (block-skip serving
 // reproduces the cold pass bit for bit).
 __host__ __device__ constexpr int lin_chunk(int K) { return 256 * ((K + 256 * 16 - 1) / (256 * 16)); }
+
+// LayerNorm of a row of width d (d % 64 == 0, d <= 2048), eps 1e-5, with the
+// statistics summed in one fixed order, so the stand-alone kernel below and
+// the few-row map that normalizes its own x rows give the same bits.  The row
+// is cut as a linear map cuts K: chunks of 256, each of 32-wide steps, each
+// step of four 8-wide groups.  The partial of (chunk, group) adds its values
+// in ascending k; a chunk's four partials add as (g0 + g1) + (g2 + g3); the
+// chunk totals add in ascending chunk order from zero.  mean = total / d; the
+// second moment sums (x - mean)^2 the same way; rstd = 1 / sqrt(m2 / d + eps).
+__device__ __forceinline__ float ln_sum8(const u32x4& c, float s) {
+  float f[8];
+  Chunk<uint16_t>::unpack(c, f);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) s += f[e];
+  return s;
+}
+__device__ __forceinline__ float ln_sq8(const u32x4& c, float mean, float s) {
+  float f[8];
+  Chunk<uint16_t>::unpack(c, f);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float t = f[e] - mean;
+    s += t * t;
+  }
+  return s;
+}
+__device__ __forceinline__ float ln_rstd(float m2, int d) { return 1.f / sqrtf(m2 / d + 1e-5f); }
+__device__ __forceinline__ u32x4 ln_apply8(const u32x4& x, const u32x4& g, const u32x4& b, float mean, float rstd) {
+  float xf[8], gf[8], bf[8];
+  Chunk<uint16_t>::unpack(x, xf);
+  Chunk<uint16_t>::unpack(g, gf);
+  Chunk<uint16_t>::unpack(b, bf);
+  uint32_t w[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float y0 = (xf[2 * e] - mean) * rstd * gf[2 * e] + bf[2 * e];
+    const float y1 = (xf[2 * e + 1] - mean) * rstd * gf[2 * e + 1] + bf[2 * e + 1];
+    w[e] = (uint32_t)f32_to_bf16_bits(y0) | ((uint32_t)f32_to_bf16_bits(y1) << 16);
+  }
+  return u32x4{w[0], w[1], w[2], w[3]};
+}
+
+// Stand-alone LayerNorm (rows x[row * ldx .. + d) -> y[row * ldy ..)): one
+// half-wave per row, lane 4c + g holding group g of chunk c, 8 rows per
+// 256-thread block.
+__global__ void __launch_bounds__(256) k_ln_rows(const uint16_t* __restrict__ x, int ldx,
+                                                 const uint16_t* __restrict__ g, const uint16_t* __restrict__ b,
+                                                 uint16_t* __restrict__ y, int ldy, int rows, int d) {
+  const int lane = threadIdx.x & 31;
+  const int row = blockIdx.x * 8 + (threadIdx.x >> 5);
+  if (row >= rows) return;
+  const int KS = d / 32, NC = (KS + 7) / 8;
+  const int c = lane >> 2, k0 = 256 * c + 8 * (lane & 3);
+  const int nt = c < NC ? min(8, KS - 8 * c) : 0;
+  const uint16_t* xr = x + (size_t)row * ldx + k0;
+  u32x4 v[8];
+  float s = 0.f;
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+    if (t < nt) {
+      v[t] = *(const u32x4*)(xr + 32 * t);
+      s = ln_sum8(v[t], s);
+    }
+  s += __shfl_xor(s, 1, 32);
+  s += __shfl_xor(s, 2, 32);
+  float tot = 0.f;
+  for (int q = 0; q < NC; ++q) tot += __shfl(s, 4 * q, 32);
+  const float mean = tot / d;
+  float m2 = 0.f;
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+    if (t < nt) m2 = ln_sq8(v[t], mean, m2);
+  m2 += __shfl_xor(m2, 1, 32);
+  m2 += __shfl_xor(m2, 2, 32);
+  float tot2 = 0.f;
+  for (int q = 0; q < NC; ++q) tot2 += __shfl(m2, 4 * q, 32);
+  const float rstd = ln_rstd(tot2, d);
+  uint16_t* yr = y + (size_t)row * ldy + k0;
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+    if (t < nt)
+      *(u32x4*)(yr + 32 * t) =
+          ln_apply8(v[t], *(const u32x4*)(g + k0 + 32 * t), *(const u32x4*)(b + k0 + 32 * t), mean, rstd);
+}
 
 template <int EPI>
 __device__ __forceinline__ void lin_store(const LinArgs& a, int m, int n, float v) {
@@ -205,6 +294,145 @@ __global__ void __launch_bounds__(1024) k_linear_skinny(LinArgs a, int row_tiles
   }
 }
 
+// Few rows with the LayerNorm fused (y = LN(x) W^T, K <= 2048, so every
+// chunk is 256 wide, 8 steps): each wave loads its chunk of the x rows whole,
+// the chunk partials of the row statistics meet in LDS in the fixed order of
+// the stand-alone kernel, and the rows are normalized in registers before the
+// MFMAs; the first U steps of W, issued with the x loads, are in flight
+// meanwhile, and each step's W registers are refilled with step t + U once
+// its MFMAs are issued.  The sums
+// are the same as k_linear_skinny's on LN(x) rows, so the output is bitwise
+// the unfused pair's.
+// Dynamic LDS: gain and bias (4 K bytes) and two statistics planes of
+// n_chunks x 16 RT floats, then, in the same space, n_chunks x RT x G KiB of
+// partial sums.
+// An empty asm that claims to rewrite the packed x rows, so the compiler
+// unpacks them again where they are next used instead of keeping 8 floats
+// per register live across the statistics barriers.
+template <int T, int R>
+__device__ __forceinline__ void opaque(u32x4 (&X)[T][R]) {
+#pragma unroll
+  for (int t = 0; t < T; ++t)
+#pragma unroll
+    for (int i = 0; i < R; ++i) asm volatile("" : "+v"(X[t][i]));
+}
+
+template <int EPI, class C>
+__global__ void __launch_bounds__(512) k_linear_skinny_ln(LinArgs a, int row_tiles, int col_groups) {
+  constexpr int RT = C::RT, G = C::G, U = C::U, W16 = 16 * G;
+  extern __shared__ float part[];   // [n_chunks][16 RT][16 G]
+  const int pid = xcd_order(blockIdx.x, row_tiles * col_groups);
+  if (pid < 0) return;
+  const int m0 = (pid % row_tiles) * 16 * RT, n0 = (pid / row_tiles) * W16;
+  const int lane = threadIdx.x & 63;
+  const int c = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave c computes chunk c
+  const int kofs = (lane >> 4) * 8;
+  const int KS = a.K / 32, NC = (KS + 7) / 8;
+  uint16_t* gb = (uint16_t*)part;                                // gain [K], bias [K] (until the MFMAs)
+  float* st0 = (float*)(gb + 2 * a.K);                           // [n_chunks][16 RT] sums, then second moments
+  float* st1 = st0 + NC * 16 * RT;
+  const int s0 = c * 8, ns = min(8, KS - s0);
+  const uint16_t* ap[RT];
+  const uint16_t* bp[G];
+#pragma unroll
+  for (int i = 0; i < RT; ++i) ap[i] = a.x + (size_t)min(m0 + i * 16 + (lane & 15), a.M - 1) * a.ldx + kofs;
+#pragma unroll
+  for (int j = 0; j < G; ++j) bp[j] = lin_wrow(a, min(n0 + j * 16 + (lane & 15), a.N - 1)) + kofs;
+  u32x4 X[8][RT], B[U][G];
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+#pragma unroll
+    for (int i = 0; i < RT; ++i) X[t][i] = *(const u32x4*)(ap[i] + (s0 + min(t, ns - 1)) * 32);
+  const int q8 = threadIdx.x * 8;
+  u32x4 g16 = {0, 0, 0, 0}, b16 = {0, 0, 0, 0};
+  if (q8 < a.K) {
+    g16 = *(const u32x4*)(a.lng + q8);
+    b16 = *(const u32x4*)(a.lnb + q8);
+  }
+#pragma unroll
+  for (int t = 0; t < U; ++t)
+#pragma unroll
+    for (int j = 0; j < G; ++j) B[t][j] = *(const u32x4*)(bp[j] + (s0 + min(t, ns - 1)) * 32);
+  if (q8 < a.K) {
+    *(u32x4*)(gb + q8) = g16;
+    *(u32x4*)(gb + a.K + q8) = b16;
+  }
+  float mean[RT], rstd[RT];
+#pragma unroll
+  for (int i = 0; i < RT; ++i) {
+    float v = 0.f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      if (t < ns) v = ln_sum8(X[t][i], v);
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    if (lane < 16) st0[c * 16 * RT + i * 16 + lane] = v;
+  }
+  opaque(X);
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < RT; ++i) {
+    float tot = 0.f;
+    for (int q = 0; q < NC; ++q) tot += st0[q * 16 * RT + i * 16 + (lane & 15)];
+    mean[i] = tot / a.K;
+    float v = 0.f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      if (t < ns) v = ln_sq8(X[t][i], mean[i], v);
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    if (lane < 16) st1[c * 16 * RT + i * 16 + lane] = v;
+  }
+  opaque(X);
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < RT; ++i) {
+    float tot = 0.f;
+    for (int q = 0; q < NC; ++q) tot += st1[q * 16 * RT + i * 16 + (lane & 15)];
+    rstd[i] = ln_rstd(tot, a.K);
+  }
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    const int k = (s0 + min(t, ns - 1)) * 32 + kofs;
+    const u32x4 g8 = *(const u32x4*)(gb + k), b8 = *(const u32x4*)(gb + a.K + k);
+#pragma unroll
+    for (int i = 0; i < RT; ++i) X[t][i] = ln_apply8(X[t][i], g8, b8, mean[i], rstd[i]);
+  }
+  __syncthreads();                       // gain, bias and statistics are read; part may be written
+  f32x4 acc[RT][G];
+#pragma unroll
+  for (int i = 0; i < RT; ++i)
+#pragma unroll
+    for (int j = 0; j < G; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    if (t < ns) {
+#pragma unroll
+      for (int i = 0; i < RT; ++i)
+#pragma unroll
+        for (int j = 0; j < G; ++j) acc[i][j] = mfma16(B[t % U][j], X[t][i], acc[i][j]);
+    }
+    if (t + U < 8) {                     // refill this step's W registers with step t + U
+#pragma unroll
+      for (int j = 0; j < G; ++j) B[t % U][j] = *(const u32x4*)(bp[j] + (s0 + min(t + U, ns - 1)) * 32);
+    }
+  }
+  float* pc = part + c * (256 * RT * G);
+#pragma unroll
+  for (int i = 0; i < RT; ++i)
+#pragma unroll
+    for (int j = 0; j < G; ++j)
+      *(f32x4*)(pc + (i * 16 + (lane & 15)) * W16 + j * 16 + 4 * (lane >> 4)) = acc[i][j];
+  __syncthreads();
+  for (int q = threadIdx.x; q < 64 * RT * G; q += blockDim.x) {
+    const int row = q / (4 * G), c0 = (q % (4 * G)) * 4;
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    for (int ch = 0; ch < NC; ++ch) v += *(const f32x4*)(part + ch * (256 * RT * G) + row * W16 + c0);
+    const int m = m0 + row;
+    if (m < a.M) lin_store4<EPI>(a, m, n0 + c0, v);
+  }
+}
+
 template <int EPI, class C>
 static void launch_skinny_cfg(const LinArgs& a, int nc, hipStream_t s) {
   const int rt = (a.M + 16 * C::RT - 1) / (16 * C::RT), cg = (a.N + 16 * C::G - 1) / (16 * C::G);
@@ -230,6 +458,31 @@ static void launch_skinny(const LinArgs& a, hipStream_t s) {
   else if (fits(2, 2)) launch_skinny_cfg<EPI, SkinnyCfg<2, 2, 4>>(a, nc, s);
   else if (fits(1, 2)) launch_skinny_cfg<EPI, SkinnyCfg<1, 2, 8>>(a, nc, s);
   else launch_skinny_cfg<EPI, SkinnyCfg<1, 1, 8>>(a, nc, s);
+}
+
+inline size_t skinny_ln_lds(int nc, int rt, int g, int K) {
+  return std::max((size_t)nc * 1024 * rt * g, (size_t)4 * K + (size_t)2 * nc * 16 * rt * 4);
+}
+
+template <int EPI, class C>
+static void launch_skinny_ln_cfg(const LinArgs& a, int nc, hipStream_t s) {
+  const int rt = (a.M + 16 * C::RT - 1) / (16 * C::RT), cg = (a.N + 16 * C::G - 1) / (16 * C::G);
+  hipLaunchKernelGGL((k_linear_skinny_ln<EPI, C>), dim3(xcd_grid(rt * cg)), dim3(64 * nc),
+                     skinny_ln_lds(nc, C::RT, C::G, a.K), s, a, rt, cg);
+}
+
+// The tiling rule of launch_skinny, with the LayerNorm's LDS counted.
+template <int EPI>
+static void launch_skinny_ln(const LinArgs& a, hipStream_t s) {
+  const int nc = (a.K + 255) / 256;
+  auto fits = [&](int rt, int g) {
+    const long wgs = (long)((a.M + 16 * rt - 1) / (16 * rt)) * ((a.N + 16 * g - 1) / (16 * g));
+    return wgs >= 192 && skinny_ln_lds(nc, rt, g, a.K) <= 65536;
+  };
+  if (fits(2, 4)) launch_skinny_ln_cfg<EPI, SkinnyCfg<2, 4, 4>>(a, nc, s);
+  else if (fits(2, 2)) launch_skinny_ln_cfg<EPI, SkinnyCfg<2, 2, 8>>(a, nc, s);
+  else if (fits(1, 2)) launch_skinny_ln_cfg<EPI, SkinnyCfg<1, 2, 8>>(a, nc, s);
+  else launch_skinny_ln_cfg<EPI, SkinnyCfg<1, 1, 8>>(a, nc, s);
 }
 
 // Many rows: BM x BN tiles, WAVES_M x WAVES_N waves (each (BM/WAVES_M) x
@@ -377,6 +630,21 @@ static hipError_t linear(const LinArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   if (a.K <= 0 || a.K % 64) return hipErrorInvalidValue;
   if (EPI != kLinF32 && (a.ldy % 4 || (EPI == kLinSplit && a.ns % 4))) return hipErrorInvalidValue;
+  if (a.lng) {
+    if (!a.lnb || a.K > 2048 || a.ldx % 8) return hipErrorInvalidValue;
+    if (a.M <= 128) {
+      launch_skinny_ln<EPI>(a, s);
+      return hipGetLastError();
+    }
+    if (!a.lnout) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_ln_rows, dim3((a.M + 7) / 8), dim3(256), 0, s, a.x, a.ldx, a.lng, a.lnb, a.lnout, a.K, a.M,
+                       a.K);
+    LinArgs n = a;
+    n.x = a.lnout;
+    n.ldx = a.K;
+    n.lng = n.lnb = nullptr;
+    return linear<EPI>(n, s);
+  }
   if (a.M <= 128) {
     launch_skinny<EPI>(a, s);
   } else if ((size_t)((a.N + GemmBig::BN - 1) / GemmBig::BN) * ((a.M + GemmBig::BM - 1) / GemmBig::BM) >= 256) {

@@ -18,63 +18,6 @@
 
 namespace smem {
 
-// LayerNorm of rows of width d (d % 8 == 0, d <= 2048): one wave per row,
-// statistics in fp32 (mean, then the centred second moment), eps 1e-5.
-__global__ void __launch_bounds__(256) k_layernorm(const uint16_t* __restrict__ x, const uint16_t* __restrict__ g,
-                                                   const uint16_t* __restrict__ bta, uint16_t* __restrict__ y,
-                                                   int rows, int d) {
-  const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= rows) return;
-  const uint16_t* xr = x + (size_t)row * d;
-  float v[4][8];
-  float s = 0.f;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = i * 512 + lane * 8;
-    if (c < d) {
-      Chunk<uint16_t>::unpack(*(const u32x4*)(xr + c), v[i]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) s += v[i][e];
-    }
-  }
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) s += __shfl_xor(s, o);
-  const float mean = s / d;
-  float q = 0.f;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = i * 512 + lane * 8;
-    if (c < d) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float t = v[i][e] - mean;
-        q += t * t;
-      }
-    }
-  }
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) q += __shfl_xor(q, o);
-  const float rstd = 1.f / sqrtf(q / d + 1e-5f);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = i * 512 + lane * 8;
-    if (c < d) {
-      float gf[8], bf[8];
-      Chunk<uint16_t>::unpack(*(const u32x4*)(g + c), gf);
-      Chunk<uint16_t>::unpack(*(const u32x4*)(bta + c), bf);
-      uint32_t w[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float y0 = (v[i][2 * e] - mean) * rstd * gf[2 * e] + bf[2 * e];
-        const float y1 = (v[i][2 * e + 1] - mean) * rstd * gf[2 * e + 1] + bf[2 * e + 1];
-        w[e] = (uint32_t)f32_to_bf16_bits(y0) | ((uint32_t)f32_to_bf16_bits(y1) << 16);
-      }
-      *(u32x4*)(y + (size_t)row * d + c) = u32x4{w[0], w[1], w[2], w[3]};
-    }
-  }
-}
-
 struct EmbArgs {
   const int32_t* tokens;   // [rows]
   const uint16_t* tok_emb; // [vocab][d]
@@ -191,7 +134,8 @@ enum { E_LN1G, E_LN1B, E_QKV, E_O, E_LN2G, E_LN2B, E_FF1, E_FF2 };
 enum { R_LN1G, R_LN1B, R_QKV, R_O, R_LN2G, R_LN2B, R_Q, R_K, R_V, R_OC, R_LN3G, R_LN3B, R_FF1, R_FF2 };
 
 hipError_t lnorm(const uint16_t* x, const uint16_t* g, const uint16_t* b, uint16_t* y, int rows, int d, hipStream_t s) {
-  hipLaunchKernelGGL(k_layernorm, dim3((rows + 3) / 4), dim3(256), 0, s, x, g, b, y, rows, d);
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_ln_rows, dim3((rows + 7) / 8), dim3(256), 0, s, x, d, g, b, y, d, rows, d);
   return hipGetLastError();
 }
 
@@ -200,6 +144,15 @@ LinArgs lin(const uint16_t* x, int ldx, const uint16_t* w, int M, int N, int K, 
   memset(&a, 0, sizeof a);
   a.x = x; a.ldx = ldx; a.w = w; a.w2 = w; a.n2 = N;
   a.M = M; a.N = N; a.K = K; a.y = y; a.ldy = ldy;
+  return a;
+}
+
+// y = LN(x) W^T: the few-row maps normalize their own rows; many rows go
+// through the LayerNorm kernel into h first.
+LinArgs lin_ln(const smem_model* m, const uint16_t* g, const uint16_t* b, const uint16_t* w, int M, int N,
+               uint16_t* y, int ldy) {
+  LinArgs a = lin(m->x, m->d.d, w, M, N, m->d.d, y, ldy);
+  a.lng = g; a.lnb = b; a.lnout = m->h;
   return a;
 }
 
@@ -232,8 +185,7 @@ smem_status embed(smem_model* m, int nb, const int32_t* blocks, const int32_t* t
 smem_status ffn(smem_model* m, int rows, const uint16_t* g, const uint16_t* b, const uint16_t* w1, const uint16_t* w2,
                 hipStream_t s) {
   const int D = m->d.d;
-  MCHECK(lnorm(m->x, g, b, m->h, rows, D, s), "layernorm");
-  MCHECK(linear<kLinGelu>(lin(m->h, D, w1, rows, 4 * D, D, m->f, 4 * D), s), "ffn up");
+  MCHECK(linear<kLinGelu>(lin_ln(m, g, b, w1, rows, 4 * D, m->f, 4 * D), s), "ffn up");
   LinArgs a = lin(m->f, 4 * D, w2, rows, D, 4 * D, m->x, D);
   a.res = m->x;
   MCHECK(linear<kLinResid>(a, s), "ffn down");
@@ -243,8 +195,7 @@ smem_status ffn(smem_model* m, int rows, const uint16_t* g, const uint16_t* b, c
 smem_status self_attn(smem_model* m, int rows, int nb, const uint16_t* g, const uint16_t* b, const uint16_t* wqkv,
                       const uint16_t* wo, int mask, hipStream_t s) {
   const int D = m->d.d;
-  MCHECK(lnorm(m->x, g, b, m->h, rows, D, s), "layernorm");
-  LinArgs a = lin(m->h, D, wqkv, rows, 3 * D, D, m->q, D);
+  LinArgs a = lin_ln(m, g, b, wqkv, rows, 3 * D, m->q, D);
   a.y1 = m->k; a.y2 = m->v; a.ns = D;
   MCHECK(linear<kLinSplit>(a, s), "qkv");
   const smem_attn_desc shape{m->d.b, m->d.H, m->d.dh, SMEM_BF16};
@@ -269,8 +220,8 @@ smem_status read_chunk(smem_model* m, int seq, int nb, const int32_t* qblk, cons
     MSTATUS(self_attn(m, rows, nb, w.dec(l, R_LN1G), w.dec(l, R_LN1B), w.dec(l, R_QKV), w.dec(l, R_O),
                       SMEM_MASK_CAUSAL, s));
     // cross-attention into the memory of strictly earlier blocks, with the null row
-    MCHECK(lnorm(m->x, w.dec(l, R_LN2G), w.dec(l, R_LN2B), m->h, rows, D, s), "layernorm");
-    MCHECK(linear<kLinStore>(lin(m->h, D, w.dec(l, R_Q), rows, D, D, m->q, D), s), "cross-attention query");
+    MCHECK(linear<kLinStore>(lin_ln(m, w.dec(l, R_LN2G), w.dec(l, R_LN2B), w.dec(l, R_Q), rows, D, m->q, D), s),
+           "cross-attention query");
     MSTATUS(smem_reader_prefill_block(m->stores[l], nb, seqs.data(), qblk, m->q, nullptr, nullptr,
                                       m->null_kv + (size_t)l * 2 * D, m->o, s));
     LinArgs o = lin(m->o, D, w.dec(l, R_OC), rows, D, D, m->x, D);
@@ -315,8 +266,7 @@ smem_status decode_chunk(smem_model* m, int first, int n, const int32_t* qblk, c
     uint16_t* kc = m->cache + (size_t)l * 2 * plane + (size_t)first * d.b * D;
     uint16_t* vc = kc + plane;
     // self-attention over the block's cached tokens 0..pos
-    MCHECK(lnorm(m->x, w.dec(l, R_LN1G), w.dec(l, R_LN1B), m->h, n, D, s), "layernorm");
-    LinArgs a = lin(m->h, D, w.dec(l, R_QKV), n, 3 * D, D, m->q, D);
+    LinArgs a = lin_ln(m, w.dec(l, R_LN1G), w.dec(l, R_LN1B), w.dec(l, R_QKV), n, 3 * D, m->q, D);
     a.y1 = m->k; a.y2 = m->v; a.ns = D;
     MCHECK(linear<kLinSplit>(a, s), "qkv");
     MSTATUS(smem_reader_decode(m->stores[l], n, seqs.data(), zero.data(), pos, m->q, m->k, m->v, kc, vc, nullptr,
@@ -325,8 +275,8 @@ smem_status decode_chunk(smem_model* m, int first, int n, const int32_t* qblk, c
     o.res = m->x;
     MCHECK(linear<kLinResid>(o, s), "attention out");
     // cross-attention into the memory of strictly earlier blocks, with the null row
-    MCHECK(lnorm(m->x, w.dec(l, R_LN2G), w.dec(l, R_LN2B), m->h, n, D, s), "layernorm");
-    MCHECK(linear<kLinStore>(lin(m->h, D, w.dec(l, R_Q), n, D, D, m->q, D), s), "cross-attention query");
+    MCHECK(linear<kLinStore>(lin_ln(m, w.dec(l, R_LN2G), w.dec(l, R_LN2B), w.dec(l, R_Q), n, D, m->q, D), s),
+           "cross-attention query");
     MSTATUS(smem_reader_decode(m->stores[l], n, seqs.data(), qblk, pos, m->q, nullptr, nullptr, nullptr, nullptr,
                                m->null_kv + (size_t)l * 2 * D, m->o, s));
     LinArgs oc = lin(m->o, D, w.dec(l, R_OC), n, D, D, m->x, D);

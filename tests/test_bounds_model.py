@@ -366,13 +366,83 @@ def test_model_kernel_indexing(d, vocab, rows):
         assert hi["w"] < wrows * K
         assert hi["w2"] < max(w2rows, 0) * K or hi["w2"] == -1
         assert hi["y"] < (M * ns if split else M * ldy)
-    # LayerNorm / embedding: lane chunks c = i*512 + 8*lane (i < 4) guarded by c < d, 8 values each
+    # embedding: lane chunks c = i*512 + 8*lane (i < 4) guarded by c < d, 8 values each
     assert d % 8 == 0 and d <= 2048
     for i, lane in itertools.product(range(4), range(64)):
         c = i * 512 + lane * 8
         if c < d:
             assert c + 7 < d
     assert 3 * 512 + 63 * 8 + 8 >= 2048         # the four chunks cover d = 2048
+
+
+def _ln_groups_rows(d):
+    """k_ln_rows: the (chunk, group) partial each active lane of a row's
+    half-wave sums, as the ordered k list it reads."""
+    KS, NC = d // 32, (d // 32 + 7) // 8
+    assert NC <= 8                                  # 4 NC lanes <= 32
+    out = {}
+    for lane in range(32):
+        c, g = lane >> 2, lane & 3
+        nt = min(8, KS - 8 * c) if c < NC else 0
+        k0 = 256 * c + 8 * g
+        ks = [k0 + 32 * t + e for t in range(nt) for e in range(8)]
+        if ks:
+            out[(c, g)] = ks
+    return out
+
+
+def _ln_groups_skinny(d):
+    """k_linear_skinny_ln: the same partials as wave c, lane group g = lane >> 4
+    hold them (steps s0 + t, t < ns, of the wave's chunk)."""
+    KS, NC = d // 32, (d // 32 + 7) // 8
+    out = {}
+    for c in range(NC):
+        s0, ns = 8 * c, min(8, KS - 8 * c)
+        for g in range(4):
+            kofs = 8 * g
+            out[(c, g)] = [(s0 + t) * 32 + kofs + e for t in range(ns) for e in range(8)]
+    return out
+
+
+def skinny_ln_lds(nc, rt, g, K):                   # bytes (linear.h): statistics, then partial sums, in one space
+    return max(nc * 1024 * rt * g, 4 * K + 2 * nc * 16 * rt * 4)
+
+
+@pytest.mark.parametrize("M,N,K", [(64, 3072, 1024), (64, 6144, 2048), (64, 8192, 2048), (64, 1024, 1024),
+                                   (128, 3072, 768), (1, 4096, 1024), (33, 4160, 832), (64, 2048, 128)])
+def test_layernorm_fused_indexing_and_order(M, N, K):
+    """The LayerNorm fused into a few-row map and the stand-alone LayerNorm
+    kernel sum every row over the same (chunk, group) partials, each in the
+    same ascending k order, covering the row once; the fused kernel's loads,
+    LDS regions and tile choice stay inside their buffers."""
+    rows, sk = _ln_groups_rows(K), _ln_groups_skinny(K)
+    assert rows == sk
+    allk = sorted(k for ks in sk.values() for k in ks)
+    assert allk == list(range(K))
+    NC = (K + 255) // 256
+    fits = lambda rt, g: (-(-M // (16 * rt)) * -(-N // (16 * g)) >= 192
+                          and skinny_ln_lds(NC, rt, g, K) <= 65536)
+    RT, G = next(c for c in ((2, 4), (2, 2), (1, 2), (1, 1)) if c == (1, 1) or fits(*c))
+    lds = skinny_ln_lds(NC, RT, G, K)
+    assert lds <= 65536 and 64 * NC <= 512          # __launch_bounds__(512)
+    part, gb0 = NC * 256 * RT * G * 4, 0              # gain/bias/statistics until the MFMAs, then partial sums
+    st0 = gb0 + 4 * K
+    st1 = st0 + NC * 16 * RT * 4
+    assert st0 % 16 == 0 and st1 + NC * 16 * RT * 4 <= lds and part <= lds
+    for tid in range(64 * NC):                      # gain / bias staging
+        q8 = tid * 8
+        if q8 < K:
+            assert gb0 + 2 * (K + q8 + 7) < st0
+    assert 8 * 64 * NC >= K
+    for c, lane in itertools.product(range(NC), (0, 15, 16, 63)):
+        KS = K // 32
+        s0, ns = 8 * c, min(8, KS - 8 * c)
+        assert ns >= 1
+        for t in range(8):                          # x, W and gain loads at the clamped step
+            k = (s0 + min(t, ns - 1)) * 32 + (lane >> 4) * 8
+            assert k + 7 < K
+        for i in range(RT):                         # statistics slots
+            assert c * 16 * RT + i * 16 + (lane & 15) < NC * 16 * RT
 
 
 def test_gelu_erf_formula_in_source():
