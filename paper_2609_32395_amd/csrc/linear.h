@@ -97,26 +97,33 @@ __device__ __forceinline__ u32x4 ln_apply8(const u32x4& x, const u32x4& g, const
 }
 
 // Stand-alone LayerNorm (rows x[row * ldx .. + d) -> y[row * ldy ..)): one
-// half-wave per row, lane 4c + g holding group g of chunk c, 8 rows per
-// 256-thread block.
-__global__ void __launch_bounds__(256) k_ln_rows(const uint16_t* __restrict__ x, int ldx,
-                                                 const uint16_t* __restrict__ g, const uint16_t* __restrict__ b,
-                                                 uint16_t* __restrict__ y, int ldy, int rows, int d) {
+// half-wave per row, lane 4c + g holding group g of chunk c, one wave (two
+// rows) per block so that a few hundred rows still spread over the CUs; the
+// gain and bias are loaded with the row.
+__global__ void __launch_bounds__(64) k_ln_rows(const uint16_t* __restrict__ x, int ldx,
+                                                const uint16_t* __restrict__ g, const uint16_t* __restrict__ b,
+                                                uint16_t* __restrict__ y, int ldy, int rows, int d) {
   const int lane = threadIdx.x & 31;
-  const int row = blockIdx.x * 8 + (threadIdx.x >> 5);
+  const int row = blockIdx.x * 2 + (threadIdx.x >> 5);
   if (row >= rows) return;
   const int KS = d / 32, NC = (KS + 7) / 8;
   const int c = lane >> 2, k0 = 256 * c + 8 * (lane & 3);
   const int nt = c < NC ? min(8, KS - 8 * c) : 0;
   const uint16_t* xr = x + (size_t)row * ldx + k0;
-  u32x4 v[8];
-  float s = 0.f;
+  u32x4 v[8], gv[8], bv[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+    if (t < nt) v[t] = *(const u32x4*)(xr + 32 * t);
 #pragma unroll
   for (int t = 0; t < 8; ++t)
     if (t < nt) {
-      v[t] = *(const u32x4*)(xr + 32 * t);
-      s = ln_sum8(v[t], s);
+      gv[t] = *(const u32x4*)(g + k0 + 32 * t);
+      bv[t] = *(const u32x4*)(b + k0 + 32 * t);
     }
+  float s = 0.f;
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+    if (t < nt) s = ln_sum8(v[t], s);
   s += __shfl_xor(s, 1, 32);
   s += __shfl_xor(s, 2, 32);
   float tot = 0.f;
@@ -134,9 +141,7 @@ __global__ void __launch_bounds__(256) k_ln_rows(const uint16_t* __restrict__ x,
   uint16_t* yr = y + (size_t)row * ldy + k0;
 #pragma unroll
   for (int t = 0; t < 8; ++t)
-    if (t < nt)
-      *(u32x4*)(yr + 32 * t) =
-          ln_apply8(v[t], *(const u32x4*)(g + k0 + 32 * t), *(const u32x4*)(b + k0 + 32 * t), mean, rstd);
+    if (t < nt) *(u32x4*)(yr + 32 * t) = ln_apply8(v[t], gv[t], bv[t], mean, rstd);
 }
 
 template <int EPI>
@@ -637,7 +642,7 @@ static hipError_t linear(const LinArgs& a, hipStream_t s) {
       return hipGetLastError();
     }
     if (!a.lnout) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_ln_rows, dim3((a.M + 7) / 8), dim3(256), 0, s, a.x, a.ldx, a.lng, a.lnb, a.lnout, a.K, a.M,
+    hipLaunchKernelGGL(k_ln_rows, dim3((a.M + 1) / 2), dim3(64), 0, s, a.x, a.ldx, a.lng, a.lnb, a.lnout, a.K, a.M,
                        a.K);
     LinArgs n = a;
     n.x = a.lnout;
