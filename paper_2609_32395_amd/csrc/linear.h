@@ -96,19 +96,21 @@ __device__ __forceinline__ u32x4 ln_apply8(const u32x4& x, const u32x4& g, const
   return u32x4{w[0], w[1], w[2], w[3]};
 }
 
-// Stand-alone LayerNorm (rows x[row * ldx .. + d) -> y[row * ldy ..)): one
-// half-wave per row, lane 4c + g holding group g of chunk c, one wave (two
-// rows) per block so that a few hundred rows still spread over the CUs; the
+// Stand-alone LayerNorm (rows x[row * ldx .. + d) -> y[row * ldy ..)): a
+// row takes 4 n_chunks lanes, lane 4c + g holding group g of chunk c, and a
+// wave holds 64 / (4 n_chunks) rows (4 at d = 1024), so every lane sums; the
 // gain and bias are loaded with the row.
+__host__ __device__ constexpr int ln_rows_per_wave(int d) { return 64 / (4 * ((d / 32 + 7) / 8)); }
+
 __global__ void __launch_bounds__(64) k_ln_rows(const uint16_t* __restrict__ x, int ldx,
                                                 const uint16_t* __restrict__ g, const uint16_t* __restrict__ b,
                                                 uint16_t* __restrict__ y, int ldy, int rows, int d) {
-  const int lane = threadIdx.x & 31;
-  const int row = blockIdx.x * 2 + (threadIdx.x >> 5);
-  if (row >= rows) return;
-  const int KS = d / 32, NC = (KS + 7) / 8;
-  const int c = lane >> 2, k0 = 256 * c + 8 * (lane & 3);
-  const int nt = c < NC ? min(8, KS - 8 * c) : 0;
+  const int KS = d / 32, NC = (KS + 7) / 8, LPR = 4 * NC, R = 64 / LPR;
+  const int lane = threadIdx.x, rl = lane / LPR, base = rl * LPR, l = lane - base;
+  const int row = blockIdx.x * R + rl;
+  if (rl >= R || row >= rows) return;
+  const int c = l >> 2, k0 = 256 * c + 8 * (l & 3);
+  const int nt = min(8, KS - 8 * c);
   const uint16_t* xr = x + (size_t)row * ldx + k0;
   u32x4 v[8], gv[8], bv[8];
 #pragma unroll
@@ -124,19 +126,19 @@ __global__ void __launch_bounds__(64) k_ln_rows(const uint16_t* __restrict__ x, 
 #pragma unroll
   for (int t = 0; t < 8; ++t)
     if (t < nt) s = ln_sum8(v[t], s);
-  s += __shfl_xor(s, 1, 32);
-  s += __shfl_xor(s, 2, 32);
+  s += __shfl_xor(s, 1);
+  s += __shfl_xor(s, 2);
   float tot = 0.f;
-  for (int q = 0; q < NC; ++q) tot += __shfl(s, 4 * q, 32);
+  for (int q = 0; q < NC; ++q) tot += __shfl(s, base + 4 * q);
   const float mean = tot / d;
   float m2 = 0.f;
 #pragma unroll
   for (int t = 0; t < 8; ++t)
     if (t < nt) m2 = ln_sq8(v[t], mean, m2);
-  m2 += __shfl_xor(m2, 1, 32);
-  m2 += __shfl_xor(m2, 2, 32);
+  m2 += __shfl_xor(m2, 1);
+  m2 += __shfl_xor(m2, 2);
   float tot2 = 0.f;
-  for (int q = 0; q < NC; ++q) tot2 += __shfl(m2, 4 * q, 32);
+  for (int q = 0; q < NC; ++q) tot2 += __shfl(m2, base + 4 * q);
   const float rstd = ln_rstd(tot2, d);
   uint16_t* yr = y + (size_t)row * ldy + k0;
 #pragma unroll
@@ -642,8 +644,9 @@ static hipError_t linear(const LinArgs& a, hipStream_t s) {
       return hipGetLastError();
     }
     if (!a.lnout) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_ln_rows, dim3((a.M + 1) / 2), dim3(64), 0, s, a.x, a.ldx, a.lng, a.lnb, a.lnout, a.K, a.M,
-                       a.K);
+    const int rpw = ln_rows_per_wave(a.K);
+    hipLaunchKernelGGL(k_ln_rows, dim3((a.M + rpw - 1) / rpw), dim3(64), 0, s, a.x, a.ldx, a.lng, a.lnb, a.lnout, a.K,
+                       a.M, a.K);
     LinArgs n = a;
     n.x = a.lnout;
     n.ldx = a.K;

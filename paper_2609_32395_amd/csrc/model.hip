@@ -135,7 +135,8 @@ enum { R_LN1G, R_LN1B, R_QKV, R_O, R_LN2G, R_LN2B, R_Q, R_K, R_V, R_OC, R_LN3G, 
 
 hipError_t lnorm(const uint16_t* x, const uint16_t* g, const uint16_t* b, uint16_t* y, int rows, int d, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_ln_rows, dim3((rows + 1) / 2), dim3(64), 0, s, x, d, g, b, y, d, rows, d);
+  const int rpw = ln_rows_per_wave(d);
+  hipLaunchKernelGGL(k_ln_rows, dim3((rows + rpw - 1) / rpw), dim3(64), 0, s, x, d, g, b, y, d, rows, d);
   return hipGetLastError();
 }
 

@@ -375,20 +375,33 @@ def test_model_kernel_indexing(d, vocab, rows):
     assert 3 * 512 + 63 * 8 + 8 >= 2048         # the four chunks cover d = 2048
 
 
-def _ln_groups_rows(d):
-    """k_ln_rows: the (chunk, group) partial each active lane of a row's
-    half-wave sums, as the ordered k list it reads."""
+def _ln_groups_rows(d, rows=5):
+    """k_ln_rows: the (chunk, group) partial each active lane sums, as the
+    ordered k list it reads; every row of a wave (and of the last, partial
+    wave) sees the same partials, and its shuffles stay inside its lanes."""
     KS, NC = d // 32, (d // 32 + 7) // 8
-    assert NC <= 8                                  # 4 NC lanes <= 32
-    out = {}
-    for lane in range(32):
-        c, g = lane >> 2, lane & 3
-        nt = min(8, KS - 8 * c) if c < NC else 0
-        k0 = 256 * c + 8 * g
-        ks = [k0 + 32 * t + e for t in range(nt) for e in range(8)]
-        if ks:
-            out[(c, g)] = ks
-    return out
+    LPR = 4 * NC
+    R = 64 // LPR                                   # ln_rows_per_wave
+    assert NC <= 8 and R >= 2
+    per_row = {}
+    for blk in range(-(-rows // R)):
+        for lane in range(64):
+            rl = lane // LPR
+            base, l = rl * LPR, lane - rl * LPR
+            row = blk * R + rl
+            if rl >= R or row >= rows:
+                continue
+            c, g = l >> 2, l & 3
+            for o in (1, 2):                        # xor partners: the same row, the same chunk
+                assert (lane ^ o) // LPR == rl and ((lane ^ o) - base) >> 2 == c
+            assert all(base + 4 * q < base + LPR for q in range(NC))
+            nt = min(8, KS - 8 * c)
+            k0 = 256 * c + 8 * g
+            per_row.setdefault(row, {})[(c, g)] = [k0 + 32 * t + e for t in range(nt) for e in range(8)]
+    assert sorted(per_row) == list(range(rows))
+    first = per_row[0]
+    assert all(v == first for v in per_row.values())
+    return first
 
 
 def _ln_groups_skinny(d):
