@@ -345,7 +345,7 @@ def _linear_ranges(M, N, K, ldx, ldy, n2, ns, split):
 
 
 @pytest.mark.parametrize("d,vocab,rows", [(128, 256, 448), (768, 1000, 130), (2048, 77, 64), (256, 300, 100),
-                                         (768, 50257, 64), (1024, 4000, 4096)])
+                                         (768, 50257, 64), (1024, 4000, 4096), (832, 300, 256), (2048, 300, 256)])
 def test_model_kernel_indexing(d, vocab, rows):
     """Every linear-map launch the model makes stays inside its operands (x
     [rows, K] in a [max_tokens, ldx] buffer, W [N or n2, K] and [N - n2, K],
@@ -422,7 +422,8 @@ def skinny_ln_lds(nc, rt, g, K):                   # bytes (linear.h): statistic
 
 
 @pytest.mark.parametrize("M,N,K", [(64, 3072, 1024), (64, 6144, 2048), (64, 8192, 2048), (64, 1024, 1024),
-                                   (128, 3072, 768), (1, 4096, 1024), (33, 4160, 832), (64, 2048, 128)])
+                                   (128, 3072, 768), (1, 4096, 1024), (33, 4160, 832), (64, 2048, 128),
+                                   (64, 2496, 832), (64, 3328, 832), (64, 832, 832)])
 def test_layernorm_fused_indexing_and_order(M, N, K):
     """The LayerNorm fused into a few-row map and the stand-alone LayerNorm
     kernel sum every row over the same (chunk, group) partials, each in the

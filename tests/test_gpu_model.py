@@ -182,6 +182,30 @@ def test_tilings_agree_bitwise():
     assert float(np.max(np.abs(y - expect)) / np.sqrt(np.mean(expect ** 2))) <= tol(SHAPE["E"], SHAPE["D"], y.size)
 
 
+@pytest.mark.parametrize("d,H", [(2048, 16), (832, 26)], ids=["d2048", "d832"])
+def test_fused_layernorm_widths_bitwise(d, H):
+    """Block-skip serving normalizes its 64 rows inside the few-row maps (at
+    d = 2048 the q|k|v and FFN-up maps take the 4-column-group tile with its
+    W refill; at d = 832 the last 256-chunk of every row is 2 steps); the
+    cold pass over 4 blocks runs the stand-alone LayerNorm and the tiled
+    GEMM.  The final block's logits agree bit for bit and match the oracle."""
+    say("model: fused LayerNorm widths", d, H)
+    over = dict(E=1, D=1, d=d, H=H, vocab=300, n_pos=0)
+    m, ref, _ = build(max_blocks=4, n_pages=8, max_tokens=256, **over)
+    g = np.random.default_rng(16)
+    B = 4
+    tokens = g.integers(0, 300, size=(B, SHAPE["b"]))
+    cold = smem.smem_model_prefill(m, 0, 0, B, tok(tokens))
+    skip = smem.smem_model_read(m, 0, [B - 1], tok(tokens[B - 1:]))
+    assert torch.equal(cold, skip)
+    ref.encode(0, tokens[:B - 1], list(range(B - 1)))
+    expect = ref.read(0, tokens[B - 1:], [B - 1])[0]
+    y = host(skip)
+    err = float(np.max(np.abs(y - expect)) / np.sqrt(np.mean(expect ** 2)))
+    say("rel err", err)
+    assert err <= tol(1, 1, y.size), err
+
+
 def test_160m_full_size_block_skip_matches_oracle():
     """At the bench's 160M shape (d 768, E 3, D 7, 24 heads of 32, vocabulary
     50257, 1024 positions) and its 1k context, in the bench's launch
