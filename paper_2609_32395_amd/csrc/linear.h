@@ -447,7 +447,8 @@ static void launch_skinny_cfg(const LinArgs& a, int nc, hipStream_t s) {
                      a, rt, cg);
 }
 
-// The widest tile that still gives at least 192 workgroups: every workgroup
+// The widest tile that still gives at least 192 workgroups (one row tile
+// when M <= 16, where a second row tile is padding only): every workgroup
 // reads its rows of x and its columns of W whole, and reads issued at the
 // same time by several workgroups each cost close to a full read, so wider
 // tiles (fewer duplicated reads) win until too few workgroups remain to keep
@@ -459,7 +460,7 @@ static void launch_skinny(const LinArgs& a, hipStream_t s) {
   const int nc = (a.K + lin_chunk(a.K) - 1) / lin_chunk(a.K);
   auto fits = [&](int rt, int g) {
     const long wgs = (long)((a.M + 16 * rt - 1) / (16 * rt)) * ((a.N + 16 * g - 1) / (16 * g));
-    return wgs >= 192 && nc * rt * g <= 64;
+    return wgs >= 192 && nc * rt * g <= 64 && (rt == 1 || a.M > 16);
   };
   if (fits(2, 4)) launch_skinny_cfg<EPI, SkinnyCfg<2, 4, 4>>(a, nc, s);
   else if (fits(2, 2)) launch_skinny_cfg<EPI, SkinnyCfg<2, 2, 4>>(a, nc, s);
@@ -484,7 +485,7 @@ static void launch_skinny_ln(const LinArgs& a, hipStream_t s) {
   const int nc = (a.K + 255) / 256;
   auto fits = [&](int rt, int g) {
     const long wgs = (long)((a.M + 16 * rt - 1) / (16 * rt)) * ((a.N + 16 * g - 1) / (16 * g));
-    return wgs >= 192 && skinny_ln_lds(nc, rt, g, a.K) <= 65536;
+    return wgs >= 192 && skinny_ln_lds(nc, rt, g, a.K) <= 65536 && (rt == 1 || a.M > 16);
   };
   if (fits(2, 4)) launch_skinny_ln_cfg<EPI, SkinnyCfg<2, 4, 4>>(a, nc, s);
   else if (fits(2, 2)) launch_skinny_ln_cfg<EPI, SkinnyCfg<2, 2, 8>>(a, nc, s);

@@ -258,7 +258,8 @@ def _linear_ranges(M, N, K, ldx, ldy, n2, ns, split):
     if M <= 128:
         KS, CS = K // 32, lin_chunk(K) // 32
         NC = -(-KS // CS)
-        fits = lambda rt, g: -(-M // (16 * rt)) * -(-N // (16 * g)) >= 192 and NC * rt * g <= 64
+        fits = lambda rt, g: (-(-M // (16 * rt)) * -(-N // (16 * g)) >= 192 and NC * rt * g <= 64
+                              and (rt == 1 or M > 16))
         RT, G = next(c for c in ((2, 4), (2, 2), (1, 2), (1, 1)) if c == (1, 1) or fits(*c))   # launch_skinny
         PART = 256 * RT * G                      # floats per chunk
         assert NC <= 16 and NC * PART * 4 <= 64 * 1024
@@ -423,7 +424,8 @@ def skinny_ln_lds(nc, rt, g, K):                   # bytes (linear.h): statistic
 
 @pytest.mark.parametrize("M,N,K", [(64, 3072, 1024), (64, 6144, 2048), (64, 8192, 2048), (64, 1024, 1024),
                                    (128, 3072, 768), (1, 4096, 1024), (33, 4160, 832), (64, 2048, 128),
-                                   (64, 2496, 832), (64, 3328, 832), (64, 832, 832)])
+                                   (64, 2496, 832), (64, 3328, 832), (64, 832, 832), (16, 6144, 2048),
+                                   (16, 8192, 2048)])
 def test_layernorm_fused_indexing_and_order(M, N, K):
     """The LayerNorm fused into a few-row map and the stand-alone LayerNorm
     kernel sum every row over the same (chunk, group) partials, each in the
@@ -435,7 +437,7 @@ def test_layernorm_fused_indexing_and_order(M, N, K):
     assert allk == list(range(K))
     NC = (K + 255) // 256
     fits = lambda rt, g: (-(-M // (16 * rt)) * -(-N // (16 * g)) >= 192
-                          and skinny_ln_lds(NC, rt, g, K) <= 65536)
+                          and skinny_ln_lds(NC, rt, g, K) <= 65536 and (rt == 1 or M > 16))
     RT, G = next(c for c in ((2, 4), (2, 2), (1, 2), (1, 1)) if c == (1, 1) or fits(*c))
     lds = skinny_ln_lds(NC, RT, G, K)
     assert lds <= 65536 and 64 * NC <= 512          # __launch_bounds__(512)
