@@ -180,6 +180,23 @@ smem_status smem_reader_decode(smem_store* st, int32_t n_seq, const int32_t* seq
                                const void* k_new, const void* v_new, void* k_cache, void* v_cache,
                                const void* null_kv, void* out, hipStream_t s);
 
+/* smem_reader_decode for callers that cannot allocate device memory or touch
+ * a workspace (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): same arguments, layouts, results (bit for bit) and
+ * errors, but the split partials go to a 16 MiB device array that the library
+ * holds on each GPU it runs on, instead of the store's workspace.  It calls no
+ * allocator.  The partials of one launch (up to 128 sequences) take
+ * n_seq x H x splits x (dh + 4) floats, splits = ceil(memory pages read /
+ * max(8, ceil(pages / 64))) + 1 for the longest read of the launch; a call
+ * that needs more than 4 Mi floats returns SMEM_EINVAL before anything is
+ * enqueued.  Every call on one GPU shares that GPU's array: calls that overlap
+ * on one GPU (unordered streams or threads) race; calls ordered on one stream
+ * do not.  No rotary variant. */
+smem_status smem_reader_decode_static(smem_store* st, int32_t n_seq, const int32_t* seq_ids,
+                                      const int32_t* query_block, const int32_t* pos, const void* q,
+                                      const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                                      const void* null_kv, void* out, hipStream_t s);
+
 /* Exact deletion (Theorem 1): remove block `block_idx` of sequence `seq`.
  * The remaining blocks keep their indices, and every later read equals a
  * read of the memory in which the block was never inserted.  Cost is O(1)

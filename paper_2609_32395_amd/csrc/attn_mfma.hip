@@ -722,7 +722,7 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
   if (nms == 0) {
     store_out<DH>((uint16_t*)a.out + qs * rs + (size_t)h * DH, o, l, lane);
   } else {
-    float* part = a.ws + ((qs * a.H + h) * kSplitStride + split) * (DH + 4);
+    float* part = a.ws + ((qs * a.H + h) * a.ws_stride + split) * (DH + 4);
 #pragma unroll
     for (int dt = 0; dt < DH / 16; ++dt) {
       const int d0 = dt * 16 + (lane >> 4) * 4;

@@ -246,7 +246,8 @@ struct ReaderArgs {
   const void* null_kv;    // [2][H][dh] or NULL
   const void* pages;      // page pool
   const int32_t* live_page;  // [n_seq][max_blocks] dense live list -> page
-  float* ws;              // split partials, (dh+4) floats each
+  float* ws;              // split partials, (dh+4) floats each: split k of (query row qr, head h)
+                          // at ws + ((qr*H + h)*ws_stride + k)*(dh+4)
   void* out;              // output, same indexing as q
   void* page_sink;        // encoder (fp32): also write O as key and value rows of page aux[i]
   int32_t max_blocks;
@@ -272,6 +273,7 @@ struct ReaderArgs {
   // workgroup z takes slot order[z] (slots with the most pages first).
   int32_t fuse;
   int16_t order[kMaxSlots];
+  int32_t ws_stride;          // split records per (query row, head) in ws (>= the launch's most splits)
 };
 
 // Row-plane decode (bf16): rows of width d, absorbed queries, split partials.
@@ -366,6 +368,13 @@ hipError_t launch_prefill_mfma(int b, int dh, const ReaderArgs& a, hipStream_t s
 hipError_t launch_rows(int d, int dh, const RowsArgs& a, const RowsPrepArgs& pa, int stage, hipStream_t s);
 // Plain device copy (16-byte multiples).
 hipError_t launch_copy16(void* dst, const void* src, size_t bytes, hipStream_t s);
+// Reader decode (smem_reader_decode and its variants).  ws_ext == NULL: split
+// partials in the store's workspace; otherwise in ws_ext, which holds
+// ws_ext_floats floats (the call is rejected if its partials do not fit).
+smem_status decode_impl(smem_store* st, const smem_rope* rope, int32_t n_seq, const int32_t* seq_ids,
+                        const int32_t* query_block, const int32_t* pos, const void* q, const void* k_new,
+                        const void* v_new, void* k_cache, void* v_cache, const void* null_kv, void* out,
+                        float* ws_ext, size_t ws_ext_floats, hipStream_t s);
 // Record a failure for smem_last_error() (defined with the C ABI); returns st.
 smem_status set_error(smem_status st, const char* msg);
 // Rotary table of n_phases rows for heads of width dh, computed in fp64.

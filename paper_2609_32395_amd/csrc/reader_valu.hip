@@ -288,7 +288,7 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
       }
     } else {
       float* part = a.intra_partial ? a.ws + ((size_t)qs * a.H + h) * (DH + 4)
-                                    : a.ws + (((size_t)qs * a.H + h) * kSplitStride + split) * (DH + 4);
+                                    : a.ws + (((size_t)qs * a.H + h) * a.ws_stride + split) * (DH + 4);
       part[tid] = A;
       if (tid == 0) { part[DH] = M; part[DH + 1] = L; }
     }
@@ -310,7 +310,7 @@ __global__ void __launch_bounds__(128) k_merge(ReaderArgs a) {
   __shared__ FoldScale c_sh[kSplitStride];
   __shared__ float inv_sh;
   const int tid = threadIdx.x;
-  const float* base = a.ws + ((size_t)qs * a.H + h) * kSplitStride * (DH + 4);
+  const float* base = a.ws + ((size_t)qs * a.H + h) * a.ws_stride * (DH + 4);
   if (tid < S) {
     m_sh[tid] = base[(size_t)tid * (DH + 4) + DH];
     l_sh[tid] = base[(size_t)tid * (DH + 4) + DH + 1];

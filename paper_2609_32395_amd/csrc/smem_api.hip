@@ -589,6 +589,7 @@ static smem_status prefill_impl(smem_store* st, const smem_rope* rope, int32_t n
     a.pages = st->d_pages;
     a.live_page = st->d_live_page;
     a.ws = st->d_ws;
+    a.ws_stride = kSplitStride;
     a.max_blocks = d.max_blocks;
     a.H = d.H; a.b = d.b; a.nq = d.b; a.intra_mode = 1;
     a.n_slots = n; a.scale_log2 = scale_log2;
@@ -610,10 +611,16 @@ static smem_status prefill_impl(smem_store* st, const smem_rope* rope, int32_t n
   return SMEM_OK;
 }
 
-static smem_status decode_impl(smem_store* st, const smem_rope* rope, int32_t n_seq, const int32_t* seq_ids,
-                               const int32_t* query_block, const int32_t* pos, const void* q, const void* k_new,
-                               const void* v_new, void* k_cache, void* v_cache, const void* null_kv, void* out,
-                               hipStream_t s) {
+}  // extern "C"
+
+// ws_ext == NULL: split partials in the store's workspace (kSplitStride records
+// per (query, head)).  Otherwise in ws_ext (ws_ext_floats floats), each launch
+// packing its partials at a stride of its own largest split count; a call that
+// would not fit is rejected before anything is enqueued.
+smem_status smem::decode_impl(smem_store* st, const smem_rope* rope, int32_t n_seq, const int32_t* seq_ids,
+                              const int32_t* query_block, const int32_t* pos, const void* q, const void* k_new,
+                              const void* v_new, void* k_cache, void* v_cache, const void* null_kv, void* out,
+                              float* ws_ext, size_t ws_ext_floats, hipStream_t s) {
   if (!st) return fail(SMEM_EINVAL, "store is NULL");
   if (st->meta_only) return fail(SMEM_EINVAL, "metadata-only store");
   if (st->kind != 0) return fail(SMEM_EINVAL, "a row store is read by smem_reader_decode_rows");
@@ -642,6 +649,24 @@ static smem_status decode_impl(smem_store* st, const smem_rope* rope, int32_t n_
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
   const size_t es = esize(d.dtype);
   const size_t tok = (size_t)d.H * d.dh;
+  // splits of each launch's slots (one launch per kMaxSlots sequences)
+  std::vector<int32_t> nr(n_seq), pp(n_seq);
+  std::vector<int32_t> stride((n_seq + kMaxSlots - 1) / kMaxSlots, 1);
+  for (int i = 0; i < n_seq; ++i) {
+    nr[i] = n_read_of(st, seq_ids[i], query_block[i]);
+    pp[i] = pages_per_split(nr[i], kMinPagesDecode);
+    int32_t& w = stride[i / kMaxSlots];
+    w = std::max(w, (int32_t)total_splits(nr[i], pp[i]));
+  }
+  if (ws_ext) {
+    for (size_t c = 0; c < stride.size(); ++c) {
+      const size_t n = std::min(kMaxSlots, n_seq - (int)c * kMaxSlots);
+      const size_t need = n * d.H * (size_t)stride[c] * (d.dh + 4);
+      if (need > ws_ext_floats)
+        return fail(SMEM_EINVAL, "split partials of %zu sequences x %d heads x %d splits need %zu floats; the "
+                                 "scratch holds %zu", n, d.H, stride[c], need, ws_ext_floats);
+    }
+  }
   for (int i0 = 0; i0 < n_seq; i0 += kMaxSlots) {
     const int n = std::min(kMaxSlots, n_seq - i0);
     ReaderArgs a;
@@ -659,7 +684,8 @@ static smem_status decode_impl(smem_store* st, const smem_rope* rope, int32_t n_
     a.null_kv = null_kv;
     a.pages = st->d_pages;
     a.live_page = st->d_live_page;
-    a.ws = st->d_ws;
+    a.ws = ws_ext ? ws_ext : st->d_ws;
+    a.ws_stride = ws_ext ? stride[i0 / kMaxSlots] : kSplitStride;
     a.max_blocks = d.max_blocks;
     a.H = d.H; a.b = d.b; a.nq = 1; a.intra_mode = 2;
     a.n_slots = n; a.scale_log2 = scale_log2;
@@ -668,8 +694,8 @@ static smem_status decode_impl(smem_store* st, const smem_rope* rope, int32_t n_
       const int sq = seq_ids[i0 + i];
       a.seq[i] = sq;
       a.qblk[i] = query_block[i0 + i];
-      a.n_read[i] = n_read_of(st, sq, query_block[i0 + i]);
-      a.pps[i] = pages_per_split(a.n_read[i], kMinPagesDecode);
+      a.n_read[i] = nr[i0 + i];
+      a.pps[i] = pp[i0 + i];
       a.aux[i] = n_given == 4 ? pos[i0 + i] : 0;
     }
     hipError_t e = launch_reader_valu(d.dtype, d.b, d.dh, a, s);
@@ -677,6 +703,8 @@ static smem_status decode_impl(smem_store* st, const smem_rope* rope, int32_t n_
   }
   return SMEM_OK;
 }
+
+extern "C" {
 
 smem_status smem_reader_prefill_block(smem_store* st, int32_t n_seq, const int32_t* seq_ids,
                                       const int32_t* query_block, const void* q, const void* k_intra,
@@ -696,7 +724,7 @@ smem_status smem_reader_decode(smem_store* st, int32_t n_seq, const int32_t* seq
                                const int32_t* pos, const void* q, const void* k_new, const void* v_new,
                                void* k_cache, void* v_cache, const void* null_kv, void* out, hipStream_t s) {
   return decode_impl(st, nullptr, n_seq, seq_ids, query_block, pos, q, k_new, v_new, k_cache, v_cache, null_kv,
-                     out, s);
+                     out, nullptr, 0, s);
 }
 
 smem_status smem_reader_decode_rope(smem_store* st, const smem_rope* rope, int32_t n_seq, const int32_t* seq_ids,
@@ -705,7 +733,7 @@ smem_status smem_reader_decode_rope(smem_store* st, const smem_rope* rope, int32
                                     const void* null_kv, void* out, hipStream_t s) {
   if (!rope) return fail(SMEM_EINVAL, "rope is NULL");
   return decode_impl(st, rope, n_seq, seq_ids, query_block, pos, q, k_new, v_new, k_cache, v_cache, null_kv,
-                     out, s);
+                     out, nullptr, 0, s);
 }
 
 size_t smem_rows_bytes(const smem_rows_desc* desc) {

@@ -87,6 +87,7 @@ SIGNATURES = {
     "smem_reencode_blocks": (_I, [_P, ctypes.POINTER(AttnDesc), _I, _IP, _IP, _P, _P, _P, _P, _I, _P]),
     "smem_reader_prefill_block": (_I, [_P, _I, _IP, _IP, _P, _P, _P, _P, _P, _P]),
     "smem_reader_decode": (_I, [_P, _I, _IP, _IP, _IP, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "smem_reader_decode_static": (_I, [_P, _I, _IP, _IP, _IP, _P, _P, _P, _P, _P, _P, _P, _P]),
     "smem_delete_block": (_I, [_P, _I, _I, _I, _P]),
     "smem_store_export": (_I, [_P, _I, _IP, _IP, _P, _P, _P]),
     "smem_rope_bytes": (ctypes.c_size_t, [ctypes.POINTER(RopeDesc)]),
@@ -618,6 +619,13 @@ def smem_reader_decode(st: Store, seq_ids, query_block, pos, q, k_new=None, v_ne
     return _decode(st, None, seq_ids, query_block, pos, q, k_new, v_new, k_cache, v_cache, null_kv, out, stream)
 
 
+def smem_reader_decode_static(st: Store, seq_ids, query_block, pos, q, k_new=None, v_new=None, k_cache=None,
+                              v_cache=None, null_kv=None, out=None, stream=None):
+    """smem_reader_decode with the split partials in the library's own device
+    array instead of the store's workspace (no allocation by the library)."""
+    return _decode(st, "static", seq_ids, query_block, pos, q, k_new, v_new, k_cache, v_cache, null_kv, out, stream)
+
+
 def smem_reader_decode_rope(st: Store, rope: Rope, seq_ids, query_block, pos, q, k_new=None, v_new=None,
                             k_cache=None, v_cache=None, null_kv=None, out=None, stream=None):
     """smem_reader_decode with the composite's rotary phases."""
@@ -639,6 +647,8 @@ def _decode(st, rope, seq_ids, query_block, pos, q, k_new, v_new, k_cache, v_cac
     rest = (n, _i32(seq_ids), _i32(query_block), pa, *args, _stream(stream))
     if rope is None:
         _check(lib().smem_reader_decode(st.handle, *rest))
+    elif rope == "static":
+        _check(lib().smem_reader_decode_static(st.handle, *rest))
     else:
         _check(lib().smem_reader_decode_rope(st.handle, rope.handle, *rest))
     return out
