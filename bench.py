@@ -38,10 +38,10 @@ Timing uses HIP events on the stream the kernels are launched on (torch's
 current stream, handed to the library).  The 160M encoder and prefill calls
 are shorter than the host's cost of issuing them, so they are captured in a
 HIP graph (repetitions of the call, no memory sets) and the replays are
-timed.  The 160M encoder/prefill and the 1.5B serve also report one call
-issued on an idle GPU after a 512 MiB read pass (`*_single_flushed`): the
-latency of a call whose data are out of the caches, against the
-back-to-back throughput above.  The CPU baseline is the fp64 numpy
+timed.  The 160M encoder/prefill and the 1.5B serve also report single
+calls run right after a 512 MiB read pass and enqueued while it runs
+(`*_single_flushed`): the device time of a call whose data are out of the
+caches, against the back-to-back throughput above.  The CPU baseline is the fp64 numpy
 oracle timed on a bounded sample of the headline workload on this host
 (all threads, and one thread for reference).
 Prints ONE JSON line.
@@ -96,18 +96,20 @@ def _events_time(fn, steps, stream):
 
 
 def _flushed_time(fn, reps, stream, scratch):
-    """Median seconds of single calls of fn, each issued on an idle GPU after
-    a read pass over `scratch` (512 MiB, twice the 256 MiB last-level cache),
-    so every call starts with its working set out of the caches.  The flush
-    only reads: dirty lines left by a writing flush would be written back
-    during the timed call and slow it for reasons of its own."""
+    """Median seconds of single calls of fn, each run right after a read pass
+    over `scratch` (512 MiB, twice the 256 MiB last-level cache), so every
+    call starts with its working set out of the caches.  The call is enqueued
+    while the flush still runs, so the interval between the two events is the
+    device's time for the call (the host's enqueue cost is not in it).  The
+    flush only reads: dirty lines left by a writing flush would be written
+    back during the timed call and slow it for reasons of its own."""
     import torch
     ts = []
     for r in range(reps):
-        scratch.sum()
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
+        scratch.sum()
         e0.record(stream)
         fn(r)
         e1.record(stream)

@@ -226,13 +226,21 @@ __device__ __forceinline__ void pv(floatx4 (&o)[DH / 16], const Tiles<DH>& T, co
 // pair it returns, the lane's own value and its partner's (l^16, l^32), so
 // op(pair) is the two-lane reduction -- a VALU exchange instead of an LDS
 // permute; both operations are commutative, so every lane gets the same bits.
+// The exchanged values are already canonical floats (maxima of MFMA results),
+// so the maximum is taken with a plain v_max_f32: fmaxf would first
+// canonicalise both operands (two more instructions per exchange).
+__device__ __forceinline__ float max_plain(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
 __device__ __forceinline__ float xor16_op_max(float x) {
   const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return max_plain(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float xor32_op_max(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return max_plain(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float xor16_op_sum(float x) {
   const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -244,6 +252,7 @@ __device__ __forceinline__ float xor32_op_sum(float x) {
 }
 __device__ __forceinline__ float qmax(float x) { return xor32_op_max(xor16_op_max(x)); }
 __device__ __forceinline__ float qsum(float x) { return xor32_op_sum(xor16_op_sum(x)); }
+
 
 // One online-softmax step over a 64-key tile for the lane's query.
 // valid(kt, i) says whether key kt*16 + 4*(lane/16) + i is visible.
@@ -269,6 +278,22 @@ __device__ __forceinline__ void online_step(floatx4 (&s)[4], float& m, float& l,
     }
   }
   mx = qmax(mx) * scale_log2;
+  // When no query of the wave raises its maximum, the rescale factor is
+  // exactly 1: l and o are left as they are (the same bits as multiplying).
+  if (__all(mx <= m)) {
+    float ps = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = (CAUSAL && s[kt][i] == -INFINITY) ? 0.f : exp2w(__builtin_fmaf(s[kt][i], scale_log2, -m));
+        s[kt][i] = p;
+        ps += p;
+      }
+    }
+    l += ps;
+    return;
+  }
   const float mn = fmaxf(m, mx);
   // Without the causal mask every score is finite, so mn is finite and
   // 2^(m - mn) = 2^-inf = 0 on the first tile: the guards are only needed
@@ -515,11 +540,13 @@ __device__ __forceinline__ void wait_pages(int ahead) {
 
 // The null row, one always-visible key/value pair per head, as the first key
 // of the final split (m, l, o start empty).
+// nkh, nvh: the head's null key and value vectors (global memory or LDS).
 template <int DH, bool ROPE>
-__device__ __forceinline__ void null_row(const ReaderArgs& a, int slot, int h, const bf16x8 (&qf)[DH / 32], int lane,
-                                         float& m, float& l, floatx4 (&o)[DH / 16]) {
-  const uint16_t* nk = (const uint16_t*)a.null_kv + (size_t)h * DH + (lane >> 4) * 8;
-  const uint16_t* nv = (const uint16_t*)a.null_kv + ((size_t)a.H + h) * DH;
+__device__ __forceinline__ void null_row_at(const uint16_t* nkh, const uint16_t* nvh, const ReaderArgs& a, int slot,
+                                            const bf16x8 (&qf)[DH / 32], int lane, float& m, float& l,
+                                            floatx4 (&o)[DH / 16]) {
+  const uint16_t* nk = nkh + (lane >> 4) * 8;
+  const uint16_t* nv = nvh;
   bf16x8 qn[DH / 32];
   if constexpr (ROPE) {
     rope_q<DH>(qn, qf, a.rope + (size_t)min(a.qblk[slot], a.rope_clip) * DH, lane);
@@ -544,6 +571,13 @@ __device__ __forceinline__ void null_row(const ReaderArgs& a, int slot, int h, c
 #pragma unroll
     for (int i = 0; i < 4; ++i) o[dt][i] = bf16_bits_to_f32(nv[dt * 16 + (lane >> 4) * 4 + i]);
   }
+}
+
+template <int DH, bool ROPE>
+__device__ __forceinline__ void null_row(const ReaderArgs& a, int slot, int h, const bf16x8 (&qf)[DH / 32], int lane,
+                                         float& m, float& l, floatx4 (&o)[DH / 16]) {
+  null_row_at<DH, ROPE>((const uint16_t*)a.null_kv + (size_t)h * DH, (const uint16_t*)a.null_kv + ((size_t)a.H + h) * DH,
+                        a, slot, qf, lane, m, l, o);
 }
 
 // Fold one split's (m, l, o) into the running state (fm, fl, acc) -- the
@@ -735,6 +769,216 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
   }
 }
 
+// ------------------------------------------------------------------ few-pair prefill
+
+// Launches with few (query block, head) pairs and at most four memory splits
+// each.  A pair's 64 query rows go to 4/QW workgroups of 4 x QW waves (QW = 2:
+// two workgroups of 32 rows, launched 8 indices apart so both run on one XCD
+// and the second fetch of each page hits its L2; QW = 4: one workgroup).
+// Wave group g (QW waves of 16 rows each) reads memory split g through a DMA
+// ring of its own, so four page streams and four MFMA -> softmax -> MFMA
+// chains run on the CU at once; the groups step through their pages
+// together, one workgroup barrier per page.  The in-block tile (in the ring's
+// layout) and the null row are staged in LDS at the start; the final split
+// (null row, then the in-block keys) is read by a group that has no page at
+// that step.  At the end the other groups hand their states (m, l, o) to
+// group 0 through the ring's LDS, and group 0 folds them in split order, the
+// final split last, with the merge's functions: every split is computed as in
+// the split launch and the folding launch, so all three give the same bits.
+template <int DH, int QW>
+struct ParLds {
+  using R = PageRing<DH>;
+  static constexpr int G = 4;                          // split groups
+  static constexpr int NSP = DH == 32 ? 4 : 2;         // ring stages per group
+  static constexpr int IPW = R::TILE / 1024 / QW;      // DMA instructions per wave per page
+  static constexpr int THREADS = 64 * G * QW;
+  static constexpr int ROWS = 16 * QW;                 // query rows per workgroup
+  static constexpr int RING = G * NSP * R::TILE;
+  static constexpr int OFF_IN = RING;                  // in-block tile, ring layout
+  static constexpr int OFF_NULL = OFF_IN + R::TILE;    // null key, then null value (bf16)
+  static constexpr int BYTES = OFF_NULL + 4 * DH;
+  // a split state per (slot, wave): o as DH/16 float4 planes of 64 lanes, then (m, l) pairs;
+  // slots 0..2 hold memory splits 1..3, slot 3 the final split
+  static constexpr int STATE = (DH / 16) * 1024 + 64 * 8;
+  static_assert(G * QW * STATE <= RING, "split states fit in the ring");
+  static_assert(BYTES <= 160 * 1024, "LDS");
+  static_assert(NSP >= 2 && NSP <= 4 && 3 * IPW < 64, "wait_pages covers up to 3 pages ahead");
+};
+
+template <int DH>
+__device__ __forceinline__ void state_put(uint8_t* st, const floatx4 (&o)[DH / 16], float m, float l, int lane) {
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) *(floatx4*)(st + (dt * 64 + lane) * 16) = o[dt];
+  *(f32x2*)(st + (DH / 16) * 1024 + lane * 8) = f32x2{m, l};
+}
+
+template <int DH>
+__device__ __forceinline__ void state_get(const uint8_t* st, floatx4 (&o)[DH / 16], float& m, float& l, int lane) {
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) o[dt] = *(const floatx4*)(st + (dt * 64 + lane) * 16);
+  const f32x2 ml = *(const f32x2*)(st + (DH / 16) * 1024 + lane * 8);
+  m = ml.x;
+  l = ml.y;
+}
+
+// Workgroups of a few-pair launch: 4/QW parts per pair, 8 pairs per round of
+// 8 x (4/QW) launch indices.
+inline int par_grid(int n_pairs, int qw) { return ((n_pairs + 7) / 8) * 8 * (4 / qw); }
+
+template <int DH, int QW>
+__global__ void __launch_bounds__(64 * 4 * QW) k_prefill_mfma_par(ReaderArgs a) {
+  using P = ParLds<DH, QW>;
+  using R = PageRing<DH>;
+  constexpr int NPART = 4 / QW;
+  __shared__ __attribute__((aligned(1024))) uint8_t L[P::BYTES];
+  const int n = blockIdx.x;
+  const int pair = (n / (8 * NPART)) * 8 + (n % 8), part = (n / 8) % NPART;
+  if (pair >= a.n_slots * a.H) return;   // padding of the last round (whole workgroup)
+  const int slot = pair / a.H, h = pair % a.H;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = wave / QW, qw = wave % QW;
+  const int n_read = a.n_read[slot], pps = a.pps[slot];
+  const int nms = (n_read + pps - 1) / pps;
+  const size_t rs = (size_t)a.H * DH;
+  const int row0 = part * P::ROWS + qw * 16;             // this wave's first query row
+  const int qrow = row0 + (lane & 15);
+  const int p0 = g * pps, p1 = min(n_read, p0 + pps);    // this group's split (empty when g >= nms)
+  // the final split is read by group fg at step fstep, when fg has no page
+  const int fg = nms < P::G ? nms : P::G - 1;
+  const int fstep = nms < P::G ? 0 : n_read - (P::G - 1) * pps;
+  const int steps = max(nms > 0 ? pps : 0, fstep + 1);
+
+  // ---- page DMA of this group's split: the whole ring at once
+  const __attribute__((address_space(4))) int32_t* lpc =
+      (const __attribute__((address_space(4))) int32_t*)(a.live_page + (size_t)a.seq[slot] * a.max_blocks);
+  uint32_t src[P::IPW];
+#pragma unroll
+  for (int i = 0; i < P::IPW; ++i) {
+    const int byte = (qw * P::IPW + i) * 1024 + lane * 16;
+    if (byte < R::KBYTES) {
+      const int r = byte / R::KRB, sl = (byte % R::KRB) >> 4;
+      src[i] = r * R::KRB + ((sl ^ R::kswz(r)) << 4);
+    } else {
+      const int vb = byte - R::KBYTES, d = vb >> 7, sl = (vb & 127) >> 4;
+      src[i] = R::KBYTES + d * 128 + ((sl ^ R::vswz(d)) << 4);
+    }
+  }
+  const uint8_t* gpages = (const uint8_t*)a.pages;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)L + (uint32_t)(g * P::NSP * R::TILE + qw * P::IPW * 1024);
+  auto issue = [&](int pi, int stage) {
+    const uint8_t* t = gpages + page_head_offset(lpc[pi], h, a.H, BT, DH) * 2;
+    const uint32_t d0 = lds0 + (uint32_t)(stage * R::TILE);
+#pragma unroll
+    for (int i = 0; i < P::IPW; ++i) dma16(t + src[i], __builtin_amdgcn_readfirstlane(d0 + i * 1024));
+  };
+#pragma unroll
+  for (int k = 0; k < P::NSP; ++k)
+    if (p0 + k < p1) issue(p0 + k, k);
+
+  // ---- query fragments; the in-block tile (ring layout) and the null row into LDS
+  bf16x8 qf[DH / 32];
+  load_q<DH>(qf, (const uint16_t*)a.q + ((size_t)slot * BT + row0) * rs + (size_t)h * DH, rs, lane);
+  uint8_t* tin = L + P::OFF_IN;
+  uint16_t* nul = (uint16_t*)(L + P::OFF_NULL);
+  constexpr int CPR = DH / 8;                            // 16-byte chunks per row
+  if (a.k_in != nullptr) {
+    const size_t base = (size_t)slot * BT * rs + (size_t)h * DH;
+    const uint16_t* kin = (const uint16_t*)a.k_in + base;
+    const uint16_t* vin = (const uint16_t*)a.v_in + base;
+    constexpr int NK = BT * CPR, NJ = NK + (BT / 2) * CPR;
+    for (int j = tid; j < NJ; j += P::THREADS) {
+      if (j < NK) {                                      // key chunk (row, c8)
+        const int row = j / CPR, c8 = j % CPR;
+        const u32x4 kv = *(const u32x4*)(kin + row * rs + c8 * 8);
+        *(u32x4*)(tin + row * R::KRB + ((c8 ^ R::kswz(row)) << 4)) = kv;
+      } else {                                           // value rows (2 pr, 2 pr + 1), chunk c8
+        const int pr = (j - NK) / CPR, c8 = (j - NK) % CPR;
+        const u32x4 va = *(const u32x4*)(vin + (2 * pr) * rs + c8 * 8);
+        const u32x4 vb = *(const u32x4*)(vin + (2 * pr + 1) * rs + c8 * 8);
+        const uint32_t a4[4] = {va.x, va.y, va.z, va.w};
+        const uint32_t b4[4] = {vb.x, vb.y, vb.z, vb.w};
+        const int key = 2 * pr;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int d = c8 * 8 + 2 * q;
+          uint8_t* r0 = tin + R::KBYTES + d * 128 + (key & 7) * 2;
+          uint8_t* r1 = tin + R::KBYTES + (d + 1) * 128 + (key & 7) * 2;
+          *(uint32_t*)(r0 + (((key >> 3) ^ R::vswz(d)) << 4)) = (a4[q] & 0xffffu) | (b4[q] << 16);
+          *(uint32_t*)(r1 + (((key >> 3) ^ R::vswz(d + 1)) << 4)) = (a4[q] >> 16) | (b4[q] & 0xffff0000u);
+        }
+      }
+    }
+  }
+  if (a.null_kv != nullptr && tid < 2 * CPR) {
+    const uint16_t* nsrc = (const uint16_t*)a.null_kv + (tid < CPR ? (size_t)h * DH + tid * 8
+                                                                   : ((size_t)a.H + h) * DH + (tid - CPR) * 8);
+    *(u32x4*)(nul + tid * 8) = *(const u32x4*)nsrc;
+  }
+
+  // ---- memory pages (all groups step together) and the final split
+  floatx4 o[DH / 16], of[DH / 16];
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) {
+    o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    of[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+  float m = -INFINITY, l = 0.f, mf = -INFINITY, lf = 0.f;
+  for (int k = 0; k < steps; ++k) {
+    const int pi = p0 + k;
+    wait_pages<P::IPW>(pi < p1 ? min(k == 0 ? P::NSP - 1 : P::NSP - 2, p1 - 1 - pi) : 0);
+    lds_barrier();                       // page k of every group is in LDS; every wave is done with page k - 1
+    if (k > 0 && pi + P::NSP - 1 < p1) issue(pi + P::NSP - 1, (k + P::NSP - 1) % P::NSP);
+    if (pi < p1) {
+      const uint8_t* tile = L + (g * P::NSP + k % P::NSP) * R::TILE;
+      floatx4 s[4];
+      scores_ring<DH>(s, tile, qf, lane);
+      online_step<DH, false>(s, m, l, o, lane, qrow, a.scale_log2);
+      pv_ring<DH>(o, tile, s, lane);
+    } else if (g == fg && k == fstep) {
+      if (a.null_kv != nullptr) null_row_at<DH, false>(nul, nul + DH, a, slot, qf, lane, mf, lf, of);
+      if (a.k_in != nullptr) {
+        floatx4 s[4];
+        scores_ring<DH>(s, tin, qf, lane);
+        online_step<DH, true>(s, mf, lf, of, lane, qrow, a.scale_log2);
+        pv_ring<DH>(of, tin, s, lane);
+      }
+    }
+  }
+  lds_barrier();                         // the ring is free
+  if (g > 0 && g < nms) state_put<DH>(L + ((g - 1) * QW + qw) * P::STATE, o, m, l, lane);
+  if (g == fg) state_put<DH>(L + (3 * QW + qw) * P::STATE, of, mf, lf, lane);
+  lds_barrier();
+  if (g == 0) {
+    uint16_t* orow = (uint16_t*)a.out + ((size_t)slot * BT + qrow) * rs + (size_t)h * DH;
+    // the state slots are read NPRE at a time ahead of their fold (slots of
+    // absent splits hold stale data and are not folded); at 16 waves the
+    // register budget allows one
+    constexpr int NPRE = QW == 2 ? 4 : 1;
+    floatx4 so[4][DH / 16];
+    float sm[4], sl[4];
+#pragma unroll
+    for (int j = 0; j < NPRE; ++j) state_get<DH>(L + (j * QW + qw) * P::STATE, so[j], sm[j], sl[j], lane);
+    if (nms > 0) {
+      floatx4 acc[DH / 16];
+      float fm, fl;
+      fold_split<DH>(true, m, l, o, fm, fl, acc);
+#pragma unroll
+      for (int j = 1; j < P::G; ++j) {
+        if (j < nms) {
+          if (j - 1 >= NPRE) state_get<DH>(L + ((j - 1) * QW + qw) * P::STATE, so[j - 1], sm[j - 1], sl[j - 1], lane);
+          fold_split<DH>(false, sm[j - 1], sl[j - 1], so[j - 1], fm, fl, acc);
+        }
+      }
+      if (3 >= NPRE) state_get<DH>(L + (3 * QW + qw) * P::STATE, so[3], sm[3], sl[3], lane);
+      fold_split<DH>(false, sm[3], sl[3], so[3], fm, fl, acc);
+      store_out<DH>(orow, acc, fl, lane);
+    } else {
+      if (3 >= NPRE) state_get<DH>(L + (3 * QW + qw) * P::STATE, so[3], sm[3], sl[3], lane);
+      store_out<DH>(orow, so[3], qsum(sl[3]), lane);
+    }
+  }
+}
+
 template <int DH>
 __global__ void __launch_bounds__(256) k_prefill_mfma(ReaderArgs a) {
   __shared__ PrefillLds<DH, false> L;
@@ -762,6 +1006,16 @@ static hipError_t launch_pre(const ReaderArgs& a, hipStream_t s) {
   for (int i = 0; i < a.n_slots; ++i) {
     const int ns = total_splits(a.n_read[i], a.pps[i]) - 1;
     if (ns > max_split) max_split = ns;
+  }
+  if (a.fuse == 2) {
+    constexpr int D = DH > 64 ? 64 : DH;                 // (no few-pair variant at d_h 128)
+    if (a.rope || DH > 64 || max_split > ParLds<D, 4>::G) return hipErrorInvalidValue;
+    const int n_pairs = a.n_slots * a.H;
+    if (n_pairs <= kParHalfPairs)
+      hipLaunchKernelGGL((k_prefill_mfma_par<D, 2>), dim3(par_grid(n_pairs, 2)), dim3(512), 0, s, a);
+    else
+      hipLaunchKernelGGL((k_prefill_mfma_par<D, 4>), dim3(par_grid(n_pairs, 4)), dim3(1024), 0, s, a);
+    return hipGetLastError();
   }
   if (a.fuse) {
     if (a.rope) return hipErrorInvalidValue;

@@ -559,3 +559,77 @@ def test_export_indexing_and_transpose(b, dh, es):
         for cc in range(CR):
             off = ((r // E) ^ (cc % CB)) * E + r % E
             assert [tile[(cc * E + j) * b + off] for j in range(E)] == [(cc * E + j, r) for j in range(E)]
+
+
+@pytest.mark.parametrize("dh,qw", [(32, 2), (32, 4), (64, 2), (64, 4)])
+def test_prefill_par_lds_and_thread_ranges(dh, qw):
+    """The few-pair prefill (4 wave groups of qw waves): each group's DMA ring,
+    the in-block tile, the null row and the split-state slots stay inside the
+    workgroup's LDS; the in-block keys and transposed values are written once
+    each, where the ring's key and value operand reads look for them; the
+    launch indices cover every (pair, part) once, the parts of a pair on one
+    XCD; every query row is owned by one wave."""
+    BT, G = 64, 4
+    NSP = 4 if dh == 32 else 2
+    TILE, KBYTES, KRB, KCH = 2 * BT * dh * 2, BT * dh * 2, dh * 2, dh // 8
+    IPW = TILE // 1024 // qw
+    THREADS, ROWS = 64 * G * qw, 16 * qw
+    RING = G * NSP * TILE
+    OFF_IN = RING
+    OFF_NULL = OFF_IN + TILE
+    BYTES = OFF_NULL + 4 * dh
+    STATE = (dh // 16) * 1024 + 64 * 8
+    assert BYTES <= 160 * 1024 and G * qw * STATE <= RING and 3 * IPW < 64
+    kswz = lambda r: (r // (256 // KRB)) % KCH
+    vswz = lambda d: (d >> 1) & 7
+    seen = set()
+    for g, w, stage, i, lane in itertools.product(range(G), range(qw), range(NSP), range(IPW), range(64)):
+        lds = g * NSP * TILE + w * IPW * 1024 + stage * TILE + i * 1024 + lane * 16
+        assert 0 <= lds and lds + 16 <= RING and lds not in seen
+        seen.add(lds)
+    assert len(seen) * 16 == RING
+    CPR = dh // 8
+    NK, NJ = BT * CPR, BT * CPR + (BT // 2) * CPR
+    keys, vals = {}, {}
+    for tid in range(THREADS):
+        for j in range(tid, NJ, THREADS):
+            if j < NK:
+                row, c8 = j // CPR, j % CPR
+                off = row * KRB + ((c8 ^ kswz(row)) << 4)
+                assert 0 <= off and off + 16 <= KBYTES and off not in keys
+                keys[off] = (row, c8)
+            else:
+                pr, c8 = (j - NK) // CPR, (j - NK) % CPR
+                key = 2 * pr
+                for q in range(4):
+                    for d in (c8 * 8 + 2 * q, c8 * 8 + 2 * q + 1):
+                        off = KBYTES + d * 128 + (((key >> 3) ^ vswz(d)) << 4) + (key & 7) * 2
+                        assert KBYTES <= off and off + 4 <= TILE and off not in vals
+                        vals[off] = (d, key)
+    assert len(keys) * 16 == KBYTES and len(vals) * 4 == TILE - KBYTES
+    for lane, kt, kk in itertools.product(range(64), range(4), range(dh // 32)):   # scores_ring's reads
+        r, c = kt * 16 + (lane & 15), kk * 4 + (lane >> 4)
+        assert keys[r * KRB + ((c ^ kswz(r)) << 4)] == (r, c)
+    for lane, dt, q in itertools.product(range(64), range(dh // 16), range(4)):      # pv_ring's reads
+        gg, d = lane >> 4, dt * 16 + (lane & 15)
+        off = KBYTES + d * 128 + ((((gg >> 1) + 2 * q) ^ vswz(d)) << 4) + (gg & 1) * 8
+        assert vals[off] == (d, 4 * gg + 16 * q) and vals[off + 4] == (d, 4 * gg + 16 * q + 2)
+    assert 2 * CPR <= THREADS and OFF_NULL + 2 * CPR * 16 <= BYTES                    # null row
+    for j, w in itertools.product(range(4), range(qw)):                               # split states
+        base = (j * qw + w) * STATE
+        assert base + (dh // 16 - 1) * 1024 + 63 * 16 + 16 <= RING
+        assert base + (dh // 16) * 1024 + 63 * 8 + 8 <= (j * qw + w + 1) * STATE
+    npart = 4 // qw
+    for n_pairs in (1, 7, 8, 9, 96, 128, 511):
+        grid = ((n_pairs + 7) // 8) * 8 * npart
+        got = {}
+        for n in range(grid):
+            pair, part = (n // (8 * npart)) * 8 + n % 8, (n // 8) % npart
+            if pair >= n_pairs:
+                continue
+            assert (pair, part) not in got
+            got[(pair, part)] = n % 8                   # the XCD the index lands on
+        assert len(got) == n_pairs * npart
+        assert all(got[(p, 0)] == got[(p, k)] for p in range(n_pairs) for k in range(npart))
+    rows = sorted(part * ROWS + w * 16 + r for part in range(npart) for w in range(qw) for r in range(16))
+    assert rows == list(range(BT))
