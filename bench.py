@@ -62,8 +62,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
-MFMA_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
-BF16_PEAK_TFLOPS = 2516.6      # MI355X dense bf16 MFMA, published
+MFMA_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published (2.5 PFLOP/s, no sparsity)
 
 # HBM bytes per decode call measured with rocprofv3 FETCH_SIZE/WRITE_SIZE
 # (scaled by a plain copy of known size), keyed by a hash of the decode
@@ -513,6 +512,95 @@ def stress_workload(args, torch, smem, synth):
                 export_hbm_frac=ex_bytes / ex_secs / 1e9 / HBM_PEAK_GBS)
 
 
+def delete_sweep_workload(args, torch, smem, synth):
+    """Deletion latency against the number of cached blocks of one sequence
+    (the paper's deletion-latency sweep, 512 to 65,536 blocks): a store of
+    1.5B-shaped pages (16 heads x d_h 128, b = 64, 512 KiB a page) holding
+    every block, then seeded single-block deletions at random indices (one
+    at index 0, the whole live list behind it), each followed by the block's
+    re-insertion.  Per size: the call as the host sees it (wall clock around
+    the C call), the device time of its kernels (events around the call
+    enqueued behind a running kernel), and delete with scrub (the freed page
+    zeroed); a batch-1 decode over the remaining rows after a deletion is
+    timed too.  Page contents do not enter deletion; every page holds the
+    same seeded rows."""
+    w = synth.STRESS_1P5B
+    H, dh, b = w.H, w.dh, w.b
+    dt = torch.bfloat16
+    L = smem.lib()
+    stream = torch.cuda.current_stream()
+    raw = ctypes.c_void_p(stream.cuda_stream)
+    g = synth.rng(args.seed, w.wid, synth.ROLE_EDIT, 5, 0, 0)
+    chunk = 128
+    rows = torch.from_numpy(synth.bf16_round((g.standard_normal((chunk * b, H, dh)) * w.scale).astype(np.float32)))
+    rows = rows.to("cuda").to(dt)
+    busy = torch.empty(64 << 20, dtype=torch.float32, device="cuda")
+    out = {}
+    for NB in [int(x) for x in args.delete_sizes.split(",")]:
+        st = smem.Store(1, NB, NB, b, H, dh, dt)
+        for j0 in range(0, NB, chunk):
+            n = min(chunk, NB - j0)
+            smem.smem_store_put_blocks(st, [0] * n, list(range(j0, j0 + n)), rows[: n * b], rows[: n * b])
+        torch.cuda.synchronize()
+        order = [0] + [int(x) for x in g.integers(0, NB, 24)]
+        host_us, wall_us, dev_us, scrub_us, reins_us = [], [], [], [], []
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for it, j in enumerate(order):
+            # device time: the call enqueued while a kernel still runs
+            torch.cuda.synchronize()
+            busy.mul_(1.0)
+            e0.record(stream)
+            smem.check_status(L.smem_delete_block(st.handle, 0, j, 0, raw))
+            e1.record(stream)
+            e1.synchronize()
+            dev_us.append(e0.elapsed_time(e1) * 1e3)
+            smem.check_status(L.smem_store_put_block(st.handle, 0, j, ctypes.c_void_p(rows.data_ptr()),
+                                                     ctypes.c_void_p(rows.data_ptr()), raw))
+            # the call on an idle GPU: host time and wall time to completion
+            torch.cuda.synchronize()
+            e0.record(stream)
+            t0 = time.perf_counter()
+            smem.check_status(L.smem_delete_block(st.handle, 0, j, 0, raw))
+            t1 = time.perf_counter()
+            e1.record(stream)
+            e1.synchronize()
+            host_us.append((t1 - t0) * 1e6)
+            wall_us.append(e0.elapsed_time(e1) * 1e3)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            smem.check_status(L.smem_store_put_block(st.handle, 0, j, ctypes.c_void_p(rows.data_ptr()),
+                                                     ctypes.c_void_p(rows.data_ptr()), raw))
+            e1.record(stream)
+            e1.synchronize()
+            reins_us.append(e0.elapsed_time(e1) * 1e3)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            smem.check_status(L.smem_delete_block(st.handle, 0, j, 1, raw))
+            e1.record(stream)
+            e1.synchronize()
+            scrub_us.append(e0.elapsed_time(e1) * 1e3)
+            smem.check_status(L.smem_store_put_block(st.handle, 0, j, ctypes.c_void_p(rows.data_ptr()),
+                                                     ctypes.c_void_p(rows.data_ptr()), raw))
+        # a read after a deletion: batch-1 decode over the remaining rows
+        smem.check_status(L.smem_delete_block(st.handle, 0, order[-1], 0, raw))
+        q = rows[:1].contiguous()
+        dout = torch.empty_like(q)
+        for _ in range(2):
+            smem.smem_reader_decode(st, [0], [NB], None, q, out=dout)
+        reps = 5
+        read_s = _events_time(lambda t: smem.smem_reader_decode(st, [0], [NB], None, q, out=dout), reps, stream) / reps
+        st.close()
+        med = lambda xs: float(np.median(xs))
+        out[str(NB)] = dict(delete_device_us=round(med(dev_us), 2), delete_host_us=round(med(host_us), 2),
+                            delete_idle_gpu_us=round(med(wall_us), 2), delete_front_device_us=round(dev_us[0], 2),
+                            delete_scrub_idle_gpu_us=round(med(scrub_us), 2),
+                            reinsert_idle_gpu_us=round(med(reins_us), 2),
+                            read_after_delete_ms=round(read_s * 1e3, 4),
+                            read_gbs=round((NB - 1) * H * 2 * b * dh * 2 / read_s / 1e9, 1))
+    del busy
+    return out
+
+
 def model_workload(args, torch, smem, synth):
     """Whole model at random weights (Appendix A scales): block-skip serving
     of a fully cached context (the reader on the final block alone) against
@@ -755,11 +843,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-secondary", action="store_true")
-    ap.add_argument("--workloads", default="encode,serve,stream,rows,stress,rope,model,model_decode",
+    ap.add_argument("--workloads", default="encode,serve,stream,rows,stress,delete_sweep,rope,model,model_decode",
                     help="secondary workloads to run (comma list of encode, serve, stream, rows, stress, rope: "
                          "the rotary composite timed beside the headline decode and the serve; model: the whole "
                          "model's block-skip serve against its cold prefill; model_decode: the whole model's "
-                         "batched KV-cached decode at the paper's cells)")
+                         "batched KV-cached decode at the paper's cells; delete_sweep: deletion latency from "
+                         "512 to 65,536 cached blocks)")
+    ap.add_argument("--delete-sizes", default="512,1024,4096,16384,65536")
     ap.add_argument("--model-scales", default="160M,410M,1.5B")
     ap.add_argument("--model-lengths", default="1024,2048,4096,8192")
     ap.add_argument("--model-reps", type=int, default=3)
@@ -805,6 +895,8 @@ def main():
             secondary["rope_decode_410M"] = dec["rope"]
         if "stress" in wl:
             secondary["stress_1p5B"] = stress_workload(args, torch, smem, synth)
+        if "delete_sweep" in wl:
+            secondary["delete_sweep_1p5B_pages"] = delete_sweep_workload(args, torch, smem, synth)
         if "model" in wl:
             secondary["model_block_skip"] = model_workload(args, torch, smem, synth)
         if "model_decode" in wl:

@@ -17,8 +17,13 @@ namespace smem {
 // arguments (sequence ids, block counts, positions).  Larger batches are
 // split into several launches by the host.
 constexpr int kMaxSlots = 128;
-// Edits applied by one metadata launch.
+// Edits applied by one metadata launch, and its (sequence, table chunk) work
+// items: each item is one workgroup that applies the edits falling in its
+// chunk of kMetaChunk table entries and writes the chunk's live blocks into
+// the dense lists at a position the host computes.
 constexpr int kMaxEdits = 128;
+constexpr int kMaxMetaItems = 128;
+constexpr int kMetaChunk = 1024;
 // Split-K: memory pages of one (query, head) are cut into at most kSplitCap
 // splits of whole pages, plus possibly one split for the null row and the
 // in-block keys.
@@ -342,11 +347,14 @@ struct MetaArgs {
   int32_t* n_live;
   int32_t max_blocks;
   int32_t n_edits;
-  int32_t n_seqs;                 // sequences to rebuild (one workgroup each)
+  int32_t n_items;                // work items (one workgroup each)
   int32_t e_seq[kMaxEdits];
   int32_t e_blk[kMaxEdits];
   int32_t e_page[kMaxEdits];      // -1: delete
-  int32_t r_seq[kMaxEdits];
+  int32_t i_seq[kMaxMetaItems];   // item: sequence
+  int32_t i_chunk[kMaxMetaItems]; //       table entries i_chunk*kMetaChunk ..
+  int32_t i_base[kMaxMetaItems];  //       list position of the chunk's first live block
+  int8_t i_last[kMaxMetaItems];   //       1: the last chunk that can hold a live block (writes n_live)
 };
 
 // ---------------------------------------------------------------- launchers

@@ -23,6 +23,75 @@
 
 using namespace smem;
 
+namespace {
+
+// Live block indices of one sequence: a bitset over 0..max_blocks-1 and a
+// Fenwick tree over the words' popcounts, so an insert, a delete, the rank
+// of an index (how many live blocks lie below it) and the position of the
+// k-th live block each cost O(log max_blocks), whatever the table's size.
+class LiveSet {
+ public:
+  void init(int n) {
+    n_ = n;
+    count_ = 0;
+    w_.assign((size_t)(n + 63) / 64, 0);
+    f_.assign(w_.size() + 1, 0);
+  }
+  int size() const { return count_; }
+  bool contains(int j) const { return (w_[(size_t)j >> 6] >> (j & 63)) & 1u; }
+  void insert(int j) {
+    w_[(size_t)j >> 6] |= 1ull << (j & 63);
+    add((int)(j >> 6), 1);
+    ++count_;
+  }
+  void erase(int j) {
+    w_[(size_t)j >> 6] &= ~(1ull << (j & 63));
+    add((int)(j >> 6), -1);
+    --count_;
+  }
+  // live indices below J
+  int rank(int J) const {
+    if (J <= 0) return 0;
+    if (J >= n_) return count_;
+    const int wi = J >> 6;
+    const uint64_t below = (J & 63) ? (w_[(size_t)wi] & ((1ull << (J & 63)) - 1)) : 0ull;
+    return prefix(wi) + __builtin_popcountll(below);
+  }
+  // index of the k-th live block (0-based), k < size()
+  int select(int k) const {
+    int pos = 0, step = 1;
+    while (step * 2 <= (int)w_.size()) step *= 2;
+    for (; step > 0; step >>= 1)               // largest word count whose prefix sum is <= k
+      if (pos + step <= (int)w_.size() && f_[(size_t)(pos + step)] <= k) {
+        pos += step;
+        k -= f_[(size_t)pos];
+      }
+    uint64_t w = w_[(size_t)pos];
+    for (int i = 0; i < k; ++i) w &= w - 1;    // drop the k lowest set bits
+    return pos * 64 + __builtin_ctzll(w);
+  }
+  // live indices in ascending order
+  void copy_to(int32_t* out) const {
+    for (size_t wi = 0; wi < w_.size(); ++wi)
+      for (uint64_t w = w_[wi]; w; w &= w - 1) *out++ = (int32_t)(wi * 64 + __builtin_ctzll(w));
+  }
+
+ private:
+  void add(int wi, int d) {
+    for (int i = wi + 1; i <= (int)w_.size(); i += i & -i) f_[(size_t)i] += d;
+  }
+  int prefix(int wi) const {                   // live blocks in words 0..wi-1
+    int r = 0;
+    for (int i = wi; i > 0; i -= i & -i) r += f_[(size_t)i];
+    return r;
+  }
+  int n_ = 0, count_ = 0;
+  std::vector<uint64_t> w_;
+  std::vector<int32_t> f_;
+};
+
+}  // namespace
+
 struct smem_store {
   smem_store_desc d;          // row stores: H = 1, dh = 0; the row width is rows_d
   int kind = 0;               // 0: key/value planes, 1: rows of width rows_d
@@ -37,7 +106,7 @@ struct smem_store {
   float* d_ws = nullptr;
   void* d_pages = nullptr;
   std::vector<int32_t> table;              // [n_seq * max_blocks]: page or -1
-  std::vector<std::vector<int32_t>> live;  // per sequence, ascending block indices
+  std::vector<LiveSet> live;               // per sequence, the live block indices
   std::vector<int32_t> free_pages;         // stack; back() is handed out next
 };
 
@@ -170,36 +239,69 @@ void rope_args(ReaderArgs& a, const smem_store* st, const smem_rope* rope) {
   a.rope_clip = rope->d.max_offset > 0 ? rope->d.max_offset : INT32_MAX;
 }
 
-int n_read_of(const smem_store* st, int seq, int J) {
-  const auto& lv = st->live[seq];
-  return (int)(std::lower_bound(lv.begin(), lv.end(), J) - lv.begin());
-}
+int n_read_of(const smem_store* st, int seq, int J) { return st->live[seq].rank(J); }
 
-// Apply edits (seq, blk, page or -1) on the device: table entries, then
-// rebuild the affected sequences' live lists.
+// Apply edits (seq, blk, page or -1) on the device: table entries, then the
+// affected part of each edited sequence's dense live list.  Called before the
+// host metadata takes the edits, so the list positions after them are the
+// host's current ranks plus the edits' own shifts.  Only the table chunks
+// from the first edited one up to the sequence's last live block are
+// rewritten, each by its own workgroup, so an edit's cost does not grow with
+// the table.
 smem_status push_edits(smem_store* st, const std::vector<int32_t>& es, const std::vector<int32_t>& eb,
                        const std::vector<int32_t>& ep, hipStream_t s) {
+  const int mb = st->d.max_blocks;
+  const int n_chunks = (mb + kMetaChunk - 1) / kMetaChunk;
   for (size_t i0 = 0; i0 < es.size(); i0 += kMaxEdits) {
+    const size_t i1 = std::min(es.size(), i0 + (size_t)kMaxEdits);
     MetaArgs a;
     memset(&a, 0, sizeof a);
     a.table = st->d_table;
     a.live_page = st->d_live_page;
     a.live_blk = st->d_live_blk;
     a.n_live = st->d_n_live;
-    a.max_blocks = st->d.max_blocks;
-    const size_t n = std::min((size_t)kMaxEdits, es.size() - i0);
-    a.n_edits = (int32_t)n;
+    a.max_blocks = mb;
+    a.n_edits = (int32_t)(i1 - i0);
     std::set<int32_t> seqs;
-    for (size_t i = 0; i < n; ++i) {
-      a.e_seq[i] = es[i0 + i];
-      a.e_blk[i] = eb[i0 + i];
-      a.e_page[i] = ep[i0 + i];
-      seqs.insert(es[i0 + i]);
+    for (size_t i = i0; i < i1; ++i) {
+      a.e_seq[i - i0] = es[i];
+      a.e_blk[i - i0] = eb[i];
+      a.e_page[i - i0] = ep[i];
+      seqs.insert(es[i]);
     }
-    a.n_seqs = 0;
-    for (int32_t q : seqs) a.r_seq[a.n_seqs++] = q;
-    hipError_t e = launch_meta(a, s);
-    if (e != hipSuccess) return hip_fail(e, "metadata update");
+    auto flush = [&]() -> smem_status {
+      hipError_t e = launch_meta(a, s);
+      if (e != hipSuccess) return hip_fail(e, "metadata update");
+      a.n_items = 0;
+      return SMEM_OK;
+    };
+    for (int32_t q : seqs) {
+      const LiveSet& lv = st->live[q];
+      // chunks from the first edited one to the last that can hold a live block
+      int c0 = n_chunks, c1 = lv.size() > 0 ? lv.select(lv.size() - 1) / kMetaChunk : 0;
+      for (size_t i = i0; i < i1; ++i)
+        if (es[i] == q) c0 = std::min(c0, eb[i] / kMetaChunk);
+      for (size_t i = 0; i < i1; ++i)
+        if (es[i] == q) c1 = std::max(c1, eb[i] / kMetaChunk);
+      for (int c = c0; c <= c1; ++c) {
+        // list position of the chunk's first live block once edits 0 .. i1 - 1 are in
+        int base = lv.rank(c * kMetaChunk);
+        for (size_t i = 0; i < i1; ++i)
+          if (es[i] == q && eb[i] < c * kMetaChunk) base += ep[i] >= 0 ? 1 : -1;
+        a.i_seq[a.n_items] = q;
+        a.i_chunk[a.n_items] = c;
+        a.i_base[a.n_items] = base;
+        a.i_last[a.n_items] = c == c1;
+        if (++a.n_items == kMaxMetaItems) {
+          const smem_status r = flush();
+          if (r != SMEM_OK) return r;
+        }
+      }
+    }
+    if (a.n_items > 0) {
+      const smem_status r = flush();
+      if (r != SMEM_OK) return r;
+    }
   }
   return SMEM_OK;
 }
@@ -248,7 +350,8 @@ smem_status smem_store_create(const smem_store_desc* desc, void* dev_pool, size_
   st->lay = L;
   st->meta_only = dev_pool == nullptr;
   st->table.assign((size_t)desc->n_seq * desc->max_blocks, -1);
-  st->live.assign(desc->n_seq, {});
+  st->live.assign(desc->n_seq, LiveSet());
+  for (auto& lv : st->live) lv.init(desc->max_blocks);
   st->free_pages.resize(desc->n_pages);
   for (int i = 0; i < desc->n_pages; ++i) st->free_pages[i] = desc->n_pages - 1 - i;
   if (!st->meta_only) {
@@ -307,8 +410,7 @@ smem_status smem_store_put_block(smem_store* st, int32_t seq, int32_t block_idx,
   }
   st->free_pages.pop_back();
   st->table[ti] = page;
-  auto& lv = st->live[seq];
-  lv.insert(std::lower_bound(lv.begin(), lv.end(), block_idx), block_idx);
+  st->live[seq].insert(block_idx);
   return SMEM_OK;
 }
 
@@ -356,8 +458,7 @@ smem_status smem_store_put_blocks(smem_store* st, int32_t n_blocks, const int32_
   st->free_pages.resize(st->free_pages.size() - n_blocks);
   for (int i = 0; i < n_blocks; ++i) {
     st->table[(size_t)seq_ids[i] * d.max_blocks + block_idx[i]] = pages[i];
-    auto& lv = st->live[seq_ids[i]];
-    lv.insert(std::lower_bound(lv.begin(), lv.end(), block_idx[i]), block_idx[i]);
+    st->live[seq_ids[i]].insert(block_idx[i]);
   }
   return SMEM_OK;
 }
@@ -380,8 +481,7 @@ smem_status smem_delete_block(smem_store* st, int32_t seq, int32_t block_idx, in
     }
   }
   st->table[ti] = -1;
-  auto& lv = st->live[seq];
-  lv.erase(std::lower_bound(lv.begin(), lv.end(), block_idx));
+  st->live[seq].erase(block_idx);
   st->free_pages.push_back(page);
   return SMEM_OK;
 }
@@ -397,7 +497,7 @@ smem_status smem_store_export(smem_store* st, int32_t seq, int32_t* live_idx, in
   if (k_out && st->meta_only) return fail(SMEM_EINVAL, "metadata-only store has no rows to export");
   const auto& lv = st->live[seq];
   if (n_live) *n_live = (int32_t)lv.size();
-  if (live_idx) std::copy(lv.begin(), lv.end(), live_idx);
+  if (live_idx) lv.copy_to(live_idx);
   if (k_out) {
     hipError_t e = launch_export(d.dtype, st->d_pages, st->d_live_page + (size_t)seq * d.max_blocks,
                                  (int)lv.size(), d.H, d.b, d.dh, k_out, v_out, s);
@@ -503,8 +603,7 @@ static smem_status encode_impl(smem_store* st, const smem_attn_desc* shape, int3
     st->free_pages.resize(st->free_pages.size() - n_blocks);
     for (int i = 0; i < n_blocks; ++i) {
       st->table[(size_t)seq_ids[i] * st->d.max_blocks + block_idx[i]] = pages[i];
-      auto& lv = st->live[seq_ids[i]];
-      lv.insert(std::lower_bound(lv.begin(), lv.end(), block_idx[i]), block_idx[i]);
+      st->live[seq_ids[i]].insert(block_idx[i]);
     }
   }
   return SMEM_OK;
@@ -765,7 +864,8 @@ smem_status smem_rows_create(const smem_rows_desc* desc, void* dev_pool, size_t 
   st->rows_d = desc->d;
   st->lay = L;
   st->table.assign((size_t)desc->n_seq * desc->max_blocks, -1);
-  st->live.assign(desc->n_seq, {});
+  st->live.assign(desc->n_seq, LiveSet());
+  for (auto& lv : st->live) lv.init(desc->max_blocks);
   st->free_pages.resize(desc->n_pages);
   for (int i = 0; i < desc->n_pages; ++i) st->free_pages[i] = desc->n_pages - 1 - i;
   st->pool = (char*)dev_pool;
@@ -802,8 +902,7 @@ smem_status smem_rows_put_block(smem_store* st, int32_t seq, int32_t block_idx, 
   if (r != SMEM_OK) return r;
   st->free_pages.pop_back();
   st->table[ti] = page;
-  auto& lv = st->live[seq];
-  lv.insert(std::lower_bound(lv.begin(), lv.end(), block_idx), block_idx);
+  st->live[seq].insert(block_idx);
   return SMEM_OK;
 }
 
@@ -815,11 +914,13 @@ smem_status smem_rows_export(smem_store* st, int32_t seq, int32_t* live_idx, int
   if (!aligned16(rows_out)) return fail(SMEM_EINVAL, "rows_out must be 16-byte aligned");
   const auto& lv = st->live[seq];
   if (n_live) *n_live = (int32_t)lv.size();
-  if (live_idx) std::copy(lv.begin(), lv.end(), live_idx);
+  if (live_idx) lv.copy_to(live_idx);
   if (rows_out) {
     const size_t pb = page_bytes(st);
-    for (size_t i = 0; i < lv.size(); ++i) {
-      const int32_t page = st->table[(size_t)seq * st->d.max_blocks + lv[i]];
+    std::vector<int32_t> idx((size_t)lv.size());
+    lv.copy_to(idx.data());
+    for (size_t i = 0; i < idx.size(); ++i) {
+      const int32_t page = st->table[(size_t)seq * st->d.max_blocks + idx[i]];
       hipError_t e = launch_copy16((char*)rows_out + i * pb, (const char*)st->d_pages + (size_t)page * pb, pb, s);
       if (e != hipSuccess) return hip_fail(e, "row export");
     }

@@ -31,63 +31,61 @@ hipError_t launch_init_meta(int32_t* table, int32_t* n_live, size_t n_table, int
   return hipGetLastError();
 }
 
-// One workgroup per sequence to rebuild: apply this launch's edits of that
-// sequence to the table, then compact the table into the live lists.  Each
-// thread takes 16 consecutive table entries per 4096-entry chunk, so a table
-// of up to 4096 blocks is compacted in one scan (wave prefix sums by shuffle,
-// wave totals through LDS).
-constexpr int kMetaPerThread = 16;
+// One workgroup per (sequence, table chunk) item: apply this launch's edits
+// that fall in the chunk to the table, then write the chunk's live blocks,
+// in index order, into the dense lists from the position the host computed
+// for it (the live blocks of the earlier chunks, after the edits).  Each
+// thread takes kMetaPerThread consecutive entries; offsets inside the chunk
+// come from wave prefix sums (shuffles) and wave totals in LDS.
+constexpr int kMetaPerThread = kMetaChunk / 256;
 
 __global__ void __launch_bounds__(256) k_meta(MetaArgs a) {
-  const int seq = a.r_seq[blockIdx.x];
+  const int it = blockIdx.x;
+  const int seq = a.i_seq[it];
+  const int j0 = a.i_chunk[it] * kMetaChunk;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int32_t* trow = a.table + (size_t)seq * a.max_blocks;
   for (int e = tid; e < a.n_edits; e += 256)
-    if (a.e_seq[e] == seq) trow[a.e_blk[e]] = a.e_page[e];
+    if (a.e_seq[e] == seq && a.e_blk[e] >= j0 && a.e_blk[e] < j0 + kMetaChunk) trow[a.e_blk[e]] = a.e_page[e];
   __syncthreads();
 
   __shared__ int wave_tot[4];
   int32_t* lp = a.live_page + (size_t)seq * a.max_blocks;
   int32_t* lb = a.live_blk + (size_t)seq * a.max_blocks;
-  int base = 0;
-  for (int c0 = 0; c0 < a.max_blocks; c0 += 256 * kMetaPerThread) {
-    const int j0 = c0 + tid * kMetaPerThread;
-    int32_t v[kMetaPerThread];
-    int cnt = 0;
+  const int jt = j0 + tid * kMetaPerThread;
+  int32_t v[kMetaPerThread];
+  int cnt = 0;
 #pragma unroll
-    for (int e = 0; e < kMetaPerThread; ++e) {
-      const int j = j0 + e;
-      v[e] = (j < a.max_blocks) ? trow[j] : -1;
-      cnt += v[e] >= 0 ? 1 : 0;
-    }
-    int incl = cnt;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(incl, o);
-      if (lane >= o) incl += y;
-    }
-    if (lane == 63) wave_tot[wave] = incl;
-    __syncthreads();
-    int off = base + incl - cnt;
-    for (int w = 0; w < wave; ++w) off += wave_tot[w];
-    const int total = wave_tot[0] + wave_tot[1] + wave_tot[2] + wave_tot[3];
-#pragma unroll
-    for (int e = 0; e < kMetaPerThread; ++e) {
-      if (v[e] >= 0) {
-        lp[off] = v[e];
-        lb[off] = j0 + e;
-        ++off;
-      }
-    }
-    base += total;
-    __syncthreads();
+  for (int e = 0; e < kMetaPerThread; ++e) {
+    const int j = jt + e;
+    v[e] = (j < a.max_blocks) ? trow[j] : -1;
+    cnt += v[e] >= 0 ? 1 : 0;
   }
-  if (tid == 0) a.n_live[seq] = base;
+  int incl = cnt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) wave_tot[wave] = incl;
+  __syncthreads();
+  int off = a.i_base[it] + incl - cnt;
+  for (int w = 0; w < wave; ++w) off += wave_tot[w];
+#pragma unroll
+  for (int e = 0; e < kMetaPerThread; ++e) {
+    if (v[e] >= 0) {
+      lp[off] = v[e];
+      lb[off] = jt + e;
+      ++off;
+    }
+  }
+  if (a.i_last[it] && tid == 0)
+    a.n_live[seq] = a.i_base[it] + wave_tot[0] + wave_tot[1] + wave_tot[2] + wave_tot[3];
 }
 
 hipError_t launch_meta(const MetaArgs& a, hipStream_t s) {
-  if (a.n_seqs <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_meta, dim3(a.n_seqs), dim3(256), 0, s, a);
+  if (a.n_items <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_meta, dim3(a.n_items), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -633,3 +633,88 @@ def test_prefill_par_lds_and_thread_ranges(dh, qw):
         assert all(got[(p, 0)] == got[(p, k)] for p in range(n_pairs) for k in range(npart))
     rows = sorted(part * ROWS + w * 16 + r for part in range(npart) for w in range(qw) for r in range(16))
     assert rows == list(range(BT))
+
+
+def _meta_items(live, edits, mb, chunk=1024, max_edits=128, max_items=128):
+    """The host side of a metadata update (push_edits): per group of edits,
+    (sequence, chunk, base, last) items from the host's live sets before the
+    edits; returns the launches as (edits, items)."""
+    import bisect
+    launches = []
+    n_chunks = (mb + chunk - 1) // chunk
+    for i0 in range(0, len(edits), max_edits):
+        i1 = min(len(edits), i0 + max_edits)
+        group = edits[i0:i1]
+        items = []
+        for q in sorted({e[0] for e in group}):
+            lv = live[q]
+            c0 = min([b // chunk for s, b, _ in group if s == q] + [n_chunks])
+            c1 = max([lv[-1] // chunk if lv else 0] + [b // chunk for s, b, _ in edits[:i1] if s == q])
+            for c in range(c0, c1 + 1):
+                base = bisect.bisect_left(lv, c * chunk)
+                base += sum(1 if p >= 0 else -1 for s, b, p in edits[:i1] if s == q and b < c * chunk)
+                items.append((q, c, base, c == c1))
+        for k in range(0, len(items), max_items):
+            launches.append((group, items[k:k + max_items]))
+    return launches
+
+
+def _meta_kernel(table, live_page, live_blk, n_live, mb, group, items, chunk=1024):
+    """k_meta: each item applies its chunk's edits, then writes the chunk's live
+    blocks at the host's position; every access is checked against the arrays."""
+    for q, c, base, last in items:
+        j0 = c * chunk
+        for s, b, p in group:
+            if s == q and j0 <= b < j0 + chunk:
+                table[q][b] = p
+        off = base
+        for j in range(j0, min(mb, j0 + chunk)):
+            if table[q][j] >= 0:
+                assert 0 <= off < mb
+                live_page[q][off], live_blk[q][off] = table[q][j], j
+                off += 1
+        if last:
+            n_live[q] = off
+
+
+@pytest.mark.parametrize("mb,n_seq", [(64, 3), (1024, 2), (4096, 2), (65536, 1)])
+def test_metadata_chunk_rebuild_equals_full_rebuild(mb, n_seq):
+    """Deletions and insertions (single and in batches of more than 128 edits,
+    across sequences): the chunked metadata rebuild leaves the dense live
+    lists and counts equal to a full rebuild from the table."""
+    import bisect
+    import random
+    rnd = random.Random(mb)
+    table = [[-1] * mb for _ in range(n_seq)]
+    live_page = [[-7] * mb for _ in range(n_seq)]
+    live_blk = [[-7] * mb for _ in range(n_seq)]
+    n_live = [0] * n_seq
+    live = [[] for _ in range(n_seq)]
+    free = list(range(n_seq * mb))
+    rnd.shuffle(free)
+
+    def apply(edits):
+        for group, items in _meta_items(live, edits, mb):
+            _meta_kernel(table, live_page, live_blk, n_live, mb, group, items)
+        for s, b, p in edits:                      # the host update after the launches
+            if p >= 0:
+                bisect.insort(live[s], b)
+            else:
+                live[s].remove(b)
+        for q in range(n_seq):
+            assert n_live[q] == len(live[q])
+            assert live_blk[q][:n_live[q]] == live[q]
+            assert live_page[q][:n_live[q]] == [table[q][j] for j in live[q]]
+
+    # a batch insert of many blocks (several groups of 128 edits, several sequences)
+    first = [(q, b, free.pop()) for q in range(n_seq) for b in rnd.sample(range(mb), min(mb, 300))]
+    apply(first)
+    for _ in range(40):                              # single edits anywhere, as the store does them
+        q = rnd.randrange(n_seq)
+        if live[q] and rnd.random() < 0.6:
+            apply([(q, rnd.choice(live[q]), -1)])
+        else:
+            absent = rnd.randrange(mb)
+            if absent not in live[q]:
+                apply([(q, absent, free.pop())])
+    apply([(q, b, -1) for q in range(n_seq) for b in list(live[q])[::3]])   # a batch of deletes

@@ -359,6 +359,70 @@ def test_delete_equals_never_inserted_bitwise(dt, b, H, dh):
     assert torch.equal(smem.smem_reader_prefill_block(a, [0], [nb], q, ki, ki, nkv), rc)
 
 
+def test_store_edits_at_65536_blocks_bitwise():
+    """The deletion-latency sweep's largest table (65,536 block indices of one
+    sequence, half of them present, a tiny page shape so the oracle can hold
+    every row): single deletions and re-insertions anywhere (the first live
+    block among them, which shifts the whole live list), then a batch of
+    more than 128 edits; the live list and the exported rows equal the oracle
+    store's bit for bit after each round, and reads over all 32,768 blocks
+    match the oracle."""
+    dtype = torch.float32
+    b, H, dh, NB = 16, 1, 32, 65536
+    say("store edits at", NB, "blocks")
+    g = np.random.default_rng(65536)
+    st = smem.Store(1, NB, NB, b, H, dh, dtype)
+    ref = O.Store(1, NB, b, H, dh)
+    present = sorted(int(j) for j in g.choice(NB, NB // 2, replace=False))
+    K = g.standard_normal((len(present), b, H, dh)).astype(np.float32)
+    V = g.standard_normal((len(present), b, H, dh)).astype(np.float32)
+    rows_of = {j: i for i, j in enumerate(present)}
+    for i0 in range(0, len(present), 4096):
+        blk = present[i0:i0 + 4096]
+        smem.smem_store_put_blocks(st, [0] * len(blk), blk, dev(K[i0:i0 + len(blk)].reshape(-1, H, dh), dtype),
+                                   dev(V[i0:i0 + len(blk)].reshape(-1, H, dh), dtype))
+    for j in present:
+        ref.put(0, j, K[rows_of[j]], V[rows_of[j]])
+
+    def same():
+        idx, Kx, Vx = smem.smem_store_export(st, 0)
+        ridx, RK, RV = ref.export(0)
+        assert idx == ridx
+        assert np.array_equal(host(Kx), RK) and np.array_equal(host(Vx), RV)
+
+    same()
+    live = list(present)
+    for r in range(3):
+        gone = [live[0]] + [int(j) for j in g.choice(live, 40, replace=False) if j != live[0]]
+        for j in gone:
+            smem.smem_delete_block(st, 0, j, scrub=(j % 2 == 0))
+            ref.delete(0, j)
+        back = gone[: len(gone) // 2]
+        for j in back:
+            smem.smem_store_put_block(st, 0, j, dev(K[rows_of[j]], dtype), dev(V[rows_of[j]], dtype))
+            ref.put(0, j, K[rows_of[j]], V[rows_of[j]])
+        live = sorted(set(live) - set(gone) | set(back))
+        same()
+    # a batch of 300 inserts (three groups of edits) of absent blocks, with new rows
+    absent = sorted(set(range(NB)) - set(live))
+    new = sorted(int(j) for j in g.choice(absent, 300, replace=False))
+    Kn = g.standard_normal((len(new), b, H, dh)).astype(np.float32)
+    Vn = g.standard_normal((len(new), b, H, dh)).astype(np.float32)
+    smem.smem_store_put_blocks(st, [0] * len(new), new, dev(Kn.reshape(-1, H, dh), dtype),
+                               dev(Vn.reshape(-1, H, dh), dtype))
+    for i, j in enumerate(new):
+        ref.put(0, j, Kn[i], Vn[i])
+    same()
+    # reads over every present block
+    q = g.standard_normal((1, b, H, dh)).astype(np.float32)
+    out = smem.smem_reader_prefill_block(st, [0], [NB], dev(q.reshape(b, H, dh), dtype))
+    check(out, O.reader_prefill_block(ref, [0], [NB], q).reshape(b, H, dh), dtype, "prefill over 65536 blocks")
+    qd = q[:, 3]
+    dec = smem.smem_reader_decode(st, [0], [NB], None, dev(qd, dtype))
+    check(dec, O.reader_decode(ref, [0], [NB], [0], qd)[0], dtype, "decode over 65536 blocks")
+    st.close()
+
+
 @pytest.mark.parametrize("dt,b,H,dh", [("f32", 16, 2, 32), ("bf16", 64, 2, 64)])
 def test_edit_path_independence_bitwise(dt, b, H, dh):
     """Gate G8 on the GPU: random edit sequences reaching one multiset give
