@@ -40,19 +40,6 @@ typedef f32x4 floatx4;
 
 constexpr int BT = 64;         // block / page size handled here
 
-// LDS tile strides, chosen against bank conflicts (32 four-byte banks; also
-// conflict-free with 64).  Key rows: 16-byte operand reads by 8 lanes of
-// consecutive rows -> a stride of 4 (mod 8) dwords puts each lane on its own
-// 4 banks.  Transposed value rows: 8-byte reads by 16 lanes of consecutive
-// rows -> a stride of 2 (mod 4) dwords, 136 bytes at 64 keys.
-template <int DH>
-struct Tiles {
-  static constexpr int KS = DH + 8;      // key tile row stride (elements)
-  static constexpr int VS = BT + 4;      // transposed value tile row stride (elements)
-  __attribute__((aligned(16))) uint16_t k[BT * KS];
-  __attribute__((aligned(16))) uint16_t vt[DH * VS];
-};
-
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 u) {
   bf16x8 r;
   __builtin_memcpy(&r, &u, 16);
@@ -66,69 +53,6 @@ __device__ __forceinline__ bf16x8 pack_p(const floatx4& a, const floatx4& b) {
   return r;
 }
 
-// In-block tile from token-major tensors ([row][H][dh], row stride H*dh):
-// keys row-major, values transposed into LDS.  tile_load issues every global
-// load of the tile into registers; tile_store writes them to LDS.  The
-// transpose packs two token rows per 32-bit LDS write; consecutive lanes take
-// consecutive 16-byte chunks of a row pair, so the global loads of a row are
-// contiguous.
-template <int DH>
-struct TileRegs {
-  static constexpr int CPR = DH / 8;                  // 16-byte chunks per token row
-  static constexpr int NK = BT * CPR / 256;           // key chunks per thread
-  static constexpr int NP = (BT / 2) * CPR;           // (row pair, chunk) jobs for the values
-  static constexpr int NV = (NP + 255) / 256;
-  u32x4 k[NK];
-  u32x4 va[NV], vb[NV];
-};
-
-template <int DH>
-__device__ __forceinline__ void tile_load(TileRegs<DH>& r, const uint16_t* __restrict__ kin,
-                                          const uint16_t* __restrict__ vin, size_t row_stride, int tid) {
-  using R = TileRegs<DH>;
-#pragma unroll
-  for (int it = 0; it < R::NK; ++it) {
-    const int c = tid + it * 256;
-    const int row = c / R::CPR, c8 = c % R::CPR;
-    r.k[it] = *(const u32x4*)(kin + row * row_stride + c8 * 8);
-  }
-#pragma unroll
-  for (int it = 0; it < R::NV; ++it) {
-    const int j = tid + it * 256;
-    if (j < R::NP) {
-      const int pr = j / R::CPR, c8 = j % R::CPR;
-      r.va[it] = *(const u32x4*)(vin + (2 * pr) * row_stride + c8 * 8);
-      r.vb[it] = *(const u32x4*)(vin + (2 * pr + 1) * row_stride + c8 * 8);
-    }
-  }
-}
-
-template <int DH>
-__device__ __forceinline__ void tile_store(const TileRegs<DH>& r, Tiles<DH>& T, int tid) {
-  using R = TileRegs<DH>;
-#pragma unroll
-  for (int it = 0; it < R::NK; ++it) {
-    const int c = tid + it * 256;
-    const int row = c / R::CPR, c8 = c % R::CPR;
-    *(u32x4*)&T.k[row * Tiles<DH>::KS + c8 * 8] = r.k[it];
-  }
-#pragma unroll
-  for (int it = 0; it < R::NV; ++it) {
-    const int j = tid + it * 256;
-    if (j < R::NP) {
-      const int pr = j / R::CPR, c8 = j % R::CPR;
-      const uint32_t a4[4] = {r.va[it].x, r.va[it].y, r.va[it].z, r.va[it].w};
-      const uint32_t b4[4] = {r.vb[it].x, r.vb[it].y, r.vb[it].z, r.vb[it].w};
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        // dims d = c8*8 + 2q (low halves) and d + 1 (high halves)
-        *(uint32_t*)&T.vt[(c8 * 8 + 2 * q) * Tiles<DH>::VS + 2 * pr] = (a4[q] & 0xffffu) | (b4[q] << 16);
-        *(uint32_t*)&T.vt[(c8 * 8 + 2 * q + 1) * Tiles<DH>::VS + 2 * pr] = (a4[q] >> 16) | (b4[q] & 0xffff0000u);
-      }
-    }
-  }
-}
-
 __device__ __forceinline__ u32x4 pack8(const float (&x)[8]) {
   u32x4 r;
   r.x = (uint32_t)f32_to_bf16_bits(x[0]) | ((uint32_t)f32_to_bf16_bits(x[1]) << 16);
@@ -136,32 +60,6 @@ __device__ __forceinline__ u32x4 pack8(const float (&x)[8]) {
   r.z = (uint32_t)f32_to_bf16_bits(x[4]) | ((uint32_t)f32_to_bf16_bits(x[5]) << 16);
   r.w = (uint32_t)f32_to_bf16_bits(x[6]) | ((uint32_t)f32_to_bf16_bits(x[7]) << 16);
   return r;
-}
-
-// Turn the tile's key rows by their in-block offsets (rotary phase = row).
-template <int DH>
-__device__ __forceinline__ void tile_rope(TileRegs<DH>& r, const float* __restrict__ tab, int tid) {
-  using R = TileRegs<DH>;
-#pragma unroll
-  for (int it = 0; it < R::NK; ++it) {
-    const int c = tid + it * 256;
-    const int row = c / R::CPR, c8 = c % R::CPR;
-    float x[8];
-    Chunk<uint16_t>::unpack(r.k[it], x);
-    rope_turn<8>(x, tab + (size_t)row * DH, c8 * 4);
-    r.k[it] = pack8(x);
-  }
-}
-
-// tab == NULL: no rotary phases.
-template <int DH>
-__device__ __forceinline__ void intra_store(Tiles<DH>& T, const uint16_t* __restrict__ kin,
-                                            const uint16_t* __restrict__ vin, size_t row_stride, int tid,
-                                            const float* __restrict__ tab = nullptr) {
-  TileRegs<DH> r;
-  tile_load<DH>(r, kin, vin, row_stride, tid);
-  if (tab) tile_rope<DH>(r, tab, tid);
-  tile_store<DH>(r, T, tid);
 }
 
 // Query fragments of one wave (B operand of S^T = K Q^T): query row
@@ -186,38 +84,6 @@ __device__ __forceinline__ void rope_q(bf16x8 (&dst)[DH / 32], const bf16x8 (&sr
     rope_turn<8>(x, row, kk * 16 + (lane >> 4) * 4);
 #pragma unroll
     for (int j = 0; j < 8; ++j) dst[kk][j] = (__bf16)x[j];
-  }
-}
-
-// S^T for this wave's 16 queries against the 64 keys in LDS.
-template <int DH>
-__device__ __forceinline__ void scores(floatx4 (&s)[4], const Tiles<DH>& T, const bf16x8 (&qf)[DH / 32], int lane) {
-#pragma unroll
-  for (int kt = 0; kt < 4; ++kt) {
-    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-    const uint16_t* kr = &T.k[(kt * 16 + (lane & 15)) * Tiles<DH>::KS + (lane >> 4) * 8];
-#pragma unroll
-    for (int kk = 0; kk < DH / 32; ++kk)
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(*(const u32x4*)(kr + kk * 32)), qf[kk], acc, 0, 0, 0);
-    s[kt] = acc;
-  }
-}
-
-// O^T += V^T P^T over the 64 keys in LDS.
-template <int DH>
-__device__ __forceinline__ void pv(floatx4 (&o)[DH / 16], const Tiles<DH>& T, const floatx4 (&p)[4], int lane) {
-  const bf16x8 p0 = pack_p(p[0], p[1]);
-  const bf16x8 p1 = pack_p(p[2], p[3]);
-#pragma unroll
-  for (int dt = 0; dt < DH / 16; ++dt) {
-    const uint16_t* vr = &T.vt[(dt * 16 + (lane & 15)) * Tiles<DH>::VS + (lane >> 4) * 4];
-    u32x4 a0, a1;
-    const u32x2 x0 = *(const u32x2*)(vr + 0), y0 = *(const u32x2*)(vr + 16);
-    const u32x2 x1 = *(const u32x2*)(vr + 32), y1 = *(const u32x2*)(vr + 48);
-    a0 = u32x4{x0.x, x0.y, y0.x, y0.y};
-    a1 = u32x4{x1.x, x1.y, y1.x, y1.y};
-    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a0), p0, o[dt], 0, 0, 0);
-    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a1), p1, o[dt], 0, 0, 0);
   }
 }
 
@@ -318,6 +184,146 @@ __device__ __forceinline__ void online_step(floatx4 (&s)[4], float& m, float& l,
   }
 }
 
+// ------------------------------------------------------------------ LDS tile layout
+
+// A 64-key tile in LDS -- a memory page's (page, head) tile, or a block's own
+// keys and values -- keeps the page layout: the key plane [b][d_h] followed by
+// the transposed value plane [d_h][b], with the 16-byte slots of each row
+// permuted (key row r: slot = chunk ^ kswz(r); value row d: slot = chunk ^
+// vswz(d)), so the rows one MFMA operand read touches fall on distinct banks
+// (measured on gfx950: no bank conflicts for the key and value operand reads).
+// Memory pages of the non-rotary prefill move global -> LDS by DMA
+// (global_load_lds_dwordx4, 16 bytes per lane) through a ring of NS page
+// stages, so NS - 1 pages are in flight while one is read and no register
+// holds a page in transit.
+#ifndef SMEM_PREFILL_STAGES32
+#define SMEM_PREFILL_STAGES32 4
+#endif
+#ifndef SMEM_PREFILL_STAGES64
+#define SMEM_PREFILL_STAGES64 4
+#endif
+#ifndef SMEM_PREFILL_STAGES128
+#define SMEM_PREFILL_STAGES128 2
+#endif
+template <int DH>
+struct PageRing {
+  static constexpr int TILE = 2 * BT * DH * 2;         // bytes per (page, head)
+  static constexpr int KBYTES = BT * DH * 2;           // key plane bytes
+  static constexpr int KRB = DH * 2;                   // key row bytes
+  static constexpr int KCH = DH / 8;                   // 16-byte chunks per key row
+  static constexpr int NS = DH == 32 ? SMEM_PREFILL_STAGES32 : DH == 64 ? SMEM_PREFILL_STAGES64 : SMEM_PREFILL_STAGES128;
+  static constexpr int IPW = TILE / 1024 / 4;          // DMA instructions per wave per page
+  static_assert(NS >= 2 && NS <= 5, "wait_pages covers up to 3 pages ahead");
+  __device__ static constexpr int kswz(int r) { return (r / (256 / KRB)) % KCH; }
+  // the 16-row group (d >> 4) enters the value permutation so that the
+  // reads of rows d and d + 16 are never a fixed distance apart: merged into
+  // one read2 instruction, their two halves fell on the same banks
+  __device__ static constexpr int vswz(int d) { return ((d >> 1) ^ (d >> 4)) & 7; }
+};
+
+// S^T for this wave's 16 queries against the 64 keys of a tile.
+template <int DH>
+__device__ __forceinline__ void scores_ring(floatx4 (&s)[4], const uint8_t* tile, const bf16x8 (&qf)[DH / 32],
+                                            int lane) {
+  using R = PageRing<DH>;
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt) {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    const int r = kt * 16 + (lane & 15);
+#pragma unroll
+    for (int kk = 0; kk < DH / 32; ++kk) {
+      const int c = kk * 4 + (lane >> 4);
+      const u32x4 kf = *(const u32x4*)(tile + r * R::KRB + ((c ^ R::kswz(r)) << 4));
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kf), qf[kk], acc, 0, 0, 0);
+    }
+    s[kt] = acc;
+  }
+}
+
+// O^T += V^T P^T over the 64 keys of a tile: lane reads keys
+// 4 (l/16) + 16 q .. +3 of value row dt*16 + l%16, q = 0..3.
+template <int DH>
+__device__ __forceinline__ void pv_ring(floatx4 (&o)[DH / 16], const uint8_t* tile, const floatx4 (&p)[4],
+                                        int lane) {
+  using R = PageRing<DH>;
+  const bf16x8 p0 = pack_p(p[0], p[1]);
+  const bf16x8 p1 = pack_p(p[2], p[3]);
+  const int g = lane >> 4;
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) {
+    const int d = dt * 16 + (lane & 15);
+    const uint8_t* row = tile + R::KBYTES + d * 128 + (g & 1) * 8;
+    u32x2 x[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) x[q] = *(const u32x2*)(row + ((((g >> 1) + 2 * q) ^ R::vswz(d)) << 4));
+    const u32x4 a0 = u32x4{x[0].x, x[0].y, x[1].x, x[1].y};
+    const u32x4 a1 = u32x4{x[2].x, x[2].y, x[3].x, x[3].y};
+    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a0), p0, o[dt], 0, 0, 0);
+    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a1), p1, o[dt], 0, 0, 0);
+  }
+}
+
+
+// A block's own keys and values from token-major tensors ([row][H][dh], row
+// stride rs) into an LDS tile in the layout above, by NT threads: a key job
+// is one 16-byte chunk of a row; a value job is one chunk of a row pair,
+// written transposed as 32-bit pairs of consecutive keys.  tab: rotary table
+// (keys turned by their in-block offsets), or NULL.
+template <int DH, int NT>
+__device__ __forceinline__ void intra_ring_store(uint8_t* tile, const uint16_t* __restrict__ kin,
+                                                 const uint16_t* __restrict__ vin, size_t rs, int tid,
+                                                 const float* __restrict__ tab = nullptr) {
+  using R = PageRing<DH>;
+  constexpr int CPR = DH / 8, NK = BT * CPR, NJ = NK + (BT / 2) * CPR, NIT = (NJ + NT - 1) / NT;
+  // every global load first, then the LDS writes
+  u32x4 ra[NIT], rb[NIT];
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    const int j = tid + it * NT;
+    if (j < NK) {                                      // key chunk (row, c8)
+      ra[it] = *(const u32x4*)(kin + (j / CPR) * rs + (j % CPR) * 8);
+    } else if (j < NJ) {                               // value rows (2 pr, 2 pr + 1), chunk c8
+      const int pr = (j - NK) / CPR, c8 = (j - NK) % CPR;
+      ra[it] = *(const u32x4*)(vin + (2 * pr) * rs + c8 * 8);
+      rb[it] = *(const u32x4*)(vin + (2 * pr + 1) * rs + c8 * 8);
+    }
+  }
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    const int j = tid + it * NT;
+    if (j < NK) {
+      const int row = j / CPR, c8 = j % CPR;
+      u32x4 kv = ra[it];
+      if (tab) {
+        float x[8];
+        Chunk<uint16_t>::unpack(kv, x);
+        rope_turn<8>(x, tab + (size_t)row * DH, c8 * 4);
+        kv = pack8(x);
+      }
+      *(u32x4*)(tile + row * R::KRB + ((c8 ^ R::kswz(row)) << 4)) = kv;
+    } else if (j < NJ) {
+      const int pr = (j - NK) / CPR, c8 = (j - NK) % CPR;
+      const uint32_t a4[4] = {ra[it].x, ra[it].y, ra[it].z, ra[it].w};
+      const uint32_t b4[4] = {rb[it].x, rb[it].y, rb[it].z, rb[it].w};
+      const int key = 2 * pr;
+      // odd chunks write the odd dimension of each pair first: the lanes of
+      // one write then cover both parities of rows (the two bank halves)
+      const int flip = c8 & 1;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int d = c8 * 8 + 2 * q;
+        const uint32_t lo = (a4[q] & 0xffffu) | (b4[q] << 16), hi = (a4[q] >> 16) | (b4[q] & 0xffff0000u);
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          const int dd = d + (k ^ flip);
+          *(uint32_t*)(tile + R::KBYTES + dd * 128 + (key & 7) * 2 + (((key >> 3) ^ R::vswz(dd)) << 4)) =
+              (k ^ flip) ? hi : lo;
+        }
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------------ encoder
 
 struct EncArgs {
@@ -337,10 +343,12 @@ struct EncArgs {
 // One workgroup per (block, head) tile, heads fastest: neighbouring
 // workgroups read neighbouring head slices of the same token rows.  Every
 // tile's loads are issued at once; with all tiles resident, tiles whose data
-// arrive first compute while the rest are still loading.
+// arrive first compute while the rest are still loading.  The tile sits in
+// LDS in the page layout, so the operand reads are the prefill's.
 template <int DH, bool CAUSAL, bool ROPE>
 __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
-  __shared__ Tiles<DH> T;
+  using R = PageRing<DH>;
+  __shared__ __attribute__((aligned(1024))) uint8_t T[R::TILE];
   const int h = blockIdx.x, blk = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const size_t rs = (size_t)a.H * DH;
@@ -349,26 +357,26 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
   bf16x8 qf[DH / 32];
   load_q<DH>(qf, a.q + base + (size_t)wave * 16 * rs, rs, lane);
   if constexpr (ROPE) rope_q<DH>(qf, qf, a.rope + (size_t)qrow * DH, lane);
-  intra_store<DH>(T, a.k + base, a.v + base, rs, tid, ROPE ? a.rope : nullptr);
+  intra_ring_store<DH, 256>(T, a.k + base, a.v + base, rs, tid, ROPE ? a.rope : nullptr);
   __syncthreads();
   floatx4 s4[4];
-  scores<DH>(s4, T, qf, lane);
+  scores_ring<DH>(s4, T, qf, lane);
   floatx4 o[DH / 16];
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, l = 0.f;
   online_step<DH, CAUSAL>(s4, m, l, o, lane, qrow, a.scale_log2);
-  pv<DH>(o, T, s4, lane);
+  pv_ring<DH>(o, T, s4, lane);
   l = qsum(l);
   const float inv = 1.f / l;
   const int pg = a.sink[blk];
   uint16_t* kp = (a.pages && pg >= 0) ? a.pages + page_head_offset(pg, h, a.H, BT, DH) : nullptr;
-  // The block's output rows go through LDS (the key tile's space, row pitch
-  // KS) so that global stores are whole 16-byte chunks of consecutive rows:
-  // a lane's fragment is 4 dims of one query row, 8 bytes scattered over 64
-  // rows.  A page insert writes the key plane from the same rows and the
-  // transposed value plane by gathering 8 rows per chunk.
-  constexpr int KS = Tiles<DH>::KS;
+  // The block's output rows go through LDS (the key plane's space and
+  // layout) so that global stores are whole 16-byte chunks of consecutive
+  // rows: a lane's fragment is 4 dims of one query row, 8 bytes scattered
+  // over 64 rows.  A page insert writes the key plane from the same rows and
+  // the transposed value plane by gathering each chunk's 8 rows (the lanes
+  // of one instruction read one row).
   __syncthreads();                           // every wave is done with the key and value tiles
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) {
@@ -376,23 +384,28 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
     uint16_t rr[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) rr[i] = f32_to_bf16_bits(o[dt][i] * inv);
-    *(u32x2*)&T.k[qrow * KS + d0] = u32x2{(uint32_t)rr[0] | ((uint32_t)rr[1] << 16),
-                                          (uint32_t)rr[2] | ((uint32_t)rr[3] << 16)};
+    *(u32x2*)(T + qrow * R::KRB + (((d0 >> 3) ^ R::kswz(qrow)) << 4) + (d0 & 7) * 2) =
+        u32x2{(uint32_t)rr[0] | ((uint32_t)rr[1] << 16), (uint32_t)rr[2] | ((uint32_t)rr[3] << 16)};
   }
   __syncthreads();
   for (int c = tid; c < BT * DH / 8; c += 256) {
     const int row = c / (DH / 8), c8 = c % (DH / 8);
-    const u32x4 v16 = *(const u32x4*)&T.k[row * KS + c8 * 8];
+    const u32x4 v16 = *(const u32x4*)(T + row * R::KRB + ((c8 ^ R::kswz(row)) << 4));
     if (a.out) *(u32x4*)(a.out + ((size_t)blk * BT + row) * rs + (size_t)h * DH + c8 * 8) = v16;
     if (kp) *(u32x4*)(kp + row * DH + c8 * 8) = v16;
   }
   if (kp) {
     for (int c = tid; c < DH * BT / 8; c += 256) {
-      const int d = c / (BT / 8), r8 = c % (BT / 8);
+      const int d = c % DH, r8 = c / DH;
+      const uint8_t* col = T + (d & 7) * 2;
       uint32_t w[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        w[j] = (uint32_t)T.k[(r8 * 8 + 2 * j) * KS + d] | ((uint32_t)T.k[(r8 * 8 + 2 * j + 1) * KS + d] << 16);
+      for (int j = 0; j < 4; ++j) {
+        const int r0 = r8 * 8 + 2 * j, r1 = r0 + 1;
+        const uint32_t x0 = *(const uint16_t*)(col + r0 * R::KRB + (((d >> 3) ^ R::kswz(r0)) << 4));
+        const uint32_t x1 = *(const uint16_t*)(col + r1 * R::KRB + (((d >> 3) ^ R::kswz(r1)) << 4));
+        w[j] = x0 | (x1 << 16);
+      }
       *(u32x4*)(kp + BT * DH + d * BT + r8 * 8) = u32x4{w[0], w[1], w[2], w[3]};
     }
   }
@@ -442,93 +455,17 @@ hipError_t launch_encoder_mfma(int b, int dh, const void* q, const void* k, cons
 // never waits on a global load issued behind the in-flight pages.
 constexpr int kRopeRows = 24;
 
-// Memory pages of the non-rotary prefill move global -> LDS by DMA
-// (global_load_lds_dwordx4, 16 bytes per lane) through a ring of NS page
-// stages, so NS - 1 pages are in flight while one is read and no register
-// holds a page in transit.  A (page, head) tile is the key plane [b][d_h]
-// followed by the transposed value plane [d_h][b]; in LDS both keep that
-// layout with 16-byte slots permuted per row (key row r: slot = chunk ^
-// kswz(r); value row d: slot = chunk ^ vswz(d)), so the 16 rows one MFMA
-// operand read touches cover every bank once.
-#ifndef SMEM_PREFILL_STAGES32
-#define SMEM_PREFILL_STAGES32 4
-#endif
-#ifndef SMEM_PREFILL_STAGES64
-#define SMEM_PREFILL_STAGES64 4
-#endif
-#ifndef SMEM_PREFILL_STAGES128
-#define SMEM_PREFILL_STAGES128 2
-#endif
-template <int DH>
-struct PageRing {
-  static constexpr int TILE = 2 * BT * DH * 2;         // bytes per (page, head)
-  static constexpr int KBYTES = BT * DH * 2;           // key plane bytes
-  static constexpr int KRB = DH * 2;                   // key row bytes
-  static constexpr int KCH = DH / 8;                   // 16-byte chunks per key row
-  static constexpr int NS = DH == 32 ? SMEM_PREFILL_STAGES32 : DH == 64 ? SMEM_PREFILL_STAGES64 : SMEM_PREFILL_STAGES128;
-  static constexpr int IPW = TILE / 1024 / 4;          // DMA instructions per wave per page
-  static_assert(NS >= 2 && NS <= 5, "wait_pages covers up to 3 pages ahead");
-  __device__ static constexpr int kswz(int r) { return (r / (256 / KRB)) % KCH; }
-  __device__ static constexpr int vswz(int d) { return (d >> 1) & 7; }
-};
-
+// The final split's in-block tile uses the ring's first stage (split
+// workgroups leave the ring unused; the folding one has drained it).
 template <int DH, bool ROPE>
 struct PrefillLds {
-  union {
-    Tiles<DH> T;                                       // final split: null row and in-block keys
-    __attribute__((aligned(1024))) uint8_t ring[PageRing<DH>::NS * PageRing<DH>::TILE];
-  };
+  __attribute__((aligned(1024))) uint8_t ring[PageRing<DH>::NS * PageRing<DH>::TILE];
 };
 template <int DH>
 struct PrefillLds<DH, true> {
-  union {
-    Tiles<DH> T;                                       // final split: null row and in-block keys
-    __attribute__((aligned(1024))) uint8_t ring[PageRing<DH>::NS * PageRing<DH>::TILE];
-  };
+  __attribute__((aligned(1024))) uint8_t ring[PageRing<DH>::NS * PageRing<DH>::TILE];
   float rows[kRopeRows * DH];                          // turns d_lo .. d_lo + kRopeRows - 1
 };
-
-// S^T for this wave's 16 queries against a page's 64 keys in a ring stage.
-template <int DH>
-__device__ __forceinline__ void scores_ring(floatx4 (&s)[4], const uint8_t* tile, const bf16x8 (&qf)[DH / 32],
-                                            int lane) {
-  using R = PageRing<DH>;
-#pragma unroll
-  for (int kt = 0; kt < 4; ++kt) {
-    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-    const int r = kt * 16 + (lane & 15);
-#pragma unroll
-    for (int kk = 0; kk < DH / 32; ++kk) {
-      const int c = kk * 4 + (lane >> 4);
-      const u32x4 kf = *(const u32x4*)(tile + r * R::KRB + ((c ^ R::kswz(r)) << 4));
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kf), qf[kk], acc, 0, 0, 0);
-    }
-    s[kt] = acc;
-  }
-}
-
-// O^T += V^T P^T over a page's 64 keys in a ring stage: lane reads keys
-// 4 (l/16) + 16 q .. +3 of value row dt*16 + l%16, q = 0..3.
-template <int DH>
-__device__ __forceinline__ void pv_ring(floatx4 (&o)[DH / 16], const uint8_t* tile, const floatx4 (&p)[4],
-                                        int lane) {
-  using R = PageRing<DH>;
-  const bf16x8 p0 = pack_p(p[0], p[1]);
-  const bf16x8 p1 = pack_p(p[2], p[3]);
-  const int g = lane >> 4;
-#pragma unroll
-  for (int dt = 0; dt < DH / 16; ++dt) {
-    const int d = dt * 16 + (lane & 15);
-    const uint8_t* row = tile + R::KBYTES + d * 128 + (g & 1) * 8;
-    u32x2 x[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) x[q] = *(const u32x2*)(row + ((((g >> 1) + 2 * q) ^ R::vswz(d)) << 4));
-    const u32x4 a0 = u32x4{x[0].x, x[0].y, x[1].x, x[1].y};
-    const u32x4 a1 = u32x4{x[2].x, x[2].y, x[3].x, x[3].y};
-    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a0), p0, o[dt], 0, 0, 0);
-    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a1), p1, o[dt], 0, 0, 0);
-  }
-}
 
 template <int N>
 __device__ __forceinline__ void wait_pages(int ahead) {
@@ -629,7 +566,6 @@ __device__ __forceinline__ void store_out(uint16_t* orow, const floatx4 (&o)[DH 
 template <int DH, bool ROPE, bool FUSE>
 __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH, ROPE>& L) {
   static_assert(!(FUSE && ROPE), "the one-workgroup mode has no rotary variant");
-  Tiles<DH>& T = L.T;
   // heads fastest: neighbouring workgroups stream the adjacent head tiles of
   // the same pages
   const int h = blockIdx.x;
@@ -737,13 +673,13 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
     if (a.k_in != nullptr) {
       const size_t base = (size_t)slot * BT * rs + (size_t)h * DH;
       if constexpr (ROPE) rope_q<DH>(qf, qf, a.rope + (size_t)qrow * DH, lane);
-      intra_store<DH>(T, (const uint16_t*)a.k_in + base, (const uint16_t*)a.v_in + base, rs, tid,
-                      ROPE ? a.rope : nullptr);
+      intra_ring_store<DH, 256>(L.ring, (const uint16_t*)a.k_in + base, (const uint16_t*)a.v_in + base, rs, tid,
+                                ROPE ? a.rope : nullptr);
       __syncthreads();
       floatx4 s[4];
-      scores<DH>(s, T, qf, lane);
+      scores_ring<DH>(s, L.ring, qf, lane);
       online_step<DH, true>(s, m, l, o, lane, qrow, a.scale_log2);
-      pv<DH>(o, T, s, lane);
+      pv_ring<DH>(o, L.ring, s, lane);
     }
   }
   const size_t qs = (size_t)slot * BT + qrow;
@@ -772,9 +708,9 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
 // ------------------------------------------------------------------ few-pair prefill
 
 // Launches with few (query block, head) pairs and at most four memory splits
-// each.  A pair's 64 query rows go to 4/QW workgroups of 4 x QW waves (QW = 2:
-// two workgroups of 32 rows, launched 8 indices apart so both run on one XCD
-// and the second fetch of each page hits its L2; QW = 4: one workgroup).
+// each.  A pair's 64 query rows go to 4/QW workgroups of 4 x QW waves (QW = 2,
+// the one launched: two workgroups of 32 rows, launched 8 indices apart so
+// both run on one XCD and the second fetch of each page hits its L2).
 // Wave group g (QW waves of 16 rows each) reads memory split g through a DMA
 // ring of its own, so four page streams and four MFMA -> softmax -> MFMA
 // chains run on the CU at once; the groups step through their pages
@@ -883,31 +819,7 @@ __global__ void __launch_bounds__(64 * 4 * QW) k_prefill_mfma_par(ReaderArgs a) 
   constexpr int CPR = DH / 8;                            // 16-byte chunks per row
   if (a.k_in != nullptr) {
     const size_t base = (size_t)slot * BT * rs + (size_t)h * DH;
-    const uint16_t* kin = (const uint16_t*)a.k_in + base;
-    const uint16_t* vin = (const uint16_t*)a.v_in + base;
-    constexpr int NK = BT * CPR, NJ = NK + (BT / 2) * CPR;
-    for (int j = tid; j < NJ; j += P::THREADS) {
-      if (j < NK) {                                      // key chunk (row, c8)
-        const int row = j / CPR, c8 = j % CPR;
-        const u32x4 kv = *(const u32x4*)(kin + row * rs + c8 * 8);
-        *(u32x4*)(tin + row * R::KRB + ((c8 ^ R::kswz(row)) << 4)) = kv;
-      } else {                                           // value rows (2 pr, 2 pr + 1), chunk c8
-        const int pr = (j - NK) / CPR, c8 = (j - NK) % CPR;
-        const u32x4 va = *(const u32x4*)(vin + (2 * pr) * rs + c8 * 8);
-        const u32x4 vb = *(const u32x4*)(vin + (2 * pr + 1) * rs + c8 * 8);
-        const uint32_t a4[4] = {va.x, va.y, va.z, va.w};
-        const uint32_t b4[4] = {vb.x, vb.y, vb.z, vb.w};
-        const int key = 2 * pr;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int d = c8 * 8 + 2 * q;
-          uint8_t* r0 = tin + R::KBYTES + d * 128 + (key & 7) * 2;
-          uint8_t* r1 = tin + R::KBYTES + (d + 1) * 128 + (key & 7) * 2;
-          *(uint32_t*)(r0 + (((key >> 3) ^ R::vswz(d)) << 4)) = (a4[q] & 0xffffu) | (b4[q] << 16);
-          *(uint32_t*)(r1 + (((key >> 3) ^ R::vswz(d + 1)) << 4)) = (a4[q] >> 16) | (b4[q] & 0xffff0000u);
-        }
-      }
-    }
+    intra_ring_store<DH, P::THREADS>(tin, (const uint16_t*)a.k_in + base, (const uint16_t*)a.v_in + base, rs, tid);
   }
   if (a.null_kv != nullptr && tid < 2 * CPR) {
     const uint16_t* nsrc = (const uint16_t*)a.null_kv + (tid < CPR ? (size_t)h * DH + tid * 8
@@ -1011,10 +923,7 @@ static hipError_t launch_pre(const ReaderArgs& a, hipStream_t s) {
     constexpr int D = DH > 64 ? 64 : DH;                 // (no few-pair variant at d_h 128)
     if (a.rope || DH > 64 || max_split > ParLds<D, 4>::G) return hipErrorInvalidValue;
     const int n_pairs = a.n_slots * a.H;
-    if (n_pairs <= kParHalfPairs)
-      hipLaunchKernelGGL((k_prefill_mfma_par<D, 2>), dim3(par_grid(n_pairs, 2)), dim3(512), 0, s, a);
-    else
-      hipLaunchKernelGGL((k_prefill_mfma_par<D, 4>), dim3(par_grid(n_pairs, 4)), dim3(1024), 0, s, a);
+    hipLaunchKernelGGL((k_prefill_mfma_par<D, 2>), dim3(par_grid(n_pairs, 2)), dim3(512), 0, s, a);
     return hipGetLastError();
   }
   if (a.fuse) {

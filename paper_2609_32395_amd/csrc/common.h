@@ -69,20 +69,15 @@ constexpr int kFoldSerial = SMEM_FOLD_SERIAL;
 inline bool fold_in_workgroup(long n_pairs, int max_pages, int dh) {
   return n_pairs >= kFoldPairs || (long)max_pages * (dh > 64 ? dh : 64) <= kFoldSerial;
 }
-// A folding launch of fewer than kParPairs pairs at d_h <= 64 whose reads have
-// at most four memory splits runs the 16-wave variant instead: one wave group
-// per split, the four read at once (same splits, same fold, same bits).
+// A folding launch of at most kParPairs pairs at d_h <= 64 whose reads have
+// at most four memory splits runs the few-pair variant instead: one wave
+// group per split, the four read at once, each pair's query rows split over
+// two workgroups (same splits, same fold, same bits).
 #ifndef SMEM_PAR_PAIRS
-#define SMEM_PAR_PAIRS 512
+#define SMEM_PAR_PAIRS 128
 #endif
 constexpr int kParPairs = SMEM_PAR_PAIRS;
 constexpr int kParSplits = 4;
-// Up to kParHalfPairs pairs, each pair's query rows are split over two
-// workgroups (32 rows each), so the launch spreads over twice the CUs.
-#ifndef SMEM_PAR_HALF_PAIRS
-#define SMEM_PAR_HALF_PAIRS 128
-#endif
-constexpr int kParHalfPairs = SMEM_PAR_HALF_PAIRS;
 // Query slots whose prefill partials the workspace must hold at once.
 constexpr int kPrefillSlotChunk = 16;
 // Row-plane decode: pages per split max(kMinPagesRows, ceil(n_read /

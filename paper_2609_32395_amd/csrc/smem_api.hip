@@ -703,7 +703,7 @@ static smem_status prefill_impl(smem_store* st, const smem_rope* rope, int32_t n
       a.aux[i] = -1;
     }
     a.fuse = fuse;
-    if (fuse && d.dh <= 64 && (long)n * d.H < kParPairs) {
+    if (fuse && d.dh <= 64 && (long)n * d.H <= kParPairs) {
       bool few = true;
       for (int i = 0; i < n; ++i) few = few && total_splits(a.n_read[i], a.pps[i]) - 1 <= kParSplits;
       if (few) a.fuse = 2;

@@ -497,7 +497,7 @@ def test_prefill_page_ring_indexing(dh, ns):
     TILE, KBYTES, KRB, KCH = 2 * BT * dh * 2, BT * dh * 2, dh * 2, dh // 8
     IPW = TILE // 1024 // 4
     kswz = lambda r: (r // (256 // KRB)) % KCH
-    vswz = lambda d: (d >> 1) & 7
+    vswz = lambda d: ((d >> 1) ^ (d >> 4)) & 7
     placed = {}                                   # LDS byte offset in the stage -> source byte offset
     for wave, i, lane in itertools.product(range(4), range(IPW), range(64)):
         byte = (wave * IPW + i) * 1024 + lane * 16
@@ -581,7 +581,7 @@ def test_prefill_par_lds_and_thread_ranges(dh, qw):
     STATE = (dh // 16) * 1024 + 64 * 8
     assert BYTES <= 160 * 1024 and G * qw * STATE <= RING and 3 * IPW < 64
     kswz = lambda r: (r // (256 // KRB)) % KCH
-    vswz = lambda d: (d >> 1) & 7
+    vswz = lambda d: ((d >> 1) ^ (d >> 4)) & 7
     seen = set()
     for g, w, stage, i, lane in itertools.product(range(G), range(qw), range(NSP), range(IPW), range(64)):
         lds = g * NSP * TILE + w * IPW * 1024 + stage * TILE + i * 1024 + lane * 16
