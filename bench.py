@@ -860,8 +860,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
-                    help="after the timed region, copy a MIB-MiB tensor once (a plain copy kernel of known "
-                         "size, used to scale hardware traffic counters)")
+                    help="after the headline, copy a MIB-MiB tensor three times (torch's copy kernel, the "
+                         "library's register copy and its LDS-DMA copy: known sizes, used to scale hardware "
+                         "traffic counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported (the path is single-GPU; "
@@ -874,10 +875,14 @@ def main():
 
     dec = None if args.no_headline else decode_workload(args, torch, smem, synth)
     if args.copy_probe:
+        # copies of known size for scaling the traffic counters: torch's copy
+        # kernel, the library's 16-byte register copy, and its LDS-DMA copy
         src = torch.ones(args.copy_probe * (1 << 20) // 2, dtype=torch.bfloat16, device="cuda")
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
         dst.copy_(src)
+        smem.smem_device_copy(dst, src, via_lds=False)
+        smem.smem_device_copy(dst, src, via_lds=True)
         torch.cuda.synchronize()
         del src, dst
     secondary = {}

@@ -443,6 +443,15 @@ smem_status smem_model_delete_block(smem_model* m, int32_t seq, int32_t block_id
 /* Host-side facts about a store: pages in use and free. */
 smem_status smem_store_stats(const smem_store* st, int32_t* pages_used, int32_t* pages_free);
 
+/* Device copy of `bytes` from src to dst (device pointers, 16-byte aligned,
+ * not overlapping) on stream s.  Not an operation of the method: a copy of
+ * known size whose hardware traffic counters calibrate the counts of the
+ * attention kernels.  via_lds = 0: through registers (16-byte loads and
+ * stores; bytes a multiple of 16); via_lds = 1: through LDS by DMA, the way
+ * the MFMA kernels bring pages in (bytes a multiple of 16384).  SMEM_EINVAL
+ * for other sizes or flags. */
+smem_status smem_device_copy(void* dst, const void* src, size_t bytes, int32_t via_lds, hipStream_t s);
+
 const char* smem_status_string(smem_status st);
 
 /* Message of the calling thread's last failed call ("" if none). */

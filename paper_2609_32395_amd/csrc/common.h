@@ -384,8 +384,10 @@ hipError_t launch_prefill_mfma(int b, int dh, const ReaderArgs& a, hipStream_t s
 // Row-plane decode: stage 0 = absorbed queries (+ null row projection),
 // stage 1 = row reader + merge.
 hipError_t launch_rows(int d, int dh, const RowsArgs& a, const RowsPrepArgs& pa, int stage, hipStream_t s);
-// Plain device copy (16-byte multiples).
+// Plain device copy (16-byte multiples), and the same through LDS by DMA
+// (16 KiB multiples).
 hipError_t launch_copy16(void* dst, const void* src, size_t bytes, hipStream_t s);
+hipError_t launch_copy_dma(void* dst, const void* src, size_t bytes, hipStream_t s);
 // Reader decode (smem_reader_decode and its variants).  ws_ext == NULL: split
 // partials in the store's workspace; otherwise in ws_ext, which holds
 // ws_ext_floats floats (the call is rejected if its partials do not fit).

@@ -377,6 +377,17 @@ smem_status smem_store_destroy(smem_store* st) {
   return SMEM_OK;
 }
 
+smem_status smem_device_copy(void* dst, const void* src, size_t bytes, int32_t via_lds, hipStream_t s) {
+  if (!dst || !src) return fail(SMEM_EINVAL, "dst and src are required");
+  if (!aligned16(dst) || !aligned16(src)) return fail(SMEM_EINVAL, "dst and src must be 16-byte aligned");
+  if (via_lds != 0 && via_lds != 1) return fail(SMEM_EINVAL, "via_lds is 0 or 1");
+  const size_t unit = via_lds ? 16384 : 16;
+  if (bytes % unit) return fail(SMEM_EINVAL, "bytes must be a multiple of %zu", unit);
+  const hipError_t e = via_lds ? launch_copy_dma(dst, src, bytes, s) : launch_copy16(dst, src, bytes, s);
+  if (e != hipSuccess) return hip_fail(e, "device copy");
+  return SMEM_OK;
+}
+
 smem_status smem_store_stats(const smem_store* st, int32_t* pages_used, int32_t* pages_free) {
   if (!st) return fail(SMEM_EINVAL, "store is NULL");
   if (pages_free) *pages_free = (int32_t)st->free_pages.size();

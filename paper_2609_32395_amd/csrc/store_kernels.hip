@@ -231,6 +231,36 @@ hipError_t launch_copy16(void* dst, const void* src, size_t bytes, hipStream_t s
   return hipGetLastError();
 }
 
+// The same copy through LDS by DMA (global_load_lds_dwordx4, the way the
+// attention kernels bring pages in): each workgroup moves 16 KiB tiles, the
+// four waves loading 4 KiB each into LDS, then storing them from LDS.
+// bytes is a multiple of 16 KiB.
+__global__ void __launch_bounds__(256) k_copy_dma(uint8_t* __restrict__ dst, const uint8_t* __restrict__ src,
+                                                  size_t n_tiles) {
+  __shared__ __attribute__((aligned(1024))) uint8_t buf[16384];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)buf + (uint32_t)(wave * 4096);
+  for (size_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+    const uint8_t* s = src + t * 16384 + wave * 4096 + lane * 16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16(s + i * 1024, __builtin_amdgcn_readfirstlane(lds0 + i * 1024));
+    wait_vm<0>();
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *(u32x4*)(dst + t * 16384 + (i * 256 + tid) * 16) = *(const u32x4*)(buf + (i * 256 + tid) * 16);
+    __syncthreads();
+  }
+}
+
+hipError_t launch_copy_dma(void* dst, const void* src, size_t bytes, hipStream_t s) {
+  const size_t n_tiles = bytes / 16384;
+  if (n_tiles == 0) return hipSuccess;
+  const unsigned grid = (unsigned)(n_tiles < 2048 ? n_tiles : 2048);
+  hipLaunchKernelGGL(k_copy_dma, dim3(grid), dim3(256), 0, s, (uint8_t*)dst, (const uint8_t*)src, n_tiles);
+  return hipGetLastError();
+}
+
 // Rotary table (the SMem+RoPE composite): entry (p, k) = (cos, sin) of
 // p * base^(-2k/dh), evaluated in fp64 and stored as fp32.
 __global__ void __launch_bounds__(256) k_rope_table(float* __restrict__ tab, int dh, int n_phases, double base) {

@@ -113,6 +113,7 @@ SIGNATURES = {
     "smem_model_decode": (_I, [_P, _I, _I, _IP, _IP, _P, _P, _P]),
     "smem_model_delete_block": (_I, [_P, _I, _I, _P]),
     "smem_store_stats": (_I, [_P, _IP, _IP]),
+    "smem_device_copy": (_I, [_P, _P, ctypes.c_size_t, _I, _P]),
     "smem_status_string": (ctypes.c_char_p, [_I]),
     "smem_last_error": (ctypes.c_char_p, []),
 }
@@ -505,6 +506,17 @@ def smem_store_put_blocks(st: Store, seq_ids, block_idx, k_rows, v_rows, stream=
     kp = _dev(k_rows, shape, st.dtype, "k_rows")
     vp = _dev(v_rows, shape, st.dtype, "v_rows")
     _check(lib().smem_store_put_blocks(st.handle, n, _i32(seq_ids), _i32(block_idx), kp, vp, _stream(stream)))
+
+
+def smem_device_copy(dst, src, via_lds: bool = False, stream=None):
+    """Copy src into dst (device tensors of equal byte size) through registers
+    or, via_lds=True, through LDS by DMA (a copy of known size, for
+    calibrating hardware traffic counters)."""
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nbytes or not dst.is_contiguous() or not src.is_contiguous():
+        raise ValueError("dst and src: contiguous, same byte size")
+    _check(lib().smem_device_copy(ctypes.c_void_p(dst.data_ptr()), ctypes.c_void_p(src.data_ptr()), nbytes,
+                                  int(bool(via_lds)), _stream(stream)))
 
 
 def smem_delete_block(st: Store, seq: int, block_idx: int, scrub: bool = False, stream=None):

@@ -529,3 +529,17 @@ def test_large_batches_span_several_launches():
                                          dev(qp.reshape(-1, H, dh), dtype), dev(qp.reshape(-1, H, dh), dtype))
     exp = O.reader_prefill_block(ref, seqs, [3] * 20, qp, qp, qp)
     check(out, exp.reshape(-1, H, dh), dtype, "prefill 20 query blocks")
+
+
+def test_device_copy_both_paths():
+    """The calibration copies (registers, LDS by DMA) reproduce their source
+    bit for bit; sizes off their unit are rejected before anything runs."""
+    say("device copy")
+    src = torch.arange(3 * 4096 * 2, dtype=torch.int32, device="cuda").view(torch.float32)   # 96 KiB
+    for via in (False, True):
+        dst = torch.zeros_like(src)
+        smem.smem_device_copy(dst, src, via_lds=via)
+        torch.cuda.synchronize()
+        assert torch.equal(dst.view(torch.int32), src.view(torch.int32))
+    with pytest.raises(smem.SmemError):
+        smem.smem_device_copy(torch.zeros(1000, device="cuda"), torch.zeros(1000, device="cuda"), via_lds=True)
