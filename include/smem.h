@@ -440,6 +440,24 @@ smem_status smem_model_decode(smem_model* m, int32_t first_seq, int32_t n_seq, c
  * (Theorem 1).  SMEM_ENOENT if absent. */
 smem_status smem_model_delete_block(smem_model* m, int32_t seq, int32_t block_idx, hipStream_t s);
 
+/* One linear map of the model's layers (Appendix A: pre-LN layers, linear
+ * maps without bias, a GELU feed-forward), on the same kernels and in the
+ * same reduction order the model uses: y = epi(LN(x) W^T), or epi(x W^T)
+ * with ln_g = ln_b = NULL.
+ *   x: device bf16 [M, K] (K % 64 == 0); w: device bf16 [N, K];
+ *   ln_g, ln_b: device bf16 [K] (LayerNorm gain and shift, eps 1e-5;
+ *     K <= 2048) or both NULL;
+ *   epi: 0 store bf16 [M, N]; 1 GELU (erf form) then bf16; 2 add res
+ *     (device bf16 [M, N], may be y) then bf16; 3 store fp32 [M, N];
+ *   ln_tmp: device bf16 [M, K]: receives LN(x) when ln_g is set and M > 128
+ *     (those rows are normalised by a separate pass before the map; up to
+ *     128 rows the map normalises them itself); else unused, may be NULL.
+ * bf16 outputs need N % 4 == 0; every pointer 16-byte aligned.  Each output
+ * element is computed in one order whatever M and N are, so a row's result
+ * does not depend on the other rows.  SMEM_EINVAL for bad shapes. */
+smem_status smem_linear(int32_t M, int32_t N, int32_t K, const void* x, const void* w, const void* ln_g,
+                        const void* ln_b, int32_t epi, const void* res, void* y, void* ln_tmp, hipStream_t s);
+
 /* Host-side facts about a store: pages in use and free. */
 smem_status smem_store_stats(const smem_store* st, int32_t* pages_used, int32_t* pages_free);
 

@@ -489,4 +489,33 @@ smem_status smem_model_delete_block(smem_model* m, int32_t seq, int32_t block_id
   return SMEM_OK;
 }
 
+smem_status smem_linear(int32_t M, int32_t N, int32_t K, const void* x, const void* w, const void* ln_g,
+                        const void* ln_b, int32_t epi, const void* res, void* y, void* ln_tmp, hipStream_t s) {
+  if (M < 0 || N < 0 || K <= 0) return mfail(SMEM_EINVAL, "M, N >= 0 and K > 0 are required");
+  if (K % 64) return mfail(SMEM_EINVAL, "K must be a multiple of 64");
+  if (!x || !w || !y) return mfail(SMEM_EINVAL, "x, w, y are required");
+  if ((ln_g == nullptr) != (ln_b == nullptr)) return mfail(SMEM_EINVAL, "ln_g and ln_b: both or neither");
+  if (ln_g && K > 2048) return mfail(SMEM_EINVAL, "a fused LayerNorm needs K <= 2048");
+  if (ln_g && M > 128 && !ln_tmp) return mfail(SMEM_EINVAL, "ln_tmp is required with a LayerNorm and M > 128");
+  if (epi < 0 || epi > 3) return mfail(SMEM_EINVAL, "epi is 0 (store), 1 (GELU), 2 (residual) or 3 (fp32)");
+  if (epi == 2 && !res) return mfail(SMEM_EINVAL, "res is required with epi = 2");
+  if (epi != 3 && N % 4) return mfail(SMEM_EINVAL, "bf16 outputs need N % 4 == 0");
+  const void* ptrs[] = {x, w, ln_g, ln_b, res, y, ln_tmp};
+  for (const void* p : ptrs)
+    if ((uintptr_t)p & 15u) return mfail(SMEM_EINVAL, "tensors must be 16-byte aligned");
+  LinArgs a = lin((const uint16_t*)x, K, (const uint16_t*)w, M, N, K, (uint16_t*)y, N);
+  a.lng = (const uint16_t*)ln_g;
+  a.lnb = (const uint16_t*)ln_b;
+  a.lnout = (uint16_t*)ln_tmp;
+  hipError_t e;
+  switch (epi) {
+    case 0: e = linear<kLinStore>(a, s); break;
+    case 1: e = linear<kLinGelu>(a, s); break;
+    case 2: a.res = (const uint16_t*)res; e = linear<kLinResid>(a, s); break;
+    default: a.y = nullptr; a.yf = (float*)y; e = linear<kLinF32>(a, s); break;
+  }
+  if (e != hipSuccess) return mfail(SMEM_EHIP, "linear map launch");
+  return SMEM_OK;
+}
+
 }  // extern "C"

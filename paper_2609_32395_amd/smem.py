@@ -112,6 +112,7 @@ SIGNATURES = {
     "smem_model_prefill": (_I, [_P, _I, _I, _I, _P, _P, _P]),
     "smem_model_decode": (_I, [_P, _I, _I, _IP, _IP, _P, _P, _P]),
     "smem_model_delete_block": (_I, [_P, _I, _I, _P]),
+    "smem_linear": (_I, [_I, _I, _I, _P, _P, _P, _P, _I, _P, _P, _P, _P]),
     "smem_store_stats": (_I, [_P, _IP, _IP]),
     "smem_device_copy": (_I, [_P, _P, ctypes.c_size_t, _I, _P]),
     "smem_status_string": (ctypes.c_char_p, [_I]),
@@ -450,6 +451,29 @@ def smem_model_decode(m: Model, first_seq: int, query_block, pos, tokens, logits
     _check(lib().smem_model_decode(m.handle, int(first_seq), n, _i32(query_block), _i32(pos),
                                    ctypes.c_void_p(tokens.data_ptr()), lp, _stream(stream)))
     return logits
+
+
+LIN_STORE, LIN_GELU, LIN_RESID, LIN_F32 = 0, 1, 2, 3
+
+
+def smem_linear(x, w, ln_g=None, ln_b=None, epi=LIN_STORE, res=None, y=None, ln_tmp=None, stream=None):
+    """One of the model's linear maps: y = epi(LN(x) W^T) (or epi(x W^T)); x [M, K]
+    and w [N, K] bf16; y bf16 [M, N], fp32 for epi=LIN_F32."""
+    M, K = x.shape
+    N = w.shape[0]
+    if w.shape[1] != K:
+        raise ValueError("w must be [N, K]")
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float32 if epi == LIN_F32 else torch.bfloat16, device=x.device)
+    if ln_g is not None and M > 128 and ln_tmp is None:
+        ln_tmp = torch.empty((M, K), dtype=torch.bfloat16, device=x.device)
+    p = lambda t, shape, dt, n: _dev(t, shape, dt, n)
+    _check(lib().smem_linear(M, N, K, p(x, (M, K), torch.bfloat16, "x"), p(w, (N, K), torch.bfloat16, "w"),
+                             p(ln_g, (K,), torch.bfloat16, "ln_g"), p(ln_b, (K,), torch.bfloat16, "ln_b"), int(epi),
+                             p(res, (M, N), torch.bfloat16, "res"),
+                             p(y, (M, N), torch.float32 if epi == LIN_F32 else torch.bfloat16, "y"),
+                             p(ln_tmp, (M, K), torch.bfloat16, "ln_tmp"), _stream(stream)))
+    return y
 
 
 def smem_model_delete_block(m: Model, seq: int, block_idx: int, stream=None):

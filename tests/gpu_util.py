@@ -42,17 +42,27 @@ def host(t):
 UNIT_ROUNDOFF = {torch.float32: 2.0 ** -24, torch.bfloat16: 2.0 ** -8}
 
 
-def check(y, ref, dtype, what="", roundings=1):
+# Every check's numbers, printed at the end of the session (tests/conftest.py):
+# (what, dtype name, raw max|y - ref| / rms(ref), error beyond output rounding,
+# tolerance, full-size workload or not).
+RECORDS = []
+
+
+def check(y, ref, dtype, what="", roundings=1, full=False):
     """Elementwise |y - ref| <= TOL * rms(ref) + u |ref|: the tolerance bounds the
     fp32-accumulated result; u |ref| is the exact bound of the final store in
     the output dtype (its own rounding, counted once; twice when ``ref`` is
-    itself a rounded output)."""
+    itself a rounded output).  The raw max|y - ref| / rms(ref) (output
+    rounding included) is recorded beside it and printed with the case."""
     y = host(y) if isinstance(y, torch.Tensor) else np.asarray(y, np.float64)
     ref = np.asarray(ref, np.float64)
     rms = float(np.sqrt(np.mean(ref * ref))) if ref.size else 0.0
     excess = np.abs(y - ref) - roundings * UNIT_ROUNDOFF[dtype] * np.abs(ref)
     e = float(np.max(excess)) / rms if ref.size and rms > 0 else float(np.max(np.abs(y - ref), initial=0.0))
     raw = O.rel_err(y, ref)
+    name = "bf16" if dtype == torch.bfloat16 else "fp32"
+    RECORDS.append((what, name, raw, e, TOL[dtype], full))
+    say(f"check {what}: raw max|y-ref|/rms {raw:.3e}, beyond output rounding {e:.3e} (limit {TOL[dtype]:.0e})")
     assert np.all(np.isfinite(y)), f"{what}: non-finite output"
     assert e <= TOL[dtype], f"{what}: error beyond output rounding {e:.3e} > {TOL[dtype]:.1e} (raw {raw:.3e})"
     return e

@@ -346,7 +346,8 @@ def _linear_ranges(M, N, K, ldx, ldy, n2, ns, split):
 
 
 @pytest.mark.parametrize("d,vocab,rows", [(128, 256, 448), (768, 1000, 130), (2048, 77, 64), (256, 300, 100),
-                                         (768, 50257, 64), (1024, 4000, 4096), (832, 300, 256), (2048, 300, 256)])
+                                         (768, 50257, 64), (1024, 4000, 4096), (832, 300, 256), (2048, 300, 256),
+                                         (2048, 50257, 520), (2048, 50257, 136), (2048, 50257, 1), (832, 1000, 200)])
 def test_model_kernel_indexing(d, vocab, rows):
     """Every linear-map launch the model makes stays inside its operands (x
     [rows, K] in a [max_tokens, ldx] buffer, W [N or n2, K] and [N - n2, K],

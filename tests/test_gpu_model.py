@@ -10,7 +10,8 @@ Appendix A) through the C ABI, against the fp64 model oracle.
 * error codes of the store operations.
 
 Tolerance.  Every activation is rounded to bf16 once per producing step
-(unit roundoff u = 2^-9, RMS relative error u/sqrt 3 per rounding).  Along
+(unit roundoff u = 2^-8, the same u the attention checks use; RMS relative
+error u/sqrt 3 per rounding).  Along
 the longest path a logit sees R roundings: the embedding, 7 per encoder
 layer (LayerNorm, q|k|v, attention, residual, LayerNorm, FFN hidden,
 residual), the memory LayerNorm and the key/value maps, 11 per reader layer
@@ -18,7 +19,12 @@ residual), the memory LayerNorm and the key/value maps, 11 per reader layer
 third LayerNorm) and the final LayerNorm.  Independent roundings add as a
 random walk, so the logits' relative RMS error is about sqrt(R) u / sqrt 3,
 and the largest of n logits lies within sqrt(2 ln n) of that; the bound
-allows twice this: max |y - y_ref| / rms(y_ref) <= tol(R, n).
+allows twice this: max |y - y_ref| / rms(y_ref) <= tol(R, n).  The RMS
+relative error itself must stay within twice its random-walk size,
+rms(y - y_ref) / rms(y_ref) <= 2 sqrt(R) u / sqrt 3, which a systematic
+error of a few percent in one op would exceed, and the predicted tokens
+(argmax over the vocabulary) must agree with the oracle's for at least 90%
+of the positions.
 """
 import math
 
@@ -38,8 +44,38 @@ def roundings(E, D):
     return 1 + 7 * E + 2 + 11 * D + 1
 
 
+U_BF16 = 2.0 ** -8
+
+
 def tol(E, D, n):
-    return 2.0 * math.sqrt(2.0 * math.log(n)) * math.sqrt(roundings(E, D)) * 2.0 ** -9 / math.sqrt(3.0)
+    return 2.0 * math.sqrt(2.0 * math.log(n)) * math.sqrt(roundings(E, D)) * U_BF16 / math.sqrt(3.0)
+
+
+def tol_rms(E, D):
+    return 2.0 * math.sqrt(roundings(E, D)) * U_BF16 / math.sqrt(3.0)
+
+
+def model_check(y, expect, E, D, what, full=False, argmax=True):
+    """Logits against the oracle: the max bound, the RMS bound and (for a
+    vocabulary row) the argmax agreement; the numbers are recorded for the
+    session summary."""
+    from tests import gpu_util
+    y = np.asarray(y, np.float64)
+    expect = np.asarray(expect, np.float64)
+    rms = float(np.sqrt(np.mean(expect ** 2)))
+    err = float(np.max(np.abs(y - expect))) / rms
+    err_rms = float(np.sqrt(np.mean((y - expect) ** 2))) / rms
+    agree = float(np.mean(y.reshape(-1, y.shape[-1]).argmax(-1) == expect.reshape(-1, y.shape[-1]).argmax(-1)))
+    t, tr = tol(E, D, y.size), tol_rms(E, D)
+    gpu_util.RECORDS.append((f"{what} (max)", "bf16", err, err, t, full))
+    gpu_util.RECORDS.append((f"{what} (rms)", "bf16", err_rms, err_rms, tr, full))
+    say(f"check {what}: max {err:.3e} (limit {t:.3e}), rms {err_rms:.3e} (limit {tr:.3e}), argmax agreement {agree:.3f}")
+    assert np.all(np.isfinite(y)), what
+    assert err <= t, (what, err, t)
+    assert err_rms <= tr, (what, err_rms, tr)
+    if argmax:
+        assert agree >= 0.9, (what, agree)
+    return err
 SHAPE = dict(E=1, D=2, d=128, H=4, b=64, vocab=256, n_pos=256)
 
 
@@ -82,14 +118,11 @@ def test_served_block_matches_oracle(over):
     ref.encode(0, tokens[:B - 1], list(range(B - 1)))
     expect = ref.read(0, tokens[B - 1:], [B - 1])[0]
     y = host(logits)
-    err = float(np.max(np.abs(y - expect)) / np.sqrt(np.mean(expect ** 2)))
-    say("model rel err", err, "argmax agreement", float(np.mean(y.argmax(-1) == expect.argmax(-1))))
-    assert np.all(np.isfinite(y))
-    assert err <= tol(s["E"], s["D"], y.size), err
+    model_check(y, expect, s["E"], s["D"], f"model served block {over}")
     # the first block reads the null row alone
     first = host(smem.smem_model_read(m, 0, [0], tok(tokens[:1])))
     e0 = ref.read(0, tokens[:1], [0])[0]
-    assert float(np.max(np.abs(first - e0)) / np.sqrt(np.mean(e0 ** 2))) <= tol(s["E"], s["D"], first.size)
+    model_check(first, e0, s["E"], s["D"], f"model first block (null row only) {over}")
 
 
 def test_prefill_cold_and_partial_reuse_bitwise():
@@ -179,7 +212,7 @@ def test_tilings_agree_bitwise():
     ref.encode(0, tokens[:15], list(range(15)))
     expect = ref.read(0, tokens[15:], [15])[0]
     y = host(full[15 * 64:])
-    assert float(np.max(np.abs(y - expect)) / np.sqrt(np.mean(expect ** 2))) <= tol(SHAPE["E"], SHAPE["D"], y.size)
+    model_check(y, expect, SHAPE["E"], SHAPE["D"], "model block 15 of a 16-block tiled read")
 
 
 @pytest.mark.parametrize("d,H", [(2048, 16), (832, 26)], ids=["d2048", "d832"])
@@ -201,9 +234,7 @@ def test_fused_layernorm_widths_bitwise(d, H):
     ref.encode(0, tokens[:B - 1], list(range(B - 1)))
     expect = ref.read(0, tokens[B - 1:], [B - 1])[0]
     y = host(skip)
-    err = float(np.max(np.abs(y - expect)) / np.sqrt(np.mean(expect ** 2)))
-    say("rel err", err)
-    assert err <= tol(1, 1, y.size), err
+    model_check(y, expect, 1, 1, f"model fused LayerNorm d={d}")
 
 
 def test_160m_full_size_block_skip_matches_oracle():
@@ -225,9 +256,7 @@ def test_160m_full_size_block_skip_matches_oracle():
     ref.encode(0, tokens[:J - 1], list(range(J - 1)))
     expect = ref.read(0, tokens[J - 1:], [J - 1])[0]
     y = host(skip)
-    err = float(np.max(np.abs(y - expect)) / np.sqrt(np.mean(expect ** 2)))
-    say("160M rel err", err, "argmax agreement", float(np.mean(y.argmax(-1) == expect.argmax(-1))))
-    assert err <= tol(E, D, y.size), err
+    model_check(y, expect, E, D, "160M model block-skip read at 1024 tokens", full=True)
 
 
 def test_model_edge_cases():
@@ -249,7 +278,7 @@ def test_model_edge_cases():
     q_ref = q.copy()
     q_ref[0, 3] = q_ref[0, 9] = 0
     expect = ref.read(0, q_ref, [6])[0]
-    assert float(np.max(np.abs(y - expect)) / np.sqrt(np.mean(expect ** 2))) <= tol(SHAPE["E"], SHAPE["D"], y.size)
+    model_check(y, expect, SHAPE["E"], SHAPE["D"], "model read over every cached block")
     with pytest.raises(smem.SmemError) as e:
         smem.smem_model_read(m, 0, [7], tok(q))            # beyond max_blocks
     assert e.value.code == smem.SMEM_EINVAL
@@ -282,10 +311,7 @@ def test_decode_matches_reader_and_oracle_across_a_boundary():
         rows.append(smem.smem_model_decode(m, 0, [J], [p], tok(tokens[J, p:p + 1])))
     y = host(torch.cat(rows))
     t = tol(SHAPE["E"], SHAPE["D"], y.size)
-    err = float(np.max(np.abs(y - expect)) / np.sqrt(np.mean(expect ** 2)))
-    say("decode vs oracle", err, "vs GPU block read",
-        float(np.max(np.abs(y - host(block))) / np.sqrt(np.mean(expect ** 2))))
-    assert err <= t
+    model_check(y, expect, SHAPE["E"], SHAPE["D"], "model decode, 64 tokens of a block")
     assert float(np.max(np.abs(y - host(block))) / np.sqrt(np.mean(expect ** 2))) <= t
     # append the completed block, continue into block J + 1
     smem.smem_model_encode(m, 0, [J], tok(tokens[J:J + 1]))

@@ -1,0 +1,138 @@
+"""Op-level parity of the model's kernels through the C ABI (smem_linear):
+the few-row linear map (k_linear_skinny), the same with the LayerNorm fused
+(k_linear_skinny_ln), the stand-alone LayerNorm (k_ln_rows, whose output the
+call returns in ln_tmp for more than 128 rows), the tiled GEMM (k_gemm) and
+the GELU / residual / fp32 epilogues, against the model oracle's fp64
+layer_norm, gelu and linear on the same bf16 input bytes.
+
+Bounds (per output element), from the arithmetic: the inputs are exact bf16
+values and the accumulation is fp32, so y differs from the fp64 value by at
+most the output's own rounding, u |y_ref| (u = 2^-8, bf16), plus the fp32
+accumulation error, at most K 2^-24 sum_k |a_k w_k|; with a LayerNorm the
+normalised row a is rounded to bf16 before the product (one more rounding,
+u sum_k |a_k w_k|, plus 1e-5 of it for the fp32 statistics); GELU's erf
+(Abramowitz-Stegun 7.1.26, |error| <= 1.5e-7) adds 1e-6 |acc| and scales the
+accumulation error by at most 1.13.  These worst-case bounds are checked for
+every element; the RMS error must also stay within twice what independent
+roundings give (u / sqrt 3 of rms(y_ref), plus u / sqrt 3 of the rms of
+sqrt(sum_k (a_k w_k)^2) per LayerNorm rounding), which a systematic error of
+a percent in one op would exceed.  Shapes: the 1.5B model's maps (d 2048,
+4d 8192, vocabulary 50257) at 64 rows (few-row kernels) and at 520 or 136
+rows (LayerNorm pass + GEMM, ragged row tiles), and a ragged width (d 832,
+N 1000)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import smem_model as MO
+from paper_2609_32395_amd import smem, synth
+from tests import gpu_util
+from tests.gpu_util import require_gpu, say
+
+pytestmark = pytest.mark.gpu
+U = 2.0 ** -8
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+    yield
+    torch.cuda.synchronize()
+
+
+def _bf(g, shape, scale=1.0):
+    return synth.bf16_round((g.standard_normal(shape) * scale).astype(np.float32))
+
+
+def _d(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(torch.bfloat16)
+
+
+CASES = [  # name, M, N, K, layernorm, epilogue
+    ("1.5B q|k|v map, 64 rows", 64, 6144, 2048, True, smem.LIN_STORE),
+    ("1.5B q|k|v map, 520 rows", 520, 6144, 2048, True, smem.LIN_STORE),
+    ("1.5B FFN up + GELU, 64 rows", 64, 8192, 2048, True, smem.LIN_GELU),
+    ("1.5B FFN up + GELU, 520 rows", 520, 8192, 2048, True, smem.LIN_GELU),
+    ("1.5B FFN down + residual, 64 rows", 64, 2048, 8192, False, smem.LIN_RESID),
+    ("1.5B FFN down + residual, 520 rows", 520, 2048, 8192, False, smem.LIN_RESID),
+    ("1.5B attention out + residual, 64 rows", 64, 2048, 2048, False, smem.LIN_RESID),
+    ("1.5B head (fp32), 1 row", 1, 50257, 2048, True, smem.LIN_F32),
+    ("1.5B head (fp32), 64 rows", 64, 50257, 2048, True, smem.LIN_F32),
+    ("1.5B head (fp32), 136 rows", 136, 50257, 2048, True, smem.LIN_F32),
+    ("ragged d 832 x N 1000, 200 rows", 200, 1000, 832, True, smem.LIN_STORE),
+    ("ragged d 832 x N 1000, 16 rows", 16, 1000, 832, False, smem.LIN_GELU),
+]
+
+
+@pytest.mark.parametrize("name,M,N,K,ln,epi", CASES, ids=[c[0] for c in CASES])
+def test_linear_map_against_fp64(name, M, N, K, ln, epi):
+    say("op parity", name)
+    g = np.random.default_rng(M * 7 + N + K)
+    x = _bf(g, (M, K))
+    w = _bf(g, (N, K), 1.0 / math.sqrt(K))
+    lg = synth.bf16_round((1.0 + 0.1 * g.standard_normal(K)).astype(np.float32)) if ln else None
+    lb = synth.bf16_round((0.1 * g.standard_normal(K)).astype(np.float32)) if ln else None
+    res = _bf(g, (M, N)) if epi == smem.LIN_RESID else None
+    tmp = torch.empty((M, K), dtype=torch.bfloat16, device="cuda") if ln and M > 128 else None
+    y = smem.smem_linear(_d(x), _d(w), None if lg is None else _d(lg), None if lb is None else _d(lb), epi,
+                         None if res is None else _d(res), ln_tmp=tmp)
+    torch.cuda.synchronize()
+    y = y.float().cpu().numpy().astype(np.float64)
+    a = MO.layer_norm(x.astype(np.float64), lg, lb) if ln else x.astype(np.float64)
+    acc = MO.linear(a, w.astype(np.float64))
+    ref = acc
+    if epi == smem.LIN_GELU:
+        ref = MO.gelu(acc)
+    elif epi == smem.LIN_RESID:
+        ref = acc + res
+    absum = np.abs(a) @ np.abs(w.astype(np.float64)).T           # sum_k |a_k w_k|
+    sq = np.sqrt((a * a) @ (w.astype(np.float64) ** 2).T)        # sqrt(sum_k (a_k w_k)^2)
+    u_out = 0.0 if epi == smem.LIN_F32 else U
+    acc_err = K * 2.0 ** -24 * absum
+    bound = u_out * np.abs(ref) + acc_err * (1.13 if epi == smem.LIN_GELU else 1.0)
+    if ln:
+        bound = bound + (U + 1e-5) * absum * (1.13 if epi == smem.LIN_GELU else 1.0)
+    if epi == smem.LIN_GELU:
+        bound = bound + 1e-6 * np.abs(acc)
+    excess = np.abs(y - ref) - bound
+    rms_ref = float(np.sqrt(np.mean(ref * ref)))
+    err_rms = float(np.sqrt(np.mean((y - ref) ** 2)))
+    rms_limit = 2.0 * (u_out / math.sqrt(3.0) * rms_ref
+                       + (U / math.sqrt(3.0) * float(np.sqrt(np.mean(sq * sq))) if ln else 0.0)) + 1e-9 * rms_ref
+    raw = float(np.max(np.abs(y - ref))) / rms_ref
+    gpu_util.RECORDS.append((f"op {name} (rms error / its limit)", "op", raw, err_rms / rms_limit, 1.0, True))
+    say(f"op {name}: raw max|y-ref|/rms {raw:.3e}, rms err {err_rms / rms_ref:.3e} (limit {rms_limit / rms_ref:.3e}), "
+        f"worst element {float(np.max(np.abs(y - ref) / np.maximum(bound, 1e-30))):.3f} of its bound")
+    assert np.all(np.isfinite(y))
+    assert np.all(excess <= 0), f"{name}: {int(np.sum(excess > 0))} elements beyond their bound"
+    assert err_rms <= rms_limit, (name, err_rms, rms_limit)
+    if tmp is not None:                                          # the stand-alone LayerNorm's rows
+        ln_rows = tmp.float().cpu().numpy().astype(np.float64)
+        assert np.all(np.abs(ln_rows - a) <= U * np.abs(a) + 1e-5 * (1.0 + np.abs(a)))
+
+
+def test_linear_rows_independent_bitwise():
+    """A row's output does not depend on the other rows of the call: the same
+    rows at 64 (few-row kernel) and inside 520 (GEMM) give the same bits."""
+    say("op parity: row independence")
+    g = np.random.default_rng(3)
+    K, N = 2048, 6144
+    x = _bf(g, (520, K))
+    w = _d(_bf(g, (N, K), 1.0 / math.sqrt(K)))
+    lg = _d(synth.bf16_round((1.0 + 0.1 * g.standard_normal(K)).astype(np.float32)))
+    lb = _d(synth.bf16_round((0.1 * g.standard_normal(K)).astype(np.float32)))
+    big = smem.smem_linear(_d(x), w, lg, lb, smem.LIN_GELU)
+    small = smem.smem_linear(_d(x[100:164]), w, lg, lb, smem.LIN_GELU)
+    assert torch.equal(big[100:164], small)
+
+
+def test_linear_argument_errors():
+    """Shapes the kernels do not take are rejected before anything runs."""
+    z = lambda *shape: torch.zeros(shape, dtype=torch.bfloat16, device="cuda")
+    for x, w in [(z(4, 100), z(8, 100)),        # K not a multiple of 64
+                 (z(4, 64), z(6, 64))]:         # bf16 output with N % 4 != 0
+        with pytest.raises(smem.SmemError) as e:
+            smem.smem_linear(x, w)
+        assert e.value.code == smem.SMEM_EINVAL

@@ -43,7 +43,7 @@ def test_encode_prefill_160M():
     Q, K, V = (dev(x.reshape(-1, H, dh), BF) for x in (q, k, v))
     out = smem.smem_encode_blocks(st, Q, K, V, seq_ids=seqs, block_idx=blks, mask=smem.MASK_BIDIR)
     renc = O.encode_into_store(ref, seqs, blks, q, k, v, O.MASK_BIDIR)
-    check(out, renc.reshape(-1, H, dh), BF, "encoder, 128 blocks")
+    check(out, renc.reshape(-1, H, dh), BF, "160M encoder, 128 blocks x 12 heads", full=True)
     # stored rows are the output bits
     for s in (0, S - 1):
         idx, Ks, Vs = smem.smem_store_export(st, s)
@@ -57,7 +57,7 @@ def test_encode_prefill_160M():
                                           dev(kp.reshape(-1, H, dh), BF), dev(vp.reshape(-1, H, dh), BF))
     # end to end against the oracle's own encoder outputs (fp64 memory rows)
     rpre = O.reader_prefill_block(ref, list(range(S)), [NB - 1] * S, qp, kp, vp)
-    check(pout, rpre.reshape(-1, H, dh), BF, "prefill over oracle-encoded memory")
+    check(pout, rpre.reshape(-1, H, dh), BF, "160M final-block prefill over oracle-encoded memory", full=True)
 
 
 def _decode_inputs(w, seed, S, H, dh, b, steps):
@@ -80,7 +80,7 @@ def test_decode_410M_sampled():
         Kd, Vd = dev(Kh[0], BF), dev(Vh[0], BF)
         for j in range(NB):
             smem.smem_store_put_block(st, s, j, Kd[j], Vd[j])
-    steps = 3
+    steps = b                 # every sequence's in-block position wraps once
     qs, kn, vn, kc0, vc0 = _decode_inputs(w, 0, S, H, dh, b, steps)
     p0 = synth.decode_positions(w, 0, S)
     kc, vc = dev(kc0, BF), dev(vc0, BF)
@@ -91,6 +91,7 @@ def test_decode_410M_sampled():
         Kh, Vh = synth.memory_blocks(w, 0, [s], range(NB), threads=16)
         for j in range(NB):
             refs[s].put(s, j, Kh[0, j], Vh[0, j])
+    worst = (0.0, None)
     for t in range(steps):
         pos = [int((p0[s] + t) % b) for s in range(S)]
         out = smem.smem_reader_decode(st, list(range(S)), [NB] * S, pos, dev(qs[t], BF), dev(kn[t], BF),
@@ -100,10 +101,14 @@ def test_decode_410M_sampled():
             r, kcs, vcs = O.reader_decode(refs[s], [s], [NB], [pos[s]], qs[t, s:s + 1], kn[t, s:s + 1],
                                           vn[t, s:s + 1], kc_h[s:s + 1], vc_h[s:s + 1])
             kc_h[s], vc_h[s] = kcs[0], vcs[0]
-            check(got[s:s + 1], r, BF, f"decode step {t} seq {s}")
+            e = check(got[s:s + 1], r, BF, f"decode step {t} seq {s}")
+            if e >= worst[0]:
+                worst = (e, (got[s:s + 1], r, t, s))
         # the in-block caches of every sequence took the new row at pos
         kch = host(kc).reshape(S, b, H, dh)
         assert all(np.array_equal(kch[s, pos[s]], kn[t, s]) for s in range(S))
+    g_, r_, t_, s_ = worst[1]
+    check(g_, r_, BF, f"410M decode, {steps} steps x sequences {sample}: worst (step {t_}, seq {s_})", full=True)
 
 
 def _heads(x, hs):
@@ -133,13 +138,16 @@ def test_serve_1p5B_delete_reserve():
         return O.reader_prefill_block(ref, [0], [NB], _heads(q, hs)[None], _heads(k, hs)[None], _heads(v, hs)[None])[0]
 
     out = smem.smem_reader_prefill_block(st, [0], [NB], qd, kd, vd)
-    check(host(out)[:, hs], oracle_serve(range(NB)), BF, "serve over 32768 rows (4 heads)")
+    check(host(out)[:, hs], oracle_serve(range(NB)), BF, "1.5B serve over 32768 rows (heads 0,5,10,15)", full=True)
     order = synth.rng(0, w.wid, synth.ROLE_EDIT, 0, 0, 0).permutation(NB)[:100]
     for i, j in enumerate(order):
         smem.smem_delete_block(st, 0, int(j))
         out = smem.smem_reader_prefill_block(st, [0], [NB], qd, kd, vd)
+        if (i + 1) % 10 == 0:           # every 10th re-serve against the oracle
+            left = sorted(set(range(NB)) - set(int(x) for x in order[:i + 1]))
+            check(host(out)[:, hs], oracle_serve(left), BF, f"1.5B re-serve after {i + 1} deletes (4 heads)",
+                  full=(i + 1) == 100)
     remaining = sorted(set(range(NB)) - set(int(j) for j in order))
-    check(host(out)[:, hs], oracle_serve(remaining), BF, "re-serve after 100 deletes (4 heads)")
     # exact deletion: bit-identical to a store where the 100 blocks were never inserted
     fresh = smem.Store(1, NB + 1, NB, b, H, dh, BF)
     for j in reversed(remaining):
@@ -174,7 +182,8 @@ def test_stress_1p5B_edits_final_state():
     p0 = synth.decode_positions(w, 0, S)
     kc, vc = dev(kc0, BF), dev(vc0, BF)
     kc_h, vc_h = kc0.reshape(S, b, H, dh).copy(), vc0.reshape(S, b, H, dh).copy()
-    sample_seqs, hs = [3, 11], [0, 9]
+    sample_seqs = [3, 11]
+    snap_steps = [int(x) for x in np.linspace(0, steps - 1, 8).round()]
     snap = {}
     for t in range(steps):
         back = []
@@ -193,11 +202,11 @@ def test_stress_1p5B_edits_final_state():
         pos = [int((p0[s] + t) % b) for s in range(S)]
         out = smem.smem_reader_decode(st, list(range(S)), [NB] * S, pos, dev(qs[t], BF), dev(kn[t], BF),
                                       dev(vn[t], BF), kc, vc)
-        if t in (0, steps - 1):
-            snap[t] = (host(out), [sorted(live[s]) for s in sample_seqs], pos,
-                       kc_h[sample_seqs].copy(), vc_h[sample_seqs].copy())
         for s in range(S):
             kc_h[s, pos[s]], vc_h[s, pos[s]] = kn[t, s], vn[t, s]
+        if t in snap_steps:             # caches as the reader saw them (the new row written at pos)
+            snap[t] = (host(out), [sorted(live[s]) for s in sample_seqs], pos,
+                       kc_h[sample_seqs].copy(), vc_h[sample_seqs].copy())
     torch.cuda.synchronize()
     say("stress decode done; checking final state")
     # final state: live lists and every block's bytes
@@ -229,17 +238,37 @@ def test_stress_1p5B_edits_final_state():
     alt.close()
     del alt
     torch.cuda.empty_cache()
-    # attention parity on sampled sequences and heads at the first and last step
-    for t, (got, lives, pos, kcs, vcs) in snap.items():
-        for i, s in enumerate(sample_seqs):
-            ref = O.Store(1, NB, b, len(hs), dh)
-            blocks = lives[i]
-            for j0 in range(0, len(blocks), 512):
-                pairs = [synth.memory_block_device(w, 0, s, j) for j in blocks[j0:j0 + 512]]
-                Kc = torch.stack([p[0] for p in pairs])[:, :, hs].float().cpu().numpy()
-                Vc = torch.stack([p[1] for p in pairs])[:, :, hs].float().cpu().numpy()
-                for n, j in enumerate(blocks[j0:j0 + 512]):
-                    ref.put(0, j, Kc[n], Vc[n])
-            r, _, _ = O.reader_decode(ref, [0], [NB], [pos[s]], _heads(qs[t, s:s + 1], hs), _heads(kn[t, s:s + 1], hs),
-                                      _heads(vn[t, s:s + 1], hs), _heads(kcs[i:i + 1], hs), _heads(vcs[i:i + 1], hs))
-            check(got[s:s + 1][:, hs], r, BF, f"stress decode step {t} seq {s} heads {hs}")
+    # attention parity: 2 sequences x all 16 heads at 8 steps spread over the 128.
+    # One oracle store per head (heads are independent), brought to each
+    # snapshot's live set by the same edits in step order.
+    worst = (0.0, None)
+    for i, s in enumerate(sample_seqs):
+        Kall = np.empty((NB, b, H, dh), np.float32)
+        Vall = np.empty((NB, b, H, dh), np.float32)
+        for j0 in range(0, NB, 512):
+            pairs = [synth.memory_block_device(w, 0, s, j) for j in range(j0, min(NB, j0 + 512))]
+            Kall[j0:j0 + len(pairs)] = torch.stack([p[0] for p in pairs]).float().cpu().numpy()
+            Vall[j0:j0 + len(pairs)] = torch.stack([p[1] for p in pairs]).float().cpu().numpy()
+        refs = [O.Store(1, NB, b, 1, dh) for _ in range(H)]
+        cur = set()
+        for t in snap_steps:
+            got, lives, pos, kcs, vcs = snap[t]
+            want = set(lives[i])
+            for j in sorted(cur - want):
+                for h in range(H):
+                    refs[h].delete(0, j)
+            for j in sorted(want - cur):
+                for h in range(H):
+                    refs[h].put(0, j, Kall[j][:, h:h + 1], Vall[j][:, h:h + 1])
+            cur = want
+            r = np.concatenate([O.reader_decode(refs[h], [0], [NB], [pos[s]], _heads(qs[t, s:s + 1], [h]),
+                                                _heads(kn[t, s:s + 1], [h]), _heads(vn[t, s:s + 1], [h]),
+                                                _heads(kcs[i:i + 1], [h]), _heads(vcs[i:i + 1], [h]))[0]
+                                for h in range(H)], axis=1)
+            e = check(got[s:s + 1], r, BF, f"stress decode step {t} seq {s}, 16 heads")
+            if e >= worst[0]:
+                worst = (e, (got[s:s + 1], r, t, s))
+        del Kall, Vall, refs
+    g_, r_, t_, s_ = worst[1]
+    check(g_, r_, BF, f"1.5B stress decode, sequences {sample_seqs} x 16 heads x steps {snap_steps}: worst "
+                      f"(step {t_}, seq {s_})", full=True)
