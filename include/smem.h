@@ -415,7 +415,7 @@ smem_status smem_model_read(smem_model* m, int32_t seq, int32_t n_blocks, const 
  * reader layer, then run the reader on each of them; logits (device fp32
  * [b, vocab]) of the final block only.  first_block = 0 is the cold prefill
  * of a context; first_block > 0 with blocks 0 .. first_block - 1 cached is
- * partial reuse: the reader runs from the first uncached block (Section 3.1).
+ * partial reuse: only the blocks not yet cached are encoded before the read (Section 3.1).
  * The blocks must be absent (SMEM_EEXIST otherwise; nothing is changed). */
 smem_status smem_model_prefill(smem_model* m, int32_t seq, int32_t first_block, int32_t n_blocks,
                                const int32_t* tokens, float* logits, hipStream_t s);

@@ -342,7 +342,8 @@ def slot_indices(n_blocks: int, B: int):
 
 
 # ---------------------------------------------------------------- decode from the row plane
-# Appendix K (recomputing K/V from the memory rows instead of storing it) and
+# Appendix K (the decode arm that derives keys and values from the rows at
+# read time rather than keeping them) and
 # Appendix A ("Positions and memory"): one plane of rows per block, shared by
 # all reader layers; a layer's keys and values are the rows through that
 # layer's key and value maps, the null row a d-vector mapped the same way.
