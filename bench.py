@@ -67,8 +67,9 @@ MFMA_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published (2.5 PFLOP/s,
 # HBM bytes per decode call measured with rocprofv3 FETCH_SIZE/WRITE_SIZE
 # (scaled by a plain copy of known size), keyed by a hash of the decode
 # kernel's sources: a changed kernel reports traffic as null until measured
-# again.  Figures: profiles/k_reader_valu_decode_410M_hbm_traffic.md
-DECODE_TRAFFIC_BYTES = {"14938d8a7ab2c12d": 1.0885e+09}
+# again.  Figures: profiles/hbm_traffic_attention_kernels.md (reader + merge,
+# read + written per step).
+DECODE_TRAFFIC_BYTES = {"8dad1c9ebea57911": 1.0890e+09}
 DECODE_SOURCES = ("paper_2609_32395_amd/csrc/reader_valu.hip", "paper_2609_32395_amd/csrc/common.h")
 
 
@@ -825,9 +826,20 @@ def cpu_baseline(dec, budget_s, seed):
         single = round(n1 / t1s, 3)
     except Exception:
         pass
+    # /proc/cpuinfo's model name as the host reports it (a virtual machine may
+    # report a short one), with the family / model / stepping numbers
     cpu_model = ""
     try:
-        cpu_model = next(l.split(":", 1)[1].strip() for l in open("/proc/cpuinfo") if l.startswith("model name"))
+        info = {}
+        for l in open("/proc/cpuinfo"):
+            if ":" in l:
+                k, v = (x.strip() for x in l.split(":", 1))
+                info.setdefault(k, v)
+            elif info:
+                break
+        cpu_model = "%s (family %s, model %s, stepping %s, %d logical CPUs)" % (
+            info.get("model name", "?"), info.get("cpu family", "?"), info.get("model", "?"),
+            info.get("stepping", "?"), os.cpu_count() or 0)
     except Exception:
         pass
     return {"value": round(n_tok / spent, 3), "unit": "tokens/s", "cores": int(blas_threads), "kind": "oracle",
