@@ -753,6 +753,59 @@ def model_decode_workload(args, torch, smem, synth):
     return out
 
 
+def delete_generate_workload(args, torch, smem, synth):
+    """Whole-model delete-then-generate, the SMem arm (the serving appendix's
+    cell grid): a context of J cached blocks (batch 1) loses block j at 25, 50
+    or 75% of the context (row slice: the block leaves every reader layer's
+    store), then the final block is read alone (block-skip) for the next
+    token's logits.  Timed: the deletion and the read, from one event to the
+    next; the block is re-encoded afterwards, untimed, for the next cell."""
+    stream = torch.cuda.current_stream()
+    sizes = [int(x) for x in args.delgen_blocks.split(",")]
+    out = {}
+    for name, d, E, D in [sc for sc in synth.MODEL_SCALES if sc[0] in args.model_scales.split(",")]:
+        H, b, vocab, T = d // 32, 64, synth.MODEL_VOCAB, synth.MODEL_T
+        W = synth.model_weights_device(smem.model_weight_shapes(E, D, d, vocab, T), args.seed)
+        for J in sizes:
+            m = smem.Model(W, E, D, d, H, b, vocab, T, 1, J, J, max_tokens=128 * b)
+            ctx = torch.from_numpy(synth.model_tokens(args.seed, name, J * b, vocab)).to("cuda")
+            for j0 in range(0, J - 1, 128):             # cache blocks 0 .. J-2; block J-1 is the query
+                j1 = min(J - 1, j0 + 128)
+                smem.smem_model_encode(m, 0, list(range(j0, j1)), ctx[j0 * b:j1 * b])
+            last = ctx[(J - 1) * b:].contiguous()
+            logits = torch.empty((b, vocab), dtype=torch.float32, device="cuda")
+            smem.smem_model_read(m, 0, [J - 1], last, logits=logits)      # warm the path
+            cells = {}
+            for frac in (25, 50, 75):
+                j = (J - 1) * frac // 100
+                ts = []
+                for rep in range(3):
+                    torch.cuda.synchronize()
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    smem.smem_model_delete_block(m, 0, j)
+                    smem.smem_model_read(m, 0, [J - 1], last, logits=logits)
+                    e1.record(stream)
+                    e1.synchronize()
+                    ts.append(e0.elapsed_time(e1))
+                    smem.smem_model_encode(m, 0, [j], ctx[j * b:(j + 1) * b])
+                cells[f"{frac}%"] = round(float(np.median(ts)), 3)
+            torch.cuda.synchronize()
+            mem_bytes = 4.0 * D * (J - 2) * b * d                 # memory keys/values read after the deletion
+            wbytes = 2.0 * (14 * D * d * d + vocab * d)
+            ms = float(np.median(list(cells.values())))
+            out[f"{name} {J} blocks"] = dict(delete_then_generate_ms=cells,
+                                             hbm_gbs=round((mem_bytes + wbytes) / (ms / 1e3) / 1e9, 1))
+            print(f"[bench] delete-then-generate {name} {J} blocks: {cells} ms", file=sys.stderr, flush=True)
+            m.close()
+            del ctx, last, logits
+            torch.cuda.empty_cache()
+        del W
+        torch.cuda.empty_cache()
+    return out
+
+
 def model_oracle_time(args, torch, smem, synth, W, E, D, d, H, b, vocab, T, n):
     """The fp64 model oracle's block-skip read of the final block of an
     n-token context (the same unit as the GPU's block_skip_ms), on this host;
@@ -855,13 +908,16 @@ def main():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-secondary", action="store_true")
-    ap.add_argument("--workloads", default="encode,serve,stream,rows,stress,delete_sweep,rope,model,model_decode",
+    ap.add_argument("--workloads", default="encode,serve,stream,rows,stress,delete_sweep,rope,model,model_decode,"
+                                           "delete_generate",
                     help="secondary workloads to run (comma list of encode, serve, stream, rows, stress, rope: "
                          "the rotary composite timed beside the headline decode and the serve; model: the whole "
                          "model's block-skip serve against its cold prefill; model_decode: the whole model's "
                          "batched KV-cached decode at the paper's cells; delete_sweep: deletion latency from "
-                         "512 to 65,536 cached blocks)")
+                         "512 to 65,536 cached blocks; delete_generate: the whole model's delete-then-generate "
+                         "cycle at 512 and 4096 cached blocks)")
     ap.add_argument("--delete-sizes", default="512,1024,4096,16384,65536")
+    ap.add_argument("--delgen-blocks", default="512,4096")
     ap.add_argument("--model-scales", default="160M,410M,1.5B")
     ap.add_argument("--model-lengths", default="1024,2048,4096,8192")
     ap.add_argument("--model-reps", type=int, default=3)
@@ -918,6 +974,8 @@ def main():
             secondary["model_block_skip"] = model_workload(args, torch, smem, synth)
         if "model_decode" in wl:
             secondary["model_decode"] = model_decode_workload(args, torch, smem, synth)
+        if "delete_generate" in wl:
+            secondary["delete_then_generate"] = delete_generate_workload(args, torch, smem, synth)
     cpu = None
     if dec is None:
         print(json.dumps({"metric": "profiling run (no headline)", "value": None, "secondary": secondary}))
