@@ -771,7 +771,9 @@ __global__ void __launch_bounds__(64 * 4 * QW) k_prefill_mfma_par(ReaderArgs a) 
   const int pair = (n / (8 * NPART)) * 8 + (n % 8), part = (n / 8) % NPART;
   if (pair >= a.n_slots * a.H) return;   // padding of the last round (whole workgroup)
   const int slot = pair / a.H, h = pair % a.H;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // wave-uniform values held as such (scalar registers): the page lookups
+  // below are then scalar loads, which no vector-memory wait covers
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = wave / QW, qw = wave % QW;
   const int n_read = a.n_read[slot], pps = a.pps[slot];
   const int nms = (n_read + pps - 1) / pps;
@@ -801,15 +803,14 @@ __global__ void __launch_bounds__(64 * 4 * QW) k_prefill_mfma_par(ReaderArgs a) 
   }
   const uint8_t* gpages = (const uint8_t*)a.pages;
   const uint32_t lds0 = (uint32_t)(uintptr_t)L + (uint32_t)(g * P::NSP * R::TILE + qw * P::IPW * 1024);
-  auto issue = [&](int pi, int stage) {
-    const uint8_t* t = gpages + page_head_offset(lpc[pi], h, a.H, BT, DH) * 2;
+  auto issue_page = [&](int page, int stage) {
+    const uint8_t* t = gpages + page_head_offset(page, h, a.H, BT, DH) * 2;
     const uint32_t d0 = lds0 + (uint32_t)(stage * R::TILE);
 #pragma unroll
     for (int i = 0; i < P::IPW; ++i) dma16(t + src[i], __builtin_amdgcn_readfirstlane(d0 + i * 1024));
   };
-#pragma unroll
-  for (int k = 0; k < P::NSP; ++k)
-    if (p0 + k < p1) issue(p0 + k, k);
+  auto issue = [&](int pi, int stage) { issue_page(lpc[pi], stage); };
+  if (p0 < p1) issue(p0, 0);              // the first page; the rest of the ring after the loads below
 
   // ---- query fragments; the in-block tile (ring layout) and the null row into LDS
   bf16x8 qf[DH / 32];
@@ -826,6 +827,14 @@ __global__ void __launch_bounds__(64 * 4 * QW) k_prefill_mfma_par(ReaderArgs a) 
                                                                    : ((size_t)a.H + h) * DH + (tid - CPR) * 8);
     *(u32x4*)(nul + tid * 8) = *(const u32x4*)nsrc;
   }
+  // The loads above are waited for here, with the first page (the compiler
+  // waits for every vector-memory load before their first use, the page DMA
+  // included); the rest of the ring is issued only now, so that wait does
+  // not cover it.
+  wait_vm<0>();
+#pragma unroll
+  for (int k = 1; k < P::NSP; ++k)
+    if (p0 + k < p1) issue(p0 + k, k);
 
   // ---- memory pages (all groups step together) and the final split
   floatx4 o[DH / 16], of[DH / 16];
@@ -837,9 +846,13 @@ __global__ void __launch_bounds__(64 * 4 * QW) k_prefill_mfma_par(ReaderArgs a) 
   float m = -INFINITY, l = 0.f, mf = -INFINITY, lf = 0.f;
   for (int k = 0; k < steps; ++k) {
     const int pi = p0 + k;
+    // the page this step refills the ring with: its number is looked up
+    // before the waits below, so the lookup overlaps them
+    const bool refill = k > 0 && pi + P::NSP - 1 < p1;
+    const int next_page = refill ? lpc[pi + P::NSP - 1] : 0;
     wait_pages<P::IPW>(pi < p1 ? min(k == 0 ? P::NSP - 1 : P::NSP - 2, p1 - 1 - pi) : 0);
     lds_barrier();                       // page k of every group is in LDS; every wave is done with page k - 1
-    if (k > 0 && pi + P::NSP - 1 < p1) issue(pi + P::NSP - 1, (k + P::NSP - 1) % P::NSP);
+    if (refill) issue_page(next_page, (k + P::NSP - 1) % P::NSP);
     if (pi < p1) {
       const uint8_t* tile = L + (g * P::NSP + k % P::NSP) * R::TILE;
       floatx4 s[4];
