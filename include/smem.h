@@ -289,20 +289,23 @@ typedef struct {
   int32_t max_blocks;
   int32_t n_pages;
   int32_t b;          /* 16 or 64 */
-  int32_t d;          /* row width: 512, 1024 or 2048 */
+  int32_t d;          /* row width: 512, 768, 1024 or 2048 */
   int32_t dtype;      /* SMEM_BF16 */
 } smem_rows_desc;
 
 /* One reader layer's maps, device bf16: w_k, w_v [H*dh, d] (a linear
  * layer's out x in layout: the key of row r is w_k r, head h taking outputs
- * h*dh .. h*dh+dh-1), null_row [d] or NULL.  1 <= H <= 16, dh in
- * {32, 64, 128}. */
+ * h*dh .. h*dh+dh-1), null_row [d] or NULL.  null_kv: NULL, or the null
+ * row already through the maps, [2, H, dh] (keys then values; null_row is
+ * then ignored), for callers that map it once rather than on every call.
+ * 1 <= H <= 64, dh in {32, 64, 128}. */
 typedef struct {
   int32_t H;
   int32_t dh;
   const void* w_k;
   const void* w_v;
   const void* null_row;
+  const void* null_kv;
 } smem_rows_layer;
 
 /* Device bytes of a row store: pages, block table, live lists and the

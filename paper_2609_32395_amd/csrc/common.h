@@ -292,15 +292,17 @@ struct ReaderArgs {
 };
 
 // Row-plane decode (bf16): rows of width d, absorbed queries, split partials.
+// Heads are read in tiles of 16 (one MFMA row tile): ht = ceil(H / 16) tiles,
+// head h in tile h / 16, padded heads zero.
 struct RowsArgs {
   const uint16_t* pages;      // row pages [n_pages][b][d]
   const int32_t* live_page;   // [n_seq][max_blocks]
-  const uint16_t* qabs;       // absorbed queries [slot][16][d]
-  float* part;                // split partials: U[16][d], m[16], l[16]
+  const uint16_t* qabs;       // absorbed queries [slot][ht*16][d]
+  float* part;                // split partials per (slot, split, tile): U[16][d], m[16], l[16]
   const float* intra;         // in-block / null partials [slot][H][dh+4]
   const uint16_t* w_v;        // value map [H*dh][d]
-  uint16_t* ubuf;             // combined weighted rows [slot][16][d] (bf16)
-  float* sw;                  // in-block weight / L per [slot][16]
+  uint16_t* ubuf;             // combined weighted rows [slot][ht*16][d] (bf16)
+  float* sw;                  // in-block weight / L per [slot][ht*16]
   uint16_t* out;              // [slot][H][dh]
   // in-block keys and the mapped null row (the split after the row splits)
   const uint16_t* q;          // [slot][H][dh]
@@ -314,23 +316,27 @@ struct RowsArgs {
   int32_t max_blocks;
   int32_t b;
   int32_t H;
+  int32_t ht;                 // head tiles
+  int32_t max_split;          // row splits of the launch's longest read
   int32_t n_slots;
   int32_t seq[kMaxSlots];
   int32_t n_read[kMaxSlots];
   int32_t pps[kMaxSlots];
-  int32_t pbase[kMaxSlots];   // first partial of the slot
+  int32_t pbase[kMaxSlots];   // first partial of the slot; split k, tile t at pbase + k*ht + t
   int32_t pos[kMaxSlots];     // in-block position of the new token
 };
+constexpr int kRowsMaxHeads = 64;
 
 struct RowsPrepArgs {
   const uint16_t* q;          // [slot][H][dh]
   const uint16_t* w_k;        // key map [H*dh][d]
   const uint16_t* w_v;
   const uint16_t* null_row;   // [d] or NULL
-  uint16_t* qabs;             // [slot][16][d]
+  uint16_t* qabs;             // [slot][ht*16][d]
   uint16_t* null_kv;          // [2][H][dh]
   int32_t d;
   int32_t H;
+  int32_t ht;
   int32_t n_slots;
   float scale_log2;
 };

@@ -32,7 +32,8 @@ struct RowsCfg {
   static constexpr int MP = D + 8;                 // LDS row pitch (elements): 16-byte pad per row
   // ring stages (LDS: NS * 16 rows * MP * 2 bytes; at most 2 at d = 2048)
   static constexpr int NS = D >= 2048 ? 2 : SMEM_ROWS_STAGES;
-  static constexpr int KW = kRowChunk * D / 512 / 4;   // 1 KiB DMA instructions per wave per chunk
+  static constexpr int RI = (D + 511) / 512;          // DMA instructions per row (the last partial at d = 768)
+  static constexpr int KW = kRowChunk * RI / 4;        // DMA instructions per wave per chunk
   static constexpr int DW = D / 4;                 // dims per wave (score reduction, U ownership)
   static constexpr int NT = DW / 16;               // U tiles per wave
 };
@@ -53,7 +54,8 @@ struct RowsLds {
 constexpr float kLazy = 8.f;
 
 // Wave `wave` moves rows 4*wave .. 4*wave+3 of chunk c into stage st: each
-// row is D*2 bytes = D/512 DMA instructions of 1 KiB.
+// row is D*2 bytes, DMA instructions of 1 KiB (512 elements) and, at
+// d = 768, one of 512 bytes (the lanes past the row's end stay idle).
 template <int D>
 __device__ __forceinline__ void chunk_dma(RowsLds<D>& L, int st, const uint16_t* __restrict__ src, int wave,
                                           int lane) {
@@ -61,10 +63,10 @@ __device__ __forceinline__ void chunk_dma(RowsLds<D>& L, int st, const uint16_t*
   for (int r = 0; r < 4; ++r) {
     const int row = wave * 4 + r;
 #pragma unroll
-    for (int hk = 0; hk < D / 512; ++hk) {
+    for (int hk = 0; hk < RowsCfg<D>::RI; ++hk) {
       const uint16_t* g = src + (size_t)row * D + hk * 512 + lane * 8;
       const uint32_t l = (uint32_t)(uintptr_t)&L.mu[st][row * RowsCfg<D>::MP + hk * 512];
-      dma16(g, __builtin_amdgcn_readfirstlane(l));
+      if (hk * 512 + 512 <= D || hk * 512 + lane * 8 < D) dma16(g, __builtin_amdgcn_readfirstlane(l));
     }
   }
 }
@@ -146,13 +148,21 @@ __device__ __forceinline__ void rows_intra(const RowsArgs& a, int slot, int h, i
   }
 }
 
-// One workgroup per (sequence slot, split).  Wave w reduces dims
-// [w*D/4, (w+1)*D/4) of the scores and owns the same dims of U.
+// One workgroup per (sequence slot, split, head tile).  The head tiles of one
+// (slot, split) read the same rows: their launch indices are 8 apart, so
+// they run on one XCD (workgroups are dealt to the 8 XCDs in turn) and share
+// its L2.  Wave w reduces dims [w*D/4, (w+1)*D/4) of the scores and owns the
+// same dims of U.
+inline int rows_grid(int units, int ht) { return ((units + 7) / 8) * 8 * ht; }
+
 template <int D, int DHq>
 __global__ void __launch_bounds__(256) k_reader_rows(RowsArgs a) {
   using C = RowsCfg<D>;
   __shared__ RowsLds<D> L;
-  const int split = blockIdx.x, slot = blockIdx.y;
+  const int n = blockIdx.x;
+  const int unit = (n / (8 * a.ht)) * 8 + n % 8, tile = (n / 8) % a.ht;
+  const int slot = unit / a.max_split, split = unit % a.max_split;
+  if (slot >= a.n_slots) return;            // padding of the last round (whole workgroup)
   const int n_read = a.n_read[slot], pps = a.pps[slot];
   const int nsp = (n_read + pps - 1) / pps;
   if (split >= nsp) return;
@@ -163,7 +173,7 @@ __global__ void __launch_bounds__(256) k_reader_rows(RowsArgs a) {
   // absorbed-query fragments of this wave's dims stay in registers (A operand)
   u32x4 qa[DW / 32];
   {
-    const uint16_t* qs = a.qabs + ((size_t)slot * 16 + (lane & 15)) * D + wave * DW + (lane >> 4) * 8;
+    const uint16_t* qs = a.qabs + ((size_t)(slot * a.ht + tile) * 16 + (lane & 15)) * D + wave * DW + (lane >> 4) * 8;
 #pragma unroll
     for (int kk = 0; kk < DW / 32; ++kk) qa[kk] = *(const u32x4*)(qs + kk * 32);
   }
@@ -268,7 +278,7 @@ __global__ void __launch_bounds__(256) k_reader_rows(RowsArgs a) {
     }
   }
   // partial: U[16][D], then m[16], l[16]
-  float* part = a.part + (size_t)(a.pbase[slot] + split) * (16 * D + 32);
+  float* part = a.part + (size_t)(a.pbase[slot] + split * a.ht + tile) * (16 * D + 32);
 #pragma unroll
   for (int n = 0; n < NT; ++n) {
     const int dim = wave * DW + n * 16 + (lane & 15);
@@ -282,7 +292,7 @@ __global__ void __launch_bounds__(256) k_reader_rows(RowsArgs a) {
 }
 
 // Absorbed queries: qabs[slot][h][c] = scale_log2 * sum_j W_K[h*dh + j][c] q[slot][h][j]
-// (bf16; zero rows for heads h >= H).  The maps are [H*dh][d] (a linear
+// (bf16; zero rows for the padded heads H <= h < ht*16).  The maps are [H*dh][d] (a linear
 // layer's out x in layout), so a thread per c reads them coalesced; a
 // workgroup serves kAbsorbSlots query slots, the j loop unrolled so several
 // map loads are in flight.
@@ -314,7 +324,7 @@ __global__ void __launch_bounds__(256) k_rows_absorb_q(RowsPrepArgs a) {
   }
 #pragma unroll
   for (int sl = 0; sl < kAbsorbSlots; ++sl)
-    if (sl < ns) a.qabs[((size_t)(s0 + sl) * 16 + h) * a.d + c] = f32_to_bf16_bits(acc[sl] * a.scale_log2);
+    if (sl < ns) a.qabs[((size_t)(s0 + sl) * a.ht * 16 + h) * a.d + c] = f32_to_bf16_bits(acc[sl] * a.scale_log2);
 }
 
 // The null row through each head's key and value maps:
@@ -350,7 +360,9 @@ __global__ void __launch_bounds__(256) k_rows_combine(RowsArgs a) {
   __shared__ float pw[64];
   __shared__ float stat[4];   // m_i, l_i, Mr, l'
   __shared__ float fin[1];    // scale of u' (times 1/L)
-  const float* pb = a.part + (size_t)a.pbase[slot] * (16 * D + 32);
+  const int tile = h / 16, hh = h % 16;     // the head's tile and its row in the tile
+  const size_t ustride = (size_t)a.ht * (16 * D + 32);    // one split of the slot to the next
+  const float* pb = a.part + (size_t)(a.pbase[slot] + tile) * (16 * D + 32);
   const int lane = tid & 63, wave = tid >> 6;
   if (wave == 0) {
     float mi, li;
@@ -361,7 +373,7 @@ __global__ void __launch_bounds__(256) k_rows_combine(RowsArgs a) {
     }
   } else {
     // each of waves 1-3 derives the split weights itself (no block barrier)
-    const float mk = lane < nsp ? pb[(size_t)lane * (16 * D + 32) + 16 * D + h] : -INFINITY;
+    const float mk = lane < nsp ? pb[(size_t)lane * ustride + 16 * D + hh] : -INFINITY;
     float Mr = mk;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) Mr = fmaxf(Mr, __shfl_xor(Mr, o));
@@ -371,13 +383,13 @@ __global__ void __launch_bounds__(256) k_rows_combine(RowsArgs a) {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     if (wave == 1 && lane == 0) {
       float l = 0.f;
-      for (int k = 0; k < nsp; ++k) l += w_sh[1][k] * pb[(size_t)k * (16 * D + 32) + 16 * D + 16 + h];
+      for (int k = 0; k < nsp; ++k) l += w_sh[1][k] * pb[(size_t)k * ustride + 16 * D + 16 + hh];
       stat[2] = Mr;
       stat[3] = l;
     }
     for (int c = (wave - 1) * 64 + lane; c < D; c += 192) {
       float x = 0.f;
-      for (int k = 0; k < nsp; ++k) x += w_sh[wave][k] * pb[(size_t)k * (16 * D + 32) + (size_t)h * D + c];
+      for (int k = 0; k < nsp; ++k) x += w_sh[wave][k] * pb[(size_t)k * ustride + (size_t)hh * D + c];
       u_sh[c] = x;
     }
   }
@@ -390,11 +402,11 @@ __global__ void __launch_bounds__(256) k_rows_combine(RowsArgs a) {
     const float L = wr * stat[3] + wi * stat[1];
     const float inv = (L > 0.f) ? 1.f / L : 0.f;
     fin[0] = wr * inv;
-    a.sw[(size_t)slot * 16 + h] = wi * inv;
+    a.sw[(size_t)slot * a.ht * 16 + h] = wi * inv;
   }
   __syncthreads();
   const float sc = fin[0];
-  for (int c = tid; c < D; c += 256) a.ubuf[((size_t)slot * 16 + h) * D + c] = f32_to_bf16_bits(u_sh[c] * sc);
+  for (int c = tid; c < D; c += 256) a.ubuf[((size_t)slot * a.ht * 16 + h) * D + c] = f32_to_bf16_bits(u_sh[c] * sc);
 }
 
 // out[s][h][j] = sum_c u[s][h][c] W_V[h*dh + j][c] + (w_i/L)[s][h] acc_i[s][h][j]:
@@ -407,7 +419,7 @@ __global__ void __launch_bounds__(256) k_rows_project(RowsArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int srow = s0 + (lane & 15);
   const bool valid = srow < a.n_slots;
-  const uint16_t* ua = a.ubuf + ((size_t)(valid ? srow : 0) * 16 + h) * D + (lane >> 4) * 8;
+  const uint16_t* ua = a.ubuf + ((size_t)(valid ? srow : 0) * a.ht * 16 + h) * D + (lane >> 4) * 8;
   const uint16_t* wb = a.w_v + ((size_t)h * DHq + j0 + (lane & 15)) * D + (lane >> 4) * 8;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -429,7 +441,7 @@ __global__ void __launch_bounds__(256) k_rows_project(RowsArgs a) {
     const int s = s0 + 4 * (lane >> 4) + i;
     if (s < a.n_slots) {
       const float* ip = a.intra + ((size_t)s * a.H + h) * (DHq + 4);
-      const float o = acc[i] + a.sw[(size_t)s * 16 + h] * ip[j];
+      const float o = acc[i] + a.sw[(size_t)s * a.ht * 16 + h] * ip[j];
       a.out[((size_t)s * a.H + h) * DHq + j] = f32_to_bf16_bits(o);
     }
   }
@@ -439,14 +451,19 @@ template <int D, int DHq>
 static hipError_t launch_rows_dd(const RowsArgs& a, const RowsPrepArgs& pa, int max_split, int stage,
                                  hipStream_t s) {
   if (stage == 0) {   // absorbed queries (and the null row's keys and values)
-    hipLaunchKernelGGL((k_rows_absorb_q<DHq>), dim3((D + 255) / 256, 16, (pa.n_slots + kAbsorbSlots - 1) / kAbsorbSlots),
-                       dim3(256), 0, s, pa);
+    hipLaunchKernelGGL((k_rows_absorb_q<DHq>),
+                       dim3((D + 255) / 256, pa.ht * 16, (pa.n_slots + kAbsorbSlots - 1) / kAbsorbSlots), dim3(256),
+                       0, s, pa);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || pa.null_row == nullptr) return e;
     hipLaunchKernelGGL((k_rows_null<DHq>), dim3(pa.H, 2), dim3(256), 0, s, pa);
     return hipGetLastError();
   }
-  if (max_split > 0) hipLaunchKernelGGL((k_reader_rows<D, DHq>), dim3(max_split, a.n_slots), dim3(256), 0, s, a);
+  if (max_split > 0) {
+    RowsArgs r = a;
+    r.max_split = max_split;
+    hipLaunchKernelGGL((k_reader_rows<D, DHq>), dim3(rows_grid(a.n_slots * max_split, a.ht)), dim3(256), 0, s, r);
+  }
   hipLaunchKernelGGL((k_rows_combine<D, DHq>), dim3(a.n_slots, a.H), dim3(256), 0, s, a);
   hipLaunchKernelGGL((k_rows_project<D, DHq>), dim3(a.H, (a.n_slots + 15) / 16, DHq / 16), dim3(256), 0, s, a);
   return hipGetLastError();
@@ -469,6 +486,7 @@ hipError_t launch_rows(int d, int dh, const RowsArgs& a, const RowsPrepArgs& pa,
     if (ns > max_split) max_split = ns;
   }
   if (d == 512) return launch_rows_d<512>(dh, a, pa, max_split, stage, s);
+  if (d == 768) return launch_rows_d<768>(dh, a, pa, max_split, stage, s);
   if (d == 1024) return launch_rows_d<1024>(dh, a, pa, max_split, stage, s);
   if (d == 2048) return launch_rows_d<2048>(dh, a, pa, max_split, stage, s);
   return hipErrorInvalidValue;

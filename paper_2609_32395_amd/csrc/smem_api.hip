@@ -183,11 +183,13 @@ int splits_rows(int n_read) { return n_read > 0 ? (n_read + pps_rows(n_read) - 1
 bool rows_layout_of(const smem_rows_desc* d, DevLayout* L) {
   if (!d) return false;
   if (d->n_seq < 1 || d->max_blocks < 1 || d->n_pages < 1) return false;
-  if (!(d->b == 16 || d->b == 64) || !(d->d == 512 || d->d == 1024 || d->d == 2048) || d->dtype != BF16) return false;
+  if (!(d->b == 16 || d->b == 64) || !(d->d == 512 || d->d == 768 || d->d == 1024 || d->d == 2048) || d->dtype != BF16)
+    return false;
   const size_t nt = (size_t)d->n_seq * d->max_blocks;
   // splits of one read never exceed min(kRowsSplitCap, ceil(n_read / kMinPagesRows)), n_read <= max_blocks
   const int64_t per_seq = std::min(kRowsSplitCap, (d->max_blocks + kMinPagesRows - 1) / kMinPagesRows);
-  const int64_t cap = std::min<int64_t>(kRowsPartials, (int64_t)d->n_seq * per_seq);
+  // one partial per (split, head tile): a read takes at most per_seq splits of up to 4 tiles
+  const int64_t cap = std::min<int64_t>(kRowsPartials, (int64_t)d->n_seq * per_seq * (kRowsMaxHeads / 16));
   L->part_cap = (int32_t)std::max<int64_t>(cap, 1);
   L->ws_floats = 0;
   size_t off = 0;
@@ -195,10 +197,10 @@ bool rows_layout_of(const smem_rows_desc* d, DevLayout* L) {
   L->off_live_page = off; off = align256(off + nt * 4);
   L->off_live_blk = off;  off = align256(off + nt * 4);
   L->off_n_live = off;    off = align256(off + (size_t)d->n_seq * 4);
-  L->off_qabs = off;      off = align256(off + (size_t)kMaxSlots * 16 * d->d * 2);
-  L->off_intra = off;     off = align256(off + (size_t)kMaxSlots * 16 * (128 + 4) * 4);
-  L->off_null_kv = off;   off = align256(off + (size_t)2 * 16 * 128 * 2);
-  L->off_sw = off;        off = align256(off + (size_t)kMaxSlots * 16 * 4);
+  L->off_qabs = off;      off = align256(off + (size_t)kMaxSlots * kRowsMaxHeads * d->d * 2);
+  L->off_intra = off;     off = align256(off + (size_t)kMaxSlots * kRowsMaxHeads * (128 + 4) * 4);
+  L->off_null_kv = off;   off = align256(off + (size_t)2 * kRowsMaxHeads * 128 * 2);
+  L->off_sw = off;        off = align256(off + (size_t)kMaxSlots * kRowsMaxHeads * 4);
   L->off_part = off;      off = align256(off + (size_t)L->part_cap * (16 * (size_t)d->d + 32) * 4);
   L->off_ws = L->off_part;
   L->off_pages = off;     off = align256(off + (size_t)d->n_pages * d->b * d->d * 2);
@@ -947,8 +949,9 @@ smem_status smem_reader_decode_rows(smem_store* st, const smem_rows_layer* layer
   if (st->kind != 1) return fail(SMEM_EINVAL, "not a row store");
   if (!layer) return fail(SMEM_EINVAL, "layer is NULL");
   const int H = layer->H, dh = layer->dh, D = st->rows_d, b = st->d.b;
-  if (H < 1 || H > 16 || !(dh == 32 || dh == 64 || dh == 128))
-    return fail(SMEM_EINVAL, "layer shape H=%d dh=%d (need 1 <= H <= 16, dh in {32,64,128})", H, dh);
+  if (H < 1 || H > kRowsMaxHeads || !(dh == 32 || dh == 64 || dh == 128))
+    return fail(SMEM_EINVAL, "layer shape H=%d dh=%d (need 1 <= H <= %d, dh in {32,64,128})", H, dh, kRowsMaxHeads);
+  const int ht = (H + 15) / 16;
   if (!layer->w_k || !layer->w_v) return fail(SMEM_EINVAL, "w_k and w_v are required");
   if (n_seq < 0) return fail(SMEM_EINVAL, "n_seq < 0");
   if (n_seq == 0) return SMEM_OK;
@@ -957,7 +960,8 @@ smem_status smem_reader_decode_rows(smem_store* st, const smem_rows_layer* layer
   if (n_given != 0 && n_given != 4) return fail(SMEM_EINVAL, "k_new, v_new, k_cache, v_cache: all or none");
   if (n_given == 4 && !pos) return fail(SMEM_EINVAL, "pos is required with in-block keys");
   if (!aligned16(q) || !aligned16(out) || !aligned16(k_new) || !aligned16(v_new) || !aligned16(k_cache) ||
-      !aligned16(v_cache) || !aligned16(layer->w_k) || !aligned16(layer->w_v) || !aligned16(layer->null_row))
+      !aligned16(v_cache) || !aligned16(layer->w_k) || !aligned16(layer->w_v) || !aligned16(layer->null_row) ||
+      !aligned16(layer->null_kv))
     return fail(SMEM_EINVAL, "tensors must be 16-byte aligned");
   std::set<int32_t> seen;
   for (int i = 0; i < n_seq; ++i) {
@@ -974,7 +978,8 @@ smem_status smem_reader_decode_rows(smem_store* st, const smem_rows_layer* layer
   float* intra = (float*)(st->pool + L.off_intra);
   uint16_t* null_kv = (uint16_t*)(st->pool + L.off_null_kv);
   float* part = (float*)(st->pool + L.off_part);
-  bool null_done = false;
+  // the null row through the layer's maps: given, or mapped by the first launch
+  bool null_done = layer->null_kv != nullptr;
   int i0 = 0;
   while (i0 < n_seq) {
     // a launch: at most kMaxSlots sequences whose split partials fit the workspace
@@ -982,7 +987,7 @@ smem_status smem_reader_decode_rows(smem_store* st, const smem_rows_layer* layer
     int32_t nread[kMaxSlots];
     while (i0 + n < n_seq && n < kMaxSlots) {
       const int nr = n_read_of(st, seq_ids[i0 + n], query_block[i0 + n]);
-      const int sp = splits_rows(nr);
+      const int sp = splits_rows(nr) * ht;
       if (n > 0 && used + sp > L.part_cap) break;
       nread[n] = nr;
       used += sp;
@@ -996,7 +1001,7 @@ smem_status smem_reader_decode_rows(smem_store* st, const smem_rows_layer* layer
     pa.null_row = null_done ? nullptr : (const uint16_t*)layer->null_row;
     pa.qabs = qabs;
     pa.null_kv = null_kv;
-    pa.d = D; pa.H = H; pa.n_slots = n; pa.scale_log2 = scale_log2;
+    pa.d = D; pa.H = H; pa.ht = ht; pa.n_slots = n; pa.scale_log2 = scale_log2;
     RowsArgs ra;
     memset(&ra, 0, sizeof ra);
     ra.pages = (const uint16_t*)st->d_pages;
@@ -1008,14 +1013,14 @@ smem_status smem_reader_decode_rows(smem_store* st, const smem_rows_layer* layer
     ra.ubuf = qabs;     // the absorbed queries are spent once the row reader has run
     ra.sw = (float*)(st->pool + L.off_sw);
     ra.out = (uint16_t*)out + i0 * tok;
-    ra.max_blocks = st->d.max_blocks; ra.b = b; ra.H = H; ra.n_slots = n;
+    ra.max_blocks = st->d.max_blocks; ra.b = b; ra.H = H; ra.ht = ht; ra.n_slots = n;
     int base = 0;
     for (int i = 0; i < n; ++i) {
       ra.seq[i] = seq_ids[i0 + i];
       ra.n_read[i] = nread[i];
       ra.pps[i] = pps_rows(nread[i]);
       ra.pbase[i] = base;
-      base += splits_rows(nread[i]);
+      base += splits_rows(nread[i]) * ht;
     }
     hipError_t e = launch_rows(D, dh, ra, pa, 0, s);
     if (e != hipSuccess) return hip_fail(e, "absorbed queries");
@@ -1028,7 +1033,7 @@ smem_status smem_reader_decode_rows(smem_store* st, const smem_rows_layer* layer
       ra.k_cache = (uint16_t*)k_cache + (size_t)i0 * b * tok;
       ra.v_cache = (uint16_t*)v_cache + (size_t)i0 * b * tok;
     }
-    ra.null_kv = layer->null_row ? null_kv : nullptr;
+    ra.null_kv = layer->null_kv ? (const uint16_t*)layer->null_kv : layer->null_row ? null_kv : nullptr;
     ra.intra_w = intra;
     ra.scale_log2 = scale_log2;
     for (int i = 0; i < n; ++i) ra.pos[i] = n_given == 4 ? pos[i0 + i] : 0;

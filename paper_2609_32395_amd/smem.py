@@ -58,7 +58,7 @@ class RowsDesc(ctypes.Structure):
 
 class RowsLayer(ctypes.Structure):
     _fields_ = [("H", ctypes.c_int32), ("dh", ctypes.c_int32), ("w_k", ctypes.c_void_p), ("w_v", ctypes.c_void_p),
-                ("null_row", ctypes.c_void_p)]
+                ("null_row", ctypes.c_void_p), ("null_kv", ctypes.c_void_p)]
 
 
 class ModelDesc(ctypes.Structure):
@@ -288,10 +288,11 @@ def smem_rows_export(st: RowStore, seq: int, rows: bool = True, stream=None):
 
 
 def smem_reader_decode_rows(st: RowStore, w_k, w_v, seq_ids, query_block, pos, q, k_new=None, v_new=None,
-                            k_cache=None, v_cache=None, null_row=None, out=None, stream=None):
+                            k_cache=None, v_cache=None, null_row=None, out=None, stream=None, null_kv=None):
     """One layer's reader decode from the row plane: w_k, w_v [H*dh, d]
     (bf16, a linear layer's out x in layout), q etc. [n, H, dh], null_row
-    [d] or None."""
+    [d] or None; null_kv [2, H, dh]: the null row already through the maps
+    (null_row is then ignored)."""
     n, H, dh = q.shape
     if len(seq_ids) != n or len(query_block) != n or (pos is not None and len(pos) != n):
         raise ValueError("seq_ids, query_block and pos need one entry per query")
@@ -299,7 +300,9 @@ def smem_reader_decode_rows(st: RowStore, w_k, w_v, seq_ids, query_block, pos, q
     wk = _dev(w_k, (H * dh, st.d), bt, "w_k")
     wv = _dev(w_v, (H * dh, st.d), bt, "w_v")
     nr = _dev(null_row, (st.d,), bt, "null_row")
-    layer = RowsLayer(H, dh, wk.value, wv.value, nr.value if nr is not None else None)
+    nkv = _dev(null_kv, (2, H, dh), bt, "null_kv")
+    layer = RowsLayer(H, dh, wk.value, wv.value, nr.value if nr is not None else None,
+                      nkv.value if nkv is not None else None)
     tok = (n, H, dh)
     cache = (n * st.b, H, dh)
     if out is None:

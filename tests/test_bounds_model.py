@@ -201,7 +201,7 @@ def _pps_rows(n):
     return max(8, -(-n // 32))
 
 
-@pytest.mark.parametrize("b,D", [(b, D) for b in (16, 64) for D in (512, 1024, 2048)])
+@pytest.mark.parametrize("b,D", [(b, D) for b in (16, 64) for D in (512, 768, 1024, 2048)])
 def test_rows_reader_indexing(b, D):
     """Row-plane reader: chunk loads stay inside a page, LDS reads inside the
     chunk and query tiles, and a launch's split partials inside the workspace."""
@@ -209,6 +209,30 @@ def test_rows_reader_indexing(b, D):
     assert N * 256 * 8 == 16 * D
     assert (255 + (N - 1) * 256) * 8 + 7 < 16 * D               # one 16-row chunk
     assert (b // 16 - 1) * 16 * D + 16 * D <= b * D              # last chunk of a page
+    # chunk DMA: per row ceil(D / 512) instructions of 64 lanes x 8 elements;
+    # a lane loads only inside its row, and the row's elements are all loaded
+    RI = -(-D // 512)
+    loaded = set()
+    for hk in range(RI):
+        for lane in range(64):
+            if hk * 512 + 512 <= D or hk * 512 + lane * 8 < D:
+                e0 = hk * 512 + lane * 8
+                assert e0 + 7 < D
+                loaded.update(range(e0, e0 + 8))
+    assert loaded == set(range(D))
+    # head tiles: absorbed queries of (slot, tile) and the tile's 16 heads stay in the
+    # kMaxSlots x 64-head region; launch index -> (unit, tile) covers every pair once
+    for H in (1, 16, 17, 24, 32, 48, 64):
+        ht = -(-H // 16)
+        assert ((127 * ht + ht - 1) * 16 + 15) < 128 * 64
+        for units in (1, 7, 8, 9, 100):
+            grid = -(-units // 8) * 8 * ht
+            seen = set()
+            for n in range(grid):
+                unit, tile = (n // (8 * ht)) * 8 + n % 8, (n // 8) % ht
+                if unit < units:
+                    seen.add((unit, tile))
+            assert seen == {(u, t) for u in range(units) for t in range(ht)}
     DW = D // 4
     for wave in range(4):
         for kk in range(DW // 32):
@@ -216,9 +240,14 @@ def test_rows_reader_indexing(b, D):
                 assert wave * DW + kk * 32 + g4 * 8 + 7 < D
         for n in range(DW // 16):
             assert wave * DW + n * 16 + 15 < D
-    # splits per read stay within the per-sequence bound the workspace is sized for
+    # splits per read stay within the per-sequence bound the workspace is sized for,
+    # and one read's partials (a split per head tile, up to 4 tiles) fit the
+    # launch cap however few sequences the store holds
     for max_blocks in (1, 7, 8, 9, 64, 255, 256, 257, 300, 4096):
         per_seq = min(32, -(-max_blocks // 8))
+        for n_seq in (1, 2, 130):
+            cap = max(1, min(1024, n_seq * per_seq * 4))
+            assert per_seq * 4 <= cap
         for n_read in range(0, max_blocks + 1):
             sp = -(-n_read // _pps_rows(n_read)) if n_read else 0
             assert sp <= per_seq

@@ -35,7 +35,11 @@ def _row_store(g, b, d, n_seq=3, max_blocks=40, live=0.8, blocks=None):
     return st, ref
 
 
-CASES = [(64, 1024, 16, 64), (64, 512, 8, 64), (64, 2048, 16, 128), (16, 512, 3, 32), (64, 1024, 4, 128)]
+# (b, d, H, dh); more than 16 heads run in tiles of 16 (the last one padded):
+# the model's reader layers at 160M (768 wide, 24 x 32), 410M (1024, 32 x 32)
+# and 1.5B (2048, 64 x 32), and a ragged 20-head case
+CASES = [(64, 1024, 16, 64), (64, 512, 8, 64), (64, 2048, 16, 128), (16, 512, 3, 32), (64, 1024, 4, 128),
+         (64, 768, 24, 32), (64, 1024, 32, 32), (64, 2048, 64, 32), (16, 1024, 20, 64)]
 
 
 @pytest.mark.parametrize("b,d,H,dh", CASES)
@@ -73,6 +77,25 @@ def test_rows_decode_parity(b, d, H, dh, with_null, with_intra):
                                              [pos[i]] if with_intra else None, dev(q[sl], BF),
                                              null_row=dev(nr, BF) if with_null else None, **a1)
         assert torch.equal(alone, out[sl])
+
+
+def test_rows_decode_premapped_null_row():
+    """The null row given already through the maps ([2, H, dh]) reads as the
+    oracle's null row does; 48 heads (three tiles)."""
+    say("rows decode, premapped null row")
+    g = np.random.default_rng(91)
+    b, d, H, dh = 64, 1024, 48, 32
+    st, ref = _row_store(g, b, d)
+    wk = rows(g, (H * dh, d), BF, 1.0 / np.sqrt(d))
+    wv = rows(g, (H * dh, d), BF, 1.0 / np.sqrt(d))
+    nr = rows(g, (d,), BF)
+    nkv = np.stack([(wk.astype(np.float64) @ nr).reshape(H, dh), (wv.astype(np.float64) @ nr).reshape(H, dh)])
+    seqs, J = [2, 0, 1], [40, 17, 0]
+    q = rows(g, (3, H, dh), BF)
+    out = smem.smem_reader_decode_rows(st, dev(wk, BF), dev(wv, BF), seqs, J, None, dev(q, BF),
+                                       null_kv=dev(nkv.astype(np.float32), BF))
+    expect, _, _ = O.reader_decode_rows(ref, wk, wv, nr, seqs, J, [0, 0, 0], q)
+    check(out, expect, BF, "rows decode premapped null row")
 
 
 def test_rows_many_sequences_span_launches():
@@ -133,7 +156,7 @@ def test_rows_kind_errors():
                                                 None) == smem.SMEM_EINVAL
     r = dev(rows(g, (64, 512), BF), BF)
     assert smem.lib().smem_rows_put_block(kv.handle, 0, 0, ctypes.c_void_p(r.data_ptr()), None) == smem.SMEM_EINVAL
-    wk = dev(rows(g, (17 * 32, 512), BF), BF)
-    with pytest.raises(smem.SmemError) as e:          # more than 16 heads
-        smem.smem_reader_decode_rows(rs, wk, wk, [0], [1], None, dev(rows(g, (1, 17, 32), BF), BF))
+    wk = dev(rows(g, (65 * 8, 512), BF), BF)
+    with pytest.raises(smem.SmemError) as e:          # more than 64 heads
+        smem.smem_reader_decode_rows(rs, wk, wk, [0], [1], None, dev(rows(g, (1, 65, 8), BF), BF))
     assert e.value.code == smem.SMEM_EINVAL
