@@ -771,9 +771,7 @@ __global__ void __launch_bounds__(64 * 4 * QW) k_prefill_mfma_par(ReaderArgs a) 
   const int pair = (n / (8 * NPART)) * 8 + (n % 8), part = (n / 8) % NPART;
   if (pair >= a.n_slots * a.H) return;   // padding of the last round (whole workgroup)
   const int slot = pair / a.H, h = pair % a.H;
-  // wave-uniform values held as such (scalar registers): the page lookups
-  // below are then scalar loads, which no vector-memory wait covers
-  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = wave / QW, qw = wave % QW;
   const int n_read = a.n_read[slot], pps = a.pps[slot];
   const int nms = (n_read + pps - 1) / pps;
@@ -809,7 +807,10 @@ __global__ void __launch_bounds__(64 * 4 * QW) k_prefill_mfma_par(ReaderArgs a) 
 #pragma unroll
     for (int i = 0; i < P::IPW; ++i) dma16(t + src[i], __builtin_amdgcn_readfirstlane(d0 + i * 1024));
   };
-  auto issue = [&](int pi, int stage) { issue_page(lpc[pi], stage); };
+  // A page number is the same for the whole wave: looked up with a
+  // wave-uniform index it is a scalar load, which no vector-memory wait covers.
+  auto page_of = [&](int pi) { return lpc[__builtin_amdgcn_readfirstlane(pi)]; };
+  auto issue = [&](int pi, int stage) { issue_page(page_of(pi), stage); };
   if (p0 < p1) issue(p0, 0);              // the first page; the rest of the ring after the loads below
 
   // ---- query fragments; the in-block tile (ring layout) and the null row into LDS
@@ -832,7 +833,7 @@ __global__ void __launch_bounds__(64 * 4 * QW) k_prefill_mfma_par(ReaderArgs a) 
   // included); the rest of the ring is issued only now, so that wait does
   // not cover it.
   wait_vm<0>();
-#pragma unroll
+#pragma unroll 1
   for (int k = 1; k < P::NSP; ++k)
     if (p0 + k < p1) issue(p0 + k, k);
 
@@ -849,7 +850,7 @@ __global__ void __launch_bounds__(64 * 4 * QW) k_prefill_mfma_par(ReaderArgs a) 
     // the page this step refills the ring with: its number is looked up
     // before the waits below, so the lookup overlaps them
     const bool refill = k > 0 && pi + P::NSP - 1 < p1;
-    const int next_page = refill ? lpc[pi + P::NSP - 1] : 0;
+    const int next_page = refill ? page_of(pi + P::NSP - 1) : 0;
     wait_pages<P::IPW>(pi < p1 ? min(k == 0 ? P::NSP - 1 : P::NSP - 2, p1 - 1 - pi) : 0);
     lds_barrier();                       // page k of every group is in LDS; every wave is done with page k - 1
     if (refill) issue_page(next_page, (k + P::NSP - 1) % P::NSP);
