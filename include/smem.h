@@ -355,7 +355,8 @@ smem_status smem_reader_decode_rows(smem_store* st, const smem_rows_layer* layer
  * weights and activations, fp32 accumulation, fp32 logits.
  * Each reader layer keeps its keys and values (the memory rows through its
  * maps) in a store of its own, so encode, serve, delete and re-encode are the
- * store operations applied to every layer.
+ * store operations applied to every layer; or (row_plane = 1) the rows are
+ * kept once and every layer reads them through its maps.
  *
  * Weights: an array of smem_model_n_weights() device pointers, in order:
  *   tok_emb [vocab, d], pos_emb [n_pos, d] (NULL when n_pos = 0),
@@ -378,6 +379,13 @@ typedef struct {
   int32_t n_seq, max_blocks, n_pages;   /* every reader layer's memory store */
   int32_t max_tokens;   /* tokens one launch sequence processes (a multiple of b, <= 128 b);
                            longer calls are cut into chunks of this size */
+  int32_t row_plane;    /* 0: every reader layer keeps its keys and values (key/value layers);
+                           1: one row store shared by all reader layers, each layer's
+                           cross-attention reading it through its own key and value maps at
+                           decode time (Appendix K, decode recomputing K/V from the rows;
+                           Appendix A, "Positions and memory").  d in {512, 768, 1024, 2048}.
+                           A row-plane model encodes, decodes and deletes; block reads
+                           (smem_model_read, smem_model_prefill) return SMEM_EINVAL. */
 } smem_model_desc;
 
 typedef struct smem_model smem_model;

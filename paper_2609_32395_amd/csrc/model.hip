@@ -64,7 +64,9 @@ using namespace smem;
 struct smem_model {
   smem_model_desc d;
   std::vector<const uint16_t*> W;
-  std::vector<smem_store*> stores;   // one per reader layer
+  std::vector<smem_store*> stores;   // one per reader layer (key/value layers)
+  smem_store* rows = nullptr;        // row plane: the memory rows, shared by every reader layer
+  smem_store* blockless = nullptr;   // row plane: an empty store for the decode's in-block self-attention
   char* pool = nullptr;
   uint16_t *x = nullptr, *h = nullptr, *q = nullptr, *k = nullptr, *v = nullptr, *o = nullptr, *f = nullptr;
   uint16_t* null_kv = nullptr;       // [D][2][d]
@@ -81,6 +83,8 @@ int n_weights(const smem_model_desc* d) { return 2 + 8 * d->E + 3 + 14 * d->D + 
 
 bool desc_ok(const smem_model_desc* d) {
   if (!d) return false;
+  if (d->row_plane != 0 && d->row_plane != 1) return false;
+  if (d->row_plane && !(d->d == 512 || d->d == 768 || d->d == 1024 || d->d == 2048)) return false;
   if (d->E < 0 || d->D < 1 || d->b != 64 || d->H < 1 || !(d->dh == 32 || d->dh == 64 || d->dh == 128)) return false;
   if (d->d != d->H * d->dh || d->d % 64 || d->d > 2048) return false;
   if (d->vocab < 1 || d->n_pos < 0 || d->n_pos % d->b) return false;
@@ -92,17 +96,37 @@ bool desc_ok(const smem_model_desc* d) {
 smem_store_desc store_desc(const smem_model_desc* d) {
   return smem_store_desc{d->n_seq, d->max_blocks, d->n_pages, d->b, d->H, d->dh, SMEM_BF16};
 }
+// Row plane: the rows, and a store that holds no block (a decode read of
+// block 0 through it is the in-block self-attention alone).
+smem_rows_desc rows_desc(const smem_model_desc* d) {
+  return smem_rows_desc{d->n_seq, d->max_blocks, d->n_pages, d->b, d->d, SMEM_BF16};
+}
+smem_store_desc blockless_desc(const smem_model_desc* d) {
+  return smem_store_desc{d->n_seq, 1, 1, d->b, d->H, d->dh, SMEM_BF16};
+}
 
 struct Layout {
   size_t store_bytes, off_ws, off_null, off_cache, total;
+  size_t rows_bytes;    // row plane: the row store, then the blockless store (store_bytes)
 };
 
 bool layout(const smem_model_desc* d, Layout* L) {
   if (!desc_ok(d)) return false;
-  const smem_store_desc sd = store_desc(d);
-  L->store_bytes = a256(smem_store_bytes(&sd));
-  if (L->store_bytes == 0) return false;
-  size_t off = L->store_bytes * d->D;
+  size_t off;
+  if (d->row_plane) {
+    const smem_rows_desc rd = rows_desc(d);
+    const smem_store_desc bd = blockless_desc(d);
+    L->rows_bytes = a256(smem_rows_bytes(&rd));
+    L->store_bytes = a256(smem_store_bytes(&bd));
+    if (L->rows_bytes == 0 || L->store_bytes == 0) return false;
+    off = L->rows_bytes + L->store_bytes;
+  } else {
+    const smem_store_desc sd = store_desc(d);
+    L->rows_bytes = 0;
+    L->store_bytes = a256(smem_store_bytes(&sd));
+    if (L->store_bytes == 0) return false;
+    off = L->store_bytes * d->D;
+  }
   L->off_ws = off;
   off += a256((size_t)d->max_tokens * d->d * 2) * 6 + a256((size_t)d->max_tokens * 4 * d->d * 2);
   L->off_null = off;
@@ -270,16 +294,24 @@ smem_status decode_chunk(smem_model* m, int first, int n, const int32_t* qblk, c
     LinArgs a = lin_ln(m, w.dec(l, R_LN1G), w.dec(l, R_LN1B), w.dec(l, R_QKV), n, 3 * D, m->q, D);
     a.y1 = m->k; a.y2 = m->v; a.ns = D;
     MCHECK(linear<kLinSplit>(a, s), "qkv");
-    MSTATUS(smem_reader_decode(m->stores[l], n, seqs.data(), zero.data(), pos, m->q, m->k, m->v, kc, vc, nullptr,
-                               m->o, s));
+    smem_store* sa = m->d.row_plane ? m->blockless : m->stores[l];
+    MSTATUS(smem_reader_decode(sa, n, seqs.data(), zero.data(), pos, m->q, m->k, m->v, kc, vc, nullptr, m->o, s));
     LinArgs o = lin(m->o, D, w.dec(l, R_O), n, D, D, m->x, D);
     o.res = m->x;
     MCHECK(linear<kLinResid>(o, s), "attention out");
     // cross-attention into the memory of strictly earlier blocks, with the null row
     MCHECK(linear<kLinStore>(lin_ln(m, w.dec(l, R_LN2G), w.dec(l, R_LN2B), w.dec(l, R_Q), n, D, m->q, D), s),
            "cross-attention query");
-    MSTATUS(smem_reader_decode(m->stores[l], n, seqs.data(), qblk, pos, m->q, nullptr, nullptr, nullptr, nullptr,
-                               m->null_kv + (size_t)l * 2 * D, m->o, s));
+    if (m->d.row_plane) {
+      // the shared rows through this layer's key and value maps (folded into
+      // the query and the output), the null row mapped once at creation
+      const smem_rows_layer layer{d.H, d.dh, w.dec(l, R_K), w.dec(l, R_V), nullptr, m->null_kv + (size_t)l * 2 * D};
+      MSTATUS(smem_reader_decode_rows(m->rows, &layer, n, seqs.data(), qblk, nullptr, m->q, nullptr, nullptr,
+                                      nullptr, nullptr, m->o, s));
+    } else {
+      MSTATUS(smem_reader_decode(m->stores[l], n, seqs.data(), qblk, pos, m->q, nullptr, nullptr, nullptr, nullptr,
+                                 m->null_kv + (size_t)l * 2 * D, m->o, s));
+    }
     LinArgs oc = lin(m->o, D, w.dec(l, R_OC), n, D, D, m->x, D);
     oc.res = m->x;
     MCHECK(linear<kLinResid>(oc, s), "cross-attention out");
@@ -324,15 +356,26 @@ smem_status smem_model_create(const smem_model_desc* desc, const void* const* we
   m->d = *desc;
   m->pool = (char*)dev_pool;
   for (int i = 0; i < nw; ++i) m->W.push_back((const uint16_t*)weights[i]);
-  const smem_store_desc sd = store_desc(desc);
-  for (int l = 0; l < desc->D; ++l) {
-    smem_store* st = nullptr;
-    smem_status r = smem_store_create(&sd, m->pool + L.store_bytes * l, L.store_bytes, s, &st);
+  if (desc->row_plane) {
+    const smem_rows_desc rd = rows_desc(desc);
+    const smem_store_desc bd = blockless_desc(desc);
+    smem_status r = smem_rows_create(&rd, m->pool, L.rows_bytes, s, &m->rows);
+    if (r == SMEM_OK) r = smem_store_create(&bd, m->pool + L.rows_bytes, L.store_bytes, s, &m->blockless);
     if (r != SMEM_OK) {
       smem_model_destroy(m);
       return r;
     }
-    m->stores.push_back(st);
+  } else {
+    const smem_store_desc sd = store_desc(desc);
+    for (int l = 0; l < desc->D; ++l) {
+      smem_store* st = nullptr;
+      smem_status r = smem_store_create(&sd, m->pool + L.store_bytes * l, L.store_bytes, s, &st);
+      if (r != SMEM_OK) {
+        smem_model_destroy(m);
+        return r;
+      }
+      m->stores.push_back(st);
+    }
   }
   const size_t T = desc->max_tokens, D = desc->d;
   char* ws = m->pool + L.off_ws;
@@ -362,6 +405,8 @@ smem_status smem_model_create(const smem_model_desc* desc, const void* const* we
 smem_status smem_model_destroy(smem_model* m) {
   if (!m) return SMEM_OK;
   for (smem_store* st : m->stores) smem_store_destroy(st);
+  smem_store_destroy(m->rows);
+  smem_store_destroy(m->blockless);
   delete m;
   return SMEM_OK;
 }
@@ -380,18 +425,20 @@ smem_status smem_model_encode_blocks(smem_model* m, int32_t n_blocks, const int3
     if (!seen.insert({seq_ids[i], block_idx[i]}).second) return mfail(SMEM_EEXIST, "a block is given twice");
   }
   // every layer's store holds the same blocks: check occupancy and space on the first
+  smem_store* mem = m->d.row_plane ? m->rows : m->stores[0];
   {
     std::set<int32_t> seqs_in;
     for (int i = 0; i < n_blocks; ++i) seqs_in.insert(seq_ids[i]);
     std::vector<int32_t> live(d.max_blocks);
     for (int32_t q : seqs_in) {
       int32_t n_live = 0;
-      MSTATUS(smem_store_export(m->stores[0], q, live.data(), &n_live, nullptr, nullptr, s));
+      MSTATUS(m->d.row_plane ? smem_rows_export(mem, q, live.data(), &n_live, nullptr, s)
+                             : smem_store_export(mem, q, live.data(), &n_live, nullptr, nullptr, s));
       for (int i = 0; i < n_live; ++i)
         if (seen.count({q, live[i]})) return mfail(SMEM_EEXIST, "a block index is occupied");
     }
     int32_t used = 0, free_pages = 0;
-    MSTATUS(smem_store_stats(m->stores[0], &used, &free_pages));
+    MSTATUS(smem_store_stats(mem, &used, &free_pages));
     if (free_pages < n_blocks) return mfail(SMEM_ENOMEM, "not enough free pages");
   }
   Wts w{m};
@@ -405,6 +452,11 @@ smem_status smem_model_encode_blocks(smem_model* m, int32_t n_blocks, const int3
       MSTATUS(ffn(m, rows, w.enc(l, E_LN2G), w.enc(l, E_LN2B), w.enc(l, E_FF1), w.enc(l, E_FF2), s));
     }
     MCHECK(lnorm(m->x, w.mem_g(), w.mem_b(), m->h, rows, D, s), "memory layernorm");
+    if (d.row_plane) {          // the rows themselves, once for every layer
+      for (int i = 0; i < nb; ++i)
+        MSTATUS(smem_rows_put_block(m->rows, seq_ids[i0 + i], block_idx[i0 + i], m->h + (size_t)i * d.b * D, s));
+      continue;
+    }
     for (int l = 0; l < d.D; ++l) {
       LinArgs a = lin(m->h, D, w.dec(l, R_K), rows, 2 * D, D, m->q, D);
       a.w2 = w.dec(l, R_V); a.n2 = D; a.y1 = m->k; a.ns = D;
@@ -429,6 +481,7 @@ smem_status smem_model_read(smem_model* m, int32_t seq, int32_t n_blocks, const 
   if (n_blocks < 0) return mfail(SMEM_EINVAL, "n_blocks < 0");
   if (n_blocks == 0) return SMEM_OK;
   if (!query_block || !tokens || !logits) return mfail(SMEM_EINVAL, "query_block, tokens and logits are required");
+  if (d.row_plane) return mfail(SMEM_EINVAL, "a row-plane model decodes; block reads need the key/value layers");
   if (seq < 0 || seq >= d.n_seq) return mfail(SMEM_EINVAL, "seq out of range");
   for (int i = 0; i < n_blocks; ++i)
     if (query_block[i] < 0 || query_block[i] > d.max_blocks) return mfail(SMEM_EINVAL, "query block out of range");
@@ -447,6 +500,7 @@ smem_status smem_model_prefill(smem_model* m, int32_t seq, int32_t first_block, 
   const auto& d = m->d;
   if (n_blocks < 1) return mfail(SMEM_EINVAL, "n_blocks < 1");
   if (!tokens || !logits) return mfail(SMEM_EINVAL, "tokens and logits are required");
+  if (d.row_plane) return mfail(SMEM_EINVAL, "a row-plane model decodes; block reads need the key/value layers");
   if (first_block < 0 || (int64_t)first_block + n_blocks > d.max_blocks)
     return mfail(SMEM_EINVAL, "blocks first_block .. first_block + n_blocks - 1 out of range");
   std::vector<int32_t> blocks(n_blocks);
@@ -485,6 +539,7 @@ smem_status smem_model_decode(smem_model* m, int32_t first_seq, int32_t n_seq, c
 
 smem_status smem_model_delete_block(smem_model* m, int32_t seq, int32_t block_idx, hipStream_t s) {
   if (!m) return mfail(SMEM_EINVAL, "model is NULL");
+  if (m->d.row_plane) return smem_delete_block(m->rows, seq, block_idx, 0, s);
   for (smem_store* st : m->stores) MSTATUS(smem_delete_block(st, seq, block_idx, 0, s));
   return SMEM_OK;
 }

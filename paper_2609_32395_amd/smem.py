@@ -63,7 +63,7 @@ class RowsLayer(ctypes.Structure):
 
 class ModelDesc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("E", "D", "d", "H", "dh", "b", "vocab", "n_pos", "n_seq", "max_blocks",
-                                               "n_pages", "max_tokens")]
+                                               "n_pages", "max_tokens", "row_plane")]
 
 
 class RopeDesc(ctypes.Structure):
@@ -358,10 +358,12 @@ class Model:
     here with torch."""
 
     def __init__(self, weights, E, D, d, H, b, vocab, n_pos, n_seq, max_blocks, n_pages, max_tokens=4096,
-                 device="cuda", stream=None):
+                 device="cuda", stream=None, row_plane=False):
         self.E, self.D, self.d, self.H, self.b, self.vocab = E, D, d, H, b, vocab
         self.dh = d // H
-        self.desc = ModelDesc(E, D, d, H, d // H, b, vocab, n_pos, n_seq, max_blocks, n_pages, max_tokens)
+        self.row_plane = bool(row_plane)
+        self.desc = ModelDesc(E, D, d, H, d // H, b, vocab, n_pos, n_seq, max_blocks, n_pages, max_tokens,
+                              int(self.row_plane))
         L = lib()
         n = L.smem_model_n_weights(ctypes.byref(self.desc))
         if n == 0:

@@ -170,5 +170,18 @@ def test_model_descriptor_and_weight_list():
         setattr(bd, field, bad)
         assert L.smem_model_n_weights(ctypes.byref(bd)) == 0, field
         assert L.smem_model_bytes(ctypes.byref(bd)) == 0, field
+    # row plane: one row store and a one-page store instead of D key/value stores
+    rd = smem.ModelDesc.from_buffer_copy(desc)
+    rd.row_plane = 1
+    rows = (L.smem_rows_bytes(ctypes.byref(smem.RowsDesc(1, 128, 128, b, d, smem.BF16))) + 255) // 256 * 256
+    one = (L.smem_store_bytes(ctypes.byref(smem.StoreDesc(1, 1, 1, b, H, d // H, smem.BF16))) + 255) // 256 * 256
+    assert rows > 0 and one > 0
+    assert L.smem_model_bytes(ctypes.byref(rd)) == rows + one + ws + cache
+    for field, bad in (("row_plane", 2), ("d", 1536)):
+        bd = smem.ModelDesc.from_buffer_copy(rd)
+        setattr(bd, field, bad)
+        if field == "d":
+            bd.H = bad // 32
+        assert L.smem_model_bytes(ctypes.byref(bd)) == 0, field
     out = ctypes.c_void_p()
     assert L.smem_model_create(ctypes.byref(desc), None, None, 0, None, ctypes.byref(out)) == smem.SMEM_EINVAL

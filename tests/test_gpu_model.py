@@ -86,12 +86,12 @@ def _gpu():
     torch.cuda.synchronize()
 
 
-def build(seed=5, n_pages=16, max_blocks=12, max_tokens=256, **over):
+def build(seed=5, n_pages=16, max_blocks=12, max_tokens=256, row_plane=False, n_seq=1, **over):
     s = dict(SHAPE, **over)
     W = synth.model_weights(smem.model_weight_shapes(s["E"], s["D"], s["d"], s["vocab"], s["n_pos"]), seed)
     dW = {k: torch.from_numpy(v).to("cuda").to(torch.bfloat16).contiguous() for k, v in W.items()}
-    m = smem.Model(dW, s["E"], s["D"], s["d"], s["H"], s["b"], s["vocab"], s["n_pos"], 1, max_blocks, n_pages,
-                   max_tokens)
+    m = smem.Model(dW, s["E"], s["D"], s["d"], s["H"], s["b"], s["vocab"], s["n_pos"], n_seq, max_blocks, n_pages,
+                   max_tokens, row_plane=row_plane)
     ref = MO.Model(W, s["E"], s["D"], s["d"], s["H"], s["b"], s["vocab"], s["n_pos"], 1, max_blocks)
     return m, ref, dW
 
@@ -343,3 +343,74 @@ def test_decode_batch_invariant_bitwise():
     for q in range(3):
         alone = smem.smem_model_decode(m, q, [J[q]], [P[q]], tok(toks[q, P[q]:P[q] + 1]))
         assert torch.equal(alone[0], batch[q]), q
+
+
+# Row plane (Appendix K, the decode arm that derives each layer's keys and
+# values from the memory rows; Appendix A, "Positions and memory"): the model
+# keeps the rows once, and every reader layer's cross-attention reads them
+# through its own key and value maps.  Rows of 512 (the narrowest the row
+# reader takes), 16 heads of 32.
+ROWS_SHAPE = dict(d=512, H=16)
+
+
+def test_row_plane_decode_matches_oracle_across_a_boundary():
+    """Decoding block J's 64 tokens on the row plane gives the oracle's
+    reader pass over the block (the key/value model's decode too, up to
+    rounding); the completed block is appended and decoding continues."""
+    say("model: row-plane decode across a boundary")
+    m, ref, _ = build(max_blocks=10, n_pages=10, row_plane=True, **ROWS_SHAPE)
+    kv, _, _ = build(max_blocks=10, n_pages=10, **ROWS_SHAPE)
+    g = np.random.default_rng(27)
+    J = 5
+    tokens = g.integers(0, SHAPE["vocab"], size=(J + 2, SHAPE["b"]))
+    for model in (m, kv):
+        smem.smem_model_encode(model, 0, list(range(J)), tok(tokens[:J]))
+    ref.encode(0, tokens[:J], list(range(J)))
+    expect = ref.read(0, tokens[J:J + 1], [J])[0]
+    rows, kv_rows = [], []
+    for p in range(SHAPE["b"]):
+        rows.append(smem.smem_model_decode(m, 0, [J], [p], tok(tokens[J, p:p + 1])))
+        kv_rows.append(smem.smem_model_decode(kv, 0, [J], [p], tok(tokens[J, p:p + 1])))
+    y, ykv = host(torch.cat(rows)), host(torch.cat(kv_rows))
+    model_check(y, expect, SHAPE["E"], SHAPE["D"], "model row-plane decode, 64 tokens of a block")
+    t = tol(SHAPE["E"], SHAPE["D"], y.size)
+    assert float(np.max(np.abs(y - ykv)) / np.sqrt(np.mean(expect ** 2))) <= t
+    smem.smem_model_encode(m, 0, [J], tok(tokens[J:J + 1]))
+    ref.encode(0, tokens[J:J + 1], [J])
+    nxt = [host(smem.smem_model_decode(m, 0, [J + 1], [p], tok(tokens[J + 1, p:p + 1])))[0] for p in range(4)]
+    e2 = ref.read(0, tokens[J + 1:J + 2], [J + 1])[0][:4]
+    model_check(np.stack(nxt), e2, SHAPE["E"], SHAPE["D"], "model row-plane decode, next block", argmax=False)
+
+
+def test_row_plane_decode_batch_invariant_and_delete_bitwise():
+    """Three sequences decoded in one call equal each decoded alone, bit for
+    bit; deleting a block equals never encoding it; block reads are refused."""
+    say("model: row-plane batch invariance, deletion")
+    m, _, _ = build(max_blocks=8, n_pages=24, row_plane=True, n_seq=3, **ROWS_SHAPE)
+    c, _, _ = build(max_blocks=8, n_pages=24, row_plane=True, n_seq=3, **ROWS_SHAPE)
+    g = np.random.default_rng(28)
+    J, P = [2, 5, 0], [3, 7, 5]
+    blocks = {q: g.integers(0, SHAPE["vocab"], size=(max(J[q], 1), SHAPE["b"])) for q in range(3)}
+    for q in range(3):
+        if J[q]:
+            smem.smem_model_encode(m, q, list(range(J[q])), tok(blocks[q][:J[q]]))
+            keep = [j for j in range(J[q]) if not (q == 1 and j == 2)]
+            smem.smem_model_encode(c, q, keep, tok(blocks[q][keep]))
+    smem.smem_model_delete_block(m, 1, 2)
+    toks = g.integers(0, SHAPE["vocab"], size=(3, max(P) + 1))
+    for p in range(max(P)):
+        for q in range(3):
+            if p < P[q]:
+                a = smem.smem_model_decode(m, q, [J[q]], [p], tok(toks[q, p:p + 1]))
+                b = smem.smem_model_decode(c, q, [J[q]], [p], tok(toks[q, p:p + 1]))
+                assert torch.equal(a, b), (q, p)
+    batch = smem.smem_model_decode(m, 0, J, P, tok(toks[np.arange(3), P]))
+    for q in range(3):
+        alone = smem.smem_model_decode(c, q, [J[q]], [P[q]], tok(toks[q, P[q]:P[q] + 1]))
+        assert torch.equal(alone[0], batch[q]), q
+    with pytest.raises(smem.SmemError) as e:
+        smem.smem_model_read(m, 0, [2], tok(blocks[0][:1]))
+    assert e.value.code == smem.SMEM_EINVAL
+    with pytest.raises(smem.SmemError) as e:
+        smem.smem_model_prefill(m, 2, 0, 1, tok(blocks[2][:1]))
+    assert e.value.code == smem.SMEM_EINVAL
