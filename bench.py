@@ -685,12 +685,15 @@ DECODE_CELLS = [("160M", 4096, 64), ("160M", 8192, 16), ("160M", 8192, 64), ("41
                 ("410M", 8192, 16), ("1.5B", 1024, 64), ("1.5B", 4096, 16)]
 
 
-def model_decode_workload(args, torch, smem, synth):
+def model_decode_workload(args, torch, smem, synth, row_plane=False):
     """Whole-model KV-cached batched decode at the paper's cells: every
     sequence holds a context of n tokens (n / b encoded blocks) and decodes
     the next tokens one step at a time, appending each block as it completes
     (one multi-sequence encode per boundary, inside the timed steps).  Token
-    ids are drawn, not sampled from the logits: the work per step is the same."""
+    ids are drawn, not sampled from the logits: the work per step is the same.
+    row_plane: the memory is kept as rows, read by every layer through its
+    own key and value maps (the decode arm that derives keys and values from
+    the rows); otherwise every layer keeps its keys and values."""
     stream = torch.cuda.current_stream()
     out = {}
     scales = {sc[0]: sc for sc in synth.MODEL_SCALES}
@@ -707,7 +710,7 @@ def model_decode_workload(args, torch, smem, synth):
         J0 = n // b
         steps, warm = args.decode_steps, args.decode_warmup
         nb = J0 + (steps + warm) // b + 2
-        m = smem.Model(W, E, D, d, H, b, vocab, T, S, nb, S * nb, max_tokens=8192)
+        m = smem.Model(W, E, D, d, H, b, vocab, T, S, nb, S * nb, max_tokens=8192, row_plane=row_plane)
         ctx = torch.from_numpy(synth.model_tokens(args.seed, name, S * n, vocab)).to("cuda")
         per = max(1, 128 // J0)                     # sequences per encode call (128 blocks)
         for s0 in range(0, S, per):
@@ -739,14 +742,17 @@ def model_decode_workload(args, torch, smem, synth):
         e1.record(stream)
         e1.synchronize()
         ms = e0.elapsed_time(e1)
-        kv = S * D * (J0 + (warm + steps / 2) / b) * b * d * 2 * 2     # memory K/V read per step (average)
-        wbytes = 2.0 * (14 * D * d * d + vocab * d)
+        # memory read per step (average): every layer's keys and values, or
+        # the rows once per layer; the row arm also reads each layer's key
+        # and value maps (the query absorption and the output projection)
+        kv = S * D * (J0 + (warm + steps / 2) / b) * b * d * 2 * (1 if row_plane else 2)
+        wbytes = 2.0 * ((16 if row_plane else 14) * D * d * d + vocab * d)
         key = f"{name} {n}/{S}"
         out[key] = dict(tokens_per_s=round(S * steps / (ms / 1e3), 1), ms_per_step=round(ms / steps, 4),
                         hbm_gbs=round((kv + wbytes) / (ms / steps / 1e3) / 1e9, 1),
                         appends_timed=sum(1 for t in range(warm, warm + steps) if t % b == b - 1))
-        print(f"[bench] decode {key}: {out[key]['tokens_per_s']:.0f} tok/s, {out[key]['ms_per_step']:.3f} ms/step",
-              file=sys.stderr, flush=True)
+        print(f"[bench] decode{' (row plane)' if row_plane else ''} {key}: {out[key]['tokens_per_s']:.0f} tok/s, "
+              f"{out[key]['ms_per_step']:.3f} ms/step", file=sys.stderr, flush=True)
         m.close()
         del ctx, gen
         torch.cuda.empty_cache()
@@ -909,11 +915,13 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--workloads", default="encode,serve,stream,rows,stress,delete_sweep,rope,model,model_decode,"
-                                           "delete_generate",
+                                           "model_decode_rows,delete_generate",
                     help="secondary workloads to run (comma list of encode, serve, stream, rows, stress, rope: "
                          "the rotary composite timed beside the headline decode and the serve; model: the whole "
                          "model's block-skip serve against its cold prefill; model_decode: the whole model's "
-                         "batched KV-cached decode at the paper's cells; delete_sweep: deletion latency from "
+                         "batched KV-cached decode at the paper's cells; model_decode_rows: the same cells with "
+                         "the memory kept as rows and every layer reading them through its maps; "
+                         "delete_sweep: deletion latency from "
                          "512 to 65,536 cached blocks; delete_generate: the whole model's delete-then-generate "
                          "cycle at 512 and 4096 cached blocks)")
     ap.add_argument("--delete-sizes", default="512,1024,4096,16384,65536")
@@ -974,6 +982,8 @@ def main():
             secondary["model_block_skip"] = model_workload(args, torch, smem, synth)
         if "model_decode" in wl:
             secondary["model_decode"] = model_decode_workload(args, torch, smem, synth)
+        if "model_decode_rows" in wl:
+            secondary["model_decode_row_plane"] = model_decode_workload(args, torch, smem, synth, row_plane=True)
         if "delete_generate" in wl:
             secondary["delete_then_generate"] = delete_generate_workload(args, torch, smem, synth)
     cpu = None
