@@ -717,10 +717,11 @@ __device__ __forceinline__ void prefill_body(const ReaderArgs& a, PrefillLds<DH,
 // together, one workgroup barrier per page.  The in-block tile (in the ring's
 // layout) and the null row are staged in LDS at the start; the final split
 // (null row, then the in-block keys) is read by a group that has no page at
-// that step.  At the end the other groups hand their states (m, l, o) to
-// group 0 through the ring's LDS, and group 0 folds them in split order, the
-// final split last, with the merge's functions: every split is computed as in
-// the split launch and the folding launch, so all three give the same bits.
+// that step.  At the end every group puts its split's state (m, l, o) into
+// the ring's LDS, and the waves fold them in split order, the final split
+// last, with the merge's functions, each wave one 16-wide dimension tile of
+// its rows: every split is computed as in the split launch and the folding
+// launch, so all three give the same bits.
 template <int DH, int QW>
 struct ParLds {
   using R = PageRing<DH>;
@@ -734,9 +735,9 @@ struct ParLds {
   static constexpr int OFF_NULL = OFF_IN + R::TILE;    // null key, then null value (bf16)
   static constexpr int BYTES = OFF_NULL + 4 * DH;
   // a split state per (slot, wave): o as DH/16 float4 planes of 64 lanes, then (m, l) pairs;
-  // slots 0..2 hold memory splits 1..3, slot 3 the final split
+  // slots 0..3 hold memory splits 0..3, slot 4 the final split
   static constexpr int STATE = (DH / 16) * 1024 + 64 * 8;
-  static_assert(G * QW * STATE <= RING, "split states fit in the ring");
+  static_assert((G + 1) * QW * STATE <= RING, "split states fit in the ring");
   static_assert(BYTES <= 160 * 1024, "LDS");
   static_assert(NSP >= 2 && NSP <= 4 && 3 * IPW < 64, "wait_pages covers up to 3 pages ahead");
 };
@@ -871,37 +872,42 @@ __global__ void __launch_bounds__(64 * 4 * QW) k_prefill_mfma_par(ReaderArgs a) 
     }
   }
   lds_barrier();                         // the ring is free
-  if (g > 0 && g < nms) state_put<DH>(L + ((g - 1) * QW + qw) * P::STATE, o, m, l, lane);
-  if (g == fg) state_put<DH>(L + (3 * QW + qw) * P::STATE, of, mf, lf, lane);
+  // every split's state into LDS: slot j*QW + qw for memory split j, slot
+  // G*QW + qw for the final split
+  if (g < nms) state_put<DH>(L + (g * QW + qw) * P::STATE, o, m, l, lane);
+  if (g == fg) state_put<DH>(L + (P::G * QW + qw) * P::STATE, of, mf, lf, lane);
   lds_barrier();
-  if (g == 0) {
-    uint16_t* orow = (uint16_t*)a.out + ((size_t)slot * BT + qrow) * rs + (size_t)h * DH;
-    // the state slots are read NPRE at a time ahead of their fold (slots of
-    // absent splits hold stale data and are not folded); at 16 waves the
-    // register budget allows one
-    constexpr int NPRE = QW == 2 ? 4 : 1;
-    floatx4 so[4][DH / 16];
-    float sm[4], sl[4];
+  // Wave (g, qw) folds dimension tile g of its 16 rows over the splits in
+  // split order (per element the merge's arithmetic, so the split launch's
+  // bits) and stores that tile: the fold runs on DH/16 waves at once.
+  constexpr int NT = DH / 16;
+  if (g < NT) {
+    auto get = [&](int sl, floatx4& ot, float& ms, float& ls) {
+      const uint8_t* st = L + (sl * QW + qw) * P::STATE;
+      ot = *(const floatx4*)(st + (g * 64 + lane) * 16);
+      const f32x2 ml = *(const f32x2*)(st + NT * 1024 + lane * 8);
+      ms = ml.x;
+      ls = qsum(ml.y);
+    };
+    floatx4 acc;
+    float fm, fl;
+    get(nms > 0 ? 0 : P::G, acc, fm, fl);
+    for (int j = 1; j <= nms; ++j) {     // memory splits 1 .. nms-1, then the final split
+      floatx4 ot;
+      float ms, ls;
+      get(j < nms ? j : P::G, ot, ms, ls);
+      const FoldScale c = fold_scale(fm, ms);
+      fl = fold_value(fl, c, ls);
 #pragma unroll
-    for (int j = 0; j < NPRE; ++j) state_get<DH>(L + (j * QW + qw) * P::STATE, so[j], sm[j], sl[j], lane);
-    if (nms > 0) {
-      floatx4 acc[DH / 16];
-      float fm, fl;
-      fold_split<DH>(true, m, l, o, fm, fl, acc);
-#pragma unroll
-      for (int j = 1; j < P::G; ++j) {
-        if (j < nms) {
-          if (j - 1 >= NPRE) state_get<DH>(L + ((j - 1) * QW + qw) * P::STATE, so[j - 1], sm[j - 1], sl[j - 1], lane);
-          fold_split<DH>(false, sm[j - 1], sl[j - 1], so[j - 1], fm, fl, acc);
-        }
-      }
-      if (3 >= NPRE) state_get<DH>(L + (3 * QW + qw) * P::STATE, so[3], sm[3], sl[3], lane);
-      fold_split<DH>(false, sm[3], sl[3], so[3], fm, fl, acc);
-      store_out<DH>(orow, acc, fl, lane);
-    } else {
-      if (3 >= NPRE) state_get<DH>(L + (3 * QW + qw) * P::STATE, so[3], sm[3], sl[3], lane);
-      store_out<DH>(orow, so[3], qsum(sl[3]), lane);
+      for (int i = 0; i < 4; ++i) acc[i] = fold_value(acc[i], c, ot[i]);
     }
+    const float inv = (fl > 0.f) ? 1.f / fl : 0.f;
+    uint16_t* orow = (uint16_t*)a.out + ((size_t)slot * BT + qrow) * rs + (size_t)h * DH;
+    const int d0 = g * 16 + (lane >> 4) * 4;
+    uint16_t r4[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r4[i] = f32_to_bf16_bits(acc[i] * inv);
+    *(u32x2*)(orow + d0) = u32x2{(uint32_t)r4[0] | ((uint32_t)r4[1] << 16), (uint32_t)r4[2] | ((uint32_t)r4[3] << 16)};
   }
 }
 

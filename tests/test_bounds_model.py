@@ -609,7 +609,7 @@ def test_prefill_par_lds_and_thread_ranges(dh, qw):
     OFF_NULL = OFF_IN + TILE
     BYTES = OFF_NULL + 4 * dh
     STATE = (dh // 16) * 1024 + 64 * 8
-    assert BYTES <= 160 * 1024 and G * qw * STATE <= RING and 3 * IPW < 64
+    assert BYTES <= 160 * 1024 and (G + 1) * qw * STATE <= RING and 3 * IPW < 64
     kswz = lambda r: (r // (256 // KRB)) % KCH
     vswz = lambda d: ((d >> 1) ^ (d >> 4)) & 7
     seen = set()
@@ -645,7 +645,10 @@ def test_prefill_par_lds_and_thread_ranges(dh, qw):
         off = KBYTES + d * 128 + ((((gg >> 1) + 2 * q) ^ vswz(d)) << 4) + (gg & 1) * 8
         assert vals[off] == (d, 4 * gg + 16 * q) and vals[off + 4] == (d, 4 * gg + 16 * q + 2)
     assert 2 * CPR <= THREADS and OFF_NULL + 2 * CPR * 16 <= BYTES                    # null row
-    for j, w in itertools.product(range(4), range(qw)):                               # split states
+    # split states: slots 0..3 the memory splits, slot 4 the final split; the
+    # folding wave (g, w) reads dimension tile g < dh/16 of each
+    assert dh // 16 <= G
+    for j, w in itertools.product(range(G + 1), range(qw)):
         base = (j * qw + w) * STATE
         assert base + (dh // 16 - 1) * 1024 + 63 * 16 + 16 <= RING
         assert base + (dh // 16) * 1024 + 63 * 8 + 8 <= (j * qw + w + 1) * STATE
