@@ -64,13 +64,30 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 MFMA_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published (2.5 PFLOP/s, no sparsity)
 
-# HBM bytes per decode call measured with rocprofv3 FETCH_SIZE/WRITE_SIZE
-# (scaled by a plain copy of known size), keyed by a hash of the decode
-# kernel's sources: a changed kernel reports traffic as null until measured
-# again.  Figures: profiles/hbm_traffic_attention_kernels.md (reader + merge,
-# read + written per step).
-DECODE_TRAFFIC_BYTES = {"8dad1c9ebea57911": 1.0890e+09}
-DECODE_SOURCES = ("paper_2609_32395_amd/csrc/reader_valu.hip", "paper_2609_32395_amd/csrc/common.h")
+# Memory-side bytes per call (read + written) measured with rocprofv3
+# FETCH_SIZE / WRITE_SIZE, scaled by copies of known size (bench.py
+# --copy-probe), keyed by a hash of the sources of the kernels the call runs:
+# a changed kernel reports traffic as null until measured again.  Figures
+# and commands: profiles/hbm_traffic_attention_kernels.md.
+CSRC = "paper_2609_32395_amd/csrc/"
+TRAFFIC = {
+    # 410M decode step: k_reader_valu + k_merge
+    "decode": ((CSRC + "reader_valu.hip", CSRC + "common.h"), {"3b1f089ddfea81b8": 1.0890e+09}),
+    # 160M encoder: k_encoder_mfma (attention only)
+    "encoder": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"e1308621f6f43b5b": 5.0442e+07}),
+    # 160M final-block prefill: k_prefill_mfma_par
+    "prefill": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"e1308621f6f43b5b": 2.6964e+07}),
+    # 1.5B serve: k_prefill_mfma + k_merge
+    "serve": ((CSRC + "attn_mfma.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"606fa157139442ac": 3.0607e+08}),
+    # 410M row-plane decode step: k_rows_absorb_q, k_reader_rows, k_rows_combine (with the
+    # in-block keys), k_rows_project
+    "rows": ((CSRC + "rows.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"639cb4ab09aeecf6": 6.4295e+08}),
+}
+
+
+def traffic_of(name):
+    srcs, table = TRAFFIC[name]
+    return table.get(_sources_hash(srcs))
 
 
 def _sources_hash(paths):
@@ -276,7 +293,8 @@ def encode_prefill_workload(args, torch, smem, synth):
                 encoder_flops=enc_flops, encoder_bytes=enc_bytes,
                 encoder_ms_single_flushed=enc_flushed_s * 1e3, encoder_gbs_single_flushed=enc_bytes / enc_flushed_s / 1e9,
                 prefill_ms=pre_s * 1e3, prefill_tflops=pre_flops / pre_s / 1e12, prefill_gbs=pre_bytes / pre_s / 1e9,
-                prefill_ms_single_flushed=pre_flushed_s * 1e3, prefill_gbs_single_flushed=pre_bytes / pre_flushed_s / 1e9)
+                prefill_ms_single_flushed=pre_flushed_s * 1e3, prefill_gbs_single_flushed=pre_bytes / pre_flushed_s / 1e9,
+                encoder_traffic=traffic_of("encoder"), prefill_traffic=traffic_of("prefill"))
 
 
 def serve_workload(args, torch, smem, synth):
@@ -342,7 +360,7 @@ def serve_workload(args, torch, smem, synth):
                 serve_ms_single_flushed=serve_flushed_s * 1e3, serve_gbs_single_flushed=bytes_ / serve_flushed_s / 1e9,
                 rope_serve_ms=rope_ms,
                 delete_us_median=float(np.median(del_t)) * 1e3, reserve_ms_median=float(np.median(re_t)),
-                rows_after_deletes=(NB - 100) * b)
+                rows_after_deletes=(NB - 100) * b, serve_bytes=bytes_, serve_traffic=traffic_of("serve"))
 
 
 def stream_workload(args, torch, smem, synth):
@@ -439,7 +457,8 @@ def rows_workload(args, torch, smem, synth):
     row_bytes = S * NB * b * d * 2
     st.close()
     return dict(tokens_per_s=S * args.steps / secs, ms_per_step=secs / args.steps * 1e3, d=d,
-                row_bytes_per_step=row_bytes, row_gbs=row_bytes / (secs / args.steps) / 1e9)
+                row_bytes_per_step=row_bytes, row_gbs=row_bytes / (secs / args.steps) / 1e9,
+                traffic=traffic_of("rows"))
 
 
 def stress_workload(args, torch, smem, synth):
@@ -1012,7 +1031,7 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": DECODE_TRAFFIC_BYTES.get(_sources_hash(DECODE_SOURCES)),
+                     "traffic": traffic_of("decode"),
                      "kernel": "smem_reader_decode (k_reader_valu + k_merge)",
                      "bytes_per_launch": dec["bytes_per_step"]},
         "hbm_gbs": round(achieved, 1),
