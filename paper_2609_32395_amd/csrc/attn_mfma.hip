@@ -749,15 +749,6 @@ __device__ __forceinline__ void state_put(uint8_t* st, const floatx4 (&o)[DH / 1
   *(f32x2*)(st + (DH / 16) * 1024 + lane * 8) = f32x2{m, l};
 }
 
-template <int DH>
-__device__ __forceinline__ void state_get(const uint8_t* st, floatx4 (&o)[DH / 16], float& m, float& l, int lane) {
-#pragma unroll
-  for (int dt = 0; dt < DH / 16; ++dt) o[dt] = *(const floatx4*)(st + (dt * 64 + lane) * 16);
-  const f32x2 ml = *(const f32x2*)(st + (DH / 16) * 1024 + lane * 8);
-  m = ml.x;
-  l = ml.y;
-}
-
 // Workgroups of a few-pair launch: 4/QW parts per pair, 8 pairs per round of
 // 8 x (4/QW) launch indices.
 inline int par_grid(int n_pairs, int qw) { return ((n_pairs + 7) / 8) * 8 * (4 / qw); }
