@@ -38,13 +38,15 @@ struct RowsCfg {
   static constexpr int NT = DW / 16;               // U tiles per wave
 };
 
-template <int D>
+// TG head tiles per workgroup: wave group g (4 waves) takes tile g of the
+// workgroup's TG; the row chunks in LDS serve every group.
+template <int D, int TG>
 struct RowsLds {
   uint16_t mu[RowsCfg<D>::NS][kRowChunk * RowsCfg<D>::MP];
-  float sred[4][256];                       // per-wave partial scores
-  uint16_t p[16 * 16];                      // P[head][row], bf16
-  float alpha[16];
-  int rescale;                              // some head's reference maximum moved this chunk
+  float sred[TG][4][256];                   // per-wave partial scores
+  uint16_t p[TG][16 * 16];                  // P[head][row], bf16
+  float alpha[TG][16];
+  int rescale[TG];                          // some head's reference maximum moved this chunk
 };
 
 // Lazy rescaling: a head's reference maximum moves only when a score exceeds
@@ -56,8 +58,8 @@ constexpr float kLazy = 8.f;
 // Wave `wave` moves rows 4*wave .. 4*wave+3 of chunk c into stage st: each
 // row is D*2 bytes, DMA instructions of 1 KiB (512 elements) and, at
 // d = 768, one of 512 bytes (the lanes past the row's end stay idle).
-template <int D>
-__device__ __forceinline__ void chunk_dma(RowsLds<D>& L, int st, const uint16_t* __restrict__ src, int wave,
+template <int D, int TG>
+__device__ __forceinline__ void chunk_dma(RowsLds<D, TG>& L, int st, const uint16_t* __restrict__ src, int wave,
                                           int lane) {
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
@@ -148,25 +150,29 @@ __device__ __forceinline__ void rows_intra(const RowsArgs& a, int slot, int h, i
   }
 }
 
-// One workgroup per (sequence slot, split, head tile).  The head tiles of one
-// (slot, split) read the same rows: their launch indices are 8 apart, so
-// they run on one XCD (workgroups are dealt to the 8 XCDs in turn) and share
-// its L2.  Wave w reduces dims [w*D/4, (w+1)*D/4) of the scores and owns the
-// same dims of U.
-inline int rows_grid(int units, int ht) { return ((units + 7) / 8) * 8 * ht; }
+// One workgroup per (sequence slot, split, group of TG head tiles), 4 waves
+// per tile: the chunks of rows are moved into LDS once for the TG tiles.
+// The tile groups of one (slot, split) read the same rows: their launch
+// indices are 8 apart, so they run on one XCD (workgroups are dealt to the 8
+// XCDs in turn) and share its L2.  Wave w of a group reduces dims
+// [w*D/4, (w+1)*D/4) of its tile's scores and owns the same dims of U.
+inline int rows_grid(int units, int groups) { return ((units + 7) / 8) * 8 * groups; }
 
-template <int D, int DHq>
-__global__ void __launch_bounds__(256) k_reader_rows(RowsArgs a) {
+template <int D, int DHq, int TG>
+__global__ void __launch_bounds__(256 * TG) k_reader_rows(RowsArgs a) {
   using C = RowsCfg<D>;
-  __shared__ RowsLds<D> L;
+  __shared__ RowsLds<D, TG> L;
+  const int n_groups = a.ht / TG;
   const int n = blockIdx.x;
-  const int unit = (n / (8 * a.ht)) * 8 + n % 8, tile = (n / 8) % a.ht;
+  const int unit = (n / (8 * n_groups)) * 8 + n % 8, tgi = (n / 8) % n_groups;
   const int slot = unit / a.max_split, split = unit % a.max_split;
   if (slot >= a.n_slots) return;            // padding of the last round (whole workgroup)
   const int n_read = a.n_read[slot], pps = a.pps[slot];
   const int nsp = (n_read + pps - 1) / pps;
   if (split >= nsp) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid_all = threadIdx.x, lane = tid_all & 63, wave_all = tid_all >> 6;
+  const int grp = wave_all / 4, wave = wave_all % 4, tid = tid_all % 256;
+  const int tile = tgi * TG + grp;
   constexpr int MP = C::MP, DW = C::DW, NT = C::NT, NS = C::NS;
   const int b = a.b;
 
@@ -198,15 +204,16 @@ __global__ void __launch_bounds__(256) k_reader_rows(RowsArgs a) {
     return a.pages + ((size_t)pg * b + (size_t)(c % cpp) * kRowChunk) * D;
   };
   wait_vm<0>();                             // the query fragments
+  // the first group's waves move the chunks
 #pragma unroll
   for (int c = 0; c < NS - 1; ++c)
-    if (c < n_chunks) chunk_dma<D>(L, c, chunk_src(c), wave, lane);
+    if (grp == 0 && c < n_chunks) chunk_dma<D, TG>(L, c, chunk_src(c), wave, lane);
 
   for (int c = 0; c < n_chunks; ++c) {
     const int st = c % NS;
     lds_barrier();                        // every wave is done with chunk c-1 (its stage, sred, p)
     const int nxt = c + NS - 1;
-    if (nxt < n_chunks) chunk_dma<D>(L, nxt % NS, chunk_src(nxt), wave, lane);
+    if (grp == 0 && nxt < n_chunks) chunk_dma<D, TG>(L, nxt % NS, chunk_src(nxt), wave, lane);
     wait_chunk<D>(min(NS - 1, n_chunks - 1 - c));
     lds_barrier();                        // chunk c is in LDS for every wave
     // S partial over this wave's dims: D[m = head][n = row]
@@ -222,12 +229,12 @@ __global__ void __launch_bounds__(256) k_reader_rows(RowsArgs a) {
       s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8r, qa[kk + 1]),
                                                    __builtin_bit_cast(bf16x8r, m1), s1, 0, 0, 0);
     }
-    *(f32x4*)&L.sred[wave][lane * 4] = s0 + s1;
-    if (tid == 0) L.rescale = 0;
+    *(f32x4*)&L.sred[grp][wave][lane * 4] = s0 + s1;
+    if (tid == 0) L.rescale[grp] = 0;
     lds_barrier();
     // online softmax per head over the chunk's 16 rows, lazily rescaled
     {
-      const float x = L.sred[0][tid] + L.sred[1][tid] + L.sred[2][tid] + L.sred[3][tid];
+      const float x = L.sred[grp][0][tid] + L.sred[grp][1][tid] + L.sred[grp][2][tid] + L.sred[grp][3][tid];
       float mx = x;
       mx = fmaxf(mx, __shfl_xor(mx, 4));
       mx = fmaxf(mx, __shfl_xor(mx, 8));
@@ -237,7 +244,7 @@ __global__ void __launch_bounds__(256) k_reader_rows(RowsArgs a) {
       if (mx > m_h + kLazy) {               // the same for the 16 threads of a head
         al = exp2w(m_h - mx);
         m_h = mx;
-        if (s_row == 0) L.rescale = 1;
+        if (s_row == 0) L.rescale[grp] = 1;
       }
       const float p = exp2w(x - m_h);
       float ps = p;
@@ -246,23 +253,23 @@ __global__ void __launch_bounds__(256) k_reader_rows(RowsArgs a) {
       ps += __shfl_xor(ps, 16);
       ps += __shfl_xor(ps, 32);
       l_h = l_h * al + ps;
-      L.p[s_head * 16 + s_row] = f32_to_bf16_bits(p);
-      if (s_row == 0) L.alpha[s_head] = al;
+      L.p[grp][s_head * 16 + s_row] = f32_to_bf16_bits(p);
+      if (s_row == 0) L.alpha[grp][s_head] = al;
     }
     lds_barrier();
     // U = U * alpha + P mu over this wave's dims
     {
-      if (L.rescale) {
+      if (L.rescale[grp]) {
         float al4[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) al4[i] = L.alpha[4 * (lane >> 4) + i];
+        for (int i = 0; i < 4; ++i) al4[i] = L.alpha[grp][4 * (lane >> 4) + i];
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) u[n][i] *= al4[i];
         }
       }
-      const u32x2 pa = *(const u32x2*)&L.p[(lane & 15) * 16 + (lane >> 4) * 4];
+      const u32x2 pa = *(const u32x2*)&L.p[grp][(lane & 15) * 16 + (lane >> 4) * 4];
       const s16x4 A = __builtin_bit_cast(s16x4, pa);
       const int rbase = (lane >> 4) * 4;
 #pragma unroll
@@ -462,7 +469,16 @@ static hipError_t launch_rows_dd(const RowsArgs& a, const RowsPrepArgs& pa, int 
   if (max_split > 0) {
     RowsArgs r = a;
     r.max_split = max_split;
-    hipLaunchKernelGGL((k_reader_rows<D, DHq>), dim3(rows_grid(a.n_slots * max_split, a.ht)), dim3(256), 0, s, r);
+    // Two head tiles per workgroup (one chunk stream for both) at d = 2048,
+    // when the tiles pair up: there one tile's workgroup fills a CU's LDS and
+    // runs one wave per SIMD, so the second tile's waves come for free.  At
+    // the narrower widths several workgroups already share a CU and the
+    // measured decode cells were as fast or faster with one tile each.
+    if (D >= 2048 && a.ht % 2 == 0)
+      hipLaunchKernelGGL((k_reader_rows<D, DHq, 2>), dim3(rows_grid(a.n_slots * max_split, a.ht / 2)), dim3(512), 0, s,
+                         r);
+    else
+      hipLaunchKernelGGL((k_reader_rows<D, DHq, 1>), dim3(rows_grid(a.n_slots * max_split, a.ht)), dim3(256), 0, s, r);
   }
   hipLaunchKernelGGL((k_rows_combine<D, DHq>), dim3(a.n_slots, a.H), dim3(256), 0, s, a);
   hipLaunchKernelGGL((k_rows_project<D, DHq>), dim3(a.H, (a.n_slots + 15) / 16, DHq / 16), dim3(256), 0, s, a);

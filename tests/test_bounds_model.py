@@ -221,18 +221,21 @@ def test_rows_reader_indexing(b, D):
                 loaded.update(range(e0, e0 + 8))
     assert loaded == set(range(D))
     # head tiles: absorbed queries of (slot, tile) and the tile's 16 heads stay in the
-    # kMaxSlots x 64-head region; launch index -> (unit, tile) covers every pair once
+    # kMaxSlots x 64-head region; launch index -> (unit, tile group) and the group's
+    # TG tiles (TG = 2 when the tiles pair up) cover every (unit, tile) once
     for H in (1, 16, 17, 24, 32, 48, 64):
         ht = -(-H // 16)
         assert ((127 * ht + ht - 1) * 16 + 15) < 128 * 64
+        tg = 2 if ht % 2 == 0 else 1
+        groups = ht // tg
         for units in (1, 7, 8, 9, 100):
-            grid = -(-units // 8) * 8 * ht
-            seen = set()
+            grid = -(-units // 8) * 8 * groups
+            seen = []
             for n in range(grid):
-                unit, tile = (n // (8 * ht)) * 8 + n % 8, (n // 8) % ht
+                unit, tgi = (n // (8 * groups)) * 8 + n % 8, (n // 8) % groups
                 if unit < units:
-                    seen.add((unit, tile))
-            assert seen == {(u, t) for u in range(units) for t in range(ht)}
+                    seen += [(unit, tgi * tg + grp) for grp in range(tg)]
+            assert sorted(seen) == [(u, t) for u in range(units) for t in range(ht)]
     DW = D // 4
     for wave in range(4):
         for kk in range(DW // 32):
