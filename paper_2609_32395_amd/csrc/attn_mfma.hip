@@ -374,9 +374,14 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
   // The block's output rows go through LDS (the key plane's space and
   // layout) so that global stores are whole 16-byte chunks of consecutive
   // rows: a lane's fragment is 4 dims of one query row, 8 bytes scattered
-  // over 64 rows.  A page insert writes the key plane from the same rows and
-  // the transposed value plane by gathering each chunk's 8 rows (the lanes
-  // of one instruction read one row).
+  // over 64 rows.  An 8-byte write serves 16 consecutive lanes (16 rows, one
+  // dim group) per pass over 128 bytes of banks, and the key swizzle maps two
+  // of those rows to the same 16-byte slot modulo 128 bytes; a slot in the
+  // upper 128 bytes of its 256-byte bank row therefore stores its two 8-byte
+  // halves swapped (swapped back when read), which gives the 16 lanes 16
+  // distinct 8-byte places.  A page insert writes the key plane from the
+  // same rows and the transposed value plane by gathering each chunk's 8 rows
+  // (the lanes of one instruction read one row).
   __syncthreads();                           // every wave is done with the key and value tiles
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) {
@@ -384,28 +389,30 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
     uint16_t rr[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) rr[i] = f32_to_bf16_bits(o[dt][i] * inv);
-    *(u32x2*)(T + qrow * R::KRB + (((d0 >> 3) ^ R::kswz(qrow)) << 4) + (d0 & 7) * 2) =
+    const int slot = qrow * R::KRB + (((d0 >> 3) ^ R::kswz(qrow)) << 4);
+    const int half = ((d0 >> 2) & 1) ^ ((slot >> 7) & 1);   // halves swapped in the upper 128 bytes
+    *(u32x2*)(T + slot + half * 8) =
         u32x2{(uint32_t)rr[0] | ((uint32_t)rr[1] << 16), (uint32_t)rr[2] | ((uint32_t)rr[3] << 16)};
   }
   __syncthreads();
   for (int c = tid; c < BT * DH / 8; c += 256) {
     const int row = c / (DH / 8), c8 = c % (DH / 8);
-    const u32x4 v16 = *(const u32x4*)(T + row * R::KRB + ((c8 ^ R::kswz(row)) << 4));
+    const int slot = row * R::KRB + ((c8 ^ R::kswz(row)) << 4);
+    u32x4 v16 = *(const u32x4*)(T + slot);
+    if ((slot >> 7) & 1) v16 = u32x4{v16.z, v16.w, v16.x, v16.y};
     if (a.out) *(u32x4*)(a.out + ((size_t)blk * BT + row) * rs + (size_t)h * DH + c8 * 8) = v16;
     if (kp) *(u32x4*)(kp + row * DH + c8 * 8) = v16;
   }
   if (kp) {
     for (int c = tid; c < DH * BT / 8; c += 256) {
       const int d = c % DH, r8 = c / DH;
-      const uint8_t* col = T + (d & 7) * 2;
+      auto at = [&](int r) {
+        const int slot = r * R::KRB + (((d >> 3) ^ R::kswz(r)) << 4);
+        return (uint32_t) * (const uint16_t*)(T + slot + (((d & 7) * 2) ^ (((slot >> 7) & 1) * 8)));
+      };
       uint32_t w[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r0 = r8 * 8 + 2 * j, r1 = r0 + 1;
-        const uint32_t x0 = *(const uint16_t*)(col + r0 * R::KRB + (((d >> 3) ^ R::kswz(r0)) << 4));
-        const uint32_t x1 = *(const uint16_t*)(col + r1 * R::KRB + (((d >> 3) ^ R::kswz(r1)) << 4));
-        w[j] = x0 | (x1 << 16);
-      }
+      for (int j = 0; j < 4; ++j) w[j] = at(r8 * 8 + 2 * j) | (at(r8 * 8 + 2 * j + 1) << 16);
       *(u32x4*)(kp + BT * DH + d * BT + r8 * 8) = u32x4{w[0], w[1], w[2], w[3]};
     }
   }

@@ -754,3 +754,47 @@ def test_metadata_chunk_rebuild_equals_full_rebuild(mb, n_seq):
             if absent not in live[q]:
                 apply([(q, absent, free.pop())])
     apply([(q, b, -1) for q in range(n_seq) for b in list(live[q])[::3]])   # a batch of deletes
+
+
+@pytest.mark.parametrize("dh", [32, 64, 128])
+def test_encoder_output_staging(dh):
+    """The encoder's output rows pass through LDS in the key-plane layout, a
+    slot in the upper 128 bytes of its 256-byte bank row holding its 8-byte
+    halves swapped: every (row, dim) lands in one place, the 16-byte reads
+    (halves swapped back) and the transposed gather of a page insert find each
+    dim where it was written, and each 16-lane group of an 8-byte write (the
+    lanes one pass serves, over 128 bytes of banks) touches each bank once.
+    Without the swap the same check fails: two rows of a group share a slot
+    modulo 128 bytes."""
+    BT, KRB, KCH = 64, dh * 2, dh // 8
+    kswz = lambda r: (r // (256 // KRB)) % KCH
+
+    def layout(swap):
+        where, clean = {}, True
+        for wave, dt in itertools.product(range(4), range(dh // 16)):
+            for g in range(4):
+                banks = []
+                for lane in range(16 * g, 16 * g + 16):
+                    qrow, d0 = wave * 16 + (lane & 15), dt * 16 + (lane >> 4) * 4
+                    slot = qrow * KRB + (((d0 >> 3) ^ kswz(qrow)) << 4)
+                    off = slot + (((d0 >> 2) & 1) ^ (((slot >> 7) & 1) if swap else 0)) * 8
+                    assert 0 <= off and off + 8 <= BT * KRB
+                    for i in range(4):
+                        assert off + 2 * i not in where
+                        where[off + 2 * i] = (qrow, d0 + i)
+                    banks += [(off // 4) % 32, (off // 4 + 1) % 32]
+                clean &= len(banks) == len(set(banks))
+        return where, clean
+
+    assert not layout(False)[1]
+    where, clean = layout(True)
+    assert clean and len(where) == BT * dh
+    for row, c8 in itertools.product(range(BT), range(dh // 8)):       # 16-byte reads, halves swapped back
+        slot = row * KRB + ((c8 ^ kswz(row)) << 4)
+        elems = [where[slot + 2 * e] for e in range(8)]
+        if (slot >> 7) & 1:
+            elems = elems[4:] + elems[:4]
+        assert elems == [(row, c8 * 8 + e) for e in range(8)]
+    for d, r in itertools.product(range(dh), range(BT)):               # the page insert's transposed gather
+        slot = r * KRB + (((d >> 3) ^ kswz(r)) << 4)
+        assert where[slot + (((d & 7) * 2) ^ (((slot >> 7) & 1) * 8))] == (r, d)
