@@ -74,14 +74,14 @@ TRAFFIC = {
     # 410M decode step: k_reader_valu + k_merge
     "decode": ((CSRC + "reader_valu.hip", CSRC + "common.h"), {"3b1f089ddfea81b8": 1.0890e+09}),
     # 160M encoder: k_encoder_mfma (attention only)
-    "encoder": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"e1308621f6f43b5b": 5.0442e+07}),
+    "encoder": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"c8ed6113250b822e": 5.0445e+07}),
     # 160M final-block prefill: k_prefill_mfma_par
-    "prefill": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"e1308621f6f43b5b": 2.6964e+07}),
+    "prefill": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"c8ed6113250b822e": 2.6971e+07}),
     # 1.5B serve: k_prefill_mfma + k_merge
-    "serve": ((CSRC + "attn_mfma.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"606fa157139442ac": 3.0607e+08}),
+    "serve": ((CSRC + "attn_mfma.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"5c7540b5a80824c9": 3.0618e+08}),
     # 410M row-plane decode step: k_rows_absorb_q, k_reader_rows, k_rows_combine (with the
     # in-block keys), k_rows_project
-    "rows": ((CSRC + "rows.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"639cb4ab09aeecf6": 6.4295e+08}),
+    "rows": ((CSRC + "rows.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"6b1ade5070885bd6": 6.4296e+08}),
 }
 
 
