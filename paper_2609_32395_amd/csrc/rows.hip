@@ -91,8 +91,8 @@ __device__ __forceinline__ void wait_chunk(int ahead) {
 // take the value dimensions (weights read back from LDS).  Writes the
 // compact partial (acc[dh], max, sum) of each head.
 template <int DHq>
-__device__ __forceinline__ void rows_intra(const RowsArgs& a, int slot, int h, int lane, float* pw, float& M_out,
-                                           float& L_out) {
+__device__ __forceinline__ void rows_intra(const RowsArgs& a, int slot, int h, int lane, float* pw, float* red,
+                                           float& M_out, float& L_out) {
   const int H = a.H, pos = a.pos[slot];
   const int n_in = a.k_new ? pos + 1 : 0;
   const size_t tok = (size_t)H * DHq;
@@ -130,14 +130,39 @@ __device__ __forceinline__ void rows_intra(const RowsArgs& a, int slot, int h, i
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   float* part = a.intra_w + ((size_t)slot * H + h) * (DHq + 4);
   const uint16_t* vc = a.v_cache + (size_t)slot * a.b * tok + (size_t)h * DHq;
+  // cached values (rows below pos): lane (g, c) sums rows g, g + RG, ... of
+  // its 8-dim chunk c with 16-byte loads, all issued at once; the RG group
+  // sums then meet in LDS and are added in group order
+  constexpr int C = DHq / 8, RG = 64 / C;
+  const int rg = lane / C, c8 = lane % C;
+  const int nr = min(pos, n_in);
+  float a8[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) a8[e] = 0.f;
+#pragma unroll
+  for (int i = 0; i < 64 / RG; ++i) {
+    const int r = rg + RG * i;
+    if (r < nr) {
+      float vf[8];
+      Chunk<uint16_t>::unpack(*(const u32x4*)(vc + (size_t)r * tok + c8 * 8), vf);
+      const float w = pw[r];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) a8[e] += w * vf[e];
+    }
+  }
+  *(f32x4*)(red + rg * DHq + c8 * 8) = f32x4{a8[0], a8[1], a8[2], a8[3]};
+  *(f32x4*)(red + rg * DHq + c8 * 8 + 4) = f32x4{a8[4], a8[5], a8[6], a8[7]};
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
   for (int dd = 0; dd < (DHq + 63) / 64; ++dd) {
     const int d = lane + dd * 64;
     if (d < DHq) {
       float acc = a.null_kv ? pn * bf16_bits_to_f32(a.null_kv[((size_t)H + h) * DHq + d]) : 0.f;
       if (n_in > 0) acc += pw[pos] * bf16_bits_to_f32(vnew[d]);
-#pragma unroll 8
-      for (int r = 0; r < pos && r < n_in; ++r) acc += pw[r] * bf16_bits_to_f32(vc[(size_t)r * tok + d]);
+#pragma unroll
+      for (int g = 0; g < RG; ++g) acc += red[g * DHq + d];
       part[d] = acc;
     }
   }
@@ -365,6 +390,7 @@ __global__ void __launch_bounds__(256) k_rows_combine(RowsArgs a) {
   __shared__ float w_sh[4][kRowsSplitCap];
   __shared__ float u_sh[D];
   __shared__ float pw[64];
+  __shared__ __attribute__((aligned(16))) float ired[512];   // in-block value sums of the row groups
   __shared__ float stat[4];   // m_i, l_i, Mr, l'
   __shared__ float fin[1];    // scale of u' (times 1/L)
   const int tile = h / 16, hh = h % 16;     // the head's tile and its row in the tile
@@ -373,7 +399,7 @@ __global__ void __launch_bounds__(256) k_rows_combine(RowsArgs a) {
   const int lane = tid & 63, wave = tid >> 6;
   if (wave == 0) {
     float mi, li;
-    rows_intra<DHq>(a, slot, h, lane, pw, mi, li);
+    rows_intra<DHq>(a, slot, h, lane, pw, ired, mi, li);
     if (lane == 0) {
       stat[0] = mi;
       stat[1] = li;
