@@ -81,7 +81,7 @@ TRAFFIC = {
     "serve": ((CSRC + "attn_mfma.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"5c7540b5a80824c9": 3.0618e+08}),
     # 410M row-plane decode step: k_rows_absorb_q, k_reader_rows, k_rows_combine (with the
     # in-block keys), k_rows_project
-    "rows": ((CSRC + "rows.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"6b1ade5070885bd6": 6.4296e+08}),
+    "rows": ((CSRC + "rows.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"855177fe013f4c63": 6.4295e+08}),
 }
 
 
