@@ -19,6 +19,7 @@ namespace smem {
 
 typedef __bf16 bf16x8r __attribute__((ext_vector_type(8)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 constexpr int kRowChunk = 16;     // rows per chunk (one MFMA column tile)
 
@@ -42,7 +43,7 @@ struct RowsCfg {
 // workgroup's TG; the row chunks in LDS serve every group.
 template <int D, int TG>
 struct RowsLds {
-  uint16_t mu[RowsCfg<D>::NS][kRowChunk * RowsCfg<D>::MP];
+  alignas(16) uint16_t mu[RowsCfg<D>::NS][kRowChunk * RowsCfg<D>::MP];
   float sred[TG][4][256];                   // per-wave partial scores
   uint16_t p[TG][16 * 16];                  // P[head][row], bf16
   float alpha[TG][16];
@@ -296,15 +297,16 @@ __global__ void __launch_bounds__(256 * TG) k_reader_rows(RowsArgs a) {
       }
       const u32x2 pa = *(const u32x2*)&L.p[grp][(lane & 15) * 16 + (lane >> 4) * 4];
       const s16x4 A = __builtin_bit_cast(s16x4, pa);
-      const int rbase = (lane >> 4) * 4;
+      // B[k][n] = chunk row k, dim d0 + n for lane (n = l%16, k = 4(l/16) + i):
+      // one transposing read per tile.  ds_read_b64_tr_b16 hands lane j of
+      // each 16-lane group element i of the 8 bytes that lane 4i + j/4 of
+      // the group addressed, element j%4; so lane l addresses row l/4,
+      // dims d0 + 4(l%4) .. +3.
+      const uint16_t* trow = mu + (lane >> 2) * MP + 4 * (lane & 3);
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
-        const int dim = wave * DW + n * 16 + (lane & 15);
-        s16x4 B;
-        B[0] = (short)mu[(rbase + 0) * MP + dim];
-        B[1] = (short)mu[(rbase + 1) * MP + dim];
-        B[2] = (short)mu[(rbase + 2) * MP + dim];
-        B[3] = (short)mu[(rbase + 3) * MP + dim];
+        const int d0 = wave * DW + n * 16;
+        const s16x4 B = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(trow + d0));
         u[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(A, B, u[n], 0, 0, 0);
       }
     }

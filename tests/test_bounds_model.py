@@ -798,3 +798,23 @@ def test_encoder_output_staging(dh):
     for d, r in itertools.product(range(dh), range(BT)):               # the page insert's transposed gather
         slot = r * KRB + (((d >> 3) ^ kswz(r)) << 4)
         assert where[slot + (((d & 7) * 2) ^ (((slot >> 7) & 1) * 8))] == (r, d)
+
+
+@pytest.mark.parametrize("D", [512, 768, 1024, 2048])
+def test_rows_value_operand_transpose_read(D):
+    """The row reader's value MFMA (16x16x16) takes B[k][n] = row k of the
+    16-row chunk, dim d0 + n, in lane l = 16 (k // 4) + n as element k % 4.
+    ds_read_b64_tr_b16 gives lane j of each 16-lane group element i of the
+    8 bytes that lane 4 i + j // 4 of the group addressed, taking element
+    j % 4 of them (the lane layout measured on gfx950 with LDS holding each
+    element's index).  Each lane addresses row l // 4, dims d0 + 4 (l % 4):
+    every lane then holds its operand, and every address lies in the chunk."""
+    MP = D + 8
+    for d0 in range(0, D, 16):
+        addr = [(l // 4) * MP + d0 + 4 * (l % 4) for l in range(64)]
+        for l in range(64):
+            assert 0 <= addr[l] and addr[l] % 4 == 0 and l // 4 < 16 and d0 + 4 * (l % 4) + 4 <= D
+            g, j = l // 16, l % 16
+            for i in range(4):
+                src = 16 * g + 4 * i + j // 4
+                assert addr[src] + j % 4 == (4 * g + i) * MP + d0 + j
