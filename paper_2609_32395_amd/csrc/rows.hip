@@ -30,7 +30,12 @@ constexpr int kRowChunk = 16;     // rows per chunk (one MFMA column tile)
 #endif
 template <int D>
 struct RowsCfg {
-  static constexpr int MP = D + 8;                 // LDS row pitch (elements): 16-byte pad per row
+  // LDS row pitch (elements): a 32-byte pad, so the pitch is 32 bytes past a
+  // multiple of 256 (D = 512 .. 2048): the score reads (16 rows, 16 bytes
+  // each) and the transposing value reads (16 rows, 4 lanes x 8 bytes each)
+  // then touch every bank once (a 16-byte pad left both 2-way conflicted;
+  // measured with a one-wave bank probe)
+  static constexpr int MP = D + 16;
   // ring stages (LDS: NS * 16 rows * MP * 2 bytes; at most 2 at d = 2048)
   static constexpr int NS = D >= 2048 ? 2 : SMEM_ROWS_STAGES;
   static constexpr int RI = (D + 511) / 512;          // DMA instructions per row (the last partial at d = 768)

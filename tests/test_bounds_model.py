@@ -809,7 +809,7 @@ def test_rows_value_operand_transpose_read(D):
     j % 4 of them (the lane layout measured on gfx950 with LDS holding each
     element's index).  Each lane addresses row l // 4, dims d0 + 4 (l % 4):
     every lane then holds its operand, and every address lies in the chunk."""
-    MP = D + 8
+    MP = D + 16
     for d0 in range(0, D, 16):
         addr = [(l // 4) * MP + d0 + 4 * (l % 4) for l in range(64)]
         for l in range(64):
@@ -818,3 +818,27 @@ def test_rows_value_operand_transpose_read(D):
             for i in range(4):
                 src = 16 * g + 4 * i + j // 4
                 assert addr[src] + j % 4 == (4 * g + i) * MP + d0 + j
+
+
+@pytest.mark.parametrize("D", [512, 768, 1024, 2048])
+def test_rows_chunk_pitch_banks(D):
+    """The row reader's chunk pitch in LDS is D + 16 bf16.  Bank model (the
+    one that fits a one-wave probe of these reads at pads of 8, 16 and 24
+    elements: only 16 is conflict-free): 128 banks of 4 bytes, a 16-byte
+    read served 32 lanes at a time, a transposing 8-byte read 64 lanes at a
+    time.  Under it the score reads (row l % 16, 16 bytes at 16 (l // 16))
+    and the transposing value reads (row l // 4, 8 bytes at 8 (l % 4)) touch
+    each bank at most once per pass, a 16-byte pad does not, and two chunk
+    stages fit in LDS beside the reduction buffers."""
+    def clean(pad):
+        P = 2 * (D + pad)
+        for half in range(2):
+            banks = [((l % 16) * P + (l // 16) * 16) // 4 % 128 + i
+                     for l in range(32 * half, 32 * half + 32) for i in range(4)]
+            if len(set(b % 128 for b in banks)) != len(banks):
+                return False
+        banks = [((l // 4) * P + (l % 4) * 8) // 4 % 128 + i for l in range(64) for i in range(2)]
+        return len(set(b % 128 for b in banks)) == len(banks)
+    assert clean(16) and not clean(8) and not clean(24)
+    stage = 16 * (D + 16) * 2
+    assert 2 * stage + 2 * 4 * 256 * 4 + 2 * 256 * 2 + 2 * 16 * 4 + 64 <= 160 * 1024
