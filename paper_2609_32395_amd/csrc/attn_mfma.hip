@@ -214,7 +214,10 @@ struct PageRing {
   static constexpr int NS = DH == 32 ? SMEM_PREFILL_STAGES32 : DH == 64 ? SMEM_PREFILL_STAGES64 : SMEM_PREFILL_STAGES128;
   static constexpr int IPW = TILE / 1024 / 4;          // DMA instructions per wave per page
   static_assert(NS >= 2 && NS <= 5, "wait_pages covers up to 3 pages ahead");
-  __device__ static constexpr int kswz(int r) { return (r / (256 / KRB)) % KCH; }
+  // key rows: slot = chunk ^ kswz(r).  Chosen by measurement (a one-wave LDS
+  // bank probe of the score reads): r / 2 for 64-byte rows (r / 4 left them
+  // 2-way conflicted), r / 2 for 128-byte rows, r for 256-byte rows.
+  __device__ static constexpr int kswz(int r) { return (DH == 32 ? r / 2 : r / (256 / KRB)) % KCH; }
   // the 16-row group (d >> 4) enters the value permutation so that the
   // reads of rows d and d + 16 are never a fixed distance apart: merged into
   // one read2 instruction, their two halves fell on the same banks
@@ -376,13 +379,15 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
   // rows: a lane's fragment is 4 dims of one query row, 8 bytes scattered
   // over 64 rows.  An 8-byte write serves 16 consecutive lanes (16 rows, one
   // dim group) per pass over 128 bytes of banks, and the key swizzle maps two
-  // of those rows to the same 16-byte slot modulo 128 bytes; a slot in the
-  // upper 128 bytes of its 256-byte bank row therefore stores its two 8-byte
-  // halves swapped (swapped back when read), which gives the 16 lanes 16
-  // distinct 8-byte places.  A page insert writes the key plane from the
+  // of those rows to the same 16-byte slot modulo 128 bytes (rows q and q ^ 1
+  // at d_h = 64, rows whose slots differ in byte-address bit 7 at d_h = 128,
+  // q and q + 8 at d_h = 32); a slot whose address bit SWB (7, or 9 at d_h =
+  // 32) is set therefore stores its two 8-byte halves swapped (swapped back
+  // when read), which gives the 16 lanes 16 distinct 8-byte places.  A page insert writes the key plane from the
   // same rows and the transposed value plane by gathering each chunk's 8 rows
   // (the lanes of one instruction read one row).
   __syncthreads();                           // every wave is done with the key and value tiles
+  constexpr int SWB = DH == 32 ? 9 : 7;
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) {
     const int d0 = dt * 16 + (lane >> 4) * 4;
@@ -390,7 +395,7 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) rr[i] = f32_to_bf16_bits(o[dt][i] * inv);
     const int slot = qrow * R::KRB + (((d0 >> 3) ^ R::kswz(qrow)) << 4);
-    const int half = ((d0 >> 2) & 1) ^ ((slot >> 7) & 1);   // halves swapped in the upper 128 bytes
+    const int half = ((d0 >> 2) & 1) ^ ((slot >> SWB) & 1);  // halves swapped where bit SWB is set
     *(u32x2*)(T + slot + half * 8) =
         u32x2{(uint32_t)rr[0] | ((uint32_t)rr[1] << 16), (uint32_t)rr[2] | ((uint32_t)rr[3] << 16)};
   }
@@ -399,7 +404,7 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
     const int row = c / (DH / 8), c8 = c % (DH / 8);
     const int slot = row * R::KRB + ((c8 ^ R::kswz(row)) << 4);
     u32x4 v16 = *(const u32x4*)(T + slot);
-    if ((slot >> 7) & 1) v16 = u32x4{v16.z, v16.w, v16.x, v16.y};
+    if ((slot >> SWB) & 1) v16 = u32x4{v16.z, v16.w, v16.x, v16.y};
     if (a.out) *(u32x4*)(a.out + ((size_t)blk * BT + row) * rs + (size_t)h * DH + c8 * 8) = v16;
     if (kp) *(u32x4*)(kp + row * DH + c8 * 8) = v16;
   }
@@ -408,7 +413,7 @@ __global__ void __launch_bounds__(256) k_encoder_mfma(EncArgs a) {
       const int d = c % DH, r8 = c / DH;
       auto at = [&](int r) {
         const int slot = r * R::KRB + (((d >> 3) ^ R::kswz(r)) << 4);
-        return (uint32_t) * (const uint16_t*)(T + slot + (((d & 7) * 2) ^ (((slot >> 7) & 1) * 8)));
+        return (uint32_t) * (const uint16_t*)(T + slot + (((d & 7) * 2) ^ (((slot >> SWB) & 1) * 8)));
       };
       uint32_t w[4];
 #pragma unroll
