@@ -74,14 +74,14 @@ TRAFFIC = {
     # 410M decode step: k_reader_valu + k_merge
     "decode": ((CSRC + "reader_valu.hip", CSRC + "common.h"), {"3b1f089ddfea81b8": 1.0890e+09}),
     # 160M encoder: k_encoder_mfma (attention only)
-    "encoder": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"c8ed6113250b822e": 5.0445e+07}),
+    "encoder": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"a944063c18395c93": 5.0445e+07}),
     # 160M final-block prefill: k_prefill_mfma_par
-    "prefill": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"c8ed6113250b822e": 2.6971e+07}),
+    "prefill": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"a944063c18395c93": 2.6971e+07}),
     # 1.5B serve: k_prefill_mfma + k_merge
-    "serve": ((CSRC + "attn_mfma.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"5c7540b5a80824c9": 3.0618e+08}),
+    "serve": ((CSRC + "attn_mfma.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"b700a321544a914b": 3.0613e+08}),
     # 410M row-plane decode step: k_rows_absorb_q, k_reader_rows, k_rows_combine (with the
     # in-block keys), k_rows_project
-    "rows": ((CSRC + "rows.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"855177fe013f4c63": 6.4295e+08}),
+    "rows": ((CSRC + "rows.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"e75aa73d76800e7c": 6.4303e+08}),
 }
 
 
