@@ -53,7 +53,12 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
-template <typename T, int DH, int B, bool ROPE>
+// MEM = false: a launch in which no slot reads a memory page (every
+// workgroup runs the null row and in-block keys only, e.g. a model layer's
+// self-attention over its in-block cache): the page path is compiled out,
+// so the kernel holds fewer registers and more workgroups run at once; the
+// arithmetic of the split it runs is the same.
+template <typename T, int DH, int B, bool ROPE, bool MEM = true>
 __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
   using C = RCfg<T, DH, B>;
   constexpr int E = C::E;
@@ -85,7 +90,7 @@ __global__ void __launch_bounds__(256) k_reader_valu(ReaderArgs a) {
   }
   float m = -INFINITY, l = 0.f;
 
-  if (split < nms) {
+  if (MEM && split < nms) {
     // ------------------------------------------------ memory pages of this split
     float acc[C::VLOADS];
 #pragma unroll
@@ -358,6 +363,8 @@ static hipError_t launch_rv(const ReaderArgs& a, hipStream_t s) {
   dim3 grid(a.H, max_split + 1, a.n_slots * a.nq);
   if (a.rope != nullptr)
     hipLaunchKernelGGL((k_reader_valu<T, DH, B, true>), grid, dim3(256), 0, s, a);
+  else if (max_split == 0)   // no slot reads a memory page
+    hipLaunchKernelGGL((k_reader_valu<T, DH, B, false, false>), grid, dim3(256), 0, s, a);
   else
     hipLaunchKernelGGL((k_reader_valu<T, DH, B, false>), grid, dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
