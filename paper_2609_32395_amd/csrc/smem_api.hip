@@ -712,7 +712,7 @@ static smem_status prefill_impl(smem_store* st, const smem_rope* rope, int32_t n
       a.qblk[i] = query_block[i0 + i];
       a.n_read[i] = nr[i0 + i];
       a.pps[i] = mfma ? pages_per_split(a.n_read[i], kMinPagesPrefill, prefill_split_cap(d.H))
-                      : pages_per_split(a.n_read[i], kMinPagesDecode);
+                      : pages_per_split(a.n_read[i], min_pages_decode(d.dh));
       a.aux[i] = -1;
     }
     a.fuse = fuse;
@@ -771,7 +771,7 @@ smem_status smem::decode_impl(smem_store* st, const smem_rope* rope, int32_t n_s
   std::vector<int32_t> stride((n_seq + kMaxSlots - 1) / kMaxSlots, 1);
   for (int i = 0; i < n_seq; ++i) {
     nr[i] = n_read_of(st, seq_ids[i], query_block[i]);
-    pp[i] = pages_per_split(nr[i], kMinPagesDecode);
+    pp[i] = pages_per_split(nr[i], min_pages_decode(d.dh));
     int32_t& w = stride[i / kMaxSlots];
     w = std::max(w, (int32_t)total_splits(nr[i], pp[i]));
   }

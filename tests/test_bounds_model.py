@@ -74,7 +74,7 @@ def test_reader_valu_indexing(b, dh, es):
         assert ((1 * H + H - 1) * dh + (LPR - 1) * E + E - 1) < 2 * H * dh
         # split partials: split index <= memory splits <= cap, rows (query rows x heads) fit the workspace
         for n_read in (0, 1, 63, 64, 65, 4096, 65536):
-            pps = pages_per_split(n_read, MIN_PAGES_DECODE)
+            pps = pages_per_split(n_read, 4 if dh <= 32 else MIN_PAGES_DECODE)
             nms = -(-n_read // pps)
             nsplit = nms + 1   # the null row and in-block keys have their own split
             assert nsplit <= SPLIT_STRIDE
