@@ -72,16 +72,16 @@ MFMA_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published (2.5 PFLOP/s,
 CSRC = "paper_2609_32395_amd/csrc/"
 TRAFFIC = {
     # 410M decode step: k_reader_valu + k_merge
-    "decode": ((CSRC + "reader_valu.hip", CSRC + "common.h"), {"aa5c80c4fd162826": 1.0890e+09}),
+    "decode": ((CSRC + "reader_valu.hip", CSRC + "common.h"), {"77e591978f5a0ddc": 1.0890e+09}),
     # 160M encoder: k_encoder_mfma (attention only)
-    "encoder": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"a944063c18395c93": 5.0445e+07}),
+    "encoder": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"f3af876805558471": 5.0445e+07}),
     # 160M final-block prefill: k_prefill_mfma_par
-    "prefill": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"a944063c18395c93": 2.6971e+07}),
+    "prefill": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"f3af876805558471": 2.6971e+07}),
     # 1.5B serve: k_prefill_mfma + k_merge
-    "serve": ((CSRC + "attn_mfma.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"d805f7f003458062": 3.0611e+08}),
+    "serve": ((CSRC + "attn_mfma.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"462c74f4978b6ee5": 3.0615e+08}),
     # 410M row-plane decode step: k_rows_absorb_q, k_reader_rows, k_rows_combine (with the
     # in-block keys), k_rows_project
-    "rows": ((CSRC + "rows.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"89ccc07c9d2758bc": 6.4302e+08}),
+    "rows": ((CSRC + "rows.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"39d68117510eaddf": 6.4302e+08}),
 }
 
 
