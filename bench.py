@@ -74,11 +74,12 @@ TRAFFIC = {
     # 410M decode step: k_reader_valu + k_merge
     "decode": ((CSRC + "reader_valu.hip", CSRC + "common.h"), {"77e591978f5a0ddc": 1.0890e+09}),
     # 160M encoder: k_encoder_mfma (attention only)
-    "encoder": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"f3af876805558471": 5.0445e+07}),
+    "encoder": ((CSRC + "attn_mfma.hip", CSRC + "attn_ring.h", CSRC + "common.h"), {"2e5d7e7c4cc7fcae": 5.0445e+07}),
     # 160M final-block prefill: k_prefill_mfma_par
-    "prefill": ((CSRC + "attn_mfma.hip", CSRC + "common.h"), {"f3af876805558471": 2.6971e+07}),
+    "prefill": ((CSRC + "attn_mfma.hip", CSRC + "attn_ring.h", CSRC + "common.h"), {"2e5d7e7c4cc7fcae": 2.6971e+07}),
     # 1.5B serve: k_prefill_mfma + k_merge
-    "serve": ((CSRC + "attn_mfma.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"462c74f4978b6ee5": 3.0615e+08}),
+    "serve": ((CSRC + "attn_mfma.hip", CSRC + "attn_ring.h", CSRC + "reader_valu.hip", CSRC + "common.h"),
+              {"d0b754a9272c091a": 3.0615e+08}),
     # 410M row-plane decode step: k_rows_absorb_q, k_reader_rows, k_rows_combine (with the
     # in-block keys), k_rows_project
     "rows": ((CSRC + "rows.hip", CSRC + "reader_valu.hip", CSRC + "common.h"), {"39d68117510eaddf": 6.4302e+08}),

@@ -451,6 +451,30 @@ smem_status smem_model_decode(smem_model* m, int32_t first_seq, int32_t n_seq, c
  * (Theorem 1).  SMEM_ENOENT if absent. */
 smem_status smem_model_delete_block(smem_model* m, int32_t seq, int32_t block_idx, hipStream_t s);
 
+/* The attention part of one self-attention sub-layer of the model (Section
+ * 2, "Model"; Appendix A, "Encoder" and "Reader"): per block of 64 rows and
+ * per head, out = softmax(q k^T / sqrt(d_h)) v over the block's own rows
+ * (all of them: mask SMEM_MASK_BIDIR, the encoder; keys up to the query's
+ * row: SMEM_MASK_CAUSAL, the reader), with q | k | v = LN(x) W_qkv^T, on the
+ * kernels the model uses.
+ *   n_blocks: blocks of 64 rows (<= 65535); d = H d_h, d % 64 == 0,
+ *     d <= 2048, d_h in {32, 64, 128};
+ *   x: device bf16 [n_blocks * 64, d]; ln_g, ln_b: device bf16 [d]
+ *     (LayerNorm gain and shift, eps 1e-5); w_qkv: device bf16 [3d, d]
+ *     (the q, k and v maps' rows in that order, head h in rows
+ *     h d_h .. h d_h + d_h - 1 of each);
+ *   path: 1 the q|k|v map, then the block-local attention launch; 0 the
+ *     model's choice, which is path 1 (faster at every size measured on
+ *     MI355X); 2 one fused launch per call (d_h = 32 and d a multiple of 256
+ *     up to 1024 only, else SMEM_EINVAL);
+ *   out: device bf16 [n_blocks * 64, d], head h in columns h d_h ..;
+ *   work: device bf16 [4, n_blocks * 64, d] (normalized rows, q, k, v),
+ *     caller-owned; may be NULL on the fused path with n_blocks * 64 <= 128.
+ * Every path gives the same bits.  Pointers 16-byte aligned. */
+smem_status smem_self_attention(int32_t n_blocks, int32_t d, int32_t H, const void* x, const void* ln_g,
+                                const void* ln_b, const void* w_qkv, int32_t mask, int32_t path, void* out, void* work,
+                                hipStream_t s);
+
 /* One linear map of the model's layers (Appendix A: pre-LN layers, linear
  * maps without bias, a GELU feed-forward), on the same kernels and in the
  * same reduction order the model uses: y = epi(LN(x) W^T), or epi(x W^T)

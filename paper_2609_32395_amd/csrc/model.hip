@@ -12,6 +12,7 @@
 #include <set>
 #include <vector>
 
+#include "attn_ring.h"
 #include "common.h"
 #include "linear.h"
 #include "smem.h"
@@ -53,6 +54,208 @@ __global__ void __launch_bounds__(256) k_embed(EmbArgs a) {
     for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f32_to_bf16_bits(e[2 * i]) | ((uint32_t)f32_to_bf16_bits(e[2 * i + 1]) << 16);
     *(u32x4*)(a.x + (size_t)r * a.d + c) = u32x4{w[0], w[1], w[2], w[3]};
   }
+}
+
+
+// ---------------------------------------------------------------- fused self-attention
+
+// The attention part of a self-attention sub-layer for d_h = 32 (Section 2,
+// "Model"; Appendix A, "Encoder" and "Reader"): o = Attn(q, k, v) per
+// (block, head) with q | k | v = LN(x) W_qkv^T, in one workgroup per
+// (block, head) instead of a linear-map launch followed by the block-local
+// attention launch.  Two waves per reduction chunk (256 wide), 32 rows each,
+// compute the chunk's share of the head's 64 x 96 tile (its q, k and v
+// columns) exactly as the few-row map computes a chunk: the rows normalized in registers with the
+// statistics met in LDS in the LayerNorm's fixed order, one 16x16x32 MFMA
+// per 32-wide step from zero, the W tile as the row operand; the chunk sums
+// are added in chunk order from zero and rounded to bf16 into LDS.  Four
+// waves then run the block-local attention kernel's steps on that tile
+// (the same helpers in the same order), so q, k, v and the output carry the
+// bits of the unfused pair.  PRE: x already holds LN(x) (many rows: one
+// LayerNorm pass serves every head) and the normalization is skipped.
+struct QkvAttnArgs {
+  const uint16_t* x;    // [n_blocks * 64][d]: rows, or normalized rows (PRE)
+  const uint16_t* lng;  // LayerNorm gain and shift [d] (not read with PRE)
+  const uint16_t* lnb;
+  const uint16_t* w;    // [3d][d]: q rows [0, d), k rows [d, 2d), v rows [2d, 3d)
+  uint16_t* out;        // [n_blocks * 64][d]: head h in columns [32 h, 32 h + 32)
+  float scale_log2;     // log2(e) / sqrt(d_h)
+};
+
+constexpr int kQkvDh = 32, kQkvCols = 3 * kQkvDh, kQkvMaxChunks = 4;
+
+template <int NC, bool CAUSAL, bool PRE>
+__global__ void __launch_bounds__(512) k_qkv_attn(QkvAttnArgs a) {
+  // wave w < 2 NC: chunk w / 2, row tiles 2 (w % 2) and 2 (w % 2) + 1
+  constexpr int DH = kQkvDh, NCOL = kQkvCols, CT = NCOL / 16, D = 256 * NC, U = 4, RT = 2;
+  using R = PageRing<DH>;
+  __shared__ __attribute__((aligned(1024))) uint8_t T[R::TILE];
+  __shared__ __attribute__((aligned(16))) float part[NC * BT * NCOL];   // [chunk][row][column] sums
+  __shared__ __attribute__((aligned(16))) uint16_t stage[BT * NCOL];    // q | k | v rows, bf16
+  __shared__ __attribute__((aligned(16))) uint16_t gb[PRE ? 8 : 2 * D]; // gain, then shift
+  __shared__ float st0[PRE ? 1 : NC * BT], st1[PRE ? 1 : NC * BT];      // [chunk][row] statistics
+  const int h = blockIdx.x, blk = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c = w >> 1, r0 = (w & 1) * RT * 16;                        // chunk, first row
+  const int kofs = (lane >> 4) * 8;
+  const bool worker = c < NC;
+
+  u32x4 X[8][RT], B[U][CT];
+  const uint16_t* wr[CT];
+  if (worker) {
+    const uint16_t* xr = a.x + ((size_t)blk * BT + r0 + (lane & 15)) * D + c * 256 + kofs;
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+#pragma unroll
+      for (int i = 0; i < RT; ++i) X[t][i] = *(const u32x4*)(xr + (size_t)i * 16 * D + t * 32);
+#pragma unroll
+    for (int j = 0; j < CT; ++j)
+      wr[j] = a.w + ((size_t)(j >> 1) * D + h * DH + (j & 1) * 16 + (lane & 15)) * D + c * 256 + kofs;
+#pragma unroll
+    for (int t = 0; t < U; ++t)
+#pragma unroll
+      for (int j = 0; j < CT; ++j) B[t][j] = *(const u32x4*)(wr[j] + t * 32);
+  }
+  if constexpr (!PRE) {
+    const int q8 = tid * 8;
+    if (q8 < D) {
+      *(u32x4*)(gb + q8) = *(const u32x4*)(a.lng + q8);
+      *(u32x4*)(gb + D + q8) = *(const u32x4*)(a.lnb + q8);
+    }
+    float mean[RT], rstd[RT];
+    if (worker) {
+#pragma unroll
+      for (int i = 0; i < RT; ++i) {
+        float v = 0.f;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) v = ln_sum8(X[t][i], v);
+        v += __shfl_xor(v, 16);
+        v += __shfl_xor(v, 32);
+        if (lane < 16) st0[c * BT + r0 + i * 16 + lane] = v;
+      }
+      opaque(X);
+    }
+    __syncthreads();
+    if (worker) {
+#pragma unroll
+      for (int i = 0; i < RT; ++i) {
+        float tot = 0.f;
+        for (int q = 0; q < NC; ++q) tot += st0[q * BT + r0 + i * 16 + (lane & 15)];
+        mean[i] = tot / D;
+        float v = 0.f;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) v = ln_sq8(X[t][i], mean[i], v);
+        v += __shfl_xor(v, 16);
+        v += __shfl_xor(v, 32);
+        if (lane < 16) st1[c * BT + r0 + i * 16 + lane] = v;
+      }
+      opaque(X);
+    }
+    __syncthreads();
+    if (worker) {
+#pragma unroll
+      for (int i = 0; i < RT; ++i) {
+        float tot = 0.f;
+        for (int q = 0; q < NC; ++q) tot += st1[q * BT + r0 + i * 16 + (lane & 15)];
+        rstd[i] = ln_rstd(tot, D);
+      }
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int k = c * 256 + t * 32 + kofs;
+        const u32x4 g8 = *(const u32x4*)(gb + k), b8 = *(const u32x4*)(gb + D + k);
+#pragma unroll
+        for (int i = 0; i < RT; ++i) X[t][i] = ln_apply8(X[t][i], g8, b8, mean[i], rstd[i]);
+      }
+    }
+  }
+  if (worker) {
+    f32x4 acc[RT][CT];
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+#pragma unroll
+      for (int j = 0; j < CT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+#pragma unroll
+      for (int i = 0; i < RT; ++i)
+#pragma unroll
+        for (int j = 0; j < CT; ++j) acc[i][j] = mfma16(B[t % U][j], X[t][i], acc[i][j]);
+      if (t + U < 8) {
+#pragma unroll
+        for (int j = 0; j < CT; ++j) B[t % U][j] = *(const u32x4*)(wr[j] + (t + U) * 32);
+      }
+    }
+    // lane: row r0 + i*16 + l%16, columns j*16 + 4 (l/16) .. +3
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+#pragma unroll
+      for (int j = 0; j < CT; ++j)
+        *(f32x4*)(part + (c * BT + r0 + i * 16 + (lane & 15)) * NCOL + j * 16 + 4 * (lane >> 4)) = acc[i][j];
+  }
+  __syncthreads();
+  for (int q = tid; q < BT * NCOL / 4; q += 512) {
+    const int row = q / (NCOL / 4), c0 = (q % (NCOL / 4)) * 4;
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    for (int ch = 0; ch < NC; ++ch) v += *(const f32x4*)(part + (ch * BT + row) * NCOL + c0);
+    *(u32x2*)(stage + row * NCOL + c0) =
+        u32x2{(uint32_t)f32_to_bf16_bits(v[0]) | ((uint32_t)f32_to_bf16_bits(v[1]) << 16),
+              (uint32_t)f32_to_bf16_bits(v[2]) | ((uint32_t)f32_to_bf16_bits(v[3]) << 16)};
+  }
+  __syncthreads();
+  // block-local attention: waves 0..3 take 16 query rows each
+  intra_ring_store<DH, 512>(T, stage + DH, stage + 2 * DH, NCOL, tid);
+  __syncthreads();
+  if (w >= 4) return;                    // no barrier follows
+  const int qrow = w * 16 + (lane & 15);
+  bf16x8 qf[DH / 32];
+  load_q<DH>(qf, stage + w * 16 * NCOL, NCOL, lane);
+  floatx4 s4[4];
+  scores_ring<DH>(s4, T, qf, lane);
+  floatx4 o[DH / 16];
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY, l = 0.f;
+  online_step<DH, CAUSAL>(s4, m, l, o, lane, qrow, a.scale_log2);
+  pv_ring<DH>(o, T, s4, lane);
+  l = qsum(l);
+  const float inv = 1.f / l;
+  uint16_t* orow = a.out + ((size_t)blk * BT + qrow) * D + h * DH;
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) {
+    const int d0 = dt * 16 + (lane >> 4) * 4;
+    uint16_t r4[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r4[i] = f32_to_bf16_bits(o[dt][i] * inv);
+    *(u32x2*)(orow + d0) = u32x2{(uint32_t)r4[0] | ((uint32_t)r4[1] << 16), (uint32_t)r4[2] | ((uint32_t)r4[3] << 16)};
+  }
+}
+
+template <int NC>
+static void launch_qkv_attn_nc(const QkvAttnArgs& a, int H, int nb, bool causal, bool pre, hipStream_t s) {
+  const dim3 grid(H, nb);
+  if (causal) {
+    if (pre) hipLaunchKernelGGL((k_qkv_attn<NC, true, true>), grid, dim3(512), 0, s, a);
+    else hipLaunchKernelGGL((k_qkv_attn<NC, true, false>), grid, dim3(512), 0, s, a);
+  } else {
+    if (pre) hipLaunchKernelGGL((k_qkv_attn<NC, false, true>), grid, dim3(512), 0, s, a);
+    else hipLaunchKernelGGL((k_qkv_attn<NC, false, false>), grid, dim3(512), 0, s, a);
+  }
+}
+
+// d = 32 H with d a multiple of 256 up to 1024 (the LDS of the chunk sums
+// bounds the chunk count); nb blocks of 64 rows.
+bool qkv_attn_fits(int d, int H) { return d == kQkvDh * H && d % 256 == 0 && d / 256 <= kQkvMaxChunks; }
+
+hipError_t launch_qkv_attn(const QkvAttnArgs& a, int d, int H, int nb, bool causal, bool pre, hipStream_t s) {
+  if (!qkv_attn_fits(d, H) || nb <= 0 || nb > 65535) return hipErrorInvalidValue;
+  switch (d / 256) {
+    case 1: launch_qkv_attn_nc<1>(a, H, nb, causal, pre, s); break;
+    case 2: launch_qkv_attn_nc<2>(a, H, nb, causal, pre, s); break;
+    case 3: launch_qkv_attn_nc<3>(a, H, nb, causal, pre, s); break;
+    default: launch_qkv_attn_nc<4>(a, H, nb, causal, pre, s); break;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace smem
@@ -217,14 +420,42 @@ smem_status ffn(smem_model* m, int rows, const uint16_t* g, const uint16_t* b, c
   return SMEM_OK;
 }
 
+// The attention part of a self-attention sub-layer: out = Attn(q, k, v) per
+// (block, head) with q | k | v = LN(x) W_qkv^T.  path 1 (also path 0, the
+// model's choice): the q|k|v map (its few-row or tiled kernel) into q, k, v,
+// then the block-local attention launch; path 2: the fused kernel (d_h = 32,
+// d <= 1024), whose rows above 128 are normalized by one LayerNorm pass into
+// hn first.  Both paths give the same bits.  The fused kernel measured slower
+// at every block count: a workgroup per (block, head) pulls the head's
+// weights and the block's rows through one CU, where the map spreads them
+// over hundreds of workgroups, and at many blocks its 64 x 96 tile re-reads
+// the weights per block.
+smem_status attn_sublayer(int nb, int d, int H, const uint16_t* x, const uint16_t* g, const uint16_t* b,
+                          const uint16_t* wqkv, int mask, int path, uint16_t* out, uint16_t* hn, uint16_t* q,
+                          uint16_t* k, uint16_t* v, hipStream_t s) {
+  const int rows = nb * BT;
+  if (path == 2) {
+    const bool pre = rows > 128;
+    if (pre) MCHECK(lnorm(x, g, b, hn, rows, d, s), "self-attention layernorm");
+    QkvAttnArgs f;
+    f.x = pre ? hn : x;
+    f.lng = g; f.lnb = b; f.w = wqkv; f.out = out;
+    f.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)kQkvDh));
+    MCHECK(launch_qkv_attn(f, d, H, nb, mask == SMEM_MASK_CAUSAL, pre, s), "fused q|k|v and self-attention");
+    return SMEM_OK;
+  }
+  LinArgs a = lin(x, d, wqkv, rows, 3 * d, d, q, d);
+  a.lng = g; a.lnb = b; a.lnout = hn;
+  a.y1 = k; a.y2 = v; a.ns = d;
+  MCHECK(linear<kLinSplit>(a, s), "qkv");
+  const smem_attn_desc shape{BT, H, d / H, SMEM_BF16};
+  return smem_encode_blocks(nullptr, &shape, nb, nullptr, nullptr, q, k, v, out, mask, s);
+}
+
 smem_status self_attn(smem_model* m, int rows, int nb, const uint16_t* g, const uint16_t* b, const uint16_t* wqkv,
                       const uint16_t* wo, int mask, hipStream_t s) {
   const int D = m->d.d;
-  LinArgs a = lin_ln(m, g, b, wqkv, rows, 3 * D, m->q, D);
-  a.y1 = m->k; a.y2 = m->v; a.ns = D;
-  MCHECK(linear<kLinSplit>(a, s), "qkv");
-  const smem_attn_desc shape{m->d.b, m->d.H, m->d.dh, SMEM_BF16};
-  MSTATUS(smem_encode_blocks(nullptr, &shape, nb, nullptr, nullptr, m->q, m->k, m->v, m->o, mask, s));
+  MSTATUS(attn_sublayer(nb, D, m->d.H, m->x, g, b, wqkv, mask, 0, m->o, m->h, m->q, m->k, m->v, s));
   LinArgs o = lin(m->o, D, wo, rows, D, D, m->x, D);
   o.res = m->x;
   MCHECK(linear<kLinResid>(o, s), "attention out");
@@ -542,6 +773,31 @@ smem_status smem_model_delete_block(smem_model* m, int32_t seq, int32_t block_id
   if (m->d.row_plane) return smem_delete_block(m->rows, seq, block_idx, 0, s);
   for (smem_store* st : m->stores) MSTATUS(smem_delete_block(st, seq, block_idx, 0, s));
   return SMEM_OK;
+}
+
+smem_status smem_self_attention(int32_t n_blocks, int32_t d, int32_t H, const void* x, const void* ln_g,
+                                const void* ln_b, const void* w_qkv, int32_t mask, int32_t path, void* out, void* work,
+                                hipStream_t s) {
+  if (n_blocks < 0 || H < 1 || d < 64 || d % 64 || d > 2048 || d % H) return mfail(SMEM_EINVAL, "bad shape");
+  const int dh = d / H;
+  if (dh != 32 && dh != 64 && dh != 128) return mfail(SMEM_EINVAL, "d / H must be 32, 64 or 128");
+  if (mask != SMEM_MASK_BIDIR && mask != SMEM_MASK_CAUSAL) return mfail(SMEM_EINVAL, "bad mask");
+  if (path < 0 || path > 2) return mfail(SMEM_EINVAL, "path is 0 (the model's choice), 1 (unfused) or 2 (fused)");
+  if (path == 2 && !qkv_attn_fits(d, H))
+    return mfail(SMEM_EINVAL, "the fused path needs d / H = 32 and d a multiple of 256 up to 1024");
+  if (n_blocks > 65535) return mfail(SMEM_EINVAL, "at most 65535 blocks per call");
+  if (!x || !ln_g || !ln_b || !w_qkv || !out) return mfail(SMEM_EINVAL, "x, ln_g, ln_b, w_qkv, out are required");
+  const int eff = path == 2 ? 2 : 1;
+  const size_t rows = (size_t)n_blocks * BT, plane = rows * d;
+  if (!work && (eff == 1 || rows > 128)) return mfail(SMEM_EINVAL, "work is required for this path and size");
+  const void* ptrs[] = {x, ln_g, ln_b, w_qkv, out, work};
+  for (const void* p : ptrs)
+    if ((uintptr_t)p & 15u) return mfail(SMEM_EINVAL, "tensors must be 16-byte aligned");
+  if (n_blocks == 0) return SMEM_OK;
+  uint16_t* wk = (uint16_t*)work;
+  return attn_sublayer(n_blocks, d, H, (const uint16_t*)x, (const uint16_t*)ln_g, (const uint16_t*)ln_b,
+                       (const uint16_t*)w_qkv, mask, eff, (uint16_t*)out, wk, wk ? wk + plane : nullptr,
+                       wk ? wk + 2 * plane : nullptr, wk ? wk + 3 * plane : nullptr, s);
 }
 
 smem_status smem_linear(int32_t M, int32_t N, int32_t K, const void* x, const void* w, const void* ln_g,

@@ -113,6 +113,7 @@ SIGNATURES = {
     "smem_model_decode": (_I, [_P, _I, _I, _IP, _IP, _P, _P, _P]),
     "smem_model_delete_block": (_I, [_P, _I, _I, _P]),
     "smem_linear": (_I, [_I, _I, _I, _P, _P, _P, _P, _I, _P, _P, _P, _P]),
+    "smem_self_attention": (_I, [_I, _I, _I, _P, _P, _P, _P, _I, _I, _P, _P, _P]),
     "smem_store_stats": (_I, [_P, _IP, _IP]),
     "smem_device_copy": (_I, [_P, _P, ctypes.c_size_t, _I, _P]),
     "smem_status_string": (ctypes.c_char_p, [_I]),
@@ -479,6 +480,29 @@ def smem_linear(x, w, ln_g=None, ln_b=None, epi=LIN_STORE, res=None, y=None, ln_
                              p(y, (M, N), torch.float32 if epi == LIN_F32 else torch.bfloat16, "y"),
                              p(ln_tmp, (M, K), torch.bfloat16, "ln_tmp"), _stream(stream)))
     return y
+
+
+SA_AUTO, SA_UNFUSED, SA_FUSED = 0, 1, 2
+
+
+def smem_self_attention(x, ln_g, ln_b, w_qkv, H, mask, path=SA_AUTO, out=None, work=None, stream=None):
+    """The attention part of a self-attention sub-layer on the model's kernels:
+    per block of 64 rows and head, Attn(q, k, v) with q | k | v = LN(x) W_qkv^T;
+    x [n_blocks * 64, d] bf16, w_qkv [3d, d] bf16; returns out [n_blocks * 64, d]."""
+    M, d = x.shape
+    if M % 64:
+        raise ValueError("x rows must be whole blocks of 64")
+    if w_qkv.shape != (3 * d, d):
+        raise ValueError("w_qkv must be [3d, d]")
+    if out is None:
+        out = torch.empty((M, d), dtype=torch.bfloat16, device=x.device)
+    if work is None:
+        work = torch.empty((4, M, d), dtype=torch.bfloat16, device=x.device)
+    p = lambda t, shape, n: _dev(t, shape, torch.bfloat16, n)
+    _check(lib().smem_self_attention(M // 64, d, int(H), p(x, (M, d), "x"), p(ln_g, (d,), "ln_g"),
+                                     p(ln_b, (d,), "ln_b"), p(w_qkv, (3 * d, d), "w_qkv"), int(mask), int(path),
+                                     p(out, (M, d), "out"), p(work, (4, M, d), "work"), _stream(stream)))
+    return out
 
 
 def smem_model_delete_block(m: Model, seq: int, block_idx: int, stream=None):

@@ -843,3 +843,69 @@ def test_rows_chunk_pitch_banks(D):
     assert clean(16) and not clean(8) and not clean(24)
     stage = 16 * (D + 16) * 2
     assert 2 * stage + 2 * 4 * 256 * 4 + 2 * 256 * 2 + 2 * 16 * 4 + 64 <= 160 * 1024
+
+
+@pytest.mark.parametrize("nc", [1, 2, 3, 4])
+def test_fused_self_attention_indexing(nc):
+    """k_qkv_attn (d = 256 nc, d_h = 32, one workgroup of 8 waves per (block,
+    head)): every global and LDS offset stays in its buffer; the chunk
+    partials cover (chunk, row, column) exactly once for the chunks that
+    exist, and the ordered sum writes every staged q|k|v value once."""
+    D, DH, NCOL, CT, BT, RT = 256 * nc, 32, 96, 6, 64, 2
+    H = D // DH
+    part = [0] * (nc * BT * NCOL)
+    for w in range(8):
+        c, r0 = w >> 1, (w & 1) * RT * 16
+        if c >= nc:
+            continue
+        for lane in range(64):
+            kofs = (lane >> 4) * 8
+            for i in range(RT):
+                row = r0 + i * 16 + (lane & 15)
+                assert row < BT
+                for t in range(8):
+                    col = c * 256 + kofs + t * 32
+                    assert col + 8 <= D                  # x row [blk*64 + row][col .. col+7]
+            for h in (0, H - 1):
+                for j in range(CT):
+                    wrow = (j >> 1) * D + h * DH + (j & 1) * 16 + (lane & 15)
+                    assert wrow < 3 * D
+                    assert c * 256 + kofs + (8 - 1) * 32 + 8 <= D
+            for i in range(RT):
+                for j in range(CT):
+                    base = (c * BT + r0 + i * 16 + (lane & 15)) * NCOL + j * 16 + 4 * (lane >> 4)
+                    for e in range(4):
+                        part[base + e] += 1
+            if lane < 16:
+                for i in range(RT):
+                    assert c * BT + r0 + i * 16 + lane < nc * BT    # st0 / st1
+    assert part == [1] * len(part)
+    stage = [0] * (BT * NCOL)
+    for q in range(BT * NCOL // 4):
+        row, c0 = q // (NCOL // 4), (q % (NCOL // 4)) * 4
+        for ch in range(nc):
+            assert (ch * BT + row) * NCOL + c0 + 4 <= nc * BT * NCOL
+        for e in range(4):
+            stage[row * NCOL + c0 + e] += 1
+    assert stage == [1] * len(stage)
+    # attention: waves 0..3, query rows 16 w + l % 16; q fragments and the
+    # key / value rows read from the stage (row stride 96, k at 32, v at 64)
+    for w in range(4):
+        for lane in range(64):
+            qr = (w * 16 + (lane & 15)) * NCOL + (lane >> 4) * 8
+            assert qr + 8 <= BT * NCOL
+    cpr, nk = DH // 8, BT * (DH // 8)
+    nj = nk + (BT // 2) * cpr
+    assert nj <= 512                                        # one job per thread
+    for j in range(nj):
+        if j < nk:
+            assert DH + (j // cpr) * NCOL + (j % cpr) * 8 + 8 <= BT * NCOL
+        else:
+            pr, c8 = (j - nk) // cpr, (j - nk) % cpr
+            assert 2 * DH + (2 * pr + 1) * NCOL + c8 * 8 + 8 <= BT * NCOL
+    # output rows: head h in columns [32 h, 32 h + 32)
+    for lane in range(64):
+        for dt in range(DH // 16):
+            assert (H - 1) * DH + dt * 16 + (lane >> 4) * 4 + 4 <= D
+    lds = 2 * BT * DH * 2 + nc * BT * NCOL * 4 + BT * NCOL * 2 + 2 * D * 2 + 2 * nc * BT * 4
+    assert lds <= 160 * 1024

@@ -19,7 +19,9 @@ sqrt(sum_k (a_k w_k)^2) per LayerNorm rounding), which a systematic error of
 a percent in one op would exceed.  Shapes: the 1.5B model's maps (d 2048,
 4d 8192, vocabulary 50257) at 64 rows (few-row kernels) and at 520 or 136
 rows (LayerNorm pass + GEMM, ragged row tiles), and a ragged width (d 832,
-N 1000)."""
+N 1000).  The self-attention sub-layer's fused kernel (LayerNorm, q|k|v map
+and block-local attention in one launch) is held to the bits of the unfused
+pair, whose pieces are checked here and against the fp64 attention."""
 import math
 
 import numpy as np
@@ -27,6 +29,7 @@ import pytest
 import torch
 
 from oracle import smem_model as MO
+from oracle import smem_oracle as O
 from paper_2609_32395_amd import smem, synth
 from tests import gpu_util
 from tests.gpu_util import require_gpu, say
@@ -135,4 +138,59 @@ def test_linear_argument_errors():
                  (z(4, 64), z(6, 64))]:         # bf16 output with N % 4 != 0
         with pytest.raises(smem.SmemError) as e:
             smem.smem_linear(x, w)
+        assert e.value.code == smem.SMEM_EINVAL
+
+
+SA_CASES = [  # name, d, H, n_blocks, mask
+    ("d 256 x 8 heads, 1 block, causal", 256, 8, 1, 1),
+    ("d 256 x 8 heads, 3 blocks, bidirectional", 256, 8, 3, 0),
+    ("160M d 768 x 24 heads, 1 block, causal", 768, 24, 1, 1),
+    ("160M d 768 x 24 heads, 5 blocks, bidirectional", 768, 24, 5, 0),
+    ("410M d 1024 x 32 heads, 1 block, causal", 1024, 32, 1, 1),
+    ("410M d 1024 x 32 heads, 2 blocks, causal", 1024, 32, 2, 1),
+    ("410M d 1024 x 32 heads, 3 blocks, bidirectional", 1024, 32, 3, 0),
+    ("d 512 x 16 heads, 130 blocks, causal", 512, 16, 130, 1),
+]
+
+
+@pytest.mark.parametrize("name,d,H,nb,mask", SA_CASES, ids=[c[0] for c in SA_CASES])
+def test_self_attention_fused_equals_unfused(name, d, H, nb, mask):
+    """The fused q|k|v + block-local attention kernel gives the bits of the
+    unfused pair (the map into q, k, v, then the attention launch), with the
+    LayerNorm in the kernel (up to 128 rows) or from the LayerNorm pass (more
+    rows); the unfused pair's q | k | v equal the validated map's output, and
+    its attention is checked against the fp64 oracle on those q, k, v."""
+    say("op parity: self-attention", name)
+    g = np.random.default_rng(d * 31 + nb * 7 + mask)
+    M = nb * 64
+    x = _bf(g, (M, d), 1.5) + synth.bf16_round(np.full((1, d), 0.25, np.float32))
+    x = synth.bf16_round(x.astype(np.float32))
+    w = _bf(g, (3 * d, d), 1.0 / math.sqrt(d))
+    lg = synth.bf16_round((1.0 + 0.1 * g.standard_normal(d)).astype(np.float32))
+    lb = synth.bf16_round((0.1 * g.standard_normal(d)).astype(np.float32))
+    xd, wd, gd, bd = _d(x), _d(w), _d(lg), _d(lb)
+    work = torch.zeros((4, M, d), dtype=torch.bfloat16, device="cuda")
+    ref_out = smem.smem_self_attention(xd, gd, bd, wd, H, mask, path=smem.SA_UNFUSED, work=work)
+    fused = smem.smem_self_attention(xd, gd, bd, wd, H, mask, path=smem.SA_FUSED,
+                                     work=torch.empty((4, M, d), dtype=torch.bfloat16, device="cuda"))
+    auto = smem.smem_self_attention(xd, gd, bd, wd, H, mask)
+    torch.cuda.synchronize()
+    assert torch.equal(fused, ref_out), f"{name}: fused != unfused"
+    assert torch.equal(auto, ref_out), f"{name}: model's choice != unfused"
+    qkv = smem.smem_linear(xd, wd, gd, bd, smem.LIN_STORE,
+                           ln_tmp=torch.empty((M, d), dtype=torch.bfloat16, device="cuda") if M > 128 else None)
+    torch.cuda.synchronize()
+    for i in range(3):
+        assert torch.equal(work[1 + i], qkv[:, i * d:(i + 1) * d]), f"{name}: q|k|v plane {i}"
+    q, k, v = (work[1 + i].float().cpu().numpy().astype(np.float64).reshape(nb, 64, H, d // H) for i in range(3))
+    expect = O.encode_blocks(q, k, v, mask).reshape(M, d)
+    gpu_util.check(fused, expect, torch.bfloat16, f"op self-attention {name}", full=d >= 768)
+
+
+def test_self_attention_argument_errors():
+    """The fused path rejects heads other than 32 wide and widths above 1024."""
+    z = lambda *shape: torch.zeros(shape, dtype=torch.bfloat16, device="cuda")
+    for d, H in [(512, 8), (2048, 64)]:
+        with pytest.raises(smem.SmemError) as e:
+            smem.smem_self_attention(z(64, d), z(d), z(d), z(3 * d, d), H, 1, path=smem.SA_FUSED)
         assert e.value.code == smem.SMEM_EINVAL
