@@ -614,6 +614,110 @@ __global__ void __launch_bounds__(C::NT, 2 * 4 / C::NW) k_gemm(LinArgs a, int ti
   }
 }
 
+// Few rows by a very wide map (the output head: tens of thousands of
+// columns): the x rows (at most 64, K <= 1024) are loaded into LDS once per
+// workgroup and stay there, and each wave streams the weights of its 16-column
+// tiles a reduction chunk (8 steps) at a time, the next chunk's loads -- the
+// next tile's first chunk after the last -- issued before the current
+// chunk's MFMAs, so the weights are read from HBM once and x once per
+// workgroup, where the few-row kernel re-reads x once per column group.  A
+// wave computes every chunk of its tile itself -- one MFMA per 32-wide step
+// from zero inside a chunk, the chunk sums added in chunk order -- the
+// reduction order of every linear map.  LDS rows are padded by 16 bytes so
+// the 16 rows one operand read touches start on different banks.
+template <int NCH, int RT>
+__global__ void __launch_bounds__(512) k_linear_wide(LinArgs a, int n_tiles, int tiles_per_wave) {
+  constexpr int K = 256 * NCH, XP = K + 8;
+  __shared__ __attribute__((aligned(16))) uint16_t xs[RT * 16 * XP];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int q = tid; q < RT * 16 * (K / 8); q += 512) {
+    const int r = q / (K / 8), c8 = q % (K / 8);
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (r < a.M) v = *(const u32x4*)(a.x + (size_t)r * a.ldx + c8 * 8);
+    *(u32x4*)(xs + r * XP + c8 * 8) = v;     // rows M .. 16 RT - 1 are zero
+  }
+  __syncthreads();                           // the only barrier
+  const int t0 = (blockIdx.x * 8 + wave) * tiles_per_wave;
+  const int t1 = min(n_tiles, t0 + tiles_per_wave);
+  if (t0 >= t1) return;
+  const int kofs = (lane >> 4) * 8;
+  const int xo = (lane & 15) * XP + kofs;
+  auto wrow = [&](int t) { return lin_wrow(a, min(t * 16 + (lane & 15), a.N - 1)) + kofs; };
+  u32x4 W[2][8];
+  auto fetch = [&](u32x4 (&Wd)[8], const uint16_t* wp, int c) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) Wd[u] = *(const u32x4*)(wp + c * 256 + u * 32);
+  };
+  const uint16_t* wr = wrow(t0);
+  fetch(W[0], wr, 0);
+  for (int t = t0; t < t1; ++t) {
+    const uint16_t* wn = wrow(min(t + 1, t1 - 1));   // the next tile (this one again after the last)
+    // the x operands are the same for every tile: an opaque copy of their
+    // offset keeps the compiler from hoisting all of them into registers
+    // (an offset, not a pointer, so the reads stay LDS reads)
+    int xv = xo;
+    asm volatile("" : "+v"(xv));
+    const uint16_t* xt = xs + xv;
+    f32x4 tot[RT];
+#pragma unroll
+    for (int i = 0; i < RT; ++i) tot[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      if (c + 1 < NCH) fetch(W[(c + 1) & 1], wr, c + 1);
+      else fetch(W[(c + 1) & 1], wn, 0);
+      __builtin_amdgcn_sched_barrier(0);   // the next chunk's loads go out before this chunk's MFMAs
+      f32x4 acc[RT];
+#pragma unroll
+      for (int i = 0; i < RT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < 8; ++st)
+#pragma unroll
+        for (int i = 0; i < RT; ++i)
+          acc[i] = mfma16(W[c & 1][st], *(const u32x4*)(xt + i * 16 * XP + c * 256 + st * 32), acc[i]);
+#pragma unroll
+      for (int i = 0; i < RT; ++i) tot[i] += acc[i];
+    }
+    if constexpr (NCH & 1) {                 // the next tile's first chunk is to be in W[0]
+#pragma unroll
+      for (int u = 0; u < 8; ++u) W[0][u] = W[1][u];
+    }
+#pragma unroll
+    for (int i = 0; i < RT; ++i) {
+      const int m = i * 16 + (lane & 15);
+      if (m < a.M) lin_store4<kLinF32>(a, m, t * 16 + 4 * (lane >> 4), tot[i]);
+    }
+    wr = wn;
+  }
+}
+
+// The wide kernel serves fp32 maps of at most 64 rows with K a multiple of
+// 256 up to 1024 (the x rows fit in LDS) and at least 8192 columns.
+inline bool wide_fits(const LinArgs& a) {
+  return !a.lng && a.M <= 64 && a.K % 256 == 0 && a.K <= 1024 && a.N >= 8192 && a.ldx % 8 == 0;
+}
+
+template <int NCH>
+static void launch_wide_nch(const LinArgs& a, hipStream_t s) {
+  const int n_tiles = (a.N + 15) / 16, waves = 256 * 8;
+  const int tpw = (n_tiles + waves - 1) / waves;             // tiles per wave, one workgroup per CU at most
+  const dim3 grid((n_tiles + 8 * tpw - 1) / (8 * tpw));
+  switch ((a.M + 15) / 16) {
+    case 1: hipLaunchKernelGGL((k_linear_wide<NCH, 1>), grid, dim3(512), 0, s, a, n_tiles, tpw); break;
+    case 2: hipLaunchKernelGGL((k_linear_wide<NCH, 2>), grid, dim3(512), 0, s, a, n_tiles, tpw); break;
+    case 3: hipLaunchKernelGGL((k_linear_wide<NCH, 3>), grid, dim3(512), 0, s, a, n_tiles, tpw); break;
+    default: hipLaunchKernelGGL((k_linear_wide<NCH, 4>), grid, dim3(512), 0, s, a, n_tiles, tpw); break;
+  }
+}
+
+static void launch_wide(const LinArgs& a, hipStream_t s) {
+  switch (a.K / 256) {
+    case 1: launch_wide_nch<1>(a, s); break;
+    case 2: launch_wide_nch<2>(a, s); break;
+    case 3: launch_wide_nch<3>(a, s); break;
+    default: launch_wide_nch<4>(a, s); break;
+  }
+}
+
 template <int EPI, class C>
 static void launch_gemm(const LinArgs& a, hipStream_t s) {
   const int tm = (a.M + C::BM - 1) / C::BM, tn = (a.N + C::BN - 1) / C::BN;
@@ -658,7 +762,9 @@ static hipError_t linear(const LinArgs& a, hipStream_t s) {
     n.lng = n.lnb = nullptr;
     return linear<EPI>(n, s);
   }
-  if (a.M <= 128) {
+  if (EPI == kLinF32 && wide_fits(a)) {
+    launch_wide(a, s);
+  } else if (a.M <= 128) {
     launch_skinny<EPI>(a, s);
   } else if ((size_t)((a.N + GemmBig::BN - 1) / GemmBig::BN) * ((a.M + GemmBig::BM - 1) / GemmBig::BM) >= 256) {
     launch_gemm<EPI, GemmBig>(a, s);

@@ -909,3 +909,38 @@ def test_fused_self_attention_indexing(nc):
             assert (H - 1) * DH + dt * 16 + (lane >> 4) * 4 + 4 <= D
     lds = 2 * BT * DH * 2 + nc * BT * NCOL * 4 + BT * NCOL * 2 + 2 * D * 2 + 2 * nc * BT * 4
     assert lds <= 160 * 1024
+
+
+@pytest.mark.parametrize("M,K,N", [(1, 1024, 50257), (16, 768, 50257), (40, 768, 50257), (64, 1024, 50257),
+                                   (64, 256, 8192), (33, 512, 9000)])
+def test_wide_head_indexing(M, K, N):
+    """k_linear_wide (fp32 maps of <= 64 rows, K <= 1024, N >= 8192): the x
+    rows fit the LDS tile, every weight row read is < N, every step's column
+    range stays inside K, and the tiles of the grid's waves cover the output
+    columns exactly once."""
+    RT, XP, U, STEPS = (M + 15) // 16, K + 8, 8, 8 * (K // 256)
+    assert RT * 16 * XP * 2 <= 160 * 1024
+    n_tiles = (N + 15) // 16
+    tpw = -(-n_tiles // (256 * 8))
+    grid = -(-n_tiles // (8 * tpw))
+    assert grid <= 256
+    cover = [0] * N
+    for wg in range(grid):
+        for wave in range(8):
+            t0 = (wg * 8 + wave) * tpw
+            t1 = min(n_tiles, t0 + tpw)
+            for t in range(t0, t1):
+                for lane in range(64):
+                    wrow = min(t * 16 + (lane & 15), N - 1)
+                    assert 0 <= wrow < N
+                    kofs = (lane >> 4) * 8
+                    assert kofs + (STEPS - 1) * 32 + 8 <= K                  # this tile's steps
+                    assert kofs + (U - 1) * 32 + 8 <= K                      # the next tile's first U steps
+                    for i in range(RT):
+                        assert (i * 16 + (lane & 15)) * XP + kofs + (STEPS - 1) * 32 + 8 <= RT * 16 * XP
+                for g4 in range(4):
+                    for e in range(4):
+                        n = t * 16 + 4 * g4 + e
+                        if n < N:
+                            cover[n] += 1
+    assert cover == [1] * N

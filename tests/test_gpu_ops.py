@@ -15,11 +15,13 @@ u sum_k |a_k w_k|, plus 1e-5 of it for the fp32 statistics); GELU's erf
 accumulation error by at most 1.13.  These worst-case bounds are checked for
 every element; the RMS error must also stay within twice what independent
 roundings give (u / sqrt 3 of rms(y_ref), plus u / sqrt 3 of the rms of
-sqrt(sum_k (a_k w_k)^2) per LayerNorm rounding), which a systematic error of
-a percent in one op would exceed.  Shapes: the 1.5B model's maps (d 2048,
+sqrt(sum_k (a_k w_k)^2) per LayerNorm rounding, plus the fp32 accumulation's
+2^-24 / sqrt 3 * sqrt(K / 2) of that rms), which a systematic error of a
+percent in one op would exceed.  Shapes: the 1.5B model's maps (d 2048,
 4d 8192, vocabulary 50257) at 64 rows (few-row kernels) and at 520 or 136
-rows (LayerNorm pass + GEMM, ragged row tiles), and a ragged width (d 832,
-N 1000).  The self-attention sub-layer's fused kernel (LayerNorm, q|k|v map
+rows (LayerNorm pass + GEMM, ragged row tiles), the head at d 1024 and 768
+with at most 64 rows (the form that keeps the rows in LDS), and a ragged
+width (d 832, N 1000).  The self-attention sub-layer's fused kernel (LayerNorm, q|k|v map
 and block-local attention in one launch) is held to the bits of the unfused
 pair, whose pieces are checked here and against the fp64 attention."""
 import math
@@ -64,6 +66,10 @@ CASES = [  # name, M, N, K, layernorm, epilogue
     ("1.5B head (fp32), 1 row", 1, 50257, 2048, True, smem.LIN_F32),
     ("1.5B head (fp32), 64 rows", 64, 50257, 2048, True, smem.LIN_F32),
     ("1.5B head (fp32), 136 rows", 136, 50257, 2048, True, smem.LIN_F32),
+    ("410M head (fp32, rows in LDS), 64 rows", 64, 50257, 1024, False, smem.LIN_F32),
+    ("410M head (fp32, rows in LDS), 1 row", 1, 50257, 1024, False, smem.LIN_F32),
+    ("160M head (fp32, rows in LDS), 16 rows", 16, 50257, 768, False, smem.LIN_F32),
+    ("160M head (fp32, rows in LDS), 40 rows", 40, 50257, 768, False, smem.LIN_F32),
     ("ragged d 832 x N 1000, 200 rows", 200, 1000, 832, True, smem.LIN_STORE),
     ("ragged d 832 x N 1000, 16 rows", 16, 1000, 832, False, smem.LIN_GELU),
 ]
@@ -102,8 +108,14 @@ def test_linear_map_against_fp64(name, M, N, K, ln, epi):
     excess = np.abs(y - ref) - bound
     rms_ref = float(np.sqrt(np.mean(ref * ref)))
     err_rms = float(np.sqrt(np.mean((y - ref) ** 2)))
+    # fp32 accumulation: K sums whose partial sums grow like sqrt(k) carry
+    # independent roundings of at most 2^-24 relative, about
+    # 2^-24 / sqrt(3) * sqrt(K / 2) * sqrt(sum_k (a_k w_k)^2) in RMS (the
+    # only term left for an fp32 output of un-normalized rows)
+    rms_sq = float(np.sqrt(np.mean(sq * sq)))
     rms_limit = 2.0 * (u_out / math.sqrt(3.0) * rms_ref
-                       + (U / math.sqrt(3.0) * float(np.sqrt(np.mean(sq * sq))) if ln else 0.0)) + 1e-9 * rms_ref
+                       + (U / math.sqrt(3.0) * rms_sq if ln else 0.0)
+                       + 2.0 ** -24 / math.sqrt(3.0) * math.sqrt(K / 2.0) * rms_sq) + 1e-9 * rms_ref
     raw = float(np.max(np.abs(y - ref))) / rms_ref
     gpu_util.RECORDS.append((f"op {name} (rms error / its limit)", "op", raw, err_rms / rms_limit, 1.0, True))
     say(f"op {name}: raw max|y-ref|/rms {raw:.3e}, rms err {err_rms / rms_ref:.3e} (limit {rms_limit / rms_ref:.3e}), "
@@ -129,6 +141,24 @@ def test_linear_rows_independent_bitwise():
     big = smem.smem_linear(_d(x), w, lg, lb, smem.LIN_GELU)
     small = smem.smem_linear(_d(x[100:164]), w, lg, lb, smem.LIN_GELU)
     assert torch.equal(big[100:164], small)
+
+
+def test_wide_head_rows_independent_bitwise():
+    """The fp32 head's few-row form (x rows kept in LDS, one workgroup per CU
+    streaming the weights) gives the bits of the tiled GEMM for the same rows:
+    rows 100..163 of a 200-row call, and single rows, at d 1024 and 768."""
+    say("op parity: wide head row independence")
+    g = np.random.default_rng(5)
+    for K in (1024, 768):
+        N = 50257
+        x = _bf(g, (200, K))
+        w = _d(_bf(g, (N, K), 1.0 / math.sqrt(K)))
+        big = smem.smem_linear(_d(x), w, epi=smem.LIN_F32)
+        small = smem.smem_linear(_d(x[100:164]), w, epi=smem.LIN_F32)
+        one = smem.smem_linear(_d(x[131:132]), w, epi=smem.LIN_F32)
+        torch.cuda.synchronize()
+        assert torch.equal(big[100:164], small), K
+        assert torch.equal(big[131:132], one), K
 
 
 def test_linear_argument_errors():
