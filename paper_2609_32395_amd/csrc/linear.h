@@ -615,9 +615,10 @@ __global__ void __launch_bounds__(C::NT, 2 * 4 / C::NW) k_gemm(LinArgs a, int ti
 }
 
 // Few rows by a very wide map (the output head: tens of thousands of
-// columns): the x rows (at most 64, K <= 1024) are loaded into LDS once per
-// workgroup and stay there, and each wave streams the weights of its 16-column
-// tiles a reduction chunk (8 steps) at a time, the next chunk's loads -- the
+// columns): the x rows (at most 64 when K <= 1024, 32 at K = 2048) are
+// loaded into LDS once per workgroup and stay there, and each wave streams
+// the weights of its 16-column tiles a reduction chunk (8 steps) at a time,
+// the next chunk's loads -- the
 // next tile's first chunk after the last -- issued before the current
 // chunk's MFMAs, so the weights are read from HBM once and x once per
 // workgroup, where the few-row kernel re-reads x once per column group.  A
@@ -691,9 +692,19 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a, int n_tiles, int
 }
 
 // The wide kernel serves fp32 maps of at most 64 rows with K a multiple of
-// 256 up to 1024 (the x rows fit in LDS) and at least 8192 columns.
+// 256 up to 2048 whose x rows fit in LDS (16 row tiles of K + 8 bf16 each:
+// 64 rows up to K = 1024, 32 rows at K = 2048) and at least 8192 columns.
+constexpr int kWideLds = 160 * 1024;
+__host__ __device__ constexpr int wide_lds(int rt, int k) { return rt * 16 * (k + 8) * 2; }
 inline bool wide_fits(const LinArgs& a) {
-  return !a.lng && a.M <= 64 && a.K % 256 == 0 && a.K <= 1024 && a.N >= 8192 && a.ldx % 8 == 0;
+  return !a.lng && a.M >= 1 && a.M <= 64 && a.K % 256 == 0 && a.K <= 2048 && a.N >= 8192 && a.ldx % 8 == 0 &&
+         wide_lds((a.M + 15) / 16, a.K) <= kWideLds;
+}
+
+template <int NCH, int RT>
+static void launch_wide_rt(const LinArgs& a, int n_tiles, int tpw, dim3 grid, hipStream_t s) {
+  if constexpr (wide_lds(RT, 256 * NCH) <= kWideLds)
+    hipLaunchKernelGGL((k_linear_wide<NCH, RT>), grid, dim3(512), 0, s, a, n_tiles, tpw);
 }
 
 template <int NCH>
@@ -702,10 +713,10 @@ static void launch_wide_nch(const LinArgs& a, hipStream_t s) {
   const int tpw = (n_tiles + waves - 1) / waves;             // tiles per wave, one workgroup per CU at most
   const dim3 grid((n_tiles + 8 * tpw - 1) / (8 * tpw));
   switch ((a.M + 15) / 16) {
-    case 1: hipLaunchKernelGGL((k_linear_wide<NCH, 1>), grid, dim3(512), 0, s, a, n_tiles, tpw); break;
-    case 2: hipLaunchKernelGGL((k_linear_wide<NCH, 2>), grid, dim3(512), 0, s, a, n_tiles, tpw); break;
-    case 3: hipLaunchKernelGGL((k_linear_wide<NCH, 3>), grid, dim3(512), 0, s, a, n_tiles, tpw); break;
-    default: hipLaunchKernelGGL((k_linear_wide<NCH, 4>), grid, dim3(512), 0, s, a, n_tiles, tpw); break;
+    case 1: launch_wide_rt<NCH, 1>(a, n_tiles, tpw, grid, s); break;
+    case 2: launch_wide_rt<NCH, 2>(a, n_tiles, tpw, grid, s); break;
+    case 3: launch_wide_rt<NCH, 3>(a, n_tiles, tpw, grid, s); break;
+    default: launch_wide_rt<NCH, 4>(a, n_tiles, tpw, grid, s); break;
   }
 }
 
@@ -714,7 +725,11 @@ static void launch_wide(const LinArgs& a, hipStream_t s) {
     case 1: launch_wide_nch<1>(a, s); break;
     case 2: launch_wide_nch<2>(a, s); break;
     case 3: launch_wide_nch<3>(a, s); break;
-    default: launch_wide_nch<4>(a, s); break;
+    case 4: launch_wide_nch<4>(a, s); break;
+    case 5: launch_wide_nch<5>(a, s); break;
+    case 6: launch_wide_nch<6>(a, s); break;
+    case 7: launch_wide_nch<7>(a, s); break;
+    default: launch_wide_nch<8>(a, s); break;
   }
 }
 

@@ -912,10 +912,10 @@ def test_fused_self_attention_indexing(nc):
 
 
 @pytest.mark.parametrize("M,K,N", [(1, 1024, 50257), (16, 768, 50257), (40, 768, 50257), (64, 1024, 50257),
-                                   (64, 256, 8192), (33, 512, 9000)])
+                                   (64, 256, 8192), (33, 512, 9000), (32, 2048, 50257), (1, 2048, 50257)])
 def test_wide_head_indexing(M, K, N):
-    """k_linear_wide (fp32 maps of <= 64 rows, K <= 1024, N >= 8192): the x
-    rows fit the LDS tile, every weight row read is < N, every step's column
+    """k_linear_wide (fp32 maps of <= 64 rows, K <= 2048, N >= 8192, the x
+    rows in LDS: at most 32 rows at K = 2048): the x rows fit the LDS tile, every weight row read is < N, every step's column
     range stays inside K, and the tiles of the grid's waves cover the output
     columns exactly once."""
     RT, XP, U, STEPS = (M + 15) // 16, K + 8, 8, 8 * (K // 256)

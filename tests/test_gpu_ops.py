@@ -70,6 +70,8 @@ CASES = [  # name, M, N, K, layernorm, epilogue
     ("410M head (fp32, rows in LDS), 1 row", 1, 50257, 1024, False, smem.LIN_F32),
     ("160M head (fp32, rows in LDS), 16 rows", 16, 50257, 768, False, smem.LIN_F32),
     ("160M head (fp32, rows in LDS), 40 rows", 40, 50257, 768, False, smem.LIN_F32),
+    ("1.5B head (fp32, rows in LDS), 16 rows", 16, 50257, 2048, False, smem.LIN_F32),
+    ("1.5B head (fp32, rows in LDS), 32 rows", 32, 50257, 2048, False, smem.LIN_F32),
     ("ragged d 832 x N 1000, 200 rows", 200, 1000, 832, True, smem.LIN_STORE),
     ("ragged d 832 x N 1000, 16 rows", 16, 1000, 832, False, smem.LIN_GELU),
 ]
@@ -146,18 +148,19 @@ def test_linear_rows_independent_bitwise():
 def test_wide_head_rows_independent_bitwise():
     """The fp32 head's few-row form (x rows kept in LDS, one workgroup per CU
     streaming the weights) gives the bits of the tiled GEMM for the same rows:
-    rows 100..163 of a 200-row call, and single rows, at d 1024 and 768."""
+    rows 100..163 of a 200-row call, and single rows, at d 1024 and 768;
+    rows 100..131 and a single row at d 2048."""
     say("op parity: wide head row independence")
     g = np.random.default_rng(5)
-    for K in (1024, 768):
+    for K, rows in ((1024, 64), (768, 64), (2048, 32)):
         N = 50257
         x = _bf(g, (200, K))
         w = _d(_bf(g, (N, K), 1.0 / math.sqrt(K)))
         big = smem.smem_linear(_d(x), w, epi=smem.LIN_F32)
-        small = smem.smem_linear(_d(x[100:164]), w, epi=smem.LIN_F32)
+        small = smem.smem_linear(_d(x[100:100 + rows]), w, epi=smem.LIN_F32)
         one = smem.smem_linear(_d(x[131:132]), w, epi=smem.LIN_F32)
         torch.cuda.synchronize()
-        assert torch.equal(big[100:164], small), K
+        assert torch.equal(big[100:100 + rows], small), K
         assert torch.equal(big[131:132], one), K
 
 
