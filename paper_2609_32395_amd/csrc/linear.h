@@ -616,18 +616,18 @@ __global__ void __launch_bounds__(C::NT, 2 * 4 / C::NW) k_gemm(LinArgs a, int ti
 
 // Few rows by a very wide map (the output head: tens of thousands of
 // columns): the x rows (at most 64 when K <= 1024, 32 at K = 2048) are
-// loaded into LDS once per workgroup and stay there, and each wave streams
-// the weights of its 16-column tiles a reduction chunk (8 steps) at a time,
-// the next chunk's loads -- the
-// next tile's first chunk after the last -- issued before the current
-// chunk's MFMAs, so the weights are read from HBM once and x once per
-// workgroup, where the few-row kernel re-reads x once per column group.  A
-// wave computes every chunk of its tile itself -- one MFMA per 32-wide step
-// from zero inside a chunk, the chunk sums added in chunk order -- the
-// reduction order of every linear map.  LDS rows are padded by 16 bytes so
-// the 16 rows one operand read touches start on different banks.
+// loaded into LDS once per workgroup and stay there, and each wave computes
+// two 16-column tiles side by side, streaming their weights a reduction
+// chunk (8 steps) at a time with the next chunk's loads (16 KB) issued
+// before the current chunk's MFMAs; each x fragment read from LDS feeds both
+// tiles.  The weights are read from HBM once and x once per workgroup, where
+// the few-row kernel re-reads x once per column group.  A wave sums every
+// chunk of its tiles itself -- one MFMA per 32-wide step from zero inside a
+// chunk, the chunk sums added in chunk order -- the reduction order of every
+// linear map.  LDS rows are padded by 16 bytes so the 16 rows one operand
+// read touches start on different banks.
 template <int NCH, int RT>
-__global__ void __launch_bounds__(512) k_linear_wide(LinArgs a, int n_tiles, int tiles_per_wave) {
+__global__ void __launch_bounds__(512) k_linear_wide(LinArgs a, int n_tiles) {
   constexpr int K = 256 * NCH, XP = K + 8;
   __shared__ __attribute__((aligned(16))) uint16_t xs[RT * 16 * XP];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -638,56 +638,61 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a, int n_tiles, int
     *(u32x4*)(xs + r * XP + c8 * 8) = v;     // rows M .. 16 RT - 1 are zero
   }
   __syncthreads();                           // the only barrier
-  const int t0 = (blockIdx.x * 8 + wave) * tiles_per_wave;
-  const int t1 = min(n_tiles, t0 + tiles_per_wave);
-  if (t0 >= t1) return;
+  const int t0 = (blockIdx.x * 8 + wave) * 2;
+  if (t0 >= n_tiles) return;
+  const bool second = t0 + 1 < n_tiles;      // else the second tile re-reads the first and is not stored
   const int kofs = (lane >> 4) * 8;
-  const int xo = (lane & 15) * XP + kofs;
   auto wrow = [&](int t) { return lin_wrow(a, min(t * 16 + (lane & 15), a.N - 1)) + kofs; };
-  u32x4 W[2][8];
-  auto fetch = [&](u32x4 (&Wd)[8], const uint16_t* wp, int c) {
+  const uint16_t* wp[2] = {wrow(t0), wrow(second ? t0 + 1 : t0)};
+  u32x4 W[2][2][8];                          // [chunk parity][tile][step]
+  auto fetch = [&](u32x4 (&Wd)[2][8], int c) {
 #pragma unroll
-    for (int u = 0; u < 8; ++u) Wd[u] = *(const u32x4*)(wp + c * 256 + u * 32);
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) Wd[j][u] = *(const u32x4*)(wp[j] + c * 256 + u * 32);
   };
-  const uint16_t* wr = wrow(t0);
-  fetch(W[0], wr, 0);
-  for (int t = t0; t < t1; ++t) {
-    const uint16_t* wn = wrow(min(t + 1, t1 - 1));   // the next tile (this one again after the last)
-    // the x operands are the same for every tile: an opaque copy of their
-    // offset keeps the compiler from hoisting all of them into registers
-    // (an offset, not a pointer, so the reads stay LDS reads)
-    int xv = xo;
+  fetch(W[0], 0);
+  f32x4 tot[2][RT];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int i = 0; i < RT; ++i) tot[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    if (c + 1 < NCH) fetch(W[(c + 1) & 1], c + 1);
+    __builtin_amdgcn_sched_barrier(0);     // the next chunk's loads go out before this chunk's MFMAs
+    // an opaque copy of the x offset keeps the compiler from holding x
+    // fragments in registers across chunks (an offset, not a pointer, so
+    // the reads stay LDS reads)
+    int xv = (lane & 15) * XP + kofs + c * 256;
     asm volatile("" : "+v"(xv));
     const uint16_t* xt = xs + xv;
-    f32x4 tot[RT];
+    f32x4 acc[2][RT];
 #pragma unroll
-    for (int i = 0; i < RT; ++i) tot[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      if (c + 1 < NCH) fetch(W[(c + 1) & 1], wr, c + 1);
-      else fetch(W[(c + 1) & 1], wn, 0);
-      __builtin_amdgcn_sched_barrier(0);   // the next chunk's loads go out before this chunk's MFMAs
-      f32x4 acc[RT];
+      for (int i = 0; i < RT; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < RT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int st = 0; st < 8; ++st)
 #pragma unroll
-      for (int st = 0; st < 8; ++st)
+      for (int i = 0; i < RT; ++i) {
+        const u32x4 xf = *(const u32x4*)(xt + i * 16 * XP + st * 32);
 #pragma unroll
-        for (int i = 0; i < RT; ++i)
-          acc[i] = mfma16(W[c & 1][st], *(const u32x4*)(xt + i * 16 * XP + c * 256 + st * 32), acc[i]);
+        for (int j = 0; j < 2; ++j) acc[j][i] = mfma16(W[c & 1][j][st], xf, acc[j][i]);
+      }
 #pragma unroll
-      for (int i = 0; i < RT; ++i) tot[i] += acc[i];
-    }
-    if constexpr (NCH & 1) {                 // the next tile's first chunk is to be in W[0]
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int u = 0; u < 8; ++u) W[0][u] = W[1][u];
-    }
+      for (int i = 0; i < RT; ++i) tot[j][i] += acc[j][i];
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    if (j == 1 && !second) break;
 #pragma unroll
     for (int i = 0; i < RT; ++i) {
       const int m = i * 16 + (lane & 15);
-      if (m < a.M) lin_store4<kLinF32>(a, m, t * 16 + 4 * (lane >> 4), tot[i]);
+      if (m < a.M) lin_store4<kLinF32>(a, m, (t0 + j) * 16 + 4 * (lane >> 4), tot[j][i]);
     }
-    wr = wn;
   }
 }
 
@@ -702,21 +707,20 @@ inline bool wide_fits(const LinArgs& a) {
 }
 
 template <int NCH, int RT>
-static void launch_wide_rt(const LinArgs& a, int n_tiles, int tpw, dim3 grid, hipStream_t s) {
+static void launch_wide_rt(const LinArgs& a, int n_tiles, dim3 grid, hipStream_t s) {
   if constexpr (wide_lds(RT, 256 * NCH) <= kWideLds)
-    hipLaunchKernelGGL((k_linear_wide<NCH, RT>), grid, dim3(512), 0, s, a, n_tiles, tpw);
+    hipLaunchKernelGGL((k_linear_wide<NCH, RT>), grid, dim3(512), 0, s, a, n_tiles);
 }
 
 template <int NCH>
 static void launch_wide_nch(const LinArgs& a, hipStream_t s) {
-  const int n_tiles = (a.N + 15) / 16, waves = 256 * 8;
-  const int tpw = (n_tiles + waves - 1) / waves;             // tiles per wave, one workgroup per CU at most
-  const dim3 grid((n_tiles + 8 * tpw - 1) / (8 * tpw));
+  const int n_tiles = (a.N + 15) / 16;
+  const dim3 grid((n_tiles + 15) / 16);                      // 8 waves of two tiles each
   switch ((a.M + 15) / 16) {
-    case 1: launch_wide_rt<NCH, 1>(a, n_tiles, tpw, grid, s); break;
-    case 2: launch_wide_rt<NCH, 2>(a, n_tiles, tpw, grid, s); break;
-    case 3: launch_wide_rt<NCH, 3>(a, n_tiles, tpw, grid, s); break;
-    default: launch_wide_rt<NCH, 4>(a, n_tiles, tpw, grid, s); break;
+    case 1: launch_wide_rt<NCH, 1>(a, n_tiles, grid, s); break;
+    case 2: launch_wide_rt<NCH, 2>(a, n_tiles, grid, s); break;
+    case 3: launch_wide_rt<NCH, 3>(a, n_tiles, grid, s); break;
+    default: launch_wide_rt<NCH, 4>(a, n_tiles, grid, s); break;
   }
 }
 

@@ -915,29 +915,33 @@ def test_fused_self_attention_indexing(nc):
                                    (64, 256, 8192), (33, 512, 9000), (32, 2048, 50257), (1, 2048, 50257)])
 def test_wide_head_indexing(M, K, N):
     """k_linear_wide (fp32 maps of <= 64 rows, K <= 2048, N >= 8192, the x
-    rows in LDS: at most 32 rows at K = 2048): the x rows fit the LDS tile, every weight row read is < N, every step's column
-    range stays inside K, and the tiles of the grid's waves cover the output
-    columns exactly once."""
-    RT, XP, U, STEPS = (M + 15) // 16, K + 8, 8, 8 * (K // 256)
+    rows in LDS: at most 32 rows at K = 2048): the x rows fit the LDS tile,
+    every weight row read is < N, every chunk's column range stays inside K,
+    and the two tiles of each wave cover the output columns exactly once."""
+    RT, XP = (M + 15) // 16, K + 8
+    NCH = K // 256
     assert RT * 16 * XP * 2 <= 160 * 1024
     n_tiles = (N + 15) // 16
-    tpw = -(-n_tiles // (256 * 8))
-    grid = -(-n_tiles // (8 * tpw))
-    assert grid <= 256
+    grid = (n_tiles + 15) // 16
     cover = [0] * N
     for wg in range(grid):
         for wave in range(8):
-            t0 = (wg * 8 + wave) * tpw
-            t1 = min(n_tiles, t0 + tpw)
-            for t in range(t0, t1):
-                for lane in range(64):
-                    wrow = min(t * 16 + (lane & 15), N - 1)
-                    assert 0 <= wrow < N
-                    kofs = (lane >> 4) * 8
-                    assert kofs + (STEPS - 1) * 32 + 8 <= K                  # this tile's steps
-                    assert kofs + (U - 1) * 32 + 8 <= K                      # the next tile's first U steps
+            t0 = (wg * 8 + wave) * 2
+            if t0 >= n_tiles:
+                continue
+            second = t0 + 1 < n_tiles
+            tiles = [t0, t0 + 1 if second else t0]
+            for lane in range(64):
+                kofs = (lane >> 4) * 8
+                for t in tiles:
+                    assert 0 <= min(t * 16 + (lane & 15), N - 1) < N
+                for c in range(NCH):
+                    assert c * 256 + 7 * 32 + kofs + 8 <= K           # weights and x of chunk c
                     for i in range(RT):
-                        assert (i * 16 + (lane & 15)) * XP + kofs + (STEPS - 1) * 32 + 8 <= RT * 16 * XP
+                        assert (i * 16 + (lane & 15)) * XP + kofs + c * 256 + 7 * 32 + 8 <= RT * 16 * XP
+            for j, t in enumerate(tiles):
+                if j == 1 and not second:
+                    break
                 for g4 in range(4):
                     for e in range(4):
                         n = t * 16 + 4 * g4 + e
