@@ -32,7 +32,10 @@ Secondary workloads, timed in the same run and reported under "secondary":
     learned positions): block-skip serving of a fully cached context against
     the cold prefill, batch 1, contexts 1k / 2k / 4k / 8k; and batched
     KV-cached decode at the paper's (scale, context, batch) cells, 128 timed
-    tokens after 66 warm-up tokens, completed blocks appended in the loop.
+    tokens after 66 warm-up tokens, completed blocks appended in the loop;
+  * on request only (--workloads selfattn): the self-attention sub-layer's
+    attention part at the 160M and 410M widths, the model's map + attention
+    pair against the fused LayerNorm + q|k|v + attention kernel.
 
 Timing uses HIP events on the stream the kernels are launched on (torch's
 current stream, handed to the library).  The 160M encoder and prefill calls
@@ -832,6 +835,43 @@ def delete_generate_workload(args, torch, smem, synth):
     return out
 
 
+def selfattn_workload(args, torch, smem, synth):
+    """The attention part of a self-attention sub-layer at the model scales'
+    widths (heads of 32, causal): the q|k|v map followed by the block-local
+    attention launch (the model's path) against the fused kernel that runs
+    the LayerNorm, the map and the attention of a (block, head) in one
+    workgroup; back-to-back calls at 1, 2, 16 and 128 blocks, synthetic
+    normal rows and weights of the model's scales, the two outputs compared
+    bitwise."""
+    stream = torch.cuda.current_stream()
+    g = torch.Generator(device="cuda")
+    g.manual_seed(args.seed)
+    out = {}
+    for name, d in (("160M", 768), ("410M", 1024)):
+        H = d // 32
+        w = (torch.randn(3 * d, d, generator=g, device="cuda") / math.sqrt(d)).to(torch.bfloat16)
+        lg = (1.0 + 0.1 * torch.randn(d, generator=g, device="cuda")).to(torch.bfloat16)
+        lb = (0.1 * torch.randn(d, generator=g, device="cuda")).to(torch.bfloat16)
+        for nb in (1, 2, 16, 128):
+            M = nb * 64
+            x = torch.randn(M, d, generator=g, device="cuda").to(torch.bfloat16)
+            work = torch.empty((4, M, d), dtype=torch.bfloat16, device="cuda")
+            ys = {p: torch.empty((M, d), dtype=torch.bfloat16, device="cuda") for p in (1, 2)}
+            us = {}
+            for p in (1, 2):
+                call = lambda _t, p=p: smem.smem_self_attention(x, lg, lb, w, H, smem.MASK_CAUSAL, path=p,
+                                                                out=ys[p], work=work)
+                for t in range(5):
+                    call(t)
+                us[p] = _events_time(call, 50, stream) / 50 * 1e6
+            out[f"{name} {nb} blocks"] = dict(unfused_us=round(us[1], 2), fused_us=round(us[2], 2),
+                                              bitwise_equal=bool(torch.equal(ys[1], ys[2])))
+            print(f"[bench] self-attention {name} {nb} blocks: unfused {us[1]:.1f} us, fused {us[2]:.1f} us",
+                  file=sys.stderr, flush=True)
+            del x, work, ys
+    return out
+
+
 def model_oracle_time(args, torch, smem, synth, W, E, D, d, H, b, vocab, T, n):
     """The fp64 model oracle's block-skip read of the final block of an
     n-token context (the same unit as the GPU's block_skip_ms), on this host;
@@ -943,7 +983,8 @@ def main():
                          "the memory kept as rows and every layer reading them through its maps; "
                          "delete_sweep: deletion latency from "
                          "512 to 65,536 cached blocks; delete_generate: the whole model's delete-then-generate "
-                         "cycle at 512 and 4096 cached blocks)")
+                         "cycle at 512 and 4096 cached blocks; selfattn, not run by default: the fused "
+                         "self-attention kernel against the model's map + attention pair)")
     ap.add_argument("--delete-sizes", default="512,1024,4096,16384,65536")
     ap.add_argument("--delgen-blocks", default="512,4096")
     ap.add_argument("--model-scales", default="160M,410M,1.5B")
@@ -1006,6 +1047,8 @@ def main():
             secondary["model_decode_row_plane"] = model_decode_workload(args, torch, smem, synth, row_plane=True)
         if "delete_generate" in wl:
             secondary["delete_then_generate"] = delete_generate_workload(args, torch, smem, synth)
+        if "selfattn" in wl:
+            secondary["self_attention_fused_vs_unfused"] = selfattn_workload(args, torch, smem, synth)
     cpu = None
     if dec is None:
         print(json.dumps({"metric": "profiling run (no headline)", "value": None, "secondary": secondary}))
