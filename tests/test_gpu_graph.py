@@ -1,6 +1,8 @@
 """HIP-graph capture of the library's calls.
 
-The whole model's block-skip read (embedding, the LayerNorm-fused few-row
+Store-level reads at the serve's head shape (a prefill over many pages: the
+split launch and the merge; a batched decode step: the decode reader and its
+merge) and the whole model's block-skip read (embedding, the LayerNorm-fused few-row
 maps, the block-local attention, the few-pair prefill into the memory, the
 output head) and its batched KV-cached decode step (the decode reader over
 the in-block caches and the memory, with its split merge) are captured on a
@@ -90,4 +92,44 @@ def test_decode_step_graph_replays_bitwise():
         # eager work between replays: sequence 1's next position (a cache row
         # the captured step does not read)
         smem.smem_model_decode(m, 1, [J[1]], [P[1] + 1], tok(toks[1, P[1] + 1:P[1] + 2]))
+        torch.cuda.synchronize()
+
+
+def test_store_reads_graph_replays_bitwise():
+    """Store-level reads at the serve's head shape (16 heads of 128): a
+    block's prefill over 70 memory pages (one workgroup per split, then the
+    merge launch) and a 4-sequence decode step (the decode reader and its
+    merge), captured and replayed against the eager calls."""
+    say("graph: store prefill (split + merge) and decode")
+    b, H, dh, S, J = 64, 16, 128, 4, 70
+    st = smem.Store(S, J + 1, S * J, b, H, dh, torch.bfloat16)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(43)
+    rnd = lambda *shape: torch.randn(*shape, generator=gen, device="cuda").to(torch.bfloat16)
+    for s in range(S):
+        for j in range(J):
+            smem.smem_store_put_block(st, s, j, rnd(b, H, dh), rnd(b, H, dh))
+    q, ki, vi, nkv = rnd(b, H, dh), rnd(b, H, dh), rnd(b, H, dh), rnd(2, H, dh)
+    eager_p = smem.smem_reader_prefill_block(st, [0], [J], q, ki, vi, nkv)
+    out_p = torch.empty_like(eager_p)
+    qd, kn, vn = rnd(S, H, dh), rnd(S, H, dh), rnd(S, H, dh)
+    kc, vc = rnd(S * b, H, dh), rnd(S * b, H, dh)
+    pos = [3, 17, 40, 63]
+    eager_d = smem.smem_reader_decode(st, list(range(S)), [J] * S, pos, qd, kn, vn, kc, vc, nkv)
+    out_d = torch.empty_like(eager_d)
+
+    def calls():
+        smem.smem_reader_prefill_block(st, [0], [J], q, ki, vi, nkv, out=out_p)
+        smem.smem_reader_decode(st, list(range(S)), [J] * S, pos, qd, kn, vn, kc, vc, nkv, out=out_d)
+
+    graph = _capture(calls)
+    for rep in range(3):
+        out_p.fill_(float("nan"))
+        out_d.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out_p, eager_p), f"prefill, replay {rep}"
+        assert torch.equal(out_d, eager_d), f"decode, replay {rep}"
+        smem.smem_reader_prefill_block(st, [1], [J - 3], q, ki, vi, nkv)   # eager work between replays
         torch.cuda.synchronize()
